@@ -1,0 +1,86 @@
+"""The oracle's pins must catch plausible slips.
+
+Each case below plants one mistake in a copy of the oracle's C source (on the
+CPU, in a temporary directory), builds it, and runs the pins of test_oracle.py
+against it: at least one pin has to fail.  The unmodified oracle passes all of
+them (test_oracle.py).
+"""
+import os
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import oracle as oracle_mod
+import test_oracle as pins
+
+SRC = os.path.join(os.path.dirname(oracle_mod.__file__), "lapattn_oracle.c")
+
+MUTANTS = {
+    "scale gradient dropped": ("dW[a * m + bs] += dc * ninf", "dW[a * m + bs] += 0 * dc * ninf"),
+    "X0 without transpose": ("Xs[a * m + b] = W[b * m + a] / c", "Xs[a * m + b] = W[a * m + b] / c"),
+    "landmark-key gradient sign": ("dkt[l * d + c] -= t;", "dkt[l * d + c] += t;"),
+    "centring term halved": ("o = y + (1.0 - si) * s->vbar[c];", "o = y + (1.0 - si) * s->vbar[c] * 0.5;"),
+    "segments rounded up": ("starts[l] = (int)(((long long)l * n) / m);",
+                            "starts[l] = (int)(((long long)l * n + m - 1) / m);"),
+    "row norm used twice": ("double c = n1 * ninf;", "double c = ninf * ninf;"),
+    "mean-value gradient dropped": ("tv + dvbar[c] / n", "tv"),
+    "NS factors swapped": ("matmul(X, WX, Xn, m, m, m);", "matmul(WX, X, Xn, m, m, m);"),
+    "kernel gradient sign": ("dD[(size_t)i * m + l] = -s->A", "dD[(size_t)i * m + l] = s->A"),
+    "K_LL backward dropped": ("dqt[a * d + c] += g * sg;", "dqt[a * d + c] += 0 * g * sg;"),
+    "rowsum backward power": ("dYi[d] = -t / (si * si);", "dYi[d] = -t / si;"),
+    "ones column wrong": ("(c < d ? v[(size_t)j * d + c] : 1.0)", "(c < d ? v[(size_t)j * d + c] : 0.5)"),
+    "l2 instead of l1": ("dist += fabs(x[c] - y[c]);", "dist += (x[c] - y[c]) * (x[c] - y[c]);"),
+    "eps ignored": ("for (int a = 0; a < m; ++a) W[a * m + a] += eps;", "(void)eps;"),
+    "query/key landmarks swapped in K_LL": (
+        "s->Wk[a * m + b] = lapattn_oracle_kernel(s->qt + a * d, s->kt + b * d, d, lambda);",
+        "s->Wk[a * m + b] = lapattn_oracle_kernel(s->kt + a * d, s->qt + b * d, d, lambda);"),
+}
+
+PIN_CALLS = [
+    lambda: pins.test_kernel_identity_and_unit_distance(None),
+    lambda: pins.test_kernel_gradient_norm_appendix_a(None),
+    lambda: pins.test_segments_golden(None),
+    lambda: pins.test_ns_golden_examples(None),
+    lambda: pins.test_ns_x0_uses_transpose_and_induced_norms(None),
+    lambda: pins.test_ns_residual_identity(None, 16, 6),
+    lambda: pins.test_ns_special_cases(None),
+    lambda: pins.test_forward_golden_examples(None),
+    lambda: pins.test_forward_landmarks_equal_tokens_is_dense_attention(None, oracle.NORM_INLINE, 16, 8, 8 ** 0.5),
+    lambda: pins.test_forward_one_landmark_closed_form(None),
+    lambda: pins.test_forward_inline_rows_sum_to_one(None),
+    lambda: pins.test_forward_permutation_within_hand_stated_segments(None),
+    lambda: pins.test_forward_factored_equals_explicit_nystrom(None),
+    lambda: pins.test_backward_matches_finite_differences(None, oracle.NORM_ROWSUM, 13, 3, 5, 4, 1.5),
+    lambda: pins.test_backward_matches_finite_differences(None, oracle.NORM_INLINE, 17, 4, 4, 6, 4.0),
+    lambda: pins.test_backward_with_perturbation_and_two_heads(None),
+]
+
+
+def _count_failures():
+    fails = 0
+    for call in PIN_CALLS:
+        try:
+            call()
+        except (AssertionError, ValueError):
+            fails += 1
+    return fails
+
+
+def test_unmodified_oracle_passes_the_pin_subset(oracle_lib):
+    assert _count_failures() == 0
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(oracle_lib, tmp_path, name):
+    a, b = MUTANTS[name]
+    src = open(SRC).read()
+    assert src.count(a) == 1, "mutation anchor not found: %s" % name
+    mpath = tmp_path / "mut.c"
+    mpath.write_text(src.replace(a, b))
+    so = tmp_path / "libmut.so"
+    subprocess.check_call(["gcc", "-O2", "-ffp-contract=off", "-fopenmp", "-fPIC", "-shared", "-std=c11",
+                           "-I", os.path.dirname(SRC), "-o", str(so), str(mpath), "-lm"])
+    with oracle_mod.using(str(so)):
+        assert _count_failures() >= 1, "no pin caught the mutant '%s'" % name

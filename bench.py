@@ -1,0 +1,148 @@
+"""Benchmark: Nystrom-Laplacian attention forward throughput on one MI355X.
+
+One step = one lapattn_forward over the high-resolution workload (B=8, H=2,
+n=16384, d=64, m=64, T=8, bf16 inputs, lambda=8), inputs resident in HBM.
+Prints one JSON line with tokens/s (B*n per step), the roofline of the
+dominant kernel (measured with HIP events inside the library over the timed
+region) and the fp64 CPU oracle timed on a bounded sample of the same workload.
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+import workloads as W  # noqa: E402
+
+METRIC = "Laplacian-Nyström attention fwd tokens/sec at n=3136/16384; % of HBM/VALU roofline"
+WORKLOAD = "highres"
+
+# MI355X published peaks used for the roofline.
+PEAK_FP32_VECTOR_TFLOPS = 157.3   # 256 CUs x 64 lanes x 2 (packed/dual issue) x 2 (FMA) x 2.4 GHz
+PEAK_HBM_GBS = 8000.0
+
+
+def alu_ops(kernel, w):
+    """Algorithmic ALU work of one launch: every kernel value k(x, y) needs d
+    subtractions, d absolute-value accumulations and one exponential (2d + 1
+    operations); the contractions are not counted (they run on the matrix cores
+    or are a small fraction)."""
+    pairs = {"key_summary": w.BH * w.n * w.m, "query_out": w.BH * w.n * w.m,
+             "ns_solve": w.BH * w.m * w.m}.get(kernel)
+    return None if pairs is None else pairs * (2 * w.d + 1)
+
+
+def traffic_record(kernel):
+    """HBM traffic measured with rocprofv3 counters for this kernel, if the
+    committed record matches the current kernel sources (else None)."""
+    path = os.path.join(ROOT, "profiles", "traffic_%s_%s.json" % (kernel, WORKLOAD))
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path))
+    except (OSError, ValueError):
+        return None
+    import hashlib
+    h = hashlib.sha256()
+    for src in rec.get("sources", []):
+        with open(os.path.join(ROOT, src), "rb") as f:
+            h.update(f.read())
+    if h.hexdigest() != rec.get("sources_sha256"):
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(w, x, budget_s=12.0):
+    """The fp64 oracle on a bounded sample: whole heads of the same workload,
+    until about budget_s seconds of work; scaled to tokens/s of the full
+    workload (one token = all H heads of one position)."""
+    import oracle
+    heads, t_used = 0, 0.0
+    BH = w.BH
+    while heads < BH and t_used < budget_s:
+        sub = {k: np.ascontiguousarray(v.reshape(BH, w.n, w.d)[heads:heads + 1][None]) for k, v in x.items()}
+        t0 = time.perf_counter()
+        oracle.forward(sub["Q"], sub["K"], sub["V"], w.m, w.lam, w.T)
+        t_used += time.perf_counter() - t0
+        heads += 1
+    tokens = w.B * w.n * heads / BH
+    return {"value": tokens / t_used, "unit": "tokens/s", "cores": oracle.threads(), "kind": "oracle",
+            "sample": "%d of %d heads of the %s workload (n=%d, d=%d, m=%d, T=%d), fp64, %.1f s"
+                      % (heads, BH, w.name, w.n, w.d, w.m, w.T, t_used)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build runs on a single MI355X and has no multi-GPU path "
+              "(every head is independent; see DESIGN.md for how the work would shard).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2604_20368_amd import lapattn
+
+    w = W.WORKLOADS[WORKLOAD]
+    x = W.make_inputs(w, with_grad=False)
+    dev = torch.device("cuda:0")
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    Q, K, V = (torch.from_numpy(x[k]).to(dev).to(dt) for k in ("Q", "K", "V"))
+    out = torch.empty_like(Q)
+    ws = lapattn.workspace(Q, w.m, w.T)
+
+    def step():
+        lapattn.forward(Q, K, V, w.m, w.lam, w.T, out=out, ws=ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    lapattn.lapattn_timing_enable(1)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    lapattn.lapattn_timing_enable(0)
+    launches = lapattn.lapattn_timing_read(cap=64 * args.steps + 64)
+
+    ms = (t1 - t0) * 1e3 / args.steps
+    tokens = w.B * w.n
+    per = {}
+    for name, t in launches:
+        per.setdefault(name, []).append(t)
+    avg = {k: sum(v) / len(v) for k, v in per.items()}
+    dom = max(avg, key=avg.get)
+    ops = alu_ops(dom, w)
+    roof = None
+    if ops is not None:
+        ach = ops / (avg[dom] * 1e-3) / 1e12
+        roof = {"bound": "alu", "kernel": dom, "achieved": round(ach, 3), "peak": PEAK_FP32_VECTOR_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(ach / PEAK_FP32_VECTOR_TFLOPS, 4),
+                "traffic": traffic_record(dom), "avg_ms": round(avg[dom], 5)}
+    res = {
+        "metric": METRIC, "value": tokens / (ms * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16-in/f32", "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "H": w.H, "n": w.n, "d": w.d, "m": w.m, "T": w.T,
+                   "lambda": w.lam, "inputs": w.dtype, "tokens_per_step": tokens},
+        "kernels_ms": {k: round(v, 5) for k, v in avg.items()},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(w, x)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,129 @@
+/*
+ * lapattn.h -- C ABI of the MI355X (gfx950) library for Nystrom-approximated
+ * Laplacian-kernel attention (LaplacianFormer, arXiv 2604.20368).
+ *
+ * Per head (b, h), with q_i, k_j, v_j the rows of Q, K, V (n x d):
+ *   k(x, y)   = exp(-||x - y||_1 / lambda)                 Sec. 1; Sec. 4.1; Eq. (8)
+ *   landmarks qt_l, kt_l = means of the tokens of segment l,
+ *             segment l = [floor(l n/m), floor((l+1) n/m))  Sec. 4.2, sampling (1-D reading)
+ *   K_LL[a][b] = k(qt_a, kt_b)                              Algorithm 1, kernel on sampled points
+ *   K_QL[i][l] = k(q_i, kt_l)                               Eq. (8), cross-kernel
+ *   K_LK[a][j] = k(qt_a, k_j)
+ *   X_T       = Newton-Schulz iterate of Algorithm 2 on W = K_LL + eps I:
+ *               X_0 = W^T / (||W||_1 ||W||_inf),  X_{t+1} = X_t (2I - W X_t);
+ *               X := 0 when the scale ||W||_1 ||W||_inf is 0
+ *   G^        = K_QL X_T K_LK  (never formed: Y = K_QL (X_T (K_LK [V | 1])))
+ *   s_i       = (G^ 1)_i,  vbar = mean_j v_j
+ *   Out_i     = LAPATTN_NORM_INLINE:  (G^ V)_i + (1 - s_i) vbar
+ *                 i.e. Z V with z_ij = g^_ij - s_i/n + 1/n, the injective centring
+ *                 of Eq. (4) with the whitening taken as the identity
+ *               LAPATTN_NORM_ROWSUM:  (G^ V)_i / s_i       (Eq. (3))
+ *               LAPATTN_NORM_NONE:    (G^ V)_i
+ * The depth-wise convolution branch of Eq. (7) is not part of this operation.
+ *
+ * Layout: Q, K, V, Out, dOut, dQ, dK, dV are device pointers to contiguous
+ * row-major [B][H][n][d] arrays of the element type `dtype` (fp32, or bf16 as
+ * raw 16-bit patterns).  The value head dimension equals d.
+ *
+ * Ownership: the caller owns every buffer, including the workspace (device
+ * memory of at least lapattn_workspace_size() bytes).  The library never
+ * allocates or frees device memory and keeps no state between calls apart from
+ * the optional timing switch below.  Outputs are overwritten, never accumulated.
+ * Outputs must not alias inputs, each other, or the workspace.
+ *
+ * Asynchrony: every call validates its arguments on the host, enqueues its
+ * kernels on `stream` (a hipStream_t; NULL = the default stream) and returns
+ * without synchronising.  Results are valid once the stream has reached that
+ * point.  Calls on different streams with different workspaces may run
+ * concurrently; calls sharing a workspace must be ordered by the caller.
+ * Results are bitwise deterministic for identical inputs (no float atomics).
+ *
+ * Errors: a nonzero return means nothing was enqueued and nothing was written,
+ * except LAPATTN_ERR_HIP, which reports a failed kernel launch (work enqueued
+ * before the failure may have run).  No C++ exception crosses this interface.
+ */
+#ifndef LAPATTN_H
+#define LAPATTN_H
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t* lapattn_stream_t;   /* the same type as hipStream_t */
+
+typedef enum { LAPATTN_FP32 = 0, LAPATTN_BF16 = 1 } lapattn_dtype;
+
+typedef enum {
+    LAPATTN_NORM_INLINE = 0,
+    LAPATTN_NORM_ROWSUM = 1,
+    LAPATTN_NORM_NONE = 2
+} lapattn_norm;
+
+enum {
+    LAPATTN_OK = 0,
+    LAPATTN_ERR_NULL = 1,         /* a required pointer is NULL */
+    LAPATTN_ERR_SHAPE = 2,        /* B, H, n < 1, m < 1, m > n, or B*H*n*d >= 2^31 */
+    LAPATTN_ERR_PARAM = 3,        /* lambda not finite or <= 0, ns_iters outside [0, 64],
+                                     eps not finite or < 0, unknown norm or dtype */
+    LAPATTN_ERR_UNSUPPORTED = 4,  /* d not in {32, 64}, m > 64, or bf16 backward */
+    LAPATTN_ERR_WORKSPACE = 5,    /* workspace NULL or smaller than lapattn_workspace_size() */
+    LAPATTN_ERR_HIP = 6           /* a HIP launch failed */
+};
+
+/* Options; a NULL pointer means {LAPATTN_NORM_INLINE, 0.0f}.
+ * eps is the diagonal perturbation W <- W + eps I of Algorithm 2 (>= 0). */
+typedef struct {
+    int norm;      /* lapattn_norm */
+    float eps;
+} lapattn_opts;
+
+/* Bytes of device workspace lapattn_forward (for_backward = 0) or
+ * lapattn_backward (for_backward = 1) needs for these sizes; 0 if the sizes
+ * are invalid.  Pure host function, callable without a GPU. */
+size_t lapattn_workspace_size(int B, int H, int n, int d, int m, int ns_iters,
+                              int dtype, int for_backward);
+
+/* Forward pass (Algorithm 1 with Algorithm 2 as the pseudoinverse, the
+ * key-summary reordering of Sec. 3.2, and the normalisation chosen in opts).
+ * lambda > 0 is the kernel scale, m the number of landmarks (1 <= m <= min(n, 64)),
+ * ns_iters the number T of Newton-Schulz updates (T = 0 uses X_0). */
+int lapattn_forward(const void* Q, const void* K, const void* V, void* Out,
+                    int B, int H, int n, int d, int m, float lambda, int ns_iters,
+                    int dtype, const lapattn_opts* opts,
+                    void* workspace, size_t workspace_bytes, lapattn_stream_t stream);
+
+/* Backward pass: dQ, dK, dV = gradients of sum(Out * dOut) with respect to
+ * Q, K, V, through the landmark means, the three kernel blocks and every
+ * Newton-Schulz update including the scale of X_0 (kernel gradient of App. A,
+ * with sign(0) = 0; ties in the norm maxima go to the lowest index).  The
+ * forward internals are recomputed; nothing is kept from a forward call.
+ * Only dtype = LAPATTN_FP32 is supported. */
+int lapattn_backward(const void* Q, const void* K, const void* V, const void* dOut,
+                     void* dQ, void* dK, void* dV,
+                     int B, int H, int n, int d, int m, float lambda, int ns_iters,
+                     int dtype, const lapattn_opts* opts,
+                     void* workspace, size_t workspace_bytes, lapattn_stream_t stream);
+
+/* Human-readable name of a status code (static storage). */
+const char* lapattn_status_str(int status);
+
+/* Kernel timing (a measurement aid).  lapattn_timing_enable(1) clears the record
+ * and makes every following forward/backward call record a HIP event pair around
+ * each kernel it launches, on the caller's stream; lapattn_timing_enable(0) stops
+ * recording (the record is kept).  lapattn_timing_read() waits for the recorded
+ * events, writes up to `cap` per-launch durations in milliseconds (launch order,
+ * over all calls since timing was enabled) into ms, and returns the number of
+ * recorded launches (-1 on a HIP error).  lapattn_timing_name(i) names launch i
+ * (static storage; "" when out of range).  Timing is process-wide state guarded
+ * by a mutex and adds two event records per kernel: keep it off outside
+ * measurement.  Returns of lapattn_timing_enable: the previous setting. */
+int lapattn_timing_enable(int enable);
+int lapattn_timing_read(float* ms, int cap);
+const char* lapattn_timing_name(int index);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LAPATTN_H */

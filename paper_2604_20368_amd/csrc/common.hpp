@@ -1,0 +1,48 @@
+// common.hpp -- small device helpers shared by the lapattn HIP kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace lapattn {
+
+enum { DT_F32 = 0, DT_BF16 = 1 };
+enum { NORM_INLINE = 0, NORM_ROWSUM = 1, NORM_NONE = 2 };
+
+// Element access for the two storage types.  bf16 is carried as raw 16-bit
+// patterns; widening is exact, narrowing rounds to nearest even.
+template <int DT> struct elem;
+template <> struct elem<DT_F32> {
+    using type = float;
+    static __device__ __forceinline__ float load(const float* p, size_t i) { return p[i]; }
+    static __device__ __forceinline__ void store(float* p, size_t i, float v) { p[i] = v; }
+};
+template <> struct elem<DT_BF16> {
+    using type = uint16_t;
+    static __device__ __forceinline__ float load(const uint16_t* p, size_t i) {
+        return __uint_as_float(((uint32_t)p[i]) << 16);
+    }
+    static __device__ __forceinline__ void store(uint16_t* p, size_t i, float v) {
+        uint32_t u = __float_as_uint(v);
+        if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) {
+            p[i] = (uint16_t)((u >> 16) | 0x0040u);           // quiet NaN stays NaN
+        } else {
+            u += 0x7fffu + ((u >> 16) & 1u);                  // round to nearest even
+            p[i] = (uint16_t)(u >> 16);
+        }
+    }
+};
+
+// Landmark segments: segment l covers tokens [floor(l n/m), floor((l+1) n/m)).
+__device__ __host__ __forceinline__ int seg_start(int l, int n, int m) {
+    return (int)(((long long)l * n) / m);
+}
+// The segment holding token i: the largest l with seg_start(l) <= i.
+__device__ __host__ __forceinline__ int seg_of(int i, int n, int m) {
+    return (int)((((long long)i + 1) * m - 1) / n);
+}
+
+__device__ __forceinline__ float sgnf(float x) { return (float)((x > 0.f) - (x < 0.f)); }
+__device__ __forceinline__ double sgnd(double x) { return (double)((x > 0.0) - (x < 0.0)); }
+
+}  // namespace lapattn

@@ -1,0 +1,396 @@
+// fwd.hip -- forward kernels of Nystrom-approximated Laplacian-kernel attention.
+//
+//   pool_kernel         landmark means (Sec. 4.2, sampling; 1-D segments)
+//   key_summary_kernel  U = K_LK [V | 1], split over key chunks (Sec. 3.2, Eq. (3) key summaries;
+//                       K_LK of Algorithm 1 in the orientation K_QL X K_LK)
+//   ns_solve_kernel     K_LL, Algorithm 2 in fp64, then M = X_T U
+//   query_out_kernel    Y = K_QL M and the normalisation (Eq. (8), Eq. (4))
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace lapattn {
+
+// ------------------------------------------------------------------------------------------
+// Landmark means.  grid (m, BH), 256 threads: thread (r, c) sums rows r, r+R, ... of the
+// segment in column c; the R partial sums are added in a fixed order (deterministic).
+template <int DT>
+__global__ __launch_bounds__(256) void pool_kernel(const typename elem<DT>::type* __restrict__ Q,
+                                                   const typename elem<DT>::type* __restrict__ K,
+                                                   const typename elem<DT>::type* __restrict__ V,
+                                                   float* __restrict__ qt, float* __restrict__ kt,
+                                                   double* __restrict__ vseg, int n, int d, int m) {
+    const int l = blockIdx.x, h = blockIdx.y;
+    const int s0 = seg_start(l, n, m), s1 = seg_start(l + 1, n, m);
+    const int c = threadIdx.x % d, r = threadIdx.x / d, R = blockDim.x / d;
+    const size_t base = (size_t)h * n * d;
+    double sq = 0.0, sk = 0.0, sv = 0.0;
+    for (int i = s0 + r; i < s1; i += R) {
+        const size_t idx = base + (size_t)i * d + c;
+        sq += elem<DT>::load(Q, idx);
+        sk += elem<DT>::load(K, idx);
+        sv += elem<DT>::load(V, idx);
+    }
+    __shared__ double red[3][256];
+    red[0][threadIdx.x] = sq;
+    red[1][threadIdx.x] = sk;
+    red[2][threadIdx.x] = sv;
+    __syncthreads();
+    if (r == 0) {
+        double a = 0.0, b = 0.0, e = 0.0;
+        for (int rr = 0; rr < R; ++rr) {
+            a += red[0][rr * d + c];
+            b += red[1][rr * d + c];
+            e += red[2][rr * d + c];
+        }
+        const double cnt = (double)(s1 - s0);
+        const size_t o = ((size_t)h * m + l) * d + c;
+        qt[o] = (float)(a / cnt);
+        kt[o] = (float)(b / cnt);
+        vseg[o] = e;
+    }
+}
+
+// ------------------------------------------------------------------------------------------
+// Key-side summary.  grid (nkc, BH), 256 threads.  Each block walks its chunk of keys in
+// tiles of 64: thread (jl, g) evaluates k(qt_a, k_j) for key jl of the tile and landmarks
+// 16g..16g+15 into LDS, then every thread accumulates its share of the m x (d+1) product
+// with the value tile.  Rows a >= m are zero.
+template <int DT, int D>
+__global__ __launch_bounds__(256) void key_summary_kernel(const typename elem<DT>::type* __restrict__ K,
+                                                          const typename elem<DT>::type* __restrict__ V,
+                                                          const float* __restrict__ qt,
+                                                          float* __restrict__ Upart, int n, int m,
+                                                          float kscale, int chunk_keys, int nkc) {
+    constexpr int TJ = 64;
+    constexpr int D1 = D + 1;
+    constexpr int NO = (64 * D1 + 255) / 256;
+    const int chunk = blockIdx.x, h = blockIdx.y, tid = threadIdx.x;
+    __shared__ float sQ[64 * D];
+    __shared__ float sB[64][TJ + 1];
+    __shared__ float sV[TJ][D + 1];
+    for (int e = tid; e < 64 * D; e += 256) sQ[e] = (e < m * D) ? qt[(size_t)h * m * D + e] : 0.f;
+    const int j0 = chunk * chunk_keys, j1 = min(n, j0 + chunk_keys);
+    float acc[NO];
+#pragma unroll
+    for (int r = 0; r < NO; ++r) acc[r] = 0.f;
+    const int jl = tid & 63, g = tid >> 6;
+    for (int jt = j0; jt < j1; jt += TJ) {
+        const int nj = min(TJ, j1 - jt);
+        __syncthreads();
+        for (int e = tid; e < TJ * D; e += 256) {
+            const int r = e / D, c = e % D;
+            sV[r][c] = (r < nj) ? elem<DT>::load(V, ((size_t)h * n + jt + r) * D + c) : 0.f;
+        }
+        if (jl < nj) {
+            float kreg[D];
+#pragma unroll
+            for (int c = 0; c < D; ++c) kreg[c] = elem<DT>::load(K, ((size_t)h * n + jt + jl) * D + c);
+            for (int a = 16 * g; a < 16 * g + 16; ++a) {
+                float v = 0.f;
+                if (a < m) {
+                    float dist = 0.f;
+#pragma unroll
+                    for (int c = 0; c < D; ++c) dist += fabsf(sQ[a * D + c] - kreg[c]);
+                    v = exp2f(dist * kscale);
+                }
+                sB[a][jl] = v;
+            }
+        } else {
+            for (int a = 16 * g; a < 16 * g + 16; ++a) sB[a][jl] = 0.f;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int r = 0; r < NO; ++r) {
+            const int o = tid + 256 * r;
+            if (o < 64 * D1) {
+                const int a = o / D1, c = o % D1;
+                float s = 0.f;
+                if (c < D) {
+                    for (int j = 0; j < TJ; ++j) s += sB[a][j] * sV[j][c];
+                } else {
+                    for (int j = 0; j < TJ; ++j) s += sB[a][j];
+                }
+                acc[r] += s;
+            }
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < NO; ++r) {
+        const int o = tid + 256 * r;
+        if (o < 64 * D1) {
+            const int a = o / D1, c = o % D1;
+            if (a < m) Upart[(((size_t)h * nkc + chunk) * m + a) * D1 + c] = acc[r];
+        }
+    }
+}
+
+// ------------------------------------------------------------------------------------------
+// Register-blocked MP x MP fp64 product for 256 threads: thread (br, bc) of a 16 x 16 grid
+// owns the RB x RB block at rows RB*br.., columns RB*bc.. of op(A) op(B).
+template <int MP, bool TA, bool TB>
+__device__ __forceinline__ void mm_block(const double* __restrict__ A, const double* __restrict__ B,
+                                         double (&r)[MP / 16][MP / 16]) {
+    constexpr int RB = MP / 16;
+    const int br = threadIdx.x / 16, bc = threadIdx.x % 16;
+#pragma unroll
+    for (int i = 0; i < RB; ++i)
+#pragma unroll
+        for (int j = 0; j < RB; ++j) r[i][j] = 0.0;
+    for (int k = 0; k < MP; ++k) {
+        double a[RB], b[RB];
+#pragma unroll
+        for (int i = 0; i < RB; ++i) a[i] = TA ? A[k * MP + RB * br + i] : A[(RB * br + i) * MP + k];
+#pragma unroll
+        for (int j = 0; j < RB; ++j) b[j] = TB ? B[(RB * bc + j) * MP + k] : B[k * MP + RB * bc + j];
+#pragma unroll
+        for (int i = 0; i < RB; ++i)
+#pragma unroll
+            for (int j = 0; j < RB; ++j) r[i][j] = fma(a[i], b[j], r[i][j]);
+    }
+}
+
+// ------------------------------------------------------------------------------------------
+// Newton-Schulz solve, one block of 256 threads per head, fp64 in LDS, matrices padded to
+// MP x MP with zeros (the padding stays zero under every update).
+//   W = K_LL + eps I,  c = ||W||_1 ||W||_inf,  X0 = W^T / c (X := 0 if c = 0),
+//   X_{t+1} = X_t (2I - W X_t);  then U = sum of the key-chunk partials, M = X_T U.
+template <int MP, int D>
+__global__ __launch_bounds__(256) void ns_solve_kernel(const float* __restrict__ qt, const float* __restrict__ kt,
+                                                       const float* __restrict__ Upart,
+                                                       const double* __restrict__ vseg,
+                                                       double* __restrict__ Xs, double* __restrict__ cinfo,
+                                                       float* __restrict__ U, float* __restrict__ M,
+                                                       float* __restrict__ vbar, int n, int m, int T,
+                                                       double lambda, double eps, int nkc, int store_all) {
+    constexpr int RB = MP / 16;
+    constexpr int D1 = D + 1;
+    // X, W, T (MP x MP each); after the iteration U (MP x D1) reuses the space from W on.
+    constexpr int LDSN = (3 * MP * MP > MP * MP + MP * D1) ? 3 * MP * MP : MP * MP + MP * D1;
+    __shared__ double lds[LDSN];
+    __shared__ double sred[2 * MP];
+    __shared__ double sc;
+    double* sX = lds;
+    double* sW = lds + MP * MP;
+    double* sT = lds + 2 * MP * MP;
+    const int h = blockIdx.x, tid = threadIdx.x;
+    const float* q = qt + (size_t)h * m * D;
+    const float* k = kt + (size_t)h * m * D;
+
+    for (int e = tid; e < MP * MP; e += 256) {
+        const int a = e / MP, b = e % MP;
+        double w = 0.0;
+        if (a < m && b < m) {
+            double dist = 0.0;
+            for (int c = 0; c < D; ++c) dist += fabs((double)q[a * D + c] - (double)k[b * D + c]);
+            w = exp(-dist / lambda);
+            if (a == b) w += eps;
+        }
+        sW[e] = w;
+    }
+    __syncthreads();
+    if (tid < MP) {
+        double cs = 0.0, rsum = 0.0;
+        for (int a = 0; a < MP; ++a) cs += fabs(sW[a * MP + tid]);
+        for (int b = 0; b < MP; ++b) rsum += fabs(sW[tid * MP + b]);
+        sred[tid] = cs;
+        sred[MP + tid] = rsum;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        double n1 = -1.0, ninf = -1.0;
+        int bs = 0, as = 0;
+        for (int b = 0; b < MP; ++b)
+            if (sred[b] > n1) { n1 = sred[b]; bs = b; }
+        for (int a = 0; a < MP; ++a)
+            if (sred[MP + a] > ninf) { ninf = sred[MP + a]; as = a; }
+        const double c = n1 * ninf;
+        sc = c;
+        cinfo[h * 4 + 0] = c;
+        cinfo[h * 4 + 1] = n1;
+        cinfo[h * 4 + 2] = ninf;
+        cinfo[h * 4 + 3] = (double)(as * 256 + bs);
+    }
+    __syncthreads();
+    const double c = sc;
+    const size_t mm = (size_t)MP * MP;
+    double* Xh = Xs + (size_t)h * (store_all ? (T + 1) : 1) * mm;
+    for (int e = tid; e < MP * MP; e += 256) {
+        const int a = e / MP, b = e % MP;
+        const double x = (c > 0.0) ? sW[b * MP + a] / c : 0.0;
+        sX[e] = x;
+        if (store_all) Xh[e] = x;
+    }
+    __syncthreads();
+    const int br = tid / 16, bc = tid % 16;
+    for (int t = 0; t < T; ++t) {
+        double r[RB][RB];
+        mm_block<MP, false, false>(sW, sX, r);            // W X
+#pragma unroll
+        for (int i = 0; i < RB; ++i)
+#pragma unroll
+            for (int j = 0; j < RB; ++j) {
+                const int a = RB * br + i, b = RB * bc + j;
+                sT[a * MP + b] = (a == b ? 2.0 : 0.0) - r[i][j];
+            }
+        __syncthreads();
+        mm_block<MP, false, false>(sX, sT, r);            // X (2I - W X)
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < RB; ++i)
+#pragma unroll
+            for (int j = 0; j < RB; ++j) {
+                const int a = RB * br + i, b = RB * bc + j;
+                sX[a * MP + b] = r[i][j];
+                if (store_all) Xh[(size_t)(t + 1) * mm + a * MP + b] = r[i][j];
+            }
+        __syncthreads();
+    }
+    if (!store_all)
+        for (int e = tid; e < MP * MP; e += 256) Xh[e] = sX[e];
+
+    // U = sum over key chunks (fixed order), kept in fp64 from the W region on.
+    double* sU = sW;
+    for (int e = tid; e < MP * D1; e += 256) {
+        const int a = e / D1;
+        double u = 0.0;
+        if (a < m)
+            for (int ch = 0; ch < nkc; ++ch) u += (double)Upart[(((size_t)h * nkc + ch) * m) * D1 + e];
+        sU[e] = u;
+        if (a < m) U[(size_t)h * m * D1 + e] = (float)u;
+    }
+    __syncthreads();
+    for (int e = tid; e < m * D1; e += 256) {
+        const int a = e / D1, cc = e % D1;
+        double s = 0.0;
+        for (int b = 0; b < m; ++b) s += sX[a * MP + b] * sU[b * D1 + cc];
+        M[(size_t)h * m * D1 + e] = (float)s;
+    }
+    for (int cc = tid; cc < D; cc += 256) {
+        double s = 0.0;
+        for (int l = 0; l < m; ++l) s += vseg[((size_t)h * m + l) * D + cc];
+        vbar[(size_t)h * D + cc] = (float)(s / n);
+    }
+}
+
+// ------------------------------------------------------------------------------------------
+// Query side.  grid (ceil(n/256), BH), one query per thread:
+//   y = sum_l k(q_i, kt_l) M_l  (d+1 columns),  s_i = y[d],  then the normalisation.
+template <int DT, int D, int NORM>
+__global__ __launch_bounds__(256) void query_out_kernel(const typename elem<DT>::type* __restrict__ Q,
+                                                        typename elem<DT>::type* __restrict__ Out,
+                                                        const float* __restrict__ kt,
+                                                        const float* __restrict__ M,
+                                                        const float* __restrict__ vbar, int n, int m,
+                                                        float kscale) {
+    constexpr int D1 = D + 1;
+    __shared__ float sK[64 * D];
+    __shared__ float sM[64 * D1];
+    __shared__ float sVb[D];
+    const int h = blockIdx.y, tid = threadIdx.x;
+    for (int e = tid; e < m * D; e += 256) sK[e] = kt[(size_t)h * m * D + e];
+    for (int e = tid; e < m * D1; e += 256) sM[e] = M[(size_t)h * m * D1 + e];
+    if (tid < D) sVb[tid] = vbar[(size_t)h * D + tid];
+    __syncthreads();
+    const int i = blockIdx.x * 256 + tid;
+    if (i >= n) return;
+    const size_t row = ((size_t)h * n + i) * D;
+    float q[D], y[D1];
+#pragma unroll
+    for (int c = 0; c < D; ++c) q[c] = elem<DT>::load(Q, row + c);
+#pragma unroll
+    for (int c = 0; c < D1; ++c) y[c] = 0.f;
+    for (int l = 0; l < m; ++l) {
+        float dist = 0.f;
+#pragma unroll
+        for (int c = 0; c < D; ++c) dist += fabsf(q[c] - sK[l * D + c]);
+        const float a = exp2f(dist * kscale);
+#pragma unroll
+        for (int c = 0; c < D1; ++c) y[c] = fmaf(a, sM[l * D1 + c], y[c]);
+    }
+    const float s = y[D];
+#pragma unroll
+    for (int c = 0; c < D; ++c) {
+        float o;
+        if (NORM == NORM_INLINE) o = y[c] + (1.f - s) * sVb[c];
+        else if (NORM == NORM_ROWSUM) o = y[c] / s;
+        else o = y[c];
+        elem<DT>::store(Out, row + c, o);
+    }
+}
+
+// ------------------------------------------------------------------------------------------
+// Launch wrappers.
+
+static inline float kscale_of(float lambda) { return (float)(-1.4426950408889634 / (double)lambda); }
+
+hipError_t launch_pool(int dt, const void* Q, const void* K, const void* V, float* qt, float* kt, double* vseg,
+                       int BH, int n, int d, int m, hipStream_t st) {
+    dim3 grid(m, BH);
+    if (dt == DT_F32)
+        hipLaunchKernelGGL(pool_kernel<DT_F32>, grid, dim3(256), 0, st, (const float*)Q, (const float*)K,
+                           (const float*)V, qt, kt, vseg, n, d, m);
+    else
+        hipLaunchKernelGGL(pool_kernel<DT_BF16>, grid, dim3(256), 0, st, (const uint16_t*)Q, (const uint16_t*)K,
+                           (const uint16_t*)V, qt, kt, vseg, n, d, m);
+    return hipGetLastError();
+}
+
+template <int DT, int D>
+static void key_summary_launch(const void* K, const void* V, const float* qt, float* Upart, int BH, int n, int m,
+                               float kscale, int chunk_keys, int nkc, hipStream_t st) {
+    using T = typename elem<DT>::type;
+    hipLaunchKernelGGL((key_summary_kernel<DT, D>), dim3(nkc, BH), dim3(256), 0, st, (const T*)K, (const T*)V, qt,
+                       Upart, n, m, kscale, chunk_keys, nkc);
+}
+
+hipError_t launch_key_summary(int dt, const void* K, const void* V, const float* qt, float* Upart, int BH, int n,
+                              int d, int m, float lambda, int chunk_keys, int nkc, hipStream_t st) {
+    const float ks = kscale_of(lambda);
+    if (dt == DT_F32 && d == 32) key_summary_launch<DT_F32, 32>(K, V, qt, Upart, BH, n, m, ks, chunk_keys, nkc, st);
+    else if (dt == DT_F32) key_summary_launch<DT_F32, 64>(K, V, qt, Upart, BH, n, m, ks, chunk_keys, nkc, st);
+    else if (d == 32) key_summary_launch<DT_BF16, 32>(K, V, qt, Upart, BH, n, m, ks, chunk_keys, nkc, st);
+    else key_summary_launch<DT_BF16, 64>(K, V, qt, Upart, BH, n, m, ks, chunk_keys, nkc, st);
+    return hipGetLastError();
+}
+
+hipError_t launch_ns_solve(const float* qt, const float* kt, const float* Upart, const double* vseg, double* Xs,
+                           double* cinfo, float* U, float* M, float* vbar, int BH, int n, int d, int m, int T,
+                           double lambda, double eps, int nkc, int store_all, int MP, hipStream_t st) {
+#define LAPATTN_NS(MPv, Dv)                                                                                  \
+    hipLaunchKernelGGL((ns_solve_kernel<MPv, Dv>), dim3(BH), dim3(256), 0, st, qt, kt, Upart, vseg, Xs, cinfo, \
+                       U, M, vbar, n, m, T, lambda, eps, nkc, store_all)
+    if (MP == 32 && d == 32) LAPATTN_NS(32, 32);
+    else if (MP == 32) LAPATTN_NS(32, 64);
+    else if (d == 32) LAPATTN_NS(64, 32);
+    else LAPATTN_NS(64, 64);
+#undef LAPATTN_NS
+    return hipGetLastError();
+}
+
+template <int DT, int D>
+static void query_out_launch(int norm, const void* Q, void* Out, const float* kt, const float* M, const float* vbar,
+                             int BH, int n, int m, float kscale, hipStream_t st) {
+    using T = typename elem<DT>::type;
+    dim3 grid((n + 255) / 256, BH);
+    if (norm == NORM_INLINE)
+        hipLaunchKernelGGL((query_out_kernel<DT, D, NORM_INLINE>), grid, dim3(256), 0, st, (const T*)Q, (T*)Out, kt,
+                           M, vbar, n, m, kscale);
+    else if (norm == NORM_ROWSUM)
+        hipLaunchKernelGGL((query_out_kernel<DT, D, NORM_ROWSUM>), grid, dim3(256), 0, st, (const T*)Q, (T*)Out, kt,
+                           M, vbar, n, m, kscale);
+    else
+        hipLaunchKernelGGL((query_out_kernel<DT, D, NORM_NONE>), grid, dim3(256), 0, st, (const T*)Q, (T*)Out, kt, M,
+                           vbar, n, m, kscale);
+}
+
+hipError_t launch_query_out(int dt, int norm, const void* Q, void* Out, const float* kt, const float* M,
+                            const float* vbar, int BH, int n, int d, int m, float lambda, hipStream_t st) {
+    const float ks = kscale_of(lambda);
+    if (dt == DT_F32 && d == 32) query_out_launch<DT_F32, 32>(norm, Q, Out, kt, M, vbar, BH, n, m, ks, st);
+    else if (dt == DT_F32) query_out_launch<DT_F32, 64>(norm, Q, Out, kt, M, vbar, BH, n, m, ks, st);
+    else if (d == 32) query_out_launch<DT_BF16, 32>(norm, Q, Out, kt, M, vbar, BH, n, m, ks, st);
+    else query_out_launch<DT_BF16, 64>(norm, Q, Out, kt, M, vbar, BH, n, m, ks, st);
+    return hipGetLastError();
+}
+
+}  // namespace lapattn

@@ -1,0 +1,329 @@
+// host.cpp -- the C ABI declared in include/lapattn.h: argument validation, workspace
+// planning, launch sequencing on the caller's stream, optional per-kernel timing.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <mutex>
+#include <new>
+#include <vector>
+
+#include "../../include/lapattn.h"
+#include "kernels.hpp"
+
+namespace {
+
+constexpr int kMaxM = 64;
+constexpr int kMaxT = 64;
+constexpr int kKeyChunk = 512;   // keys per block of the key-summary kernel
+constexpr int kLmChunk = 64;     // tokens per block of the landmark-major backward passes
+
+// ------------------------------------------------------------------------------- validation
+
+int check_shape(int B, int H, int n, int d, int m, float lambda, int T, int dtype, int norm, float eps) {
+    if (B < 1 || H < 1 || n < 1 || m < 1 || m > n) return LAPATTN_ERR_SHAPE;
+    if ((long long)B * H * (long long)n * (d > 0 ? d : 1) >= (1LL << 31)) return LAPATTN_ERR_SHAPE;
+    if (!(std::isfinite(lambda) && lambda > 0.f)) return LAPATTN_ERR_PARAM;
+    if (T < 0 || T > kMaxT) return LAPATTN_ERR_PARAM;
+    if (dtype != LAPATTN_FP32 && dtype != LAPATTN_BF16) return LAPATTN_ERR_PARAM;
+    if (norm != LAPATTN_NORM_INLINE && norm != LAPATTN_NORM_ROWSUM && norm != LAPATTN_NORM_NONE)
+        return LAPATTN_ERR_PARAM;
+    if (!(std::isfinite(eps) && eps >= 0.f)) return LAPATTN_ERR_PARAM;
+    if (d != 32 && d != 64) return LAPATTN_ERR_UNSUPPORTED;
+    if (m > kMaxM) return LAPATTN_ERR_UNSUPPORTED;
+    return LAPATTN_OK;
+}
+
+// ------------------------------------------------------------------------------- workspace plan
+
+struct Plan {
+    size_t qt, kt, vseg, Upart, Xs, cinfo, U, M, vbar;                   // forward
+    size_t Aq, dDq, rs, dYd, dvbar_part, dM_part, dkt_part, dU, dvbar,   // backward
+        dqtW, dktW, dDk, dqt_part;
+    size_t total;
+    int MP, nkc, nqb, nlc;
+};
+
+struct Carver {
+    size_t off = 0;
+    size_t take(size_t bytes) {
+        off = (off + 255) & ~size_t(255);
+        size_t o = off;
+        off += bytes;
+        return o;
+    }
+};
+
+Plan make_plan(int BH, int n, int d, int m, int T, bool bwd) {
+    Plan p{};
+    p.MP = m <= 32 ? 32 : 64;
+    p.nkc = (n + kKeyChunk - 1) / kKeyChunk;
+    p.nqb = (n + 255) / 256;
+    p.nlc = (n + kLmChunk - 1) / kLmChunk;
+    const size_t bh = (size_t)BH, d1 = (size_t)d + 1, f = sizeof(float), g = sizeof(double);
+    const size_t mpp = (size_t)p.MP * p.MP;
+    Carver c;
+    p.qt = c.take(bh * m * d * f);
+    p.kt = c.take(bh * m * d * f);
+    p.vseg = c.take(bh * m * d * g);
+    p.Upart = c.take(bh * p.nkc * m * d1 * f);
+    p.Xs = c.take(bh * (bwd ? (size_t)T + 1 : 1) * mpp * g);
+    p.cinfo = c.take(bh * 4 * g);
+    p.U = c.take(bh * m * d1 * f);
+    p.M = c.take(bh * m * d1 * f);
+    p.vbar = c.take(bh * d * f);
+    if (bwd) {
+        p.Aq = c.take(bh * n * m * f);
+        p.dDq = c.take(bh * n * m * f);
+        p.rs = c.take(bh * n * f);
+        p.dYd = c.take(bh * n * f);
+        p.dvbar_part = c.take(bh * p.nqb * d * f);
+        p.dM_part = c.take(bh * p.nlc * m * d1 * f);
+        p.dkt_part = c.take(bh * p.nlc * m * d * f);
+        p.dU = c.take(bh * m * d1 * f);
+        p.dvbar = c.take(bh * d * f);
+        p.dqtW = c.take(bh * m * d * f);
+        p.dktW = c.take(bh * m * d * f);
+        p.dDk = c.take(bh * n * m * f);
+        p.dqt_part = c.take(bh * p.nlc * m * d * f);
+    }
+    p.total = (c.off + 255) & ~size_t(255);
+    return p;
+}
+
+template <typename T>
+T* at(void* ws, size_t off) {
+    return reinterpret_cast<T*>(static_cast<char*>(ws) + off);
+}
+
+// ------------------------------------------------------------------------------- timing
+
+struct Timing {
+    std::mutex mu;
+    bool enabled = false;
+    std::vector<const char*> names;
+    std::vector<hipEvent_t> ev;   // 2 per kernel of the last call
+    size_t used = 0;
+};
+
+Timing& timing() {
+    static Timing* t = new Timing();
+    return *t;
+}
+
+// Records one (start, stop) pair around each launch while timing is enabled; the
+// record accumulates over calls until timing is enabled again.
+class Recorder {
+  public:
+    explicit Recorder(hipStream_t st) : st_(st) {
+        Timing& t = timing();
+        std::lock_guard<std::mutex> g(t.mu);
+        on_ = t.enabled;
+    }
+    hipError_t run(const char* name, hipError_t (*fn)(void*), void* ctx) {
+        if (!on_) return fn(ctx);
+        Timing& t = timing();
+        std::lock_guard<std::mutex> g(t.mu);
+        while (t.ev.size() < t.used + 2) {
+            hipEvent_t e;
+            hipError_t err = hipEventCreate(&e);
+            if (err != hipSuccess) return err;
+            t.ev.push_back(e);
+        }
+        hipEvent_t a = t.ev[t.used], b = t.ev[t.used + 1];
+        hipError_t err = hipEventRecord(a, st_);
+        if (err != hipSuccess) return err;
+        err = fn(ctx);
+        if (err != hipSuccess) return err;
+        err = hipEventRecord(b, st_);
+        t.used += 2;
+        t.names.push_back(name);
+        return err;
+    }
+
+  private:
+    hipStream_t st_;
+    bool on_ = false;
+};
+
+// A launch is a lambda captured by reference; this adapter turns it into (fn, ctx).
+template <typename F>
+hipError_t run_named(Recorder& rec, const char* name, F&& f) {
+    return rec.run(name, [](void* ctx) -> hipError_t { return (*static_cast<F*>(ctx))(); }, (void*)&f);
+}
+
+int norm_of(const lapattn_opts* o) { return o ? o->norm : LAPATTN_NORM_INLINE; }
+float eps_of(const lapattn_opts* o) { return o ? o->eps : 0.f; }
+
+// The forward stages shared by lapattn_forward and lapattn_backward (which recomputes them).
+hipError_t forward_internals(Recorder& rec, const Plan& p, const void* Q, const void* K, const void* V, void* ws,
+                             int BH, int n, int d, int m, float lambda, int T, int dtype, float eps, bool store_all,
+                             hipStream_t st) {
+    float* qt = at<float>(ws, p.qt);
+    float* kt = at<float>(ws, p.kt);
+    double* vseg = at<double>(ws, p.vseg);
+    float* Upart = at<float>(ws, p.Upart);
+    hipError_t e;
+    e = run_named(rec, "pool", [&] { return lapattn::launch_pool(dtype, Q, K, V, qt, kt, vseg, BH, n, d, m, st); });
+    if (e != hipSuccess) return e;
+    e = run_named(rec, "key_summary", [&] {
+        return lapattn::launch_key_summary(dtype, K, V, qt, Upart, BH, n, d, m, lambda, kKeyChunk, p.nkc, st);
+    });
+    if (e != hipSuccess) return e;
+    e = run_named(rec, "ns_solve", [&] {
+        return lapattn::launch_ns_solve(qt, kt, Upart, vseg, at<double>(ws, p.Xs), at<double>(ws, p.cinfo),
+                                        at<float>(ws, p.U), at<float>(ws, p.M), at<float>(ws, p.vbar), BH, n, d, m, T,
+                                        (double)lambda, (double)eps, p.nkc, store_all ? 1 : 0, p.MP, st);
+    });
+    return e;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t lapattn_workspace_size(int B, int H, int n, int d, int m, int ns_iters, int dtype, int for_backward) {
+    if (check_shape(B, H, n, d, m, 1.f, ns_iters, dtype, LAPATTN_NORM_INLINE, 0.f) != LAPATTN_OK) return 0;
+    return make_plan(B * H, n, d, m, ns_iters, for_backward != 0).total;
+}
+
+int lapattn_forward(const void* Q, const void* K, const void* V, void* Out, int B, int H, int n, int d, int m,
+                    float lambda, int ns_iters, int dtype, const lapattn_opts* opts, void* workspace,
+                    size_t workspace_bytes, lapattn_stream_t stream) {
+    try {
+        if (!Q || !K || !V || !Out) return LAPATTN_ERR_NULL;
+        const int norm = norm_of(opts);
+        const float eps = eps_of(opts);
+        int rc = check_shape(B, H, n, d, m, lambda, ns_iters, dtype, norm, eps);
+        if (rc) return rc;
+        const int BH = B * H;
+        const Plan p = make_plan(BH, n, d, m, ns_iters, false);
+        if (!workspace || workspace_bytes < p.total) return LAPATTN_ERR_WORKSPACE;
+        hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+        Recorder rec(st);
+        hipError_t e = forward_internals(rec, p, Q, K, V, workspace, BH, n, d, m, lambda, ns_iters, dtype, eps,
+                                         false, st);
+        if (e != hipSuccess) return LAPATTN_ERR_HIP;
+        e = run_named(rec, "query_out", [&] {
+            return lapattn::launch_query_out(dtype, norm, Q, Out, at<float>(workspace, p.kt),
+                                             at<float>(workspace, p.M), at<float>(workspace, p.vbar), BH, n, d, m,
+                                             lambda, st);
+        });
+        return e == hipSuccess ? LAPATTN_OK : LAPATTN_ERR_HIP;
+    } catch (...) {
+        return LAPATTN_ERR_HIP;
+    }
+}
+
+int lapattn_backward(const void* Q, const void* K, const void* V, const void* dOut, void* dQ, void* dK, void* dV,
+                     int B, int H, int n, int d, int m, float lambda, int ns_iters, int dtype,
+                     const lapattn_opts* opts, void* workspace, size_t workspace_bytes, lapattn_stream_t stream) {
+    try {
+        if (!Q || !K || !V || !dOut || !dQ || !dK || !dV) return LAPATTN_ERR_NULL;
+        const int norm = norm_of(opts);
+        const float eps = eps_of(opts);
+        int rc = check_shape(B, H, n, d, m, lambda, ns_iters, dtype, norm, eps);
+        if (rc) return rc;
+        if (dtype != LAPATTN_FP32) return LAPATTN_ERR_UNSUPPORTED;
+        const int BH = B * H;
+        const Plan p = make_plan(BH, n, d, m, ns_iters, true);
+        if (!workspace || workspace_bytes < p.total) return LAPATTN_ERR_WORKSPACE;
+        hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+        void* ws = workspace;
+        Recorder rec(st);
+        hipError_t e = forward_internals(rec, p, Q, K, V, ws, BH, n, d, m, lambda, ns_iters, dtype, eps, true, st);
+        if (e != hipSuccess) return LAPATTN_ERR_HIP;
+        const float* q = static_cast<const float*>(Q);
+        const float* k = static_cast<const float*>(K);
+        const float* v = static_cast<const float*>(V);
+        const float* g = static_cast<const float*>(dOut);
+        float* dq = static_cast<float*>(dQ);
+        float* dk = static_cast<float*>(dK);
+        float* dv = static_cast<float*>(dV);
+        e = run_named(rec, "bwd_query", [&] {
+            return lapattn::launch_bwd_query(norm, q, g, dq, at<float>(ws, p.kt), at<float>(ws, p.M),
+                                             at<float>(ws, p.vbar), at<float>(ws, p.Aq), at<float>(ws, p.dDq),
+                                             at<float>(ws, p.rs), at<float>(ws, p.dYd), at<float>(ws, p.dvbar_part),
+                                             BH, n, d, m, lambda, p.nqb, st);
+        });
+        if (e != hipSuccess) return LAPATTN_ERR_HIP;
+        e = run_named(rec, "bwd_query_lm", [&] {
+            return lapattn::launch_bwd_query_lm(q, g, at<float>(ws, p.kt), at<float>(ws, p.Aq), at<float>(ws, p.dDq),
+                                                at<float>(ws, p.rs), at<float>(ws, p.dYd), at<float>(ws, p.dM_part),
+                                                at<float>(ws, p.dkt_part), BH, n, d, m, kLmChunk, p.nlc, st);
+        });
+        if (e != hipSuccess) return LAPATTN_ERR_HIP;
+        e = run_named(rec, "bwd_ns", [&] {
+            return lapattn::launch_bwd_ns(at<float>(ws, p.qt), at<float>(ws, p.kt), at<double>(ws, p.Xs),
+                                          at<double>(ws, p.cinfo), at<float>(ws, p.U), at<float>(ws, p.dM_part),
+                                          at<float>(ws, p.dvbar_part), at<float>(ws, p.dU), at<float>(ws, p.dvbar),
+                                          at<float>(ws, p.dqtW), at<float>(ws, p.dktW), BH, n, d, m, ns_iters,
+                                          (double)lambda, (double)eps, p.nlc, p.nqb, p.MP, st);
+        });
+        if (e != hipSuccess) return LAPATTN_ERR_HIP;
+        e = run_named(rec, "bwd_key", [&] {
+            return lapattn::launch_bwd_key(k, v, dk, dv, at<float>(ws, p.qt), at<float>(ws, p.dU),
+                                           at<float>(ws, p.dvbar), at<float>(ws, p.dDk), BH, n, d, m, lambda, st);
+        });
+        if (e != hipSuccess) return LAPATTN_ERR_HIP;
+        e = run_named(rec, "bwd_key_lm", [&] {
+            return lapattn::launch_bwd_key_lm(k, at<float>(ws, p.qt), at<float>(ws, p.dDk), at<float>(ws, p.dqt_part),
+                                              BH, n, d, m, kLmChunk, p.nlc, st);
+        });
+        if (e != hipSuccess) return LAPATTN_ERR_HIP;
+        e = run_named(rec, "bwd_pool", [&] {
+            return lapattn::launch_bwd_pool(dq, dk, at<float>(ws, p.dqtW), at<float>(ws, p.dktW),
+                                            at<float>(ws, p.dqt_part), at<float>(ws, p.dkt_part), BH, n, d, m, p.nlc,
+                                            st);
+        });
+        return e == hipSuccess ? LAPATTN_OK : LAPATTN_ERR_HIP;
+    } catch (...) {
+        return LAPATTN_ERR_HIP;
+    }
+}
+
+const char* lapattn_status_str(int status) {
+    switch (status) {
+        case LAPATTN_OK: return "ok";
+        case LAPATTN_ERR_NULL: return "null pointer argument";
+        case LAPATTN_ERR_SHAPE: return "invalid shape (B, H, n >= 1, 1 <= m <= n, B*H*n*d < 2^31)";
+        case LAPATTN_ERR_PARAM: return "invalid parameter (lambda, ns_iters, eps, norm or dtype)";
+        case LAPATTN_ERR_UNSUPPORTED: return "unsupported configuration (d in {32, 64}, m <= 64, fp32 backward)";
+        case LAPATTN_ERR_WORKSPACE: return "workspace missing or too small";
+        case LAPATTN_ERR_HIP: return "HIP launch failed";
+        default: return "unknown status";
+    }
+}
+
+int lapattn_timing_enable(int enable) {
+    Timing& t = timing();
+    std::lock_guard<std::mutex> g(t.mu);
+    int prev = t.enabled ? 1 : 0;
+    t.enabled = enable != 0;
+    if (t.enabled) {
+        t.names.clear();
+        t.used = 0;
+    }
+    return prev;
+}
+
+int lapattn_timing_read(float* ms, int cap) {
+    Timing& t = timing();
+    std::lock_guard<std::mutex> g(t.mu);
+    const int nk = (int)t.names.size();
+    for (int i = 0; i < nk && i < cap && ms; ++i) {
+        if (hipEventSynchronize(t.ev[2 * i + 1]) != hipSuccess) return -1;
+        float v = 0.f;
+        if (hipEventElapsedTime(&v, t.ev[2 * i], t.ev[2 * i + 1]) != hipSuccess) return -1;
+        ms[i] = v;
+    }
+    return nk;
+}
+
+const char* lapattn_timing_name(int index) {
+    Timing& t = timing();
+    std::lock_guard<std::mutex> g(t.mu);
+    if (index < 0 || index >= (int)t.names.size()) return "";
+    return t.names[index];
+}
+
+}  // extern "C"

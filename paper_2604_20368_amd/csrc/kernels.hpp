@@ -1,0 +1,75 @@
+// kernels.hpp -- launch wrappers of the lapattn HIP kernels (internal to the library).
+//
+// Workspace arrays are described in host.cpp; every pointer here is device memory.
+// All wrappers enqueue on `st` and return the launch status.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+
+namespace lapattn {
+
+// Forward ---------------------------------------------------------------------
+
+// Landmark means qt, kt [BH][m][d] (fp32) and per-segment value sums vseg [BH][m][d] (fp64).
+hipError_t launch_pool(int dt, const void* Q, const void* K, const void* V,
+                       float* qt, float* kt, double* vseg,
+                       int BH, int n, int d, int m, hipStream_t st);
+
+// Key-side summary: per key chunk, Upart[h][chunk][a][c] = sum_j k(qt_a, k_j) [v_j | 1]_c.
+hipError_t launch_key_summary(int dt, const void* K, const void* V, const float* qt, float* Upart,
+                              int BH, int n, int d, int m, float lambda, int chunk_keys, int nkc,
+                              hipStream_t st);
+
+// Newton-Schulz on K_LL and the solved matrix M = X_T U.
+//   Xs:    [BH][store_all ? T+1 : 1][MP][MP] fp64 iterates (padded to MP)
+//   cinfo: [BH][4] fp64: scale c, ||W||_1, ||W||_inf, (a* * 256 + b*)
+//   U, M:  [BH][m][d+1] fp32;  vbar: [BH][d] fp32
+hipError_t launch_ns_solve(const float* qt, const float* kt, const float* Upart, const double* vseg,
+                           double* Xs, double* cinfo, float* U, float* M, float* vbar,
+                           int BH, int n, int d, int m, int T, double lambda, double eps, int nkc,
+                           int store_all, int MP, hipStream_t st);
+
+// Query side: Out_i = normalise(sum_l k(q_i, kt_l) M_l).
+hipError_t launch_query_out(int dt, int norm, const void* Q, void* Out, const float* kt, const float* M,
+                            const float* vbar, int BH, int n, int d, int m, float lambda, hipStream_t st);
+
+// Backward (fp32 inputs) --------------------------------------------------------
+
+// Query-major pass: writes the direct dQ term, the kernel values Aq and dDq = -A dA / lambda
+// ([BH][n][m]), per-query dY scale rs and last column dYd ([BH][n]), and per-block
+// partial sums of dvbar ([BH][nqb][d]).
+hipError_t launch_bwd_query(int norm, const float* Q, const float* dO, float* dQ,
+                            const float* kt, const float* M, const float* vbar,
+                            float* Aq, float* dDq, float* rs, float* dYd, float* dvbar_part,
+                            int BH, int n, int d, int m, float lambda, int nqb, hipStream_t st);
+
+// Landmark-major pass over queries: partial dM [BH][nlc][m][d+1] and dkt [BH][nlc][m][d].
+hipError_t launch_bwd_query_lm(const float* Q, const float* dO, const float* kt,
+                               const float* Aq, const float* dDq, const float* rs, const float* dYd,
+                               float* dM_part, float* dkt_part,
+                               int BH, int n, int d, int m, int chunk, int nlc, hipStream_t st);
+
+// Newton-Schulz backward: dU [BH][m][d+1], dvbar [BH][d], and the K_LL gradient
+// mapped to the landmarks, dqtW, dktW [BH][m][d].
+hipError_t launch_bwd_ns(const float* qt, const float* kt, const double* Xs, const double* cinfo,
+                         const float* U, const float* dM_part, const float* dvbar_part,
+                         float* dU, float* dvbar, float* dqtW, float* dktW,
+                         int BH, int n, int d, int m, int T, double lambda, double eps,
+                         int nlc, int nqb, int MP, hipStream_t st);
+
+// Key-major pass: direct dK, final dV, and dDk = -B dB / lambda ([BH][n][m]).
+hipError_t launch_bwd_key(const float* K, const float* V, float* dK, float* dV,
+                          const float* qt, const float* dU, const float* dvbar, float* dDk,
+                          int BH, int n, int d, int m, float lambda, hipStream_t st);
+
+// Landmark-major pass over keys: partial dqt [BH][nlc][m][d].
+hipError_t launch_bwd_key_lm(const float* K, const float* qt, const float* dDk, float* dqt_part,
+                             int BH, int n, int d, int m, int chunk, int nlc, hipStream_t st);
+
+// Landmark-mean backward: dQ_i += dqt_{l(i)} / |S_l|, dK_j += dkt_{l(j)} / |S_l|.
+hipError_t launch_bwd_pool(float* dQ, float* dK, const float* dqtW, const float* dktW,
+                           const float* dqt_part, const float* dkt_part,
+                           int BH, int n, int d, int m, int nlc, hipStream_t st);
+
+}  // namespace lapattn

@@ -1,0 +1,166 @@
+"""ctypes binding of the lapattn C ABI (include/lapattn.h).
+
+Argument marshalling only: tensors are passed as device pointers, the stream is
+torch's current HIP stream, and every step of the computation runs in the HIP
+library.  If the library is missing the calls raise; there is no fallback.
+"""
+import ctypes
+import os
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblapattn.so")
+
+LAPATTN_FP32, LAPATTN_BF16 = 0, 1
+LAPATTN_NORM_INLINE, LAPATTN_NORM_ROWSUM, LAPATTN_NORM_NONE = 0, 1, 2
+LAPATTN_OK, LAPATTN_ERR_NULL, LAPATTN_ERR_SHAPE, LAPATTN_ERR_PARAM = 0, 1, 2, 3
+LAPATTN_ERR_UNSUPPORTED, LAPATTN_ERR_WORKSPACE, LAPATTN_ERR_HIP = 4, 5, 6
+
+EXPORTS = ("lapattn_workspace_size", "lapattn_forward", "lapattn_backward", "lapattn_status_str",
+           "lapattn_timing_enable", "lapattn_timing_read", "lapattn_timing_name")
+
+
+class lapattn_opts(ctypes.Structure):
+    _fields_ = [("norm", ctypes.c_int), ("eps", ctypes.c_float)]
+
+
+class LapattnError(RuntimeError):
+    def __init__(self, code, where):
+        super().__init__("%s failed: %s (status %d)" % (where, lapattn_status_str(code), code))
+        self.code = code
+
+
+_lib = None
+
+
+def library():
+    """Open liblapattn.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError("HIP library %s is missing: build it with __graft_entry__.build() "
+                           "or python -m paper_2604_20368_amd.build" % LIB_PATH)
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, ci, cf, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+    lib.lapattn_workspace_size.restype = sz
+    lib.lapattn_workspace_size.argtypes = [ci] * 8
+    lib.lapattn_forward.restype = ci
+    lib.lapattn_forward.argtypes = [vp] * 4 + [ci] * 5 + [cf, ci, ci, ctypes.POINTER(lapattn_opts), vp, sz, vp]
+    lib.lapattn_backward.restype = ci
+    lib.lapattn_backward.argtypes = [vp] * 7 + [ci] * 5 + [cf, ci, ci, ctypes.POINTER(lapattn_opts), vp, sz, vp]
+    lib.lapattn_status_str.restype = ctypes.c_char_p
+    lib.lapattn_status_str.argtypes = [ci]
+    lib.lapattn_timing_enable.restype = ci
+    lib.lapattn_timing_enable.argtypes = [ci]
+    lib.lapattn_timing_read.restype = ci
+    lib.lapattn_timing_read.argtypes = [ctypes.POINTER(ctypes.c_float), ci]
+    lib.lapattn_timing_name.restype = ctypes.c_char_p
+    lib.lapattn_timing_name.argtypes = [ci]
+    _lib = lib
+    return lib
+
+
+# ------------------------------------------------------------------------------ raw C-ABI calls
+
+def lapattn_status_str(code):
+    return library().lapattn_status_str(int(code)).decode()
+
+
+def lapattn_workspace_size(B, H, n, d, m, ns_iters, dtype, for_backward):
+    return int(library().lapattn_workspace_size(B, H, n, d, m, ns_iters, dtype, int(bool(for_backward))))
+
+
+def _opts(norm, eps):
+    return ctypes.byref(lapattn_opts(int(norm), float(eps)))
+
+
+def lapattn_forward(Q, K, V, Out, B, H, n, d, m, lam, ns_iters, dtype, norm=LAPATTN_NORM_INLINE, eps=0.0,
+                    workspace=0, workspace_bytes=0, stream=0):
+    """Raw call with integer device addresses; returns the status code."""
+    return library().lapattn_forward(Q, K, V, Out, B, H, n, d, m, float(lam), ns_iters, dtype, _opts(norm, eps),
+                                     workspace, workspace_bytes, stream)
+
+
+def lapattn_backward(Q, K, V, dO, dQ, dK, dV, B, H, n, d, m, lam, ns_iters, dtype, norm=LAPATTN_NORM_INLINE,
+                     eps=0.0, workspace=0, workspace_bytes=0, stream=0):
+    return library().lapattn_backward(Q, K, V, dO, dQ, dK, dV, B, H, n, d, m, float(lam), ns_iters, dtype,
+                                      _opts(norm, eps), workspace, workspace_bytes, stream)
+
+
+def lapattn_timing_enable(on):
+    return library().lapattn_timing_enable(int(bool(on)))
+
+
+def lapattn_timing_read(cap=32):
+    buf = (ctypes.c_float * cap)()
+    k = library().lapattn_timing_read(buf, cap)
+    if k < 0:
+        raise RuntimeError("lapattn_timing_read failed")
+    return [(library().lapattn_timing_name(i).decode(), buf[i]) for i in range(min(k, cap))]
+
+
+# ------------------------------------------------------------------------------ torch marshalling
+
+def _dtype_code(t):
+    import torch
+    if t.dtype == torch.float32:
+        return LAPATTN_FP32
+    if t.dtype == torch.bfloat16:
+        return LAPATTN_BF16
+    raise TypeError("lapattn takes float32 or bfloat16 tensors, got %s" % t.dtype)
+
+
+def _check(*ts):
+    import torch
+    ref = ts[0]
+    for t in ts:
+        if not isinstance(t, torch.Tensor) or not t.is_cuda:
+            raise TypeError("lapattn needs device tensors")
+        if not t.is_contiguous() or t.shape != ref.shape or t.dtype != ref.dtype or t.device != ref.device:
+            raise ValueError("lapattn needs contiguous [B,H,n,d] tensors of one dtype and device")
+    if ref.dim() != 4:
+        raise ValueError("lapattn needs [B,H,n,d] tensors")
+
+
+def _stream(t):
+    import torch
+    return torch.cuda.current_stream(t.device).cuda_stream
+
+
+def workspace(Q, m, ns_iters, for_backward=False):
+    import torch
+    B, H, n, d = Q.shape
+    nbytes = lapattn_workspace_size(B, H, n, d, m, ns_iters, _dtype_code(Q), for_backward)
+    if nbytes == 0:
+        raise ValueError("invalid lapattn sizes")
+    return torch.empty(nbytes, dtype=torch.uint8, device=Q.device)
+
+
+def forward(Q, K, V, m, lam, ns_iters, norm=LAPATTN_NORM_INLINE, eps=0.0, out=None, ws=None):
+    """Out = lapattn(Q, K, V) on torch's current stream."""
+    import torch
+    _check(Q, K, V)
+    out = torch.empty_like(Q) if out is None else out
+    _check(Q, out)
+    ws = workspace(Q, m, ns_iters, False) if ws is None else ws
+    B, H, n, d = Q.shape
+    rc = lapattn_forward(Q.data_ptr(), K.data_ptr(), V.data_ptr(), out.data_ptr(), B, H, n, d, m, lam, ns_iters,
+                         _dtype_code(Q), norm, eps, ws.data_ptr(), ws.numel(), _stream(Q))
+    if rc != LAPATTN_OK:
+        raise LapattnError(rc, "lapattn_forward")
+    return out
+
+
+def backward(Q, K, V, dO, m, lam, ns_iters, norm=LAPATTN_NORM_INLINE, eps=0.0, grads=None, ws=None):
+    """(dQ, dK, dV) of sum(Out * dO) on torch's current stream."""
+    import torch
+    _check(Q, K, V, dO)
+    dQ, dK, dV = grads if grads is not None else (torch.empty_like(Q), torch.empty_like(Q), torch.empty_like(Q))
+    _check(Q, dQ, dK, dV)
+    ws = workspace(Q, m, ns_iters, True) if ws is None else ws
+    B, H, n, d = Q.shape
+    rc = lapattn_backward(Q.data_ptr(), K.data_ptr(), V.data_ptr(), dO.data_ptr(), dQ.data_ptr(), dK.data_ptr(),
+                          dV.data_ptr(), B, H, n, d, m, lam, ns_iters, _dtype_code(Q), norm, eps, ws.data_ptr(),
+                          ws.numel(), _stream(Q))
+    if rc != LAPATTN_OK:
+        raise LapattnError(rc, "lapattn_backward")
+    return dQ, dK, dV

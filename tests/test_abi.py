@@ -1,0 +1,99 @@
+"""The C ABI on the host (no GPU needed): the library loads, exports every entry
+point the header declares, and rejects bad arguments before touching the device.
+Invalid calls only: a rejected call returns before any HIP call."""
+import os
+import re
+
+import pytest
+
+from paper_2604_20368_amd import lapattn as L
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "lapattn.h")
+
+FAKE = 0x1000   # non-null address that is never dereferenced: every call below is rejected first
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(lapattn_\w+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    lib = L.library()
+    names = declared_functions()
+    assert set(names) == set(L.EXPORTS)
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def test_status_strings():
+    for code in range(7):
+        assert L.lapattn_status_str(code) and L.lapattn_status_str(code) != "unknown status"
+    assert L.lapattn_status_str(99) == "unknown status"
+
+
+def fwd(**kw):
+    args = dict(Q=FAKE, K=FAKE, V=FAKE, Out=FAKE, B=1, H=2, n=100, d=32, m=8, lam=1.0, ns_iters=4, dtype=0,
+                norm=0, eps=0.0, workspace=FAKE, workspace_bytes=0)
+    args.update(kw)
+    return L.lapattn_forward(**args)
+
+
+def bwd(**kw):
+    args = dict(Q=FAKE, K=FAKE, V=FAKE, dO=FAKE, dQ=FAKE, dK=FAKE, dV=FAKE, B=1, H=2, n=100, d=32, m=8, lam=1.0,
+                ns_iters=4, dtype=0, norm=0, eps=0.0, workspace=FAKE, workspace_bytes=0)
+    args.update(kw)
+    return L.lapattn_backward(**args)
+
+
+@pytest.mark.parametrize("call", [fwd, bwd])
+def test_argument_validation(call):
+    ptrs = ["Q", "K", "V"] + (["Out"] if call is fwd else ["dO", "dQ", "dK", "dV"])
+    for p in ptrs:
+        assert call(**{p: 0}) == L.LAPATTN_ERR_NULL
+    assert call(B=0) == L.LAPATTN_ERR_SHAPE
+    assert call(H=0) == L.LAPATTN_ERR_SHAPE
+    assert call(n=0) == L.LAPATTN_ERR_SHAPE
+    assert call(m=0) == L.LAPATTN_ERR_SHAPE
+    assert call(m=101) == L.LAPATTN_ERR_SHAPE                     # m > n
+    assert call(B=1 << 12, H=1 << 10, n=1 << 10, d=32) == L.LAPATTN_ERR_SHAPE   # B*H*n*d >= 2^31
+    assert call(lam=0.0) == L.LAPATTN_ERR_PARAM
+    assert call(lam=-1.0) == L.LAPATTN_ERR_PARAM
+    assert call(lam=float("inf")) == L.LAPATTN_ERR_PARAM
+    assert call(lam=float("nan")) == L.LAPATTN_ERR_PARAM
+    assert call(ns_iters=-1) == L.LAPATTN_ERR_PARAM
+    assert call(ns_iters=65) == L.LAPATTN_ERR_PARAM
+    assert call(dtype=2) == L.LAPATTN_ERR_PARAM
+    assert call(norm=3) == L.LAPATTN_ERR_PARAM
+    assert call(eps=-0.1) == L.LAPATTN_ERR_PARAM
+    assert call(eps=float("nan")) == L.LAPATTN_ERR_PARAM
+    assert call(d=48) == L.LAPATTN_ERR_UNSUPPORTED
+    assert call(m=65) == L.LAPATTN_ERR_UNSUPPORTED
+    assert call(workspace_bytes=0) == L.LAPATTN_ERR_WORKSPACE    # valid sizes, workspace too small
+    need = L.lapattn_workspace_size(1, 2, 100, 32, 8, 4, 0, call is bwd)
+    assert call(workspace_bytes=need - 1) == L.LAPATTN_ERR_WORKSPACE
+    assert call(workspace=0, workspace_bytes=need) == L.LAPATTN_ERR_WORKSPACE
+
+
+def test_backward_rejects_bf16_before_launch():
+    need = L.lapattn_workspace_size(1, 2, 100, 32, 8, 4, 1, 1)
+    assert bwd(dtype=1, workspace_bytes=need) == L.LAPATTN_ERR_UNSUPPORTED
+
+
+def test_workspace_size_monotone_and_invalid():
+    for bwd_flag in (0, 1):
+        sizes = [L.lapattn_workspace_size(2, 2, n, 64, 64, 8, 0, bwd_flag) for n in (64, 197, 512, 3136, 16384)]
+        assert all(b >= a > 0 for a, b in zip(sizes, sizes[1:])) and sizes[-1] > sizes[0]
+        prev = 0
+        for BH in (1, 2, 16, 384):
+            s = L.lapattn_workspace_size(BH, 1, 3136, 32, 64, 6, 0, bwd_flag)
+            assert s > prev
+            prev = s
+    assert L.lapattn_workspace_size(1, 1, 10, 32, 11, 4, 0, 0) == 0      # m > n
+    assert L.lapattn_workspace_size(1, 1, 10, 40, 4, 4, 0, 0) == 0       # d unsupported
+    # the forward workspace is O(n) in the sequence length: no n x m or n x n buffer
+    a = L.lapattn_workspace_size(8, 2, 16384, 64, 64, 8, 1, 0)
+    b = L.lapattn_workspace_size(8, 2, 4 * 16384, 64, 64, 8, 1, 0)
+    assert b < 4.2 * a
+    assert a < 16 * 16384 * 64 * 4    # well under one fp32 n x m matrix per head

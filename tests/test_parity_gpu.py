@@ -1,0 +1,209 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle.
+
+Metric: for every head (b, h), ||O_gpu - O_ref||_F / ||O_ref||_F, maximum over heads.
+Bar: 1e-4 for fp32 inputs, 2e-2 for bf16 inputs (applied to Out and to each of
+dQ, dK, dV).  Reduced sizes compare every output and span several tiles plus a
+ragged tail; the full workload sizes run exactly the launch configuration the
+benchmark times and compare a sample of heads, which the oracle computes
+independently (every head is an independent problem).
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+TOL = {"fp32": 1e-4, "bf16": 2e-2}
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2604_20368_amd import lapattn
+    lapattn.library()
+    return lapattn
+
+
+def to_dev(x, dtype):
+    t = torch.from_numpy(np.ascontiguousarray(x)).to("cuda")
+    return t.to(torch.bfloat16) if dtype == "bf16" else t
+
+
+def to_np(t):
+    return t.float().cpu().numpy().astype(np.float64)
+
+
+def head_rel(gpu, ref):
+    BH = gpu.shape[0] * gpu.shape[1]
+    g = gpu.reshape(BH, -1)
+    r = ref.reshape(BH, -1)
+    return float((np.linalg.norm(g - r, axis=1) / np.maximum(np.linalg.norm(r, axis=1), 1e-300)).max())
+
+
+def say(msg):
+    print(msg, flush=True)
+
+
+def run_forward(L, x, w, norm=0, eps=0.0):
+    Q, K, V = (to_dev(x[k], w.dtype) for k in ("Q", "K", "V"))
+    out = L.forward(Q, K, V, w.m, w.lam, w.T, norm=norm, eps=eps)
+    torch.cuda.synchronize()
+    return to_np(out)
+
+
+def check_forward(L, w, norm=0, eps=0.0, tol=None):
+    say("forward %s B=%d H=%d n=%d d=%d m=%d T=%d %s norm=%d eps=%g" %
+        (w.name, w.B, w.H, w.n, w.d, w.m, w.T, w.dtype, norm, eps))
+    x = W.make_inputs(w, with_grad=False)
+    got = run_forward(L, x, w, norm, eps)
+    ref = oracle.forward(x["Q"], x["K"], x["V"], w.m, w.lam, w.T, norm, eps)
+    err = head_rel(got, ref)
+    say("  max head rel err %.3e" % err)
+    assert np.isfinite(got).all()
+    assert err <= (tol if tol is not None else TOL[w.dtype])
+    return err
+
+
+# ------------------------------------------------------------------------------ reduced sizes, every output
+
+@pytest.mark.parametrize("name", list(W.WORKLOADS))
+def test_forward_reduced(L, name):
+    w = W.WORKLOADS[name]
+    for n in (w.n, 1000):
+        check_forward(L, W.small(w, n=n, B=1, H=3))
+
+
+@pytest.mark.parametrize("norm", [0, 1, 2])
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("d", [32, 64])
+def test_forward_norms_dtypes(L, norm, dtype, d):
+    w = W.Workload("mix", 2, 2, 777, d, 37, 5, dtype, 1 / math.sqrt(d), math.sqrt(d), 7, False)
+    check_forward(L, w, norm=norm)
+
+
+def test_forward_tiny_workload(L):
+    check_forward(L, W.WORKLOADS["tiny"])
+
+
+@pytest.mark.parametrize("nm", [16, 32, 64])
+def test_forward_landmarks_equal_tokens(L, nm):
+    """m = n: with enough updates the method is exact dense attention; the GPU
+    must agree with the oracle at the same T (both converged)."""
+    w = W.Workload("dense", 1, 2, nm, 32, nm, 50, "fp32", 1.0, math.sqrt(32), 11, False)
+    check_forward(L, w)
+    check_forward(L, w.with_(T=6))
+
+
+@pytest.mark.parametrize("n,m", [(1, 1), (5, 1), (63, 7), (64, 64), (65, 64), (513, 1), (300, 33)])
+def test_forward_edge_shapes(L, n, m):
+    w = W.Workload("edge", 1, 2, n, 64, m, 4, "fp32", 0.125, 8.0, 12, False)
+    check_forward(L, w)
+
+
+def test_forward_lambda4_and_eps(L):
+    w = W.WORKLOADS["pvt_stage1"].with_(B=2, lam=4.0)
+    check_forward(L, w)
+    check_forward(L, W.WORKLOADS["deit_small"].with_(B=2), eps=0.05)
+
+
+def test_forward_deterministic(L):
+    w = W.small(W.WORKLOADS["highres"], n=4096, B=1, H=2)
+    x = W.make_inputs(w, with_grad=False)
+    a = run_forward(L, x, w)
+    b = run_forward(L, x, w)
+    assert np.array_equal(a, b)
+
+
+def test_forward_nan_propagates(L):
+    w = W.Workload("nan", 1, 2, 300, 32, 10, 3, "fp32", 0.2, 4.0, 13, False)
+    x = W.make_inputs(w, with_grad=False)
+    x["Q"][0, 1, 17, 3] = np.nan
+    got = run_forward(L, x, w)
+    assert np.isnan(got[0, 1]).any()
+    ref = oracle.forward(x["Q"][:, :1], x["K"][:, :1], x["V"][:, :1], w.m, w.lam, w.T)
+    assert head_rel(got[:, :1], ref) <= 1e-4
+
+
+# ------------------------------------------------------------------------------ full workload sizes, sampled heads
+
+@pytest.mark.parametrize("name", list(W.WORKLOADS))
+def test_forward_full_size_sampled_heads(L, name):
+    w = W.WORKLOADS[name]
+    say("forward full %s" % name)
+    x = W.make_inputs(w, with_grad=False)
+    got = run_forward(L, x, w)
+    BH = w.BH
+    heads = sorted(set([0, BH - 1, BH // 2, (7 * BH) // 11]))
+    sub = {k: np.ascontiguousarray(v.reshape(BH, w.n, w.d)[heads][None]) for k, v in x.items()}
+    ref = oracle.forward(sub["Q"], sub["K"], sub["V"], w.m, w.lam, w.T)
+    err = head_rel(got.reshape(BH, w.n, w.d)[heads][None], ref)
+    say("  heads %s max rel err %.3e" % (heads, err))
+    assert np.isfinite(got).all()
+    assert err <= TOL[w.dtype]
+
+
+# ------------------------------------------------------------------------------ backward
+
+def check_backward(L, w, norm=0, eps=0.0, heads=None):
+    say("backward %s B=%d H=%d n=%d d=%d m=%d T=%d norm=%d eps=%g" % (w.name, w.B, w.H, w.n, w.d, w.m, w.T, norm, eps))
+    x = W.make_inputs(w, with_grad=True)
+    Q, K, V, dO = (to_dev(x[k], "fp32") for k in ("Q", "K", "V", "dO"))
+    dQ, dK, dV = L.backward(Q, K, V, dO, w.m, w.lam, w.T, norm=norm, eps=eps)
+    torch.cuda.synchronize()
+    got = [to_np(t) for t in (dQ, dK, dV)]
+    BH = w.BH
+    if heads is None:
+        sub, gsub = x, got
+    else:
+        sub = {k: np.ascontiguousarray(v.reshape(BH, w.n, w.d)[heads][None]) for k, v in x.items()}
+        gsub = [g.reshape(BH, w.n, w.d)[heads][None] for g in got]
+    ref = oracle.backward(sub["Q"], sub["K"], sub["V"], sub["dO"], w.m, w.lam, w.T, norm, eps)
+    errs = [head_rel(g, r) for g, r in zip(gsub, ref)]
+    say("  dQ %.3e dK %.3e dV %.3e" % tuple(errs))
+    for g in got:
+        assert np.isfinite(g).all()
+    assert max(errs) <= TOL["fp32"]
+
+
+@pytest.mark.parametrize("norm", [0, 1, 2])
+def test_backward_reduced(L, norm):
+    w = W.small(W.WORKLOADS["train"], n=700, B=1, H=2)
+    check_backward(L, w, norm=norm)
+
+
+@pytest.mark.parametrize("d,m,n", [(64, 64, 500), (32, 20, 197), (64, 9, 64), (32, 1, 33)])
+def test_backward_shapes(L, d, m, n):
+    w = W.Workload("bshape", 1, 2, n, d, m, 4, "fp32", 1 / math.sqrt(d), math.sqrt(d), 14, True)
+    check_backward(L, w)
+
+
+def test_backward_eps(L):
+    w = W.Workload("beps", 1, 2, 300, 32, 16, 5, "fp32", 0.2, 4.0, 15, True)
+    check_backward(L, w, eps=0.1)
+
+
+def test_backward_full_size_sampled_heads(L):
+    w = W.WORKLOADS["train"]
+    check_backward(L, w, heads=[0, 37, 91, w.BH - 1])
+
+
+def test_backward_deterministic(L):
+    w = W.small(W.WORKLOADS["train"], n=1000, B=1, H=2)
+    x = W.make_inputs(w, with_grad=True)
+    Q, K, V, dO = (to_dev(x[k], "fp32") for k in ("Q", "K", "V", "dO"))
+    a = [to_np(t) for t in L.backward(Q, K, V, dO, w.m, w.lam, w.T)]
+    b = [to_np(t) for t in L.backward(Q, K, V, dO, w.m, w.lam, w.T)]
+    assert all(np.array_equal(p, q) for p, q in zip(a, b))
+
+
+def test_backward_rejects_bf16(L):
+    x = torch.zeros((1, 1, 64, 32), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(L.LapattnError) as e:
+        L.backward(x, x, x, x, 4, 1.0, 2)
+    assert e.value.code == L.LAPATTN_ERR_UNSUPPORTED

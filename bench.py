@@ -33,8 +33,8 @@ def alu_ops(kernel, w):
     subtractions, d absolute-value accumulations and one exponential (2d + 1
     operations); the contractions are not counted (they run on the matrix cores
     or are a small fraction)."""
-    pairs = {"key_summary": w.BH * w.n * w.m, "query_out": w.BH * w.n * w.m,
-             "ns_solve": w.BH * w.m * w.m}.get(kernel)
+    pairs = {"key_summary": w.BH * w.n * w.m, "query_out": w.BH * w.n * w.m, "query": w.BH * w.n * w.m,
+             "ns_key": w.BH * w.n * w.m, "ns_solve": w.BH * w.m * w.m}.get(kernel)
     return None if pairs is None else pairs * (2 * w.d + 1)
 
 
@@ -58,23 +58,25 @@ def traffic_record(kernel):
     return rec.get("bytes_per_launch")
 
 
-def cpu_baseline(w, x, budget_s=12.0):
+def cpu_baseline(w, x, budget_s=10.0):
     """The fp64 oracle on a bounded sample: whole heads of the same workload,
-    until about budget_s seconds of work; scaled to tokens/s of the full
-    workload (one token = all H heads of one position)."""
+    one after another (wrapping around), until about budget_s seconds of work;
+    scaled to tokens/s of the full workload (one token = all H heads of one
+    position)."""
     import oracle
     heads, t_used = 0, 0.0
     BH = w.BH
-    while heads < BH and t_used < budget_s:
-        sub = {k: np.ascontiguousarray(v.reshape(BH, w.n, w.d)[heads:heads + 1][None]) for k, v in x.items()}
+    while t_used < budget_s and heads < 64 * BH:
+        hh = heads % BH
+        sub = {k: np.ascontiguousarray(v.reshape(BH, w.n, w.d)[hh:hh + 1][None]) for k, v in x.items()}
         t0 = time.perf_counter()
         oracle.forward(sub["Q"], sub["K"], sub["V"], w.m, w.lam, w.T)
         t_used += time.perf_counter() - t0
         heads += 1
     tokens = w.B * w.n * heads / BH
     return {"value": tokens / t_used, "unit": "tokens/s", "cores": oracle.threads(), "kind": "oracle",
-            "sample": "%d of %d heads of the %s workload (n=%d, d=%d, m=%d, T=%d), fp64, %.1f s"
-                      % (heads, BH, w.name, w.n, w.d, w.m, w.T, t_used)}
+            "sample": "%d head-passes over the %d heads of the %s workload (n=%d, d=%d, m=%d, T=%d), fp64 "
+                      "forward, %.1f s" % (heads, BH, w.name, w.n, w.d, w.m, w.T, t_used)}
 
 
 def main():
@@ -106,13 +108,18 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    lapattn.lapattn_timing_enable(1)
-    torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
         step()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    # the same steps again with HIP events around every kernel (on the stream the
+    # library launches on) for the per-kernel durations behind the roofline
+    lapattn.lapattn_timing_enable(1)
+    torch.cuda.synchronize()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
     lapattn.lapattn_timing_enable(0)
     launches = lapattn.lapattn_timing_read(cap=64 * args.steps + 64)
 

@@ -7,7 +7,7 @@
 #include <new>
 #include <vector>
 
-#include "../../include/lapattn.h"
+#include "lapattn.h"
 #include "kernels.hpp"
 
 namespace {
@@ -34,6 +34,12 @@ int check_shape(int B, int H, int n, int d, int m, float lambda, int T, int dtyp
 }
 
 // ------------------------------------------------------------------------------- workspace plan
+
+struct FastPlan {
+    size_t qt, kt, vseg, segmax, vsegmax, frame, qfix, kfix, vbar, XT, cinfo, Upart, Mt, mscale, U, M;
+    size_t total;
+    int kpb, nkb;
+};
 
 struct Plan {
     size_t qt, kt, vseg, Upart, Xs, cinfo, U, M, vbar;                   // forward
@@ -86,6 +92,37 @@ Plan make_plan(int BH, int n, int d, int m, int T, bool bwd) {
         p.dDk = c.take(bh * n * m * f);
         p.dqt_part = c.take(bh * p.nlc * m * d * f);
     }
+    p.total = (c.off + 255) & ~size_t(255);
+    return p;
+}
+
+// The bf16 forward: key blocks of kpb keys (a multiple of 256), sized so the key-side launch
+// has about two 64-key tiles per wave when the work allows it.
+FastPlan make_fast_plan(int BH, int n, int d, int m) {
+    FastPlan p{};
+    const long long tiles = (long long)BH * ((n + 63) / 64);
+    const long long per_wave = tiles / 2048 > 1 ? tiles / 2048 : 1;
+    p.kpb = (int)(256 * per_wave);
+    p.nkb = (n + p.kpb - 1) / p.kpb;
+    const size_t bh = (size_t)BH, d1 = (size_t)d + 1, f = sizeof(float), g = sizeof(double);
+    const size_t cbp = (size_t)d / 32 + 1;
+    Carver c;
+    p.qt = c.take(bh * m * d * f);
+    p.kt = c.take(bh * m * d * f);
+    p.vseg = c.take(bh * m * d * g);
+    p.segmax = c.take(bh * m * f);
+    p.vsegmax = c.take(bh * m * f);
+    p.frame = c.take(bh * 4 * f);
+    p.qfix = c.take(bh * 64 * (d / 2) * 4);
+    p.kfix = c.take(bh * 64 * (d / 2) * 4);
+    p.vbar = c.take(bh * d * f);
+    p.XT = c.take(bh * 64 * 64 * f);
+    p.cinfo = c.take(bh * 4 * f);
+    p.Upart = c.take(bh * p.nkb * m * d1 * f);
+    p.Mt = c.take(bh * 4 * cbp * 2 * 512 * 2);
+    p.mscale = c.take(bh * 2 * f);
+    p.U = c.take(bh * m * d1 * f);
+    p.M = c.take(bh * m * d1 * f);
     p.total = (c.off + 255) & ~size_t(255);
     return p;
 }
@@ -177,12 +214,50 @@ hipError_t forward_internals(Recorder& rec, const Plan& p, const void* Q, const 
     return e;
 }
 
+hipError_t forward_fast(Recorder& rec, const FastPlan& p, const void* Q, const void* K, const void* V, void* Out,
+                        void* ws, int BH, int n, int d, int m, float lambda, int T, int norm, float eps,
+                        hipStream_t st) {
+    hipError_t e;
+    e = run_named(rec, "pool", [&] {
+        return lapattn::launch_fast_pool(Q, K, V, at<float>(ws, p.qt), at<float>(ws, p.kt), at<double>(ws, p.vseg),
+                                         at<float>(ws, p.segmax), at<float>(ws, p.vsegmax), BH, n, d, m, st);
+    });
+    if (e != hipSuccess) return e;
+    e = run_named(rec, "frame", [&] {
+        return lapattn::launch_fast_frame(at<float>(ws, p.qt), at<float>(ws, p.kt), at<double>(ws, p.vseg),
+                                          at<float>(ws, p.segmax), at<float>(ws, p.vsegmax), at<float>(ws, p.frame),
+                                          at<uint32_t>(ws, p.qfix), at<uint32_t>(ws, p.kfix), at<float>(ws, p.vbar),
+                                          BH, n, d, m, lambda, st);
+    });
+    if (e != hipSuccess) return e;
+    e = run_named(rec, "ns_key", [&] {
+        return lapattn::launch_fast_nskey(at<float>(ws, p.qt), at<float>(ws, p.kt), at<float>(ws, p.XT),
+                                          at<float>(ws, p.cinfo), K, V, at<uint32_t>(ws, p.qfix),
+                                          at<float>(ws, p.frame), at<float>(ws, p.Upart), BH, n, d, m, T, lambda, eps,
+                                          p.kpb, p.nkb, st);
+    });
+    if (e != hipSuccess) return e;
+    e = run_named(rec, "m_final", [&] {
+        return lapattn::launch_fast_mfinal(at<float>(ws, p.Upart), at<float>(ws, p.XT), at<_Float16>(ws, p.Mt),
+                                           at<float>(ws, p.mscale), at<float>(ws, p.U), at<float>(ws, p.M), BH, d, m,
+                                           p.nkb, st);
+    });
+    if (e != hipSuccess) return e;
+    e = run_named(rec, "query", [&] {
+        return lapattn::launch_fast_query(norm, Q, Out, at<uint32_t>(ws, p.kfix), at<float>(ws, p.frame),
+                                          at<_Float16>(ws, p.Mt), at<float>(ws, p.mscale), at<float>(ws, p.vbar), BH,
+                                          n, d, m, st);
+    });
+    return e;
+}
+
 }  // namespace
 
 extern "C" {
 
 size_t lapattn_workspace_size(int B, int H, int n, int d, int m, int ns_iters, int dtype, int for_backward) {
     if (check_shape(B, H, n, d, m, 1.f, ns_iters, dtype, LAPATTN_NORM_INLINE, 0.f) != LAPATTN_OK) return 0;
+    if (dtype == LAPATTN_BF16 && !for_backward) return make_fast_plan(B * H, n, d, m).total;
     return make_plan(B * H, n, d, m, ns_iters, for_backward != 0).total;
 }
 
@@ -196,9 +271,16 @@ int lapattn_forward(const void* Q, const void* K, const void* V, void* Out, int 
         int rc = check_shape(B, H, n, d, m, lambda, ns_iters, dtype, norm, eps);
         if (rc) return rc;
         const int BH = B * H;
+        hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+        if (dtype == LAPATTN_BF16) {
+            const FastPlan fp = make_fast_plan(BH, n, d, m);
+            if (!workspace || workspace_bytes < fp.total) return LAPATTN_ERR_WORKSPACE;
+            Recorder rec(st);
+            hipError_t e = forward_fast(rec, fp, Q, K, V, Out, workspace, BH, n, d, m, lambda, ns_iters, norm, eps, st);
+            return e == hipSuccess ? LAPATTN_OK : LAPATTN_ERR_HIP;
+        }
         const Plan p = make_plan(BH, n, d, m, ns_iters, false);
         if (!workspace || workspace_bytes < p.total) return LAPATTN_ERR_WORKSPACE;
-        hipStream_t st = reinterpret_cast<hipStream_t>(stream);
         Recorder rec(st);
         hipError_t e = forward_internals(rec, p, Q, K, V, workspace, BH, n, d, m, lambda, ns_iters, dtype, eps,
                                          false, st);

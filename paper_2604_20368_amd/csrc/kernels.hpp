@@ -6,6 +6,7 @@
 
 #include <hip/hip_runtime.h>
 #include <stddef.h>
+#include <stdint.h>
 
 namespace lapattn {
 
@@ -71,5 +72,21 @@ hipError_t launch_bwd_key_lm(const float* K, const float* qt, const float* dDk, 
 hipError_t launch_bwd_pool(float* dQ, float* dK, const float* dqtW, const float* dktW,
                            const float* dqt_part, const float* dkt_part,
                            int BH, int n, int d, int m, int nlc, hipStream_t st);
+
+// bf16 fast forward path (fast.hip) -------------------------------------------------------
+
+hipError_t launch_fast_pool(const void* Q, const void* K, const void* V, float* qt, float* kt, double* vseg,
+                            float* segmax, float* vsegmax, int BH, int n, int d, int m, hipStream_t st);
+hipError_t launch_fast_frame(const float* qt, const float* kt, const double* vseg, const float* segmax,
+                             const float* vsegmax, float* frame, uint32_t* qfix, uint32_t* kfix, float* vbar, int BH,
+                             int n, int d, int m, float lambda, hipStream_t st);
+hipError_t launch_fast_nskey(const float* qt, const float* kt, float* XT, float* cinfo, const void* K, const void* V,
+                             const uint32_t* qfix, const float* frame, float* Upart, int BH, int n, int d, int m,
+                             int T, float lambda, float eps, int kpb, int nkb, hipStream_t st);
+hipError_t launch_fast_mfinal(const float* Upart, const float* XT, _Float16* Mt, float* mscale, float* U, float* M,
+                              int BH, int d, int m, int nkb, hipStream_t st);
+hipError_t launch_fast_query(int norm, const void* Q, void* Out, const uint32_t* kfix, const float* frame,
+                             const _Float16* Mt, const float* mscale, const float* vbar, int BH, int n, int d, int m,
+                             hipStream_t st);
 
 }  // namespace lapattn

@@ -41,7 +41,7 @@ def alu_ops(kernel, w):
 def traffic_record(kernel):
     """HBM traffic measured with rocprofv3 counters for this kernel, if the
     committed record matches the current kernel sources (else None)."""
-    path = os.path.join(ROOT, "profiles", "traffic_%s_%s.json" % (kernel, WORKLOAD))
+    path = os.path.join(ROOT, "profiles", "traffic_%s_%s.txt" % (kernel, WORKLOAD))
     if not os.path.exists(path):
         return None
     try:
@@ -79,13 +79,89 @@ def cpu_baseline(w, x, budget_s=10.0):
                       "forward, %.1f s" % (heads, BH, w.name, w.n, w.d, w.m, w.T, t_used)}
 
 
+KERNEL_SOURCES = ["paper_2604_20368_amd/csrc/fast.hip", "paper_2604_20368_amd/csrc/common.hpp",
+                  "paper_2604_20368_amd/csrc/host.cpp"]
+COPY_BYTES = 512 * 1024 * 1024
+
+
+def calibrate_copy():
+    """A plain device copy of COPY_BYTES (read COPY_BYTES, write COPY_BYTES), run a few
+    times under rocprofv3 --pmc to scale FETCH_SIZE / WRITE_SIZE to bytes."""
+    import torch
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)              # the runtime's copy kernel
+        torch.neg(src, out=dst)     # an elementwise kernel of the same size
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": COPY_BYTES, "launches": 3}), flush=True)
+
+
+def _pmc_per_dispatch(csv_dir, counter, kernel_substr):
+    import csv
+    import glob
+    vals = []
+    for f in glob.glob(os.path.join(csv_dir, "**", "*counter_collection.csv"), recursive=True):
+        for r in csv.DictReader(open(f)):
+            if r["Counter_Name"] == counter and kernel_substr in r["Kernel_Name"]:
+                vals.append(float(r["Counter_Value"]))
+    return sum(vals) / len(vals) if vals else None
+
+
+def ingest_traffic(kernel, fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, out_path):
+    """Turn two rocprofv3 --pmc runs of the benchmark (FETCH_SIZE, WRITE_SIZE; KiB per
+    dispatch) and the same two counters on the plain copy into HBM bytes per launch of
+    `kernel`, stamped with a hash of the kernel sources (bench.py reports null once the
+    sources change)."""
+    import hashlib
+    symbol = {"ns_key": "nskey_kernel", "query": "query2_kernel", "pool": "pool2_kernel"}[kernel]
+    f_k = _pmc_per_dispatch(fetch_dir, "FETCH_SIZE", symbol)
+    w_k = _pmc_per_dispatch(write_dir, "WRITE_SIZE", symbol)
+    f_c = _pmc_per_dispatch(copy_fetch_dir, "FETCH_SIZE", "__amd_rocclr_copyBuffer")
+    w_c = _pmc_per_dispatch(copy_write_dir, "WRITE_SIZE", "__amd_rocclr_copyBuffer")
+    ff, fw = COPY_BYTES / (f_c * 1024.0), COPY_BYTES / (w_c * 1024.0)
+    h = hashlib.sha256()
+    for src in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, src), "rb") as f:
+            h.update(f.read())
+    rec = {"kernel": kernel, "workload": WORKLOAD, "fetch_kib": f_k, "write_kib": w_k,
+           "copy_fetch_kib": f_c, "copy_write_kib": w_c, "fetch_scale": ff, "write_scale": fw,
+           "bytes_per_launch": f_k * 1024.0 * ff + w_k * 1024.0 * fw,
+           "sources": KERNEL_SOURCES, "sources_sha256": h.hexdigest(),
+           "commands": ["rocprofv3 --pmc FETCH_SIZE --output-format csv -d FETCH_DIR -o run -- "
+                        "python3 bench.py --steps 3 --warmup 1 --no-cpu-baseline",
+                        "rocprofv3 --pmc WRITE_SIZE --output-format csv -d WRITE_DIR -o run -- "
+                        "python3 bench.py --steps 3 --warmup 1 --no-cpu-baseline",
+                        "rocprofv3 --pmc FETCH_SIZE --output-format csv -d COPY_FETCH_DIR -o run -- "
+                        "python3 bench.py --calibrate-copy",
+                        "rocprofv3 --pmc WRITE_SIZE --output-format csv -d COPY_WRITE_DIR -o run -- "
+                        "python3 bench.py --calibrate-copy",
+                        "python3 bench.py --ingest-traffic %s FETCH_DIR WRITE_DIR COPY_FETCH_DIR COPY_WRITE_DIR" % kernel]}
+    with open(out_path, "w") as f:
+        json.dump(rec, f, indent=1)
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="run only the plain copy used to scale the HBM byte counters")
+    ap.add_argument("--ingest-traffic", nargs=5, metavar=("KERNEL", "FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR",
+                                                          "COPY_WRITE_DIR"),
+                    help="write profiles/traffic_<KERNEL>_<workload>.txt from rocprofv3 --pmc CSV directories")
     args = ap.parse_args()
+    if args.ingest_traffic:
+        k = args.ingest_traffic[0]
+        ingest_traffic(k, *args.ingest_traffic[1:], out_path=os.path.join(
+            ROOT, "profiles", "traffic_%s_%s.txt" % (k, WORKLOAD)))
+        return
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
     if args.gpus != 1:
         print("bench.py measures one GPU: this build runs on a single MI355X and has no multi-GPU path "
               "(every head is independent; see DESIGN.md for how the work would shard).", file=sys.stderr)

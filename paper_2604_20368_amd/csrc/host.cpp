@@ -231,10 +231,9 @@ hipError_t forward_fast(Recorder& rec, const FastPlan& p, const void* Q, const v
     });
     if (e != hipSuccess) return e;
     e = run_named(rec, "ns_key", [&] {
-        return lapattn::launch_fast_nskey(at<float>(ws, p.qt), at<float>(ws, p.kt), at<float>(ws, p.XT),
-                                          at<float>(ws, p.cinfo), K, V, at<uint32_t>(ws, p.qfix),
-                                          at<float>(ws, p.frame), at<float>(ws, p.Upart), BH, n, d, m, T, lambda, eps,
-                                          p.kpb, p.nkb, st);
+        return lapattn::launch_fast_nskey(at<float>(ws, p.XT), at<float>(ws, p.cinfo), K, V, at<uint32_t>(ws, p.qfix),
+                                          at<uint32_t>(ws, p.kfix), at<float>(ws, p.frame), at<float>(ws, p.Upart),
+                                          BH, n, d, m, T, eps, p.kpb, p.nkb, st);
     });
     if (e != hipSuccess) return e;
     e = run_named(rec, "m_final", [&] {

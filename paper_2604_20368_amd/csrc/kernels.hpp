@@ -80,9 +80,9 @@ hipError_t launch_fast_pool(const void* Q, const void* K, const void* V, float* 
 hipError_t launch_fast_frame(const float* qt, const float* kt, const double* vseg, const float* segmax,
                              const float* vsegmax, float* frame, uint32_t* qfix, uint32_t* kfix, float* vbar, int BH,
                              int n, int d, int m, float lambda, hipStream_t st);
-hipError_t launch_fast_nskey(const float* qt, const float* kt, float* XT, float* cinfo, const void* K, const void* V,
-                             const uint32_t* qfix, const float* frame, float* Upart, int BH, int n, int d, int m,
-                             int T, float lambda, float eps, int kpb, int nkb, hipStream_t st);
+hipError_t launch_fast_nskey(float* XT, float* cinfo, const void* K, const void* V, const uint32_t* qfix,
+                             const uint32_t* kfix, const float* frame, float* Upart, int BH, int n, int d, int m,
+                             int T, float eps, int kpb, int nkb, hipStream_t st);
 hipError_t launch_fast_mfinal(const float* Upart, const float* XT, _Float16* Mt, float* mscale, float* U, float* M,
                               int BH, int d, int m, int nkb, hipStream_t st);
 hipError_t launch_fast_query(int norm, const void* Q, void* Out, const uint32_t* kfix, const float* frame,

@@ -29,7 +29,9 @@
  * memory of at least lapattn_workspace_size() bytes).  The library never
  * allocates or frees device memory and keeps no state between calls apart from
  * the optional timing switch below.  Outputs are overwritten, never accumulated.
- * Outputs must not alias inputs, each other, or the workspace.
+ * Outputs must not alias inputs, each other, or the workspace.  Every tensor
+ * pointer must be 16-byte aligned and the workspace 256-byte aligned (device
+ * allocations are; offset views may not be).
  *
  * Asynchrony: every call validates its arguments on the host, enqueues its
  * kernels on `stream` (a hipStream_t; NULL = the default stream) and returns
@@ -69,7 +71,9 @@ enum {
                                      eps not finite or < 0, unknown norm or dtype */
     LAPATTN_ERR_UNSUPPORTED = 4,  /* d not in {32, 64}, m > 64, or bf16 backward */
     LAPATTN_ERR_WORKSPACE = 5,    /* workspace NULL or smaller than lapattn_workspace_size() */
-    LAPATTN_ERR_HIP = 6           /* a HIP launch failed */
+    LAPATTN_ERR_HIP = 6,          /* a HIP launch failed */
+    LAPATTN_ERR_ALIGN = 7         /* a tensor pointer is not 16-byte aligned, or the
+                                     workspace is not 256-byte aligned */
 };
 
 /* Options; a NULL pointer means {LAPATTN_NORM_INLINE, 0.0f}.

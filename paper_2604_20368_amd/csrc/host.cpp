@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <initializer_list>
 #include <mutex>
 #include <new>
 #include <vector>
@@ -30,6 +31,16 @@ int check_shape(int B, int H, int n, int d, int m, float lambda, int T, int dtyp
     if (!(std::isfinite(eps) && eps >= 0.f)) return LAPATTN_ERR_PARAM;
     if (d != 32 && d != 64) return LAPATTN_ERR_UNSUPPORTED;
     if (m > kMaxM) return LAPATTN_ERR_UNSUPPORTED;
+    return LAPATTN_OK;
+}
+
+// Tensors are read and written in 16-byte vectors; workspace slices are carved at 256-byte offsets.
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+int check_align(std::initializer_list<const void*> tensors, const void* workspace) {
+    for (const void* t : tensors)
+        if (!aligned(t, 16)) return LAPATTN_ERR_ALIGN;
+    if (workspace && !aligned(workspace, 256)) return LAPATTN_ERR_ALIGN;
     return LAPATTN_OK;
 }
 
@@ -269,6 +280,8 @@ int lapattn_forward(const void* Q, const void* K, const void* V, void* Out, int 
         const float eps = eps_of(opts);
         int rc = check_shape(B, H, n, d, m, lambda, ns_iters, dtype, norm, eps);
         if (rc) return rc;
+        rc = check_align({Q, K, V, Out}, workspace);
+        if (rc) return rc;
         const int BH = B * H;
         hipStream_t st = reinterpret_cast<hipStream_t>(stream);
         if (dtype == LAPATTN_BF16) {
@@ -305,6 +318,8 @@ int lapattn_backward(const void* Q, const void* K, const void* V, const void* dO
         int rc = check_shape(B, H, n, d, m, lambda, ns_iters, dtype, norm, eps);
         if (rc) return rc;
         if (dtype != LAPATTN_FP32) return LAPATTN_ERR_UNSUPPORTED;
+        rc = check_align({Q, K, V, dOut, dQ, dK, dV}, workspace);
+        if (rc) return rc;
         const int BH = B * H;
         const Plan p = make_plan(BH, n, d, m, ns_iters, true);
         if (!workspace || workspace_bytes < p.total) return LAPATTN_ERR_WORKSPACE;
@@ -371,6 +386,7 @@ const char* lapattn_status_str(int status) {
         case LAPATTN_ERR_UNSUPPORTED: return "unsupported configuration (d in {32, 64}, m <= 64, fp32 backward)";
         case LAPATTN_ERR_WORKSPACE: return "workspace missing or too small";
         case LAPATTN_ERR_HIP: return "HIP launch failed";
+        case LAPATTN_ERR_ALIGN: return "a tensor is not 16-byte aligned or the workspace not 256-byte aligned";
         default: return "unknown status";
     }
 }

@@ -12,7 +12,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblapattn.
 LAPATTN_FP32, LAPATTN_BF16 = 0, 1
 LAPATTN_NORM_INLINE, LAPATTN_NORM_ROWSUM, LAPATTN_NORM_NONE = 0, 1, 2
 LAPATTN_OK, LAPATTN_ERR_NULL, LAPATTN_ERR_SHAPE, LAPATTN_ERR_PARAM = 0, 1, 2, 3
-LAPATTN_ERR_UNSUPPORTED, LAPATTN_ERR_WORKSPACE, LAPATTN_ERR_HIP = 4, 5, 6
+LAPATTN_ERR_UNSUPPORTED, LAPATTN_ERR_WORKSPACE, LAPATTN_ERR_HIP, LAPATTN_ERR_ALIGN = 4, 5, 6, 7
 
 EXPORTS = ("lapattn_workspace_size", "lapattn_forward", "lapattn_backward", "lapattn_status_str",
            "lapattn_timing_enable", "lapattn_timing_read", "lapattn_timing_name")

@@ -28,7 +28,7 @@ def test_library_exports_every_declared_function():
 
 
 def test_status_strings():
-    for code in range(7):
+    for code in range(8):
         assert L.lapattn_status_str(code) and L.lapattn_status_str(code) != "unknown status"
     assert L.lapattn_status_str(99) == "unknown status"
 
@@ -58,6 +58,9 @@ def test_argument_validation(call):
     assert call(m=0) == L.LAPATTN_ERR_SHAPE
     assert call(m=101) == L.LAPATTN_ERR_SHAPE                     # m > n
     assert call(B=1 << 12, H=1 << 10, n=1 << 10, d=32) == L.LAPATTN_ERR_SHAPE   # B*H*n*d >= 2^31
+    for p in ptrs:
+        assert call(**{p: FAKE + 8}) == L.LAPATTN_ERR_ALIGN       # 16-byte vectors
+    assert call(workspace=FAKE + 16) == L.LAPATTN_ERR_ALIGN      # 256-byte slices
     assert call(lam=0.0) == L.LAPATTN_ERR_PARAM
     assert call(lam=-1.0) == L.LAPATTN_ERR_PARAM
     assert call(lam=float("inf")) == L.LAPATTN_ERR_PARAM

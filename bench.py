@@ -34,7 +34,7 @@ def alu_ops(kernel, w):
     operations); the contractions are not counted (they run on the matrix cores
     or are a small fraction)."""
     pairs = {"key_summary": w.BH * w.n * w.m, "query_out": w.BH * w.n * w.m, "query": w.BH * w.n * w.m,
-             "ns_key": w.BH * w.n * w.m, "ns_solve": w.BH * w.m * w.m}.get(kernel)
+             "key": w.BH * w.n * w.m, "ns_solve": w.BH * w.m * w.m}.get(kernel)
     return None if pairs is None else pairs * (2 * w.d + 1)
 
 
@@ -114,7 +114,7 @@ def ingest_traffic(kernel, fetch_dir, write_dir, copy_fetch_dir, copy_write_dir,
     `kernel`, stamped with a hash of the kernel sources (bench.py reports null once the
     sources change)."""
     import hashlib
-    symbol = {"ns_key": "nskey_kernel", "query": "query2_kernel", "pool": "pool2_kernel"}[kernel]
+    symbol = {"key": "key_kernel", "query": "query2_kernel", "pool": "pool2_kernel"}[kernel]
     f_k = _pmc_per_dispatch(fetch_dir, "FETCH_SIZE", symbol)
     w_k = _pmc_per_dispatch(write_dir, "WRITE_SIZE", symbol)
     f_c = _pmc_per_dispatch(copy_fetch_dir, "FETCH_SIZE", "__amd_rocclr_copyBuffer")

@@ -3,11 +3,11 @@
 //
 //   pool2_kernel     landmark means (Sec. 4.2, sampling; 1-D segments) and per-segment
 //                    value sums / magnitudes, 16-byte vector loads
-//   frame_kernel     per head: the fixed-point frame of the L1 distances, the landmark
-//                    tables in that frame, the value mean and the value prescale
-//   nskey_kernel     one launch, two roles: blocks [0, BH) run Algorithm 2 on K_LL with
-//                    fp16-pair MFMA; the other blocks form U = K_LK [V | 1] over key chunks
-//                    (Sec. 3.2 key summaries) with v_sad_u16 distances and fp16 MFMA
+//   frame_ns_kernel  per head: the fixed-point frame of the L1 distances, the landmark
+//                    tables in that frame, the value mean and prescale, then Algorithm 2
+//                    on K_LL with fp16-pair MFMA
+//   key_kernel       U = K_LK [V | 1] over key chunks (Sec. 3.2 key summaries) with
+//                    v_sad_u16 distances and fp16 MFMA
 //   mfinal_kernel    U = sum of the chunk partials, M = X_T U, split into fp16 hi/lo
 //                    MFMA operand tiles with a power-of-two scale per column
 //   query2_kernel    Y = K_QL M (Eq. (8)) and the normalisation (Eq. (4) / Eq. (3))
@@ -180,68 +180,6 @@ __global__ __launch_bounds__(256) void pool2_kernel(const uint16_t* __restrict__
     }
 }
 
-// ------------------------------------------------------------------------------------------
-// Per-head frame.  grid (BH), 256 threads.
-//   frame[h] = {R, 1/(2R), escale = -log2(e) / (lambda S), vscale}; R is NaN when Q, K or V hold a
-//   non-finite value (the outputs of that head are then NaN, as the plain computation gives).
-//   qfix/kfix[h][a][c/2] = u(x_{a,c}) | u(x_{a,c+1}) << 16 for landmarks a < 64 (zero rows >= m).
-//   vbar[h] = mean of the values; vscale = 2^-e keeps the fp16 copies of V below 2^14.
-template <int D>
-__global__ __launch_bounds__(256) void frame_kernel(const float* __restrict__ qt, const float* __restrict__ kt,
-                                                    const double* __restrict__ vseg,
-                                                    const float* __restrict__ segmax,
-                                                    const float* __restrict__ vsegmax, float* __restrict__ frame,
-                                                    uint32_t* __restrict__ qfix, uint32_t* __restrict__ kfix,
-                                                    float* __restrict__ vbar, int n, int m, float lambda) {
-    constexpr int D2 = D / 2;
-    constexpr int PER = 64 * D2 / 256;   // table words per thread
-    const int h = blockIdx.x, tid = threadIdx.x;
-    __shared__ float sS;   // 1 / (2R)
-    // every global read this block needs, issued before the first use
-    float q0[PER], q1[PER], k0[PER], k1[PER];
-#pragma unroll
-    for (int r = 0; r < PER; ++r) {
-        const int e = tid + 256 * r, a = e / D2, c2 = e % D2;
-        const size_t o = ((size_t)h * m + (a < m ? a : 0)) * D + 2 * c2;
-        q0[r] = qt[o]; q1[r] = qt[o + 1]; k0[r] = kt[o]; k1[r] = kt[o + 1];
-    }
-    double vs = 0.0;
-    if (tid < D) {
-#pragma unroll 16
-        for (int l = 0; l < m; ++l) vs += vseg[((size_t)h * m + l) * D + tid];
-    }
-    if (tid < 64) {
-        float a = 0.f, b = 0.f;
-        if (tid < m) {
-            a = segmax[(size_t)h * m + tid];
-            b = vsegmax[(size_t)h * m + tid];
-        }
-        const bool bad = __any(!(isfinite(a) && isfinite(b)));
-        float R = wave_max(a);
-        const float vm = wave_max(b);
-        if (tid == 0) {
-            if (R == 0.f) R = 1.f;
-            const float S = (float)(65535.0 / (2.0 * (double)R));
-            float vscale = 1.f;
-            if (vm > 16384.f) vscale = exp2f(-ceilf(log2f(vm / 16384.f)));
-            sS = (float)(0.5 / (double)R);
-            frame[h * 4 + 0] = bad ? __builtin_nanf("") : R;
-            frame[h * 4 + 1] = sS;
-            frame[h * 4 + 2] = (float)(-1.4426950408889634 / ((double)lambda * (double)S));
-            frame[h * 4 + 3] = vscale;
-        }
-    }
-    if (tid < D) vbar[(size_t)h * D + tid] = (float)(vs / n);
-    __syncthreads();
-    const float inv2R = sS;
-#pragma unroll
-    for (int r = 0; r < PER; ++r) {
-        const int e = tid + 256 * r, a = e / D2;
-        qfix[(size_t)h * 64 * D2 + e] = a < m ? fix2(q0[r], q1[r], inv2R) : 0u;
-        kfix[(size_t)h * 64 * D2 + e] = a < m ? fix2(k0[r], k1[r], inv2R) : 0u;
-    }
-}
-
 __device__ __forceinline__ int c_row(int r, int l) { return 8 * (r >> 2) + 4 * (l >> 5) + (r & 3); }
 
 __device__ __forceinline__ void split_f16(float v, _Float16& hi, _Float16& lo) {
@@ -249,115 +187,257 @@ __device__ __forceinline__ void split_f16(float v, _Float16& hi, _Float16& lo) {
     lo = (_Float16)(v - (float)hi);
 }
 
-// One wave's 32 x 32 block (rb, cb) of the 64 x 64 product A B with both factors carried as an
-// fp16 pair (value + residual, ~22 significant bits): A row-major and B transposed ([col][k]),
-// LDS row pitch kLP.  A B ~ Ahi Bhi + Ahi Blo + Alo Bhi on v_mfma_f32_32x32x16_f16; lane l
-// supplies A[row l%32][k 8(l/32)..+8] and B^T[col l%32][k 8(l/32)..+8]; result register r holds
-// row 32rb + c_row(r, l), column 32cb + l%32.
-__device__ __forceinline__ f32x16_t mm_split(const _Float16* __restrict__ Ah, const _Float16* __restrict__ Al,
-                                             const _Float16* __restrict__ BTh, const _Float16* __restrict__ BTl,
-                                             int rb, int cb) {
-    const int l = threadIdx.x & 63;
-    f32x16_t acc = {};
-    const int ao = (32 * rb + (l & 31)) * kLP + 8 * (l >> 5);
-    const int bo = (32 * cb + (l & 31)) * kLP + 8 * (l >> 5);
+// Power-of-two exponent that brings a maximum magnitude into [2^14, 2^15) (0 when mx is 0).
+__device__ __forceinline__ int pow2_exp(float mx) { return (mx > 0.f && isfinite(mx)) ? ilogbf(mx) - 14 : 0; }
+
+typedef short s4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s4_t lds_s4_t;
+
+// Scalar loads of one landmark row (D/2 words) into `t`.
+template <int D2>
+__device__ __forceinline__ void load_row(uint32_t (&t)[D2], const uint32_t* __restrict__ row) {
 #pragma unroll
-    for (int s4 = 0; s4 < 4; ++s4) {
-        const h8_t ah = *reinterpret_cast<const h8_t*>(Ah + ao + 16 * s4);
-        const h8_t al = *reinterpret_cast<const h8_t*>(Al + ao + 16 * s4);
-        const h8_t bh = *reinterpret_cast<const h8_t*>(BTh + bo + 16 * s4);
-        const h8_t bl = *reinterpret_cast<const h8_t*>(BTl + bo + 16 * s4);
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah, bh, acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah, bl, acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(al, bh, acc, 0, 0, 0);
-    }
-    return acc;
+    for (int c = 0; c < D2; ++c) t[c] = row[c];
 }
 
-// Store one wave's C block (scaled by `scale`) as an fp16 pair, row-major (Mh/Ml) and, when
-// MTh is given, transposed (MTh/MTl, four consecutive rows per 8-byte write).
-__device__ __forceinline__ void store_split(const f32x16_t& v, float scale, int rb, int cb, _Float16* Mh,
-                                            _Float16* Ml, _Float16* MTh, _Float16* MTl) {
+// The kernel value of one (lane's key, landmark row) pair: two sad chains over the even and
+// odd coordinate pairs; the first sad (the wait point for `t`) is issued before the scalar
+// loads of the next row, which go into `nt`.
+template <int D2>
+__device__ __forceinline__ float lap_row(const uint32_t (&kf)[D2], const uint32_t (&t)[D2], uint32_t (&nt)[D2],
+                                         const uint32_t* __restrict__ next_row, float esc, float ebias) {
+    uint32_t u0 = __builtin_amdgcn_sad_u16(kf[0], t[0], 0x4B000000u);
+    __builtin_amdgcn_sched_barrier(0);
+    load_row<D2>(nt, next_row);
+    __builtin_amdgcn_sched_barrier(0);
+    uint32_t u1 = __builtin_amdgcn_sad_u16(kf[1], t[1], 0u);
+#pragma unroll
+    for (int c = 2; c < D2; c += 2) {
+        u0 = __builtin_amdgcn_sad_u16(kf[c], t[c], u0);
+        u1 = __builtin_amdgcn_sad_u16(kf[c + 1], t[c + 1], u1);
+    }
+    return __builtin_amdgcn_exp2f(fmaf(__uint_as_float(u0 + u1), esc, ebias));
+}
+
+// ------------------------------------------------------------------------------------------
+// Per-head frame and Newton-Schulz solve.  grid (BH), 256 threads (4 waves).
+//
+// Frame: frame[h] = {R, 1/(2R), escale = -log2(e) / (lambda S), vscale}; R is NaN when Q, K or
+// V hold a non-finite value (the outputs of that head are then NaN, as the plain computation
+// gives).  qfix/kfix[h][a][c/2] = u(x_{a,c}) | u(x_{a,c+1}) << 16 for landmarks a < 64 (zero
+// rows >= m).  vbar[h] = mean of the values; vscale = 2^-e keeps fp16 copies of V below 2^14.
+//
+// Solve (Algorithm 2): W = K_LL + eps I padded to 64 x 64 (lane = row a, sixteen columns b per
+// wave: v_sad_u16 against the key-landmark rows, which come through scalar loads of the table
+// just written); c = ||W||_1 ||W||_inf (first maximising column / row); X0 = W^T / c (0 if
+// c = 0); X_{t+1} = X_t (2I - W X_t).  Wave w owns the 32 x 32 block (w/2, w%2) of both
+// products, on fp16-pair MFMA 32x32x16 (A B ~ Ahi Bhi + Ahi Blo + Alo Bhi, ~22 significant
+// bits, three independent accumulators); the wave's rows of W stay in registers.  Only
+// transposed copies are stored (X^T, and T1^T for T1 = 2I - W X), with 8-byte writes straight
+// from the MFMA result layout; X enters X T1 as the A factor through transposing LDS reads.
+// X^T alternates between two buffers, so each update needs two block barriers.
+// X is carried with a power-of-two scale: X0's from its exact maximum (largest entry in
+// [2^14, 2^15)), X_{t+1}'s from the maximum of X_t, placing that maximum in [2^7, 2^8).  In
+// exact arithmetic I - W X_t = (I - W X0)^(2^t) with ||I - W X0||_2 <= 1, so
+// ||X_{t+1}||_2 <= 2 ||X_t||_2 and the largest entry grows by at most 2 * 64 = 2^7 per update:
+// stored values stay below 2^15 (fp16 holds 65504).
+//   Writes X_T (fp32, row-major [64][64]) and cinfo = {c, n1, ninf, a* 256 + b*}.
+constexpr int kSolveLds = 6 * 64 * kLP * 2 + 64 * 4;
+
+// The A operand of MFMA 32x32x16 (8 halves: row 32 rb + l%32, k = k0 + 8(l/32)..+8) of a
+// matrix held transposed in LDS (Mt[k][row], pitch kLP), via two ds_read_b64_tr_b16.  Within a
+// 16-lane group that instruction gives lane i element i%4 of the 4-element reads of lanes
+// 4q + i/4 (q = 0..3): when lane j of the group points at Mt[r0 + j/4][c0 + 4(j%4)], lane i
+// receives Mt[r0 + q][c0 + i], q = 0..3 -- column c0 + i (a row of M) over 4 k values.
+__device__ __forceinline__ h8_t a_from_transposed(const _Float16* Mt, int rb, int k0) {
+    const int l = threadIdx.x & 63, g = l >> 4, i = l & 15;
+    const _Float16* p = Mt + (k0 + 8 * (g >> 1) + (i >> 2)) * kLP + 32 * rb + 16 * (g & 1) + 4 * (i & 3);
+    const s4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4_t*)p);
+    const s4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4_t*)(p + 4 * kLP));
+    typedef short s8_t __attribute__((ext_vector_type(8)));
+    return __builtin_bit_cast(h8_t, (s8_t)__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
+// One wave's 32 x 32 block of a 64 x 64 product, both factors fp16 pairs, B read from its
+// transposed copy (BT[col][k]); the A operands of the four k steps are given (hi, lo).
+// Result register r holds row 32 rb + c_row(r, l), column 32 cb + l%32.
+__device__ __forceinline__ f32x16_t mm32_split(const h8_t (&ah)[4], const h8_t (&al)[4],
+                                               const _Float16* __restrict__ BTh, const _Float16* __restrict__ BTl,
+                                               int cb) {
+    const int l = threadIdx.x & 63;
+    const int bo = (32 * cb + (l & 31)) * kLP + 8 * (l >> 5);
+    f32x16_t hh = {}, hl = {}, lh = {};
+#pragma unroll
+    for (int s4 = 0; s4 < 4; ++s4) {
+        const h8_t bh = *reinterpret_cast<const h8_t*>(BTh + bo + 16 * s4);
+        const h8_t bl = *reinterpret_cast<const h8_t*>(BTl + bo + 16 * s4);
+        hh = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah[s4], bh, hh, 0, 0, 0);
+        hl = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah[s4], bl, hl, 0, 0, 0);
+        lh = __builtin_amdgcn_mfma_f32_32x32x16_f16(al[s4], bh, lh, 0, 0, 0);
+    }
+    return hh + (hl + lh);
+}
+
+// Store a wave's 32 x 32 block (times `scale`) transposed as an fp16 pair: four consecutive
+// rows of one column per 8-byte write.
+// Two floats as packed fp16 pairs: hi = rn(x), lo = rn(x - hi) (each one v_cvt_pk_f16_f32).
+__device__ __forceinline__ void split_pk(float x0, float x1, uint32_t& hi, uint32_t& lo) {
+    const f16x2_t h = __builtin_convertvector((f32x2_t){x0, x1}, f16x2_t);
+    const f32x2_t back = __builtin_convertvector(h, f32x2_t);
+    hi = __builtin_bit_cast(uint32_t, h);
+    lo = pk_f16(x0 - back[0], x1 - back[1]);
+}
+
+__device__ __forceinline__ void store32_t(const f32x16_t& v, float scale, int rb, int cb, _Float16* MTh,
+                                          _Float16* MTl) {
     const int l = threadIdx.x & 63;
     const int col = 32 * cb + (l & 31);
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-        _Float16 hi[4], lo[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            split_f16(v[4 * g + i] * scale, hi[i], lo[i]);
-            const int row = 32 * rb + 8 * g + 4 * (l >> 5) + i;
-            if (Mh) {
-                Mh[row * kLP + col] = hi[i];
-                Ml[row * kLP + col] = lo[i];
-            }
-        }
-        if (MTh) {
-            const int row0 = 32 * rb + 8 * g + 4 * (l >> 5);
-            typedef _Float16 h4_t __attribute__((ext_vector_type(4)));
-            *reinterpret_cast<h4_t*>(MTh + col * kLP + row0) = (h4_t){hi[0], hi[1], hi[2], hi[3]};
-            *reinterpret_cast<h4_t*>(MTl + col * kLP + row0) = (h4_t){lo[0], lo[1], lo[2], lo[3]};
-        }
+        uint32_t h0, l0, h1, l1;
+        split_pk(v[4 * g] * scale, v[4 * g + 1] * scale, h0, l0);
+        split_pk(v[4 * g + 2] * scale, v[4 * g + 3] * scale, h1, l1);
+        const int o = col * kLP + 32 * rb + 8 * g + 4 * (l >> 5);
+        *reinterpret_cast<uint2*>(MTh + o) = make_uint2(h0, h1);
+        *reinterpret_cast<uint2*>(MTl + o) = make_uint2(l0, l1);
     }
 }
 
-// Power-of-two exponent that brings a maximum magnitude into [2^14, 2^15) (0 when mx is 0).
-__device__ __forceinline__ int pow2_exp(float mx) { return (mx > 0.f && isfinite(mx)) ? ilogbf(mx) - 14 : 0; }
+// One DPP step of wave_argmax_dpp: keep the larger (value bits, 63 - lane) key.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ void argmax_step(int& hi, int& lo) {
+    const int h2 = __builtin_amdgcn_update_dpp(0, hi, CTRL, ROW_MASK, 0xF, false);
+    const int l2 = __builtin_amdgcn_update_dpp(0, lo, CTRL, ROW_MASK, 0xF, false);
+    if (h2 > hi || (h2 == hi && l2 > lo)) {
+        hi = h2;
+        lo = l2;
+    }
+}
 
-// ------------------------------------------------------------------------------------------
-// Newton-Schulz role (one block per head, 4 waves; wave w owns the 32 x 32 block (w/2, w%2)).
-//   W = K_LL + eps I padded to 64 x 64, from the landmark tables in the fixed-point frame
-//   (v_sad_u16, lane = row a, the landmark-key row b wave-uniform);
-//   c = ||W||_1 ||W||_inf (first maximising column / row); X0 = W^T / c (0 if c = 0);
-//   X_{t+1} = X_t (2I - W X_t) with both products on fp16-pair MFMA, X carried with a
-//   power-of-two scale so its largest entry sits in [2^14, 2^15).
-//   Writes X_T (fp32, [64][64]) and cinfo = {c, n1, ninf, a* 256 + b*}.
-constexpr int kNsLds = 8 * 64 * kLP * 2 + 16 * 4 + 128 * 4;
+// Maximum of a non-negative v over the wave and the lowest lane holding it, by DPP on
+// (value bits, 63 - lane): a larger key is a larger value or, on a tie, a lower lane.  The
+// result is wave-uniform.
+__device__ __forceinline__ void wave_argmax_dpp(float& v, int& idx) {
+    int hi = __float_as_int(v), lo = 63 - (int)(threadIdx.x & 63);
+    argmax_step<0xB1, 0xF>(hi, lo);    // quad_perm [1,0,3,2]
+    argmax_step<0x4E, 0xF>(hi, lo);    // quad_perm [2,3,0,1]
+    argmax_step<0x141, 0xF>(hi, lo);   // row_half_mirror
+    argmax_step<0x140, 0xF>(hi, lo);   // row_mirror
+    argmax_step<0x142, 0xA>(hi, lo);   // row_bcast:15
+    argmax_step<0x143, 0xC>(hi, lo);   // row_bcast:31
+    v = __int_as_float(__builtin_amdgcn_readlane(hi, 63));
+    idx = 63 - __builtin_amdgcn_readlane(lo, 63);
+}
 
 template <int D>
-__device__ void ns_role(int h, char* lds_raw, const uint32_t* __restrict__ qfix, const uint32_t* __restrict__ kfix,
-                        const float* __restrict__ frame, int m, int T, float eps, float* __restrict__ XT,
-                        float* __restrict__ cinfo) {
+__global__ __launch_bounds__(256) void frame_ns_kernel(
+    const float* __restrict__ qt, const float* __restrict__ kt, const double* __restrict__ vseg,
+    const float* __restrict__ segmax, const float* __restrict__ vsegmax, float* __restrict__ frame,
+    uint32_t* __restrict__ qfix, uint32_t* __restrict__ kfix, float* __restrict__ vbar, float* __restrict__ XT,
+    float* __restrict__ cinfo, int n, int m, float lambda, int T, float eps) {
     constexpr int D2 = D / 2;
-    const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
-    const int rb = w >> 1, cb = w & 1;
-    _Float16* base = reinterpret_cast<_Float16*>(lds_raw);
-    _Float16* Wh = base;
-    _Float16* Wl = base + 1 * 64 * kLP;
-    _Float16* Xh = base + 2 * 64 * kLP;
-    _Float16* Xl = base + 3 * 64 * kLP;
-    _Float16* XTh = base + 4 * 64 * kLP;
-    _Float16* XTl = base + 5 * 64 * kLP;
-    _Float16* TTh = base + 6 * 64 * kLP;
-    _Float16* TTl = base + 7 * 64 * kLP;
-    // set-up only: W in fp32 and the landmark-key table (alias XT*/TT* and X*)
-    float* sWf = reinterpret_cast<float*>(base + 4 * 64 * kLP);
-    uint32_t* sK = reinterpret_cast<uint32_t*>(base + 2 * 64 * kLP);
-    unsigned* sred = reinterpret_cast<unsigned*>(base + 8 * 64 * kLP);   // 16 words
-    const float esc = frame[h * 4 + 2];
-    const float ebias = -kTwo23 * esc;
+    constexpr int WPT = 64 * D2 / 256;   // table words per thread (8 at d = 64, 4 at d = 32)
+    constexpr int G = 256 / D;           // landmark groups of the value-mean partial sums
+    constexpr int LPG = 64 / G;          // landmarks per group
+    constexpr int WP = 68;               // fp32 pitch of the set-up copy of W
+    __shared__ __attribute__((aligned(16))) char lds[kSolveLds];
+    const int h = blockIdx.x, tid = threadIdx.x, w = tid >> 6, l = tid & 63;
+    _Float16* base = reinterpret_cast<_Float16*>(lds);
+    _Float16* XTh[2] = {base, base + 2 * 64 * kLP};
+    _Float16* XTl[2] = {base + 64 * kLP, base + 3 * 64 * kLP};
+    _Float16* TTh = base + 4 * 64 * kLP;
+    _Float16* TTl = base + 5 * 64 * kLP;
+    float* sred = reinterpret_cast<float*>(base + 6 * 64 * kLP);   // 64 floats
+    // set-up aliases (all dead before the first writes of the iterations): the landmark
+    // tables and the norm partials in XT[1]; the value partials, then W in fp32, in TT
+    uint32_t* sQ = reinterpret_cast<uint32_t*>(XTh[1]);
+    uint32_t* sK = sQ + 64 * D2;
+    float* part = reinterpret_cast<float*>(sK + 64 * D2);   // 8 x 64 floats
+    float* sWf = reinterpret_cast<float*>(TTh);
+    double* vpart = reinterpret_cast<double*>(TTh);         // G x D = 256 doubles, before sWf
+    static_assert(2 * 64 * D2 * 4 + 512 * 4 <= 2 * 64 * kLP * 2, "set-up data exceeds XT[1]");
+    static_assert(64 * WP * 4 <= 2 * 64 * kLP * 2, "fp32 W exceeds TT");
+    static_assert(G * D == 256, "value partials");
 
-    // landmark-query row of lane a in registers, landmark-key table in LDS (one round trip each)
-    uint32_t qa[D2];
-    {
-        const uint4* qp = reinterpret_cast<const uint4*>(qfix + ((size_t)h * 64 + l) * D2);
+    // ---- frame: every global read first
+    float q0[WPT], q1[WPT], k0[WPT], k1[WPT];
 #pragma unroll
-        for (int c4 = 0; c4 < D2 / 4; ++c4) {
-            const uint4 x = qp[c4];
-            qa[4 * c4] = x.x; qa[4 * c4 + 1] = x.y; qa[4 * c4 + 2] = x.z; qa[4 * c4 + 3] = x.w;
-        }
-        const uint4* kp = reinterpret_cast<const uint4*>(kfix + (size_t)h * 64 * D2);
-        uint4* sk4 = reinterpret_cast<uint4*>(sK);
-#pragma unroll
-        for (int r = 0; r < 64 * D2 / 4 / 256; ++r) sk4[tid + 256 * r] = kp[tid + 256 * r];
+    for (int r = 0; r < WPT; ++r) {
+        const int e = tid + 256 * r, a = e / D2, c2 = e % D2;
+        const size_t o = ((size_t)h * m + (a < m ? a : 0)) * D + 2 * c2;
+        q0[r] = qt[o]; q1[r] = qt[o + 1]; k0[r] = kt[o]; k1[r] = kt[o + 1];
     }
-    if (tid < 16) sred[tid] = 0u;
+    double vs = 0.0;
+    {
+        // all loads issued before the first add (landmarks past m read row 0 and are dropped)
+        const int c = tid % D, g = tid / D;
+        double vv[LPG];
+#pragma unroll
+        for (int i = 0; i < LPG; ++i) {
+            const int lm = g * LPG + i;
+            vv[i] = vseg[((size_t)h * m + (lm < m ? lm : 0)) * D + c];
+        }
+#pragma unroll
+        for (int i = 0; i < LPG; ++i) vs += g * LPG + i < m ? vv[i] : 0.0;
+    }
+    const int tm = tid < m ? tid : 0;
+    float sa = segmax[(size_t)h * m + tm], sb = vsegmax[(size_t)h * m + tm];
+    if (tid >= m) sa = sb = 0.f;
+    vpart[tid] = vs;   // [g][c]
+    if (w == 0) {
+        const bool bad = __any(!(isfinite(sa) && isfinite(sb)));
+        float R = wave_max_dpp(sa);
+        const float vm = wave_max_dpp(sb);
+        if (l == 0) {
+            if (R == 0.f) R = 1.f;
+            const float S = (float)(65535.0 / (2.0 * (double)R));
+            float vscale = 1.f;
+            if (vm > 16384.f) vscale = exp2f(-ceilf(log2f(vm / 16384.f)));
+            const float inv2R = (float)(0.5 / (double)R);
+            const float escale = (float)(-1.4426950408889634 / ((double)lambda * (double)S));
+            frame[h * 4 + 0] = bad ? __builtin_nanf("") : R;
+            frame[h * 4 + 1] = inv2R;
+            frame[h * 4 + 2] = escale;
+            frame[h * 4 + 3] = vscale;
+            sred[0] = inv2R;
+            sred[1] = escale;
+        }
+    }
     __syncthreads();
-    // W[a][b] = k(qt_a, kt_b) (+ eps on the diagonal): lane a, wave w takes b in [16w, 16w+16)
-#pragma unroll 2
+    if (tid < D) {
+        double t = 0.0;
+#pragma unroll
+        for (int g = 0; g < G; ++g) t += vpart[g * D + tid];
+        vbar[(size_t)h * D + tid] = (float)(t / n);
+    }
+    const float inv2R = sred[0], esc = sred[1];
+    const float ebias = -kTwo23 * esc;
+    uint32_t* qtab = qfix + (size_t)h * 64 * D2;
+    uint32_t* ktab = kfix + (size_t)h * 64 * D2;
+#pragma unroll
+    for (int r = 0; r < WPT; ++r) {
+        const int e = tid + 256 * r, a = e / D2;
+        const uint32_t uq = a < m ? fix2(q0[r], q1[r], inv2R) : 0u;
+        const uint32_t uk = a < m ? fix2(k0[r], k1[r], inv2R) : 0u;
+        qtab[e] = uq;
+        ktab[e] = uk;
+        sQ[e] = uq;
+        sK[e] = uk;
+    }
+    __syncthreads();
+
+    // ---- W[a][b] = k(qt_a, kt_b) (+ eps on the diagonal): lane a, columns b = 16w..16w+15
+    uint32_t qa[D2];
+#pragma unroll
+    for (int c4 = 0; c4 < D2 / 4; ++c4) {
+        const uint4 x = reinterpret_cast<const uint4*>(sQ + l * D2)[c4];
+        qa[4 * c4] = x.x; qa[4 * c4 + 1] = x.y; qa[4 * c4 + 2] = x.z; qa[4 * c4 + 3] = x.w;
+    }
+    // the key-landmark rows b are read by the whole wave at one address (LDS broadcast)
+    float wv[16];
+#pragma unroll 4
     for (int bb = 0; bb < 16; ++bb) {
-        const int b = 16 * w + bb;
-        const uint4* kr = reinterpret_cast<const uint4*>(sK + b * D2);
+        const uint4* kr = reinterpret_cast<const uint4*>(sK + (16 * w + bb) * D2);
         uint32_t u0 = 0x4B000000u, u1 = 0u;
 #pragma unroll
         for (int c4 = 0; c4 < D2 / 4; ++c4) {
@@ -367,95 +447,121 @@ __device__ void ns_role(int h, char* lds_raw, const uint32_t* __restrict__ qfix,
             u0 = __builtin_amdgcn_sad_u16(qa[4 * c4 + 2], t.z, u0);
             u1 = __builtin_amdgcn_sad_u16(qa[4 * c4 + 3], t.w, u1);
         }
-        float v = __builtin_amdgcn_exp2f(fmaf(__uint_as_float(u0 + u1), esc, ebias));
-        if (l == b) v += eps;
-        sWf[l * 65 + b] = (l < m && b < m) ? v : 0.f;
+        wv[bb] = __builtin_amdgcn_exp2f(fmaf(__uint_as_float(u0 + u1), esc, ebias));
+    }
+#pragma unroll
+    for (int bb = 0; bb < 16; ++bb) {
+        const int b = 16 * w + bb;
+        if (l == b) wv[bb] += eps;
+        wv[bb] = (l < m && b < m) ? wv[bb] : 0.f;
+    }
+    // row partial sums from registers, W (fp32) to LDS for the column partial sums
+    float rsum = 0.f, wmax = 0.f;
+#pragma unroll
+    for (int bb = 0; bb < 16; ++bb) {
+        rsum += fabsf(wv[bb]);
+        wmax = fmaxf(wmax, fabsf(wv[bb]));
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+        *reinterpret_cast<float4*>(sWf + l * WP + 16 * w + 4 * q) =
+            make_float4(wv[4 * q], wv[4 * q + 1], wv[4 * q + 2], wv[4 * q + 3]);
+    wmax = wave_max_dpp(wmax);
+    if (l == 0) sred[16 + w] = wmax;
+    __syncthreads();
+    {
+        float csum = 0.f;   // column l, rows 16w..16w+15
+#pragma unroll
+        for (int i = 0; i < 16; ++i) csum += fabsf(sWf[(16 * w + i) * WP + l]);
+        part[w * 64 + l] = csum;
+        part[256 + w * 64 + l] = rsum;   // row l, columns 16w..16w+15
     }
     __syncthreads();
-    // column sums (wave 0) and row sums (wave 1) into LDS, the largest |W| by LDS atomic max
-    float* csum = reinterpret_cast<float*>(sred + 16);   // 128 floats after the 16 words
-    if (w < 2) {
-        float sum = 0.f, mx = 0.f;
-#pragma unroll
-        for (int i = 0; i < 64; ++i) {
-            const float x = fabsf(w == 0 ? sWf[i * 65 + l] : sWf[l * 65 + i]);
-            sum += x;
-            mx = fmaxf(mx, x);
+    if (w == 0) {
+        // column and row sums in a fixed order, then the first maximising column / row
+        float n1 = ((part[l] + part[64 + l]) + part[128 + l]) + part[192 + l];
+        float ninf = ((part[256 + l] + part[320 + l]) + part[384 + l]) + part[448 + l];
+        int bs, as;
+        wave_argmax_dpp(n1, bs);
+        wave_argmax_dpp(ninf, as);
+        if (l == 0) {
+            const float c = n1 * ninf;
+            sred[2] = c;
+            sred[3] = fmaxf(fmaxf(sred[16], sred[17]), fmaxf(sred[18], sred[19]));
+            cinfo[h * 4 + 0] = c;
+            cinfo[h * 4 + 1] = n1;
+            cinfo[h * 4 + 2] = ninf;
+            cinfo[h * 4 + 3] = (float)(as * 256 + bs);
         }
-        csum[64 * w + l] = sum;
-        mx = wave_max_dpp(mx);
-        if (l == 0 && w == 0) sred[0] = __float_as_uint(mx);
     }
     __syncthreads();
-    // first maximising column / row (all 128 sums loaded at once, then a serial scan)
-    if (tid == 0) {
-        float sums[128];
-#pragma unroll
-        for (int i = 0; i < 128; ++i) sums[i] = csum[i];
-        float n1 = -1.f, ninf = -1.f;
-        int bs = 0, as = 0;
-#pragma unroll
-        for (int i = 0; i < 64; ++i) {
-            if (sums[i] > n1) { n1 = sums[i]; bs = i; }
-            if (sums[64 + i] > ninf) { ninf = sums[64 + i]; as = i; }
-        }
-        const float c = n1 * ninf;
-        reinterpret_cast<float*>(sred)[1] = c;
-        cinfo[h * 4 + 0] = c;
-        cinfo[h * 4 + 1] = n1;
-        cinfo[h * 4 + 2] = ninf;
-        cinfo[h * 4 + 3] = (float)(as * 256 + bs);
-    }
-    // W and X0 = W^T / c into the fp16-pair tiles (all of sWf is read before it is overwritten)
-    float wv[16];
-#pragma unroll
-    for (int k = 0; k < 16; ++k) wv[k] = sWf[((tid + 256 * k) >> 6) * 65 + ((tid + 256 * k) & 63)];
-    __syncthreads();
-    const float c = reinterpret_cast<float*>(sred)[1];
+    const float c = sred[2];
     const float inv_c = c > 0.f ? 1.f / c : 0.f;
-    float xs = ldexpf(1.f, pow2_exp(__uint_as_float(sred[0]) * inv_c));   // X_true = X_stored * xs
-    const float x0s = inv_c / xs;
+    float mx = sred[3] * inv_c;             // max |X0|
+    float xs = ldexpf(1.f, pow2_exp(mx));   // X_true = X_stored * xs
+    // X0^T = W / c (X0's transposed copy): sixteen consecutive b of row a
+    {
+        const float x0s = inv_c / xs;
+        _Float16 xh[16], xl[16];
 #pragma unroll
-    for (int k = 0; k < 16; ++k) {
-        const int e = tid + 256 * k, a = e >> 6, b = e & 63;
-        _Float16 hi, lo;
-        split_f16(wv[k], hi, lo);
-        Wh[a * kLP + b] = hi;
-        Wl[a * kLP + b] = lo;
-        split_f16(wv[k] * x0s, hi, lo);   // X0[b][a]
-        Xh[b * kLP + a] = hi;
-        Xl[b * kLP + a] = lo;
-        XTh[a * kLP + b] = hi;
-        XTl[a * kLP + b] = lo;
-        if (T == 0) XT[(size_t)h * 4096 + b * 64 + a] = wv[k] * inv_c;
+        for (int bb = 0; bb < 16; ++bb) split_f16(wv[bb] * x0s, xh[bb], xl[bb]);
+        const int o = l * kLP + 16 * w;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            *reinterpret_cast<h8_t*>(XTh[0] + o + 8 * q) = *reinterpret_cast<const h8_t*>(xh + 8 * q);
+            *reinterpret_cast<h8_t*>(XTl[0] + o + 8 * q) = *reinterpret_cast<const h8_t*>(xl + 8 * q);
+        }
+        if (T == 0) {
+#pragma unroll
+            for (int bb = 0; bb < 16; ++bb) XT[(size_t)h * 4096 + (16 * w + bb) * 64 + l] = wv[bb] * inv_c;
+        }
+    }
+    const int rb = w >> 1, cb = w & 1;
+    // the wave's rows of W as MFMA A operands (rows 32 rb + l%32, k = 16 s4 + 8(l/32)..+8),
+    // taken from the fp32 copy
+    h8_t wah[4], wal[4];
+#pragma unroll
+    for (int s4 = 0; s4 < 4; ++s4) {
+        const float* src = sWf + (32 * rb + (l & 31)) * WP + 16 * s4 + 8 * (l >> 5);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            _Float16 a, b;
+            split_f16(src[i], a, b);
+            wah[s4][i] = a;
+            wal[s4][i] = b;
+        }
     }
     __syncthreads();
     for (int t = 0; t < T; ++t) {
-        // T1 = 2I - W X
-        f32x16_t p = mm_split(Wh, Wl, XTh, XTl, rb, cb);
+        const int cur = t & 1;
+        // T1 = 2I - W X, stored transposed
+        f32x16_t p = mm32_split(wah, wal, XTh[cur], XTl[cur], cb);
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const int row = 32 * rb + c_row(r, l), col = 32 * cb + (l & 31);
             p[r] = (row == col ? 2.f : 0.f) - p[r] * xs;
         }
-        store_split(p, 1.f, rb, cb, nullptr, nullptr, TTh, TTl);
+        store32_t(p, 1.f, rb, cb, TTh, TTl);
         __syncthreads();
-        // X_{t+1} = X T1, its largest magnitude by LDS atomic max (slot 2 + t % 8, reset ahead)
-        f32x16_t xn = mm_split(Xh, Xl, TTh, TTl, rb, cb);
-        float mx = 0.f;
+        // X_{t+1} = X T1
+        h8_t xah[4], xal[4];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            xn[r] *= xs;
-            mx = fmaxf(mx, fabsf(xn[r]));
+        for (int s4 = 0; s4 < 4; ++s4) {
+            xah[s4] = a_from_transposed(XTh[cur], rb, 16 * s4);
+            xal[s4] = a_from_transposed(XTl[cur], rb, 16 * s4);
         }
-        mx = wave_max_dpp(mx);
-        float* slot = reinterpret_cast<float*>(&sred[4 + 4 * (t & 1)]);   // alternating sets of 4
-        if (l == 0) slot[w] = mx;
-        __syncthreads();
+        f32x16_t xn = mm32_split(xah, xal, TTh, TTl, cb) * xs;
         if (t + 1 < T) {
-            xs = ldexpf(1.f, pow2_exp(fmaxf(fmaxf(slot[0], slot[1]), fmaxf(slot[2], slot[3]))));
-            store_split(xn, 1.f / xs, rb, cb, Xh, Xl, XTh, XTl);
+            // scale of X_{t+1} from the maximum of X_t (mx)
+            xs = ldexpf(1.f, (mx > 0.f && isfinite(mx)) ? ilogbf(mx) - 7 : 0);
+            store32_t(xn, 1.f / xs, rb, cb, XTh[cur ^ 1], XTl[cur ^ 1]);
+            float lm = 0.f;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) lm = fmaxf(lm, fabsf(xn[r]));
+            lm = wave_max_dpp(lm);
+            if (l == 0) sred[32 + 4 * cur + w] = lm;
             __syncthreads();
+            mx = fmaxf(fmaxf(sred[32 + 4 * cur], sred[33 + 4 * cur]), fmaxf(sred[34 + 4 * cur], sred[35 + 4 * cur]));
         } else {
 #pragma unroll
             for (int r = 0; r < 16; ++r)
@@ -469,9 +575,17 @@ __device__ void ns_role(int h, char* lds_raw, const uint32_t* __restrict__ qfix,
 // takes 64-key tiles (lane = key) on its own, with its own LDS region (no block barrier in the
 // loop).  Per tile: u(k_j) in registers, the value row to fp16 in LDS transposed ([c][j]), the
 // m kernel values exp(-||qt_a - k_j||_1/lambda) from v_sad_u16 against the landmark table
-// (wave-uniform, scalar loads) into LDS as [a][j], then U[a][c] += sum_j B[a][j] V[j][c] (and
-// the ones column) on fp16 MFMA 32x32x16.  The raw rows of the next tile are loaded while the
-// current one is computed.
+// into LDS as [a][j], then U[a][c] += sum_j B[a][j] V[j][c] (and the ones column) on fp16
+// MFMA 32x32x16.  The raw rows of the next tile are loaded while the current one is computed.
+//
+// The landmark rows are wave-uniform and come through scalar registers, one row per step in
+// two alternating buffers: the scalar loads of row a+1 are issued right after the first use
+// of row a (which is the point where the wave waits for row a), so each row's load has a
+// whole step of 32 v_sad_u16 to arrive.  Scalar loads complete out of order, so the wait
+// cannot be narrowed to one of several outstanding rows; issuing after the wait keeps exactly
+// one row in flight.
+constexpr int kKeyTileLds = 4 * 2 * 64 * kLP * 2;   // four waves' [a][j] and [c][j] fp16 tiles
+
 __device__ __forceinline__ void wave_lds_sync() {
     // LDS requests of one wave complete in order; this only keeps the compiler from moving
     // the reads of other lanes' writes above the writes.
@@ -495,6 +609,7 @@ __device__ void key_role(int h, int kb, char* lds_raw, const uint16_t* __restric
     const int j_begin = kb * kpb, j_end = min(n, j_begin + kpb);
     const int ntiles = (j_end - j_begin + 63) / 64;
     const int RB = m > 32 ? 2 : 1;
+    const int mp = (m + 1) & ~1;   // landmark rows written per tile (an odd m writes one zero row)
     f32x16_t acc[2][CB + 1];
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb)
@@ -503,64 +618,85 @@ __device__ void key_role(int h, int kb, char* lds_raw, const uint16_t* __restric
     h8_t ones;
 #pragma unroll
     for (int i = 0; i < 8; ++i) ones[i] = (l & 31) == 0 ? (_Float16)1.f : (_Float16)0.f;
-    for (int a = m; a < 64; ++a) sB[a * kLP + l] = (_Float16)0.f;   // rows a >= m stay zero
+    for (int a = mp; a < 64; ++a) sB[a * kLP + l] = (_Float16)0.f;   // rows a >= m stay zero
 
-    uint4 kr[D8], vr[D8];
-    auto load_rows = [&](int tile) {
+    // rows of keys past the end keep stale values: their kernel values and value pairs are
+    // masked to zero below
+    uint4 kr[D8] = {}, vr[D8] = {};
+    auto row_ptrs = [&](int tile, const uint4*& kp, const uint4*& vp) {
         const int j = j_begin + tile * 64 + l;
-        if (tile < ntiles && j < j_end) {
-            const uint4* kp = reinterpret_cast<const uint4*>(K + ((size_t)h * n + j) * D);
-            const uint4* vp = reinterpret_cast<const uint4*>(V + ((size_t)h * n + j) * D);
-#pragma unroll
-            for (int c8 = 0; c8 < D8; ++c8) {
-                kr[c8] = kp[c8];
-                vr[c8] = vp[c8];
-            }
-        }
+        const bool ok = tile < ntiles && j < j_end;
+        kp = ok ? reinterpret_cast<const uint4*>(K + ((size_t)h * n + j) * D) : nullptr;
+        vp = ok ? reinterpret_cast<const uint4*>(V + ((size_t)h * n + j) * D) : nullptr;
     };
-    load_rows(w);
-    for (int tile = w; tile < ntiles; tile += 4) {
-        const int j = j_begin + tile * 64 + l;
-        const bool valid = j < j_end;
-        uint32_t kf[D2];
-        if (valid) {
+    {
+        // the first tile: keys first (the landmark loop needs them), values behind them
+        const uint4 *kp, *vp;
+        row_ptrs(w, kp, vp);
+        if (kp) {
 #pragma unroll
-            for (int c8 = 0; c8 < D8; ++c8) {
-                const uint32_t xw[4] = {kr[c8].x, kr[c8].y, kr[c8].z, kr[c8].w};
-                const uint32_t yw[4] = {vr[c8].x, vr[c8].y, vr[c8].z, vr[c8].w};
+            for (int c8 = 0; c8 < D8; ++c8) kr[c8] = kp[c8];
 #pragma unroll
-                for (int t = 0; t < 4; ++t) {
-                    kf[4 * c8 + t] = fix2_bf16(xw[t], inv2R);
-                    sV[(8 * c8 + 2 * t) * kLP + l] = (_Float16)(bf16_lo(yw[t]) * vsc);
-                    sV[(8 * c8 + 2 * t + 1) * kLP + l] = (_Float16)(bf16_hi(yw[t]) * vsc);
-                }
-            }
-        } else {
-#pragma unroll
-            for (int c = 0; c < D2; ++c) kf[c] = 0u;
-#pragma unroll
-            for (int c = 0; c < D; ++c) sV[c * kLP + l] = (_Float16)0.f;
+            for (int c8 = 0; c8 < D8; ++c8) vr[c8] = vp[c8];
         }
-        load_rows(tile + 4);
-        // two landmarks per step: one scalar fetch of 2 table rows, two independent sad chains;
-        // rows 2p, 2p+1 of the [a][j] tile (rows >= m were zeroed once; an odd m writes the
-        // zero of landmark m into row m, which stays zero)
-        uint16_t* brow = reinterpret_cast<uint16_t*>(sB) + l;
-#pragma unroll 1
-        for (int p = 0; 2 * p < m; ++p) {
-            const uint32_t* t0 = tab + (2 * p) * D2;
-            const uint32_t* t1 = t0 + D2;
-            uint32_t u0 = 0x4B000000u, u1 = 0x4B000000u;
+    }
+    // Each wave walks the landmark rows from its own starting pair, so that the waves sharing
+    // a CU (and its scalar cache) fetch different rows of the table at first instead of all
+    // waiting on the same row.  The order only decides which row of the B tile is written
+    // when, not the result.
+    const int npairs = (m + 1) >> 1;
+    const int rot = ((__builtin_amdgcn_readfirstlane(w) + 4 * (int)(blockIdx.x & 1)) * npairs) >> 3;
+    for (int tile = w; tile < ntiles; tile += 4) {
+        // keys past the end of the chunk have zero rows; their kernel values are masked to 0
+        const uint32_t vmask = j_begin + tile * 64 + l < j_end ? 0xffffffffu : 0u;
+        uint32_t kf[D2];
 #pragma unroll
-            for (int c = 0; c < D2; ++c) {
-                u0 = __builtin_amdgcn_sad_u16(kf[c], t0[c], u0);
-                u1 = __builtin_amdgcn_sad_u16(kf[c], t1[c], u1);
+        for (int c8 = 0; c8 < D8; ++c8) {
+            kf[4 * c8 + 0] = fix2_bf16(kr[c8].x, inv2R);
+            kf[4 * c8 + 1] = fix2_bf16(kr[c8].y, inv2R);
+            kf[4 * c8 + 2] = fix2_bf16(kr[c8].z, inv2R);
+            kf[4 * c8 + 3] = fix2_bf16(kr[c8].w, inv2R);
+        }
+        // The next tile's keys are fetched in D/8 column groups spread over the landmark
+        // loop, so that the key stream reaches memory as a steady flow rather than one burst
+        // per tile from every wave at once; its values follow after this tile's values have
+        // been moved to LDS.
+        const uint4 *kp, *vp;
+        row_ptrs(tile + 4, kp, vp);
+        // landmark pairs (2p, 2p+1): rows 2p, 2p+1 of the [a][j] tile; table rows >= m are zero
+        // and the value of landmark m (odd m) is replaced by 0
+        uint16_t* brow = reinterpret_cast<uint16_t*>(sB) + l;
+        uint32_t ta[D2], tb[D2];
+        load_row<D2>(ta, tab + (2 * rot) * D2);
+        int p = rot;
+#pragma unroll
+        for (int c8 = 0; c8 < D8; ++c8) {
+            if (kp) kr[c8] = kp[c8];
+#pragma unroll 1
+            for (int i = c8 * npairs / D8; i < (c8 + 1) * npairs / D8; ++i) {
+                const int pn = p + 1 < npairs ? p + 1 : 0;
+                const float b0 = lap_row<D2>(kf, ta, tb, tab + (2 * p + 1) * D2, esc, ebias);
+                const float b1 = lap_row<D2>(kf, tb, ta, tab + (2 * pn) * D2, esc, ebias);
+                const uint32_t v = pk_f16(b0, 2 * p + 1 < m ? b1 : 0.f) & vmask;
+                brow[(2 * p) * kLP] = (uint16_t)(v & 0xffffu);
+                brow[(2 * p + 1) * kLP] = (uint16_t)(v >> 16);
+                p = pn;
             }
-            const float b0 = __builtin_amdgcn_exp2f(fmaf(__uint_as_float(u0), esc, ebias));
-            const float b1 = __builtin_amdgcn_exp2f(fmaf(__uint_as_float(u1), esc, ebias));
-            const uint32_t v = valid ? pk_f16(b0, 2 * p + 1 < m ? b1 : 0.f) : 0u;
-            brow[(2 * p) * kLP] = (uint16_t)(v & 0xffffu);
-            brow[(2 * p + 1) * kLP] = (uint16_t)(v >> 16);
+        }
+        // this tile's values to fp16 (times the value prescale), transposed into LDS
+#pragma unroll
+        for (int c8 = 0; c8 < D8; ++c8) {
+            const uint32_t yw[4] = {vr[c8].x, vr[c8].y, vr[c8].z, vr[c8].w};
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const uint32_t pv = pk_f16(bf16_lo(yw[t]) * vsc, bf16_hi(yw[t]) * vsc) & vmask;
+                reinterpret_cast<uint16_t*>(sV)[(8 * c8 + 2 * t) * kLP + l] = (uint16_t)(pv & 0xffffu);
+                reinterpret_cast<uint16_t*>(sV)[(8 * c8 + 2 * t + 1) * kLP + l] = (uint16_t)(pv >> 16);
+            }
+        }
+        if (vp) {
+#pragma unroll
+            for (int c8 = 0; c8 < D8; ++c8) vr[c8] = vp[c8];
         }
         wave_lds_sync();
 #pragma unroll
@@ -583,10 +719,12 @@ __device__ void key_role(int h, int kb, char* lds_raw, const uint16_t* __restric
         wave_lds_sync();
     }
     __syncthreads();
-    // per-wave partials to LDS as [a][c] (64 x (D+1) floats), then a fixed-order block sum;
-    // the value columns were formed from V * vscale
+    // per-wave partials to LDS as [c][a] (pitch 65: the 32 lanes of a row block write 32
+    // columns to 32 different banks), then a fixed-order block sum to Upart[h][kb][c][a]
+    // (64 rows a per column); the value columns were formed from V * vscale
+    constexpr int PP = 65;
     const float inv_vsc = 1.f / vsc;
-    float* sP = reinterpret_cast<float*>(lds_raw) + w * (64 * (D + 1));
+    float* sP = reinterpret_cast<float*>(lds_raw) + w * ((D + 1) * PP);
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
@@ -595,133 +733,136 @@ __device__ void key_role(int h, int kb, char* lds_raw, const uint16_t* __restric
             for (int r = 0; r < 16; ++r) {
                 const int a = 32 * rb + c_row(r, l);
                 const int c = cb < CB ? 32 * cb + (l & 31) : D;
-                if (cb < CB || (l & 31) == 0) sP[a * (D + 1) + c] = acc[rb][cb][r] * (cb < CB ? inv_vsc : 1.f);
+                if (cb < CB || (l & 31) == 0) sP[c * PP + a] = acc[rb][cb][r] * (cb < CB ? inv_vsc : 1.f);
             }
     __syncthreads();
     const float* base = reinterpret_cast<const float*>(lds_raw);
-    for (int e = tid; e < m * (D + 1); e += 256) {
+    float* dst = Upart + ((size_t)h * nkb + kb) * (D + 1) * 64;
+    for (int e = tid; e < (D + 1) * 64; e += 256) {
+        const int c = e >> 6, a = e & 63;
         float t = 0.f;
 #pragma unroll
-        for (int ww = 0; ww < 4; ++ww) t += base[ww * 64 * (D + 1) + e];
-        Upart[((size_t)h * nkb + kb) * m * (D + 1) + e] = t;
+        for (int ww = 0; ww < 4; ++ww) t += base[ww * (D + 1) * PP + c * PP + a];
+        dst[e] = t;
     }
 }
 
 // ------------------------------------------------------------------------------------------
-// One launch for both independent halves of the middle of the forward: blocks [0, BH) solve
-// Newton-Schulz (they only need the landmarks), blocks [BH, BH + BH*nkb) form the key-side
-// partial sums.  The solver blocks come first so they start at once.
-constexpr int kKeyLds = 4 * 2 * 64 * kLP * 2;
-constexpr int kNsKeyLds = kNsLds > kKeyLds ? kNsLds : kKeyLds;
+// Key-side partial sums: blocks [0, BH*nkb), one key chunk each.
+constexpr int kKeyLds = kKeyTileLds;
+static_assert(4 * 65 * 65 * 4 <= kKeyTileLds, "key partials exceed the tile space");
 
 template <int D>
-__global__ __launch_bounds__(256) void nskey_kernel(float* __restrict__ XT, float* __restrict__ cinfo,
-                                                    const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
-                                                    const uint32_t* __restrict__ qfix,
-                                                    const uint32_t* __restrict__ kfix,
-                                                    const float* __restrict__ frame, float* __restrict__ Upart,
-                                                    int BH, int n, int m, int T, float eps, int kpb, int nkb) {
-    __shared__ __attribute__((aligned(16))) char lds[kNsKeyLds];
-    const int b = blockIdx.x;
-    if (b < BH) {
-        ns_role<D>(b, lds, qfix, kfix, frame, m, T, eps, XT, cinfo);
-    } else {
-        const int kbb = xcd_rank(b - BH, BH * nkb, BH);
-        key_role<D>(kbb / nkb, kbb % nkb, lds, K, V, qfix, frame, Upart, n, m, kpb, nkb);
+__global__ __launch_bounds__(256, 2) void key_kernel(const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
+                                                     const uint32_t* __restrict__ qfix,
+                                                     const float* __restrict__ frame, float* __restrict__ Upart,
+                                                     int BH, int n, int m, int kpb, int nkb) {
+    __shared__ __attribute__((aligned(16))) char lds[kKeyLds];
+    const int b = blockIdx.x, nkey = BH * nkb;
+    int kbb = xcd_rank(b, nkey, 0);
+    if ((nkey & 255) == 0) {
+        // When the key blocks fill whole rounds of the 8 x 32 CUs, the blocks of one XCD that
+        // would share a CU (its 32 CUs take local blocks i, i + 32, ...) get adjacent key
+        // chunks of one head, so a CU's scalar cache holds one landmark table.
+        const int per = nkey >> 3, R = nkey >> 8, i = kbb % per;
+        kbb = kbb - i + (i & 31) * R + (i >> 5);
     }
+    key_role<D>(kbb / nkb, kbb % nkb, lds, K, V, qfix, frame, Upart, n, m, kpb, nkb);
 }
 
 // ------------------------------------------------------------------------------------------
-// U = sum over key chunks, M = X_T U, and the MFMA operand tiles of M for the query side.
-// grid (BH), 1024 threads.  Tiles: Mt[h][s][cb][part][lane][i] = part of
-// M[16s + 8(lane/32) + i][column of (cb, lane%32)] * 2^-e, part 0 = fp16 value, part 1 = fp16
-// residual; column (cb, j) is 32cb + j for cb < D/32 and, for cb = D/32, the ones column d
-// when j = 0 (else zero).  One power-of-two scale for the value columns and one for the ones
-// column (mscale[h][0], mscale[h][1] = 2^e): the largest magnitude lands in [2^14, 2^15).
+// U = sum over key chunks, M = X_T U, and the MFMA operand tiles of M for the query side, by
+// column groups: grid (NG, BH) with NG = D/8 + 1, 512 threads.  Group g < D/8 holds value
+// columns 8g..8g+7, group D/8 the ones column D.  M = X_T U is separable by columns, so each
+// block sums only its columns of the chunk partials (Upart[h][kb][c][a], four quarters of the
+// chunks combined in a fixed order) and forms only its columns of M.
+// Tiles: Mt[h][s][cb][part][lane][i] = part of M[16s + 8(lane/32) + i][column of (cb, lane%32)]
+// times 2^-e_g, part 0 = fp16 value, part 1 = fp16 residual; column (cb, j) is 32cb + j for
+// cb < D/32 and, for cb = D/32, the ones column D when j = 0 (else zero).  mscale[h][g] = 2^e_g
+// puts the largest magnitude of the group's columns in [2^14, 2^15).
 template <int D>
-__global__ __launch_bounds__(1024) void mfinal_kernel(const float* __restrict__ Upart, const float* __restrict__ XT,
-                                                      _Float16* __restrict__ Mt, float* __restrict__ mscale,
-                                                      float* __restrict__ U, float* __restrict__ Mout, int m,
-                                                      int nkb) {
+__global__ __launch_bounds__(512) void mfinal_kernel(const float* __restrict__ Upart, const float* __restrict__ XT,
+                                                     _Float16* __restrict__ Mt, float* __restrict__ mscale,
+                                                     float* __restrict__ Mout, int m, int nkb) {
     constexpr int D1 = D + 1;
     constexpr int CB = D / 32;
-    constexpr int NC = 32 * (CB + 1);       // padded columns of U and M
-    constexpr int PER = (64 * D1 + 1023) / 1024;
-    __shared__ float sU[64 * NC];
+    constexpr int NG = D / 8 + 1;
     __shared__ float sX[64 * 65];
-    __shared__ float sM[64 * NC];
-    __shared__ unsigned smax[2];
-    const int h = blockIdx.x, tid = threadIdx.x, w = tid >> 6, l = tid & 63;
-    if (tid < 2) smax[tid] = 0u;
-    // U = sum of the key-chunk partials: every thread owns PER entries and keeps PER loads in flight
-    const float* up = Upart + (size_t)h * nkb * m * D1;
-    const int mD1 = m * D1;
-    float acc[PER];
+    __shared__ __attribute__((aligned(16))) float sU[8 * 64];   // [c][b]
+    __shared__ __attribute__((aligned(16))) float sM[8 * 64];   // [c][a]
+    __shared__ __attribute__((aligned(16))) float4 red[3 * 128];
+    __shared__ float smx[8];
+    const int g = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, w = tid >> 6, l = tid & 63;
+    const bool ones = g == NG - 1;
+    const int c0 = 8 * g, nc = ones ? 1 : 8;
+    // the group's nc * 64 floats of every chunk partial, as nc * 16 float4; the chunks in four
+    // quarters, eight loads in flight per thread
+    const int f = tid & 127, qq = tid >> 7;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (f < nc * 16) {
+        const float4* src = reinterpret_cast<const float4*>(Upart + ((size_t)h * nkb * D1 + c0) * 64) + f;
+        const int k_lo = qq * nkb / 4, k_hi = (qq + 1) * nkb / 4;
+        for (int k0 = k_lo; k0 < k_hi; k0 += 8) {
+            float4 t[8];
 #pragma unroll
-    for (int r = 0; r < PER; ++r) acc[r] = 0.f;
-    for (int k0 = 0; k0 < nkb; k0 += 8) {
-        float t[8][PER];
+            for (int kk = 0; kk < 8; ++kk)
+                t[kk] = k0 + kk < k_hi ? src[(size_t)(k0 + kk) * D1 * 16] : make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-        for (int kk = 0; kk < 8; ++kk)
-#pragma unroll
-            for (int r = 0; r < PER; ++r) {
-                const int e = tid + 1024 * r;
-                t[kk][r] = (k0 + kk < nkb && e < mD1) ? up[(size_t)(k0 + kk) * mD1 + e] : 0.f;
-            }
-#pragma unroll
-        for (int kk = 0; kk < 8; ++kk)
-#pragma unroll
-            for (int r = 0; r < PER; ++r) acc[r] += t[kk][r];
-    }
-    for (int e = tid; e < 64 * NC; e += 1024) sU[e] = 0.f;
-    for (int e = tid; e < 4096; e += 1024) sX[(e >> 6) * 65 + (e & 63)] = XT[(size_t)h * 4096 + e];
-    __syncthreads();
-#pragma unroll
-    for (int r = 0; r < PER; ++r) {
-        const int e = tid + 1024 * r;
-        if (e < mD1) {
-            sU[(e / D1) * NC + e % D1] = acc[r];
-            U[(size_t)h * mD1 + e] = acc[r];
-        }
-    }
-    __syncthreads();
-    // M = X_T U on fp32 MFMA 32x32x2: wave w < 2 (CB + 1) owns block (w % 2, w / 2)
-    if (w < 2 * (CB + 1)) {
-        const int rb = w & 1, cb = w >> 1;
-        typedef float f32x16_t2 __attribute__((ext_vector_type(16)));
-        f32x16_t2 c = {};
-        const float* a = sX + (32 * rb + (l & 31)) * 65 + (l >> 5);
-        const float* b = sU + (l >> 5) * NC + 32 * cb + (l & 31);
-#pragma unroll 8
-        for (int s2 = 0; s2 < 32; ++s2) c = __builtin_amdgcn_mfma_f32_32x32x2f32(a[2 * s2], b[2 * s2 * NC], c, 0, 0, 0);
-        float mv = 0.f;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int row = 32 * rb + 8 * (r >> 2) + 4 * (l >> 5) + (r & 3), col = 32 * cb + (l & 31);
-            sM[row * NC + col] = c[r];
-            if (row < m && col < D1) {
-                Mout[(size_t)h * mD1 + row * D1 + col] = c[r];
-                mv = fmaxf(mv, fabsf(c[r]));
+            for (int kk = 0; kk < 8; ++kk) {
+                acc.x += t[kk].x; acc.y += t[kk].y; acc.z += t[kk].z; acc.w += t[kk].w;
             }
         }
-        // magnitudes are non-negative: their bit patterns order like the values
-        mv = wave_max_dpp(mv);
-        if (l == 0) atomicMax(&smax[cb == CB ? 1 : 0], __float_as_uint(mv));
+    }
+    for (int e = tid; e < 4096; e += 512) sX[(e >> 6) * 65 + (e & 63)] = XT[(size_t)h * 4096 + e];
+    if (qq > 0 && f < nc * 16) red[(qq - 1) * 128 + f] = acc;
+    __syncthreads();
+    if (qq == 0 && f < nc * 16) {
+        const float4 r1 = red[f], r2 = red[128 + f], r3 = red[256 + f];
+        reinterpret_cast<float4*>(sU)[f] = make_float4(((acc.x + r1.x) + r2.x) + r3.x, ((acc.y + r1.y) + r2.y) + r3.y,
+                                                       ((acc.z + r1.z) + r2.z) + r3.z, ((acc.w + r1.w) + r2.w) + r3.w);
     }
     __syncthreads();
-    const int ev = pow2_exp(__uint_as_float(smax[0])), e1 = pow2_exp(__uint_as_float(smax[1]));
-    if (tid < 2) mscale[h * 2 + tid] = ldexpf(1.f, tid == 0 ? ev : e1);
-    for (int e = tid; e < 4 * (CB + 1) * 64 * 8; e += 1024) {
-        const int i = e & 7, lane = (e >> 3) & 63, cb = (e >> 9) % (CB + 1), s4 = (e >> 9) / (CB + 1);
-        const int row = 16 * s4 + 8 * (lane >> 5) + i, j = lane & 31;
-        float v = 0.f;
-        if (cb < CB) v = ldexpf(sM[row * NC + 32 * cb + j], -ev);
-        else if (j == 0) v = ldexpf(sM[row * NC + D], -e1);
-        const _Float16 hi = (_Float16)v;
-        const _Float16 lo = (_Float16)(v - (float)hi);
-        const size_t o = ((((size_t)h * 4 + s4) * (CB + 1) + cb) * 2) * 512 + lane * 8 + i;
-        Mt[o] = hi;
-        Mt[o + 512] = lo;
+    // M[a][c0 + cc] = sum_b X_T[a][b] U[b][c0 + cc]: thread (cc = tid/64, a = tid%64)
+    float mv = 0.f;
+    if (w < nc) {
+        float t = 0.f;
+#pragma unroll 16
+        for (int b = 0; b < 64; ++b) t = fmaf(sX[l * 65 + b], sU[w * 64 + b], t);
+        sM[w * 64 + l] = t;
+        if (l < m) Mout[((size_t)h * m + l) * D1 + c0 + w] = t;
+        mv = fabsf(t);
+    }
+    mv = wave_max_dpp(mv);
+    if (l == 0) smx[w] = mv;
+    __syncthreads();
+    float mxg = smx[0];
+#pragma unroll
+    for (int i = 1; i < 8; ++i) mxg = fmaxf(mxg, smx[i]);
+    const int e = pow2_exp(mxg);
+    if (tid == 0) mscale[h * NG + g] = ldexpf(1.f, e);
+    // operand tiles: one 16-byte chunk (i = 0..7) per (column, s, lane half, part); the ones
+    // group also writes the zero columns j != 0 of its tile
+    const int chunks = ones ? 64 * 4 * 2 : nc * 4 * 2 * 2;
+    for (int q = tid; q < chunks; q += 512) {
+        int lane, s4, part, cc;
+        if (ones) {
+            lane = q & 63; s4 = (q >> 6) & 3; part = q >> 8; cc = 0;
+        } else {
+            cc = q & 7; const int hl = (q >> 3) & 1; s4 = (q >> 4) & 3; part = q >> 6;
+            lane = ((c0 + cc) & 31) + 32 * hl;
+        }
+        const int cb = ones ? CB : (c0 + cc) >> 5;
+        const bool live = !ones || (lane & 31) == 0;
+        _Float16 v8[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int row = 16 * s4 + 8 * (lane >> 5) + i;
+            const float v = live ? ldexpf(sM[cc * 64 + row], -e) : 0.f;
+            const _Float16 hi = (_Float16)v;
+            v8[i] = part == 0 ? hi : (_Float16)(v - (float)hi);
+        }
+        const size_t o = ((((size_t)h * 4 + s4) * (CB + 1) + cb) * 2 + part) * 512 + lane * 8;
+        *reinterpret_cast<uint4*>(Mt + o) = *reinterpret_cast<const uint4*>(v8);
     }
 }
 
@@ -754,7 +895,11 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
     }
     const float R = frame[h * 4 + 0], inv2R = frame[h * 4 + 1], esc = frame[h * 4 + 2];
     const float ebias = -kTwo23 * esc;
-    const float scv = mscale[h * 2 + 0], sc1 = mscale[h * 2 + 1];
+    constexpr int NG = D / 8 + 1;
+    float scv[D / 8];
+#pragma unroll
+    for (int g = 0; g < D / 8; ++g) scv[g] = mscale[h * NG + g];
+    const float sc1 = mscale[h * NG + D / 8];
     const uint32_t* tab = kfix + (size_t)h * 64 * D2;
     const int i0 = qblk * 256 + w * 64;
     const int i = i0 + l;
@@ -831,10 +976,10 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
         const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[0]), __float_as_uint(acc[0]), false,
                                                          false);
         const float si = __uint_as_float(sw[0]) * sc1;
-        float tmul, tadd;   // o = y * tmul + tadd * vbar
-        if (NORM == NORM_INLINE) { tmul = scv; tadd = 1.f - si; }
-        else if (NORM == NORM_ROWSUM) { tmul = scv / si; tadd = 0.f; }
-        else { tmul = scv; tadd = 0.f; }
+        float tmul, tadd;   // o = y * tmul * scv[group] + tadd * vbar
+        if (NORM == NORM_INLINE) { tmul = 1.f; tadd = 1.f - si; }
+        else if (NORM == NORM_ROWSUM) { tmul = 1.f / si; tadd = 0.f; }
+        else { tmul = 1.f; tadd = 0.f; }
         const int iq = i0 + 32 * qb + (l & 31);
         uint16_t* orow = Out + ((size_t)h * n + iq) * D;
 #pragma unroll
@@ -853,10 +998,11 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
             for (int g = 0; g < 4; ++g) {
                 const int c0 = 32 * cb + 8 * g + 4 * (l >> 5);
                 const float4 vb = *reinterpret_cast<const float4*>(&sVb[c0]);
-                float o0 = fmaf(y[4 * g + 0], tmul, tadd * vb.x);
-                float o1 = fmaf(y[4 * g + 1], tmul, tadd * vb.y);
-                float o2 = fmaf(y[4 * g + 2], tmul, tadd * vb.z);
-                float o3 = fmaf(y[4 * g + 3], tmul, tadd * vb.w);
+                const float tm = tmul * scv[4 * cb + g];   // columns c0..c0+3 are in group 4cb + g
+                float o0 = fmaf(y[4 * g + 0], tm, tadd * vb.x);
+                float o1 = fmaf(y[4 * g + 1], tm, tadd * vb.y);
+                float o2 = fmaf(y[4 * g + 2], tm, tadd * vb.z);
+                float o3 = fmaf(y[4 * g + 3], tm, tadd * vb.w);
                 if (nan_head) o0 = o1 = o2 = o3 = __builtin_nanf("");
                 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
                 const bf16x2_t p0 = {(__bf16)o0, (__bf16)o1}, p1 = {(__bf16)o2, (__bf16)o3};
@@ -886,37 +1032,37 @@ hipError_t launch_fast_pool(const void* Q, const void* K, const void* V, float* 
     return hipGetLastError();
 }
 
-hipError_t launch_fast_frame(const float* qt, const float* kt, const double* vseg, const float* segmax,
-                             const float* vsegmax, float* frame, uint32_t* qfix, uint32_t* kfix, float* vbar, int BH,
-                             int n, int d, int m, float lambda, hipStream_t st) {
+hipError_t launch_fast_frame_ns(const float* qt, const float* kt, const double* vseg, const float* segmax,
+                                const float* vsegmax, float* frame, uint32_t* qfix, uint32_t* kfix, float* vbar,
+                                float* XT, float* cinfo, int BH, int n, int d, int m, float lambda, int T, float eps,
+                                hipStream_t st) {
     if (d == 32)
-        hipLaunchKernelGGL(frame_kernel<32>, dim3(BH), dim3(256), 0, st, qt, kt, vseg, segmax, vsegmax, frame, qfix,
-                           kfix, vbar, n, m, lambda);
+        hipLaunchKernelGGL(frame_ns_kernel<32>, dim3(BH), dim3(256), 0, st, qt, kt, vseg, segmax, vsegmax, frame,
+                           qfix, kfix, vbar, XT, cinfo, n, m, lambda, T, eps);
     else
-        hipLaunchKernelGGL(frame_kernel<64>, dim3(BH), dim3(256), 0, st, qt, kt, vseg, segmax, vsegmax, frame, qfix,
-                           kfix, vbar, n, m, lambda);
+        hipLaunchKernelGGL(frame_ns_kernel<64>, dim3(BH), dim3(256), 0, st, qt, kt, vseg, segmax, vsegmax, frame,
+                           qfix, kfix, vbar, XT, cinfo, n, m, lambda, T, eps);
     return hipGetLastError();
 }
 
-hipError_t launch_fast_nskey(float* XT, float* cinfo, const void* K, const void* V, const uint32_t* qfix,
-                             const uint32_t* kfix, const float* frame, float* Upart, int BH, int n, int d, int m,
-                             int T, float eps, int kpb, int nkb, hipStream_t st) {
-    dim3 grid(BH + BH * nkb);
+hipError_t launch_fast_key(const void* K, const void* V, const uint32_t* qfix, const float* frame, float* Upart,
+                           int BH, int n, int d, int m, int kpb, int nkb, hipStream_t st) {
+    dim3 grid(BH * nkb);
     if (d == 32)
-        hipLaunchKernelGGL(nskey_kernel<32>, grid, dim3(256), 0, st, XT, cinfo, (const uint16_t*)K,
-                           (const uint16_t*)V, qfix, kfix, frame, Upart, BH, n, m, T, eps, kpb, nkb);
+        hipLaunchKernelGGL(key_kernel<32>, grid, dim3(256), 0, st, (const uint16_t*)K, (const uint16_t*)V, qfix, frame,
+                           Upart, BH, n, m, kpb, nkb);
     else
-        hipLaunchKernelGGL(nskey_kernel<64>, grid, dim3(256), 0, st, XT, cinfo, (const uint16_t*)K,
-                           (const uint16_t*)V, qfix, kfix, frame, Upart, BH, n, m, T, eps, kpb, nkb);
+        hipLaunchKernelGGL(key_kernel<64>, grid, dim3(256), 0, st, (const uint16_t*)K, (const uint16_t*)V, qfix, frame,
+                           Upart, BH, n, m, kpb, nkb);
     return hipGetLastError();
 }
 
-hipError_t launch_fast_mfinal(const float* Upart, const float* XT, _Float16* Mt, float* mscale, float* U, float* M,
-                              int BH, int d, int m, int nkb, hipStream_t st) {
+hipError_t launch_fast_mfinal(const float* Upart, const float* XT, _Float16* Mt, float* mscale, float* M, int BH,
+                              int d, int m, int nkb, hipStream_t st) {
     if (d == 32)
-        hipLaunchKernelGGL(mfinal_kernel<32>, dim3(BH), dim3(1024), 0, st, Upart, XT, Mt, mscale, U, M, m, nkb);
+        hipLaunchKernelGGL(mfinal_kernel<32>, dim3(32 / 8 + 1, BH), dim3(512), 0, st, Upart, XT, Mt, mscale, M, m, nkb);
     else
-        hipLaunchKernelGGL(mfinal_kernel<64>, dim3(BH), dim3(1024), 0, st, Upart, XT, Mt, mscale, U, M, m, nkb);
+        hipLaunchKernelGGL(mfinal_kernel<64>, dim3(64 / 8 + 1, BH), dim3(512), 0, st, Upart, XT, Mt, mscale, M, m, nkb);
     return hipGetLastError();
 }
 

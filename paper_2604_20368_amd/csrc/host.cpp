@@ -129,9 +129,9 @@ FastPlan make_fast_plan(int BH, int n, int d, int m) {
     p.vbar = c.take(bh * d * f);
     p.XT = c.take(bh * 64 * 64 * f);
     p.cinfo = c.take(bh * 4 * f);
-    p.Upart = c.take(bh * p.nkb * m * d1 * f);
+    p.Upart = c.take(bh * p.nkb * d1 * 64 * f);   // [h][kb][c][a], 64 rows a
     p.Mt = c.take(bh * 4 * cbp * 2 * 512 * 2);
-    p.mscale = c.take(bh * 2 * f);
+    p.mscale = c.take(bh * ((size_t)d / 8 + 1) * f);
     p.U = c.take(bh * m * d1 * f);
     p.M = c.take(bh * m * d1 * f);
     p.total = (c.off + 255) & ~size_t(255);
@@ -234,23 +234,22 @@ hipError_t forward_fast(Recorder& rec, const FastPlan& p, const void* Q, const v
                                          at<float>(ws, p.segmax), at<float>(ws, p.vsegmax), BH, n, d, m, st);
     });
     if (e != hipSuccess) return e;
-    e = run_named(rec, "frame", [&] {
-        return lapattn::launch_fast_frame(at<float>(ws, p.qt), at<float>(ws, p.kt), at<double>(ws, p.vseg),
-                                          at<float>(ws, p.segmax), at<float>(ws, p.vsegmax), at<float>(ws, p.frame),
-                                          at<uint32_t>(ws, p.qfix), at<uint32_t>(ws, p.kfix), at<float>(ws, p.vbar),
-                                          BH, n, d, m, lambda, st);
+    e = run_named(rec, "frame_ns", [&] {
+        return lapattn::launch_fast_frame_ns(at<float>(ws, p.qt), at<float>(ws, p.kt), at<double>(ws, p.vseg),
+                                             at<float>(ws, p.segmax), at<float>(ws, p.vsegmax), at<float>(ws, p.frame),
+                                             at<uint32_t>(ws, p.qfix), at<uint32_t>(ws, p.kfix), at<float>(ws, p.vbar),
+                                             at<float>(ws, p.XT), at<float>(ws, p.cinfo), BH, n, d, m, lambda, T, eps,
+                                             st);
     });
     if (e != hipSuccess) return e;
-    e = run_named(rec, "ns_key", [&] {
-        return lapattn::launch_fast_nskey(at<float>(ws, p.XT), at<float>(ws, p.cinfo), K, V, at<uint32_t>(ws, p.qfix),
-                                          at<uint32_t>(ws, p.kfix), at<float>(ws, p.frame), at<float>(ws, p.Upart),
-                                          BH, n, d, m, T, eps, p.kpb, p.nkb, st);
+    e = run_named(rec, "key", [&] {
+        return lapattn::launch_fast_key(K, V, at<uint32_t>(ws, p.qfix), at<float>(ws, p.frame), at<float>(ws, p.Upart),
+                                        BH, n, d, m, p.kpb, p.nkb, st);
     });
     if (e != hipSuccess) return e;
     e = run_named(rec, "m_final", [&] {
         return lapattn::launch_fast_mfinal(at<float>(ws, p.Upart), at<float>(ws, p.XT), at<_Float16>(ws, p.Mt),
-                                           at<float>(ws, p.mscale), at<float>(ws, p.U), at<float>(ws, p.M), BH, d, m,
-                                           p.nkb, st);
+                                           at<float>(ws, p.mscale), at<float>(ws, p.M), BH, d, m, p.nkb, st);
     });
     if (e != hipSuccess) return e;
     e = run_named(rec, "query", [&] {

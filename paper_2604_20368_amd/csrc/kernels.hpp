@@ -77,14 +77,14 @@ hipError_t launch_bwd_pool(float* dQ, float* dK, const float* dqtW, const float*
 
 hipError_t launch_fast_pool(const void* Q, const void* K, const void* V, float* qt, float* kt, double* vseg,
                             float* segmax, float* vsegmax, int BH, int n, int d, int m, hipStream_t st);
-hipError_t launch_fast_frame(const float* qt, const float* kt, const double* vseg, const float* segmax,
-                             const float* vsegmax, float* frame, uint32_t* qfix, uint32_t* kfix, float* vbar, int BH,
-                             int n, int d, int m, float lambda, hipStream_t st);
-hipError_t launch_fast_nskey(float* XT, float* cinfo, const void* K, const void* V, const uint32_t* qfix,
-                             const uint32_t* kfix, const float* frame, float* Upart, int BH, int n, int d, int m,
-                             int T, float eps, int kpb, int nkb, hipStream_t st);
-hipError_t launch_fast_mfinal(const float* Upart, const float* XT, _Float16* Mt, float* mscale, float* U, float* M,
-                              int BH, int d, int m, int nkb, hipStream_t st);
+hipError_t launch_fast_frame_ns(const float* qt, const float* kt, const double* vseg, const float* segmax,
+                                const float* vsegmax, float* frame, uint32_t* qfix, uint32_t* kfix, float* vbar,
+                                float* XT, float* cinfo, int BH, int n, int d, int m, float lambda, int T, float eps,
+                                hipStream_t st);
+hipError_t launch_fast_key(const void* K, const void* V, const uint32_t* qfix, const float* frame, float* Upart,
+                           int BH, int n, int d, int m, int kpb, int nkb, hipStream_t st);
+hipError_t launch_fast_mfinal(const float* Upart, const float* XT, _Float16* Mt, float* mscale, float* M, int BH,
+                              int d, int m, int nkb, hipStream_t st);
 hipError_t launch_fast_query(int norm, const void* Q, void* Out, const uint32_t* kfix, const float* frame,
                              const _Float16* Mt, const float* mscale, const float* vbar, int BH, int n, int d, int m,
                              hipStream_t st);

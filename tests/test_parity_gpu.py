@@ -120,6 +120,24 @@ def test_forward_deterministic(L):
     assert np.array_equal(a, b)
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_forward_reused_workspace(L, dtype):
+    """One workspace and one output buffer, two different inputs in turn (then the first
+    again): every call must see its own tables, never values left by the previous call."""
+    w = W.small(W.WORKLOADS["highres"], n=2048, B=1, H=2).with_(dtype=dtype)
+    xs = [W.make_inputs(w.with_(seed=s), with_grad=False) for s in (61, 62)]
+    devs = [[to_dev(x[k], dtype) for k in ("Q", "K", "V")] for x in xs]
+    out = torch.empty_like(devs[0][0])
+    ws = L.workspace(devs[0][0], w.m, w.T)
+    for i in (0, 1, 0):
+        L.forward(*devs[i], w.m, w.lam, w.T, out=out, ws=ws)
+        torch.cuda.synchronize()
+        ref = oracle.forward(xs[i]["Q"], xs[i]["K"], xs[i]["V"], w.m, w.lam, w.T)
+        err = head_rel(to_np(out), ref)
+        say("reused workspace %s input %d: max head rel err %.3e" % (dtype, i, err))
+        assert err <= TOL[dtype]
+
+
 def test_forward_nan_propagates(L):
     w = W.Workload("nan", 1, 2, 300, 32, 10, 3, "fp32", 0.2, 4.0, 13, False)
     x = W.make_inputs(w, with_grad=False)

@@ -220,35 +220,39 @@ __device__ __forceinline__ float lap_row(const uint32_t (&kf)[D2], const uint32_
 }
 
 // ------------------------------------------------------------------------------------------
-// Per-head frame and Newton-Schulz solve.  grid (BH), 256 threads (4 waves).
+// Per-head frame and Newton-Schulz solve.  grid (BH), 512 threads (8 waves).
 //
 // Frame: frame[h] = {R, 1/(2R), escale = -log2(e) / (lambda S), vscale}; R is NaN when Q, K or
 // V hold a non-finite value (the outputs of that head are then NaN, as the plain computation
 // gives).  qfix/kfix[h][a][c/2] = u(x_{a,c}) | u(x_{a,c+1}) << 16 for landmarks a < 64 (zero
 // rows >= m).  vbar[h] = mean of the values; vscale = 2^-e keeps fp16 copies of V below 2^14.
 //
-// Solve (Algorithm 2): W = K_LL + eps I padded to 64 x 64 (lane = row a, sixteen columns b per
-// wave: v_sad_u16 against the key-landmark rows, which come through scalar loads of the table
-// just written); c = ||W||_1 ||W||_inf (first maximising column / row); X0 = W^T / c (0 if
-// c = 0); X_{t+1} = X_t (2I - W X_t).  Wave w owns the 32 x 32 block (w/2, w%2) of both
-// products, on fp16-pair MFMA 32x32x16 (A B ~ Ahi Bhi + Ahi Blo + Alo Bhi, ~22 significant
-// bits, three independent accumulators); the wave's rows of W stay in registers.  Only
-// transposed copies are stored (X^T, and T1^T for T1 = 2I - W X), with 8-byte writes straight
-// from the MFMA result layout; X enters X T1 as the A factor through transposing LDS reads.
-// X^T alternates between two buffers, so each update needs two block barriers.
-// X is carried with a power-of-two scale: X0's from its exact maximum (largest entry in
-// [2^14, 2^15)), X_{t+1}'s from the maximum of X_t, placing that maximum in [2^7, 2^8).  In
-// exact arithmetic I - W X_t = (I - W X0)^(2^t) with ||I - W X0||_2 <= 1, so
-// ||X_{t+1}||_2 <= 2 ||X_t||_2 and the largest entry grows by at most 2 * 64 = 2^7 per update:
-// stored values stay below 2^15 (fp16 holds 65504).
+// Solve (Algorithm 2): W = K_LL + eps I padded to 64 x 64 (lane = row a, eight columns b per
+// wave, v_sad_u16 against the key-landmark rows read by the whole wave at one LDS address);
+// c = ||W||_1 ||W||_inf (first maximising column / row); X0 = W^T / c (0 if c = 0); then the
+// T updates X_{t+1} = X_t (2I - W X_t).  The updates satisfy I - W X_t = E^(2^t) with
+// E = I - W X0, hence X_{t+1} = X_t (I + E^(2^t)) and
+//   X_T = X0 (I + E_0)(I + E_1) ... (I + E_{T-1}),  E_0 = E,  E_{k+1} = E_k E_k,
+// the same iterates in exact arithmetic.  The two products of a step -- Z <- Z + Z E_k
+// (waves 0-3) and E_{k+1} = E_k E_k (waves 4-7) -- are independent, so a step costs one
+// product and one barrier, and the two chains share every SIMD.  Both run on fp16-pair MFMA
+// 32x32x16 (A B ~ Ahi Bhi + Ahi Blo + Alo Bhi, ~22 significant bits); Z is accumulated in fp32
+// registers.  Only transposed copies are stored (Z^T, E^T), with 8-byte writes straight from the
+// MFMA result layout, each alternating between two buffers; the A factors come through
+// transposing LDS reads.
+// Scales: ||E_k||_2 <= 1 (E's spectrum lies in [0, 1)), so E is stored unscaled.  Z carries a
+// power-of-two scale: Z_0's from its exact maximum (largest entry in [2^14, 2^15)), Z_{k+1}'s
+// from the maximum of Z_k, placing that maximum in [2^7, 2^8); ||I + E_k||_2 <= 2 bounds the
+// growth of the largest entry by 2 * 64 = 2^7 per step, so stored values stay below 2^15.
 //   Writes X_T (fp32, row-major [64][64]) and cinfo = {c, n1, ninf, a* 256 + b*}.
-constexpr int kSolveLds = 6 * 64 * kLP * 2 + 64 * 4;
+constexpr int kSolveLds = 8 * 64 * kLP * 2 + 64 * 4;
+constexpr int kSolveThreads = 512;
 
 // The A operand of MFMA 32x32x16 (8 halves: row 32 rb + l%32, k = k0 + 8(l/32)..+8) of a
 // matrix held transposed in LDS (Mt[k][row], pitch kLP), via two ds_read_b64_tr_b16.  Within a
 // 16-lane group that instruction gives lane i element i%4 of the 4-element reads of lanes
-// 4q + i/4 (q = 0..3): when lane j of the group points at Mt[r0 + j/4][c0 + 4(j%4)], lane i
-// receives Mt[r0 + q][c0 + i], q = 0..3 -- column c0 + i (a row of M) over 4 k values.
+// 4q + i/4 (q = 0..3): when lane j of the group points at Mt[k1 + j/4][r0 + 4(j%4)], lane i
+// receives Mt[k1 + q][r0 + i], q = 0..3 -- row r0 + i of M over 4 consecutive k.
 __device__ __forceinline__ h8_t a_from_transposed(const _Float16* Mt, int rb, int k0) {
     const int l = threadIdx.x & 63, g = l >> 4, i = l & 15;
     const _Float16* p = Mt + (k0 + 8 * (g >> 1) + (i >> 2)) * kLP + 32 * rb + 16 * (g & 1) + 4 * (i & 3);
@@ -278,8 +282,6 @@ __device__ __forceinline__ f32x16_t mm32_split(const h8_t (&ah)[4], const h8_t (
     return hh + (hl + lh);
 }
 
-// Store a wave's 32 x 32 block (times `scale`) transposed as an fp16 pair: four consecutive
-// rows of one column per 8-byte write.
 // Two floats as packed fp16 pairs: hi = rn(x), lo = rn(x - hi) (each one v_cvt_pk_f16_f32).
 __device__ __forceinline__ void split_pk(float x0, float x1, uint32_t& hi, uint32_t& lo) {
     const f16x2_t h = __builtin_convertvector((f32x2_t){x0, x1}, f16x2_t);
@@ -288,6 +290,8 @@ __device__ __forceinline__ void split_pk(float x0, float x1, uint32_t& hi, uint3
     lo = pk_f16(x0 - back[0], x1 - back[1]);
 }
 
+// Store a wave's 32 x 32 block (times `scale`) transposed as an fp16 pair: four consecutive
+// rows of one column per 8-byte write.
 __device__ __forceinline__ void store32_t(const f32x16_t& v, float scale, int rb, int cb, _Float16* MTh,
                                           _Float16* MTl) {
     const int l = threadIdx.x & 63;
@@ -330,40 +334,49 @@ __device__ __forceinline__ void wave_argmax_dpp(float& v, int& idx) {
 }
 
 template <int D>
-__global__ __launch_bounds__(256) void frame_ns_kernel(
+__global__ __launch_bounds__(kSolveThreads) void frame_ns_kernel(
     const float* __restrict__ qt, const float* __restrict__ kt, const double* __restrict__ vseg,
     const float* __restrict__ segmax, const float* __restrict__ vsegmax, float* __restrict__ frame,
     uint32_t* __restrict__ qfix, uint32_t* __restrict__ kfix, float* __restrict__ vbar, float* __restrict__ XT,
     float* __restrict__ cinfo, int n, int m, float lambda, int T, float eps) {
+    constexpr int NT = kSolveThreads;
+    constexpr int NW = NT / 64;          // 8 waves
     constexpr int D2 = D / 2;
-    constexpr int WPT = 64 * D2 / 256;   // table words per thread (8 at d = 64, 4 at d = 32)
-    constexpr int G = 256 / D;           // landmark groups of the value-mean partial sums
+    constexpr int WPT = 64 * D2 / NT;    // table words per thread (4 at d = 64, 2 at d = 32)
+    constexpr int G = NT / D;            // landmark groups of the value-mean partial sums
     constexpr int LPG = 64 / G;          // landmarks per group
+    constexpr int BPW = 64 / NW;         // columns b of W per wave
     constexpr int WP = 68;               // fp32 pitch of the set-up copy of W
     __shared__ __attribute__((aligned(16))) char lds[kSolveLds];
     const int h = blockIdx.x, tid = threadIdx.x, w = tid >> 6, l = tid & 63;
     _Float16* base = reinterpret_cast<_Float16*>(lds);
-    _Float16* XTh[2] = {base, base + 2 * 64 * kLP};
-    _Float16* XTl[2] = {base + 64 * kLP, base + 3 * 64 * kLP};
-    _Float16* TTh = base + 4 * 64 * kLP;
-    _Float16* TTl = base + 5 * 64 * kLP;
-    float* sred = reinterpret_cast<float*>(base + 6 * 64 * kLP);   // 64 floats
-    // set-up aliases (all dead before the first writes of the iterations): the landmark
-    // tables and the norm partials in XT[1]; the value partials, then W in fp32, in TT
-    uint32_t* sQ = reinterpret_cast<uint32_t*>(XTh[1]);
+    // transposed copies, two buffers each: Z^T (ZTh/ZTl(k & 1)) and E^T (ETh/ETl(k & 1)).
+    // Offsets from the LDS base, not an array of pointers: a pointer picked from a local array
+    // by a run-time index loses its address space and would be accessed with flat loads.
+    constexpr int TB = 64 * kLP;
+    auto ZTh = [&](int i) { return base + (2 * i) * TB; };
+    auto ZTl = [&](int i) { return base + (2 * i + 1) * TB; };
+    auto ETh = [&](int i) { return base + (4 + 2 * i) * TB; };
+    auto ETl = [&](int i) { return base + (5 + 2 * i) * TB; };
+    float* sred = reinterpret_cast<float*>(base + 8 * 64 * kLP);   // 64 floats
+    // set-up aliases, each dead before the first write to its buffer: the landmark tables in
+    // Z^T[1]; the norm partials and the value partials in E^T[0]; W in fp32 in E^T[1] (read
+    // until the barrier after E_0, which precedes the first write of E^T[1])
+    uint32_t* sQ = reinterpret_cast<uint32_t*>(ZTh(1));
     uint32_t* sK = sQ + 64 * D2;
-    float* part = reinterpret_cast<float*>(sK + 64 * D2);   // 8 x 64 floats
-    float* sWf = reinterpret_cast<float*>(TTh);
-    double* vpart = reinterpret_cast<double*>(TTh);         // G x D = 256 doubles, before sWf
-    static_assert(2 * 64 * D2 * 4 + 512 * 4 <= 2 * 64 * kLP * 2, "set-up data exceeds XT[1]");
-    static_assert(64 * WP * 4 <= 2 * 64 * kLP * 2, "fp32 W exceeds TT");
-    static_assert(G * D == 256, "value partials");
+    float* part = reinterpret_cast<float*>(ETh(0));          // 2 x NW x 64 floats
+    double* vpart = reinterpret_cast<double*>(ETh(0)) + 512;  // G x D doubles, after part
+    float* sWf = reinterpret_cast<float*>(ETh(1));
+    static_assert(2 * 64 * D2 * 4 <= 2 * 64 * kLP * 2, "landmark tables exceed Z^T[1]");
+    static_assert(2 * NW * 64 * 4 <= 512 * 8 && 512 * 8 + G * D * 8 <= 2 * 64 * kLP * 2, "partials exceed E^T[0]");
+    static_assert(64 * WP * 4 <= 2 * 64 * kLP * 2, "fp32 W exceeds E^T[1]");
+    static_assert(G * D == NT && G * LPG == 64, "value partials");
 
     // ---- frame: every global read first
     float q0[WPT], q1[WPT], k0[WPT], k1[WPT];
 #pragma unroll
     for (int r = 0; r < WPT; ++r) {
-        const int e = tid + 256 * r, a = e / D2, c2 = e % D2;
+        const int e = tid + NT * r, a = e / D2, c2 = e % D2;
         const size_t o = ((size_t)h * m + (a < m ? a : 0)) * D + 2 * c2;
         q0[r] = qt[o]; q1[r] = qt[o + 1]; k0[r] = kt[o]; k1[r] = kt[o + 1];
     }
@@ -416,7 +429,7 @@ __global__ __launch_bounds__(256) void frame_ns_kernel(
     uint32_t* ktab = kfix + (size_t)h * 64 * D2;
 #pragma unroll
     for (int r = 0; r < WPT; ++r) {
-        const int e = tid + 256 * r, a = e / D2;
+        const int e = tid + NT * r, a = e / D2;
         const uint32_t uq = a < m ? fix2(q0[r], q1[r], inv2R) : 0u;
         const uint32_t uk = a < m ? fix2(k0[r], k1[r], inv2R) : 0u;
         qtab[e] = uq;
@@ -426,68 +439,84 @@ __global__ __launch_bounds__(256) void frame_ns_kernel(
     }
     __syncthreads();
 
-    // ---- W[a][b] = k(qt_a, kt_b) (+ eps on the diagonal): lane a, columns b = 16w..16w+15
+    // ---- W[a][b] = k(qt_a, kt_b) (+ eps on the diagonal): lane a, columns b = BPW w..+BPW
     uint32_t qa[D2];
 #pragma unroll
     for (int c4 = 0; c4 < D2 / 4; ++c4) {
         const uint4 x = reinterpret_cast<const uint4*>(sQ + l * D2)[c4];
         qa[4 * c4] = x.x; qa[4 * c4 + 1] = x.y; qa[4 * c4 + 2] = x.z; qa[4 * c4 + 3] = x.w;
     }
-    // the key-landmark rows b are read by the whole wave at one address (LDS broadcast)
-    float wv[16];
-#pragma unroll 4
-    for (int bb = 0; bb < 16; ++bb) {
-        const uint4* kr = reinterpret_cast<const uint4*>(sK + (16 * w + bb) * D2);
-        uint32_t u0 = 0x4B000000u, u1 = 0u;
+    // the key-landmark rows b are read by the whole wave at one address (LDS broadcast), two
+    // rows' reads in flight at a time (fully unrolled: wv stays in registers)
+    float wv[BPW];
+    const uint4* krow = reinterpret_cast<const uint4*>(sK + BPW * w * D2);
+#pragma unroll
+    for (int bb = 0; bb < BPW; bb += 2) {
+        uint4 t0[D2 / 4], t1[D2 / 4];
 #pragma unroll
         for (int c4 = 0; c4 < D2 / 4; ++c4) {
-            const uint4 t = kr[c4];
-            u0 = __builtin_amdgcn_sad_u16(qa[4 * c4 + 0], t.x, u0);
-            u1 = __builtin_amdgcn_sad_u16(qa[4 * c4 + 1], t.y, u1);
-            u0 = __builtin_amdgcn_sad_u16(qa[4 * c4 + 2], t.z, u0);
-            u1 = __builtin_amdgcn_sad_u16(qa[4 * c4 + 3], t.w, u1);
+            t0[c4] = krow[bb * (D2 / 4) + c4];
+            t1[c4] = krow[(bb + 1) * (D2 / 4) + c4];
+        }
+        uint32_t u0 = 0x4B000000u, u1 = 0u, v0 = 0x4B000000u, v1 = 0u;
+#pragma unroll
+        for (int c4 = 0; c4 < D2 / 4; ++c4) {
+            u0 = __builtin_amdgcn_sad_u16(qa[4 * c4 + 0], t0[c4].x, u0);
+            u1 = __builtin_amdgcn_sad_u16(qa[4 * c4 + 1], t0[c4].y, u1);
+            v0 = __builtin_amdgcn_sad_u16(qa[4 * c4 + 0], t1[c4].x, v0);
+            v1 = __builtin_amdgcn_sad_u16(qa[4 * c4 + 1], t1[c4].y, v1);
+            u0 = __builtin_amdgcn_sad_u16(qa[4 * c4 + 2], t0[c4].z, u0);
+            u1 = __builtin_amdgcn_sad_u16(qa[4 * c4 + 3], t0[c4].w, u1);
+            v0 = __builtin_amdgcn_sad_u16(qa[4 * c4 + 2], t1[c4].z, v0);
+            v1 = __builtin_amdgcn_sad_u16(qa[4 * c4 + 3], t1[c4].w, v1);
         }
         wv[bb] = __builtin_amdgcn_exp2f(fmaf(__uint_as_float(u0 + u1), esc, ebias));
+        wv[bb + 1] = __builtin_amdgcn_exp2f(fmaf(__uint_as_float(v0 + v1), esc, ebias));
     }
 #pragma unroll
-    for (int bb = 0; bb < 16; ++bb) {
-        const int b = 16 * w + bb;
+    for (int bb = 0; bb < BPW; ++bb) {
+        const int b = BPW * w + bb;
         if (l == b) wv[bb] += eps;
         wv[bb] = (l < m && b < m) ? wv[bb] : 0.f;
     }
     // row partial sums from registers, W (fp32) to LDS for the column partial sums
     float rsum = 0.f, wmax = 0.f;
 #pragma unroll
-    for (int bb = 0; bb < 16; ++bb) {
+    for (int bb = 0; bb < BPW; ++bb) {
         rsum += fabsf(wv[bb]);
         wmax = fmaxf(wmax, fabsf(wv[bb]));
     }
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-        *reinterpret_cast<float4*>(sWf + l * WP + 16 * w + 4 * q) =
+    for (int q = 0; q < BPW / 4; ++q)
+        *reinterpret_cast<float4*>(sWf + l * WP + BPW * w + 4 * q) =
             make_float4(wv[4 * q], wv[4 * q + 1], wv[4 * q + 2], wv[4 * q + 3]);
     wmax = wave_max_dpp(wmax);
     if (l == 0) sred[16 + w] = wmax;
     __syncthreads();
     {
-        float csum = 0.f;   // column l, rows 16w..16w+15
+        float csum = 0.f;   // column l, rows BPW w..+BPW
 #pragma unroll
-        for (int i = 0; i < 16; ++i) csum += fabsf(sWf[(16 * w + i) * WP + l]);
+        for (int i = 0; i < BPW; ++i) csum += fabsf(sWf[(BPW * w + i) * WP + l]);
         part[w * 64 + l] = csum;
-        part[256 + w * 64 + l] = rsum;   // row l, columns 16w..16w+15
+        part[NW * 64 + w * 64 + l] = rsum;   // row l, columns BPW w..+BPW
     }
     __syncthreads();
     if (w == 0) {
         // column and row sums in a fixed order, then the first maximising column / row
-        float n1 = ((part[l] + part[64 + l]) + part[128 + l]) + part[192 + l];
-        float ninf = ((part[256 + l] + part[320 + l]) + part[384 + l]) + part[448 + l];
+        float n1 = 0.f, ninf = 0.f, mx = 0.f;
+#pragma unroll
+        for (int g = 0; g < NW; ++g) {
+            n1 += part[g * 64 + l];
+            ninf += part[NW * 64 + g * 64 + l];
+            mx = fmaxf(mx, sred[16 + g]);
+        }
         int bs, as;
         wave_argmax_dpp(n1, bs);
         wave_argmax_dpp(ninf, as);
         if (l == 0) {
             const float c = n1 * ninf;
             sred[2] = c;
-            sred[3] = fmaxf(fmaxf(sred[16], sred[17]), fmaxf(sred[18], sred[19]));
+            sred[3] = mx;
             cinfo[h * 4 + 0] = c;
             cinfo[h * 4 + 1] = n1;
             cinfo[h * 4 + 2] = ninf;
@@ -497,75 +526,97 @@ __global__ __launch_bounds__(256) void frame_ns_kernel(
     __syncthreads();
     const float c = sred[2];
     const float inv_c = c > 0.f ? 1.f / c : 0.f;
-    float mx = sred[3] * inv_c;             // max |X0|
-    float xs = ldexpf(1.f, pow2_exp(mx));   // X_true = X_stored * xs
-    // X0^T = W / c (X0's transposed copy): sixteen consecutive b of row a
+    float mx = sred[3] * inv_c;             // max |X0| = max |Z_0|
+    float zs = ldexpf(1.f, pow2_exp(mx));   // Z_true = Z_stored * zs
+    // Z_0^T = X0^T = W / c: BPW consecutive b of row a
     {
-        const float x0s = inv_c / xs;
-        _Float16 xh[16], xl[16];
+        const float x0s = inv_c / zs;
+        uint32_t xh[BPW / 2], xl[BPW / 2];
 #pragma unroll
-        for (int bb = 0; bb < 16; ++bb) split_f16(wv[bb] * x0s, xh[bb], xl[bb]);
-        const int o = l * kLP + 16 * w;
+        for (int q = 0; q < BPW / 2; ++q) split_pk(wv[2 * q] * x0s, wv[2 * q + 1] * x0s, xh[q], xl[q]);
+        const int o = l * kLP + BPW * w;
 #pragma unroll
-        for (int q = 0; q < 2; ++q) {
-            *reinterpret_cast<h8_t*>(XTh[0] + o + 8 * q) = *reinterpret_cast<const h8_t*>(xh + 8 * q);
-            *reinterpret_cast<h8_t*>(XTl[0] + o + 8 * q) = *reinterpret_cast<const h8_t*>(xl + 8 * q);
+        for (int q = 0; q < BPW / 8; ++q) {
+            *reinterpret_cast<uint4*>(ZTh(0) + o + 8 * q) = make_uint4(xh[4 * q], xh[4 * q + 1], xh[4 * q + 2], xh[4 * q + 3]);
+            *reinterpret_cast<uint4*>(ZTl(0) + o + 8 * q) = make_uint4(xl[4 * q], xl[4 * q + 1], xl[4 * q + 2], xl[4 * q + 3]);
         }
         if (T == 0) {
 #pragma unroll
-            for (int bb = 0; bb < 16; ++bb) XT[(size_t)h * 4096 + (16 * w + bb) * 64 + l] = wv[bb] * inv_c;
-        }
-    }
-    const int rb = w >> 1, cb = w & 1;
-    // the wave's rows of W as MFMA A operands (rows 32 rb + l%32, k = 16 s4 + 8(l/32)..+8),
-    // taken from the fp32 copy
-    h8_t wah[4], wal[4];
-#pragma unroll
-    for (int s4 = 0; s4 < 4; ++s4) {
-        const float* src = sWf + (32 * rb + (l & 31)) * WP + 16 * s4 + 8 * (l >> 5);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            _Float16 a, b;
-            split_f16(src[i], a, b);
-            wah[s4][i] = a;
-            wal[s4][i] = b;
+            for (int bb = 0; bb < BPW; ++bb) XT[(size_t)h * 4096 + (BPW * w + bb) * 64 + l] = wv[bb] * inv_c;
         }
     }
     __syncthreads();
-    for (int t = 0; t < T; ++t) {
-        const int cur = t & 1;
-        // T1 = 2I - W X, stored transposed
-        f32x16_t p = mm32_split(wah, wal, XTh[cur], XTl[cur], cb);
+    if (T == 0) return;
+    // waves 0-3: the Z chain; waves 4-7: the E chain; block (rb, cb) = ((w & 3) / 2, w & 1)
+    const bool zchain = w < 4;
+    const int rb = (w & 3) >> 1, cb = w & 1;
+    f32x16_t zreg;   // Z chain: this wave's block of Z_k (true values, fp32)
+    if (zchain) {
+        // Z_0 = X0: X0[row][col] = W[col][row] / c
+#pragma unroll
+        for (int r = 0; r < 16; ++r) zreg[r] = sWf[(32 * cb + (l & 31)) * WP + 32 * rb + c_row(r, l)] * inv_c;
+    } else {
+        // E_0 = I - W X0 (A = W from the fp32 copy, B = X0 through Z^T[0])
+        h8_t wah[4], wal[4];
+#pragma unroll
+        for (int s4 = 0; s4 < 4; ++s4) {
+            const float* src = sWf + (32 * rb + (l & 31)) * WP + 16 * s4 + 8 * (l >> 5);
+            uint32_t hq[4], lq[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) split_pk(src[2 * q], src[2 * q + 1], hq[q], lq[q]);
+            wah[s4] = __builtin_bit_cast(h8_t, make_uint4(hq[0], hq[1], hq[2], hq[3]));
+            wal[s4] = __builtin_bit_cast(h8_t, make_uint4(lq[0], lq[1], lq[2], lq[3]));
+        }
+        f32x16_t e0 = mm32_split(wah, wal, ZTh(0), ZTl(0), cb);
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const int row = 32 * rb + c_row(r, l), col = 32 * cb + (l & 31);
-            p[r] = (row == col ? 2.f : 0.f) - p[r] * xs;
+            e0[r] = (row == col ? 1.f : 0.f) - e0[r] * zs;
         }
-        store32_t(p, 1.f, rb, cb, TTh, TTl);
-        __syncthreads();
-        // X_{t+1} = X T1
-        h8_t xah[4], xal[4];
+        store32_t(e0, 1.f, rb, cb, ETh(0), ETl(0));
+    }
+    __syncthreads();
+    for (int k = 0; k < T; ++k) {
+        const int cur = k & 1;
+        if (zchain) {
+            // Z_{k+1} = Z_k + Z_k E_k
+            h8_t zah[4], zal[4];
 #pragma unroll
-        for (int s4 = 0; s4 < 4; ++s4) {
-            xah[s4] = a_from_transposed(XTh[cur], rb, 16 * s4);
-            xal[s4] = a_from_transposed(XTl[cur], rb, 16 * s4);
+            for (int s4 = 0; s4 < 4; ++s4) {
+                zah[s4] = a_from_transposed(ZTh(cur), rb, 16 * s4);
+                zal[s4] = a_from_transposed(ZTl(cur), rb, 16 * s4);
+            }
+            const f32x16_t d = mm32_split(zah, zal, ETh(cur), ETl(cur), cb);
+#pragma unroll
+            for (int r = 0; r < 16; ++r) zreg[r] = fmaf(d[r], zs, zreg[r]);
+            if (k + 1 < T) {
+                // scale of Z_{k+1} from the maximum of Z_k (mx)
+                zs = ldexpf(1.f, (mx > 0.f && isfinite(mx)) ? ilogbf(mx) - 7 : 0);
+                store32_t(zreg, 1.f / zs, rb, cb, ZTh(cur ^ 1), ZTl(cur ^ 1));
+                float lm = 0.f;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) lm = fmaxf(lm, fabsf(zreg[r]));
+                lm = wave_max_dpp(lm);
+                if (l == 0) sred[32 + 4 * cur + w] = lm;
+            } else {
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    XT[(size_t)h * 4096 + (32 * rb + c_row(r, l)) * 64 + 32 * cb + (l & 31)] = zreg[r];
+            }
+        } else if (k + 1 < T) {
+            // E_{k+1} = E_k E_k
+            h8_t eah[4], eal[4];
+#pragma unroll
+            for (int s4 = 0; s4 < 4; ++s4) {
+                eah[s4] = a_from_transposed(ETh(cur), rb, 16 * s4);
+                eal[s4] = a_from_transposed(ETl(cur), rb, 16 * s4);
+            }
+            const f32x16_t e = mm32_split(eah, eal, ETh(cur), ETl(cur), cb);
+            store32_t(e, 1.f, rb, cb, ETh(cur ^ 1), ETl(cur ^ 1));
         }
-        f32x16_t xn = mm32_split(xah, xal, TTh, TTl, cb) * xs;
-        if (t + 1 < T) {
-            // scale of X_{t+1} from the maximum of X_t (mx)
-            xs = ldexpf(1.f, (mx > 0.f && isfinite(mx)) ? ilogbf(mx) - 7 : 0);
-            store32_t(xn, 1.f / xs, rb, cb, XTh[cur ^ 1], XTl[cur ^ 1]);
-            float lm = 0.f;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) lm = fmaxf(lm, fabsf(xn[r]));
-            lm = wave_max_dpp(lm);
-            if (l == 0) sred[32 + 4 * cur + w] = lm;
+        if (k + 1 < T) {
             __syncthreads();
             mx = fmaxf(fmaxf(sred[32 + 4 * cur], sred[33 + 4 * cur]), fmaxf(sred[34 + 4 * cur], sred[35 + 4 * cur]));
-        } else {
-#pragma unroll
-            for (int r = 0; r < 16; ++r)
-                XT[(size_t)h * 4096 + (32 * rb + c_row(r, l)) * 64 + 32 * cb + (l & 31)] = xn[r];
         }
     }
 }
@@ -920,26 +971,24 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
 #pragma unroll
         for (int c = 0; c < D2; ++c) qf[c] = 0u;
     }
-    // kernel values, two landmarks per fp16 pair register (landmarks >= m give 0)
+    // kernel values, two landmarks per fp16 pair register (landmarks >= m give 0); the
+    // landmark rows come through scalar registers, the loads of each row issued right after
+    // the first use of the previous one (the table has 64 rows, zero past m)
     uint32_t ah[32];
+    {
+        uint32_t ta[D2], tb[D2];
+        load_row<D2>(ta, tab);
 #pragma unroll
-    for (int p = 0; p < 32; ++p) {
-        uint32_t v = 0u;
-        if (2 * p < m) {
-            const uint32_t* t0 = tab + (2 * p) * D2;
-            const uint32_t* t1 = tab + (2 * p + 1) * D2;
-            uint32_t u0 = 0x4B000000u, u1 = 0x4B000000u;
-#pragma unroll
-            for (int c = 0; c < D2; ++c) {
-                u0 = __builtin_amdgcn_sad_u16(qf[c], t0[c], u0);
-                u1 = __builtin_amdgcn_sad_u16(qf[c], t1[c], u1);
+        for (int p = 0; p < 32; ++p) {
+            if (2 * p < m) {
+                const float a0 = lap_row<D2>(qf, ta, tb, tab + (2 * p + 1) * D2, esc, ebias);
+                float a1 = lap_row<D2>(qf, tb, ta, tab + (p < 31 ? 2 * p + 2 : 63) * D2, esc, ebias);
+                if (2 * p + 1 >= m) a1 = 0.f;
+                ah[p] = pk_f16(a0, a1);
+            } else {
+                ah[p] = 0u;
             }
-            const float a0 = __builtin_amdgcn_exp2f(fmaf(__uint_as_float(u0), esc, ebias));
-            float a1 = __builtin_amdgcn_exp2f(fmaf(__uint_as_float(u1), esc, ebias));
-            if (2 * p + 1 >= m) a1 = 0.f;
-            v = pk_f16(a0, a1);
         }
-        ah[p] = v;
     }
     // lower half keeps ah[8s+t] (queries 0..31, landmarks 16s..16s+7) and receives queries
     // 32..63 / landmarks 16s..16s+7; the upper half receives queries 0..31 / 16s+8..16s+15
@@ -1037,10 +1086,10 @@ hipError_t launch_fast_frame_ns(const float* qt, const float* kt, const double* 
                                 float* XT, float* cinfo, int BH, int n, int d, int m, float lambda, int T, float eps,
                                 hipStream_t st) {
     if (d == 32)
-        hipLaunchKernelGGL(frame_ns_kernel<32>, dim3(BH), dim3(256), 0, st, qt, kt, vseg, segmax, vsegmax, frame,
+        hipLaunchKernelGGL(frame_ns_kernel<32>, dim3(BH), dim3(kSolveThreads), 0, st, qt, kt, vseg, segmax, vsegmax, frame,
                            qfix, kfix, vbar, XT, cinfo, n, m, lambda, T, eps);
     else
-        hipLaunchKernelGGL(frame_ns_kernel<64>, dim3(BH), dim3(256), 0, st, qt, kt, vseg, segmax, vsegmax, frame,
+        hipLaunchKernelGGL(frame_ns_kernel<64>, dim3(BH), dim3(kSolveThreads), 0, st, qt, kt, vseg, segmax, vsegmax, frame,
                            qfix, kfix, vbar, XT, cinfo, n, m, lambda, T, eps);
     return hipGetLastError();
 }

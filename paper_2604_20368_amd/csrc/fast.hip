@@ -104,7 +104,10 @@ __device__ __forceinline__ int xcd_rank(int i, int n, int base) {
 
 // ------------------------------------------------------------------------------------------
 // Landmark means and per-segment statistics.  grid (m, BH), 256 threads.  Thread t always
-// reads the 8-column group t % (D/8) of its rows; partial sums are combined in a fixed order.
+// reads the 8-column group t % (D/8) of its rows (rows t / (D/8) + (256 / (D/8)) i), all of a
+// segment's rows in flight four per thread at a time.  Sums: per thread in fp32, then over the
+// lanes of a wave that share a column group (a butterfly), then over the four waves in a fixed
+// order in fp64.
 template <int D>
 __global__ __launch_bounds__(256) void pool2_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
                                                     const uint16_t* __restrict__ V, float* __restrict__ qt,
@@ -113,7 +116,8 @@ __global__ __launch_bounds__(256) void pool2_kernel(const uint16_t* __restrict__
                                                     int m) {
     constexpr int CPR = D / 8;      // 16-byte chunks per row
     constexpr int RPI = 256 / CPR;  // rows per block iteration
-    const int l = blockIdx.x, h = blockIdx.y, tid = threadIdx.x;
+    constexpr int UNR = 4;          // row iterations in flight
+    const int l = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
     const int s0 = seg_start(l, n, m), s1 = seg_start(l + 1, n, m);
     const int cg = tid % CPR, r0 = tid / CPR;
     float sq[8], sk[8], sv[8];
@@ -121,62 +125,86 @@ __global__ __launch_bounds__(256) void pool2_kernel(const uint16_t* __restrict__
     for (int j = 0; j < 8; ++j) sq[j] = sk[j] = sv[j] = 0.f;
     float mx = 0.f, vmx = 0.f;
     const size_t base = (size_t)h * n * D + cg * 8;
-#pragma unroll 4
-    for (int i = s0 + r0; i < s1; i += RPI) {
-        const size_t off = base + (size_t)i * D;
-        const uint4 a = *reinterpret_cast<const uint4*>(Q + off);
-        const uint4 b = *reinterpret_cast<const uint4*>(K + off);
-        const uint4 c = *reinterpret_cast<const uint4*>(V + off);
-        const uint32_t aw[4] = {a.x, a.y, a.z, a.w}, bw[4] = {b.x, b.y, b.z, b.w}, cw[4] = {c.x, c.y, c.z, c.w};
+    for (int i0 = s0 + r0; i0 < s1; i0 += UNR * RPI) {
+        uint4 a[UNR], b[UNR], c[UNR];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const float q0 = bf16_lo(aw[j]), q1 = bf16_hi(aw[j]);
-            const float k0 = bf16_lo(bw[j]), k1 = bf16_hi(bw[j]);
-            const float v0 = bf16_lo(cw[j]), v1 = bf16_hi(cw[j]);
-            sq[2 * j] += q0; sq[2 * j + 1] += q1;
-            sk[2 * j] += k0; sk[2 * j + 1] += k1;
-            sv[2 * j] += v0; sv[2 * j + 1] += v1;
-            mx = fmaxf(fmaxf(mx, fabsf(q0)), fmaxf(fabsf(q1), fmaxf(fabsf(k0), fabsf(k1))));
-            vmx = fmaxf(vmx, fmaxf(fabsf(v0), fabsf(v1)));
+        for (int u = 0; u < UNR; ++u) {
+            const int i = i0 + u * RPI;
+            if (i < s1) {
+                const size_t off = base + (size_t)i * D;
+                a[u] = *reinterpret_cast<const uint4*>(Q + off);
+                b[u] = *reinterpret_cast<const uint4*>(K + off);
+                c[u] = *reinterpret_cast<const uint4*>(V + off);
+            } else {
+                a[u] = b[u] = c[u] = make_uint4(0u, 0u, 0u, 0u);   // +0: no effect on sums or maxima
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
+            const uint32_t aw[4] = {a[u].x, a[u].y, a[u].z, a[u].w}, bw[4] = {b[u].x, b[u].y, b[u].z, b[u].w},
+                           cw[4] = {c[u].x, c[u].y, c[u].z, c[u].w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const float q0 = bf16_lo(aw[j]), q1 = bf16_hi(aw[j]);
+                const float k0 = bf16_lo(bw[j]), k1 = bf16_hi(bw[j]);
+                const float v0 = bf16_lo(cw[j]), v1 = bf16_hi(cw[j]);
+                sq[2 * j] += q0; sq[2 * j + 1] += q1;
+                sk[2 * j] += k0; sk[2 * j + 1] += k1;
+                sv[2 * j] += v0; sv[2 * j + 1] += v1;
+                mx = fmaxf(fmaxf(mx, fabsf(q0)), fmaxf(fabsf(q1), fmaxf(fabsf(k0), fabsf(k1))));
+                vmx = fmaxf(vmx, fmaxf(fabsf(v0), fabsf(v1)));
+            }
         }
     }
-    // A non-finite input makes its column sum non-finite (fmaxf alone would hide a NaN).
-    __shared__ double red[256 * 8];
-    __shared__ float smx[4], svmx[4];
+    // Within a wave, the lanes with one column group are lane % CPR == cg.  Reduce over the
+    // other lane bits by a butterfly; lane cg's result (always the same order) is the one kept.
+    float* sums[3] = {sq, sk, sv};
+#pragma unroll
+    for (int a3 = 0; a3 < 3; ++a3)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            float v = sums[a3][j];
+            if (CPR <= 4) v += __shfl_xor(v, 4, 64);
+            v += __shfl_xor(v, 8, 64);
+            v += __shfl_xor(v, 16, 64);
+            v += __shfl_xor(v, 32, 64);
+            sums[a3][j] = v;
+        }
     mx = wave_max(mx);
     vmx = wave_max(vmx);
-    if ((tid & 63) == 0) {
-        smx[tid >> 6] = mx;
-        svmx[tid >> 6] = vmx;
+    __shared__ double red[3][4][D];
+    __shared__ float smx[4], svmx[4];
+    if (lane < CPR) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            red[0][w][lane * 8 + j] = (double)sq[j];
+            red[1][w][lane * 8 + j] = (double)sk[j];
+            red[2][w][lane * 8 + j] = (double)sv[j];
+        }
     }
+    if (lane == 0) {
+        smx[w] = mx;
+        svmx[w] = vmx;
+    }
+    __syncthreads();
     const double cnt = (double)(s1 - s0);
     bool bad = false;
-    for (int pass = 0; pass < 3; ++pass) {
-        const float* src = pass == 0 ? sq : (pass == 1 ? sk : sv);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) red[tid * 8 + j] = (double)src[j];
-        __syncthreads();
-        if (tid < D) {
-            const int g = tid / 8, j = tid % 8;
-            double t = 0.0;
-#pragma unroll
-            for (int r = 0; r < RPI; ++r) t += red[(g + CPR * r) * 8 + j];
-            const size_t o = ((size_t)h * m + l) * D + tid;
-            if (pass == 0) qt[o] = (float)(t / cnt);
-            else if (pass == 1) kt[o] = (float)(t / cnt);
-            else vseg[o] = t;
-            bad |= !isfinite(t);
-        }
-        __syncthreads();
+    if (tid < 3 * D) {
+        const int a3 = tid / D, col = tid % D;
+        const double t = ((red[a3][0][col] + red[a3][1][col]) + red[a3][2][col]) + red[a3][3][col];
+        const size_t o = ((size_t)h * m + l) * D + col;
+        if (a3 == 0) qt[o] = (float)(t / cnt);
+        else if (a3 == 1) kt[o] = (float)(t / cnt);
+        else vseg[o] = t;
+        bad = !isfinite(t);
     }
-    if (tid < 64) {   // D <= 64: every column flag lives in wave 0
-        const bool anybad = __any(bad);
-        if (tid == 0) {
-            const float a = fmaxf(fmaxf(smx[0], smx[1]), fmaxf(smx[2], smx[3]));
-            const float b = fmaxf(fmaxf(svmx[0], svmx[1]), fmaxf(svmx[2], svmx[3]));
-            segmax[(size_t)h * m + l] = anybad ? __builtin_nanf("") : a;
-            vsegmax[(size_t)h * m + l] = anybad ? __builtin_nanf("") : b;
-        }
+    // A non-finite input makes its column sum non-finite (fmaxf alone would hide a NaN).
+    const bool anybad = __syncthreads_or(bad);
+    if (tid == 0) {
+        const float a = fmaxf(fmaxf(smx[0], smx[1]), fmaxf(smx[2], smx[3]));
+        const float b = fmaxf(fmaxf(svmx[0], svmx[1]), fmaxf(svmx[2], svmx[3]));
+        segmax[(size_t)h * m + l] = anybad ? __builtin_nanf("") : a;
+        vsegmax[(size_t)h * m + l] = anybad ? __builtin_nanf("") : b;
     }
 }
 
@@ -822,19 +850,19 @@ __global__ __launch_bounds__(256, 2) void key_kernel(const uint16_t* __restrict_
 }
 
 // ------------------------------------------------------------------------------------------
-// U = sum over key chunks, M = X_T U, and the MFMA operand tiles of M for the query side, by
-// column groups: grid (NG, BH) with NG = D/8 + 1, 512 threads.  Group g < D/8 holds value
-// columns 8g..8g+7, group D/8 the ones column D.  M = X_T U is separable by columns, so each
-// block sums only its columns of the chunk partials (Upart[h][kb][c][a], four quarters of the
-// chunks combined in a fixed order) and forms only its columns of M.
-// Tiles: Mt[h][s][cb][part][lane][i] = part of M[16s + 8(lane/32) + i][column of (cb, lane%32)]
-// times 2^-e_g, part 0 = fp16 value, part 1 = fp16 residual; column (cb, j) is 32cb + j for
-// cb < D/32 and, for cb = D/32, the ones column D when j = 0 (else zero).  mscale[h][g] = 2^e_g
-// puts the largest magnitude of the group's columns in [2^14, 2^15).
+// U = sum over key chunks, M = X_T U, and the query side's copy of M, by column groups:
+// grid (NG, BH) with NG = D/8 + 1, 512 threads.  Group g < D/8 holds value columns 8g..8g+7,
+// group D/8 the ones column D.  M = X_T U is separable by columns, so each block sums only its
+// columns of the chunk partials (Upart[h][kb][c][a], four quarters of the chunks combined in a
+// fixed order) and forms only its columns of M.
+// Value columns: fp16 MFMA operand tiles Mt[h][s][cb][lane][i] = M[16s + 8(lane/32) + i]
+// [32cb + lane%32] * 2^-e_g with mscale[h][g] = 2^e_g putting the group's largest magnitude in
+// [2^14, 2^15).  Ones column: Mones[h][a] = M[a][D] in fp32.
 template <int D>
 __global__ __launch_bounds__(512) void mfinal_kernel(const float* __restrict__ Upart, const float* __restrict__ XT,
                                                      _Float16* __restrict__ Mt, float* __restrict__ mscale,
-                                                     float* __restrict__ Mout, int m, int nkb) {
+                                                     float* __restrict__ Mones, float* __restrict__ Mout, int m,
+                                                     int nkb) {
     constexpr int D1 = D + 1;
     constexpr int CB = D / 32;
     constexpr int NG = D / 8 + 1;
@@ -891,28 +919,18 @@ __global__ __launch_bounds__(512) void mfinal_kernel(const float* __restrict__ U
     for (int i = 1; i < 8; ++i) mxg = fmaxf(mxg, smx[i]);
     const int e = pow2_exp(mxg);
     if (tid == 0) mscale[h * NG + g] = ldexpf(1.f, e);
-    // operand tiles: one 16-byte chunk (i = 0..7) per (column, s, lane half, part); the ones
-    // group also writes the zero columns j != 0 of its tile
-    const int chunks = ones ? 64 * 4 * 2 : nc * 4 * 2 * 2;
-    for (int q = tid; q < chunks; q += 512) {
-        int lane, s4, part, cc;
-        if (ones) {
-            lane = q & 63; s4 = (q >> 6) & 3; part = q >> 8; cc = 0;
-        } else {
-            cc = q & 7; const int hl = (q >> 3) & 1; s4 = (q >> 4) & 3; part = q >> 6;
-            lane = ((c0 + cc) & 31) + 32 * hl;
-        }
-        const int cb = ones ? CB : (c0 + cc) >> 5;
-        const bool live = !ones || (lane & 31) == 0;
+    if (ones) {
+        if (tid < 64) Mones[(size_t)h * 64 + tid] = sM[tid];   // rows >= m are zero
+        return;
+    }
+    // operand tiles: one 16-byte chunk (i = 0..7) per (column, s, lane half)
+    if (tid < nc * 4 * 2) {
+        const int cc = tid & 7, hl = (tid >> 3) & 1, s4 = tid >> 4;
+        const int lane = ((c0 + cc) & 31) + 32 * hl, cb = (c0 + cc) >> 5;
         _Float16 v8[8];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int row = 16 * s4 + 8 * (lane >> 5) + i;
-            const float v = live ? ldexpf(sM[cc * 64 + row], -e) : 0.f;
-            const _Float16 hi = (_Float16)v;
-            v8[i] = part == 0 ? hi : (_Float16)(v - (float)hi);
-        }
-        const size_t o = ((((size_t)h * 4 + s4) * (CB + 1) + cb) * 2 + part) * 512 + lane * 8;
+        for (int i = 0; i < 8; ++i) v8[i] = (_Float16)ldexpf(sM[cc * 64 + 16 * s4 + 8 * hl + i], -e);
+        const size_t o = (((size_t)h * 4 + s4) * CB + cb) * 512 + lane * 8;
         *reinterpret_cast<uint4*>(Mt + o) = *reinterpret_cast<const uint4*>(v8);
     }
 }
@@ -921,28 +939,33 @@ __global__ __launch_bounds__(512) void mfinal_kernel(const float* __restrict__ U
 // Query side.  grid (ceil(n/256) * BH) (XCD-aware order), 256 threads, lane = query.  Per wave: u(q_i) in
 // registers, the m kernel values a_il from v_sad_u16 against the landmark-key table
 // (wave-uniform, scalar loads) packed as fp16 pairs, a permlane32 swap that turns "query per
-// lane" into the 32x32x16 operand layout for both 32-query halves, then Y^T = (M_hi + M_lo)^T A^T
-// on fp16 MFMA: the result holds, per lane, 16 output columns of one query, so the
-// normalisation and the bf16 stores happen straight from registers.
+// lane" into the 32x32x16 operand layout for both 32-query halves, then Y^T = M^T A^T on fp16
+// MFMA (M's value columns as fp16 with a power-of-two scale per column group): the result
+// holds, per lane, 16 output columns of one query, so the normalisation and the bf16 stores
+// happen straight from registers.  The row sum s_i = sum_l a_il M[l][d] (the ones column) is
+// accumulated in fp32 in the landmark loop from the unrounded kernel values.
 template <int D, int NORM>
 __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict__ Q, uint16_t* __restrict__ Out,
                                                      const uint32_t* __restrict__ kfix,
                                                      const float* __restrict__ frame, const _Float16* __restrict__ Mt,
-                                                     const float* __restrict__ mscale, const float* __restrict__ vbar,
+                                                     const float* __restrict__ mscale,
+                                                     const float* __restrict__ Mones, const float* __restrict__ vbar,
                                                      int n, int m, int nqb, int BH) {
     constexpr int D2 = D / 2;
     constexpr int D8 = D / 8;
     constexpr int CB = D / 32;
-    __shared__ __attribute__((aligned(16))) _Float16 sM[4 * (CB + 1) * 2 * 512];
+    __shared__ __attribute__((aligned(16))) _Float16 sM[4 * CB * 512];
     __shared__ __attribute__((aligned(16))) float sVb[D];
+    __shared__ __attribute__((aligned(16))) float sMo[64];
     const int lin = xcd_rank(blockIdx.x, nqb * BH, 0);
     const int h = lin / nqb, qblk = lin % nqb;
     const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
     {
-        const uint4* src = reinterpret_cast<const uint4*>(Mt + (size_t)h * 4 * (CB + 1) * 2 * 512);
+        const uint4* src = reinterpret_cast<const uint4*>(Mt + (size_t)h * 4 * CB * 512);
         uint4* dst = reinterpret_cast<uint4*>(sM);
-        for (int e = tid; e < 4 * (CB + 1) * 2 * 64; e += 256) dst[e] = src[e];
+        for (int e = tid; e < 4 * CB * 64; e += 256) dst[e] = src[e];
         if (tid < D) sVb[tid] = vbar[(size_t)h * D + tid];
+        if (tid < 64) sMo[tid] = Mones[(size_t)h * 64 + tid];
     }
     const float R = frame[h * 4 + 0], inv2R = frame[h * 4 + 1], esc = frame[h * 4 + 2];
     const float ebias = -kTwo23 * esc;
@@ -950,7 +973,7 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
     float scv[D / 8];
 #pragma unroll
     for (int g = 0; g < D / 8; ++g) scv[g] = mscale[h * NG + g];
-    const float sc1 = mscale[h * NG + D / 8];
+
     const uint32_t* tab = kfix + (size_t)h * 64 * D2;
     const int i0 = qblk * 256 + w * 64;
     const int i = i0 + l;
@@ -975,6 +998,8 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
     // landmark rows come through scalar registers, the loads of each row issued right after
     // the first use of the previous one (the table has 64 rows, zero past m)
     uint32_t ah[32];
+    float srow = 0.f;   // s_i of this lane's query
+    __syncthreads();    // sM, sMo, sVb
     {
         uint32_t ta[D2], tb[D2];
         load_row<D2>(ta, tab);
@@ -984,6 +1009,8 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
                 const float a0 = lap_row<D2>(qf, ta, tb, tab + (2 * p + 1) * D2, esc, ebias);
                 float a1 = lap_row<D2>(qf, tb, ta, tab + (p < 31 ? 2 * p + 2 : 63) * D2, esc, ebias);
                 if (2 * p + 1 >= m) a1 = 0.f;
+                const float2 mo = *reinterpret_cast<const float2*>(&sMo[2 * p]);
+                srow = fmaf(a1, mo.y, fmaf(a0, mo.x, srow));
                 ah[p] = pk_f16(a0, a1);
             } else {
                 ah[p] = 0u;
@@ -1001,8 +1028,9 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
             ah[8 * s4 + t] = r[0];
             ah[8 * s4 + 4 + t] = r[1];
         }
-    __syncthreads();   // sM, sVb
     const int NSTEP = (m + 15) / 16;
+    // s_i for the two 32-query halves in the output layout (lane l: query 32 qb + l%32)
+    const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(srow), __float_as_uint(srow), false, false);
     const bool nan_head = !isfinite(R);
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
@@ -1011,20 +1039,7 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
         for (int s4 = 0; s4 < 4; ++s4)
             A[s4] = __builtin_bit_cast(h8_t, (uint4){ah[8 * s4 + 4 * qb], ah[8 * s4 + 4 * qb + 1],
                                                      ah[8 * s4 + 4 * qb + 2], ah[8 * s4 + 4 * qb + 3]});
-        // ones column: s_i of query 32qb + l%32 lands in register 0 of lane l%32
-        f32x16_t acc = {};
-#pragma unroll
-        for (int s4 = 0; s4 < 4; ++s4) {
-            if (s4 < NSTEP) {
-                const _Float16* bt = sM + ((s4 * (CB + 1) + CB) * 2) * 512 + l * 8;
-                acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(*reinterpret_cast<const h8_t*>(bt), A[s4], acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(*reinterpret_cast<const h8_t*>(bt + 512), A[s4], acc, 0,
-                                                             0, 0);
-            }
-        }
-        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[0]), __float_as_uint(acc[0]), false,
-                                                         false);
-        const float si = __uint_as_float(sw[0]) * sc1;
+        const float si = __uint_as_float(sw[qb]);
         float tmul, tadd;   // o = y * tmul * scv[group] + tadd * vbar
         if (NORM == NORM_INLINE) { tmul = 1.f; tadd = 1.f - si; }
         else if (NORM == NORM_ROWSUM) { tmul = 1.f / si; tadd = 0.f; }
@@ -1037,10 +1052,8 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
 #pragma unroll
             for (int s4 = 0; s4 < 4; ++s4) {
                 if (s4 < NSTEP) {
-                    const _Float16* bt = sM + ((s4 * (CB + 1) + cb) * 2) * 512 + l * 8;
+                    const _Float16* bt = sM + (s4 * CB + cb) * 512 + l * 8;
                     y = __builtin_amdgcn_mfma_f32_32x32x16_f16(*reinterpret_cast<const h8_t*>(bt), A[s4], y, 0, 0, 0);
-                    y = __builtin_amdgcn_mfma_f32_32x32x16_f16(*reinterpret_cast<const h8_t*>(bt + 512), A[s4], y, 0, 0,
-                                                               0);
                 }
             }
 #pragma unroll
@@ -1106,23 +1119,25 @@ hipError_t launch_fast_key(const void* K, const void* V, const uint32_t* qfix, c
     return hipGetLastError();
 }
 
-hipError_t launch_fast_mfinal(const float* Upart, const float* XT, _Float16* Mt, float* mscale, float* M, int BH,
-                              int d, int m, int nkb, hipStream_t st) {
+hipError_t launch_fast_mfinal(const float* Upart, const float* XT, _Float16* Mt, float* mscale, float* Mones,
+                              float* M, int BH, int d, int m, int nkb, hipStream_t st) {
     if (d == 32)
-        hipLaunchKernelGGL(mfinal_kernel<32>, dim3(32 / 8 + 1, BH), dim3(512), 0, st, Upart, XT, Mt, mscale, M, m, nkb);
+        hipLaunchKernelGGL(mfinal_kernel<32>, dim3(32 / 8 + 1, BH), dim3(512), 0, st, Upart, XT, Mt, mscale, Mones, M, m,
+                           nkb);
     else
-        hipLaunchKernelGGL(mfinal_kernel<64>, dim3(64 / 8 + 1, BH), dim3(512), 0, st, Upart, XT, Mt, mscale, M, m, nkb);
+        hipLaunchKernelGGL(mfinal_kernel<64>, dim3(64 / 8 + 1, BH), dim3(512), 0, st, Upart, XT, Mt, mscale, Mones, M, m,
+                           nkb);
     return hipGetLastError();
 }
 
 hipError_t launch_fast_query(int norm, const void* Q, void* Out, const uint32_t* kfix, const float* frame,
-                             const _Float16* Mt, const float* mscale, const float* vbar, int BH, int n, int d, int m,
-                             hipStream_t st) {
+                             const _Float16* Mt, const float* mscale, const float* Mones, const float* vbar, int BH,
+                             int n, int d, int m, hipStream_t st) {
     const int nqb = (n + 255) / 256;
     dim3 grid(nqb * BH);
 #define LAPATTN_Q2(Dv, Nv)                                                                                        \
     hipLaunchKernelGGL((query2_kernel<Dv, Nv>), grid, dim3(256), 0, st, (const uint16_t*)Q, (uint16_t*)Out, kfix, \
-                       frame, Mt, mscale, vbar, n, m, nqb, BH)
+                       frame, Mt, mscale, Mones, vbar, n, m, nqb, BH)
     if (d == 32) {
         if (norm == NORM_INLINE) LAPATTN_Q2(32, NORM_INLINE);
         else if (norm == NORM_ROWSUM) LAPATTN_Q2(32, NORM_ROWSUM);

@@ -47,7 +47,7 @@ int check_align(std::initializer_list<const void*> tensors, const void* workspac
 // ------------------------------------------------------------------------------- workspace plan
 
 struct FastPlan {
-    size_t qt, kt, vseg, segmax, vsegmax, frame, qfix, kfix, vbar, XT, cinfo, Upart, Mt, mscale, U, M;
+    size_t qt, kt, vseg, segmax, vsegmax, frame, qfix, kfix, vbar, XT, cinfo, Upart, Mt, mscale, Mones, M;
     size_t total;
     int kpb, nkb;
 };
@@ -116,7 +116,6 @@ FastPlan make_fast_plan(int BH, int n, int d, int m) {
     p.kpb = (int)(256 * per_wave);
     p.nkb = (n + p.kpb - 1) / p.kpb;
     const size_t bh = (size_t)BH, d1 = (size_t)d + 1, f = sizeof(float), g = sizeof(double);
-    const size_t cbp = (size_t)d / 32 + 1;
     Carver c;
     p.qt = c.take(bh * m * d * f);
     p.kt = c.take(bh * m * d * f);
@@ -130,9 +129,9 @@ FastPlan make_fast_plan(int BH, int n, int d, int m) {
     p.XT = c.take(bh * 64 * 64 * f);
     p.cinfo = c.take(bh * 4 * f);
     p.Upart = c.take(bh * p.nkb * d1 * 64 * f);   // [h][kb][c][a], 64 rows a
-    p.Mt = c.take(bh * 4 * cbp * 2 * 512 * 2);
+    p.Mt = c.take(bh * 4 * ((size_t)d / 32) * 512 * 2);
     p.mscale = c.take(bh * ((size_t)d / 8 + 1) * f);
-    p.U = c.take(bh * m * d1 * f);
+    p.Mones = c.take(bh * 64 * f);
     p.M = c.take(bh * m * d1 * f);
     p.total = (c.off + 255) & ~size_t(255);
     return p;
@@ -249,13 +248,14 @@ hipError_t forward_fast(Recorder& rec, const FastPlan& p, const void* Q, const v
     if (e != hipSuccess) return e;
     e = run_named(rec, "m_final", [&] {
         return lapattn::launch_fast_mfinal(at<float>(ws, p.Upart), at<float>(ws, p.XT), at<_Float16>(ws, p.Mt),
-                                           at<float>(ws, p.mscale), at<float>(ws, p.M), BH, d, m, p.nkb, st);
+                                           at<float>(ws, p.mscale), at<float>(ws, p.Mones), at<float>(ws, p.M), BH, d, m,
+                                           p.nkb, st);
     });
     if (e != hipSuccess) return e;
     e = run_named(rec, "query", [&] {
         return lapattn::launch_fast_query(norm, Q, Out, at<uint32_t>(ws, p.kfix), at<float>(ws, p.frame),
-                                          at<_Float16>(ws, p.Mt), at<float>(ws, p.mscale), at<float>(ws, p.vbar), BH,
-                                          n, d, m, st);
+                                          at<_Float16>(ws, p.Mt), at<float>(ws, p.mscale), at<float>(ws, p.Mones),
+                                          at<float>(ws, p.vbar), BH, n, d, m, st);
     });
     return e;
 }

@@ -83,10 +83,10 @@ hipError_t launch_fast_frame_ns(const float* qt, const float* kt, const double* 
                                 hipStream_t st);
 hipError_t launch_fast_key(const void* K, const void* V, const uint32_t* qfix, const float* frame, float* Upart,
                            int BH, int n, int d, int m, int kpb, int nkb, hipStream_t st);
-hipError_t launch_fast_mfinal(const float* Upart, const float* XT, _Float16* Mt, float* mscale, float* M, int BH,
-                              int d, int m, int nkb, hipStream_t st);
+hipError_t launch_fast_mfinal(const float* Upart, const float* XT, _Float16* Mt, float* mscale, float* Mones,
+                              float* M, int BH, int d, int m, int nkb, hipStream_t st);
 hipError_t launch_fast_query(int norm, const void* Q, void* Out, const uint32_t* kfix, const float* frame,
-                             const _Float16* Mt, const float* mscale, const float* vbar, int BH, int n, int d, int m,
-                             hipStream_t st);
+                             const _Float16* Mt, const float* mscale, const float* Mones, const float* vbar, int BH,
+                             int n, int d, int m, hipStream_t st);
 
 }  // namespace lapattn

@@ -650,12 +650,13 @@ __global__ __launch_bounds__(kSolveThreads) void frame_ns_kernel(
 }
 
 // ------------------------------------------------------------------------------------------
-// Key-summary role: block kb of head h covers keys [kb*kpb, min(n, (kb+1)*kpb)); each wave
-// takes 64-key tiles (lane = key) on its own, with its own LDS region (no block barrier in the
-// loop).  Per tile: u(k_j) in registers, the value row to fp16 in LDS transposed ([c][j]), the
-// m kernel values exp(-||qt_a - k_j||_1/lambda) from v_sad_u16 against the landmark table
-// into LDS as [a][j], then U[a][c] += sum_j B[a][j] V[j][c] (and the ones column) on fp16
-// MFMA 32x32x16.  The raw rows of the next tile are loaded while the current one is computed.
+// Key-summary role: block kb of head h covers keys [kb*kpb, min(n, (kb+1)*kpb)) in steps of
+// 256 keys, one 64-key tile per wave (lane = key).  Per step, each wave: u(k_j) in registers,
+// the m kernel values exp(-||qt_a - k_j||_1/lambda) from v_sad_u16 against the landmark table
+// into its LDS tile as [a][j], its value rows to fp16, transposed, into LDS as [c][j]; then,
+// after a block barrier, U[a][c] += sum_j B[a][j] V[j][c] over the block's 256 keys on fp16
+// MFMA 16x16x32, wave w forming the rows a in [16w, 16w + 16) for every value column and the
+// ones column.  The raw rows of the next step are loaded while the current one is computed.
 //
 // The landmark rows are wave-uniform and come through scalar registers, one row per step in
 // two alternating buffers: the scalar loads of row a+1 are issued right after the first use
@@ -665,38 +666,34 @@ __global__ __launch_bounds__(kSolveThreads) void frame_ns_kernel(
 // one row in flight.
 constexpr int kKeyTileLds = 4 * 2 * 64 * kLP * 2;   // four waves' [a][j] and [c][j] fp16 tiles
 
-__device__ __forceinline__ void wave_lds_sync() {
-    // LDS requests of one wave complete in order; this only keeps the compiler from moving
-    // the reads of other lanes' writes above the writes.
-    __builtin_amdgcn_s_waitcnt(0xc07f);
-    __builtin_amdgcn_wave_barrier();
-}
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
+// Writes Upart[h][kb][c][a] (a < 64, rows >= m zero).
 template <int D>
 __device__ void key_role(int h, int kb, char* lds_raw, const uint16_t* __restrict__ K,
                          const uint16_t* __restrict__ V, const uint32_t* __restrict__ qfix,
                          const float* __restrict__ frame, float* __restrict__ Upart, int n, int m, int kpb, int nkb) {
     constexpr int D2 = D / 2;
     constexpr int D8 = D / 8;
-    constexpr int CB = D / 32;
+    constexpr int C16 = D / 16;   // value column blocks of the 16 x 16 products
     const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
-    _Float16* sB = reinterpret_cast<_Float16*>(lds_raw) + w * (2 * 64 * kLP);
-    _Float16* sV = sB + 64 * kLP;
+    _Float16* const tiles = reinterpret_cast<_Float16*>(lds_raw);
+    _Float16* sB = tiles + w * (2 * 64 * kLP);   // this wave's [a][j]
+    _Float16* sV = sB + 64 * kLP;                 // this wave's [c][j]
     const float inv2R = frame[h * 4 + 1], esc = frame[h * 4 + 2], vsc = frame[h * 4 + 3];
-    const float ebias = -kTwo23 * esc;
     const uint32_t* tab = qfix + (size_t)h * 64 * D2;
+    const float ebias = -kTwo23 * esc;
     const int j_begin = kb * kpb, j_end = min(n, j_begin + kpb);
     const int ntiles = (j_end - j_begin + 63) / 64;
-    const int RB = m > 32 ? 2 : 1;
+    const int nsteps = (ntiles + 3) / 4;
     const int mp = (m + 1) & ~1;   // landmark rows written per tile (an odd m writes one zero row)
-    f32x16_t acc[2][CB + 1];
+    const bool rows_live = 16 * w < m;   // this wave's rows of U are not all zero
+    f32x4_t acc[C16 + 1];
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb)
+    for (int cc = 0; cc <= C16; ++cc) acc[cc] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+    h8_t ones;   // B operand of the ones column: 1 in column 0
 #pragma unroll
-        for (int cb = 0; cb <= CB; ++cb) acc[rb][cb] = (f32x16_t){};
-    h8_t ones;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) ones[i] = (l & 31) == 0 ? (_Float16)1.f : (_Float16)0.f;
+    for (int i = 0; i < 8; ++i) ones[i] = (l & 15) == 0 ? (_Float16)1.f : (_Float16)0.f;
     for (int a = mp; a < 64; ++a) sB[a * kLP + l] = (_Float16)0.f;   // rows a >= m stay zero
 
     // rows of keys past the end keep stale values: their kernel values and value pairs are
@@ -725,111 +722,102 @@ __device__ void key_role(int h, int kb, char* lds_raw, const uint16_t* __restric
     // when, not the result.
     const int npairs = (m + 1) >> 1;
     const int rot = ((__builtin_amdgcn_readfirstlane(w) + 4 * (int)(blockIdx.x & 1)) * npairs) >> 3;
-    for (int tile = w; tile < ntiles; tile += 4) {
-        // keys past the end of the chunk have zero rows; their kernel values are masked to 0
-        const uint32_t vmask = j_begin + tile * 64 + l < j_end ? 0xffffffffu : 0u;
-        uint32_t kf[D2];
+    for (int step = 0; step < nsteps; ++step) {
+        const int tile = 4 * step + w;
+        if (tile < ntiles) {
+            // keys past the end of the chunk have zero rows; their kernel values are masked to 0
+            const uint32_t vmask = j_begin + tile * 64 + l < j_end ? 0xffffffffu : 0u;
+            uint32_t kf[D2];
 #pragma unroll
-        for (int c8 = 0; c8 < D8; ++c8) {
-            kf[4 * c8 + 0] = fix2_bf16(kr[c8].x, inv2R);
-            kf[4 * c8 + 1] = fix2_bf16(kr[c8].y, inv2R);
-            kf[4 * c8 + 2] = fix2_bf16(kr[c8].z, inv2R);
-            kf[4 * c8 + 3] = fix2_bf16(kr[c8].w, inv2R);
-        }
-        // The next tile's keys are fetched in D/8 column groups spread over the landmark
-        // loop, so that the key stream reaches memory as a steady flow rather than one burst
-        // per tile from every wave at once; its values follow after this tile's values have
-        // been moved to LDS.
-        const uint4 *kp, *vp;
-        row_ptrs(tile + 4, kp, vp);
-        // landmark pairs (2p, 2p+1): rows 2p, 2p+1 of the [a][j] tile; table rows >= m are zero
-        // and the value of landmark m (odd m) is replaced by 0
-        uint16_t* brow = reinterpret_cast<uint16_t*>(sB) + l;
-        uint32_t ta[D2], tb[D2];
-        load_row<D2>(ta, tab + (2 * rot) * D2);
-        int p = rot;
+            for (int c8 = 0; c8 < D8; ++c8) {
+                kf[4 * c8 + 0] = fix2_bf16(kr[c8].x, inv2R);
+                kf[4 * c8 + 1] = fix2_bf16(kr[c8].y, inv2R);
+                kf[4 * c8 + 2] = fix2_bf16(kr[c8].z, inv2R);
+                kf[4 * c8 + 3] = fix2_bf16(kr[c8].w, inv2R);
+            }
+            // The next tile's keys are fetched in D/8 column groups spread over the landmark
+            // loop, so that the key stream reaches memory as a steady flow rather than one
+            // burst per tile from every wave at once; its values follow after this tile's
+            // values have been moved to LDS.
+            const uint4 *kp, *vp;
+            row_ptrs(tile + 4, kp, vp);
+            // landmark pairs (2p, 2p+1): rows 2p, 2p+1 of the [a][j] tile; table rows >= m are
+            // zero and the value of landmark m (odd m) is replaced by 0
+            uint16_t* brow = reinterpret_cast<uint16_t*>(sB) + l;
+            uint32_t ta[D2], tb[D2];
+            load_row<D2>(ta, tab + (2 * rot) * D2);
+            int p = rot;
 #pragma unroll
-        for (int c8 = 0; c8 < D8; ++c8) {
-            if (kp) kr[c8] = kp[c8];
+            for (int c8 = 0; c8 < D8; ++c8) {
+                if (kp) kr[c8] = kp[c8];
 #pragma unroll 1
-            for (int i = c8 * npairs / D8; i < (c8 + 1) * npairs / D8; ++i) {
-                const int pn = p + 1 < npairs ? p + 1 : 0;
-                const float b0 = lap_row<D2>(kf, ta, tb, tab + (2 * p + 1) * D2, esc, ebias);
-                const float b1 = lap_row<D2>(kf, tb, ta, tab + (2 * pn) * D2, esc, ebias);
-                const uint32_t v = pk_f16(b0, 2 * p + 1 < m ? b1 : 0.f) & vmask;
-                brow[(2 * p) * kLP] = (uint16_t)(v & 0xffffu);
-                brow[(2 * p + 1) * kLP] = (uint16_t)(v >> 16);
-                p = pn;
+                for (int i = c8 * npairs / D8; i < (c8 + 1) * npairs / D8; ++i) {
+                    const int pn = p + 1 < npairs ? p + 1 : 0;
+                    const float b0 = lap_row<D2>(kf, ta, tb, tab + (2 * p + 1) * D2, esc, ebias);
+                    const float b1 = lap_row<D2>(kf, tb, ta, tab + (2 * pn) * D2, esc, ebias);
+                    const uint32_t v = pk_f16(b0, 2 * p + 1 < m ? b1 : 0.f) & vmask;
+                    brow[(2 * p) * kLP] = (uint16_t)(v & 0xffffu);
+                    brow[(2 * p + 1) * kLP] = (uint16_t)(v >> 16);
+                    p = pn;
+                }
+            }
+            // this tile's values to fp16 (times the value prescale), transposed into LDS
+#pragma unroll
+            for (int c8 = 0; c8 < D8; ++c8) {
+                const uint32_t yw[4] = {vr[c8].x, vr[c8].y, vr[c8].z, vr[c8].w};
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const uint32_t pv = pk_f16(bf16_lo(yw[t]) * vsc, bf16_hi(yw[t]) * vsc) & vmask;
+                    reinterpret_cast<uint16_t*>(sV)[(8 * c8 + 2 * t) * kLP + l] = (uint16_t)(pv & 0xffffu);
+                    reinterpret_cast<uint16_t*>(sV)[(8 * c8 + 2 * t + 1) * kLP + l] = (uint16_t)(pv >> 16);
+                }
+            }
+            if (vp) {
+#pragma unroll
+                for (int c8 = 0; c8 < D8; ++c8) vr[c8] = vp[c8];
             }
         }
-        // this tile's values to fp16 (times the value prescale), transposed into LDS
+        __syncthreads();   // the step's tiles are complete
+        // U rows [16w, 16w + 16) over the step's tiles, 32 keys per product: A = B[a][j]
+        // (A[l%16][8(l/16) + i]), B = V[j][c] through the transposed tile ([c][j]).
+        const int live = min(4, ntiles - 4 * step);
+        if (rows_live) {
+            const int ao = (16 * w + (l & 15)) * kLP + 8 * (l >> 4);
+            const int bo = (l & 15) * kLP + 8 * (l >> 4);
+            for (int t = 0; t < live; ++t) {
+                const _Float16* tB = tiles + t * (2 * 64 * kLP);
+                const _Float16* tV = tB + 64 * kLP;
 #pragma unroll
-        for (int c8 = 0; c8 < D8; ++c8) {
-            const uint32_t yw[4] = {vr[c8].x, vr[c8].y, vr[c8].z, vr[c8].w};
+                for (int half = 0; half < 2; ++half) {
+                    const h8_t A = *reinterpret_cast<const h8_t*>(tB + ao + 32 * half);
 #pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                const uint32_t pv = pk_f16(bf16_lo(yw[t]) * vsc, bf16_hi(yw[t]) * vsc) & vmask;
-                reinterpret_cast<uint16_t*>(sV)[(8 * c8 + 2 * t) * kLP + l] = (uint16_t)(pv & 0xffffu);
-                reinterpret_cast<uint16_t*>(sV)[(8 * c8 + 2 * t + 1) * kLP + l] = (uint16_t)(pv >> 16);
-            }
-        }
-        if (vp) {
-#pragma unroll
-            for (int c8 = 0; c8 < D8; ++c8) vr[c8] = vp[c8];
-        }
-        wave_lds_sync();
-#pragma unroll
-        for (int s4 = 0; s4 < 4; ++s4) {
-#pragma unroll
-            for (int rb = 0; rb < 2; ++rb) {
-                if (rb < RB) {
-                    const h8_t A =
-                        *reinterpret_cast<const h8_t*>(sB + (32 * rb + (l & 31)) * kLP + 16 * s4 + 8 * (l >> 5));
-#pragma unroll
-                    for (int cb = 0; cb < CB; ++cb) {
-                        const h8_t Bv =
-                            *reinterpret_cast<const h8_t*>(sV + (32 * cb + (l & 31)) * kLP + 16 * s4 + 8 * (l >> 5));
-                        acc[rb][cb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(A, Bv, acc[rb][cb], 0, 0, 0);
+                    for (int cc = 0; cc < C16; ++cc) {
+                        const h8_t Bv = *reinterpret_cast<const h8_t*>(tV + 16 * cc * kLP + bo + 32 * half);
+                        acc[cc] = __builtin_amdgcn_mfma_f32_16x16x32_f16(A, Bv, acc[cc], 0, 0, 0);
                     }
-                    acc[rb][CB] = __builtin_amdgcn_mfma_f32_32x32x16_f16(A, ones, acc[rb][CB], 0, 0, 0);
+                    acc[C16] = __builtin_amdgcn_mfma_f32_16x16x32_f16(A, ones, acc[C16], 0, 0, 0);
                 }
             }
         }
-        wave_lds_sync();
+        __syncthreads();   // the tiles are rewritten by the next step
     }
-    __syncthreads();
-    // per-wave partials to LDS as [c][a] (pitch 65: the 32 lanes of a row block write 32
-    // columns to 32 different banks), then a fixed-order block sum to Upart[h][kb][c][a]
-    // (64 rows a per column); the value columns were formed from V * vscale
-    constexpr int PP = 65;
+    // rows a = 16w + 4(l/16) + r, column 16cc + l%16 (the value columns were formed from
+    // V * vscale); the ones column from column 0 of its block
     const float inv_vsc = 1.f / vsc;
-    float* sP = reinterpret_cast<float*>(lds_raw) + w * ((D + 1) * PP);
-#pragma unroll
-    for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-        for (int cb = 0; cb <= CB; ++cb)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int a = 32 * rb + c_row(r, l);
-                const int c = cb < CB ? 32 * cb + (l & 31) : D;
-                if (cb < CB || (l & 31) == 0) sP[c * PP + a] = acc[rb][cb][r] * (cb < CB ? inv_vsc : 1.f);
-            }
-    __syncthreads();
-    const float* base = reinterpret_cast<const float*>(lds_raw);
     float* dst = Upart + ((size_t)h * nkb + kb) * (D + 1) * 64;
-    for (int e = tid; e < (D + 1) * 64; e += 256) {
-        const int c = e >> 6, a = e & 63;
-        float t = 0.f;
 #pragma unroll
-        for (int ww = 0; ww < 4; ++ww) t += base[ww * (D + 1) * PP + c * PP + a];
-        dst[e] = t;
+    for (int cc = 0; cc < C16; ++cc)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) dst[(16 * cc + (l & 15)) * 64 + 16 * w + 4 * (l >> 4) + r] = acc[cc][r] * inv_vsc;
+    if ((l & 15) == 0) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) dst[D * 64 + 16 * w + 4 * (l >> 4) + r] = acc[C16][r];
     }
 }
 
 // ------------------------------------------------------------------------------------------
 // Key-side partial sums: blocks [0, BH*nkb), one key chunk each.
 constexpr int kKeyLds = kKeyTileLds;
-static_assert(4 * 65 * 65 * 4 <= kKeyTileLds, "key partials exceed the tile space");
 
 template <int D>
 __global__ __launch_bounds__(256, 2) void key_kernel(const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,

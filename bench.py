@@ -114,7 +114,8 @@ def ingest_traffic(kernel, fetch_dir, write_dir, copy_fetch_dir, copy_write_dir,
     `kernel`, stamped with a hash of the kernel sources (bench.py reports null once the
     sources change)."""
     import hashlib
-    symbol = {"key": "key_kernel", "query": "query2_kernel", "pool": "pool2_kernel"}[kernel]
+    symbol = {"key": "key_kernel", "query": "query2_kernel", "pool": "pool2_kernel", "frame_ns": "frame_ns_kernel",
+              "m_final": "mfinal_kernel"}[kernel]
     f_k = _pmc_per_dispatch(fetch_dir, "FETCH_SIZE", symbol)
     w_k = _pmc_per_dispatch(write_dir, "WRITE_SIZE", symbol)
     f_c = _pmc_per_dispatch(copy_fetch_dir, "FETCH_SIZE", "__amd_rocclr_copyBuffer")

@@ -945,6 +945,10 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
     __shared__ __attribute__((aligned(16))) _Float16 sM[4 * CB * 512];
     __shared__ __attribute__((aligned(16))) float sVb[D];
     __shared__ __attribute__((aligned(16))) float sMo[64];
+    // per wave: the bf16 output rows of one 32-query half, staged so that they leave as whole
+    // rows (pitch D + 8 halves)
+    constexpr int OP = D + 8;
+    __shared__ __attribute__((aligned(16))) uint16_t sOut[4 * 32 * OP];
     const int lin = xcd_rank(blockIdx.x, nqb * BH, 0);
     const int h = lin / nqb, qblk = lin % nqb;
     const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
@@ -1032,8 +1036,7 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
         if (NORM == NORM_INLINE) { tmul = 1.f; tadd = 1.f - si; }
         else if (NORM == NORM_ROWSUM) { tmul = 1.f / si; tadd = 0.f; }
         else { tmul = 1.f; tadd = 0.f; }
-        const int iq = i0 + 32 * qb + (l & 31);
-        uint16_t* orow = Out + ((size_t)h * n + iq) * D;
+        uint16_t* stage = sOut + w * 32 * OP + (l & 31) * OP;
 #pragma unroll
         for (int cb = 0; cb < CB; ++cb) {
             f32x16_t y = {};
@@ -1056,14 +1059,25 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
                 if (nan_head) o0 = o1 = o2 = o3 = __builtin_nanf("");
                 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
                 const bf16x2_t p0 = {(__bf16)o0, (__bf16)o1}, p1 = {(__bf16)o2, (__bf16)o3};
-                if (iq < n) {
-                    uint2 st;
-                    st.x = __builtin_bit_cast(uint32_t, p0);
-                    st.y = __builtin_bit_cast(uint32_t, p1);
-                    *reinterpret_cast<uint2*>(orow + c0) = st;
-                }
+                uint2 st;
+                st.x = __builtin_bit_cast(uint32_t, p0);
+                st.y = __builtin_bit_cast(uint32_t, p1);
+                *reinterpret_cast<uint2*>(stage + c0) = st;
             }
         }
+        // The wave's LDS requests complete in order; the barrier keeps the compiler from moving
+        // the reads of other lanes' rows above the writes.  Rows leave as 16-byte chunks, D/8
+        // lanes per row.
+        __builtin_amdgcn_wave_barrier();
+        constexpr int CPR = D / 8, RPP = 64 / CPR;
+#pragma unroll
+        for (int r0 = 0; r0 < 32; r0 += RPP) {
+            const int r = r0 + l / CPR, c = (l % CPR) * 8;
+            const uint4 v = *reinterpret_cast<const uint4*>(sOut + (w * 32 + r) * OP + c);
+            const int iq = i0 + 32 * qb + r;
+            if (iq < n) *reinterpret_cast<uint4*>(Out + ((size_t)h * n + iq) * D + c) = v;
+        }
+        __builtin_amdgcn_wave_barrier();   // the next half overwrites the rows after these reads
     }
 }
 

@@ -80,6 +80,7 @@ __device__ __forceinline__ void wave_argmax(float& v, int& idx) {
 }
 
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
 // Two floats to a packed fp16 pair, round to nearest even (v_cvt_pk_f16_f32).
 __device__ __forceinline__ uint32_t pk_f16(float a, float b) {
@@ -1067,7 +1068,7 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
         }
         // The wave's LDS requests complete in order; the barrier keeps the compiler from moving
         // the reads of other lanes' rows above the writes.  Rows leave as 16-byte chunks, D/8
-        // lanes per row.
+        // lanes per row, with non-temporal stores (the output is not read again here).
         __builtin_amdgcn_wave_barrier();
         constexpr int CPR = D / 8, RPP = 64 / CPR;
 #pragma unroll
@@ -1075,7 +1076,9 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
             const int r = r0 + l / CPR, c = (l % CPR) * 8;
             const uint4 v = *reinterpret_cast<const uint4*>(sOut + (w * 32 + r) * OP + c);
             const int iq = i0 + 32 * qb + r;
-            if (iq < n) *reinterpret_cast<uint4*>(Out + ((size_t)h * n + iq) * D + c) = v;
+            if (iq < n)
+                __builtin_nontemporal_store(__builtin_bit_cast(u32x4_t, v),
+                                            reinterpret_cast<u32x4_t*>(Out + ((size_t)h * n + iq) * D + c));
         }
         __builtin_amdgcn_wave_barrier();   // the next half overwrites the rows after these reads
     }

@@ -79,6 +79,47 @@ def cpu_baseline(w, x, budget_s=10.0):
                       "forward, %.1f s" % (heads, BH, w.name, w.n, w.d, w.m, w.T, t_used)}
 
 
+def time_train_step(steps):
+    """The training workload's forward and backward (fp32 path; B=32, H=4, n=3136, d=32, m=64,
+    T=6), reported beside the headline: wall-clock ms per call, per-kernel ms from the library's
+    HIP events, and the fraction of the VALU peak for the pairwise work (2nm pairs per head of
+    (2d+1) operations for the forward, about 2.5 times that for the backward)."""
+    import torch
+    from paper_2604_20368_amd import lapattn
+    w = W.WORKLOADS["train"]
+    x = W.make_inputs(w, with_grad=True)
+    dev = torch.device("cuda:0")
+    Q, K, V, dO = (torch.from_numpy(x[k]).to(dev) for k in ("Q", "K", "V", "dO"))
+    out = torch.empty_like(Q)
+    wsf = lapattn.workspace(Q, w.m, w.T)
+    wsb = lapattn.workspace(Q, w.m, w.T, for_backward=True)
+    grads = tuple(torch.empty_like(Q) for _ in range(3))
+    res = {"workload": w.name, "B": w.B, "H": w.H, "n": w.n, "d": w.d, "m": w.m, "T": w.T, "inputs": w.dtype}
+    pair_ops = w.B * w.H * 2 * w.n * w.m * (2 * w.d + 1)
+    for name, fn, ops in (("forward", lambda: lapattn.forward(Q, K, V, w.m, w.lam, w.T, out=out, ws=wsf), pair_ops),
+                          ("backward", lambda: lapattn.backward(Q, K, V, dO, w.m, w.lam, w.T, grads=grads, ws=wsb),
+                           2.5 * pair_ops)):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            fn()
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / steps
+        lapattn.lapattn_timing_enable(1)
+        for _ in range(steps):
+            fn()
+        torch.cuda.synchronize()
+        lapattn.lapattn_timing_enable(0)
+        per = {}
+        for k, t in lapattn.lapattn_timing_read(cap=64 * steps + 64):
+            per.setdefault(k, []).append(t)
+        res[name] = {"ms": round(ms, 4), "kernels_ms": {k: round(sum(v) / len(v), 4) for k, v in per.items()},
+                     "alu_frac": round(ops / (ms * 1e-3) / 1e12 / PEAK_FP32_VECTOR_TFLOPS, 4)}
+    return res
+
+
 KERNEL_SOURCES = ["paper_2604_20368_amd/csrc/fast.hip", "paper_2604_20368_amd/csrc/common.hpp",
                   "paper_2604_20368_amd/csrc/host.cpp"]
 COPY_BYTES = 512 * 1024 * 1024
@@ -149,6 +190,8 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-train-step", action="store_true",
+                    help="skip the training workload's forward and backward timing")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run only the plain copy used to scale the HBM byte counters")
     ap.add_argument("--ingest-traffic", nargs=5, metavar=("KERNEL", "FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR",
@@ -223,6 +266,8 @@ def main():
         "kernels_ms": {k: round(v, 5) for k, v in avg.items()},
         "roofline": roof,
     }
+    if not args.no_train_step:
+        res["train_step"] = time_train_step(min(args.steps, 20))
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(w, x)
     print(json.dumps(res), flush=True)

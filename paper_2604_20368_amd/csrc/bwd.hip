@@ -150,11 +150,14 @@ __global__ __launch_bounds__(64) void bwd_query_lm_kernel(const float* __restric
 }
 
 // ------------------------------------------------------------------------------------------
-// Register-blocked MP x MP fp64 product for 256 threads (op(A) op(B), see fwd.hip).
+// Register-blocked MP x MP fp64 product for 256 threads (op(A) op(B), see fwd.hip); operands in
+// LDS with row pitch MP + 1 (an odd number of doubles: the 16 column blocks of a wave reading a
+// transposed operand fall on different banks).
 template <int MP, bool TA, bool TB>
 __device__ __forceinline__ void mm_block_b(const double* __restrict__ A, const double* __restrict__ B,
                                            double (&r)[MP / 16][MP / 16]) {
     constexpr int RB = MP / 16;
+    constexpr int P = MP + 1;
     const int br = threadIdx.x / 16, bc = threadIdx.x % 16;
 #pragma unroll
     for (int i = 0; i < RB; ++i)
@@ -163,9 +166,9 @@ __device__ __forceinline__ void mm_block_b(const double* __restrict__ A, const d
     for (int k = 0; k < MP; ++k) {
         double a[RB], b[RB];
 #pragma unroll
-        for (int i = 0; i < RB; ++i) a[i] = TA ? A[k * MP + RB * br + i] : A[(RB * br + i) * MP + k];
+        for (int i = 0; i < RB; ++i) a[i] = TA ? A[k * P + RB * br + i] : A[(RB * br + i) * P + k];
 #pragma unroll
-        for (int j = 0; j < RB; ++j) b[j] = TB ? B[(RB * bc + j) * MP + k] : B[k * MP + RB * bc + j];
+        for (int j = 0; j < RB; ++j) b[j] = TB ? B[(RB * bc + j) * P + k] : B[k * P + RB * bc + j];
 #pragma unroll
         for (int i = 0; i < RB; ++i)
 #pragma unroll
@@ -180,7 +183,7 @@ __device__ __forceinline__ void store_block(double* __restrict__ S, const double
 #pragma unroll
     for (int i = 0; i < RB; ++i)
 #pragma unroll
-        for (int j = 0; j < RB; ++j) S[(RB * br + i) * MP + RB * bc + j] = r[i][j];
+        for (int j = 0; j < RB; ++j) S[(RB * br + i) * (MP + 1) + RB * bc + j] = r[i][j];
 }
 
 // ------------------------------------------------------------------------------------------
@@ -203,12 +206,13 @@ __global__ __launch_bounds__(256) void bwd_ns_kernel(const float* __restrict__ q
     constexpr int D1 = D + 1;
     // W, X, G, T (MP x MP each); before the reverse iteration the same space holds
     // U (MP x D1) at 0 and dM (MP x D1) right after it.
-    constexpr int LDSN = (4 * MP * MP > 2 * MP * D1) ? 4 * MP * MP : 2 * MP * D1;
+    constexpr int P = MP + 1;   // LDS row pitch of the MP x MP matrices
+    constexpr int LDSN = (4 * MP * P > 2 * MP * D1) ? 4 * MP * P : 2 * MP * D1;
     __shared__ double lds[LDSN];
     double* sW = lds;
-    double* sX = lds + MP * MP;
-    double* sG = lds + 2 * MP * MP;
-    double* sT = lds + 3 * MP * MP;
+    double* sX = lds + MP * P;
+    double* sG = lds + 2 * MP * P;
+    double* sT = lds + 3 * MP * P;
     const int h = blockIdx.x, tid = threadIdx.x;
     const int br = tid / 16, bc = tid % 16;
     const float* q = qt + (size_t)h * m * D;
@@ -264,7 +268,7 @@ __global__ __launch_bounds__(256) void bwd_ns_kernel(const float* __restrict__ q
             w = exp(-dist / lambda);
             if (a == b) w += eps;
         }
-        sW[e] = w;
+        sW[a * P + b] = w;
     }
     store_block<MP>(sG, dX);
     double dW[RB][RB];
@@ -276,7 +280,7 @@ __global__ __launch_bounds__(256) void bwd_ns_kernel(const float* __restrict__ q
     if (c > 0.0) {
         __syncthreads();
         for (int t = T - 1; t >= 0; --t) {
-            for (int e = tid; e < MP * MP; e += 256) sX[e] = Xh[(size_t)t * mm + e];
+            for (int e = tid; e < MP * MP; e += 256) sX[(e / MP) * P + e % MP] = Xh[(size_t)t * mm + e];
             __syncthreads();
             double r[RB][RB], r2[RB][RB];
             // dW -= X^T G X^T
@@ -306,7 +310,7 @@ __global__ __launch_bounds__(256) void bwd_ns_kernel(const float* __restrict__ q
 #pragma unroll
                 for (int j = 0; j < RB; ++j) {
                     const int a = RB * br + i, b = RB * bc + j;
-                    sG[a * MP + b] = 2.0 * sG[a * MP + b] - r2[i][j] - r[i][j];
+                    sG[a * P + b] = 2.0 * sG[a * P + b] - r2[i][j] - r[i][j];
                 }
             __syncthreads();
         }
@@ -321,7 +325,7 @@ __global__ __launch_bounds__(256) void bwd_ns_kernel(const float* __restrict__ q
 #pragma unroll
             for (int j = 0; j < RB; ++j) {
                 const int a = RB * br + i, b = RB * bc + j;
-                part += sG[a * MP + b] * sW[b * MP + a];
+                part += sG[a * P + b] * sW[b * P + a];
             }
         sT[tid] = part;
         __syncthreads();
@@ -337,9 +341,9 @@ __global__ __launch_bounds__(256) void bwd_ns_kernel(const float* __restrict__ q
 #pragma unroll
             for (int j = 0; j < RB; ++j) {
                 const int a = RB * br + i, b = RB * bc + j;
-                double v = sG[b * MP + a] / c;
-                if (b == bs) v += dc * ninf * sgnd(sW[a * MP + b]);
-                if (a == as) v += dc * n1 * sgnd(sW[a * MP + b]);
+                double v = sG[b * P + a] / c;
+                if (b == bs) v += dc * ninf * sgnd(sW[a * P + b]);
+                if (a == as) v += dc * n1 * sgnd(sW[a * P + b]);
                 dW[i][j] += v;
             }
         __syncthreads();
@@ -352,20 +356,20 @@ __global__ __launch_bounds__(256) void bwd_ns_kernel(const float* __restrict__ q
 #pragma unroll
         for (int j = 0; j < RB; ++j) {
             const int a = RB * br + i, b = RB * bc + j;
-            const double kab = sW[a * MP + b] - (a == b && a < m ? eps : 0.0);
-            sT[a * MP + b] = -kab * dW[i][j] / lambda;
+            const double kab = sW[a * P + b] - (a == b && a < m ? eps : 0.0);
+            sT[a * P + b] = -kab * dW[i][j] / lambda;
         }
     __syncthreads();
     for (int e = tid; e < m * D; e += 256) {
         const int a = e / D, cc = e % D;
         double s = 0.0;
-        for (int b = 0; b < m; ++b) s += sT[a * MP + b] * sgnd((double)q[a * D + cc] - (double)k[b * D + cc]);
+        for (int b = 0; b < m; ++b) s += sT[a * P + b] * sgnd((double)q[a * D + cc] - (double)k[b * D + cc]);
         dqtW[(size_t)h * m * D + e] = (float)s;
     }
     for (int e = tid; e < m * D; e += 256) {
         const int b = e / D, cc = e % D;
         double s = 0.0;
-        for (int a = 0; a < m; ++a) s += sT[a * MP + b] * sgnd((double)q[a * D + cc] - (double)k[b * D + cc]);
+        for (int a = 0; a < m; ++a) s += sT[a * P + b] * sgnd((double)q[a * D + cc] - (double)k[b * D + cc]);
         dktW[(size_t)h * m * D + e] = (float)(-s);
     }
 }

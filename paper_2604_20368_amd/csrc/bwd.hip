@@ -13,6 +13,7 @@
 //   bwd_pool_kernel      landmark-mean backward into dQ, dK
 #include "common.hpp"
 #include "kernels.hpp"
+#include "ns_mfma.hpp"
 
 namespace lapattn {
 
@@ -150,50 +151,15 @@ __global__ __launch_bounds__(64) void bwd_query_lm_kernel(const float* __restric
 }
 
 // ------------------------------------------------------------------------------------------
-// Register-blocked MP x MP fp64 product for 256 threads (op(A) op(B), see fwd.hip); operands in
-// LDS with row pitch MP + 1 (an odd number of doubles: the 16 column blocks of a wave reading a
-// transposed operand fall on different banks).
-template <int MP, bool TA, bool TB>
-__device__ __forceinline__ void mm_block_b(const double* __restrict__ A, const double* __restrict__ B,
-                                           double (&r)[MP / 16][MP / 16]) {
-    constexpr int RB = MP / 16;
-    constexpr int P = MP + 1;
-    const int br = threadIdx.x / 16, bc = threadIdx.x % 16;
-#pragma unroll
-    for (int i = 0; i < RB; ++i)
-#pragma unroll
-        for (int j = 0; j < RB; ++j) r[i][j] = 0.0;
-    for (int k = 0; k < MP; ++k) {
-        double a[RB], b[RB];
-#pragma unroll
-        for (int i = 0; i < RB; ++i) a[i] = TA ? A[k * P + RB * br + i] : A[(RB * br + i) * P + k];
-#pragma unroll
-        for (int j = 0; j < RB; ++j) b[j] = TB ? B[(RB * bc + j) * P + k] : B[k * P + RB * bc + j];
-#pragma unroll
-        for (int i = 0; i < RB; ++i)
-#pragma unroll
-            for (int j = 0; j < RB; ++j) r[i][j] = fma(a[i], b[j], r[i][j]);
-    }
-}
-
-template <int MP>
-__device__ __forceinline__ void store_block(double* __restrict__ S, const double (&r)[MP / 16][MP / 16]) {
-    constexpr int RB = MP / 16;
-    const int br = threadIdx.x / 16, bc = threadIdx.x % 16;
-#pragma unroll
-    for (int i = 0; i < RB; ++i)
-#pragma unroll
-        for (int j = 0; j < RB; ++j) S[(RB * br + i) * (MP + 1) + RB * bc + j] = r[i][j];
-}
-
-// ------------------------------------------------------------------------------------------
-// Newton-Schulz backward, one block of 256 threads per head, fp64.
+// Newton-Schulz backward, one block of 256 threads per head, fp64, products on the fp64 matrix
+// cores (ns_mfma.hpp).
 //   dM = sum of partials;  dX_T = dM U^T;  dU = X_T^T dM.
 //   For t = T-1..0, with G = dL/dX_{t+1} and X_{t+1} = 2 X_t - X_t W X_t:
 //     dW -= X_t^T G X_t^T;   G <- 2G - G X_t^T W^T - W^T X_t^T G.
 //   X0 = W^T / c:  dW += G^T / c + dc (||W||_inf [b = b*] + ||W||_1 [a = a*]) sign(W),
 //     dc = -<G, W^T> / c^2.
 //   K_LL: dDW = -k dW / lambda;  dqt_a += sum_b dDW_ab sign(qt_a - kt_b);  dkt_b -= same.
+// W comes from the forward solve (stored after the iterates).  U and dM are held as value columns (MFMA operands) plus their ones columns.
 template <int MP, int D>
 __global__ __launch_bounds__(256) void bwd_ns_kernel(const float* __restrict__ qt, const float* __restrict__ kt,
                                                      const double* __restrict__ Xs, const double* __restrict__ cinfo,
@@ -202,145 +168,179 @@ __global__ __launch_bounds__(256) void bwd_ns_kernel(const float* __restrict__ q
                                                      float* __restrict__ dvbar, float* __restrict__ dqtW,
                                                      float* __restrict__ dktW, int n, int m, int T, double lambda,
                                                      double eps, int nlc, int nqb) {
-    constexpr int RB = MP / 16;
+    using SQ = ns_tiles<MP, MP>;
+    using SU = ns_tiles<MP, D>;
     constexpr int D1 = D + 1;
-    // W, X, G, T (MP x MP each); before the reverse iteration the same space holds
-    // U (MP x D1) at 0 and dM (MP x D1) right after it.
-    constexpr int P = MP + 1;   // LDS row pitch of the MP x MP matrices
-    constexpr int LDSN = (4 * MP * P > 2 * MP * D1) ? 4 * MP * P : 2 * MP * D1;
+    constexpr int P = ns_pitch(MP);
+    constexpr int PU = ns_pitch(D);
+    // W, X, G, T (MP x MP each, pitch P); before the reverse iteration the same space holds the
+    // value columns of U and dM (MP x D each, pitch PU) and X_T (pitch P).
+    constexpr int PRE = 2 * MP * PU + MP * P;
+    constexpr int LDSN = (4 * MP * P > PRE) ? 4 * MP * P : PRE;
     __shared__ double lds[LDSN];
+    __shared__ double su1[MP], sdm1[MP];
+    __shared__ double svb[256];
     double* sW = lds;
     double* sX = lds + MP * P;
     double* sG = lds + 2 * MP * P;
     double* sT = lds + 3 * MP * P;
     const int h = blockIdx.x, tid = threadIdx.x;
-    const int br = tid / 16, bc = tid % 16;
     const float* q = qt + (size_t)h * m * D;
     const float* k = kt + (size_t)h * m * D;
     const size_t mm = (size_t)MP * MP;
-    const double* Xh = Xs + (size_t)h * (T + 1) * mm;
+    const double* Xh = Xs + (size_t)h * (T + 2) * mm;   // X_0 .. X_T, then W
+    const double c = cinfo[h * 4 + 0], n1 = cinfo[h * 4 + 1], ninf = cinfo[h * 4 + 2];
+    const int code = (int)cinfo[h * 4 + 3];
 
-    // dvbar (inline normalisation; zeros otherwise because the partials are zero)
-    for (int c = tid; c < D; c += 256) {
+    // dvbar (inline normalisation; zeros otherwise because the partials are zero): 256 / D
+    // partial sums per column over the query blocks, then in order
+    {
+        constexpr int G = 256 / D;
+        const int g = tid / D, cc = tid % D;
         double s = 0.0;
-        for (int b = 0; b < nqb; ++b) s += dvbar_part[((size_t)h * nqb + b) * D + c];
-        dvbar[(size_t)h * D + c] = (float)s;
-    }
-    // U and dM as [MP][D1] (zero rows a >= m), consumed before W and G are written
-    double* sU = lds;
-    double* sdM = lds + MP * D1;
-    for (int e = tid; e < MP * D1; e += 256) {
-        const int a = e / D1;
-        double s = 0.0, u = 0.0;
-        if (a < m) {
-            for (int ch = 0; ch < nlc; ++ch) s += (double)dM_part[(((size_t)h * nlc + ch) * m) * D1 + e];
-            u = (double)U[(size_t)h * m * D1 + e];
+#pragma unroll 4
+        for (int b = g; b < nqb; b += G) s += dvbar_part[((size_t)h * nqb + b) * D + cc];
+        svb[tid] = s;
+        __syncthreads();
+        if (tid < D) {
+            double t = 0.0;
+#pragma unroll
+            for (int gg = 0; gg < G; ++gg) t += svb[gg * D + tid];
+            dvbar[(size_t)h * D + tid] = (float)t;
         }
-        sdM[e] = s;
-        sU[e] = u;
     }
-    __syncthreads();
-    // dX = dM U^T (MP x MP) and dU = X_T^T dM (m x D1), both into registers / global
-    double dX[RB][RB];
+    {
+        double* sU = lds;
+        double* sdM = lds + MP * PU;
+        double* sXT = lds + 2 * MP * PU;
+        // dM = sum of the landmark-chunk partials (in chunk order); each thread's entries are
+        // loaded together, chunk by chunk
+        constexpr int NE = (MP * D1 + 255) / 256;
+        double dm[NE];
 #pragma unroll
-    for (int i = 0; i < RB; ++i)
+        for (int r = 0; r < NE; ++r) dm[r] = 0.0;
+        const int lim = m * D1 - 1;
+#pragma unroll 4
+        for (int ch = 0; ch < nlc; ++ch) {
+            const float* dp = dM_part + ((size_t)h * nlc + ch) * m * D1;
 #pragma unroll
-        for (int j = 0; j < RB; ++j) {
-            const int a = RB * br + i, b = RB * bc + j;
+            for (int r = 0; r < NE; ++r) {
+                const int e = tid + 256 * r;
+                const float v = dp[min(e, lim)];
+                dm[r] += (e <= lim) ? (double)v : 0.0;
+            }
+        }
+        float uv[NE];
+#pragma unroll
+        for (int r = 0; r < NE; ++r) uv[r] = U[(size_t)h * m * D1 + min(tid + 256 * r, lim)];
+#pragma unroll
+        for (int r = 0; r < NE; ++r) {
+            const int e = tid + 256 * r;
+            if (e < MP * D1) {
+                const int a = e / D1, cc = e % D1;
+                const double u = (a < m) ? (double)uv[r] : 0.0;
+                if (cc < D) {
+                    sdM[a * PU + cc] = dm[r];
+                    sU[a * PU + cc] = u;
+                } else {
+                    sdm1[a] = dm[r];
+                    su1[a] = u;
+                }
+            }
+        }
+        ns_load<MP, P>(sXT, Xh + (size_t)T * mm);
+        __syncthreads();
+        // dX = dM U^T (registers, kept until G is stored) and dU = X_T^T dM (global)
+        f64x4_t dX[SQ::NT];
+        ns_mm<MP, MP, D, false, true, PU, PU>(sdM, sU, dX);
+#pragma unroll
+        for (int i = 0; i < SQ::NT; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) dX[i][j] += sdm1[SQ::row(i, j)] * su1[SQ::col(i)];
+        {
+            f64x4_t r[SU::NT];
+            ns_mm<MP, D, MP, true, false, P, PU>(sXT, sdM, r);
+#pragma unroll
+            for (int i = 0; i < SU::NT; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int b = SU::row(i, j), cc = SU::col(i);
+                    if (b < m) dU[((size_t)h * m + b) * D1 + cc] = (float)r[i][j];
+                }
+        }
+        if (tid < m) {
             double s = 0.0;
-            for (int c = 0; c < D1; ++c) s += sdM[a * D1 + c] * sU[b * D1 + c];
-            dX[i][j] = s;
+            for (int a = 0; a < MP; ++a) s += sXT[a * P + tid] * sdm1[a];
+            dU[((size_t)h * m + tid) * D1 + D] = (float)s;
         }
-    for (int e = tid; e < m * D1; e += 256) {
-        const int b = e / D1, c = e % D1;
-        double s = 0.0;
-        for (int a = 0; a < m; ++a) s += Xh[(size_t)T * mm + a * MP + b] * sdM[a * D1 + c];
-        dU[(size_t)h * m * D1 + e] = (float)s;
+        __syncthreads();
+        // W (kernel + eps I, as the forward solve stored it) and G = dX
+        ns_load<MP, P>(sW, Xh + (size_t)(T + 1) * mm);
+        ns_store<MP, MP, P>(sG, dX);
     }
-    __syncthreads();
-    // W (kernel + eps I) and G = dX
-    for (int e = tid; e < MP * MP; e += 256) {
-        const int a = e / MP, b = e % MP;
-        double w = 0.0;
-        if (a < m && b < m) {
-            double dist = 0.0;
-            for (int c = 0; c < D; ++c) dist += fabs((double)q[a * D + c] - (double)k[b * D + c]);
-            w = exp(-dist / lambda);
-            if (a == b) w += eps;
-        }
-        sW[a * P + b] = w;
-    }
-    store_block<MP>(sG, dX);
-    double dW[RB][RB];
+    f64x4_t dW[SQ::NT];
 #pragma unroll
-    for (int i = 0; i < RB; ++i)
-#pragma unroll
-        for (int j = 0; j < RB; ++j) dW[i][j] = 0.0;
-    const double c = cinfo[h * 4 + 0];
+    for (int i = 0; i < SQ::NT; ++i) dW[i] = f64x4_t{0.0, 0.0, 0.0, 0.0};
     if (c > 0.0) {
+        // X_t comes through registers: the loads of X_{t-1} are issued before step t's products
+        double xr[MP * MP / 256];
+        if (T > 0) ns_fetch<MP>(xr, Xh + (size_t)(T - 1) * mm);
         __syncthreads();
         for (int t = T - 1; t >= 0; --t) {
-            for (int e = tid; e < MP * MP; e += 256) sX[(e / MP) * P + e % MP] = Xh[(size_t)t * mm + e];
+            ns_put<MP, P>(sX, xr);
             __syncthreads();
-            double r[RB][RB], r2[RB][RB];
+            if (t > 0) ns_fetch<MP>(xr, Xh + (size_t)(t - 1) * mm);
+            f64x4_t r[SQ::NT], r2[SQ::NT];
             // dW -= X^T G X^T
-            mm_block_b<MP, true, false>(sX, sG, r);        // X^T G
-            store_block<MP>(sT, r);
+            ns_mm<MP, MP, MP, true, false, P, P>(sX, sG, r);       // X^T G
+            ns_store<MP, MP, P>(sT, r);
             __syncthreads();
-            mm_block_b<MP, false, true>(sT, sX, r);        // (X^T G) X^T
+            ns_mm<MP, MP, MP, false, true, P, P>(sT, sX, r);       // (X^T G) X^T
 #pragma unroll
-            for (int i = 0; i < RB; ++i)
-#pragma unroll
-                for (int j = 0; j < RB; ++j) dW[i][j] -= r[i][j];
+            for (int i = 0; i < SQ::NT; ++i) dW[i] -= r[i];
             __syncthreads();
             // G X^T W^T
-            mm_block_b<MP, false, true>(sG, sX, r);        // G X^T
-            store_block<MP>(sT, r);
+            ns_mm<MP, MP, MP, false, true, P, P>(sG, sX, r);       // G X^T
+            ns_store<MP, MP, P>(sT, r);
             __syncthreads();
-            mm_block_b<MP, false, true>(sT, sW, r2);       // (G X^T) W^T
+            ns_mm<MP, MP, MP, false, true, P, P>(sT, sW, r2);      // (G X^T) W^T
             __syncthreads();
             // W^T X^T G = (X W)^T G
-            mm_block_b<MP, true, true>(sW, sX, r);         // W^T X^T
-            store_block<MP>(sT, r);
+            ns_mm<MP, MP, MP, true, true, P, P>(sW, sX, r);        // W^T X^T
+            ns_store<MP, MP, P>(sT, r);
             __syncthreads();
-            mm_block_b<MP, false, false>(sT, sG, r);       // (W^T X^T) G
+            ns_mm<MP, MP, MP, false, false, P, P>(sT, sG, r);      // (W^T X^T) G
             __syncthreads();
 #pragma unroll
-            for (int i = 0; i < RB; ++i)
+            for (int i = 0; i < SQ::NT; ++i)
 #pragma unroll
-                for (int j = 0; j < RB; ++j) {
-                    const int a = RB * br + i, b = RB * bc + j;
+                for (int j = 0; j < 4; ++j) {
+                    const int a = SQ::row(i, j), b = SQ::col(i);
                     sG[a * P + b] = 2.0 * sG[a * P + b] - r2[i][j] - r[i][j];
                 }
             __syncthreads();
         }
         // X0 = W^T / c
-        const double n1 = cinfo[h * 4 + 1], ninf = cinfo[h * 4 + 2];
-        const int code = (int)cinfo[h * 4 + 3];
         const int as = code / 256, bs = code % 256;
         // <G, W^T>: block reduction in fixed order
         double part = 0.0;
 #pragma unroll
-        for (int i = 0; i < RB; ++i)
+        for (int i = 0; i < SQ::NT; ++i)
 #pragma unroll
-            for (int j = 0; j < RB; ++j) {
-                const int a = RB * br + i, b = RB * bc + j;
+            for (int j = 0; j < 4; ++j) {
+                const int a = SQ::row(i, j), b = SQ::col(i);
                 part += sG[a * P + b] * sW[b * P + a];
             }
-        sT[tid] = part;
-        __syncthreads();
-        if (tid == 0) {
-            double s = 0.0;
-            for (int e = 0; e < 256; ++e) s += sT[e];
-            sT[256] = s;
-        }
-        __syncthreads();
-        const double dc = -sT[256] / (c * c);
 #pragma unroll
-        for (int i = 0; i < RB; ++i)
+        for (int off = 32; off >= 1; off >>= 1) part += __shfl_xor(part, off, 64);
+        if ((tid & 63) == 0) sT[tid >> 6] = part;
+        __syncthreads();
+        const double dc = -(((sT[0] + sT[1]) + sT[2]) + sT[3]) / (c * c);
 #pragma unroll
-            for (int j = 0; j < RB; ++j) {
-                const int a = RB * br + i, b = RB * bc + j;
+        for (int i = 0; i < SQ::NT; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int a = SQ::row(i, j), b = SQ::col(i);
                 double v = sG[b * P + a] / c;
                 if (b == bs) v += dc * ninf * sgnd(sW[a * P + b]);
                 if (a == as) v += dc * n1 * sgnd(sW[a * P + b]);
@@ -350,27 +350,45 @@ __global__ __launch_bounds__(256) void bwd_ns_kernel(const float* __restrict__ q
     } else {
         __syncthreads();
     }
-    // dDW = -k dW / lambda (k = W - eps on the diagonal) into sT
+    // dDW = -k dW / lambda (k = W - eps on the diagonal), fp32, into the T region; the landmark
+    // rows (zero past m) into the X and G regions.  Entries past m are zero, so the sums below
+    // run over all MP rows.
+    float* sTf = reinterpret_cast<float*>(sT);
+    float* sqf = reinterpret_cast<float*>(sX);
+    float* skf = sqf + MP * D;
 #pragma unroll
-    for (int i = 0; i < RB; ++i)
+    for (int i = 0; i < SQ::NT; ++i)
 #pragma unroll
-        for (int j = 0; j < RB; ++j) {
-            const int a = RB * br + i, b = RB * bc + j;
+        for (int j = 0; j < 4; ++j) {
+            const int a = SQ::row(i, j), b = SQ::col(i);
             const double kab = sW[a * P + b] - (a == b && a < m ? eps : 0.0);
-            sT[a * P + b] = -kab * dW[i][j] / lambda;
+            sTf[a * MP + b] = (float)(-kab * dW[i][j] / lambda);
         }
+    ns_stage_rows<MP, D>(sqf, q, m * D);
+    ns_stage_rows<MP, D>(skf, k, m * D);
     __syncthreads();
+    // dqt_a += sum_b dDW_ab sign(qt_a - kt_b);  dkt_b -= sum_a dDW_ab sign(qt_a - kt_b)
     for (int e = tid; e < m * D; e += 256) {
         const int a = e / D, cc = e % D;
-        double s = 0.0;
-        for (int b = 0; b < m; ++b) s += sT[a * P + b] * sgnd((double)q[a * D + cc] - (double)k[b * D + cc]);
-        dqtW[(size_t)h * m * D + e] = (float)s;
+        const float qa = sqf[e];
+        float s = 0.f;
+#pragma unroll 8
+        for (int b = 0; b < MP; ++b) {
+            const float kb = skf[b * D + cc], t = sTf[a * MP + b];
+            s += (qa > kb) ? t : ((qa < kb) ? -t : 0.f);
+        }
+        dqtW[(size_t)h * m * D + e] = s;
     }
     for (int e = tid; e < m * D; e += 256) {
         const int b = e / D, cc = e % D;
-        double s = 0.0;
-        for (int a = 0; a < m; ++a) s += sT[a * P + b] * sgnd((double)q[a * D + cc] - (double)k[b * D + cc]);
-        dktW[(size_t)h * m * D + e] = (float)(-s);
+        const float kb = skf[e];
+        float s = 0.f;
+#pragma unroll 8
+        for (int a = 0; a < MP; ++a) {
+            const float qa = sqf[a * D + cc], t = sTf[a * MP + b];
+            s += (qa > kb) ? t : ((qa < kb) ? -t : 0.f);
+        }
+        dktW[(size_t)h * m * D + e] = -s;
     }
 }
 

@@ -3,10 +3,11 @@
 //   pool_kernel         landmark means (Sec. 4.2, sampling; 1-D segments)
 //   key_summary_kernel  U = K_LK [V | 1], split over key chunks (Sec. 3.2, Eq. (3) key summaries;
 //                       K_LK of Algorithm 1 in the orientation K_QL X K_LK)
-//   ns_solve_kernel     K_LL, Algorithm 2 in fp64, then M = X_T U
+//   ns_solve_kernel     K_LL, Algorithm 2 in fp64 on the matrix cores, then M = X_T U
 //   query_out_kernel    Y = K_QL M and the normalisation (Eq. (8), Eq. (4))
 #include "common.hpp"
 #include "kernels.hpp"
+#include "ns_mfma.hpp"
 
 namespace lapattn {
 
@@ -125,35 +126,14 @@ __global__ __launch_bounds__(256) void key_summary_kernel(const typename elem<DT
 }
 
 // ------------------------------------------------------------------------------------------
-// Register-blocked MP x MP fp64 product for 256 threads: thread (br, bc) of a 16 x 16 grid
-// owns the RB x RB block at rows RB*br.., columns RB*bc.. of op(A) op(B).
-template <int MP, bool TA, bool TB>
-__device__ __forceinline__ void mm_block(const double* __restrict__ A, const double* __restrict__ B,
-                                         double (&r)[MP / 16][MP / 16]) {
-    constexpr int RB = MP / 16;
-    const int br = threadIdx.x / 16, bc = threadIdx.x % 16;
-#pragma unroll
-    for (int i = 0; i < RB; ++i)
-#pragma unroll
-        for (int j = 0; j < RB; ++j) r[i][j] = 0.0;
-    for (int k = 0; k < MP; ++k) {
-        double a[RB], b[RB];
-#pragma unroll
-        for (int i = 0; i < RB; ++i) a[i] = TA ? A[k * MP + RB * br + i] : A[(RB * br + i) * MP + k];
-#pragma unroll
-        for (int j = 0; j < RB; ++j) b[j] = TB ? B[(RB * bc + j) * MP + k] : B[k * MP + RB * bc + j];
-#pragma unroll
-        for (int i = 0; i < RB; ++i)
-#pragma unroll
-            for (int j = 0; j < RB; ++j) r[i][j] = fma(a[i], b[j], r[i][j]);
-    }
-}
-
-// ------------------------------------------------------------------------------------------
 // Newton-Schulz solve, one block of 256 threads per head, fp64 in LDS, matrices padded to
-// MP x MP with zeros (the padding stays zero under every update).
+// MP x MP with zeros (the padding stays zero under every update):
 //   W = K_LL + eps I,  c = ||W||_1 ||W||_inf,  X0 = W^T / c (X := 0 if c = 0),
 //   X_{t+1} = X_t (2I - W X_t);  then U = sum of the key-chunk partials, M = X_T U.
+// With store_all, Xs[h] holds X_0 .. X_T and then W (T + 2 matrices, pitch MP) for the backward.
+// Products on the fp64 matrix cores (ns_mfma.hpp); U's value columns and the ones column are
+// kept apart so that the value part of M is one MFMA product and the ones column a matrix-vector
+// product.
 template <int MP, int D>
 __global__ __launch_bounds__(256) void ns_solve_kernel(const float* __restrict__ qt, const float* __restrict__ kt,
                                                        const float* __restrict__ Upart,
@@ -162,47 +142,56 @@ __global__ __launch_bounds__(256) void ns_solve_kernel(const float* __restrict__
                                                        float* __restrict__ U, float* __restrict__ M,
                                                        float* __restrict__ vbar, int n, int m, int T,
                                                        double lambda, double eps, int nkc, int store_all) {
-    constexpr int RB = MP / 16;
+    using SQ = ns_tiles<MP, MP>;
+    using SU = ns_tiles<MP, D>;
     constexpr int D1 = D + 1;
-    // X, W, T (MP x MP each); after the iteration U (MP x D1) reuses the space from W on.
-    constexpr int LDSN = (3 * MP * MP > MP * MP + MP * D1) ? 3 * MP * MP : MP * MP + MP * D1;
+    constexpr int P = ns_pitch(MP);
+    constexpr int PU = ns_pitch(D);
+    // X, W, T (MP x MP each, pitch P); after the iteration U's value columns (MP x D, pitch PU)
+    // reuse the space from W on.
+    constexpr int LDSN = (3 * MP * P > MP * P + MP * PU) ? 3 * MP * P : MP * P + MP * PU;
     __shared__ double lds[LDSN];
-    __shared__ double sred[2 * MP];
+    __shared__ double sred[4];
+    __shared__ double su1[MP];
+    __shared__ double svb[256];
     __shared__ double sc;
     double* sX = lds;
-    double* sW = lds + MP * MP;
-    double* sT = lds + 2 * MP * MP;
+    double* sW = lds + MP * P;
+    double* sT = lds + 2 * MP * P;
     const int h = blockIdx.x, tid = threadIdx.x;
     const float* q = qt + (size_t)h * m * D;
     const float* k = kt + (size_t)h * m * D;
 
-    for (int e = tid; e < MP * MP; e += 256) {
-        const int a = e / MP, b = e % MP;
-        double w = 0.0;
-        if (a < m && b < m) {
-            double dist = 0.0;
-            for (int c = 0; c < D; ++c) dist += fabs((double)q[a * D + c] - (double)k[b * D + c]);
-            w = exp(-dist / lambda);
-            if (a == b) w += eps;
-        }
-        sW[e] = w;
-    }
+    const size_t mm = (size_t)MP * MP;
+    double* Xh = Xs + (size_t)h * (store_all ? (T + 2) : 1) * mm;
+    ns_kll<MP, D, P>(q, k, sW, reinterpret_cast<float*>(sT), m, lambda, eps);
     __syncthreads();
-    if (tid < MP) {
-        double cs = 0.0, rsum = 0.0;
-        for (int a = 0; a < MP; ++a) cs += fabs(sW[a * MP + tid]);
-        for (int b = 0; b < MP; ++b) rsum += fabs(sW[tid * MP + b]);
-        sred[tid] = cs;
-        sred[MP + tid] = rsum;
+    if (store_all)
+        for (int e = tid; e < MP * MP; e += 256) Xh[(size_t)(T + 1) * mm + e] = sW[(e / MP) * P + e % MP];
+    // column sums (threads 0..MP-1) and row sums (MP..2MP-1) of |W|, each in index order, then
+    // the first maximising column b* and row a* by a lane butterfly
+    if (tid < 2 * MP) {
+        const int idx = tid % MP;
+        double s = 0.0;
+        if (tid < MP) {
+#pragma unroll 16
+            for (int a = 0; a < MP; ++a) s += fabs(sW[a * P + idx]);
+        } else {
+#pragma unroll 16
+            for (int b = 0; b < MP; ++b) s += fabs(sW[idx * P + b]);
+        }
+        double v = isnan(s) ? -1.0 : s;
+        int arg = idx;
+        ns_group_argmax<MP>(v, arg);
+        if (idx == 0) {
+            sred[tid < MP ? 0 : 2] = v;
+            sred[tid < MP ? 1 : 3] = (double)arg;
+        }
     }
     __syncthreads();
     if (tid == 0) {
-        double n1 = -1.0, ninf = -1.0;
-        int bs = 0, as = 0;
-        for (int b = 0; b < MP; ++b)
-            if (sred[b] > n1) { n1 = sred[b]; bs = b; }
-        for (int a = 0; a < MP; ++a)
-            if (sred[MP + a] > ninf) { ninf = sred[MP + a]; as = a; }
+        const double n1 = sred[0], ninf = sred[2];
+        const int bs = (int)sred[1], as = (int)sred[3];
         const double c = n1 * ninf;
         sc = c;
         cinfo[h * 4 + 0] = c;
@@ -212,63 +201,102 @@ __global__ __launch_bounds__(256) void ns_solve_kernel(const float* __restrict__
     }
     __syncthreads();
     const double c = sc;
-    const size_t mm = (size_t)MP * MP;
-    double* Xh = Xs + (size_t)h * (store_all ? (T + 1) : 1) * mm;
     for (int e = tid; e < MP * MP; e += 256) {
         const int a = e / MP, b = e % MP;
-        const double x = (c > 0.0) ? sW[b * MP + a] / c : 0.0;
-        sX[e] = x;
+        const double x = (c > 0.0) ? sW[b * P + a] / c : 0.0;
+        sX[a * P + b] = x;
         if (store_all) Xh[e] = x;
     }
     __syncthreads();
-    const int br = tid / 16, bc = tid % 16;
     for (int t = 0; t < T; ++t) {
-        double r[RB][RB];
-        mm_block<MP, false, false>(sW, sX, r);            // W X
+        f64x4_t r[SQ::NT];
+        ns_mm<MP, MP, MP, false, false, P, P>(sW, sX, r);      // W X
 #pragma unroll
-        for (int i = 0; i < RB; ++i)
+        for (int i = 0; i < SQ::NT; ++i)
 #pragma unroll
-            for (int j = 0; j < RB; ++j) {
-                const int a = RB * br + i, b = RB * bc + j;
-                sT[a * MP + b] = (a == b ? 2.0 : 0.0) - r[i][j];
+            for (int j = 0; j < 4; ++j) {
+                const int a = SQ::row(i, j), b = SQ::col(i);
+                sT[a * P + b] = (a == b ? 2.0 : 0.0) - r[i][j];
             }
         __syncthreads();
-        mm_block<MP, false, false>(sX, sT, r);            // X (2I - W X)
+        ns_mm<MP, MP, MP, false, false, P, P>(sX, sT, r);      // X (2I - W X)
         __syncthreads();
 #pragma unroll
-        for (int i = 0; i < RB; ++i)
+        for (int i = 0; i < SQ::NT; ++i)
 #pragma unroll
-            for (int j = 0; j < RB; ++j) {
-                const int a = RB * br + i, b = RB * bc + j;
-                sX[a * MP + b] = r[i][j];
+            for (int j = 0; j < 4; ++j) {
+                const int a = SQ::row(i, j), b = SQ::col(i);
+                sX[a * P + b] = r[i][j];
                 if (store_all) Xh[(size_t)(t + 1) * mm + a * MP + b] = r[i][j];
             }
         __syncthreads();
     }
     if (!store_all)
-        for (int e = tid; e < MP * MP; e += 256) Xh[e] = sX[e];
+        for (int e = tid; e < MP * MP; e += 256) Xh[e] = sX[(e / MP) * P + e % MP];
 
-    // U = sum over key chunks (fixed order), kept in fp64 from the W region on.
+    // U = sum over key chunks (in chunk order) in fp64: value columns from the W region on, the
+    // ones column in su1.  Each thread's entries are loaded together, chunk by chunk.
     double* sU = sW;
-    for (int e = tid; e < MP * D1; e += 256) {
-        const int a = e / D1;
-        double u = 0.0;
-        if (a < m)
-            for (int ch = 0; ch < nkc; ++ch) u += (double)Upart[(((size_t)h * nkc + ch) * m) * D1 + e];
-        sU[e] = u;
-        if (a < m) U[(size_t)h * m * D1 + e] = (float)u;
+    {
+        constexpr int NE = (MP * D1 + 255) / 256;
+        double u[NE];
+#pragma unroll
+        for (int r = 0; r < NE; ++r) u[r] = 0.0;
+        const int lim = m * D1 - 1;
+#pragma unroll 4
+        for (int ch = 0; ch < nkc; ++ch) {
+            const float* up = Upart + ((size_t)h * nkc + ch) * m * D1;
+#pragma unroll
+            for (int r = 0; r < NE; ++r) {
+                const int e = tid + 256 * r;
+                const float v = up[min(e, lim)];
+                u[r] += (e <= lim) ? (double)v : 0.0;
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < NE; ++r) {
+            const int e = tid + 256 * r;
+            if (e < MP * D1) {
+                const int a = e / D1, cc = e % D1;
+                if (cc < D) sU[a * PU + cc] = u[r];
+                else su1[a] = u[r];
+                if (a < m) U[(size_t)h * m * D1 + e] = (float)u[r];
+            }
+        }
     }
     __syncthreads();
-    for (int e = tid; e < m * D1; e += 256) {
-        const int a = e / D1, cc = e % D1;
-        double s = 0.0;
-        for (int b = 0; b < m; ++b) s += sX[a * MP + b] * sU[b * D1 + cc];
-        M[(size_t)h * m * D1 + e] = (float)s;
+    {
+        f64x4_t r[SU::NT];
+        ns_mm<MP, D, MP, false, false, P, PU>(sX, sU, r);     // X_T U (value columns)
+#pragma unroll
+        for (int i = 0; i < SU::NT; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int a = SU::row(i, j), cc = SU::col(i);
+                if (a < m) M[((size_t)h * m + a) * D1 + cc] = (float)r[i][j];
+            }
     }
-    for (int cc = tid; cc < D; cc += 256) {
+    if (tid < m) {
         double s = 0.0;
-        for (int l = 0; l < m; ++l) s += vseg[((size_t)h * m + l) * D + cc];
-        vbar[(size_t)h * D + cc] = (float)(s / n);
+#pragma unroll 16
+        for (int b = 0; b < MP; ++b) s += sX[tid * P + b] * su1[b];
+        M[((size_t)h * m + tid) * D1 + D] = (float)s;
+    }
+    // vbar = (sum of the segment value sums) / n: 256 / D partial sums per column, then in order
+    {
+        constexpr int G = 256 / D;
+        const int g = tid / D, cc = tid % D;
+        double s = 0.0;
+#pragma unroll 4
+        for (int l = g; l < m; l += G) s += vseg[((size_t)h * m + l) * D + cc];
+        svb[tid] = s;
+        __syncthreads();
+        if (tid < D) {
+            double t = 0.0;
+#pragma unroll
+            for (int gg = 0; gg < G; ++gg) t += svb[gg * D + tid];
+            vbar[(size_t)h * D + tid] = (float)(t / n);
+        }
     }
 }
 

@@ -83,7 +83,7 @@ Plan make_plan(int BH, int n, int d, int m, int T, bool bwd) {
     p.kt = c.take(bh * m * d * f);
     p.vseg = c.take(bh * m * d * g);
     p.Upart = c.take(bh * p.nkc * m * d1 * f);
-    p.Xs = c.take(bh * (bwd ? (size_t)T + 1 : 1) * mpp * g);
+    p.Xs = c.take(bh * (bwd ? (size_t)T + 2 : 1) * mpp * g);   // X_0..X_T and W for the backward
     p.cinfo = c.take(bh * 4 * g);
     p.U = c.take(bh * m * d1 * f);
     p.M = c.take(bh * m * d1 * f);

@@ -52,76 +52,149 @@ __global__ __launch_bounds__(256) void pool_kernel(const typename elem<DT>::type
 }
 
 // ------------------------------------------------------------------------------------------
-// Key-side summary.  grid (nkc, BH), 256 threads.  Each block walks its chunk of keys in
-// tiles of 64: thread (jl, g) evaluates k(qt_a, k_j) for key jl of the tile and landmarks
-// 16g..16g+15 into LDS, then every thread accumulates its share of the m x (d+1) product
-// with the value tile.  Rows a >= m are zero.
-template <int DT, int D>
-__global__ __launch_bounds__(256) void key_summary_kernel(const typename elem<DT>::type* __restrict__ K,
-                                                          const typename elem<DT>::type* __restrict__ V,
-                                                          const float* __restrict__ qt,
-                                                          float* __restrict__ Upart, int n, int m,
-                                                          float kscale, int chunk_keys, int nkc) {
-    constexpr int TJ = 64;
+// Key-side summary (fp32 inputs).  grid (nkc, BH), 256 threads; block `chunk` covers keys
+// [chunk * chunk_keys, ...) in tiles of 64, one tile per wave at a time (lane = key j).
+//   Per tile: the key row in registers; for every landmark a, the L1 distance to qt_a -- the
+//   landmark row is wave-uniform and comes through scalar registers, 32 coordinates at a time,
+//   each unit's loads issued right after the first use of the previous one -- and
+//   B_aj = exp2(dist * kscale) into the wave's LDS tile [a][j]; then U_part[a][c] +=
+//   sum_j B_aj [V_j | 1]_c on fp32 MFMA 16x16x4 (A = B from LDS, B = value rows straight from
+//   global memory, loaded before the landmark loop; the ones column is column 0 of the last
+//   column tile).  At the end the four waves' partials are added in a fixed order.
+// Writes Upart[h][chunk][a][c] for a < m, c <= d.
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+// 32 consecutive floats of a wave-uniform row (scalar loads).
+__device__ __forceinline__ void srow32(float (&t)[32], const float* __restrict__ p) {
+#pragma unroll
+    for (int c = 0; c < 32; ++c) t[c] = p[c];
+}
+
+// acc + sum_c |t_c - x_c| over 32 coordinates (t in scalar registers); the loads of the next
+// unit into `nt` are issued after the first use of `t`.
+__device__ __forceinline__ float l1_unit(const float* x, const float (&t)[32], float (&nt)[32],
+                                         const float* __restrict__ next, float acc) {
+    float a0 = acc + fabsf(t[0] - x[0]);
+    __builtin_amdgcn_sched_barrier(0);
+    srow32(nt, next);
+    __builtin_amdgcn_sched_barrier(0);
+    float a1 = fabsf(t[1] - x[1]);
+#pragma unroll
+    for (int c = 2; c < 32; c += 2) {
+        a0 += fabsf(t[c] - x[c]);
+        a1 += fabsf(t[c + 1] - x[c + 1]);
+    }
+    return a0 + a1;
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void key_summary_kernel(const float* __restrict__ K, const float* __restrict__ V,
+                                                          const float* __restrict__ qt, float* __restrict__ Upart,
+                                                          int n, int m, float kscale, int chunk_keys, int nkc) {
     constexpr int D1 = D + 1;
-    constexpr int NO = (64 * D1 + 255) / 256;
-    const int chunk = blockIdx.x, h = blockIdx.y, tid = threadIdx.x;
-    __shared__ float sQ[64 * D];
-    __shared__ float sB[64][TJ + 1];
-    __shared__ float sV[TJ][D + 1];
-    for (int e = tid; e < 64 * D; e += 256) sQ[e] = (e < m * D) ? qt[(size_t)h * m * D + e] : 0.f;
+    constexpr int NCH = D / 32;            // 32-coordinate units per landmark row
+    constexpr int CT = D / 16 + 1;         // MFMA column tiles: the values, then the ones column
+    constexpr int BP = 68;                 // LDS pitch of a wave's B tile (conflict-free reads)
+    constexpr int RP = 16 * CT;            // pitch of the partial being reduced
+    __shared__ __attribute__((aligned(16))) float lds[4 * 64 * BP];
+    const int chunk = blockIdx.x, h = blockIdx.y;
+    const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, li = l & 15, lk = l >> 4;
+    float* sB = lds + w * 64 * BP;
+    const float* tab = qt + (size_t)h * m * D;
+    const int units = m * NCH;
+    for (int a = m; a < 64; ++a) sB[a * BP + l] = 0.f;
+    f32x4_t acc[4][CT];
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) acc[rt][ct] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     const int j0 = chunk * chunk_keys, j1 = min(n, j0 + chunk_keys);
-    float acc[NO];
+    for (int jt = j0 + 64 * w; jt < j1; jt += 256) {
+        const int j = jt + l;
+        const bool live = j < n;
+        float x[D];
+        {
+            const float4* kr = reinterpret_cast<const float4*>(K + ((size_t)h * n + (live ? j : n - 1)) * D);
 #pragma unroll
-    for (int r = 0; r < NO; ++r) acc[r] = 0.f;
-    const int jl = tid & 63, g = tid >> 6;
-    for (int jt = j0; jt < j1; jt += TJ) {
-        const int nj = min(TJ, j1 - jt);
-        __syncthreads();
-        for (int e = tid; e < TJ * D; e += 256) {
-            const int r = e / D, c = e % D;
-            sV[r][c] = (r < nj) ? elem<DT>::load(V, ((size_t)h * n + jt + r) * D + c) : 0.f;
-        }
-        if (jl < nj) {
-            float kreg[D];
-#pragma unroll
-            for (int c = 0; c < D; ++c) kreg[c] = elem<DT>::load(K, ((size_t)h * n + jt + jl) * D + c);
-            for (int a = 16 * g; a < 16 * g + 16; ++a) {
-                float v = 0.f;
-                if (a < m) {
-                    float dist = 0.f;
-#pragma unroll
-                    for (int c = 0; c < D; ++c) dist += fabsf(sQ[a * D + c] - kreg[c]);
-                    v = exp2f(dist * kscale);
-                }
-                sB[a][jl] = v;
+            for (int c4 = 0; c4 < D / 4; ++c4) {
+                const float4 v = kr[c4];
+                x[4 * c4 + 0] = v.x;
+                x[4 * c4 + 1] = v.y;
+                x[4 * c4 + 2] = v.z;
+                x[4 * c4 + 3] = v.w;
             }
-        } else {
-            for (int a = 16 * g; a < 16 * g + 16; ++a) sB[a][jl] = 0.f;
         }
-        __syncthreads();
+        __builtin_amdgcn_sched_barrier(0);   // the key row's loads go first: waited for first
+        // value operands of the tile's 16 k-steps (rows jt + 4s + lk, clamped to the last key)
+        float bv[16][CT - 1];
 #pragma unroll
-        for (int r = 0; r < NO; ++r) {
-            const int o = tid + 256 * r;
-            if (o < 64 * D1) {
-                const int a = o / D1, c = o % D1;
-                float s = 0.f;
-                if (c < D) {
-                    for (int j = 0; j < TJ; ++j) s += sB[a][j] * sV[j][c];
-                } else {
-                    for (int j = 0; j < TJ; ++j) s += sB[a][j];
+        for (int s = 0; s < 16; ++s) {
+            const int r = min(jt + 4 * s + lk, n - 1);
+#pragma unroll
+            for (int ct = 0; ct < CT - 1; ++ct)
+                bv[s][ct] = V[((size_t)h * n + r) * D + 16 * ct + li];
+        }
+        // landmark loop: unit u = (a, 32-coordinate part) of the table, two units per pass in
+        // alternating buffers; both units of a pass always run (a surplus unit past the table
+        // repeats the last one and stores a zero row), so that each prefetch stays where it is
+        // issued
+        {
+            float ta[32], tb[32];
+            srow32(ta, tab);
+            float dist = 0.f;
+            for (int u = 0; u < units; u += 2) {
+                dist = l1_unit(x + 32 * (u % NCH), ta, tb, tab + 32 * min(u + 1, units - 1), dist);
+                if (NCH == 1) {
+                    sB[u * BP + l] = live ? __builtin_amdgcn_exp2f(dist * kscale) : 0.f;
+                    dist = 0.f;
                 }
-                acc[r] += s;
+                dist = l1_unit(x + 32 * ((u + 1) % NCH), tb, ta, tab + 32 * min(u + 2, units - 1), dist);
+                const int a = (u + 1) / NCH;   // < 64; a == m only past the table (zero row)
+                sB[a * BP + l] = (live && a < m) ? __builtin_amdgcn_exp2f(dist * kscale) : 0.f;
+                dist = 0.f;
             }
+            // the last prefetch is consumed here, so that no prefetch is moved next to its use
+            asm volatile("" ::"s"(ta[0]), "s"(ta[16]));
+        }
+        __builtin_amdgcn_wave_barrier();
+        // U_part += B [V | 1] over the tile's 64 keys, one 16-row tile of landmarks at a time
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt) {
+            if (16 * rt < m) {
+#pragma unroll
+                for (int s = 0; s < 16; ++s) {
+                    const float av = sB[(16 * rt + li) * BP + 4 * s + lk];
+#pragma unroll
+                    for (int ct = 0; ct < CT - 1; ++ct)
+                        acc[rt][ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv[s][ct], acc[rt][ct], 0, 0, 0);
+                    acc[rt][CT - 1] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, li == 0 ? 1.f : 0.f, acc[rt][CT - 1],
+                                                                             0, 0, 0);
+                }
+            }
+        }
+        __builtin_amdgcn_wave_barrier();
+    }
+    // partials of waves 3, 2, 1, 0 added in that order into one [64][RP] buffer; result register
+    // r of a 16x16x4 tile at lane l is row 4 (l / 16) + r, column l % 16
+    float* red = lds;
+    for (int ww = 3; ww >= 0; --ww) {
+        __syncthreads();
+        if (w == ww) {
+#pragma unroll
+            for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+                for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        float* p = red + (16 * rt + 4 * lk + r) * RP + 16 * ct + li;
+                        *p = (ww == 3) ? acc[rt][ct][r] : *p + acc[rt][ct][r];
+                    }
         }
     }
-#pragma unroll
-    for (int r = 0; r < NO; ++r) {
-        const int o = tid + 256 * r;
-        if (o < 64 * D1) {
-            const int a = o / D1, c = o % D1;
-            if (a < m) Upart[(((size_t)h * nkc + chunk) * m + a) * D1 + c] = acc[r];
-        }
+    __syncthreads();
+    for (int e = tid; e < m * D1; e += 256) {
+        const int a = e / D1, c = e % D1;
+        Upart[(((size_t)h * nkc + chunk) * m + a) * D1 + c] = red[a * RP + c];
     }
 }
 
@@ -363,21 +436,16 @@ hipError_t launch_pool(int dt, const void* Q, const void* K, const void* V, floa
     return hipGetLastError();
 }
 
-template <int DT, int D>
-static void key_summary_launch(const void* K, const void* V, const float* qt, float* Upart, int BH, int n, int m,
-                               float kscale, int chunk_keys, int nkc, hipStream_t st) {
-    using T = typename elem<DT>::type;
-    hipLaunchKernelGGL((key_summary_kernel<DT, D>), dim3(nkc, BH), dim3(256), 0, st, (const T*)K, (const T*)V, qt,
-                       Upart, n, m, kscale, chunk_keys, nkc);
-}
-
 hipError_t launch_key_summary(int dt, const void* K, const void* V, const float* qt, float* Upart, int BH, int n,
                               int d, int m, float lambda, int chunk_keys, int nkc, hipStream_t st) {
+    if (dt != DT_F32) return hipErrorInvalidValue;   // bf16 inputs take the fast path
     const float ks = kscale_of(lambda);
-    if (dt == DT_F32 && d == 32) key_summary_launch<DT_F32, 32>(K, V, qt, Upart, BH, n, m, ks, chunk_keys, nkc, st);
-    else if (dt == DT_F32) key_summary_launch<DT_F32, 64>(K, V, qt, Upart, BH, n, m, ks, chunk_keys, nkc, st);
-    else if (d == 32) key_summary_launch<DT_BF16, 32>(K, V, qt, Upart, BH, n, m, ks, chunk_keys, nkc, st);
-    else key_summary_launch<DT_BF16, 64>(K, V, qt, Upart, BH, n, m, ks, chunk_keys, nkc, st);
+    if (d == 32)
+        hipLaunchKernelGGL((key_summary_kernel<32>), dim3(nkc, BH), dim3(256), 0, st, (const float*)K,
+                           (const float*)V, qt, Upart, n, m, ks, chunk_keys, nkc);
+    else
+        hipLaunchKernelGGL((key_summary_kernel<64>), dim3(nkc, BH), dim3(256), 0, st, (const float*)K,
+                           (const float*)V, qt, Upart, n, m, ks, chunk_keys, nkc);
     return hipGetLastError();
 }
 

@@ -15,7 +15,7 @@ namespace {
 
 constexpr int kMaxM = 64;
 constexpr int kMaxT = 64;
-constexpr int kKeyChunk = 512;   // keys per block of the key-summary kernel
+constexpr int kKeyChunk = 1024;  // keys per block of the key-summary kernel (four 64-key tiles per wave)
 constexpr int kLmChunk = 64;     // tokens per block of the landmark-major backward passes
 
 // ------------------------------------------------------------------------------- validation

@@ -14,13 +14,22 @@
 #include "common.hpp"
 #include "kernels.hpp"
 #include "ns_mfma.hpp"
+#include "srows.hpp"
 
 namespace lapattn {
 
 static inline float kscale_of(float lambda) { return (float)(-1.4426950408889634 / (double)lambda); }
 
 // ------------------------------------------------------------------------------------------
-// Query-major pass.  grid (nqb, BH), one query per thread.
+// Query-major pass.  grid (nqb, BH), 256 threads, lane = query (wave w of block b covers
+// queries 256 b + 64 w ..).  Landmark rows of kt come through scalar registers (srows.hpp),
+// the rows of M are LDS broadcasts.
+//   Pass 1: a_il = k(q_i, kt_l) into the wave's [query][landmark] LDS tile, s_i (and y_i for
+//           the row-sum normalisation); rs, dYd; the tile leaves as whole rows of Aq.
+//   Pass 2: dA_il = rs_i dO_i . M_l[:d] + dYd_i M_l[d], dD_il = -a_il dA_il / lambda (back into
+//           the tile, then whole rows of dDq), dq_i += dD_il sign(q_i - kt_l).
+//   dvbar partial (inline normalisation): sum over the block's queries of (1 - s_i) dO_i,
+//   per wave through the tile, then over the waves in order.
 template <int D, int NORM>
 __global__ __launch_bounds__(256) void bwd_query_kernel(const float* __restrict__ Q, const float* __restrict__ dO,
                                                         float* __restrict__ dQ, const float* __restrict__ kt,
@@ -30,90 +39,185 @@ __global__ __launch_bounds__(256) void bwd_query_kernel(const float* __restrict_
                                                         float* __restrict__ dvbar_part, int n, int m,
                                                         float kscale, float inv_lambda, int nqb) {
     constexpr int D1 = D + 1;
-    __shared__ float sK[64 * D];
-    __shared__ float sM[64 * D1];
+    constexpr int NCH = D / 32;
+    constexpr int TP = 65;                 // tile pitch: lane-strided accesses are conflict-free
+    __shared__ __attribute__((aligned(16))) float sM[64 * D1];
     __shared__ float sVb[D];
-    __shared__ float sred[256];
-    const int h = blockIdx.y, tid = threadIdx.x;
-    for (int e = tid; e < m * D; e += 256) sK[e] = kt[(size_t)h * m * D + e];
-    for (int e = tid; e < m * D1; e += 256) sM[e] = M[(size_t)h * m * D1 + e];
+    __shared__ float sT[4 * 64 * TP];
+    __shared__ float sred[4 * D];
+    const int h = blockIdx.y, tid = threadIdx.x, w = tid >> 6, l = tid & 63;
+    for (int e = tid; e < 64 * D1; e += 256) sM[e] = (e < m * D1) ? M[(size_t)h * m * D1 + e] : 0.f;
     if (tid < D) sVb[tid] = vbar[(size_t)h * D + tid];
-    __syncthreads();
-    const int i = blockIdx.x * 256 + tid;
+    float* tile = sT + w * 64 * TP;
+    const int i0 = blockIdx.x * 256 + w * 64;
+    const int i = i0 + l;
     const bool live = i < n;
-    const size_t row = ((size_t)h * n + (live ? i : 0)) * D;
+    const size_t row = ((size_t)h * n + (live ? i : n - 1)) * D;
     float q[D], g[D];
-    float s = 0.f, rsc = 1.f, dyd = 0.f;
+#pragma unroll
+    for (int c4 = 0; c4 < D / 4; ++c4) {
+        const float4 a = reinterpret_cast<const float4*>(Q + row)[c4];
+        const float4 b = reinterpret_cast<const float4*>(dO + row)[c4];
+        q[4 * c4 + 0] = a.x; q[4 * c4 + 1] = a.y; q[4 * c4 + 2] = a.z; q[4 * c4 + 3] = a.w;
+        g[4 * c4 + 0] = b.x; g[4 * c4 + 1] = b.y; g[4 * c4 + 2] = b.z; g[4 * c4 + 3] = b.w;
+    }
+    __syncthreads();   // sM, sVb
+    const float* tab = kt + (size_t)h * m * D;
+    const int units = m * NCH;
+
+    // pass 1 (a landmark column a >= m, reached only past the table, holds zeros)
+    float s = 0.f;
+    float y[NORM == NORM_ROWSUM ? D : 1];
+#pragma unroll
+    for (int c = 0; c < (NORM == NORM_ROWSUM ? D : 1); ++c) y[c] = 0.f;
+    auto emit = [&](int a, float dist) {
+        const float av = (live && a < m) ? __builtin_amdgcn_exp2f(dist * kscale) : 0.f;
+        tile[l * TP + a] = av;
+        s = fmaf(av, sM[a * D1 + D], s);
+        if (NORM == NORM_ROWSUM) {
+#pragma unroll
+            for (int c = 0; c < D; ++c) y[c] = fmaf(av, sM[a * D1 + c], y[c]);
+        }
+    };
+    {
+        float ta[32], tb[32];
+        srow32(ta, tab);
+        float dist = 0.f;
+        for (int u = 0; u < units; u += 2) {
+            dist = l1_unit(q + 32 * (u % NCH), ta, tb, tab + 32 * min(u + 1, units - 1), dist);
+            if (NCH == 1) {
+                emit(u, dist);
+                dist = 0.f;
+            }
+            dist = l1_unit(q + 32 * ((u + 1) % NCH), tb, ta, tab + 32 * min(u + 2, units - 1), dist);
+            emit((u + 1) / NCH, dist);
+            dist = 0.f;
+        }
+        asm volatile("" ::"s"(ta[0]), "s"(ta[16]));
+    }
+    float rsc = 1.f, dyd = 0.f;
+    if (NORM == NORM_INLINE) {
+        float t = 0.f;
+#pragma unroll
+        for (int c = 0; c < D; ++c) t = fmaf(g[c], sVb[c], t);
+        dyd = -t;
+    } else if (NORM == NORM_ROWSUM) {
+        float t = 0.f;
+#pragma unroll
+        for (int c = 0; c < D; ++c) t = fmaf(g[c], y[c], t);
+        rsc = 1.f / s;
+        dyd = -t / (s * s);
+    }
     if (live) {
-#pragma unroll
-        for (int c = 0; c < D; ++c) { q[c] = Q[row + c]; g[c] = dO[row + c]; }
-        // forward recompute of y (only what the normalisation backward needs)
-        float y[D1];
-#pragma unroll
-        for (int c = 0; c < D1; ++c) y[c] = 0.f;
-        for (int l = 0; l < m; ++l) {
-            float dist = 0.f;
-#pragma unroll
-            for (int c = 0; c < D; ++c) dist += fabsf(q[c] - sK[l * D + c]);
-            const float a = exp2f(dist * kscale);
-#pragma unroll
-            for (int c = 0; c < D1; ++c) y[c] = fmaf(a, sM[l * D1 + c], y[c]);
-        }
-        s = y[D];
-        if (NORM == NORM_INLINE) {
-            float t = 0.f;
-#pragma unroll
-            for (int c = 0; c < D; ++c) t = fmaf(g[c], sVb[c], t);
-            dyd = -t;
-        } else if (NORM == NORM_ROWSUM) {
-            float t = 0.f;
-#pragma unroll
-            for (int c = 0; c < D; ++c) t = fmaf(g[c], y[c], t);
-            rsc = 1.f / s;
-            dyd = -t / (s * s);
-        }
         rs[(size_t)h * n + i] = rsc;
         dYd[(size_t)h * n + i] = dyd;
     }
-    // dvbar partial (inline only): sum over this block's queries of (1 - s_i) dO_i, fixed order;
-    // the other normalisations do not use vbar and their partials are zero.
-    if (NORM != NORM_INLINE && tid < D) dvbar_part[((size_t)h * nqb + blockIdx.x) * D + tid] = 0.f;
-    if (NORM == NORM_INLINE) {
-        for (int c = 0; c < D; ++c) {
-            sred[tid] = live ? (1.f - s) * g[c] : 0.f;
-            __syncthreads();
-            for (int w = 128; w > 0; w >>= 1) {
-                if (tid < w) sred[tid] += sred[tid + w];
-                __syncthreads();
+    __builtin_amdgcn_wave_barrier();
+    for (int r = 0; r < 64 && i0 + r < n; ++r)
+        if (l < m) Aq[((size_t)h * n + i0 + r) * 64 + l] = tile[r * TP + l];
+    __builtin_amdgcn_wave_barrier();
+
+    // pass 2
+    float dq[D], gs[D];
+#pragma unroll
+    for (int c = 0; c < D; ++c) {
+        dq[c] = 0.f;
+        gs[c] = g[c] * rsc;
+    }
+    auto ddof = [&](int a) {
+        const float* mr = sM + a * D1;
+        float da = dyd * mr[D];
+#pragma unroll
+        for (int c = 0; c < D; ++c) da = fmaf(gs[c], mr[c], da);
+        const float dd = -tile[l * TP + a] * da * inv_lambda;
+        tile[l * TP + a] = dd;
+        return dd;
+    };
+    {
+        float ta[32], tb[32];
+        srow32(ta, tab);
+        for (int u = 0; u < units; u += 2) {
+            if (NCH == 1) {
+                const float d0 = ddof(u);
+                sgn_unit(dq, q, ta, tb, tab + 32 * min(u + 1, units - 1), d0);
+                const float d1 = ddof(u + 1);
+                sgn_unit(dq, q, tb, ta, tab + 32 * min(u + 2, units - 1), d1);
+            } else {
+                const float d0 = ddof(u / NCH);
+                sgn_unit(dq, q, ta, tb, tab + 32 * min(u + 1, units - 1), d0);
+                sgn_unit(dq + 32, q + 32, tb, ta, tab + 32 * min(u + 2, units - 1), d0);
             }
-            if (tid == 0) dvbar_part[((size_t)h * nqb + blockIdx.x) * D + c] = sred[0];
-            __syncthreads();
         }
+        asm volatile("" ::"s"(ta[0]), "s"(ta[16]));
     }
-    if (!live) return;
-    float dq[D];
+    __builtin_amdgcn_wave_barrier();
+    for (int r = 0; r < 64 && i0 + r < n; ++r)
+        if (l < m) dDq[((size_t)h * n + i0 + r) * 64 + l] = tile[r * TP + l];
+    if (live) {
 #pragma unroll
-    for (int c = 0; c < D; ++c) dq[c] = 0.f;
-    for (int l = 0; l < m; ++l) {
-        float dist = 0.f;
-#pragma unroll
-        for (int c = 0; c < D; ++c) dist += fabsf(q[c] - sK[l * D + c]);
-        const float a = exp2f(dist * kscale);
-        float da = dyd * sM[l * D1 + D];
-#pragma unroll
-        for (int c = 0; c < D; ++c) da = fmaf(g[c] * rsc, sM[l * D1 + c], da);
-        const float dd = -a * da * inv_lambda;
-        Aq[((size_t)h * n + i) * m + l] = a;
-        dDq[((size_t)h * n + i) * m + l] = dd;
-#pragma unroll
-        for (int c = 0; c < D; ++c) dq[c] = fmaf(dd, sgnf(q[c] - sK[l * D + c]), dq[c]);
+        for (int c4 = 0; c4 < D / 4; ++c4)
+            reinterpret_cast<float4*>(dQ + row)[c4] = make_float4(dq[4 * c4], dq[4 * c4 + 1], dq[4 * c4 + 2], dq[4 * c4 + 3]);
     }
+    // dvbar partial
+    if (NORM == NORM_INLINE) {
+        __builtin_amdgcn_wave_barrier();
+        const float wt = live ? 1.f - s : 0.f;
 #pragma unroll
-    for (int c = 0; c < D; ++c) dQ[row + c] = dq[c];
+        for (int c = 0; c < D; ++c) tile[l * TP + c] = wt * g[c];
+        __builtin_amdgcn_wave_barrier();
+        if (l < D) {
+            float t = 0.f;
+            for (int r = 0; r < 64; ++r) t += tile[r * TP + l];
+            sred[w * D + l] = t;
+        }
+        __syncthreads();
+        if (tid < D)
+            dvbar_part[((size_t)h * nqb + blockIdx.x) * D + tid] =
+                ((sred[tid] + sred[D + tid]) + sred[2 * D + tid]) + sred[3 * D + tid];
+    } else if (tid < D) {
+        dvbar_part[((size_t)h * nqb + blockIdx.x) * D + tid] = 0.f;
+    }
 }
 
 // ------------------------------------------------------------------------------------------
-// Landmark-major pass over queries.  grid (nlc, BH), 64 threads (lane = landmark l).
+// Direct global -> LDS copies (global_load_lds_dwordx4): each instruction moves 64 lanes x 16
+// bytes to consecutive LDS addresses.  Their completion is tracked by vmcnt alone -- the
+// compiler does not order later LDS reads after them -- so a reader waits with lds_dma_wait().
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+__device__ __forceinline__ void lds_dma16(float* lds_dst, const float* src_lane) {
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(src_lane), (lds_void_t*)(lds_dst),
+                                     16, 0, 0);
+}
+__device__ __forceinline__ void lds_dma4(float* lds_dst, const float* src_lane) {
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(src_lane), (lds_void_t*)(lds_dst),
+                                     4, 0, 0);
+}
+__device__ __forceinline__ void lds_dma_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// The rows of a [token][W] array (W floats per row, W a multiple of 4) for tokens t0 .. t0 + 15
+// (clamped to the last token) into dst[16][W].
+template <int W>
+__device__ __forceinline__ void stage_rows16(float* dst, const float* base, int t0, int n) {
+    const int l = threadIdx.x & 63;
+#pragma unroll
+    for (int k = 0; k < 16 * W / 256; ++k) {
+        const int e = 256 * k + 4 * l;
+        lds_dma16(dst + 256 * k, base + (size_t)min(t0 + e / W, n - 1) * W + e % W);
+    }
+}
+
+// ------------------------------------------------------------------------------------------
+// Landmark-major pass over queries.  grid (nlc, BH), 64 threads (lane = landmark l); block ch
+// covers queries [ch * chunk, ...) in sub-tiles of 16 whose data -- rows of Q and dO, rows of
+// Aq and dDq (pitch 64), rs and dYd -- is copied to LDS one sub-tile ahead (two buffers).  Per
+// query i:
+//   dM_l[:d] += a_il rs_i dO_i on fp32 MFMA 32x32x1 (A = a_il, lane = landmark = MFMA row; B =
+//   rs_i dO_i[32 hh + l % 32], one 32-column half per instruction), dM_l[d] += a_il dYd_i;
+//   dkt_l -= dD_il sign(q_i - kt_l).
+// Queries past the chunk contribute zeros.
+typedef float f32x32_t __attribute__((ext_vector_type(32)));
+
 template <int D>
 __global__ __launch_bounds__(64) void bwd_query_lm_kernel(const float* __restrict__ Q, const float* __restrict__ dO,
                                                           const float* __restrict__ kt, const float* __restrict__ Aq,
@@ -122,32 +226,82 @@ __global__ __launch_bounds__(64) void bwd_query_lm_kernel(const float* __restric
                                                           float* __restrict__ dkt_part, int n, int m, int chunk,
                                                           int nlc) {
     constexpr int D1 = D + 1;
+    constexpr int NH = D / 32;
+    constexpr int BUF = 16 * D + 16 * 64 + 16 * 64 + 16 * D + 64;   // Q, Aq, dDq, dO, rs | dYd
+    __shared__ __attribute__((aligned(16))) float sbuf[2 * BUF];
     const int ch = blockIdx.x, h = blockIdx.y, l = threadIdx.x;
     const bool live = l < m;
-    float k[D], dm[D1], dk[D];
-#pragma unroll
-    for (int c = 0; c < D; ++c) { k[c] = live ? kt[((size_t)h * m + l) * D + c] : 0.f; dk[c] = 0.f; }
-#pragma unroll
-    for (int c = 0; c < D1; ++c) dm[c] = 0.f;
+    const int lc = live ? l : m - 1;
+    const float* Qh = Q + (size_t)h * n * D;
+    const float* dOh = dO + (size_t)h * n * D;
+    const float* Ah = Aq + (size_t)h * n * 64;
+    const float* DDh = dDq + (size_t)h * n * 64;
     const int i0 = ch * chunk, i1 = min(n, i0 + chunk);
-    for (int i = i0; i < i1; ++i) {
-        const size_t qrow = ((size_t)h * n + i) * D;
-        const float a = live ? Aq[((size_t)h * n + i) * m + l] : 0.f;
-        const float dd = live ? dDq[((size_t)h * n + i) * m + l] : 0.f;
-        const float r = rs[(size_t)h * n + i];
+    auto stage = [&](int b, int t0) {
+        float* sb = sbuf + b * BUF;
+        stage_rows16<D>(sb, Qh, t0, n);
+        stage_rows16<64>(sb + 16 * D, Ah, t0, n);
+        stage_rows16<64>(sb + 16 * D + 16 * 64, DDh, t0, n);
+        stage_rows16<D>(sb + 16 * D + 32 * 64, dOh, t0, n);
+        const int r = min(t0 + (l & 15), n - 1);
+        lds_dma4(sb + 32 * D + 32 * 64, (l < 16 ? rs : dYd) + (size_t)h * n + r);
+    };
+    float k[D], dk[D];
 #pragma unroll
-        for (int c = 0; c < D; ++c) {
-            dm[c] = fmaf(a, dO[qrow + c] * r, dm[c]);
-            dk[c] = fmaf(-dd, sgnf(Q[qrow + c] - k[c]), dk[c]);
-        }
-        dm[D] = fmaf(a, dYd[(size_t)h * n + i], dm[D]);
+    for (int c = 0; c < D; ++c) {
+        k[c] = kt[((size_t)h * m + lc) * D + c];
+        dk[c] = 0.f;
     }
+    float dml = 0.f;
+    f32x32_t acc[NH];
+#pragma unroll
+    for (int hh = 0; hh < NH; ++hh)
+#pragma unroll
+        for (int r = 0; r < 32; ++r) acc[hh][r] = 0.f;
+    if (i0 < i1) stage(0, i0);
+    int buf = 0;
+    for (int t0 = i0; t0 < i1; t0 += 16, buf ^= 1) {
+        lds_dma_wait();
+        __builtin_amdgcn_wave_barrier();
+        if (t0 + 16 < i1) stage(buf ^ 1, t0 + 16);
+        const float* sb = sbuf + buf * BUF;
+        const float* sQ = sb;
+        const float* sA = sb + 16 * D;
+        const float* sDD = sA + 16 * 64;
+        const float* sdO = sDD + 16 * 64;
+        const float* sRY = sdO + 16 * D;
+#pragma unroll 4
+        for (int r = 0; r < 16; ++r) {
+            const bool in = live && t0 + r < i1;
+            const float av = sA[r * 64 + lc], ddv = sDD[r * 64 + lc];   // unconditional reads
+            const float a = in ? av : 0.f;
+            const float dd = in ? ddv : 0.f;
+            const float rsi = sRY[r], ydi = sRY[16 + r];
+#pragma unroll
+            for (int hh = 0; hh < NH; ++hh)
+                acc[hh] = __builtin_amdgcn_mfma_f32_32x32x1f32(a, sdO[r * D + 32 * hh + (l & 31)] * rsi, acc[hh], 0, 0, 0);
+            dml = fmaf(a, ydi, dml);
+            const float* qr = sQ + r * D;
+            const float dds = -dd * 0x1p64f;
+#pragma unroll
+            for (int c = 0; c < D; ++c) dk[c] = fmaf(dds, sgn_term(qr[c], k[c]), dk[c]);
+        }
+        __builtin_amdgcn_wave_barrier();
+    }
+    // result register r of the 32x32x1 product: landmark 32 (r / 16) + 8 ((r % 16) / 4) + 4 (l / 32)
+    // + r % 4, column 32 hh + l % 32
+    const size_t o = ((size_t)h * nlc + ch) * m;
+#pragma unroll
+    for (int hh = 0; hh < NH; ++hh)
+#pragma unroll
+        for (int r = 0; r < 32; ++r) {
+            const int lm = 32 * (r / 16) + 8 * ((r % 16) / 4) + 4 * (l / 32) + r % 4;
+            if (lm < m) dM_part[(o + lm) * D1 + 32 * hh + (l & 31)] = acc[hh][r];
+        }
     if (!live) return;
-    const size_t o = ((size_t)h * nlc + ch) * m + l;
+    dM_part[(o + l) * D1 + D] = dml;
 #pragma unroll
-    for (int c = 0; c < D1; ++c) dM_part[o * D1 + c] = dm[c];
-#pragma unroll
-    for (int c = 0; c < D; ++c) dkt_part[o * D + c] = dk[c];
+    for (int c = 0; c < D; ++c) dkt_part[(o + l) * D + c] = dk[c];
 }
 
 // ------------------------------------------------------------------------------------------
@@ -393,7 +547,15 @@ __global__ __launch_bounds__(256) void bwd_ns_kernel(const float* __restrict__ q
 }
 
 // ------------------------------------------------------------------------------------------
-// Key-major pass.  grid (ceil(n/256), BH), one key per thread.
+// Key-major pass.  grid (ceil(n/256), BH), 256 threads, lane = key (wave w of block b covers
+// keys 256 b + 64 w ..).  Landmark rows of qt come through scalar registers (srows.hpp), the
+// rows of dU are LDS broadcasts.  Per landmark a:
+//   B_aj = k(qt_a, k_j);  dB_aj = dU_a[:d] . v_j + dU_a[d];  dV_j += B_aj dU_a[:d];
+//   dD_aj = -B_aj dB_aj / lambda (into the wave's [key][landmark] LDS tile, which leaves as
+//   whole rows of dDk);  dK_j -= dD_aj sign(qt_a - k_j).
+// A landmark row is streamed once for the distance and once for the signs (the table is small
+// and stays in cache); -dD sign(qt_a - k_j) is accumulated as dD sign(k_j - qt_a).  dV_j gets
+// dvbar / n at the end.
 template <int D>
 __global__ __launch_bounds__(256) void bwd_key_kernel(const float* __restrict__ K, const float* __restrict__ V,
                                                       float* __restrict__ dK, float* __restrict__ dV,
@@ -401,61 +563,132 @@ __global__ __launch_bounds__(256) void bwd_key_kernel(const float* __restrict__ 
                                                       const float* __restrict__ dvbar, float* __restrict__ dDk,
                                                       int n, int m, float kscale, float inv_lambda) {
     constexpr int D1 = D + 1;
-    __shared__ float sQ[64 * D];
-    __shared__ float sdU[64 * D1];
+    constexpr int NCH = D / 32;
+    constexpr int TP = 65;
+    __shared__ __attribute__((aligned(16))) float sdU[64 * D1];
     __shared__ float sdv[D];
-    const int h = blockIdx.y, tid = threadIdx.x;
-    for (int e = tid; e < m * D; e += 256) sQ[e] = qt[(size_t)h * m * D + e];
-    for (int e = tid; e < m * D1; e += 256) sdU[e] = dU[(size_t)h * m * D1 + e];
+    __shared__ float sT[4 * 64 * TP];
+    const int h = blockIdx.y, tid = threadIdx.x, w = tid >> 6, l = tid & 63;
+    for (int e = tid; e < 64 * D1; e += 256) sdU[e] = (e < m * D1) ? dU[(size_t)h * m * D1 + e] : 0.f;
     if (tid < D) sdv[tid] = dvbar[(size_t)h * D + tid];
-    __syncthreads();
-    const int j = blockIdx.x * 256 + tid;
-    if (j >= n) return;
-    const size_t row = ((size_t)h * n + j) * D;
+    float* tile = sT + w * 64 * TP;
+    const int j0 = blockIdx.x * 256 + w * 64;
+    const int j = j0 + l;
+    const bool live = j < n;
+    const size_t row = ((size_t)h * n + (live ? j : n - 1)) * D;
     float kk[D], v[D], dk[D], dv[D];
 #pragma unroll
-    for (int c = 0; c < D; ++c) { kk[c] = K[row + c]; v[c] = V[row + c]; dk[c] = 0.f; dv[c] = 0.f; }
-    for (int a = 0; a < m; ++a) {
-        float dist = 0.f;
-#pragma unroll
-        for (int c = 0; c < D; ++c) dist += fabsf(sQ[a * D + c] - kk[c]);
-        const float b = exp2f(dist * kscale);
-        float db = sdU[a * D1 + D];
-#pragma unroll
-        for (int c = 0; c < D; ++c) {
-            db = fmaf(sdU[a * D1 + c], v[c], db);
-            dv[c] = fmaf(b, sdU[a * D1 + c], dv[c]);
-        }
-        const float dd = -b * db * inv_lambda;
-        dDk[((size_t)h * n + j) * m + a] = dd;
-#pragma unroll
-        for (int c = 0; c < D; ++c) dk[c] = fmaf(-dd, sgnf(sQ[a * D + c] - kk[c]), dk[c]);
+    for (int c4 = 0; c4 < D / 4; ++c4) {
+        const float4 a = reinterpret_cast<const float4*>(K + row)[c4];
+        const float4 b = reinterpret_cast<const float4*>(V + row)[c4];
+        kk[4 * c4 + 0] = a.x; kk[4 * c4 + 1] = a.y; kk[4 * c4 + 2] = a.z; kk[4 * c4 + 3] = a.w;
+        v[4 * c4 + 0] = b.x; v[4 * c4 + 1] = b.y; v[4 * c4 + 2] = b.z; v[4 * c4 + 3] = b.w;
     }
-    const float invn = 1.f / (float)n;
 #pragma unroll
     for (int c = 0; c < D; ++c) {
-        dK[row + c] = dk[c];
-        dV[row + c] = dv[c] + sdv[c] * invn;
+        dk[c] = 0.f;
+        dv[c] = 0.f;
+    }
+    __syncthreads();   // sdU, sdv
+    const float* tab = qt + (size_t)h * m * D;
+    // per landmark: B, dB, dV and dD (a landmark a == m, reached only past the table on the
+    // last pass, gets B = 0)
+    auto step = [&](int a, float dist) {
+        const float b = (live && a < m) ? __builtin_amdgcn_exp2f(dist * kscale) : 0.f;
+        const float* ur = sdU + a * D1;
+        float db = ur[D];
+#pragma unroll
+        for (int c = 0; c < D; ++c) {
+            db = fmaf(ur[c], v[c], db);
+            dv[c] = fmaf(b, ur[c], dv[c]);
+        }
+        const float dd = -b * db * inv_lambda;
+        tile[l * TP + a] = dd;
+        return dd;
+    };
+    {
+        float ta[32], tb[32];
+        srow32(ta, tab);
+        if (NCH == 1) {
+            // landmark a in ta, a + 1 in tb; each row serves its distance and then its signs
+            for (int a = 0; a < m; a += 2) {
+                float dd = step(a, l1_unit(kk, ta, tb, tab + 32 * min(a + 1, m - 1), 0.f));
+                sgn_unit_nopf(dk, kk, ta, dd);
+                dd = step(a + 1, l1_unit(kk, tb, ta, tab + 32 * min(a + 2, m - 1), 0.f));
+                sgn_unit_nopf(dk, kk, tb, dd);
+            }
+        } else {
+            // units of landmark a: distance halves 0 and 1, then sign halves 0 and 1
+            for (int a = 0; a < m; ++a) {
+                const float* r0 = tab + (size_t)a * D;
+                float dist = l1_unit(kk, ta, tb, r0 + 32, 0.f);
+                dist = l1_unit(kk + 32, tb, ta, r0, dist);
+                const float dd = step(a, dist);
+                sgn_unit(dk, kk, ta, tb, r0 + 32, dd);
+                sgn_unit(dk + 32, kk + 32, tb, ta, tab + (size_t)min(a + 1, m - 1) * D, dd);
+            }
+        }
+        asm volatile("" ::"s"(ta[0]), "s"(ta[16]));
+    }
+    __builtin_amdgcn_wave_barrier();
+    for (int r = 0; r < 64 && j0 + r < n; ++r)
+        if (l < m) dDk[((size_t)h * n + j0 + r) * 64 + l] = tile[r * TP + l];
+    if (live) {
+        const float invn = 1.f / (float)n;
+#pragma unroll
+        for (int c4 = 0; c4 < D / 4; ++c4) {
+            reinterpret_cast<float4*>(dK + row)[c4] = make_float4(dk[4 * c4], dk[4 * c4 + 1], dk[4 * c4 + 2], dk[4 * c4 + 3]);
+            reinterpret_cast<float4*>(dV + row)[c4] =
+                make_float4(dv[4 * c4] + sdv[4 * c4] * invn, dv[4 * c4 + 1] + sdv[4 * c4 + 1] * invn,
+                            dv[4 * c4 + 2] + sdv[4 * c4 + 2] * invn, dv[4 * c4 + 3] + sdv[4 * c4 + 3] * invn);
+        }
     }
 }
 
 // ------------------------------------------------------------------------------------------
-// Landmark-major pass over keys.  grid (nlc, BH), 64 threads (lane = landmark a).
+// Landmark-major pass over keys.  grid (nlc, BH), 64 threads (lane = landmark a); block ch covers
+// keys [ch * chunk, ...) in sub-tiles of 16 whose rows of K and of dDk (pitch 64) are copied to
+// LDS one sub-tile ahead:  dqt_a += sum_j dD_aj sign(qt_a - k_j).
 template <int D>
 __global__ __launch_bounds__(64) void bwd_key_lm_kernel(const float* __restrict__ K, const float* __restrict__ qt,
                                                         const float* __restrict__ dDk, float* __restrict__ dqt_part,
                                                         int n, int m, int chunk, int nlc) {
+    constexpr int BUF = 16 * D + 16 * 64;
+    __shared__ __attribute__((aligned(16))) float sbuf[2 * BUF];
     const int ch = blockIdx.x, h = blockIdx.y, a = threadIdx.x;
     const bool live = a < m;
+    const int ac = live ? a : m - 1;
+    const float* Kh = K + (size_t)h * n * D;
+    const float* DDh = dDk + (size_t)h * n * 64;
     float q[D], acc[D];
 #pragma unroll
-    for (int c = 0; c < D; ++c) { q[c] = live ? qt[((size_t)h * m + a) * D + c] : 0.f; acc[c] = 0.f; }
+    for (int c = 0; c < D; ++c) {
+        q[c] = qt[((size_t)h * m + ac) * D + c];
+        acc[c] = 0.f;
+    }
     const int j0 = ch * chunk, j1 = min(n, j0 + chunk);
-    for (int j = j0; j < j1; ++j) {
-        const size_t krow = ((size_t)h * n + j) * D;
-        const float dd = live ? dDk[((size_t)h * n + j) * m + a] : 0.f;
+    auto stage = [&](int b, int t0) {
+        stage_rows16<D>(sbuf + b * BUF, Kh, t0, n);
+        stage_rows16<64>(sbuf + b * BUF + 16 * D, DDh, t0, n);
+    };
+    if (j0 < j1) stage(0, j0);
+    int buf = 0;
+    for (int t0 = j0; t0 < j1; t0 += 16, buf ^= 1) {
+        lds_dma_wait();
+        __builtin_amdgcn_wave_barrier();
+        if (t0 + 16 < j1) stage(buf ^ 1, t0 + 16);
+        const float* sK = sbuf + buf * BUF;
+        const float* sDD = sK + 16 * D;
+#pragma unroll 4
+        for (int r = 0; r < 16; ++r) {
+            const float ddv = sDD[r * 64 + ac];
+            const float dd = (live && t0 + r < j1) ? ddv : 0.f;
+            const float dds = dd * 0x1p64f;
+            const float* kr = sK + r * D;
 #pragma unroll
-        for (int c = 0; c < D; ++c) acc[c] = fmaf(dd, sgnf(q[c] - K[krow + c]), acc[c]);
+            for (int c = 0; c < D; ++c) acc[c] = fmaf(dds, sgn_term(q[c], kr[c]), acc[c]);
+        }
+        __builtin_amdgcn_wave_barrier();
     }
     if (!live) return;
     const size_t o = ((size_t)h * nlc + ch) * m + a;
@@ -464,7 +697,9 @@ __global__ __launch_bounds__(64) void bwd_key_lm_kernel(const float* __restrict_
 }
 
 // ------------------------------------------------------------------------------------------
-// Landmark-mean backward.  grid (m, BH), 256 threads.
+// Landmark-mean backward.  grid (m, BH), 256 threads: dq_l = dqtW_l + sum of the key-side
+// partials, dk_l = dktW_l + sum of the query-side partials (chunk order, fp64), then
+// dQ_i += dq_l / |S_l| and dK_i += dk_l / |S_l| over the segment's rows.
 __global__ __launch_bounds__(256) void bwd_pool_kernel(float* __restrict__ dQ, float* __restrict__ dK,
                                                        const float* __restrict__ dqtW, const float* __restrict__ dktW,
                                                        const float* __restrict__ dqt_part,
@@ -477,6 +712,7 @@ __global__ __launch_bounds__(256) void bwd_pool_kernel(float* __restrict__ dQ, f
     if (tid < d) {
         const size_t o = ((size_t)h * m + l) * d + tid;
         double aq = dqtW[o], ak = dktW[o];
+#pragma unroll 4
         for (int ch = 0; ch < nlc; ++ch) {
             const size_t p = (((size_t)h * nlc + ch) * m + l) * d + tid;
             aq += dqt_part[p];
@@ -486,11 +722,18 @@ __global__ __launch_bounds__(256) void bwd_pool_kernel(float* __restrict__ dQ, f
         sk[tid] = (float)ak * inv;
     }
     __syncthreads();
-    for (int e = tid; e < (s1 - s0) * d; e += 256) {
-        const int i = s0 + e / d, c = e % d;
-        const size_t idx = ((size_t)h * n + i) * d + c;
-        dQ[idx] += sq[c];
-        dK[idx] += sk[c];
+    // the segment's rows are contiguous: (s1 - s0) d floats from row s0, four at a time
+    const size_t base = ((size_t)h * n + s0) * d;
+    const int cnt4 = (s1 - s0) * d / 4;
+    float4* q4 = reinterpret_cast<float4*>(dQ + base);
+    float4* k4 = reinterpret_cast<float4*>(dK + base);
+    for (int e = tid; e < cnt4; e += 256) {
+        const int c = (4 * e) % d;
+        float4 a = q4[e], b = k4[e];
+        a.x += sq[c]; a.y += sq[c + 1]; a.z += sq[c + 2]; a.w += sq[c + 3];
+        b.x += sk[c]; b.y += sk[c + 1]; b.z += sk[c + 2]; b.w += sk[c + 3];
+        q4[e] = a;
+        k4[e] = b;
     }
 }
 

@@ -8,6 +8,7 @@
 #include "common.hpp"
 #include "kernels.hpp"
 #include "ns_mfma.hpp"
+#include "srows.hpp"
 
 namespace lapattn {
 
@@ -63,29 +64,6 @@ __global__ __launch_bounds__(256) void pool_kernel(const typename elem<DT>::type
 //   column tile).  At the end the four waves' partials are added in a fixed order.
 // Writes Upart[h][chunk][a][c] for a < m, c <= d.
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
-
-// 32 consecutive floats of a wave-uniform row (scalar loads).
-__device__ __forceinline__ void srow32(float (&t)[32], const float* __restrict__ p) {
-#pragma unroll
-    for (int c = 0; c < 32; ++c) t[c] = p[c];
-}
-
-// acc + sum_c |t_c - x_c| over 32 coordinates (t in scalar registers); the loads of the next
-// unit into `nt` are issued after the first use of `t`.
-__device__ __forceinline__ float l1_unit(const float* x, const float (&t)[32], float (&nt)[32],
-                                         const float* __restrict__ next, float acc) {
-    float a0 = acc + fabsf(t[0] - x[0]);
-    __builtin_amdgcn_sched_barrier(0);
-    srow32(nt, next);
-    __builtin_amdgcn_sched_barrier(0);
-    float a1 = fabsf(t[1] - x[1]);
-#pragma unroll
-    for (int c = 2; c < 32; c += 2) {
-        a0 += fabsf(t[c] - x[c]);
-        a1 += fabsf(t[c + 1] - x[c + 1]);
-    }
-    return a0 + a1;
-}
 
 template <int D>
 __global__ __launch_bounds__(256) void key_summary_kernel(const float* __restrict__ K, const float* __restrict__ V,

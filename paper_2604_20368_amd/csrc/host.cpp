@@ -16,7 +16,7 @@ namespace {
 constexpr int kMaxM = 64;
 constexpr int kMaxT = 64;
 constexpr int kKeyChunk = 1024;  // keys per block of the key-summary kernel (four 64-key tiles per wave)
-constexpr int kLmChunk = 64;     // tokens per block of the landmark-major backward passes
+constexpr int kLmChunk = 256;    // tokens per block of the landmark-major backward passes
 
 // ------------------------------------------------------------------------------- validation
 
@@ -89,8 +89,8 @@ Plan make_plan(int BH, int n, int d, int m, int T, bool bwd) {
     p.M = c.take(bh * m * d1 * f);
     p.vbar = c.take(bh * d * f);
     if (bwd) {
-        p.Aq = c.take(bh * n * m * f);
-        p.dDq = c.take(bh * n * m * f);
+        p.Aq = c.take(bh * n * 64 * f);    // rows of pitch 64 (16-byte aligned for the LDS copies)
+        p.dDq = c.take(bh * n * 64 * f);
         p.rs = c.take(bh * n * f);
         p.dYd = c.take(bh * n * f);
         p.dvbar_part = c.take(bh * p.nqb * d * f);
@@ -100,7 +100,7 @@ Plan make_plan(int BH, int n, int d, int m, int T, bool bwd) {
         p.dvbar = c.take(bh * d * f);
         p.dqtW = c.take(bh * m * d * f);
         p.dktW = c.take(bh * m * d * f);
-        p.dDk = c.take(bh * n * m * f);
+        p.dDk = c.take(bh * n * 64 * f);
         p.dqt_part = c.take(bh * p.nlc * m * d * f);
     }
     p.total = (c.off + 255) & ~size_t(255);

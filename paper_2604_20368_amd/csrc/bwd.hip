@@ -23,11 +23,12 @@ static inline float kscale_of(float lambda) { return (float)(-1.4426950408889634
 // ------------------------------------------------------------------------------------------
 // Query-major pass.  grid (nqb, BH), 256 threads, lane = query (wave w of block b covers
 // queries 256 b + 64 w ..).  Landmark rows of kt come through scalar registers (srows.hpp),
-// the rows of M are LDS broadcasts.
-//   Pass 1: a_il = k(q_i, kt_l) into the wave's [query][landmark] LDS tile, s_i (and y_i for
-//           the row-sum normalisation); rs, dYd; the tile leaves as whole rows of Aq.
-//   Pass 2: dA_il = rs_i dO_i . M_l[:d] + dYd_i M_l[d], dD_il = -a_il dA_il / lambda (back into
-//           the tile, then whole rows of dDq), dq_i += dD_il sign(q_i - kt_l).
+// the rows of M are LDS broadcasts; loops that stream rows read no LDS (see pass 1).
+//   Pass 1: a_il = k(q_i, kt_l) into the wave's [query][landmark] LDS tile.
+//   Then, from the tile: s_i (and y_i for the row-sum normalisation), rs, dYd; whole rows of
+//   Aq; dA_il = rs_i dO_i . M_l[:d] + dYd_i M_l[d] and dD_il = -a_il dA_il / lambda back into
+//   the tile; whole rows of dDq.
+//   Pass 2: dq_i += dD_il sign(q_i - kt_l).
 //   dvbar partial (inline normalisation): sum over the block's queries of (1 - s_i) dO_i,
 //   per wave through the tile, then over the waves in order.
 template <int D, int NORM>
@@ -62,22 +63,14 @@ __global__ __launch_bounds__(256) void bwd_query_kernel(const float* __restrict_
         g[4 * c4 + 0] = b.x; g[4 * c4 + 1] = b.y; g[4 * c4 + 2] = b.z; g[4 * c4 + 3] = b.w;
     }
     __syncthreads();   // sM, sVb
-    const float* tab = kt + (size_t)h * m * D;
+    const float* tab = kt + __builtin_amdgcn_readfirstlane(h * m * D);   // wave-uniform: scalar loads
     const int units = m * NCH;
 
-    // pass 1 (a landmark column a >= m, reached only past the table, holds zeros)
-    float s = 0.f;
-    float y[NORM == NORM_ROWSUM ? D : 1];
-#pragma unroll
-    for (int c = 0; c < (NORM == NORM_ROWSUM ? D : 1); ++c) y[c] = 0.f;
+    // pass 1: a_il into the tile (a landmark column a == m, reached only past the table, holds
+    // zeros).  The streaming loops read no LDS: a wait for an LDS read would also wait for the
+    // row prefetch.
     auto emit = [&](int a, float dist) {
-        const float av = (live && a < m) ? __builtin_amdgcn_exp2f(dist * kscale) : 0.f;
-        tile[l * TP + a] = av;
-        s = fmaf(av, sM[a * D1 + D], s);
-        if (NORM == NORM_ROWSUM) {
-#pragma unroll
-            for (int c = 0; c < D; ++c) y[c] = fmaf(av, sM[a * D1 + c], y[c]);
-        }
+        tile[l * TP + a] = (live && a < m) ? __builtin_amdgcn_exp2f(dist * kscale) : 0.f;
     };
     {
         float ta[32], tb[32];
@@ -94,6 +87,21 @@ __global__ __launch_bounds__(256) void bwd_query_kernel(const float* __restrict_
             dist = 0.f;
         }
         asm volatile("" ::"s"(ta[0]), "s"(ta[16]));
+    }
+    __builtin_amdgcn_wave_barrier();
+    // s_i (and y_i for the row-sum normalisation) from the tile, in landmark order
+    float s = 0.f;
+    float y[NORM == NORM_ROWSUM ? D : 1];
+#pragma unroll
+    for (int c = 0; c < (NORM == NORM_ROWSUM ? D : 1); ++c) y[c] = 0.f;
+    for (int a = 0; a < m; ++a) {
+        const float av = tile[l * TP + a];
+        const float* mr = sM + a * D1;
+        s = fmaf(av, mr[D], s);
+        if (NORM == NORM_ROWSUM) {
+#pragma unroll
+            for (int c = 0; c < D; ++c) y[c] = fmaf(av, mr[c], y[c]);
+        }
     }
     float rsc = 1.f, dyd = 0.f;
     if (NORM == NORM_INLINE) {
@@ -112,47 +120,49 @@ __global__ __launch_bounds__(256) void bwd_query_kernel(const float* __restrict_
         rs[(size_t)h * n + i] = rsc;
         dYd[(size_t)h * n + i] = dyd;
     }
-    __builtin_amdgcn_wave_barrier();
     for (int r = 0; r < 64 && i0 + r < n; ++r)
         if (l < m) Aq[((size_t)h * n + i0 + r) * 64 + l] = tile[r * TP + l];
     __builtin_amdgcn_wave_barrier();
 
-    // pass 2
+    // dA_il and dD_il into the tile (LDS only), then whole rows of dDq
     float dq[D], gs[D];
 #pragma unroll
     for (int c = 0; c < D; ++c) {
         dq[c] = 0.f;
         gs[c] = g[c] * rsc;
     }
-    auto ddof = [&](int a) {
+#pragma unroll 2
+    for (int a = 0; a < m; ++a) {
         const float* mr = sM + a * D1;
         float da = dyd * mr[D];
 #pragma unroll
         for (int c = 0; c < D; ++c) da = fmaf(gs[c], mr[c], da);
-        const float dd = -tile[l * TP + a] * da * inv_lambda;
-        tile[l * TP + a] = dd;
-        return dd;
-    };
+        tile[l * TP + a] = -tile[l * TP + a] * da * inv_lambda;
+    }
+    __builtin_amdgcn_wave_barrier();
+    for (int r = 0; r < 64 && i0 + r < n; ++r)
+        if (l < m) dDq[((size_t)h * n + i0 + r) * 64 + l] = tile[r * TP + l];
+
+    // pass 2: dq_i += dD_il sign(q_i - kt_l); each unit's dD is read before the unit's first
+    // wait (which covers it); landmarks past m have dD = 0 (a zero column when m is odd)
     {
         float ta[32], tb[32];
         srow32(ta, tab);
         for (int u = 0; u < units; u += 2) {
             if (NCH == 1) {
-                const float d0 = ddof(u);
+                const float d0 = tile[l * TP + u], d1 = tile[l * TP + u + 1];
+                __builtin_amdgcn_sched_barrier(0);
                 sgn_unit(dq, q, ta, tb, tab + 32 * min(u + 1, units - 1), d0);
-                const float d1 = ddof(u + 1);
                 sgn_unit(dq, q, tb, ta, tab + 32 * min(u + 2, units - 1), d1);
             } else {
-                const float d0 = ddof(u / NCH);
+                const float d0 = tile[l * TP + u / NCH];
+                __builtin_amdgcn_sched_barrier(0);
                 sgn_unit(dq, q, ta, tb, tab + 32 * min(u + 1, units - 1), d0);
                 sgn_unit(dq + 32, q + 32, tb, ta, tab + 32 * min(u + 2, units - 1), d0);
             }
         }
         asm volatile("" ::"s"(ta[0]), "s"(ta[16]));
     }
-    __builtin_amdgcn_wave_barrier();
-    for (int r = 0; r < 64 && i0 + r < n; ++r)
-        if (l < m) dDq[((size_t)h * n + i0 + r) * 64 + l] = tile[r * TP + l];
     if (live) {
 #pragma unroll
         for (int c4 = 0; c4 < D / 4; ++c4)
@@ -195,13 +205,14 @@ __device__ __forceinline__ void lds_dma4(float* lds_dst, const float* src_lane) 
 }
 __device__ __forceinline__ void lds_dma_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
-// The rows of a [token][W] array (W floats per row, W a multiple of 4) for tokens t0 .. t0 + 15
-// (clamped to the last token) into dst[16][W].
-template <int W>
-__device__ __forceinline__ void stage_rows16(float* dst, const float* base, int t0, int n) {
+// The rows of a [token][W] array (W floats per row, W a multiple of 4) for tokens t0 .. t0 + R - 1
+// (clamped to the last token) into dst[R][W]; R W must be a multiple of 256.
+template <int R, int W>
+__device__ __forceinline__ void stage_rows(float* dst, const float* base, int t0, int n) {
+    static_assert((R * W) % 256 == 0, "whole 1 KB copies");
     const int l = threadIdx.x & 63;
 #pragma unroll
-    for (int k = 0; k < 16 * W / 256; ++k) {
+    for (int k = 0; k < R * W / 256; ++k) {
         const int e = 256 * k + 4 * l;
         lds_dma16(dst + 256 * k, base + (size_t)min(t0 + e / W, n - 1) * W + e % W);
     }
@@ -209,8 +220,8 @@ __device__ __forceinline__ void stage_rows16(float* dst, const float* base, int 
 
 // ------------------------------------------------------------------------------------------
 // Landmark-major pass over queries.  grid (nlc, BH), 64 threads (lane = landmark l); block ch
-// covers queries [ch * chunk, ...) in sub-tiles of 16 whose data -- rows of Q and dO, rows of
-// Aq and dDq (pitch 64), rs and dYd -- is copied to LDS one sub-tile ahead (two buffers).  Per
+// covers queries [ch * chunk, ...) in sub-tiles of 8 whose data -- rows of Q and dO, rows of Aq
+// and dDq (pitch 64), rs and dYd -- is copied to LDS one sub-tile ahead (two buffers).  Per
 // query i:
 //   dM_l[:d] += a_il rs_i dO_i on fp32 MFMA 32x32x1 (A = a_il, lane = landmark = MFMA row; B =
 //   rs_i dO_i[32 hh + l % 32], one 32-column half per instruction), dM_l[d] += a_il dYd_i;
@@ -227,7 +238,8 @@ __global__ __launch_bounds__(64) void bwd_query_lm_kernel(const float* __restric
                                                           int nlc) {
     constexpr int D1 = D + 1;
     constexpr int NH = D / 32;
-    constexpr int BUF = 16 * D + 16 * 64 + 16 * 64 + 16 * D + 64;   // Q, Aq, dDq, dO, rs | dYd
+    constexpr int ST = 8;                                            // queries per sub-tile
+    constexpr int BUF = ST * D + ST * 64 + ST * 64 + ST * D + 64;   // Q, Aq, dDq, dO, rs | dYd
     __shared__ __attribute__((aligned(16))) float sbuf[2 * BUF];
     const int ch = blockIdx.x, h = blockIdx.y, l = threadIdx.x;
     const bool live = l < m;
@@ -239,12 +251,12 @@ __global__ __launch_bounds__(64) void bwd_query_lm_kernel(const float* __restric
     const int i0 = ch * chunk, i1 = min(n, i0 + chunk);
     auto stage = [&](int b, int t0) {
         float* sb = sbuf + b * BUF;
-        stage_rows16<D>(sb, Qh, t0, n);
-        stage_rows16<64>(sb + 16 * D, Ah, t0, n);
-        stage_rows16<64>(sb + 16 * D + 16 * 64, DDh, t0, n);
-        stage_rows16<D>(sb + 16 * D + 32 * 64, dOh, t0, n);
-        const int r = min(t0 + (l & 15), n - 1);
-        lds_dma4(sb + 32 * D + 32 * 64, (l < 16 ? rs : dYd) + (size_t)h * n + r);
+        stage_rows<ST, D>(sb, Qh, t0, n);
+        stage_rows<ST, 64>(sb + ST * D, Ah, t0, n);
+        stage_rows<ST, 64>(sb + ST * D + ST * 64, DDh, t0, n);
+        stage_rows<ST, D>(sb + ST * D + 2 * ST * 64, dOh, t0, n);
+        const int r = min(t0 + (l & (ST - 1)), n - 1);
+        lds_dma4(sb + 2 * ST * D + 2 * ST * 64, (l < ST ? rs : dYd) + (size_t)h * n + r);
     };
     float k[D], dk[D];
 #pragma unroll
@@ -260,23 +272,23 @@ __global__ __launch_bounds__(64) void bwd_query_lm_kernel(const float* __restric
         for (int r = 0; r < 32; ++r) acc[hh][r] = 0.f;
     if (i0 < i1) stage(0, i0);
     int buf = 0;
-    for (int t0 = i0; t0 < i1; t0 += 16, buf ^= 1) {
+    for (int t0 = i0; t0 < i1; t0 += ST, buf ^= 1) {
         lds_dma_wait();
         __builtin_amdgcn_wave_barrier();
-        if (t0 + 16 < i1) stage(buf ^ 1, t0 + 16);
+        if (t0 + ST < i1) stage(buf ^ 1, t0 + ST);
         const float* sb = sbuf + buf * BUF;
         const float* sQ = sb;
-        const float* sA = sb + 16 * D;
-        const float* sDD = sA + 16 * 64;
-        const float* sdO = sDD + 16 * 64;
-        const float* sRY = sdO + 16 * D;
+        const float* sA = sb + ST * D;
+        const float* sDD = sA + ST * 64;
+        const float* sdO = sDD + ST * 64;
+        const float* sRY = sdO + ST * D;
 #pragma unroll 4
-        for (int r = 0; r < 16; ++r) {
+        for (int r = 0; r < ST; ++r) {
             const bool in = live && t0 + r < i1;
             const float av = sA[r * 64 + lc], ddv = sDD[r * 64 + lc];   // unconditional reads
             const float a = in ? av : 0.f;
             const float dd = in ? ddv : 0.f;
-            const float rsi = sRY[r], ydi = sRY[16 + r];
+            const float rsi = sRY[r], ydi = sRY[ST + r];
 #pragma unroll
             for (int hh = 0; hh < NH; ++hh)
                 acc[hh] = __builtin_amdgcn_mfma_f32_32x32x1f32(a, sdO[r * D + 32 * hh + (l & 31)] * rsi, acc[hh], 0, 0, 0);
@@ -549,12 +561,12 @@ __global__ __launch_bounds__(256) void bwd_ns_kernel(const float* __restrict__ q
 // ------------------------------------------------------------------------------------------
 // Key-major pass.  grid (ceil(n/256), BH), 256 threads, lane = key (wave w of block b covers
 // keys 256 b + 64 w ..).  Landmark rows of qt come through scalar registers (srows.hpp), the
-// rows of dU are LDS broadcasts.  Per landmark a:
-//   B_aj = k(qt_a, k_j);  dB_aj = dU_a[:d] . v_j + dU_a[d];  dV_j += B_aj dU_a[:d];
-//   dD_aj = -B_aj dB_aj / lambda (into the wave's [key][landmark] LDS tile, which leaves as
-//   whole rows of dDk);  dK_j -= dD_aj sign(qt_a - k_j).
-// A landmark row is streamed once for the distance and once for the signs (the table is small
-// and stays in cache); -dD sign(qt_a - k_j) is accumulated as dD sign(k_j - qt_a).  dV_j gets
+// rows of dU are LDS broadcasts.  Three phases over the landmarks a:
+//   distance pass: B_aj = k(qt_a, k_j) into the wave's [key][landmark] LDS tile;
+//   from the tile (LDS only): dB_aj = dU_a[:d] . v_j + dU_a[d], dV_j += B_aj dU_a[:d],
+//   dD_aj = -B_aj dB_aj / lambda back into the tile (then whole rows of dDk);
+//   sign pass: dK_j -= dD_aj sign(qt_a - k_j).
+// The landmark rows are streamed twice (the table is small and stays in cache).  dV_j gets
 // dvbar / n at the end.
 template <int D>
 __global__ __launch_bounds__(256) void bwd_key_kernel(const float* __restrict__ K, const float* __restrict__ V,
@@ -590,11 +602,34 @@ __global__ __launch_bounds__(256) void bwd_key_kernel(const float* __restrict__ 
         dv[c] = 0.f;
     }
     __syncthreads();   // sdU, sdv
-    const float* tab = qt + (size_t)h * m * D;
-    // per landmark: B, dB, dV and dD (a landmark a == m, reached only past the table on the
-    // last pass, gets B = 0)
-    auto step = [&](int a, float dist) {
-        const float b = (live && a < m) ? __builtin_amdgcn_exp2f(dist * kscale) : 0.f;
+    const float* tab = qt + __builtin_amdgcn_readfirstlane(h * m * D);   // wave-uniform: scalar loads
+    const int units = m * NCH;
+    // distance pass: B_aj into the tile (a column a == m, reached only past the table, holds
+    // zeros); the streaming loops read no LDS
+    auto emit = [&](int a, float dist) {
+        tile[l * TP + a] = (live && a < m) ? __builtin_amdgcn_exp2f(dist * kscale) : 0.f;
+    };
+    {
+        float ta[32], tb[32];
+        srow32(ta, tab);
+        float dist = 0.f;
+        for (int u = 0; u < units; u += 2) {
+            dist = l1_unit(kk + 32 * (u % NCH), ta, tb, tab + 32 * min(u + 1, units - 1), dist);
+            if (NCH == 1) {
+                emit(u, dist);
+                dist = 0.f;
+            }
+            dist = l1_unit(kk + 32 * ((u + 1) % NCH), tb, ta, tab + 32 * min(u + 2, units - 1), dist);
+            emit((u + 1) / NCH, dist);
+            dist = 0.f;
+        }
+        asm volatile("" ::"s"(ta[0]), "s"(ta[16]));
+    }
+    __builtin_amdgcn_wave_barrier();
+    // dB, dV and dD (LDS only): dD replaces B in the tile
+#pragma unroll 2
+    for (int a = 0; a < m; ++a) {
+        const float b = tile[l * TP + a];
         const float* ur = sdU + a * D1;
         float db = ur[D];
 #pragma unroll
@@ -602,30 +637,25 @@ __global__ __launch_bounds__(256) void bwd_key_kernel(const float* __restrict__ 
             db = fmaf(ur[c], v[c], db);
             dv[c] = fmaf(b, ur[c], dv[c]);
         }
-        const float dd = -b * db * inv_lambda;
-        tile[l * TP + a] = dd;
-        return dd;
-    };
+        tile[l * TP + a] = -b * db * inv_lambda;
+    }
+    __builtin_amdgcn_wave_barrier();
+    // sign pass: dK_j -= dD_aj sign(qt_a - k_j), accumulated as dD sign(k_j - qt_a); each unit's
+    // dD is read before the unit's first wait
     {
         float ta[32], tb[32];
         srow32(ta, tab);
-        if (NCH == 1) {
-            // landmark a in ta, a + 1 in tb; each row serves its distance and then its signs
-            for (int a = 0; a < m; a += 2) {
-                float dd = step(a, l1_unit(kk, ta, tb, tab + 32 * min(a + 1, m - 1), 0.f));
-                sgn_unit_nopf(dk, kk, ta, dd);
-                dd = step(a + 1, l1_unit(kk, tb, ta, tab + 32 * min(a + 2, m - 1), 0.f));
-                sgn_unit_nopf(dk, kk, tb, dd);
-            }
-        } else {
-            // units of landmark a: distance halves 0 and 1, then sign halves 0 and 1
-            for (int a = 0; a < m; ++a) {
-                const float* r0 = tab + (size_t)a * D;
-                float dist = l1_unit(kk, ta, tb, r0 + 32, 0.f);
-                dist = l1_unit(kk + 32, tb, ta, r0, dist);
-                const float dd = step(a, dist);
-                sgn_unit(dk, kk, ta, tb, r0 + 32, dd);
-                sgn_unit(dk + 32, kk + 32, tb, ta, tab + (size_t)min(a + 1, m - 1) * D, dd);
+        for (int u = 0; u < units; u += 2) {
+            if (NCH == 1) {
+                const float d0 = tile[l * TP + u], d1 = tile[l * TP + u + 1];
+                __builtin_amdgcn_sched_barrier(0);
+                sgn_unit(dk, kk, ta, tb, tab + 32 * min(u + 1, units - 1), d0);
+                sgn_unit(dk, kk, tb, ta, tab + 32 * min(u + 2, units - 1), d1);
+            } else {
+                const float d0 = tile[l * TP + u / NCH];
+                __builtin_amdgcn_sched_barrier(0);
+                sgn_unit(dk, kk, ta, tb, tab + 32 * min(u + 1, units - 1), d0);
+                sgn_unit(dk + 32, kk + 32, tb, ta, tab + 32 * min(u + 2, units - 1), d0);
             }
         }
         asm volatile("" ::"s"(ta[0]), "s"(ta[16]));
@@ -668,8 +698,8 @@ __global__ __launch_bounds__(64) void bwd_key_lm_kernel(const float* __restrict_
     }
     const int j0 = ch * chunk, j1 = min(n, j0 + chunk);
     auto stage = [&](int b, int t0) {
-        stage_rows16<D>(sbuf + b * BUF, Kh, t0, n);
-        stage_rows16<64>(sbuf + b * BUF + 16 * D, DDh, t0, n);
+        stage_rows<16, D>(sbuf + b * BUF, Kh, t0, n);
+        stage_rows<16, 64>(sbuf + b * BUF + 16 * D, DDh, t0, n);
     };
     if (j0 < j1) stage(0, j0);
     int buf = 0;

@@ -78,7 +78,7 @@ __global__ __launch_bounds__(256) void key_summary_kernel(const float* __restric
     const int chunk = blockIdx.x, h = blockIdx.y;
     const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, li = l & 15, lk = l >> 4;
     float* sB = lds + w * 64 * BP;
-    const float* tab = qt + (size_t)h * m * D;
+    const float* tab = qt + __builtin_amdgcn_readfirstlane(h * m * D);   // wave-uniform: scalar loads
     const int units = m * NCH;
     for (int a = m; a < 64; ++a) sB[a * BP + l] = 0.f;
     f32x4_t acc[4][CT];
@@ -352,48 +352,123 @@ __global__ __launch_bounds__(256) void ns_solve_kernel(const float* __restrict__
 }
 
 // ------------------------------------------------------------------------------------------
-// Query side.  grid (ceil(n/256), BH), one query per thread:
-//   y = sum_l k(q_i, kt_l) M_l  (d+1 columns),  s_i = y[d],  then the normalisation.
-template <int DT, int D, int NORM>
-__global__ __launch_bounds__(256) void query_out_kernel(const typename elem<DT>::type* __restrict__ Q,
-                                                        typename elem<DT>::type* __restrict__ Out,
-                                                        const float* __restrict__ kt,
-                                                        const float* __restrict__ M,
-                                                        const float* __restrict__ vbar, int n, int m,
-                                                        float kscale) {
+// Query side (fp32 inputs).  grid (ceil(n/256), BH), 256 threads, lane = query (wave w of block
+// b covers queries 256 b + 64 w ..).
+//   Landmark pass: a_il = k(q_i, kt_l) into the wave's [query][landmark] LDS tile (the landmark
+//   rows of kt through scalar registers).  s_i = sum_l a_il M[l][d] in fp32 is formed with the
+//   contraction, which reads the tile anyway.
+//   Contraction: for each 32-query half, Y^T = M^T A^T on fp32 MFMA 32x32x2 (k = a pair of
+//   landmarks).  The B operands of a pair for both halves come from one permlane32 swap of the
+//   pair's two tile columns (queries 0..31 keep theirs and receive the other landmark of 32..63
+//   and vice versa).  The result holds, per lane, 16 output columns of one query: normalised
+//   (Eq. (4) / Eq. (3)) and stored four columns at a time.
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+template <int D, int NORM>
+__global__ __launch_bounds__(256) void query_out_kernel(const float* __restrict__ Q, float* __restrict__ Out,
+                                                        const float* __restrict__ kt, const float* __restrict__ M,
+                                                        const float* __restrict__ vbar, int n, int m, float kscale) {
     constexpr int D1 = D + 1;
-    __shared__ float sK[64 * D];
-    __shared__ float sM[64 * D1];
+    constexpr int NCH = D / 32;
+    constexpr int CB = D / 32;             // 32-column blocks of the output
+    constexpr int TP = 65;
+    // MFMA A operand of landmark pair s, column block cb: lane j + 32 k holds M[2s + k][32 cb + j]
+    __shared__ __attribute__((aligned(16))) float sMT[32 * CB * 64];
+    __shared__ float sMo[64];
     __shared__ float sVb[D];
-    const int h = blockIdx.y, tid = threadIdx.x;
-    for (int e = tid; e < m * D; e += 256) sK[e] = kt[(size_t)h * m * D + e];
-    for (int e = tid; e < m * D1; e += 256) sM[e] = M[(size_t)h * m * D1 + e];
-    if (tid < D) sVb[tid] = vbar[(size_t)h * D + tid];
-    __syncthreads();
-    const int i = blockIdx.x * 256 + tid;
-    if (i >= n) return;
-    const size_t row = ((size_t)h * n + i) * D;
-    float q[D], y[D1];
-#pragma unroll
-    for (int c = 0; c < D; ++c) q[c] = elem<DT>::load(Q, row + c);
-#pragma unroll
-    for (int c = 0; c < D1; ++c) y[c] = 0.f;
-    for (int l = 0; l < m; ++l) {
-        float dist = 0.f;
-#pragma unroll
-        for (int c = 0; c < D; ++c) dist += fabsf(q[c] - sK[l * D + c]);
-        const float a = exp2f(dist * kscale);
-#pragma unroll
-        for (int c = 0; c < D1; ++c) y[c] = fmaf(a, sM[l * D1 + c], y[c]);
+    __shared__ float sT[4 * 64 * TP];
+    const int h = blockIdx.y, tid = threadIdx.x, w = tid >> 6, l = tid & 63;
+    for (int e = tid; e < 32 * CB * 64; e += 256) {
+        const int s = e / (CB * 64), cb = (e / 64) % CB, ln = e % 64;
+        const int lm = 2 * s + ln / 32;
+        sMT[e] = (lm < m) ? M[((size_t)h * m + lm) * D1 + 32 * cb + ln % 32] : 0.f;
     }
-    const float s = y[D];
+    if (tid < 64) sMo[tid] = (tid < m) ? M[((size_t)h * m + tid) * D1 + D] : 0.f;
+    if (tid < D) sVb[tid] = vbar[(size_t)h * D + tid];
+    float* tile = sT + w * 64 * TP;
+    const int i0 = blockIdx.x * 256 + w * 64;
+    const int i = i0 + l;
+    const bool live = i < n;
+    float q[D];
+    {
+        const float4* qr = reinterpret_cast<const float4*>(Q + ((size_t)h * n + (live ? i : n - 1)) * D);
 #pragma unroll
-    for (int c = 0; c < D; ++c) {
-        float o;
-        if (NORM == NORM_INLINE) o = y[c] + (1.f - s) * sVb[c];
-        else if (NORM == NORM_ROWSUM) o = y[c] / s;
-        else o = y[c];
-        elem<DT>::store(Out, row + c, o);
+        for (int c4 = 0; c4 < D / 4; ++c4) {
+            const float4 v = qr[c4];
+            q[4 * c4 + 0] = v.x; q[4 * c4 + 1] = v.y; q[4 * c4 + 2] = v.z; q[4 * c4 + 3] = v.w;
+        }
+    }
+    __syncthreads();   // sMT, sMo, sVb
+    const float* tab = kt + __builtin_amdgcn_readfirstlane(h * m * D);   // wave-uniform: scalar loads
+    const int units = m * NCH;
+    // no LDS reads in this loop: a wait for one would also wait for the row prefetch
+    auto emit = [&](int a, float dist) {   // a == m only past the table: a zero column
+        tile[l * TP + a] = (live && a < m) ? __builtin_amdgcn_exp2f(dist * kscale) : 0.f;
+    };
+    {
+        float ta[32], tb[32];
+        srow32(ta, tab);
+        float dist = 0.f;
+        for (int u = 0; u < units; u += 2) {
+            dist = l1_unit(q + 32 * (u % NCH), ta, tb, tab + 32 * min(u + 1, units - 1), dist);
+            if (NCH == 1) {
+                emit(u, dist);
+                dist = 0.f;
+            }
+            dist = l1_unit(q + 32 * ((u + 1) % NCH), tb, ta, tab + 32 * min(u + 2, units - 1), dist);
+            emit((u + 1) / NCH, dist);
+            dist = 0.f;
+        }
+        asm volatile("" ::"s"(ta[0]), "s"(ta[16]));
+    }
+    __builtin_amdgcn_wave_barrier();
+    f32x16_t acc[2][CB];
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[qb][cb][r] = 0.f;
+    const int npair = (m + 1) / 2;
+    float s = 0.f;   // s_i = sum_l a_il M[l][d], in landmark order
+#pragma unroll 2
+    for (int p = 0; p < npair; ++p) {
+        const float x0 = tile[l * TP + 2 * p], x1 = tile[l * TP + 2 * p + 1];
+        s = fmaf(x1, sMo[2 * p + 1], fmaf(x0, sMo[2 * p], s));
+        const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x0), __float_as_uint(x1), false, false);
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb) {
+            const float av = sMT[(p * CB + cb) * 64 + l];
+#pragma unroll
+            for (int qb = 0; qb < 2; ++qb)
+                acc[qb][cb] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, __uint_as_float(b[qb]), acc[qb][cb], 0, 0, 0);
+        }
+    }
+    // result register r at lane l: column 8 (r / 4) + 4 (l / 32) + r % 4 of the block, query l % 32
+    // of the half; s_i of that query from the same swap
+    const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(s), __float_as_uint(s), false, false);
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+        const int iq = i0 + 32 * qb + (l & 31);
+        const float si = __uint_as_float(sw[qb]);
+        if (iq < n) {
+            float* orow = Out + ((size_t)h * n + iq) * D;
+#pragma unroll
+            for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int c0 = 32 * cb + 8 * g + 4 * (l >> 5);
+                    float o[4];
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) {
+                        const float y = acc[qb][cb][4 * g + t];
+                        if (NORM == NORM_INLINE) o[t] = fmaf(1.f - si, sVb[c0 + t], y);
+                        else if (NORM == NORM_ROWSUM) o[t] = y / si;
+                        else o[t] = y;
+                    }
+                    *reinterpret_cast<float4*>(orow + c0) = make_float4(o[0], o[1], o[2], o[3]);
+                }
+        }
     }
 }
 
@@ -441,29 +516,26 @@ hipError_t launch_ns_solve(const float* qt, const float* kt, const float* Upart,
     return hipGetLastError();
 }
 
-template <int DT, int D>
+template <int D>
 static void query_out_launch(int norm, const void* Q, void* Out, const float* kt, const float* M, const float* vbar,
                              int BH, int n, int m, float kscale, hipStream_t st) {
-    using T = typename elem<DT>::type;
     dim3 grid((n + 255) / 256, BH);
+    const float* q = (const float*)Q;
+    float* o = (float*)Out;
     if (norm == NORM_INLINE)
-        hipLaunchKernelGGL((query_out_kernel<DT, D, NORM_INLINE>), grid, dim3(256), 0, st, (const T*)Q, (T*)Out, kt,
-                           M, vbar, n, m, kscale);
+        hipLaunchKernelGGL((query_out_kernel<D, NORM_INLINE>), grid, dim3(256), 0, st, q, o, kt, M, vbar, n, m, kscale);
     else if (norm == NORM_ROWSUM)
-        hipLaunchKernelGGL((query_out_kernel<DT, D, NORM_ROWSUM>), grid, dim3(256), 0, st, (const T*)Q, (T*)Out, kt,
-                           M, vbar, n, m, kscale);
+        hipLaunchKernelGGL((query_out_kernel<D, NORM_ROWSUM>), grid, dim3(256), 0, st, q, o, kt, M, vbar, n, m, kscale);
     else
-        hipLaunchKernelGGL((query_out_kernel<DT, D, NORM_NONE>), grid, dim3(256), 0, st, (const T*)Q, (T*)Out, kt, M,
-                           vbar, n, m, kscale);
+        hipLaunchKernelGGL((query_out_kernel<D, NORM_NONE>), grid, dim3(256), 0, st, q, o, kt, M, vbar, n, m, kscale);
 }
 
 hipError_t launch_query_out(int dt, int norm, const void* Q, void* Out, const float* kt, const float* M,
                             const float* vbar, int BH, int n, int d, int m, float lambda, hipStream_t st) {
+    if (dt != DT_F32) return hipErrorInvalidValue;   // bf16 inputs take the fast path
     const float ks = kscale_of(lambda);
-    if (dt == DT_F32 && d == 32) query_out_launch<DT_F32, 32>(norm, Q, Out, kt, M, vbar, BH, n, m, ks, st);
-    else if (dt == DT_F32) query_out_launch<DT_F32, 64>(norm, Q, Out, kt, M, vbar, BH, n, m, ks, st);
-    else if (d == 32) query_out_launch<DT_BF16, 32>(norm, Q, Out, kt, M, vbar, BH, n, m, ks, st);
-    else query_out_launch<DT_BF16, 64>(norm, Q, Out, kt, M, vbar, BH, n, m, ks, st);
+    if (d == 32) query_out_launch<32>(norm, Q, Out, kt, M, vbar, BH, n, m, ks, st);
+    else query_out_launch<64>(norm, Q, Out, kt, M, vbar, BH, n, m, ks, st);
     return hipGetLastError();
 }
 

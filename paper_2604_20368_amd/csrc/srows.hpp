@@ -11,10 +11,16 @@
 
 namespace lapattn {
 
-// 32 consecutive floats of a wave-uniform row (scalar loads).
+// 32 consecutive floats of a wave-uniform row (scalar loads).  The row is read through the
+// constant address space: the tables are written by earlier launches and never within the
+// reading kernel, and this is what lets the loads be scalar (s_load) wherever the kernel also
+// stores to memory before them.
+typedef const __attribute__((address_space(4))) float cfloat_t;
+
 __device__ __forceinline__ void srow32(float (&t)[32], const float* __restrict__ p) {
+    cfloat_t* q = (cfloat_t*)p;
 #pragma unroll
-    for (int c = 0; c < 32; ++c) t[c] = p[c];
+    for (int c = 0; c < 32; ++c) t[c] = q[c];
 }
 
 // acc + sum_c |t_c - x_c| over 32 coordinates (t in scalar registers); the loads of the next

@@ -138,13 +138,19 @@ def calibrate_copy():
     print(json.dumps({"copy_bytes": COPY_BYTES, "launches": 3}), flush=True)
 
 
-def _pmc_per_dispatch(csv_dir, counter, kernel_substr):
+def _pmc_per_dispatch(csv_dir, counter, kernel_name):
+    """Average counter value per dispatch of the kernel called exactly `kernel_name` (the bare
+    name, demangled "ns::name<" or mangled "<len>nameI"; other kernels whose names contain it
+    do not count)."""
     import csv
     import glob
+    import re
+    pat = re.compile(r"(::|\d)" + re.escape(kernel_name) + r"(<|I)")
     vals = []
     for f in glob.glob(os.path.join(csv_dir, "**", "*counter_collection.csv"), recursive=True):
         for r in csv.DictReader(open(f)):
-            if r["Counter_Name"] == counter and kernel_substr in r["Kernel_Name"]:
+            name = r["Kernel_Name"]
+            if r["Counter_Name"] == counter and (name.strip() == kernel_name or pat.search(name)):
                 vals.append(float(r["Counter_Value"]))
     return sum(vals) / len(vals) if vals else None
 

@@ -228,6 +228,7 @@ __device__ __forceinline__ void stage_rows(float* dst, const float* base, int t0
 //   dkt_l -= dD_il sign(q_i - kt_l).
 // Queries past the chunk contribute zeros.
 typedef float f32x32_t __attribute__((ext_vector_type(32)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 template <int D>
 __global__ __launch_bounds__(64) void bwd_query_lm_kernel(const float* __restrict__ Q, const float* __restrict__ dO,
@@ -588,7 +589,7 @@ __global__ __launch_bounds__(256) void bwd_key_kernel(const float* __restrict__ 
     const int j = j0 + l;
     const bool live = j < n;
     const size_t row = ((size_t)h * n + (live ? j : n - 1)) * D;
-    float kk[D], v[D], dk[D], dv[D];
+    float kk[D], v[D], dk[D];
 #pragma unroll
     for (int c4 = 0; c4 < D / 4; ++c4) {
         const float4 a = reinterpret_cast<const float4*>(K + row)[c4];
@@ -597,10 +598,7 @@ __global__ __launch_bounds__(256) void bwd_key_kernel(const float* __restrict__ 
         v[4 * c4 + 0] = b.x; v[4 * c4 + 1] = b.y; v[4 * c4 + 2] = b.z; v[4 * c4 + 3] = b.w;
     }
 #pragma unroll
-    for (int c = 0; c < D; ++c) {
-        dk[c] = 0.f;
-        dv[c] = 0.f;
-    }
+    for (int c = 0; c < D; ++c) dk[c] = 0.f;
     __syncthreads();   // sdU, sdv
     const float* tab = qt + __builtin_amdgcn_readfirstlane(h * m * D);   // wave-uniform: scalar loads
     const int units = m * NCH;
@@ -626,18 +624,70 @@ __global__ __launch_bounds__(256) void bwd_key_kernel(const float* __restrict__ 
         asm volatile("" ::"s"(ta[0]), "s"(ta[16]));
     }
     __builtin_amdgcn_wave_barrier();
-    // dB, dV and dD (LDS only): dD replaces B in the tile
-#pragma unroll 2
-    for (int a = 0; a < m; ++a) {
-        const float b = tile[l * TP + a];
-        const float* ur = sdU + a * D1;
-        float db = ur[D];
+    // dV = B^T dU[:, :d] (k = a landmark pair; A operand straight from the tile), stored at once
+    // with dvbar / n; then dB = [v | 1] dU^T on the same instruction (k = a coordinate pair; the A
+    // operands of both 32-key halves from one permlane32 swap of the lane's own values) and
+    // dD = -B dB / lambda in place in the tile.  Result register r at lane l: row 8 (r / 4) +
+    // 4 (l / 32) + r % 4, column l % 32 of the 32 x 32 block.
+    const int npair = (m + 1) / 2;
+    const float invn = 1.f / (float)n;
 #pragma unroll
-        for (int c = 0; c < D; ++c) {
-            db = fmaf(ur[c], v[c], db);
-            dv[c] = fmaf(b, ur[c], dv[c]);
+    for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+        for (int cb = 0; cb < D / 32; ++cb) {
+            f32x16_t acc;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+#pragma unroll 4
+            for (int p = 0; p < npair; ++p) {
+                const float av = tile[(32 * kh + (l & 31)) * TP + 2 * p + (l >> 5)];
+                const float bv = sdU[(2 * p + (l >> 5)) * D1 + 32 * cb + (l & 31)];
+                acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc, 0, 0, 0);
+            }
+            const int c = 32 * cb + (l & 31);
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int key = 32 * kh + 8 * (r / 4) + 4 * (l >> 5) + r % 4;
+                if (j0 + key < n) dV[((size_t)h * n + j0 + key) * D + c] = acc[r] + sdv[c] * invn;
+            }
         }
-        tile[l * TP + a] = -b * db * inv_lambda;
+    {
+        f32x16_t acc[2][2];
+#pragma unroll
+        for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+            for (int lb = 0; lb < 2; ++lb)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[kh][lb][r] = 0.f;
+        const bool two = m > 32;
+#pragma unroll
+        for (int sp = 0; sp < D / 2; ++sp) {
+            const auto a2 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v[2 * sp]), __float_as_uint(v[2 * sp + 1]),
+                                                             false, false);
+#pragma unroll
+            for (int lb = 0; lb < 2; ++lb) {
+                if (lb == 1 && !two) break;
+                const float bv = sdU[(32 * lb + (l & 31)) * D1 + 2 * sp + (l >> 5)];
+#pragma unroll
+                for (int kh = 0; kh < 2; ++kh)
+                    acc[kh][lb] = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a2[kh]), bv, acc[kh][lb], 0, 0, 0);
+            }
+        }
+#pragma unroll
+        for (int lb = 0; lb < 2; ++lb) {
+            if (lb == 1 && !two) break;
+            const int a = 32 * lb + (l & 31);
+            const float u1 = sdU[a * D1 + D];
+#pragma unroll
+            for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int key = 32 * kh + 8 * (r / 4) + 4 * (l >> 5) + r % 4;
+                    float* tp = tile + key * TP + a;
+                    const float dd = -(*tp) * (acc[kh][lb][r] + u1) * inv_lambda;
+                    if (a < m) *tp = dd;
+                }
+        }
     }
     __builtin_amdgcn_wave_barrier();
     // sign pass: dK_j -= dD_aj sign(qt_a - k_j), accumulated as dD sign(k_j - qt_a); each unit's
@@ -664,14 +714,9 @@ __global__ __launch_bounds__(256) void bwd_key_kernel(const float* __restrict__ 
     for (int r = 0; r < 64 && j0 + r < n; ++r)
         if (l < m) dDk[((size_t)h * n + j0 + r) * 64 + l] = tile[r * TP + l];
     if (live) {
-        const float invn = 1.f / (float)n;
 #pragma unroll
-        for (int c4 = 0; c4 < D / 4; ++c4) {
+        for (int c4 = 0; c4 < D / 4; ++c4)
             reinterpret_cast<float4*>(dK + row)[c4] = make_float4(dk[4 * c4], dk[4 * c4 + 1], dk[4 * c4 + 2], dk[4 * c4 + 3]);
-            reinterpret_cast<float4*>(dV + row)[c4] =
-                make_float4(dv[4 * c4] + sdv[4 * c4] * invn, dv[4 * c4 + 1] + sdv[4 * c4 + 1] * invn,
-                            dv[4 * c4 + 2] + sdv[4 * c4 + 2] * invn, dv[4 * c4 + 3] + sdv[4 * c4 + 3] * invn);
-        }
     }
 }
 

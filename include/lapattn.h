@@ -69,7 +69,7 @@ enum {
     LAPATTN_ERR_SHAPE = 2,        /* B, H, n < 1, m < 1, m > n, or B*H*n*d >= 2^31 */
     LAPATTN_ERR_PARAM = 3,        /* lambda not finite or <= 0, ns_iters outside [0, 64],
                                      eps not finite or < 0, unknown norm or dtype */
-    LAPATTN_ERR_UNSUPPORTED = 4,  /* d not in {32, 64}, m > 64, or bf16 backward */
+    LAPATTN_ERR_UNSUPPORTED = 4,  /* d not in {32, 64} or m > 64 */
     LAPATTN_ERR_WORKSPACE = 5,    /* workspace NULL or smaller than lapattn_workspace_size() */
     LAPATTN_ERR_HIP = 6,          /* a HIP launch failed */
     LAPATTN_ERR_ALIGN = 7         /* a tensor pointer is not 16-byte aligned, or the
@@ -103,7 +103,9 @@ int lapattn_forward(const void* Q, const void* K, const void* V, void* Out,
  * Newton-Schulz update including the scale of X_0 (kernel gradient of App. A,
  * with sign(0) = 0; ties in the norm maxima go to the lowest index).  The
  * forward internals are recomputed; nothing is kept from a forward call.
- * Only dtype = LAPATTN_FP32 is supported. */
+ * dtype = LAPATTN_BF16 runs the fp32 computation on the exactly widened bf16
+ * inputs (held in the workspace, which is correspondingly larger) and rounds the
+ * three gradients to bf16 (nearest even); dQ, dK, dV are in the input dtype. */
 int lapattn_backward(const void* Q, const void* K, const void* V, const void* dOut,
                      void* dQ, void* dK, void* dV,
                      int B, int H, int n, int d, int m, float lambda, int ns_iters,

@@ -88,6 +88,7 @@ __global__ __launch_bounds__(256) void bwd_query_kernel(const float* __restrict_
         }
         asm volatile("" ::"s"(ta[0]), "s"(ta[16]));
     }
+    if (m & 1) tile[l * TP + m] = 0.f;   // the pair loops read column m (unwritten when d = 64)
     __builtin_amdgcn_wave_barrier();
     // s_i (and y_i for the row-sum normalisation) from the tile, in landmark order
     float s = 0.f;
@@ -623,6 +624,7 @@ __global__ __launch_bounds__(256) void bwd_key_kernel(const float* __restrict__ 
         }
         asm volatile("" ::"s"(ta[0]), "s"(ta[16]));
     }
+    if (m & 1) tile[l * TP + m] = 0.f;   // the pair loops read column m (unwritten when d = 64)
     __builtin_amdgcn_wave_barrier();
     // dV = B^T dU[:, :d] (k = a landmark pair; A operand straight from the tile), stored at once
     // with dvbar / n; then dB = [v | 1] dU^T on the same instruction (k = a coordinate pair; the A
@@ -810,6 +812,76 @@ __global__ __launch_bounds__(256) void bwd_pool_kernel(float* __restrict__ dQ, f
         q4[e] = a;
         k4[e] = b;
     }
+}
+
+// ------------------------------------------------------------------------------------------
+// bf16 backward: widening of the inputs (exact) and rounding of the gradients (nearest even,
+// NaN kept NaN), eight elements per thread and array.  grid-stride over count / 8 groups.
+__global__ __launch_bounds__(256) void widen_bf16_kernel(const uint16_t* __restrict__ a0, const uint16_t* __restrict__ a1,
+                                                         const uint16_t* __restrict__ a2, const uint16_t* __restrict__ a3,
+                                                         float* __restrict__ b0, float* __restrict__ b1,
+                                                         float* __restrict__ b2, float* __restrict__ b3, size_t groups) {
+    const uint16_t* src[4] = {a0, a1, a2, a3};
+    float* dst[4] = {b0, b1, b2, b3};
+    for (size_t gi = (size_t)blockIdx.x * 256 + threadIdx.x; gi < groups; gi += (size_t)gridDim.x * 256) {
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const uint4 v = reinterpret_cast<const uint4*>(src[t])[gi];
+            const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+            float o[8];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                o[2 * k] = __uint_as_float(w[k] << 16);
+                o[2 * k + 1] = __uint_as_float(w[k] & 0xffff0000u);
+            }
+            reinterpret_cast<float4*>(dst[t])[2 * gi] = make_float4(o[0], o[1], o[2], o[3]);
+            reinterpret_cast<float4*>(dst[t])[2 * gi + 1] = make_float4(o[4], o[5], o[6], o[7]);
+        }
+    }
+}
+
+__device__ __forceinline__ uint32_t bf16_rne(float x) {
+    uint32_t u = __float_as_uint(x);
+    if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return (u >> 16) | 0x0040u;   // quiet NaN
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+
+__global__ __launch_bounds__(256) void narrow_bf16_kernel(const float* __restrict__ a0, const float* __restrict__ a1,
+                                                          const float* __restrict__ a2, uint16_t* __restrict__ b0,
+                                                          uint16_t* __restrict__ b1, uint16_t* __restrict__ b2,
+                                                          size_t groups) {
+    const float* src[3] = {a0, a1, a2};
+    uint16_t* dst[3] = {b0, b1, b2};
+    for (size_t gi = (size_t)blockIdx.x * 256 + threadIdx.x; gi < groups; gi += (size_t)gridDim.x * 256) {
+#pragma unroll
+        for (int t = 0; t < 3; ++t) {
+            const float4 x = reinterpret_cast<const float4*>(src[t])[2 * gi];
+            const float4 y = reinterpret_cast<const float4*>(src[t])[2 * gi + 1];
+            uint4 o;
+            o.x = bf16_rne(x.x) | (bf16_rne(x.y) << 16);
+            o.y = bf16_rne(x.z) | (bf16_rne(x.w) << 16);
+            o.z = bf16_rne(y.x) | (bf16_rne(y.y) << 16);
+            o.w = bf16_rne(y.z) | (bf16_rne(y.w) << 16);
+            reinterpret_cast<uint4*>(dst[t])[gi] = o;
+        }
+    }
+}
+
+hipError_t launch_widen_bf16(const uint16_t* Q, const uint16_t* K, const uint16_t* V, const uint16_t* G, float* wQ,
+                             float* wK, float* wV, float* wG, size_t count, hipStream_t st) {
+    const size_t groups = count / 8;
+    const unsigned blocks = (unsigned)min((groups + 255) / 256, (size_t)4096);
+    hipLaunchKernelGGL(widen_bf16_kernel, dim3(blocks), dim3(256), 0, st, Q, K, V, G, wQ, wK, wV, wG, groups);
+    return hipGetLastError();
+}
+
+hipError_t launch_narrow_bf16(const float* gQ, const float* gK, const float* gV, uint16_t* dQ, uint16_t* dK,
+                              uint16_t* dV, size_t count, hipStream_t st) {
+    const size_t groups = count / 8;
+    const unsigned blocks = (unsigned)min((groups + 255) / 256, (size_t)4096);
+    hipLaunchKernelGGL(narrow_bf16_kernel, dim3(blocks), dim3(256), 0, st, gQ, gK, gV, dQ, dK, dV, groups);
+    return hipGetLastError();
 }
 
 // ------------------------------------------------------------------------------------------

@@ -421,6 +421,7 @@ __global__ __launch_bounds__(256) void query_out_kernel(const float* __restrict_
         }
         asm volatile("" ::"s"(ta[0]), "s"(ta[16]));
     }
+    if (m & 1) tile[l * TP + m] = 0.f;   // the pair loops read column m (unwritten when d = 64)
     __builtin_amdgcn_wave_barrier();
     f32x16_t acc[2][CB];
 #pragma unroll

@@ -56,6 +56,7 @@ struct Plan {
     size_t qt, kt, vseg, Upart, Xs, cinfo, U, M, vbar;                   // forward
     size_t Aq, dDq, rs, dYd, dvbar_part, dM_part, dkt_part, dU, dvbar,   // backward
         dqtW, dktW, dDk, dqt_part;
+    size_t wQ, wK, wV, wG, gQ, gK, gV;   // bf16 backward: fp32 copies of the inputs, fp32 gradients
     size_t total;
     int MP, nkc, nqb, nlc;
 };
@@ -70,7 +71,7 @@ struct Carver {
     }
 };
 
-Plan make_plan(int BH, int n, int d, int m, int T, bool bwd) {
+Plan make_plan(int BH, int n, int d, int m, int T, bool bwd, bool bf16 = false) {
     Plan p{};
     p.MP = m <= 32 ? 32 : 64;
     p.nkc = (n + kKeyChunk - 1) / kKeyChunk;
@@ -102,6 +103,16 @@ Plan make_plan(int BH, int n, int d, int m, int T, bool bwd) {
         p.dktW = c.take(bh * m * d * f);
         p.dDk = c.take(bh * n * 64 * f);
         p.dqt_part = c.take(bh * p.nlc * m * d * f);
+        if (bf16) {
+            const size_t t = bh * n * d * f;
+            p.wQ = c.take(t);
+            p.wK = c.take(t);
+            p.wV = c.take(t);
+            p.wG = c.take(t);
+            p.gQ = c.take(t);
+            p.gK = c.take(t);
+            p.gV = c.take(t);
+        }
     }
     p.total = (c.off + 255) & ~size_t(255);
     return p;
@@ -267,7 +278,7 @@ extern "C" {
 size_t lapattn_workspace_size(int B, int H, int n, int d, int m, int ns_iters, int dtype, int for_backward) {
     if (check_shape(B, H, n, d, m, 1.f, ns_iters, dtype, LAPATTN_NORM_INLINE, 0.f) != LAPATTN_OK) return 0;
     if (dtype == LAPATTN_BF16 && !for_backward) return make_fast_plan(B * H, n, d, m).total;
-    return make_plan(B * H, n, d, m, ns_iters, for_backward != 0).total;
+    return make_plan(B * H, n, d, m, ns_iters, for_backward != 0, dtype == LAPATTN_BF16).total;
 }
 
 int lapattn_forward(const void* Q, const void* K, const void* V, void* Out, int B, int H, int n, int d, int m,
@@ -316,24 +327,37 @@ int lapattn_backward(const void* Q, const void* K, const void* V, const void* dO
         const float eps = eps_of(opts);
         int rc = check_shape(B, H, n, d, m, lambda, ns_iters, dtype, norm, eps);
         if (rc) return rc;
-        if (dtype != LAPATTN_FP32) return LAPATTN_ERR_UNSUPPORTED;
         rc = check_align({Q, K, V, dOut, dQ, dK, dV}, workspace);
         if (rc) return rc;
         const int BH = B * H;
-        const Plan p = make_plan(BH, n, d, m, ns_iters, true);
+        const bool bf16 = dtype == LAPATTN_BF16;
+        const Plan p = make_plan(BH, n, d, m, ns_iters, true, bf16);
         if (!workspace || workspace_bytes < p.total) return LAPATTN_ERR_WORKSPACE;
         hipStream_t st = reinterpret_cast<hipStream_t>(stream);
         void* ws = workspace;
         Recorder rec(st);
-        hipError_t e = forward_internals(rec, p, Q, K, V, ws, BH, n, d, m, lambda, ns_iters, dtype, eps, true, st);
+        hipError_t e;
+        // bf16 inputs: the backward runs in fp32 on the exact widened values, and the gradients
+        // are rounded to bf16 at the end
+        const size_t cnt = (size_t)BH * n * d;
+        const float* q = bf16 ? at<float>(ws, p.wQ) : static_cast<const float*>(Q);
+        const float* k = bf16 ? at<float>(ws, p.wK) : static_cast<const float*>(K);
+        const float* v = bf16 ? at<float>(ws, p.wV) : static_cast<const float*>(V);
+        const float* g = bf16 ? at<float>(ws, p.wG) : static_cast<const float*>(dOut);
+        float* dq = bf16 ? at<float>(ws, p.gQ) : static_cast<float*>(dQ);
+        float* dk = bf16 ? at<float>(ws, p.gK) : static_cast<float*>(dK);
+        float* dv = bf16 ? at<float>(ws, p.gV) : static_cast<float*>(dV);
+        if (bf16) {
+            e = run_named(rec, "widen", [&] {
+                return lapattn::launch_widen_bf16(static_cast<const uint16_t*>(Q), static_cast<const uint16_t*>(K),
+                                                  static_cast<const uint16_t*>(V), static_cast<const uint16_t*>(dOut),
+                                                  at<float>(ws, p.wQ), at<float>(ws, p.wK), at<float>(ws, p.wV),
+                                                  at<float>(ws, p.wG), cnt, st);
+            });
+            if (e != hipSuccess) return LAPATTN_ERR_HIP;
+        }
+        e = forward_internals(rec, p, q, k, v, ws, BH, n, d, m, lambda, ns_iters, LAPATTN_FP32, eps, true, st);
         if (e != hipSuccess) return LAPATTN_ERR_HIP;
-        const float* q = static_cast<const float*>(Q);
-        const float* k = static_cast<const float*>(K);
-        const float* v = static_cast<const float*>(V);
-        const float* g = static_cast<const float*>(dOut);
-        float* dq = static_cast<float*>(dQ);
-        float* dk = static_cast<float*>(dK);
-        float* dv = static_cast<float*>(dV);
         e = run_named(rec, "bwd_query", [&] {
             return lapattn::launch_bwd_query(norm, q, g, dq, at<float>(ws, p.kt), at<float>(ws, p.M),
                                              at<float>(ws, p.vbar), at<float>(ws, p.Aq), at<float>(ws, p.dDq),
@@ -370,6 +394,11 @@ int lapattn_backward(const void* Q, const void* K, const void* V, const void* dO
                                             at<float>(ws, p.dqt_part), at<float>(ws, p.dkt_part), BH, n, d, m, p.nlc,
                                             st);
         });
+        if (e != hipSuccess || !bf16) return e == hipSuccess ? LAPATTN_OK : LAPATTN_ERR_HIP;
+        e = run_named(rec, "narrow", [&] {
+            return lapattn::launch_narrow_bf16(dq, dk, dv, static_cast<uint16_t*>(dQ), static_cast<uint16_t*>(dK),
+                                               static_cast<uint16_t*>(dV), cnt, st);
+        });
         return e == hipSuccess ? LAPATTN_OK : LAPATTN_ERR_HIP;
     } catch (...) {
         return LAPATTN_ERR_HIP;
@@ -382,7 +411,7 @@ const char* lapattn_status_str(int status) {
         case LAPATTN_ERR_NULL: return "null pointer argument";
         case LAPATTN_ERR_SHAPE: return "invalid shape (B, H, n >= 1, 1 <= m <= n, B*H*n*d < 2^31)";
         case LAPATTN_ERR_PARAM: return "invalid parameter (lambda, ns_iters, eps, norm or dtype)";
-        case LAPATTN_ERR_UNSUPPORTED: return "unsupported configuration (d in {32, 64}, m <= 64, fp32 backward)";
+        case LAPATTN_ERR_UNSUPPORTED: return "unsupported configuration (d in {32, 64}, m <= 64)";
         case LAPATTN_ERR_WORKSPACE: return "workspace missing or too small";
         case LAPATTN_ERR_HIP: return "HIP launch failed";
         case LAPATTN_ERR_ALIGN: return "a tensor is not 16-byte aligned or the workspace not 256-byte aligned";

@@ -73,6 +73,13 @@ hipError_t launch_bwd_pool(float* dQ, float* dK, const float* dqtW, const float*
                            const float* dqt_part, const float* dkt_part,
                            int BH, int n, int d, int m, int nlc, hipStream_t st);
 
+// bf16 backward: the four inputs widened to fp32 (exact), the three fp32 gradients rounded to
+// bf16 (nearest even); count elements each, a multiple of 8, 16-byte aligned arrays.
+hipError_t launch_widen_bf16(const uint16_t* Q, const uint16_t* K, const uint16_t* V, const uint16_t* G, float* wQ,
+                             float* wK, float* wV, float* wG, size_t count, hipStream_t st);
+hipError_t launch_narrow_bf16(const float* gQ, const float* gK, const float* gV, uint16_t* dQ, uint16_t* dK,
+                              uint16_t* dV, size_t count, hipStream_t st);
+
 // bf16 fast forward path (fast.hip) -------------------------------------------------------
 
 hipError_t launch_fast_pool(const void* Q, const void* K, const void* V, float* qt, float* kt, double* vseg,

@@ -79,9 +79,14 @@ def test_argument_validation(call):
     assert call(workspace=0, workspace_bytes=need) == L.LAPATTN_ERR_WORKSPACE
 
 
-def test_backward_rejects_bf16_before_launch():
-    need = L.lapattn_workspace_size(1, 2, 100, 32, 8, 4, 1, 1)
-    assert bwd(dtype=1, workspace_bytes=need) == L.LAPATTN_ERR_UNSUPPORTED
+def test_backward_bf16_workspace():
+    """The bf16 backward runs the fp32 backward on widened copies of its four inputs and
+    rounds the three fp32 gradients: its workspace holds seven more B*H*n*d fp32 arrays, and a
+    call given only the fp32 amount is rejected before any launch."""
+    f32 = L.lapattn_workspace_size(1, 2, 100, 32, 8, 4, 0, 1)
+    b16 = L.lapattn_workspace_size(1, 2, 100, 32, 8, 4, 1, 1)
+    assert b16 >= f32 + 7 * (2 * 100 * 32 * 4)
+    assert bwd(dtype=1, workspace_bytes=f32) == L.LAPATTN_ERR_WORKSPACE
 
 
 def test_workspace_size_monotone_and_invalid():

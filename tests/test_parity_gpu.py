@@ -171,7 +171,7 @@ def test_forward_full_size_sampled_heads(L, name):
 def check_backward(L, w, norm=0, eps=0.0, heads=None):
     say("backward %s B=%d H=%d n=%d d=%d m=%d T=%d norm=%d eps=%g" % (w.name, w.B, w.H, w.n, w.d, w.m, w.T, norm, eps))
     x = W.make_inputs(w, with_grad=True)
-    Q, K, V, dO = (to_dev(x[k], "fp32") for k in ("Q", "K", "V", "dO"))
+    Q, K, V, dO = (to_dev(x[k], w.dtype) for k in ("Q", "K", "V", "dO"))
     dQ, dK, dV = L.backward(Q, K, V, dO, w.m, w.lam, w.T, norm=norm, eps=eps)
     torch.cuda.synchronize()
     got = [to_np(t) for t in (dQ, dK, dV)]
@@ -186,7 +186,7 @@ def check_backward(L, w, norm=0, eps=0.0, heads=None):
     say("  dQ %.3e dK %.3e dV %.3e" % tuple(errs))
     for g in got:
         assert np.isfinite(g).all()
-    assert max(errs) <= TOL["fp32"]
+    assert max(errs) <= TOL[w.dtype]
 
 
 @pytest.mark.parametrize("norm", [0, 1, 2])
@@ -214,14 +214,15 @@ def test_backward_full_size_sampled_heads(L):
 def test_backward_deterministic(L):
     w = W.small(W.WORKLOADS["train"], n=1000, B=1, H=2)
     x = W.make_inputs(w, with_grad=True)
-    Q, K, V, dO = (to_dev(x[k], "fp32") for k in ("Q", "K", "V", "dO"))
+    Q, K, V, dO = (to_dev(x[k], w.dtype) for k in ("Q", "K", "V", "dO"))
     a = [to_np(t) for t in L.backward(Q, K, V, dO, w.m, w.lam, w.T)]
     b = [to_np(t) for t in L.backward(Q, K, V, dO, w.m, w.lam, w.T)]
     assert all(np.array_equal(p, q) for p, q in zip(a, b))
 
 
-def test_backward_rejects_bf16(L):
-    x = torch.zeros((1, 1, 64, 32), dtype=torch.bfloat16, device="cuda")
-    with pytest.raises(L.LapattnError) as e:
-        L.backward(x, x, x, x, 4, 1.0, 2)
-    assert e.value.code == L.LAPATTN_ERR_UNSUPPORTED
+@pytest.mark.parametrize("norm", [0, 1, 2])
+def test_backward_bf16(L, norm):
+    """bf16 inputs: the fp32 backward on the widened values, gradients rounded to bf16."""
+    w = W.small(W.WORKLOADS["train"], n=700, B=1, H=2).with_(dtype="bf16")
+    check_backward(L, w, norm=norm)
+    check_backward(L, w.with_(d=64, sigma=0.125, lam=8.0, n=333, m=37), norm=norm)

@@ -12,6 +12,7 @@ from .oracle import (  # noqa: F401
     load,
     kernel,
     segments,
+    windows,
     ns,
     forward,
     backward,

@@ -8,7 +8,9 @@
  *
  * What each step follows:
  *   kernel             k(x,y) = exp(-||x-y||_1/lambda)            Sec. 1, Sec. 4.1, Eq. (8)
- *   landmarks          segment means of consecutive tokens        Sec. 4.2 "Sampling strategies" (R5)
+ *   landmarks          segment means of consecutive tokens        Sec. 4.2 "Sampling strategies" (R5),
+ *                      or means of r x r windows of the H' x W' token map (average
+ *                      pooling with kernel r and stride r, the same passage)
  *   K_LL, K_QL, K_LK   Algorithm 1 (kernel on sampled points, cross-kernel),
  *                      in the orientation K_QL * X * K_LK           (R1)
  *   Newton-Schulz      Algorithm 2: W += eps*I, X0 = W^T/c, X <- X(2I - W X)
@@ -47,6 +49,26 @@ double lapattn_oracle_kernel(const double* x, const double* y, int d, double lam
 int lapattn_oracle_segments(int n, int m, int* starts) {
     if (n < 1 || m < 1 || m > n) return 1;
     for (int l = 0; l <= m; ++l) starts[l] = (int)(((long long)l * n) / m);
+    return 0;
+}
+
+int lapattn_oracle_windows(int n, int m, int grid_w, int r, int* starts, int* members) {
+    if (grid_w == 0 && r == 0) {
+        if (lapattn_oracle_segments(n, m, starts)) return 1;
+        for (int i = 0; i < n; ++i) members[i] = i;
+        return 0;
+    }
+    /* tokens in row-major order on an H' x W' map, W' = grid_w; r must divide H' and W' */
+    if (grid_w < 1 || r < 1 || n % grid_w) return 1;
+    const int hp = n / grid_w;
+    if (hp % r || grid_w % r || m != (hp / r) * (grid_w / r)) return 1;
+    const int mw = grid_w / r;
+    for (int l = 0; l < m; ++l) {
+        const int wy = l / mw, wx = l % mw;
+        starts[l] = l * r * r;
+        for (int t = 0; t < r * r; ++t) members[l * r * r + t] = (wy * r + t / r) * grid_w + wx * r + t % r;
+    }
+    starts[m] = m * r * r;
     return 0;
 }
 
@@ -115,7 +137,8 @@ double lapattn_oracle_ns(const double* W_in, int m, int T, double eps, double* X
 /* Everything one head's forward produces; the backward reuses it. */
 typedef struct {
     int n, d, m, T, dv;            /* dv = d + 1: values with the ones column */
-    int* starts;                   /* m + 1 */
+    int* starts;                   /* m + 1: landmark l averages members[starts[l] .. starts[l+1]) */
+    int* members;                  /* n token indices, grouped by landmark */
     double *qt, *kt;               /* m x d */
     double *Wk;                    /* m x m, kernel part plus eps on the diagonal */
     double *Xs;                    /* (T+1) x m x m */
@@ -128,9 +151,11 @@ typedef struct {
     double *vbar;                  /* d */
 } head_state;
 
-static void head_alloc(head_state* s, int n, int d, int m, int T) {
+static void head_alloc(head_state* s, int n, int d, int m, int T, int grid_w, int r) {
     s->n = n; s->d = d; s->m = m; s->T = T; s->dv = d + 1;
     s->starts = (int*)malloc((size_t)(m + 1) * sizeof(int));
+    s->members = (int*)malloc((size_t)n * sizeof(int));
+    lapattn_oracle_windows(n, m, grid_w, r, s->starts, s->members);   /* validated by the caller */
     s->qt = (double*)malloc((size_t)m * d * sizeof(double));
     s->kt = (double*)malloc((size_t)m * d * sizeof(double));
     s->Wk = (double*)malloc((size_t)m * m * sizeof(double));
@@ -144,7 +169,7 @@ static void head_alloc(head_state* s, int n, int d, int m, int T) {
 }
 
 static void head_free(head_state* s) {
-    free(s->starts); free(s->qt); free(s->kt); free(s->Wk); free(s->Xs); free(s->Bm);
+    free(s->starts); free(s->members); free(s->qt); free(s->kt); free(s->Wk); free(s->Xs); free(s->Bm);
     free(s->U); free(s->M); free(s->A); free(s->Y); free(s->vbar);
 }
 
@@ -153,13 +178,17 @@ static void head_forward(const double* q, const double* k, const double* v, doub
                          double lambda, int norm, double eps, head_state* s) {
     const int n = s->n, d = s->d, m = s->m, T = s->T, dv = s->dv;
 
-    /* Landmarks (R5): means of the balanced segments [floor(l n/m), floor((l+1) n/m)). */
-    lapattn_oracle_segments(n, m, s->starts);
+    /* Landmarks (R5): means of the balanced segments [floor(l n/m), floor((l+1) n/m)), or of
+     * the r x r windows of the token map (Sec. 4.2), members in window row-major order. */
     for (int l = 0; l < m; ++l) {
         int a0 = s->starts[l], a1 = s->starts[l + 1];
         for (int c = 0; c < d; ++c) {
             double sq = 0.0, sk = 0.0;
-            for (int i = a0; i < a1; ++i) { sq += q[(size_t)i * d + c]; sk += k[(size_t)i * d + c]; }
+            for (int t = a0; t < a1; ++t) {
+                const int i = s->members[t];
+                sq += q[(size_t)i * d + c];
+                sk += k[(size_t)i * d + c];
+            }
             s->qt[l * d + c] = sq / (a1 - a0);
             s->kt[l * d + c] = sk / (a1 - a0);
         }
@@ -233,19 +262,28 @@ static int check_args(int B, int H, int n, int d, int m, double lambda, int T, i
     return 0;
 }
 
+static int check_windows(int n, int m, int grid_w, int r) {
+    int* st = (int*)malloc((size_t)(m + 1) * sizeof(int));
+    int* mem = (int*)malloc((size_t)n * sizeof(int));
+    const int rc = lapattn_oracle_windows(n, m, grid_w, r, st, mem);
+    free(st); free(mem);
+    return rc ? 4 : 0;
+}
+
 int lapattn_oracle_forward(const double* Q, const double* K, const double* V, double* Out,
                            int B, int H, int n, int d, int m, double lambda, int T,
-                           int norm, double eps,
+                           int norm, double eps, int grid_w, int r,
                            double* Qt, double* Kt, double* Wk, double* Xs,
                            double* U, double* M, double* Y, double* vbar) {
     if (!Q || !K || !V || !Out) return 1;
     int rc = check_args(B, H, n, d, m, lambda, T, norm);
     if (rc) return rc;
+    if ((rc = check_windows(n, m, grid_w, r))) return rc;
     const int BH = B * H, dv = d + 1;
     const size_t hs = (size_t)n * d;
     for (int h = 0; h < BH; ++h) {
         head_state s;
-        head_alloc(&s, n, d, m, T);
+        head_alloc(&s, n, d, m, T, grid_w, r);
         head_forward(Q + h * hs, K + h * hs, V + h * hs, Out + h * hs, lambda, norm, eps, &s);
         if (Qt) memcpy(Qt + (size_t)h * m * d, s.qt, (size_t)m * d * sizeof(double));
         if (Kt) memcpy(Kt + (size_t)h * m * d, s.kt, (size_t)m * d * sizeof(double));
@@ -449,12 +487,13 @@ static void head_backward(const double* q, const double* k, const double* v, con
             }
         }
 
-    /* Landmark means: each token of segment l receives d(mean)/|S_l|. */
+    /* Landmark means: each token of segment (window) l receives d(mean)/|S_l|. */
     for (int l = 0; l < m; ++l) {
         int a0 = s->starts[l], a1 = s->starts[l + 1];
         double inv = 1.0 / (a1 - a0);
-        for (int i = a0; i < a1; ++i)
+        for (int t = a0; t < a1; ++t)
             for (int c = 0; c < d; ++c) {
+                const int i = s->members[t];
                 dq[(size_t)i * d + c] += dqt[l * d + c] * inv;
                 dk[(size_t)i * d + c] += dkt[l * d + c] * inv;
             }
@@ -467,15 +506,16 @@ static void head_backward(const double* q, const double* k, const double* v, con
 int lapattn_oracle_backward(const double* Q, const double* K, const double* V,
                             const double* dOut, double* dQ, double* dK, double* dV,
                             int B, int H, int n, int d, int m, double lambda, int T,
-                            int norm, double eps) {
+                            int norm, double eps, int grid_w, int r) {
     if (!Q || !K || !V || !dOut || !dQ || !dK || !dV) return 1;
     int rc = check_args(B, H, n, d, m, lambda, T, norm);
     if (rc) return rc;
+    if ((rc = check_windows(n, m, grid_w, r))) return rc;
     const int BH = B * H;
     const size_t hs = (size_t)n * d;
     for (int h = 0; h < BH; ++h) {
         head_state s;
-        head_alloc(&s, n, d, m, T);
+        head_alloc(&s, n, d, m, T, grid_w, r);
         head_backward(Q + h * hs, K + h * hs, V + h * hs, dOut + h * hs,
                       dQ + h * hs, dK + h * hs, dV + h * hs, lambda, norm, eps, &s);
         head_free(&s);

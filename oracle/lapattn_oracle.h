@@ -18,7 +18,8 @@
  *   R2  NS start X0 = K_LL^T / (||K_LL||_1 * ||K_LL||_inf), per head
  *   R3  perturbation eps of Algorithm 2 is an argument (0 by default)
  *   R4  row normalisation = the injective centring of Eq. (4) with Sigma^{-1/2} = I
- *   R5  landmarks = means of m balanced segments of consecutive tokens
+ *   R5  landmarks = means of m balanced segments of consecutive tokens, or (when a
+ *       token-map width is given) of the r x r windows of the H' x W' map
  *   R8  sign(0) = 0; argmax ties -> lowest index; gradient flows through X0's scale
  *   R9  T counts NS updates; T = 0 returns X0
  *   R10 if the X0 scale is 0, X_t := 0 for every t
@@ -38,6 +39,15 @@ double lapattn_oracle_kernel(const double* x, const double* y, int d, double lam
 /* Segment boundaries (R5): starts[l] = floor(l*n/m), l = 0..m (starts[m] = n). */
 int lapattn_oracle_segments(int n, int m, int* starts);
 
+/* Landmark membership: landmark l averages tokens members[starts[l] .. starts[l+1]).
+ * grid_w = r = 0: the balanced segments of lapattn_oracle_segments (members[i] = i).
+ * Otherwise the tokens form an H' x W' map in row-major order (W' = grid_w, H' = n / W')
+ * and landmark l = Y (W'/r) + X averages the r x r window at rows Y r.., columns X r..
+ * (Sec. 4.2, average pooling with kernel and stride r); r must divide H' and W' and
+ * m must equal (H'/r)(W'/r).  starts has m + 1 entries, members n.  Returns nonzero
+ * on invalid arguments. */
+int lapattn_oracle_windows(int n, int m, int grid_w, int r, int* starts, int* members);
+
 /* Newton-Schulz iteration of Algorithm 2 on one m x m matrix W (R2, R3, R9, R10).
  * Xs receives X_0 .. X_T, (T+1)*m*m doubles.  Returns the X0 scale c. */
 double lapattn_oracle_ns(const double* W, int m, int T, double eps, double* Xs);
@@ -51,10 +61,11 @@ double lapattn_oracle_ns(const double* W, int m, int T, double eps, double* Xs);
  *   M       [BH][m][d+1]   X_T * U
  *   Y       [BH][n][d+1]   K_QL * M   (column d is the row sum s_i of G^)
  *   vbar    [BH][d]        mean of the values
+ * grid_w, r select the landmark windows (lapattn_oracle_windows; 0, 0 = segments).
  * Returns 0 on success, nonzero on a bad argument. */
 int lapattn_oracle_forward(const double* Q, const double* K, const double* V, double* Out,
                            int B, int H, int n, int d, int m, double lambda, int T,
-                           int norm, double eps,
+                           int norm, double eps, int grid_w, int r,
                            double* Qt, double* Kt, double* Wk, double* Xs,
                            double* U, double* M, double* Y, double* vbar);
 
@@ -63,7 +74,7 @@ int lapattn_oracle_forward(const double* Q, const double* K, const double* V, do
 int lapattn_oracle_backward(const double* Q, const double* K, const double* V,
                             const double* dOut, double* dQ, double* dK, double* dV,
                             int B, int H, int n, int d, int m, double lambda, int T,
-                            int norm, double eps);
+                            int norm, double eps, int grid_w, int r);
 
 /* Number of OpenMP threads the oracle's parallel loops use. */
 int lapattn_oracle_threads(void);

@@ -68,11 +68,13 @@ def _configure(lib):
     lib.lapattn_oracle_ns.restype = ctypes.c_double
     lib.lapattn_oracle_ns.argtypes = [_dp, ctypes.c_int, ctypes.c_int, ctypes.c_double, _dp]
     lib.lapattn_oracle_forward.restype = ctypes.c_int
+    lib.lapattn_oracle_windows.restype = ctypes.c_int
+    lib.lapattn_oracle_windows.argtypes = [ctypes.c_int] * 4 + [ctypes.POINTER(ctypes.c_int)] * 2
     lib.lapattn_oracle_forward.argtypes = ([_dp] * 4 + [ctypes.c_int] * 5 + [ctypes.c_double, ctypes.c_int,
-                                           ctypes.c_int, ctypes.c_double] + [_dp] * 8)
+                                           ctypes.c_int, ctypes.c_double, ctypes.c_int, ctypes.c_int] + [_dp] * 8)
     lib.lapattn_oracle_backward.restype = ctypes.c_int
     lib.lapattn_oracle_backward.argtypes = ([_dp] * 7 + [ctypes.c_int] * 5 + [ctypes.c_double, ctypes.c_int,
-                                            ctypes.c_int, ctypes.c_double])
+                                            ctypes.c_int, ctypes.c_double, ctypes.c_int, ctypes.c_int])
     lib.lapattn_oracle_threads.restype = ctypes.c_int
     lib.lapattn_oracle_threads.argtypes = []
     return lib
@@ -104,6 +106,17 @@ def segments(n, m):
     return np.array(list(starts), dtype=np.int64)
 
 
+def windows(n, m, grid=None):
+    """(starts, members) of the landmark membership; grid = (W', r) for r x r windows of the
+    H' x W' token map, None for the balanced segments."""
+    gw, r = grid if grid is not None else (0, 0)
+    starts = (ctypes.c_int * (m + 1))()
+    members = (ctypes.c_int * n)()
+    if load().lapattn_oracle_windows(int(n), int(m), int(gw), int(r), starts, members):
+        raise ValueError("bad landmark windows n=%d m=%d grid=%r" % (n, m, grid))
+    return np.array(list(starts), dtype=np.int64), np.array(list(members), dtype=np.int64)
+
+
 def ns(W, T, eps=0.0):
     """Returns (Xs, c): Xs[t] = X_t for t = 0..T, c = the X0 scale."""
     W = _f64(W)
@@ -114,7 +127,7 @@ def ns(W, T, eps=0.0):
     return Xs, c
 
 
-def forward(Q, K, V, m, lam, T, norm=NORM_INLINE, eps=0.0, intermediates=False):
+def forward(Q, K, V, m, lam, T, norm=NORM_INLINE, eps=0.0, intermediates=False, grid=None):
     Q, K, V = _f64(Q), _f64(K), _f64(V)
     B, H, n, d = Q.shape
     assert K.shape == Q.shape and V.shape == Q.shape
@@ -127,19 +140,22 @@ def forward(Q, K, V, m, lam, T, norm=NORM_INLINE, eps=0.0, intermediates=False):
             Xs=np.empty((B, H, T + 1, m, m)), U=np.empty((B, H, m, d + 1)), M=np.empty((B, H, m, d + 1)),
             Y=np.empty((B, H, n, d + 1)), vbar=np.empty((B, H, d)))
         ptrs = [inter[k] for k in ("Qt", "Kt", "W", "Xs", "U", "M", "Y", "vbar")]
+    gw, r = grid if grid is not None else (0, 0)
     rc = load().lapattn_oracle_forward(_p(Q), _p(K), _p(V), _p(out), B, H, n, d, int(m), float(lam),
-                                       int(T), int(norm), float(eps), *[_p(a) for a in ptrs])
+                                       int(T), int(norm), float(eps), int(gw), int(r), *[_p(a) for a in ptrs])
     if rc:
         raise ValueError("oracle forward rejected its arguments (code %d)" % rc)
     return (out, inter) if intermediates else out
 
 
-def backward(Q, K, V, dO, m, lam, T, norm=NORM_INLINE, eps=0.0):
+def backward(Q, K, V, dO, m, lam, T, norm=NORM_INLINE, eps=0.0, grid=None):
     Q, K, V, dO = _f64(Q), _f64(K), _f64(V), _f64(dO)
     B, H, n, d = Q.shape
     dQ, dK, dV = np.empty_like(Q), np.empty_like(Q), np.empty_like(Q)
+    gw, r = grid if grid is not None else (0, 0)
     rc = load().lapattn_oracle_backward(_p(Q), _p(K), _p(V), _p(dO), _p(dQ), _p(dK), _p(dV),
-                                        B, H, n, d, int(m), float(lam), int(T), int(norm), float(eps))
+                                        B, H, n, d, int(m), float(lam), int(T), int(norm), float(eps),
+                                        int(gw), int(r))
     if rc:
         raise ValueError("oracle backward rejected its arguments (code %d)" % rc)
     return dQ, dK, dV

@@ -425,3 +425,60 @@ def test_backward_scale_term_is_needed(oracle_lib):
     Q, K, V = rand_qkv(rng, 1, 1, 8, 2)
     dO = rng.standard_normal(Q.shape)
     assert fd_check(Q, K, V, dO, 8, 1.0, 0, oracle.NORM_NONE) < 1e-7   # T = 0: output = A W^T/c B V
+
+
+# ----------------------------------------------------------------------------- 2-D windows
+
+def window_order(hp, wp, r):
+    """Token indices of an hp x wp row-major map grouped by r x r window (windows row-major,
+    tokens row-major inside a window), built by reshaping the map -- the layout average
+    pooling with kernel r and stride r works on (Sec. 4.2)."""
+    idx = np.arange(hp * wp).reshape(hp // r, r, wp // r, r)
+    return idx.transpose(0, 2, 1, 3).reshape(-1)
+
+
+@pytest.mark.parametrize("hp,wp,r", [(4, 6, 2), (6, 6, 3), (8, 4, 2), (3, 9, 3)])
+def test_windows_landmarks_are_average_pooling(oracle_lib, hp, wp, r):
+    """The landmark means of the windowed oracle equal numpy's r x r average pooling of the
+    token map, in the row-major order of the pooled map."""
+    rng = np.random.default_rng(hp * 100 + wp * 10 + r)
+    n, m, d = hp * wp, (hp // r) * (wp // r), 3
+    Q, K, V = rand_qkv(rng, 1, 2, n, d)
+    _, inter = oracle.forward(Q, K, V, m, 2.0, 3, intermediates=True, grid=(wp, r))
+    pool = lambda X: X.reshape(1, 2, hp // r, r, wp // r, r, d).mean(axis=(3, 5)).reshape(1, 2, m, d)
+    assert np.allclose(inter["Qt"], pool(Q), rtol=1e-13, atol=1e-14)
+    assert np.allclose(inter["Kt"], pool(K), rtol=1e-13, atol=1e-14)
+
+
+@pytest.mark.parametrize("norm", [oracle.NORM_INLINE, oracle.NORM_ROWSUM])
+def test_windows_equal_segments_of_the_window_ordered_tokens(oracle_lib, norm):
+    """Everything after pooling treats tokens alike, so the windowed forward and backward on a
+    token map equal the segment forward and backward on the tokens listed window by window
+    (each window is then one segment of r^2 consecutive tokens), permuted back."""
+    hp, wp, r, d = 6, 8, 2, 3
+    n, m = hp * wp, (hp // r) * (wp // r)
+    perm = window_order(hp, wp, r)
+    rng = np.random.default_rng(77 + norm)
+    Q, K, V = rand_qkv(rng, 1, 2, n, d, 0.6)
+    dO = rng.standard_normal(Q.shape)
+    out2 = oracle.forward(Q, K, V, m, 1.7, 4, norm, grid=(wp, r))
+    out1 = oracle.forward(Q[:, :, perm], K[:, :, perm], V[:, :, perm], m, 1.7, 4, norm)
+    assert rel(out2[:, :, perm], out1) < 1e-13
+    g2 = oracle.backward(Q, K, V, dO, m, 1.7, 4, norm, grid=(wp, r))
+    g1 = oracle.backward(Q[:, :, perm], K[:, :, perm], V[:, :, perm], dO[:, :, perm], m, 1.7, 4, norm)
+    for a, b in zip(g2, g1):
+        assert rel(a[:, :, perm], b) < 1e-12
+
+
+def test_windows_special_cases_and_rejections(oracle_lib):
+    rng = np.random.default_rng(5)
+    Q, K, V = rand_qkv(rng, 1, 1, 12, 2)
+    # r = 1: every token is a landmark, as segments with m = n
+    assert rel(oracle.forward(Q, K, V, 12, 1.0, 5, grid=(4, 1)), oracle.forward(Q, K, V, 12, 1.0, 5)) < 1e-14
+    # one window covering the map: the global mean, as one segment
+    Q2, K2, V2 = rand_qkv(rng, 1, 1, 9, 2)
+    assert rel(oracle.forward(Q2, K2, V2, 1, 1.0, 3, grid=(3, 3)), oracle.forward(Q2, K2, V2, 1, 1.0, 3)) < 1e-14
+    # r must divide both sides, n must fill the map, m must match the pooled map
+    for grid, m in (((4, 3), 1), ((5, 1), 12), ((4, 2), 4), ((6, 2), 4)):
+        with pytest.raises(ValueError):
+            oracle.forward(Q, K, V, m, 1.0, 2, grid=grid)

@@ -33,6 +33,11 @@ MUTANTS = {
     "ones column wrong": ("(c < d ? v[(size_t)j * d + c] : 1.0)", "(c < d ? v[(size_t)j * d + c] : 0.5)"),
     "l2 instead of l1": ("dist += fabs(x[c] - y[c]);", "dist += (x[c] - y[c]) * (x[c] - y[c]);"),
     "eps ignored": ("for (int a = 0; a < m; ++a) W[a * m + a] += eps;", "(void)eps;"),
+    "window rows and columns swapped": ("const int wy = l / mw, wx = l % mw;", "const int wy = l % mw, wx = l / mw;"),
+    "window row stride r instead of the map width": (
+        "members[l * r * r + t] = (wy * r + t / r) * grid_w + wx * r + t % r;",
+        "members[l * r * r + t] = (wy * r + t / r) * r + wx * r + t % r;"),
+    "window backward spread to segments": ("const int i = s->members[t];\n                dq[", "const int i = t;\n                dq["),
     "query/key landmarks swapped in K_LL": (
         "s->Wk[a * m + b] = lapattn_oracle_kernel(s->qt + a * d, s->kt + b * d, d, lambda);",
         "s->Wk[a * m + b] = lapattn_oracle_kernel(s->kt + a * d, s->qt + b * d, d, lambda);"),
@@ -55,6 +60,9 @@ PIN_CALLS = [
     lambda: pins.test_backward_matches_finite_differences(None, oracle.NORM_ROWSUM, 13, 3, 5, 4, 1.5),
     lambda: pins.test_backward_matches_finite_differences(None, oracle.NORM_INLINE, 17, 4, 4, 6, 4.0),
     lambda: pins.test_backward_with_perturbation_and_two_heads(None),
+    lambda: pins.test_windows_landmarks_are_average_pooling(None, 4, 6, 2),
+    lambda: pins.test_windows_equal_segments_of_the_window_ordered_tokens(None, oracle.NORM_INLINE),
+    lambda: pins.test_windows_special_cases_and_rejections(None),
 ]
 
 

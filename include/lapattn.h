@@ -66,9 +66,11 @@ typedef enum {
 enum {
     LAPATTN_OK = 0,
     LAPATTN_ERR_NULL = 1,         /* a required pointer is NULL */
-    LAPATTN_ERR_SHAPE = 2,        /* B, H, n < 1, m < 1, m > n, or B*H*n*d >= 2^31 */
+    LAPATTN_ERR_SHAPE = 2,        /* B, H, n < 1, m < 1, m > n, B*H*n*d >= 2^31, or landmark
+                                     windows that do not tile the token map (lapattn_opts) */
     LAPATTN_ERR_PARAM = 3,        /* lambda not finite or <= 0, ns_iters outside [0, 64],
-                                     eps not finite or < 0, unknown norm or dtype */
+                                     eps not finite or < 0, unknown norm or dtype,
+                                     window options negative or only one of them set */
     LAPATTN_ERR_UNSUPPORTED = 4,  /* d not in {32, 64} or m > 64 */
     LAPATTN_ERR_WORKSPACE = 5,    /* workspace NULL or smaller than lapattn_workspace_size() */
     LAPATTN_ERR_HIP = 6,          /* a HIP launch failed */
@@ -76,11 +78,21 @@ enum {
                                      workspace is not 256-byte aligned */
 };
 
-/* Options; a NULL pointer means {LAPATTN_NORM_INLINE, 0.0f}.
- * eps is the diagonal perturbation W <- W + eps I of Algorithm 2 (>= 0). */
+/* Options; a NULL pointer means {LAPATTN_NORM_INLINE, 0.0f, 0, 0}.
+ * eps is the diagonal perturbation W <- W + eps I of Algorithm 2 (>= 0).
+ * Landmarks (Sec. 4.2, sampling): with grid_w = pool_r = 0 they are the means of m
+ * balanced segments of consecutive tokens, [floor(l n/m), floor((l+1) n/m)).  With
+ * grid_w > 0 the n tokens form a row-major H' x W' map (W' = grid_w, H' = n / W') and
+ * the landmarks are the means of its r x r windows (r = pool_r; average pooling with
+ * kernel and stride r), landmark l = Y (W'/r) + X for the window at rows Y r..,
+ * columns X r..; r must divide H' and W', and m must equal (H'/r)(W'/r)
+ * (LAPATTN_ERR_SHAPE otherwise; a negative value, or only one of the two set, is
+ * LAPATTN_ERR_PARAM). */
 typedef struct {
     int norm;      /* lapattn_norm */
     float eps;
+    int grid_w;    /* token-map width W', or 0 for segments */
+    int pool_r;    /* window side r, or 0 for segments */
 } lapattn_opts;
 
 /* Bytes of device workspace lapattn_forward (for_backward = 0) or

@@ -776,16 +776,18 @@ __global__ __launch_bounds__(64) void bwd_key_lm_kernel(const float* __restrict_
 // ------------------------------------------------------------------------------------------
 // Landmark-mean backward.  grid (m, BH), 256 threads: dq_l = dqtW_l + sum of the key-side
 // partials, dk_l = dktW_l + sum of the query-side partials (chunk order, fp64), then
-// dQ_i += dq_l / |S_l| and dK_i += dk_l / |S_l| over the segment's rows.
+// dQ_i += dq_l / |S_l| and dK_i += dk_l / |S_l| over the landmark's tokens: one contiguous run
+// for a segment, r runs of r tokens for a window; four floats at a time.
 __global__ __launch_bounds__(256) void bwd_pool_kernel(float* __restrict__ dQ, float* __restrict__ dK,
                                                        const float* __restrict__ dqtW, const float* __restrict__ dktW,
                                                        const float* __restrict__ dqt_part,
                                                        const float* __restrict__ dkt_part, int n, int d, int m,
-                                                       int nlc) {
+                                                       int nlc, LmPool pl) {
     const int l = blockIdx.x, h = blockIdx.y, tid = threadIdx.x;
     __shared__ float sq[64], sk[64];
-    const int s0 = seg_start(l, n, m), s1 = seg_start(l + 1, n, m);
-    const float inv = 1.f / (float)(s1 - s0);
+    const LmTokens tok = lm_tokens(pl, l, n, m);
+    const int cntl = tok.count;
+    const float inv = 1.f / (float)cntl;
     if (tid < d) {
         const size_t o = ((size_t)h * m + l) * d + tid;
         double aq = dqtW[o], ak = dktW[o];
@@ -799,18 +801,20 @@ __global__ __launch_bounds__(256) void bwd_pool_kernel(float* __restrict__ dQ, f
         sk[tid] = (float)ak * inv;
     }
     __syncthreads();
-    // the segment's rows are contiguous: (s1 - s0) d floats from row s0, four at a time
-    const size_t base = ((size_t)h * n + s0) * d;
-    const int cnt4 = (s1 - s0) * d / 4;
-    float4* q4 = reinterpret_cast<float4*>(dQ + base);
-    float4* k4 = reinterpret_cast<float4*>(dK + base);
-    for (int e = tid; e < cnt4; e += 256) {
-        const int c = (4 * e) % d;
-        float4 a = q4[e], b = k4[e];
-        a.x += sq[c]; a.y += sq[c + 1]; a.z += sq[c + 2]; a.w += sq[c + 3];
-        b.x += sk[c]; b.y += sk[c + 1]; b.z += sk[c + 2]; b.w += sk[c + 3];
-        q4[e] = a;
-        k4[e] = b;
+    const int runs = pl.r ? pl.r : 1, run_len = pl.r ? pl.r : cntl;
+    for (int k = 0; k < runs; ++k) {
+        const size_t base = ((size_t)h * n + tok(k * run_len)) * d;
+        const int cnt4 = run_len * d / 4;
+        float4* q4 = reinterpret_cast<float4*>(dQ + base);
+        float4* k4 = reinterpret_cast<float4*>(dK + base);
+        for (int e = tid; e < cnt4; e += 256) {
+            const int c = (4 * e) % d;
+            float4 a = q4[e], b = k4[e];
+            a.x += sq[c]; a.y += sq[c + 1]; a.z += sq[c + 2]; a.w += sq[c + 3];
+            b.x += sk[c]; b.y += sk[c + 1]; b.z += sk[c + 2]; b.w += sk[c + 3];
+            q4[e] = a;
+            k4[e] = b;
+        }
     }
 }
 
@@ -960,9 +964,9 @@ hipError_t launch_bwd_key_lm(const float* K, const float* qt, const float* dDk, 
 }
 
 hipError_t launch_bwd_pool(float* dQ, float* dK, const float* dqtW, const float* dktW, const float* dqt_part,
-                           const float* dkt_part, int BH, int n, int d, int m, int nlc, hipStream_t st) {
+                           const float* dkt_part, int BH, int n, int d, int m, int nlc, LmPool pl, hipStream_t st) {
     hipLaunchKernelGGL(bwd_pool_kernel, dim3(m, BH), dim3(256), 0, st, dQ, dK, dqtW, dktW, dqt_part, dkt_part, n, d,
-                       m, nlc);
+                       m, nlc, pl);
     return hipGetLastError();
 }
 

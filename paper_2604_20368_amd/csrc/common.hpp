@@ -42,6 +42,37 @@ __device__ __host__ __forceinline__ int seg_of(int i, int n, int m) {
     return (int)((((long long)i + 1) * m - 1) / n);
 }
 
+// Landmark l's tokens (Sec. 4.2 sampling): with r == 0 the balanced segment above; otherwise
+// the tokens form a row-major map of width gw (height n / gw, both multiples of r) and
+// landmark l = Y (gw / r) + X averages the r x r window at rows Y r.., columns X r.. .
+struct LmPool {
+    int gw, r;
+};
+// One landmark's tokens: count, and the t-th token (window tokens in row-major order).
+struct LmTokens {
+    int count, s0, r, gw, y0, x0;
+    __device__ __host__ __forceinline__ int operator()(int t) const {
+        return r ? (y0 + t / r) * gw + x0 + t % r : s0 + t;
+    }
+};
+__device__ __host__ __forceinline__ LmTokens lm_tokens(LmPool p, int l, int n, int m) {
+    LmTokens k;
+    k.r = p.r;
+    k.gw = p.gw;
+    if (!p.r) {
+        k.s0 = seg_start(l, n, m);
+        k.count = seg_start(l + 1, n, m) - k.s0;
+        k.y0 = k.x0 = 0;
+    } else {
+        const int mw = p.gw / p.r;
+        k.s0 = 0;
+        k.count = p.r * p.r;
+        k.y0 = (l / mw) * p.r;
+        k.x0 = (l % mw) * p.r;
+    }
+    return k;
+}
+
 __device__ __forceinline__ float sgnf(float x) { return (float)((x > 0.f) - (x < 0.f)); }
 __device__ __forceinline__ double sgnd(double x) { return (double)((x > 0.0) - (x < 0.0)); }
 

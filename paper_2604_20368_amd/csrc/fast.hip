@@ -104,9 +104,9 @@ __device__ __forceinline__ int xcd_rank(int i, int n, int base) {
 }
 
 // ------------------------------------------------------------------------------------------
-// Landmark means and per-segment statistics.  grid (m, BH), 256 threads.  Thread t always
-// reads the 8-column group t % (D/8) of its rows (rows t / (D/8) + (256 / (D/8)) i), all of a
-// segment's rows in flight four per thread at a time.  Sums: per thread in fp32, then over the
+// Landmark means and per-landmark statistics.  grid (m, BH), 256 threads.  Thread t always
+// reads the 8-column group t % (D/8) of its rows (the landmark's tokens t / (D/8) + (256 / (D/8)) i
+// of its segment or window, lm_tokens), four rows per thread in flight at a time.  Sums: per thread in fp32, then over the
 // lanes of a wave that share a column group (a butterfly), then over the four waves in a fixed
 // order in fp64.
 template <int D>
@@ -114,25 +114,26 @@ __global__ __launch_bounds__(256) void pool2_kernel(const uint16_t* __restrict__
                                                     const uint16_t* __restrict__ V, float* __restrict__ qt,
                                                     float* __restrict__ kt, double* __restrict__ vseg,
                                                     float* __restrict__ segmax, float* __restrict__ vsegmax, int n,
-                                                    int m) {
+                                                    int m, LmPool pl) {
     constexpr int CPR = D / 8;      // 16-byte chunks per row
     constexpr int RPI = 256 / CPR;  // rows per block iteration
     constexpr int UNR = 4;          // row iterations in flight
     const int l = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
-    const int s0 = seg_start(l, n, m), s1 = seg_start(l + 1, n, m);
+    const LmTokens tok = lm_tokens(pl, l, n, m);   // the landmark's tokens tok(0 .. count - 1)
+    const int cntl = tok.count;
     const int cg = tid % CPR, r0 = tid / CPR;
     float sq[8], sk[8], sv[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) sq[j] = sk[j] = sv[j] = 0.f;
     float mx = 0.f, vmx = 0.f;
     const size_t base = (size_t)h * n * D + cg * 8;
-    for (int i0 = s0 + r0; i0 < s1; i0 += UNR * RPI) {
+    for (int t0 = r0; t0 < cntl; t0 += UNR * RPI) {
         uint4 a[UNR], b[UNR], c[UNR];
 #pragma unroll
         for (int u = 0; u < UNR; ++u) {
-            const int i = i0 + u * RPI;
-            if (i < s1) {
-                const size_t off = base + (size_t)i * D;
+            const int t = t0 + u * RPI;
+            if (t < cntl) {
+                const size_t off = base + (size_t)tok(t) * D;
                 a[u] = *reinterpret_cast<const uint4*>(Q + off);
                 b[u] = *reinterpret_cast<const uint4*>(K + off);
                 c[u] = *reinterpret_cast<const uint4*>(V + off);
@@ -188,7 +189,7 @@ __global__ __launch_bounds__(256) void pool2_kernel(const uint16_t* __restrict__
         svmx[w] = vmx;
     }
     __syncthreads();
-    const double cnt = (double)(s1 - s0);
+    const double cnt = (double)cntl;
     bool bad = false;
     if (tid < 3 * D) {
         const int a3 = tid / D, col = tid % D;
@@ -1088,14 +1089,14 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
 // Launch wrappers.
 
 hipError_t launch_fast_pool(const void* Q, const void* K, const void* V, float* qt, float* kt, double* vseg,
-                            float* segmax, float* vsegmax, int BH, int n, int d, int m, hipStream_t st) {
+                            float* segmax, float* vsegmax, int BH, int n, int d, int m, LmPool pl, hipStream_t st) {
     dim3 grid(m, BH);
     if (d == 32)
         hipLaunchKernelGGL(pool2_kernel<32>, grid, dim3(256), 0, st, (const uint16_t*)Q, (const uint16_t*)K,
-                           (const uint16_t*)V, qt, kt, vseg, segmax, vsegmax, n, m);
+                           (const uint16_t*)V, qt, kt, vseg, segmax, vsegmax, n, m, pl);
     else
         hipLaunchKernelGGL(pool2_kernel<64>, grid, dim3(256), 0, st, (const uint16_t*)Q, (const uint16_t*)K,
-                           (const uint16_t*)V, qt, kt, vseg, segmax, vsegmax, n, m);
+                           (const uint16_t*)V, qt, kt, vseg, segmax, vsegmax, n, m, pl);
     return hipGetLastError();
 }
 

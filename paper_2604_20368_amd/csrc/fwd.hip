@@ -13,21 +13,23 @@
 namespace lapattn {
 
 // ------------------------------------------------------------------------------------------
-// Landmark means.  grid (m, BH), 256 threads: thread (r, c) sums rows r, r+R, ... of the
-// segment in column c; the R partial sums are added in a fixed order (deterministic).
+// Landmark means.  grid (m, BH), 256 threads: thread (r, c) sums the landmark's tokens
+// r, r+R, ... (segment or window, lm_tokens) in column c; the R partial sums are added in a
+// fixed order (deterministic).
 template <int DT>
 __global__ __launch_bounds__(256) void pool_kernel(const typename elem<DT>::type* __restrict__ Q,
                                                    const typename elem<DT>::type* __restrict__ K,
                                                    const typename elem<DT>::type* __restrict__ V,
                                                    float* __restrict__ qt, float* __restrict__ kt,
-                                                   double* __restrict__ vseg, int n, int d, int m) {
+                                                   double* __restrict__ vseg, int n, int d, int m, LmPool pl) {
     const int l = blockIdx.x, h = blockIdx.y;
-    const int s0 = seg_start(l, n, m), s1 = seg_start(l + 1, n, m);
+    const LmTokens tok = lm_tokens(pl, l, n, m);
+    const int cntl = tok.count;
     const int c = threadIdx.x % d, r = threadIdx.x / d, R = blockDim.x / d;
     const size_t base = (size_t)h * n * d;
     double sq = 0.0, sk = 0.0, sv = 0.0;
-    for (int i = s0 + r; i < s1; i += R) {
-        const size_t idx = base + (size_t)i * d + c;
+    for (int t = r; t < cntl; t += R) {
+        const size_t idx = base + (size_t)tok(t) * d + c;
         sq += elem<DT>::load(Q, idx);
         sk += elem<DT>::load(K, idx);
         sv += elem<DT>::load(V, idx);
@@ -44,7 +46,7 @@ __global__ __launch_bounds__(256) void pool_kernel(const typename elem<DT>::type
             b += red[1][rr * d + c];
             e += red[2][rr * d + c];
         }
-        const double cnt = (double)(s1 - s0);
+        const double cnt = (double)cntl;
         const size_t o = ((size_t)h * m + l) * d + c;
         qt[o] = (float)(a / cnt);
         kt[o] = (float)(b / cnt);
@@ -479,14 +481,14 @@ __global__ __launch_bounds__(256) void query_out_kernel(const float* __restrict_
 static inline float kscale_of(float lambda) { return (float)(-1.4426950408889634 / (double)lambda); }
 
 hipError_t launch_pool(int dt, const void* Q, const void* K, const void* V, float* qt, float* kt, double* vseg,
-                       int BH, int n, int d, int m, hipStream_t st) {
+                       int BH, int n, int d, int m, LmPool pl, hipStream_t st) {
     dim3 grid(m, BH);
     if (dt == DT_F32)
         hipLaunchKernelGGL(pool_kernel<DT_F32>, grid, dim3(256), 0, st, (const float*)Q, (const float*)K,
-                           (const float*)V, qt, kt, vseg, n, d, m);
+                           (const float*)V, qt, kt, vseg, n, d, m, pl);
     else
         hipLaunchKernelGGL(pool_kernel<DT_BF16>, grid, dim3(256), 0, st, (const uint16_t*)Q, (const uint16_t*)K,
-                           (const uint16_t*)V, qt, kt, vseg, n, d, m);
+                           (const uint16_t*)V, qt, kt, vseg, n, d, m, pl);
     return hipGetLastError();
 }
 

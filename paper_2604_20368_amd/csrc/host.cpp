@@ -211,17 +211,28 @@ hipError_t run_named(Recorder& rec, const char* name, F&& f) {
 
 int norm_of(const lapattn_opts* o) { return o ? o->norm : LAPATTN_NORM_INLINE; }
 float eps_of(const lapattn_opts* o) { return o ? o->eps : 0.f; }
+lapattn::LmPool pool_of(const lapattn_opts* o) { return o ? lapattn::LmPool{o->grid_w, o->pool_r} : lapattn::LmPool{0, 0}; }
+
+// Landmark geometry: segments (0, 0), or r x r windows of a row-major map of width gw that r
+// divides, as is its height n / gw, with m = (n / gw / r)(gw / r) windows.
+int check_pool(int n, int m, lapattn::LmPool pl) {
+    if (pl.gw == 0 && pl.r == 0) return LAPATTN_OK;
+    if (pl.gw < 1 || pl.r < 1) return LAPATTN_ERR_PARAM;
+    if (n % pl.gw || (n / pl.gw) % pl.r || pl.gw % pl.r) return LAPATTN_ERR_SHAPE;
+    if ((long long)m != (long long)(n / pl.gw / pl.r) * (pl.gw / pl.r)) return LAPATTN_ERR_SHAPE;
+    return LAPATTN_OK;
+}
 
 // The forward stages shared by lapattn_forward and lapattn_backward (which recomputes them).
 hipError_t forward_internals(Recorder& rec, const Plan& p, const void* Q, const void* K, const void* V, void* ws,
                              int BH, int n, int d, int m, float lambda, int T, int dtype, float eps, bool store_all,
-                             hipStream_t st) {
+                             lapattn::LmPool pl, hipStream_t st) {
     float* qt = at<float>(ws, p.qt);
     float* kt = at<float>(ws, p.kt);
     double* vseg = at<double>(ws, p.vseg);
     float* Upart = at<float>(ws, p.Upart);
     hipError_t e;
-    e = run_named(rec, "pool", [&] { return lapattn::launch_pool(dtype, Q, K, V, qt, kt, vseg, BH, n, d, m, st); });
+    e = run_named(rec, "pool", [&] { return lapattn::launch_pool(dtype, Q, K, V, qt, kt, vseg, BH, n, d, m, pl, st); });
     if (e != hipSuccess) return e;
     e = run_named(rec, "key_summary", [&] {
         return lapattn::launch_key_summary(dtype, K, V, qt, Upart, BH, n, d, m, lambda, kKeyChunk, p.nkc, st);
@@ -236,12 +247,12 @@ hipError_t forward_internals(Recorder& rec, const Plan& p, const void* Q, const 
 }
 
 hipError_t forward_fast(Recorder& rec, const FastPlan& p, const void* Q, const void* K, const void* V, void* Out,
-                        void* ws, int BH, int n, int d, int m, float lambda, int T, int norm, float eps,
+                        void* ws, int BH, int n, int d, int m, float lambda, int T, int norm, float eps, lapattn::LmPool pl,
                         hipStream_t st) {
     hipError_t e;
     e = run_named(rec, "pool", [&] {
         return lapattn::launch_fast_pool(Q, K, V, at<float>(ws, p.qt), at<float>(ws, p.kt), at<double>(ws, p.vseg),
-                                         at<float>(ws, p.segmax), at<float>(ws, p.vsegmax), BH, n, d, m, st);
+                                         at<float>(ws, p.segmax), at<float>(ws, p.vsegmax), BH, n, d, m, pl, st);
     });
     if (e != hipSuccess) return e;
     e = run_named(rec, "frame_ns", [&] {
@@ -288,8 +299,10 @@ int lapattn_forward(const void* Q, const void* K, const void* V, void* Out, int 
         if (!Q || !K || !V || !Out) return LAPATTN_ERR_NULL;
         const int norm = norm_of(opts);
         const float eps = eps_of(opts);
+        const lapattn::LmPool pl = pool_of(opts);
         int rc = check_shape(B, H, n, d, m, lambda, ns_iters, dtype, norm, eps);
         if (rc) return rc;
+        if ((rc = check_pool(n, m, pl))) return rc;
         rc = check_align({Q, K, V, Out}, workspace);
         if (rc) return rc;
         const int BH = B * H;
@@ -298,14 +311,15 @@ int lapattn_forward(const void* Q, const void* K, const void* V, void* Out, int 
             const FastPlan fp = make_fast_plan(BH, n, d, m);
             if (!workspace || workspace_bytes < fp.total) return LAPATTN_ERR_WORKSPACE;
             Recorder rec(st);
-            hipError_t e = forward_fast(rec, fp, Q, K, V, Out, workspace, BH, n, d, m, lambda, ns_iters, norm, eps, st);
+            hipError_t e =
+                forward_fast(rec, fp, Q, K, V, Out, workspace, BH, n, d, m, lambda, ns_iters, norm, eps, pl, st);
             return e == hipSuccess ? LAPATTN_OK : LAPATTN_ERR_HIP;
         }
         const Plan p = make_plan(BH, n, d, m, ns_iters, false);
         if (!workspace || workspace_bytes < p.total) return LAPATTN_ERR_WORKSPACE;
         Recorder rec(st);
         hipError_t e = forward_internals(rec, p, Q, K, V, workspace, BH, n, d, m, lambda, ns_iters, dtype, eps,
-                                         false, st);
+                                         false, pl, st);
         if (e != hipSuccess) return LAPATTN_ERR_HIP;
         e = run_named(rec, "query_out", [&] {
             return lapattn::launch_query_out(dtype, norm, Q, Out, at<float>(workspace, p.kt),
@@ -325,8 +339,10 @@ int lapattn_backward(const void* Q, const void* K, const void* V, const void* dO
         if (!Q || !K || !V || !dOut || !dQ || !dK || !dV) return LAPATTN_ERR_NULL;
         const int norm = norm_of(opts);
         const float eps = eps_of(opts);
+        const lapattn::LmPool pl = pool_of(opts);
         int rc = check_shape(B, H, n, d, m, lambda, ns_iters, dtype, norm, eps);
         if (rc) return rc;
+        if ((rc = check_pool(n, m, pl))) return rc;
         rc = check_align({Q, K, V, dOut, dQ, dK, dV}, workspace);
         if (rc) return rc;
         const int BH = B * H;
@@ -356,7 +372,7 @@ int lapattn_backward(const void* Q, const void* K, const void* V, const void* dO
             });
             if (e != hipSuccess) return LAPATTN_ERR_HIP;
         }
-        e = forward_internals(rec, p, q, k, v, ws, BH, n, d, m, lambda, ns_iters, LAPATTN_FP32, eps, true, st);
+        e = forward_internals(rec, p, q, k, v, ws, BH, n, d, m, lambda, ns_iters, LAPATTN_FP32, eps, true, pl, st);
         if (e != hipSuccess) return LAPATTN_ERR_HIP;
         e = run_named(rec, "bwd_query", [&] {
             return lapattn::launch_bwd_query(norm, q, g, dq, at<float>(ws, p.kt), at<float>(ws, p.M),
@@ -392,7 +408,7 @@ int lapattn_backward(const void* Q, const void* K, const void* V, const void* dO
         e = run_named(rec, "bwd_pool", [&] {
             return lapattn::launch_bwd_pool(dq, dk, at<float>(ws, p.dqtW), at<float>(ws, p.dktW),
                                             at<float>(ws, p.dqt_part), at<float>(ws, p.dkt_part), BH, n, d, m, p.nlc,
-                                            st);
+                                            pl, st);
         });
         if (e != hipSuccess || !bf16) return e == hipSuccess ? LAPATTN_OK : LAPATTN_ERR_HIP;
         e = run_named(rec, "narrow", [&] {

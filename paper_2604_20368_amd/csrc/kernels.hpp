@@ -8,14 +8,17 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "common.hpp"
+
 namespace lapattn {
 
 // Forward ---------------------------------------------------------------------
 
-// Landmark means qt, kt [BH][m][d] (fp32) and per-segment value sums vseg [BH][m][d] (fp64).
+// Landmark means qt, kt [BH][m][d] (fp32) and per-landmark value sums vseg [BH][m][d] (fp64);
+// pl selects segments or r x r windows (common.hpp).
 hipError_t launch_pool(int dt, const void* Q, const void* K, const void* V,
                        float* qt, float* kt, double* vseg,
-                       int BH, int n, int d, int m, hipStream_t st);
+                       int BH, int n, int d, int m, LmPool pl, hipStream_t st);
 
 // Key-side summary: per key chunk, Upart[h][chunk][a][c] = sum_j k(qt_a, k_j) [v_j | 1]_c.
 hipError_t launch_key_summary(int dt, const void* K, const void* V, const float* qt, float* Upart,
@@ -71,7 +74,7 @@ hipError_t launch_bwd_key_lm(const float* K, const float* qt, const float* dDk, 
 // Landmark-mean backward: dQ_i += dqt_{l(i)} / |S_l|, dK_j += dkt_{l(j)} / |S_l|.
 hipError_t launch_bwd_pool(float* dQ, float* dK, const float* dqtW, const float* dktW,
                            const float* dqt_part, const float* dkt_part,
-                           int BH, int n, int d, int m, int nlc, hipStream_t st);
+                           int BH, int n, int d, int m, int nlc, LmPool pl, hipStream_t st);
 
 // bf16 backward: the four inputs widened to fp32 (exact), the three fp32 gradients rounded to
 // bf16 (nearest even); count elements each, a multiple of 8, 16-byte aligned arrays.
@@ -83,7 +86,8 @@ hipError_t launch_narrow_bf16(const float* gQ, const float* gK, const float* gV,
 // bf16 fast forward path (fast.hip) -------------------------------------------------------
 
 hipError_t launch_fast_pool(const void* Q, const void* K, const void* V, float* qt, float* kt, double* vseg,
-                            float* segmax, float* vsegmax, int BH, int n, int d, int m, hipStream_t st);
+                            float* segmax, float* vsegmax, int BH, int n, int d, int m, LmPool pl,
+                            hipStream_t st);
 hipError_t launch_fast_frame_ns(const float* qt, const float* kt, const double* vseg, const float* segmax,
                                 const float* vsegmax, float* frame, uint32_t* qfix, uint32_t* kfix, float* vbar,
                                 float* XT, float* cinfo, int BH, int n, int d, int m, float lambda, int T, float eps,

@@ -19,7 +19,7 @@ EXPORTS = ("lapattn_workspace_size", "lapattn_forward", "lapattn_backward", "lap
 
 
 class lapattn_opts(ctypes.Structure):
-    _fields_ = [("norm", ctypes.c_int), ("eps", ctypes.c_float)]
+    _fields_ = [("norm", ctypes.c_int), ("eps", ctypes.c_float), ("grid_w", ctypes.c_int), ("pool_r", ctypes.c_int)]
 
 
 class LapattnError(RuntimeError):
@@ -69,21 +69,23 @@ def lapattn_workspace_size(B, H, n, d, m, ns_iters, dtype, for_backward):
     return int(library().lapattn_workspace_size(B, H, n, d, m, ns_iters, dtype, int(bool(for_backward))))
 
 
-def _opts(norm, eps):
-    return ctypes.byref(lapattn_opts(int(norm), float(eps)))
+def _opts(norm, eps, grid=None):
+    gw, r = grid if grid is not None else (0, 0)
+    return ctypes.byref(lapattn_opts(int(norm), float(eps), int(gw), int(r)))
 
 
 def lapattn_forward(Q, K, V, Out, B, H, n, d, m, lam, ns_iters, dtype, norm=LAPATTN_NORM_INLINE, eps=0.0,
-                    workspace=0, workspace_bytes=0, stream=0):
-    """Raw call with integer device addresses; returns the status code."""
-    return library().lapattn_forward(Q, K, V, Out, B, H, n, d, m, float(lam), ns_iters, dtype, _opts(norm, eps),
-                                     workspace, workspace_bytes, stream)
+                    workspace=0, workspace_bytes=0, stream=0, grid=None):
+    """Raw call with integer device addresses; returns the status code.  grid = (W', r) selects
+    r x r window landmarks of the W'-wide token map (None: balanced segments)."""
+    return library().lapattn_forward(Q, K, V, Out, B, H, n, d, m, float(lam), ns_iters, dtype,
+                                     _opts(norm, eps, grid), workspace, workspace_bytes, stream)
 
 
 def lapattn_backward(Q, K, V, dO, dQ, dK, dV, B, H, n, d, m, lam, ns_iters, dtype, norm=LAPATTN_NORM_INLINE,
-                     eps=0.0, workspace=0, workspace_bytes=0, stream=0):
+                     eps=0.0, workspace=0, workspace_bytes=0, stream=0, grid=None):
     return library().lapattn_backward(Q, K, V, dO, dQ, dK, dV, B, H, n, d, m, float(lam), ns_iters, dtype,
-                                      _opts(norm, eps), workspace, workspace_bytes, stream)
+                                      _opts(norm, eps, grid), workspace, workspace_bytes, stream)
 
 
 def lapattn_timing_enable(on):
@@ -135,7 +137,7 @@ def workspace(Q, m, ns_iters, for_backward=False):
     return torch.empty(nbytes, dtype=torch.uint8, device=Q.device)
 
 
-def forward(Q, K, V, m, lam, ns_iters, norm=LAPATTN_NORM_INLINE, eps=0.0, out=None, ws=None):
+def forward(Q, K, V, m, lam, ns_iters, norm=LAPATTN_NORM_INLINE, eps=0.0, out=None, ws=None, grid=None):
     """Out = lapattn(Q, K, V) on torch's current stream."""
     import torch
     _check(Q, K, V)
@@ -144,13 +146,13 @@ def forward(Q, K, V, m, lam, ns_iters, norm=LAPATTN_NORM_INLINE, eps=0.0, out=No
     ws = workspace(Q, m, ns_iters, False) if ws is None else ws
     B, H, n, d = Q.shape
     rc = lapattn_forward(Q.data_ptr(), K.data_ptr(), V.data_ptr(), out.data_ptr(), B, H, n, d, m, lam, ns_iters,
-                         _dtype_code(Q), norm, eps, ws.data_ptr(), ws.numel(), _stream(Q))
+                         _dtype_code(Q), norm, eps, ws.data_ptr(), ws.numel(), _stream(Q), grid)
     if rc != LAPATTN_OK:
         raise LapattnError(rc, "lapattn_forward")
     return out
 
 
-def backward(Q, K, V, dO, m, lam, ns_iters, norm=LAPATTN_NORM_INLINE, eps=0.0, grads=None, ws=None):
+def backward(Q, K, V, dO, m, lam, ns_iters, norm=LAPATTN_NORM_INLINE, eps=0.0, grads=None, ws=None, grid=None):
     """(dQ, dK, dV) of sum(Out * dO) on torch's current stream."""
     import torch
     _check(Q, K, V, dO)
@@ -160,7 +162,7 @@ def backward(Q, K, V, dO, m, lam, ns_iters, norm=LAPATTN_NORM_INLINE, eps=0.0, g
     B, H, n, d = Q.shape
     rc = lapattn_backward(Q.data_ptr(), K.data_ptr(), V.data_ptr(), dO.data_ptr(), dQ.data_ptr(), dK.data_ptr(),
                           dV.data_ptr(), B, H, n, d, m, lam, ns_iters, _dtype_code(Q), norm, eps, ws.data_ptr(),
-                          ws.numel(), _stream(Q))
+                          ws.numel(), _stream(Q), grid)
     if rc != LAPATTN_OK:
         raise LapattnError(rc, "lapattn_backward")
     return dQ, dK, dV

@@ -105,3 +105,19 @@ def test_workspace_size_monotone_and_invalid():
     b = L.lapattn_workspace_size(8, 2, 4 * 16384, 64, 64, 8, 1, 0)
     assert b < 4.2 * a
     assert a < 16 * 16384 * 64 * 4    # well under one fp32 n x m matrix per head
+
+
+@pytest.mark.parametrize("call", [fwd, bwd])
+def test_window_landmark_options_validated(call):
+    """r x r window landmarks (grid = (W', r)): the windows must tile the n-token map and give
+    exactly m landmarks; otherwise the call is rejected before any launch."""
+    assert call(grid=(10, 5), m=8) == L.LAPATTN_ERR_SHAPE      # 10 x 10 map, r = 5: m must be 4
+    assert call(grid=(3, 1), m=8) == L.LAPATTN_ERR_SHAPE       # 100 tokens are not a 3-wide map
+    assert call(grid=(20, 3), m=8) == L.LAPATTN_ERR_SHAPE      # r does not divide W' = 20
+    assert call(grid=(4, 4), m=8) == L.LAPATTN_ERR_SHAPE       # r does not divide H' = 25
+    assert call(grid=(10, 0), m=4) == L.LAPATTN_ERR_PARAM      # only one of the two set
+    assert call(grid=(0, 5), m=4) == L.LAPATTN_ERR_PARAM
+    assert call(grid=(-10, 5), m=4) == L.LAPATTN_ERR_PARAM
+    # valid geometry: the call gets as far as the workspace check
+    assert call(grid=(10, 5), m=4) == L.LAPATTN_ERR_WORKSPACE
+    assert call(grid=(20, 5), m=4) == L.LAPATTN_ERR_WORKSPACE  # 5 x 20 map, r = 5: 1 x 4 windows

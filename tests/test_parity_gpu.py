@@ -50,19 +50,19 @@ def say(msg):
     print(msg, flush=True)
 
 
-def run_forward(L, x, w, norm=0, eps=0.0):
+def run_forward(L, x, w, norm=0, eps=0.0, grid=None):
     Q, K, V = (to_dev(x[k], w.dtype) for k in ("Q", "K", "V"))
-    out = L.forward(Q, K, V, w.m, w.lam, w.T, norm=norm, eps=eps)
+    out = L.forward(Q, K, V, w.m, w.lam, w.T, norm=norm, eps=eps, grid=grid)
     torch.cuda.synchronize()
     return to_np(out)
 
 
-def check_forward(L, w, norm=0, eps=0.0, tol=None):
-    say("forward %s B=%d H=%d n=%d d=%d m=%d T=%d %s norm=%d eps=%g" %
-        (w.name, w.B, w.H, w.n, w.d, w.m, w.T, w.dtype, norm, eps))
+def check_forward(L, w, norm=0, eps=0.0, tol=None, grid=None):
+    say("forward %s B=%d H=%d n=%d d=%d m=%d T=%d %s norm=%d eps=%g grid=%s" %
+        (w.name, w.B, w.H, w.n, w.d, w.m, w.T, w.dtype, norm, eps, grid))
     x = W.make_inputs(w, with_grad=False)
-    got = run_forward(L, x, w, norm, eps)
-    ref = oracle.forward(x["Q"], x["K"], x["V"], w.m, w.lam, w.T, norm, eps)
+    got = run_forward(L, x, w, norm, eps, grid)
+    ref = oracle.forward(x["Q"], x["K"], x["V"], w.m, w.lam, w.T, norm, eps, grid=grid)
     err = head_rel(got, ref)
     say("  max head rel err %.3e" % err)
     assert np.isfinite(got).all()
@@ -168,11 +168,12 @@ def test_forward_full_size_sampled_heads(L, name):
 
 # ------------------------------------------------------------------------------ backward
 
-def check_backward(L, w, norm=0, eps=0.0, heads=None):
-    say("backward %s B=%d H=%d n=%d d=%d m=%d T=%d norm=%d eps=%g" % (w.name, w.B, w.H, w.n, w.d, w.m, w.T, norm, eps))
+def check_backward(L, w, norm=0, eps=0.0, heads=None, grid=None):
+    say("backward %s B=%d H=%d n=%d d=%d m=%d T=%d %s norm=%d eps=%g grid=%s" %
+        (w.name, w.B, w.H, w.n, w.d, w.m, w.T, w.dtype, norm, eps, grid))
     x = W.make_inputs(w, with_grad=True)
     Q, K, V, dO = (to_dev(x[k], w.dtype) for k in ("Q", "K", "V", "dO"))
-    dQ, dK, dV = L.backward(Q, K, V, dO, w.m, w.lam, w.T, norm=norm, eps=eps)
+    dQ, dK, dV = L.backward(Q, K, V, dO, w.m, w.lam, w.T, norm=norm, eps=eps, grid=grid)
     torch.cuda.synchronize()
     got = [to_np(t) for t in (dQ, dK, dV)]
     BH = w.BH
@@ -181,7 +182,7 @@ def check_backward(L, w, norm=0, eps=0.0, heads=None):
     else:
         sub = {k: np.ascontiguousarray(v.reshape(BH, w.n, w.d)[heads][None]) for k, v in x.items()}
         gsub = [g.reshape(BH, w.n, w.d)[heads][None] for g in got]
-    ref = oracle.backward(sub["Q"], sub["K"], sub["V"], sub["dO"], w.m, w.lam, w.T, norm, eps)
+    ref = oracle.backward(sub["Q"], sub["K"], sub["V"], sub["dO"], w.m, w.lam, w.T, norm, eps, grid=grid)
     errs = [head_rel(g, r) for g, r in zip(gsub, ref)]
     say("  dQ %.3e dK %.3e dV %.3e" % tuple(errs))
     for g in got:
@@ -226,3 +227,24 @@ def test_backward_bf16(L, norm):
     w = W.small(W.WORKLOADS["train"], n=700, B=1, H=2).with_(dtype="bf16")
     check_backward(L, w, norm=norm)
     check_backward(L, w.with_(d=64, sigma=0.125, lam=8.0, n=333, m=37), norm=norm)
+
+
+# ------------------------------------------------------------------------------ r x r window landmarks
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_forward_window_landmarks(L, dtype):
+    """Landmarks as 7 x 7 windows of a 56 x 56 token map (m = 64), as on the PVT stage-1 grid,
+    and 4 x 4 windows of a 24 x 32 map (m = 48), every normalisation."""
+    w = W.WORKLOADS["pvt_stage1"].with_(B=1, H=2, dtype=dtype)
+    check_forward(L, w, grid=(56, 7))
+    w2 = W.Workload("grid", 1, 2, 24 * 32, 32, 48, 6, dtype, 1 / math.sqrt(32), math.sqrt(32), 31, False)
+    for norm in (0, 1, 2):
+        check_forward(L, w2, norm=norm, grid=(32, 4))
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_backward_window_landmarks(L, dtype):
+    w = W.Workload("gridb", 1, 2, 16 * 20, 32, 20, 5, dtype, 1 / math.sqrt(32), math.sqrt(32), 33, True)
+    check_backward(L, w, grid=(20, 4))
+    check_backward(L, w.with_(d=64, sigma=0.125, lam=8.0), norm=1, grid=(20, 4))
+    check_backward(L, w.with_(n=15 * 15, m=25), grid=(15, 3))

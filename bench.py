@@ -177,9 +177,9 @@ def ingest_traffic(kernel, fetch_dir, write_dir, copy_fetch_dir, copy_write_dir,
            "bytes_per_launch": f_k * 1024.0 * ff + w_k * 1024.0 * fw,
            "sources": KERNEL_SOURCES, "sources_sha256": h.hexdigest(),
            "commands": ["rocprofv3 --pmc FETCH_SIZE --output-format csv -d FETCH_DIR -o run -- "
-                        "python3 bench.py --steps 3 --warmup 1 --no-cpu-baseline",
+                        "python3 bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-train-step",
                         "rocprofv3 --pmc WRITE_SIZE --output-format csv -d WRITE_DIR -o run -- "
-                        "python3 bench.py --steps 3 --warmup 1 --no-cpu-baseline",
+                        "python3 bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-train-step",
                         "rocprofv3 --pmc FETCH_SIZE --output-format csv -d COPY_FETCH_DIR -o run -- "
                         "python3 bench.py --calibrate-copy",
                         "rocprofv3 --pmc WRITE_SIZE --output-format csv -d COPY_WRITE_DIR -o run -- "

@@ -16,6 +16,8 @@ from .oracle import (  # noqa: F401
     ns,
     forward,
     backward,
+    dwc,
+    dwc_backward,
     threads,
     NORM_INLINE,
     NORM_ROWSUM,

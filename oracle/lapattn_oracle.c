@@ -17,7 +17,9 @@
  *                      with c = ||W||_1 ||W||_inf                  (R2, R3, R9, R10)
  *   key summary        sum_j phi(k_j)^T v_j and sum_j phi(k_j)^T   Sec. 3.2, Eq. (3)
  *   normalisation      z_ij = g_ij - mean_j' g_ij' + 1/n           Eq. (4) with Sigma^{-1/2} = I (R4)
- *   output             Z V                                        Eq. (7) without DWC (R7)
+ *   output             Z V                                        Eq. (7)
+ *   DWC(V)             the depth-wise convolution term of Eq. (7)  (R14), a separate
+ *                      function: the caller adds it to Z V
  *   backward           chain rule through all of the above; kernel gradient
  *                      dk/dx = -(1/lambda) sign(x-y) k            App. A (R8)
  */
@@ -520,5 +522,89 @@ int lapattn_oracle_backward(const double* Q, const double* K, const double* V,
                       dQ + h * hs, dK + h * hs, dV + h * hs, lambda, norm, eps, &s);
         head_free(&s);
     }
+    return 0;
+}
+
+/* ---------------------------------------------------------------------------------------
+ * Depth-wise convolution branch of Eq. (7) (R14): every channel of every head is
+ * cross-correlated over the token map with its own k x k filter, zero padded to the map's
+ * size.  Plain loops over output positions, channels and taps in index order. */
+static int dwc_check(int B, int H, int n, int d, int grid_w, int k) {
+    if (B < 1 || H < 1 || n < 1 || d < 1) return 4;
+    if (grid_w < 1 || n % grid_w != 0) return 4;
+    if (k < 1 || k % 2 == 0) return 4;
+    return 0;
+}
+
+/* the token at map position (y, x) of an H' x W' map, or -1 outside it */
+static int map_token(int y, int x, int gh, int gw) {
+    if (y < 0 || y >= gh || x < 0 || x >= gw) return -1;
+    return y * gw + x;
+}
+
+int lapattn_oracle_dwc(const double* V, const double* Wt, const double* bias, double* E,
+                       int B, int H, int n, int d, int grid_w, int k) {
+    if (dwc_check(B, H, n, d, grid_w, k)) return 4;
+    const int gw = grid_w, gh = n / grid_w, p = (k - 1) / 2;
+    for (int b = 0; b < B; ++b)
+        for (int h = 0; h < H; ++h) {
+            const double* v = V + ((size_t)b * H + h) * n * d;
+            double* e = E + ((size_t)b * H + h) * n * d;
+            for (int y = 0; y < gh; ++y)
+                for (int x = 0; x < gw; ++x)
+                    for (int c = 0; c < d; ++c) {
+                        const double* w = Wt + ((size_t)h * d + c) * k * k;
+                        double acc = bias ? bias[h * d + c] : 0.0;
+                        for (int u = 0; u < k; ++u)
+                            for (int t = 0; t < k; ++t) {
+                                const int j = map_token(y + u - p, x + t - p, gh, gw);
+                                if (j >= 0) acc += w[u * k + t] * v[(size_t)j * d + c];
+                            }
+                        e[((size_t)y * gw + x) * d + c] = acc;
+                    }
+        }
+    return 0;
+}
+
+/* E_i depends on V_j through tap (u, t) exactly when j = i + (u - p, t - p); so
+ * dV_j = sum over taps of w[u][t] dE_{j - (u - p, t - p)}, dW[u][t] = sum_i dE_i V_{i + (u - p, t - p)},
+ * dbias = sum_i dE_i, per channel, the last two summed over the batch. */
+int lapattn_oracle_dwc_backward(const double* V, const double* Wt, const double* dE,
+                                double* dV, double* dWt, double* dbias,
+                                int B, int H, int n, int d, int grid_w, int k) {
+    if (dwc_check(B, H, n, d, grid_w, k)) return 4;
+    const int gw = grid_w, gh = n / grid_w, p = (k - 1) / 2;
+    for (size_t e = 0; e < (size_t)H * d * k * k; ++e) dWt[e] = 0.0;
+    for (size_t e = 0; e < (size_t)H * d; ++e) dbias[e] = 0.0;
+    for (int b = 0; b < B; ++b)
+        for (int h = 0; h < H; ++h) {
+            const double* v = V + ((size_t)b * H + h) * n * d;
+            const double* g = dE + ((size_t)b * H + h) * n * d;
+            double* dv = dV + ((size_t)b * H + h) * n * d;
+            for (int y = 0; y < gh; ++y)
+                for (int x = 0; x < gw; ++x)
+                    for (int c = 0; c < d; ++c) {
+                        const double* w = Wt + ((size_t)h * d + c) * k * k;
+                        double acc = 0.0;
+                        for (int u = 0; u < k; ++u)
+                            for (int t = 0; t < k; ++t) {
+                                const int i = map_token(y - (u - p), x - (t - p), gh, gw);
+                                if (i >= 0) acc += w[u * k + t] * g[(size_t)i * d + c];
+                            }
+                        dv[((size_t)y * gw + x) * d + c] = acc;
+                    }
+            for (int y = 0; y < gh; ++y)
+                for (int x = 0; x < gw; ++x)
+                    for (int c = 0; c < d; ++c) {
+                        const double gi = g[((size_t)y * gw + x) * d + c];
+                        double* dw = dWt + ((size_t)h * d + c) * k * k;
+                        for (int u = 0; u < k; ++u)
+                            for (int t = 0; t < k; ++t) {
+                                const int j = map_token(y + u - p, x + t - p, gh, gw);
+                                if (j >= 0) dw[u * k + t] += gi * v[(size_t)j * d + c];
+                            }
+                        dbias[h * d + c] += gi;
+                    }
+        }
     return 0;
 }

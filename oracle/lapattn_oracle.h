@@ -23,6 +23,7 @@
  *   R8  sign(0) = 0; argmax ties -> lowest index; gradient flows through X0's scale
  *   R9  T counts NS updates; T = 0 returns X0
  *   R10 if the X0 scale is 0, X_t := 0 for every t
+ *   R14 the depth-wise convolution branch of Eq. (7): k x k filters, stride 1, zero padding
  */
 #ifndef LAPATTN_ORACLE_H
 #define LAPATTN_ORACLE_H
@@ -75,6 +76,22 @@ int lapattn_oracle_backward(const double* Q, const double* K, const double* V,
                             const double* dOut, double* dQ, double* dK, double* dV,
                             int B, int H, int n, int d, int m, double lambda, int T,
                             int norm, double eps, int grid_w, int r);
+
+/* Depth-wise convolution branch of Eq. (7), DWC(V) (reading R14): the n tokens of each head
+ * form an H' x W' map in row-major order (W' = grid_w, H' = n / W'), and each value channel c
+ * of head h is cross-correlated with its own k x k filter Wt[h][c] (k odd, stride 1, zero
+ * padding (k-1)/2, so the output has the map's size), plus bias[h][c] (bias may be NULL):
+ *   E[b][h][y W' + x][c] = bias[h][c] + sum_{u,t < k} Wt[h][c][u][t] V[b][h][(y+u-p) W' + x+t-p][c]
+ * with p = (k-1)/2 and terms outside the map dropped.  Wt is [H][d][k][k], bias [H][d], V and
+ * E [B][H][n][d]; E is overwritten.  Returns nonzero on invalid arguments. */
+int lapattn_oracle_dwc(const double* V, const double* Wt, const double* bias, double* E,
+                       int B, int H, int n, int d, int grid_w, int k);
+
+/* Gradients of sum(E * dE) for E = DWC(V) above: dV (the convolution's part only,
+ * [B][H][n][d]), dWt [H][d][k][k] and dbias [H][d] (summed over the batch), all overwritten. */
+int lapattn_oracle_dwc_backward(const double* V, const double* Wt, const double* dE,
+                                double* dV, double* dWt, double* dbias,
+                                int B, int H, int n, int d, int grid_w, int k);
 
 /* Number of OpenMP threads the oracle's parallel loops use. */
 int lapattn_oracle_threads(void);

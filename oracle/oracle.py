@@ -75,6 +75,10 @@ def _configure(lib):
     lib.lapattn_oracle_backward.restype = ctypes.c_int
     lib.lapattn_oracle_backward.argtypes = ([_dp] * 7 + [ctypes.c_int] * 5 + [ctypes.c_double, ctypes.c_int,
                                             ctypes.c_int, ctypes.c_double, ctypes.c_int, ctypes.c_int])
+    lib.lapattn_oracle_dwc.restype = ctypes.c_int
+    lib.lapattn_oracle_dwc.argtypes = [_dp] * 4 + [ctypes.c_int] * 6
+    lib.lapattn_oracle_dwc_backward.restype = ctypes.c_int
+    lib.lapattn_oracle_dwc_backward.argtypes = [_dp] * 6 + [ctypes.c_int] * 6
     lib.lapattn_oracle_threads.restype = ctypes.c_int
     lib.lapattn_oracle_threads.argtypes = []
     return lib
@@ -127,7 +131,44 @@ def ns(W, T, eps=0.0):
     return Xs, c
 
 
-def forward(Q, K, V, m, lam, T, norm=NORM_INLINE, eps=0.0, intermediates=False, grid=None):
+def _attention_grid(grid):
+    """(W', r) of the landmark windows for the attention part: (0, 0) when there are none
+    (grid None, or a token map with r = 0 that only the convolution branch uses)."""
+    if grid is None or grid[1] == 0:
+        return 0, 0
+    return grid
+
+
+def dwc(V, weight, bias, grid_w):
+    """DWC(V) of Eq. (7) (R14): weight [H][d][k][k], bias [H][d] or None, over the token map
+    of width grid_w.  Returns E [B][H][n][d]."""
+    V, weight = _f64(V), _f64(weight)
+    B, H, n, d = V.shape
+    k = weight.shape[-1]
+    assert weight.shape == (H, d, k, k)
+    bias = None if bias is None else _f64(bias)
+    assert bias is None or bias.shape == (H, d)
+    E = np.empty_like(V)
+    if load().lapattn_oracle_dwc(_p(V), _p(weight), _p(bias), _p(E), B, H, n, d, int(grid_w), int(k)):
+        raise ValueError("oracle dwc rejected its arguments")
+    return E
+
+
+def dwc_backward(V, weight, dE, grid_w):
+    """(dV, dweight, dbias) of sum(DWC(V) * dE): the convolution's part of dV only."""
+    V, weight, dE = _f64(V), _f64(weight), _f64(dE)
+    B, H, n, d = V.shape
+    k = weight.shape[-1]
+    dV, dW, db = np.empty_like(V), np.empty_like(weight), np.empty((H, d))
+    if load().lapattn_oracle_dwc_backward(_p(V), _p(weight), _p(dE), _p(dV), _p(dW), _p(db),
+                                          B, H, n, d, int(grid_w), int(k)):
+        raise ValueError("oracle dwc backward rejected its arguments")
+    return dV, dW, db
+
+
+def forward(Q, K, V, m, lam, T, norm=NORM_INLINE, eps=0.0, intermediates=False, grid=None, dwc_branch=None):
+    """Out = Z V (+ DWC(V) when dwc_branch = (weight, bias) is given, over the token map of width
+    grid[0]); grid = (W', r) selects r x r landmark windows when r > 0."""
     Q, K, V = _f64(Q), _f64(K), _f64(V)
     B, H, n, d = Q.shape
     assert K.shape == Q.shape and V.shape == Q.shape
@@ -140,22 +181,32 @@ def forward(Q, K, V, m, lam, T, norm=NORM_INLINE, eps=0.0, intermediates=False, 
             Xs=np.empty((B, H, T + 1, m, m)), U=np.empty((B, H, m, d + 1)), M=np.empty((B, H, m, d + 1)),
             Y=np.empty((B, H, n, d + 1)), vbar=np.empty((B, H, d)))
         ptrs = [inter[k] for k in ("Qt", "Kt", "W", "Xs", "U", "M", "Y", "vbar")]
-    gw, r = grid if grid is not None else (0, 0)
+    gw, r = _attention_grid(grid)
     rc = load().lapattn_oracle_forward(_p(Q), _p(K), _p(V), _p(out), B, H, n, d, int(m), float(lam),
                                        int(T), int(norm), float(eps), int(gw), int(r), *[_p(a) for a in ptrs])
     if rc:
         raise ValueError("oracle forward rejected its arguments (code %d)" % rc)
+    if dwc_branch is not None:
+        if grid is None:
+            raise ValueError("the convolution branch needs the token map (grid)")
+        out = out + dwc(V, dwc_branch[0], dwc_branch[1], grid[0])
     return (out, inter) if intermediates else out
 
 
-def backward(Q, K, V, dO, m, lam, T, norm=NORM_INLINE, eps=0.0, grid=None):
+def backward(Q, K, V, dO, m, lam, T, norm=NORM_INLINE, eps=0.0, grid=None, dwc_branch=None):
+    """(dQ, dK, dV), and with dwc_branch = (weight, bias) also (dweight, dbias)."""
     Q, K, V, dO = _f64(Q), _f64(K), _f64(V), _f64(dO)
     B, H, n, d = Q.shape
     dQ, dK, dV = np.empty_like(Q), np.empty_like(Q), np.empty_like(Q)
-    gw, r = grid if grid is not None else (0, 0)
+    gw, r = _attention_grid(grid)
     rc = load().lapattn_oracle_backward(_p(Q), _p(K), _p(V), _p(dO), _p(dQ), _p(dK), _p(dV),
                                         B, H, n, d, int(m), float(lam), int(T), int(norm), float(eps),
                                         int(gw), int(r))
     if rc:
         raise ValueError("oracle backward rejected its arguments (code %d)" % rc)
-    return dQ, dK, dV
+    if dwc_branch is None:
+        return dQ, dK, dV
+    if grid is None:
+        raise ValueError("the convolution branch needs the token map (grid)")
+    dVc, dW, db = dwc_backward(V, dwc_branch[0], dO, grid[0])
+    return dQ, dK, dV + dVc, dW, db

@@ -482,3 +482,104 @@ def test_windows_special_cases_and_rejections(oracle_lib):
     for grid, m in (((4, 3), 1), ((5, 1), 12), ((4, 2), 4), ((6, 2), 4)):
         with pytest.raises(ValueError):
             oracle.forward(Q, K, V, m, 1.0, 2, grid=grid)
+
+
+# ----------------------------------------------------------------------------- DWC(V) branch (R14)
+
+def rand_dwc(rng, H, d, k, bias=True):
+    w = rng.standard_normal((H, d, k, k))
+    return w, (rng.standard_normal((H, d)) if bias else None)
+
+
+@pytest.mark.parametrize("gh,gw,k", [(5, 7, 3), (4, 4, 1), (3, 8, 5), (6, 5, 7), (2, 9, 3)])
+def test_dwc_is_library_cross_correlation(oracle_lib, gh, gw, k):
+    """Each channel's map is scipy's zero-filled 'same' cross-correlation with its filter."""
+    from scipy.signal import correlate2d
+    rng = np.random.default_rng(gh * 100 + gw * 10 + k)
+    B, H, d = 2, 2, 3
+    V = rng.standard_normal((B, H, gh * gw, d))
+    w, b = rand_dwc(rng, H, d, k)
+    E = oracle.dwc(V, w, b, gw)
+    for bi in range(B):
+        for h in range(H):
+            for c in range(d):
+                ref = correlate2d(V[bi, h, :, c].reshape(gh, gw), w[h, c], mode="same", boundary="fill") + b[h, c]
+                np.testing.assert_allclose(E[bi, h, :, c].reshape(gh, gw), ref, rtol=1e-13, atol=1e-13)
+
+
+def test_dwc_one_hot_filters_shift_the_map(oracle_lib):
+    """A filter with a single 1 at tap (u, t) copies the value at offset (u - p, t - p),
+    zero off the map; the centre tap is the identity; the bias adds per channel."""
+    rng = np.random.default_rng(3)
+    gh, gw, k, d = 4, 6, 5, 2
+    p = (k - 1) // 2
+    V = rng.standard_normal((1, 1, gh * gw, d))
+    bias = np.array([[0.25, -1.5]])
+    for u, t in ((p, p), (0, 4), (3, 1), (4, 4)):
+        w = np.zeros((1, d, k, k))
+        w[:, :, u, t] = 1.0
+        E = oracle.dwc(V, w, bias, gw)[0, 0].reshape(gh, gw, d)
+        grid = V[0, 0].reshape(gh, gw, d)
+        for y in range(gh):
+            for x in range(gw):
+                yy, xx = y + u - p, x + t - p
+                want = (grid[yy, xx] if 0 <= yy < gh and 0 <= xx < gw else np.zeros(d)) + bias[0]
+                np.testing.assert_array_equal(E[y, x], want)
+
+
+def test_dwc_backward_matches_finite_differences(oracle_lib):
+    """sum(DWC(V) * dE) is linear in V, in the filters and in the bias separately, so central
+    differences give every gradient entry up to rounding (brute force over all entries)."""
+    rng = np.random.default_rng(4)
+    B, H, gh, gw, d, k = 2, 2, 3, 4, 2, 3
+    V = rng.standard_normal((B, H, gh * gw, d))
+    w, b = rand_dwc(rng, H, d, k)
+    dE = rng.standard_normal(V.shape)
+    dV, dW, db = oracle.dwc_backward(V, w, dE, gw)
+    f = lambda V_, w_, b_: float((oracle.dwc(V_, w_, b_, gw) * dE).sum())
+    for arr, grad, name in ((V, dV, "V"), (w, dW, "W"), (b, db, "b")):
+        for idx in np.ndindex(arr.shape):
+            args = {"V": V.copy(), "W": w.copy(), "b": b.copy()}
+            args[name][idx] += 0.5
+            fp = f(args["V"], args["W"], args["b"])
+            args[name][idx] -= 1.0
+            fm = f(args["V"], args["W"], args["b"])
+            assert abs((fp - fm) - grad[idx]) < 1e-11, (name, idx)
+
+
+def test_dwc_in_the_full_path(oracle_lib):
+    """Eq. (7): Out = Z V + DWC(V).  The branch adds exactly DWC(V) to the forward; the
+    backward adds the branch's dV and gives the filter and bias gradients, checked by central
+    differences through the whole path (dQ, dK are unchanged by the branch)."""
+    rng = np.random.default_rng(6)
+    gh, gw, d, m, T, lam, k = 3, 4, 2, 3, 4, 1.5, 3
+    n = gh * gw
+    Q, K, V = rand_qkv(rng, 1, 2, n, d, 0.7)
+    w, b = rand_dwc(rng, 2, d, k)
+    dO = rng.standard_normal(Q.shape)
+    base = oracle.forward(Q, K, V, m, lam, T)
+    both = oracle.forward(Q, K, V, m, lam, T, grid=(gw, 0), dwc_branch=(w, b))
+    np.testing.assert_allclose(both - base, oracle.dwc(V, w, b, gw), rtol=0, atol=1e-14)
+    dQ, dK, dV, dW, db = oracle.backward(Q, K, V, dO, m, lam, T, grid=(gw, 0), dwc_branch=(w, b))
+    dQ0, dK0, _ = oracle.backward(Q, K, V, dO, m, lam, T)
+    assert np.array_equal(dQ, dQ0) and np.array_equal(dK, dK0)
+    h = 1e-6
+    f = lambda V_, w_, b_: float((oracle.forward(Q, K, V_, m, lam, T, grid=(gw, 0), dwc_branch=(w_, b_)) * dO).sum())
+    for arr, grad, name in ((V, dV, "V"), (w, dW, "W"), (b, db, "b")):
+        g = np.zeros_like(arr)
+        for idx in np.ndindex(arr.shape):
+            args = {"V": V.copy(), "W": w.copy(), "b": b.copy()}
+            args[name][idx] += h
+            fp = f(args["V"], args["W"], args["b"])
+            args[name][idx] -= 2 * h
+            g[idx] = (fp - f(args["V"], args["W"], args["b"])) / (2 * h)
+        assert np.abs(g - grad).max() / max(np.abs(g).max(), 1e-12) < 1e-7, name
+
+
+def test_dwc_rejections(oracle_lib):
+    rng = np.random.default_rng(7)
+    V = rng.standard_normal((1, 1, 12, 2))
+    for gw, k in ((5, 3), (0, 3), (4, 2), (4, 0), (-4, 3)):
+        w = np.zeros((1, 2, max(k, 1), max(k, 1))) if k > 0 else np.zeros((1, 2, 0, 0))
+        with pytest.raises(ValueError):
+            oracle.dwc(V, w, None, gw)

@@ -38,6 +38,16 @@ MUTANTS = {
         "members[l * r * r + t] = (wy * r + t / r) * grid_w + wx * r + t % r;",
         "members[l * r * r + t] = (wy * r + t / r) * r + wx * r + t % r;"),
     "window backward spread to segments": ("const int i = s->members[t];\n                dq[", "const int i = t;\n                dq["),
+    "DWC filter flipped": ("if (j >= 0) acc += w[u * k + t] * v[(size_t)j * d + c];",
+                           "if (j >= 0) acc += w[(k - 1 - u) * k + (k - 1 - t)] * v[(size_t)j * d + c];"),
+    "DWC map rows and columns swapped": ("return y * gw + x;", "return x * gh + y;"),
+    "DWC padding off by one": ("const int j = map_token(y + u - p, x + t - p, gh, gw);\n                                if (j >= 0) acc",
+                               "const int j = map_token(y + u - p - 1, x + t - p, gh, gw);\n                                if (j >= 0) acc"),
+    "DWC bias dropped": ("double acc = bias ? bias[h * d + c] : 0.0;", "double acc = 0.0;"),
+    "DWC value gradient not flipped": ("map_token(y - (u - p), x - (t - p), gh, gw)", "map_token(y + (u - p), x + (t - p), gh, gw)"),
+    "DWC bias gradient misses the batch": ("dbias[h * d + c] += gi;", "dbias[h * d + c] = gi;"),
+    "DWC filter gradient misses the batch": ("for (size_t e = 0; e < (size_t)H * d * k * k; ++e) dWt[e] = 0.0;\n    for (size_t e = 0; e < (size_t)H * d; ++e) dbias[e] = 0.0;\n    for (int b = 0; b < B; ++b)\n        for (int h = 0; h < H; ++h) {",
+        "for (size_t e = 0; e < (size_t)H * d; ++e) dbias[e] = 0.0;\n    for (int b = 0; b < B; ++b)\n        for (int h = 0; h < H; ++h) {\n            for (size_t e = (size_t)h * d * k * k; e < (size_t)(h + 1) * d * k * k; ++e) dWt[e] = 0.0;"),
     "query/key landmarks swapped in K_LL": (
         "s->Wk[a * m + b] = lapattn_oracle_kernel(s->qt + a * d, s->kt + b * d, d, lambda);",
         "s->Wk[a * m + b] = lapattn_oracle_kernel(s->kt + a * d, s->qt + b * d, d, lambda);"),
@@ -63,6 +73,9 @@ PIN_CALLS = [
     lambda: pins.test_windows_landmarks_are_average_pooling(None, 4, 6, 2),
     lambda: pins.test_windows_equal_segments_of_the_window_ordered_tokens(None, oracle.NORM_INLINE),
     lambda: pins.test_windows_special_cases_and_rejections(None),
+    lambda: pins.test_dwc_is_library_cross_correlation(None, 5, 7, 3),
+    lambda: pins.test_dwc_one_hot_filters_shift_the_map(None),
+    lambda: pins.test_dwc_backward_matches_finite_differences(None),
 ]
 
 

@@ -19,7 +19,9 @@
  *                 of Eq. (4) with the whitening taken as the identity
  *               LAPATTN_NORM_ROWSUM:  (G^ V)_i / s_i       (Eq. (3))
  *               LAPATTN_NORM_NONE:    (G^ V)_i
- * The depth-wise convolution branch of Eq. (7) is not part of this operation.
+ * Optional depth-wise convolution branch of Eq. (7), off by default (lapattn_opts.dwc_k):
+ *   Out_i += DWC(V)_i, each value channel of each head cross-correlated over the token map
+ *   with its own k x k filter (stride 1, zero padding (k-1)/2) plus a per-channel bias.
  *
  * Layout: Q, K, V, Out, dOut, dQ, dK, dV are device pointers to contiguous
  * row-major [B][H][n][d] arrays of the element type `dtype` (fp32, or bf16 as
@@ -66,11 +68,13 @@ typedef enum {
 enum {
     LAPATTN_OK = 0,
     LAPATTN_ERR_NULL = 1,         /* a required pointer is NULL */
-    LAPATTN_ERR_SHAPE = 2,        /* B, H, n < 1, m < 1, m > n, B*H*n*d >= 2^31, or landmark
-                                     windows that do not tile the token map (lapattn_opts) */
+    LAPATTN_ERR_SHAPE = 2,        /* B, H, n < 1, m < 1, m > n, B*H*n*d >= 2^31, n not a
+                                     multiple of grid_w, or landmark windows that do not tile
+                                     the token map (lapattn_opts) */
     LAPATTN_ERR_PARAM = 3,        /* lambda not finite or <= 0, ns_iters outside [0, 64],
                                      eps not finite or < 0, unknown norm or dtype,
-                                     window options negative or only one of them set */
+                                     window options negative or pool_r without grid_w,
+                                     dwc_k not 0, 1, 3, 5 or 7, or dwc_k without grid_w */
     LAPATTN_ERR_UNSUPPORTED = 4,  /* d not in {32, 64} or m > 64 */
     LAPATTN_ERR_WORKSPACE = 5,    /* workspace NULL or smaller than lapattn_workspace_size() */
     LAPATTN_ERR_HIP = 6,          /* a HIP launch failed */
@@ -78,28 +82,46 @@ enum {
                                      workspace is not 256-byte aligned */
 };
 
-/* Options; a NULL pointer means {LAPATTN_NORM_INLINE, 0.0f, 0, 0}.
+/* Options; a NULL pointer means all fields zero: {LAPATTN_NORM_INLINE, 0.0f, 0, 0, 0, NULL...}.
  * eps is the diagonal perturbation W <- W + eps I of Algorithm 2 (>= 0).
- * Landmarks (Sec. 4.2, sampling): with grid_w = pool_r = 0 they are the means of m
- * balanced segments of consecutive tokens, [floor(l n/m), floor((l+1) n/m)).  With
- * grid_w > 0 the n tokens form a row-major H' x W' map (W' = grid_w, H' = n / W') and
- * the landmarks are the means of its r x r windows (r = pool_r; average pooling with
- * kernel and stride r), landmark l = Y (W'/r) + X for the window at rows Y r..,
- * columns X r..; r must divide H' and W', and m must equal (H'/r)(W'/r)
- * (LAPATTN_ERR_SHAPE otherwise; a negative value, or only one of the two set, is
- * LAPATTN_ERR_PARAM). */
+ * Token map: with grid_w > 0 the n tokens form a row-major H' x W' map (W' = grid_w,
+ * H' = n / W'; n must be a multiple of W', LAPATTN_ERR_SHAPE otherwise).
+ * Landmarks (Sec. 4.2, sampling): with pool_r = 0 they are the means of m balanced
+ * segments of consecutive tokens, [floor(l n/m), floor((l+1) n/m)).  With pool_r = r > 0
+ * they are the means of the map's r x r windows (average pooling with kernel and stride r),
+ * landmark l = Y (W'/r) + X for the window at rows Y r.., columns X r..; this needs
+ * grid_w > 0 (LAPATTN_ERR_PARAM), r dividing H' and W', and m = (H'/r)(W'/r)
+ * (LAPATTN_ERR_SHAPE).  Negative values are LAPATTN_ERR_PARAM.
+ * Convolution branch (Eq. (7)): dwc_k = k in {1, 3, 5, 7} adds DWC(V) to Out:
+ *   Out[b][h][y W' + x][c] += dwc_b[h][c]
+ *       + sum_{u,t < k} dwc_w[h][c][u][t] V[b][h][(y+u-p) W' + x+t-p][c],  p = (k-1)/2,
+ * terms outside the map dropped; it needs grid_w > 0 (LAPATTN_ERR_PARAM) and dwc_w
+ * (LAPATTN_ERR_NULL), and the workspace sized with LAPATTN_WS_DWC.  dwc_w is a device array
+ * [H][d][k][k] of fp32 and dwc_b [H][d] fp32 or NULL (no bias), shared by the batch, for
+ * either dtype.  lapattn_backward adds the branch's part to dV and, when the pointers are
+ * not NULL, writes the filter gradient dwc_dw [H][d][k][k] and the bias gradient dwc_db [H][d]
+ * (fp32, summed over the batch, overwritten); lapattn_forward ignores those two. */
 typedef struct {
-    int norm;      /* lapattn_norm */
+    int norm;            /* lapattn_norm */
     float eps;
-    int grid_w;    /* token-map width W', or 0 for segments */
-    int pool_r;    /* window side r, or 0 for segments */
+    int grid_w;          /* token-map width W', or 0: no map */
+    int pool_r;          /* landmark window side r, or 0 for segments */
+    int dwc_k;           /* convolution filter side k, or 0: no convolution branch */
+    const float* dwc_w;  /* device [H][d][k][k] filters */
+    const float* dwc_b;  /* device [H][d] bias, or NULL */
+    float* dwc_dw;       /* backward: device [H][d][k][k] filter gradient, or NULL */
+    float* dwc_db;       /* backward: device [H][d] bias gradient, or NULL */
 } lapattn_opts;
 
-/* Bytes of device workspace lapattn_forward (for_backward = 0) or
- * lapattn_backward (for_backward = 1) needs for these sizes; 0 if the sizes
- * are invalid.  Pure host function, callable without a GPU. */
+/* Workspace flags. */
+enum { LAPATTN_WS_BACKWARD = 1, LAPATTN_WS_DWC = 2 };
+
+/* Bytes of device workspace that lapattn_forward (flags without LAPATTN_WS_BACKWARD) or
+ * lapattn_backward (with it) needs for these sizes, with LAPATTN_WS_DWC when the call uses
+ * the convolution branch; 0 if the sizes or flags are invalid.  Pure host function, callable
+ * without a GPU. */
 size_t lapattn_workspace_size(int B, int H, int n, int d, int m, int ns_iters,
-                              int dtype, int for_backward);
+                              int dtype, int flags);
 
 /* Forward pass (Algorithm 1 with Algorithm 2 as the pseudoinverse, the
  * key-summary reordering of Sec. 3.2, and the normalisation chosen in opts).

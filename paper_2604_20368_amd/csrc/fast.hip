@@ -940,7 +940,7 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
                                                      const float* __restrict__ frame, const _Float16* __restrict__ Mt,
                                                      const float* __restrict__ mscale,
                                                      const float* __restrict__ Mones, const float* __restrict__ vbar,
-                                                     int n, int m, int nqb, int BH) {
+                                                     const float* __restrict__ extra, int n, int m, int nqb, int BH) {
     constexpr int D2 = D / 2;
     constexpr int D8 = D / 8;
     constexpr int CB = D / 32;
@@ -1058,6 +1058,14 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
                 float o1 = fmaf(y[4 * g + 1], tm, tadd * vb.y);
                 float o2 = fmaf(y[4 * g + 2], tm, tadd * vb.z);
                 float o3 = fmaf(y[4 * g + 3], tm, tadd * vb.w);
+                if (extra) {   // the convolution branch of Eq. (7); rows past n read row n - 1
+                    const int iq = min(i0 + 32 * qb + (l & 31), n - 1);
+                    const float4 ex = *reinterpret_cast<const float4*>(extra + ((size_t)h * n + iq) * D + c0);
+                    o0 += ex.x;
+                    o1 += ex.y;
+                    o2 += ex.z;
+                    o3 += ex.w;
+                }
                 if (nan_head) o0 = o1 = o2 = o3 = __builtin_nanf("");
                 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
                 const bf16x2_t p0 = {(__bf16)o0, (__bf16)o1}, p1 = {(__bf16)o2, (__bf16)o3};
@@ -1137,13 +1145,13 @@ hipError_t launch_fast_mfinal(const float* Upart, const float* XT, _Float16* Mt,
 }
 
 hipError_t launch_fast_query(int norm, const void* Q, void* Out, const uint32_t* kfix, const float* frame,
-                             const _Float16* Mt, const float* mscale, const float* Mones, const float* vbar, int BH,
-                             int n, int d, int m, hipStream_t st) {
+                             const _Float16* Mt, const float* mscale, const float* Mones, const float* vbar,
+                             const float* extra, int BH, int n, int d, int m, hipStream_t st) {
     const int nqb = (n + 255) / 256;
     dim3 grid(nqb * BH);
 #define LAPATTN_Q2(Dv, Nv)                                                                                        \
     hipLaunchKernelGGL((query2_kernel<Dv, Nv>), grid, dim3(256), 0, st, (const uint16_t*)Q, (uint16_t*)Out, kfix, \
-                       frame, Mt, mscale, Mones, vbar, n, m, nqb, BH)
+                       frame, Mt, mscale, Mones, vbar, extra, n, m, nqb, BH)
     if (d == 32) {
         if (norm == NORM_INLINE) LAPATTN_Q2(32, NORM_INLINE);
         else if (norm == NORM_ROWSUM) LAPATTN_Q2(32, NORM_ROWSUM);

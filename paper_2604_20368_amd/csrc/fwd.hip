@@ -369,7 +369,8 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 template <int D, int NORM>
 __global__ __launch_bounds__(256) void query_out_kernel(const float* __restrict__ Q, float* __restrict__ Out,
                                                         const float* __restrict__ kt, const float* __restrict__ M,
-                                                        const float* __restrict__ vbar, int n, int m, float kscale) {
+                                                        const float* __restrict__ vbar,
+                                                        const float* __restrict__ extra, int n, int m, float kscale) {
     constexpr int D1 = D + 1;
     constexpr int NCH = D / 32;
     constexpr int CB = D / 32;             // 32-column blocks of the output
@@ -469,6 +470,13 @@ __global__ __launch_bounds__(256) void query_out_kernel(const float* __restrict_
                         else if (NORM == NORM_ROWSUM) o[t] = y / si;
                         else o[t] = y;
                     }
+                    if (extra) {   // the convolution branch of Eq. (7)
+                        const float4 ex = *reinterpret_cast<const float4*>(extra + ((size_t)h * n + iq) * D + c0);
+                        o[0] += ex.x;
+                        o[1] += ex.y;
+                        o[2] += ex.z;
+                        o[3] += ex.w;
+                    }
                     *reinterpret_cast<float4*>(orow + c0) = make_float4(o[0], o[1], o[2], o[3]);
                 }
         }
@@ -521,24 +529,28 @@ hipError_t launch_ns_solve(const float* qt, const float* kt, const float* Upart,
 
 template <int D>
 static void query_out_launch(int norm, const void* Q, void* Out, const float* kt, const float* M, const float* vbar,
-                             int BH, int n, int m, float kscale, hipStream_t st) {
+                             const float* extra, int BH, int n, int m, float kscale, hipStream_t st) {
     dim3 grid((n + 255) / 256, BH);
     const float* q = (const float*)Q;
     float* o = (float*)Out;
     if (norm == NORM_INLINE)
-        hipLaunchKernelGGL((query_out_kernel<D, NORM_INLINE>), grid, dim3(256), 0, st, q, o, kt, M, vbar, n, m, kscale);
+        hipLaunchKernelGGL((query_out_kernel<D, NORM_INLINE>), grid, dim3(256), 0, st, q, o, kt, M, vbar, extra, n, m,
+                           kscale);
     else if (norm == NORM_ROWSUM)
-        hipLaunchKernelGGL((query_out_kernel<D, NORM_ROWSUM>), grid, dim3(256), 0, st, q, o, kt, M, vbar, n, m, kscale);
+        hipLaunchKernelGGL((query_out_kernel<D, NORM_ROWSUM>), grid, dim3(256), 0, st, q, o, kt, M, vbar, extra, n, m,
+                           kscale);
     else
-        hipLaunchKernelGGL((query_out_kernel<D, NORM_NONE>), grid, dim3(256), 0, st, q, o, kt, M, vbar, n, m, kscale);
+        hipLaunchKernelGGL((query_out_kernel<D, NORM_NONE>), grid, dim3(256), 0, st, q, o, kt, M, vbar, extra, n, m,
+                           kscale);
 }
 
 hipError_t launch_query_out(int dt, int norm, const void* Q, void* Out, const float* kt, const float* M,
-                            const float* vbar, int BH, int n, int d, int m, float lambda, hipStream_t st) {
+                            const float* vbar, const float* extra, int BH, int n, int d, int m, float lambda,
+                            hipStream_t st) {
     if (dt != DT_F32) return hipErrorInvalidValue;   // bf16 inputs take the fast path
     const float ks = kscale_of(lambda);
-    if (d == 32) query_out_launch<32>(norm, Q, Out, kt, M, vbar, BH, n, m, ks, st);
-    else query_out_launch<64>(norm, Q, Out, kt, M, vbar, BH, n, m, ks, st);
+    if (d == 32) query_out_launch<32>(norm, Q, Out, kt, M, vbar, extra, BH, n, m, ks, st);
+    else query_out_launch<64>(norm, Q, Out, kt, M, vbar, extra, BH, n, m, ks, st);
     return hipGetLastError();
 }
 

@@ -17,6 +17,8 @@ constexpr int kMaxM = 64;
 constexpr int kMaxT = 64;
 constexpr int kKeyChunk = 1024;  // keys per block of the key-summary kernel (four 64-key tiles per wave)
 constexpr int kLmChunk = 256;    // tokens per block of the landmark-major backward passes
+constexpr int kDwcChunk = 256;   // tokens per block of the convolution filter gradient
+constexpr int kDwcMaxK = 7;      // largest convolution filter side
 
 // ------------------------------------------------------------------------------- validation
 
@@ -48,6 +50,7 @@ int check_align(std::initializer_list<const void*> tensors, const void* workspac
 
 struct FastPlan {
     size_t qt, kt, vseg, segmax, vsegmax, frame, qfix, kfix, vbar, XT, cinfo, Upart, Mt, mscale, Mones, M;
+    size_t E;   // convolution branch: DWC(V) + bias, fp32 [BH][n][d]
     size_t total;
     int kpb, nkb;
 };
@@ -57,6 +60,8 @@ struct Plan {
     size_t Aq, dDq, rs, dYd, dvbar_part, dM_part, dkt_part, dU, dvbar,   // backward
         dqtW, dktW, dDk, dqt_part;
     size_t wQ, wK, wV, wG, gQ, gK, gV;   // bf16 backward: fp32 copies of the inputs, fp32 gradients
+    size_t E;                            // convolution branch, forward: DWC(V) + bias [BH][n][d]
+    size_t dwc_part;                     // convolution branch, backward: filter-gradient partials
     size_t total;
     int MP, nkc, nqb, nlc;
 };
@@ -71,7 +76,7 @@ struct Carver {
     }
 };
 
-Plan make_plan(int BH, int n, int d, int m, int T, bool bwd, bool bf16 = false) {
+Plan make_plan(int BH, int n, int d, int m, int T, bool bwd, bool bf16 = false, bool dwc = false) {
     Plan p{};
     p.MP = m <= 32 ? 32 : 64;
     p.nkc = (n + kKeyChunk - 1) / kKeyChunk;
@@ -113,6 +118,10 @@ Plan make_plan(int BH, int n, int d, int m, int T, bool bwd, bool bf16 = false) 
             p.gK = c.take(t);
             p.gV = c.take(t);
         }
+        if (dwc)
+            p.dwc_part = c.take(bh * ((n + kDwcChunk - 1) / kDwcChunk) * d * (kDwcMaxK * kDwcMaxK + 1) * f);
+    } else if (dwc) {
+        p.E = c.take(bh * n * d * f);
     }
     p.total = (c.off + 255) & ~size_t(255);
     return p;
@@ -120,7 +129,7 @@ Plan make_plan(int BH, int n, int d, int m, int T, bool bwd, bool bf16 = false) 
 
 // The bf16 forward: key blocks of kpb keys (a multiple of 256), sized so the key-side launch
 // has about two 64-key tiles per wave when the work allows it.
-FastPlan make_fast_plan(int BH, int n, int d, int m) {
+FastPlan make_fast_plan(int BH, int n, int d, int m, bool dwc = false) {
     FastPlan p{};
     const long long tiles = (long long)BH * ((n + 63) / 64);
     const long long per_wave = tiles / 2048 > 1 ? tiles / 2048 : 1;
@@ -144,6 +153,7 @@ FastPlan make_fast_plan(int BH, int n, int d, int m) {
     p.mscale = c.take(bh * ((size_t)d / 8 + 1) * f);
     p.Mones = c.take(bh * 64 * f);
     p.M = c.take(bh * m * d1 * f);
+    if (dwc) p.E = c.take(bh * n * d * f);
     p.total = (c.off + 255) & ~size_t(255);
     return p;
 }
@@ -213,13 +223,31 @@ int norm_of(const lapattn_opts* o) { return o ? o->norm : LAPATTN_NORM_INLINE; }
 float eps_of(const lapattn_opts* o) { return o ? o->eps : 0.f; }
 lapattn::LmPool pool_of(const lapattn_opts* o) { return o ? lapattn::LmPool{o->grid_w, o->pool_r} : lapattn::LmPool{0, 0}; }
 
-// Landmark geometry: segments (0, 0), or r x r windows of a row-major map of width gw that r
-// divides, as is its height n / gw, with m = (n / gw / r)(gw / r) windows.
+// Token map and landmark geometry: no map (gw = 0) or a row-major map of width gw dividing n;
+// segments (r = 0), or r x r windows of the map, r dividing both sides, with
+// m = (n / gw / r)(gw / r) windows.
 int check_pool(int n, int m, lapattn::LmPool pl) {
-    if (pl.gw == 0 && pl.r == 0) return LAPATTN_OK;
-    if (pl.gw < 1 || pl.r < 1) return LAPATTN_ERR_PARAM;
-    if (n % pl.gw || (n / pl.gw) % pl.r || pl.gw % pl.r) return LAPATTN_ERR_SHAPE;
+    if (pl.gw < 0 || pl.r < 0 || (pl.r > 0 && pl.gw == 0)) return LAPATTN_ERR_PARAM;
+    if (pl.gw > 0 && n % pl.gw) return LAPATTN_ERR_SHAPE;
+    if (pl.r == 0) return LAPATTN_OK;
+    if ((n / pl.gw) % pl.r || pl.gw % pl.r) return LAPATTN_ERR_SHAPE;
     if ((long long)m != (long long)(n / pl.gw / pl.r) * (pl.gw / pl.r)) return LAPATTN_ERR_SHAPE;
+    return LAPATTN_OK;
+}
+
+// The convolution branch of Eq. (7).
+struct Dwc {
+    int k;
+    const float *w, *b;
+    float *dw, *db;
+};
+Dwc dwc_of(const lapattn_opts* o) {
+    return o ? Dwc{o->dwc_k, o->dwc_w, o->dwc_b, o->dwc_dw, o->dwc_db} : Dwc{0, nullptr, nullptr, nullptr, nullptr};
+}
+int check_dwc(const Dwc& c, lapattn::LmPool pl) {
+    if (c.k == 0) return LAPATTN_OK;
+    if (c.k < 0 || c.k > kDwcMaxK || c.k % 2 == 0 || pl.gw < 1) return LAPATTN_ERR_PARAM;
+    if (!c.w) return LAPATTN_ERR_NULL;
     return LAPATTN_OK;
 }
 
@@ -247,9 +275,16 @@ hipError_t forward_internals(Recorder& rec, const Plan& p, const void* Q, const 
 }
 
 hipError_t forward_fast(Recorder& rec, const FastPlan& p, const void* Q, const void* K, const void* V, void* Out,
-                        void* ws, int BH, int n, int d, int m, float lambda, int T, int norm, float eps, lapattn::LmPool pl,
-                        hipStream_t st) {
+                        void* ws, int BH, int H, int n, int d, int m, float lambda, int T, int norm, float eps,
+                        lapattn::LmPool pl, const Dwc& dwc, hipStream_t st) {
     hipError_t e;
+    float* E = dwc.k ? at<float>(ws, p.E) : nullptr;
+    if (E) {
+        e = run_named(rec, "dwc", [&] {
+            return lapattn::launch_dwc_fwd(lapattn::DT_BF16, V, dwc.w, dwc.b, E, BH, H, n, d, pl.gw, dwc.k, st);
+        });
+        if (e != hipSuccess) return e;
+    }
     e = run_named(rec, "pool", [&] {
         return lapattn::launch_fast_pool(Q, K, V, at<float>(ws, p.qt), at<float>(ws, p.kt), at<double>(ws, p.vseg),
                                          at<float>(ws, p.segmax), at<float>(ws, p.vsegmax), BH, n, d, m, pl, st);
@@ -277,7 +312,7 @@ hipError_t forward_fast(Recorder& rec, const FastPlan& p, const void* Q, const v
     e = run_named(rec, "query", [&] {
         return lapattn::launch_fast_query(norm, Q, Out, at<uint32_t>(ws, p.kfix), at<float>(ws, p.frame),
                                           at<_Float16>(ws, p.Mt), at<float>(ws, p.mscale), at<float>(ws, p.Mones),
-                                          at<float>(ws, p.vbar), BH, n, d, m, st);
+                                          at<float>(ws, p.vbar), E, BH, n, d, m, st);
     });
     return e;
 }
@@ -286,10 +321,12 @@ hipError_t forward_fast(Recorder& rec, const FastPlan& p, const void* Q, const v
 
 extern "C" {
 
-size_t lapattn_workspace_size(int B, int H, int n, int d, int m, int ns_iters, int dtype, int for_backward) {
+size_t lapattn_workspace_size(int B, int H, int n, int d, int m, int ns_iters, int dtype, int flags) {
     if (check_shape(B, H, n, d, m, 1.f, ns_iters, dtype, LAPATTN_NORM_INLINE, 0.f) != LAPATTN_OK) return 0;
-    if (dtype == LAPATTN_BF16 && !for_backward) return make_fast_plan(B * H, n, d, m).total;
-    return make_plan(B * H, n, d, m, ns_iters, for_backward != 0, dtype == LAPATTN_BF16).total;
+    if (flags & ~(LAPATTN_WS_BACKWARD | LAPATTN_WS_DWC)) return 0;
+    const bool bwd = (flags & LAPATTN_WS_BACKWARD) != 0, dwc = (flags & LAPATTN_WS_DWC) != 0;
+    if (dtype == LAPATTN_BF16 && !bwd) return make_fast_plan(B * H, n, d, m, dwc).total;
+    return make_plan(B * H, n, d, m, ns_iters, bwd, dtype == LAPATTN_BF16, dwc).total;
 }
 
 int lapattn_forward(const void* Q, const void* K, const void* V, void* Out, int B, int H, int n, int d, int m,
@@ -300,30 +337,39 @@ int lapattn_forward(const void* Q, const void* K, const void* V, void* Out, int 
         const int norm = norm_of(opts);
         const float eps = eps_of(opts);
         const lapattn::LmPool pl = pool_of(opts);
+        const Dwc dwc = dwc_of(opts);
         int rc = check_shape(B, H, n, d, m, lambda, ns_iters, dtype, norm, eps);
         if (rc) return rc;
         if ((rc = check_pool(n, m, pl))) return rc;
+        if ((rc = check_dwc(dwc, pl))) return rc;
         rc = check_align({Q, K, V, Out}, workspace);
         if (rc) return rc;
         const int BH = B * H;
         hipStream_t st = reinterpret_cast<hipStream_t>(stream);
         if (dtype == LAPATTN_BF16) {
-            const FastPlan fp = make_fast_plan(BH, n, d, m);
+            const FastPlan fp = make_fast_plan(BH, n, d, m, dwc.k != 0);
             if (!workspace || workspace_bytes < fp.total) return LAPATTN_ERR_WORKSPACE;
             Recorder rec(st);
-            hipError_t e =
-                forward_fast(rec, fp, Q, K, V, Out, workspace, BH, n, d, m, lambda, ns_iters, norm, eps, pl, st);
+            hipError_t e = forward_fast(rec, fp, Q, K, V, Out, workspace, BH, H, n, d, m, lambda, ns_iters, norm, eps,
+                                        pl, dwc, st);
             return e == hipSuccess ? LAPATTN_OK : LAPATTN_ERR_HIP;
         }
-        const Plan p = make_plan(BH, n, d, m, ns_iters, false);
+        const Plan p = make_plan(BH, n, d, m, ns_iters, false, false, dwc.k != 0);
         if (!workspace || workspace_bytes < p.total) return LAPATTN_ERR_WORKSPACE;
         Recorder rec(st);
         hipError_t e = forward_internals(rec, p, Q, K, V, workspace, BH, n, d, m, lambda, ns_iters, dtype, eps,
                                          false, pl, st);
         if (e != hipSuccess) return LAPATTN_ERR_HIP;
+        float* E = dwc.k ? at<float>(workspace, p.E) : nullptr;
+        if (E) {
+            e = run_named(rec, "dwc", [&] {
+                return lapattn::launch_dwc_fwd(lapattn::DT_F32, V, dwc.w, dwc.b, E, BH, H, n, d, pl.gw, dwc.k, st);
+            });
+            if (e != hipSuccess) return LAPATTN_ERR_HIP;
+        }
         e = run_named(rec, "query_out", [&] {
             return lapattn::launch_query_out(dtype, norm, Q, Out, at<float>(workspace, p.kt),
-                                             at<float>(workspace, p.M), at<float>(workspace, p.vbar), BH, n, d, m,
+                                             at<float>(workspace, p.M), at<float>(workspace, p.vbar), E, BH, n, d, m,
                                              lambda, st);
         });
         return e == hipSuccess ? LAPATTN_OK : LAPATTN_ERR_HIP;
@@ -340,14 +386,16 @@ int lapattn_backward(const void* Q, const void* K, const void* V, const void* dO
         const int norm = norm_of(opts);
         const float eps = eps_of(opts);
         const lapattn::LmPool pl = pool_of(opts);
+        const Dwc dwc = dwc_of(opts);
         int rc = check_shape(B, H, n, d, m, lambda, ns_iters, dtype, norm, eps);
         if (rc) return rc;
         if ((rc = check_pool(n, m, pl))) return rc;
+        if ((rc = check_dwc(dwc, pl))) return rc;
         rc = check_align({Q, K, V, dOut, dQ, dK, dV}, workspace);
         if (rc) return rc;
         const int BH = B * H;
         const bool bf16 = dtype == LAPATTN_BF16;
-        const Plan p = make_plan(BH, n, d, m, ns_iters, true, bf16);
+        const Plan p = make_plan(BH, n, d, m, ns_iters, true, bf16, dwc.k != 0);
         if (!workspace || workspace_bytes < p.total) return LAPATTN_ERR_WORKSPACE;
         hipStream_t st = reinterpret_cast<hipStream_t>(stream);
         void* ws = workspace;
@@ -410,7 +458,21 @@ int lapattn_backward(const void* Q, const void* K, const void* V, const void* dO
                                             at<float>(ws, p.dqt_part), at<float>(ws, p.dkt_part), BH, n, d, m, p.nlc,
                                             pl, st);
         });
-        if (e != hipSuccess || !bf16) return e == hipSuccess ? LAPATTN_OK : LAPATTN_ERR_HIP;
+        if (e != hipSuccess) return LAPATTN_ERR_HIP;
+        if (dwc.k) {
+            e = run_named(rec, "dwc_dv", [&] {
+                return lapattn::launch_dwc_bwd_dv(g, dwc.w, dv, BH, H, n, d, pl.gw, dwc.k, st);
+            });
+            if (e != hipSuccess) return LAPATTN_ERR_HIP;
+            if (dwc.dw || dwc.db) {
+                e = run_named(rec, "dwc_dw", [&] {
+                    return lapattn::launch_dwc_bwd_w(g, v, at<float>(ws, p.dwc_part), dwc.dw, dwc.db, B, H, n, d,
+                                                     pl.gw, dwc.k, kDwcChunk, st);
+                });
+                if (e != hipSuccess) return LAPATTN_ERR_HIP;
+            }
+        }
+        if (!bf16) return LAPATTN_OK;
         e = run_named(rec, "narrow", [&] {
             return lapattn::launch_narrow_bf16(dq, dk, dv, static_cast<uint16_t*>(dQ), static_cast<uint16_t*>(dK),
                                                static_cast<uint16_t*>(dV), cnt, st);
@@ -426,7 +488,7 @@ const char* lapattn_status_str(int status) {
         case LAPATTN_OK: return "ok";
         case LAPATTN_ERR_NULL: return "null pointer argument";
         case LAPATTN_ERR_SHAPE: return "invalid shape (B, H, n >= 1, 1 <= m <= n, B*H*n*d < 2^31)";
-        case LAPATTN_ERR_PARAM: return "invalid parameter (lambda, ns_iters, eps, norm or dtype)";
+        case LAPATTN_ERR_PARAM: return "invalid parameter (lambda, ns_iters, eps, norm, dtype, map or convolution options)";
         case LAPATTN_ERR_UNSUPPORTED: return "unsupported configuration (d in {32, 64}, m <= 64)";
         case LAPATTN_ERR_WORKSPACE: return "workspace missing or too small";
         case LAPATTN_ERR_HIP: return "HIP launch failed";

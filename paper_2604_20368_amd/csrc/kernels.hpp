@@ -34,9 +34,10 @@ hipError_t launch_ns_solve(const float* qt, const float* kt, const float* Upart,
                            int BH, int n, int d, int m, int T, double lambda, double eps, int nkc,
                            int store_all, int MP, hipStream_t st);
 
-// Query side: Out_i = normalise(sum_l k(q_i, kt_l) M_l).
+// Query side: Out_i = normalise(sum_l k(q_i, kt_l) M_l) (+ extra_i when extra, [BH][n][d], is given).
 hipError_t launch_query_out(int dt, int norm, const void* Q, void* Out, const float* kt, const float* M,
-                            const float* vbar, int BH, int n, int d, int m, float lambda, hipStream_t st);
+                            const float* vbar, const float* extra, int BH, int n, int d, int m, float lambda,
+                            hipStream_t st);
 
 // Backward (fp32 inputs) --------------------------------------------------------
 
@@ -97,7 +98,22 @@ hipError_t launch_fast_key(const void* K, const void* V, const uint32_t* qfix, c
 hipError_t launch_fast_mfinal(const float* Upart, const float* XT, _Float16* Mt, float* mscale, float* Mones,
                               float* M, int BH, int d, int m, int nkb, hipStream_t st);
 hipError_t launch_fast_query(int norm, const void* Q, void* Out, const uint32_t* kfix, const float* frame,
-                             const _Float16* Mt, const float* mscale, const float* Mones, const float* vbar, int BH,
-                             int n, int d, int m, hipStream_t st);
+                             const _Float16* Mt, const float* mscale, const float* Mones, const float* vbar,
+                             const float* extra, int BH, int n, int d, int m, hipStream_t st);
+
+// Depth-wise convolution branch of Eq. (7) (dwc.hip) ------------------------------------------
+// Filters W [H][d][k][k], bias [H][d] (may be NULL), over the row-major token map of width gw;
+// k odd, at most 7.
+
+// E = DWC(V) + bias, fp32 [BH][n][d]; V fp32 or bf16 (dt).
+hipError_t launch_dwc_fwd(int dt, const void* V, const float* W, const float* bias, float* E, int BH, int H, int n,
+                          int d, int gw, int k, hipStream_t st);
+// dV += DWC^T(G), all fp32 [BH][n][d].
+hipError_t launch_dwc_bwd_dv(const float* G, const float* W, float* dV, int BH, int H, int n, int d, int gw, int k,
+                             hipStream_t st);
+// dW [H][d][k][k] and db [H][d] (either may be NULL) of sum(DWC(V) * G), summed over the batch;
+// part holds B*H*ceil(n/chunk)*d*(k*k+1) floats of per-chunk partial sums.
+hipError_t launch_dwc_bwd_w(const float* G, const float* V, float* part, float* dW, float* db, int B, int H, int n,
+                            int d, int gw, int k, int chunk, hipStream_t st);
 
 }  // namespace lapattn

@@ -13,13 +13,16 @@ LAPATTN_FP32, LAPATTN_BF16 = 0, 1
 LAPATTN_NORM_INLINE, LAPATTN_NORM_ROWSUM, LAPATTN_NORM_NONE = 0, 1, 2
 LAPATTN_OK, LAPATTN_ERR_NULL, LAPATTN_ERR_SHAPE, LAPATTN_ERR_PARAM = 0, 1, 2, 3
 LAPATTN_ERR_UNSUPPORTED, LAPATTN_ERR_WORKSPACE, LAPATTN_ERR_HIP, LAPATTN_ERR_ALIGN = 4, 5, 6, 7
+LAPATTN_WS_BACKWARD, LAPATTN_WS_DWC = 1, 2
 
 EXPORTS = ("lapattn_workspace_size", "lapattn_forward", "lapattn_backward", "lapattn_status_str",
            "lapattn_timing_enable", "lapattn_timing_read", "lapattn_timing_name")
 
 
 class lapattn_opts(ctypes.Structure):
-    _fields_ = [("norm", ctypes.c_int), ("eps", ctypes.c_float), ("grid_w", ctypes.c_int), ("pool_r", ctypes.c_int)]
+    _fields_ = [("norm", ctypes.c_int), ("eps", ctypes.c_float), ("grid_w", ctypes.c_int), ("pool_r", ctypes.c_int),
+                ("dwc_k", ctypes.c_int), ("dwc_w", ctypes.c_void_p), ("dwc_b", ctypes.c_void_p),
+                ("dwc_dw", ctypes.c_void_p), ("dwc_db", ctypes.c_void_p)]
 
 
 class LapattnError(RuntimeError):
@@ -65,27 +68,30 @@ def lapattn_status_str(code):
     return library().lapattn_status_str(int(code)).decode()
 
 
-def lapattn_workspace_size(B, H, n, d, m, ns_iters, dtype, for_backward):
-    return int(library().lapattn_workspace_size(B, H, n, d, m, ns_iters, dtype, int(bool(for_backward))))
+def lapattn_workspace_size(B, H, n, d, m, ns_iters, dtype, flags):
+    """flags: LAPATTN_WS_BACKWARD and/or LAPATTN_WS_DWC (a bool counts as the backward flag)."""
+    return int(library().lapattn_workspace_size(B, H, n, d, m, ns_iters, dtype, int(flags)))
 
 
-def _opts(norm, eps, grid=None):
+def _opts(norm, eps, grid=None, dwc=None):
     gw, r = grid if grid is not None else (0, 0)
-    return ctypes.byref(lapattn_opts(int(norm), float(eps), int(gw), int(r)))
+    k, w, b, dw, db = dwc if dwc is not None else (0, None, None, None, None)
+    return ctypes.byref(lapattn_opts(int(norm), float(eps), int(gw), int(r), int(k), w, b, dw, db))
 
 
 def lapattn_forward(Q, K, V, Out, B, H, n, d, m, lam, ns_iters, dtype, norm=LAPATTN_NORM_INLINE, eps=0.0,
-                    workspace=0, workspace_bytes=0, stream=0, grid=None):
-    """Raw call with integer device addresses; returns the status code.  grid = (W', r) selects
-    r x r window landmarks of the W'-wide token map (None: balanced segments)."""
+                    workspace=0, workspace_bytes=0, stream=0, grid=None, dwc=None):
+    """Raw call with integer device addresses; returns the status code.  grid = (W', r): the
+    W'-wide token map, with r x r window landmarks when r > 0 (None: no map, balanced
+    segments).  dwc = (k, filters, bias, dfilters, dbias) addresses of the convolution branch."""
     return library().lapattn_forward(Q, K, V, Out, B, H, n, d, m, float(lam), ns_iters, dtype,
-                                     _opts(norm, eps, grid), workspace, workspace_bytes, stream)
+                                     _opts(norm, eps, grid, dwc), workspace, workspace_bytes, stream)
 
 
 def lapattn_backward(Q, K, V, dO, dQ, dK, dV, B, H, n, d, m, lam, ns_iters, dtype, norm=LAPATTN_NORM_INLINE,
-                     eps=0.0, workspace=0, workspace_bytes=0, stream=0, grid=None):
+                     eps=0.0, workspace=0, workspace_bytes=0, stream=0, grid=None, dwc=None):
     return library().lapattn_backward(Q, K, V, dO, dQ, dK, dV, B, H, n, d, m, float(lam), ns_iters, dtype,
-                                      _opts(norm, eps, grid), workspace, workspace_bytes, stream)
+                                      _opts(norm, eps, grid, dwc), workspace, workspace_bytes, stream)
 
 
 def lapattn_timing_enable(on):
@@ -128,41 +134,69 @@ def _stream(t):
     return torch.cuda.current_stream(t.device).cuda_stream
 
 
-def workspace(Q, m, ns_iters, for_backward=False):
+def workspace(Q, m, ns_iters, for_backward=False, dwc=False):
     import torch
     B, H, n, d = Q.shape
-    nbytes = lapattn_workspace_size(B, H, n, d, m, ns_iters, _dtype_code(Q), for_backward)
+    flags = (LAPATTN_WS_BACKWARD if for_backward else 0) | (LAPATTN_WS_DWC if dwc else 0)
+    nbytes = lapattn_workspace_size(B, H, n, d, m, ns_iters, _dtype_code(Q), flags)
     if nbytes == 0:
         raise ValueError("invalid lapattn sizes")
     return torch.empty(nbytes, dtype=torch.uint8, device=Q.device)
 
 
-def forward(Q, K, V, m, lam, ns_iters, norm=LAPATTN_NORM_INLINE, eps=0.0, out=None, ws=None, grid=None):
-    """Out = lapattn(Q, K, V) on torch's current stream."""
+def _dwc_args(Q, dwc, grads=None):
+    """(k, filters, bias, dfilters, dbias) addresses for dwc = (filters [H][d][k][k], bias [H][d] or
+    None), fp32 device tensors; grads = (dfilters, dbias) or None."""
+    import torch
+    if dwc is None:
+        return None
+    w, b = dwc
+    H, d = Q.shape[1], Q.shape[3]
+    k = w.shape[-1]
+    for t, shape in ((w, (H, d, k, k)), (b, (H, d))) + (() if grads is None else ((grads[0], (H, d, k, k)),
+                                                                                     (grads[1], (H, d)))):
+        if t is None:
+            continue
+        if (not isinstance(t, torch.Tensor) or not t.is_cuda or t.dtype != torch.float32 or not t.is_contiguous()
+                or tuple(t.shape) != shape or t.device != Q.device):
+            raise ValueError("convolution filters and bias are contiguous fp32 device tensors [H][d][k][k] and [H][d]")
+    dw, db = (None, None) if grads is None else grads
+    ptr = lambda t: None if t is None else t.data_ptr()
+    return (k, ptr(w), ptr(b), ptr(dw), ptr(db))
+
+
+def forward(Q, K, V, m, lam, ns_iters, norm=LAPATTN_NORM_INLINE, eps=0.0, out=None, ws=None, grid=None, dwc=None):
+    """Out = lapattn(Q, K, V) on torch's current stream; grid = (W', r) the token map (r > 0: window
+    landmarks), dwc = (filters, bias) adds the convolution branch over that map."""
     import torch
     _check(Q, K, V)
     out = torch.empty_like(Q) if out is None else out
     _check(Q, out)
-    ws = workspace(Q, m, ns_iters, False) if ws is None else ws
+    ws = workspace(Q, m, ns_iters, False, dwc is not None) if ws is None else ws
     B, H, n, d = Q.shape
     rc = lapattn_forward(Q.data_ptr(), K.data_ptr(), V.data_ptr(), out.data_ptr(), B, H, n, d, m, lam, ns_iters,
-                         _dtype_code(Q), norm, eps, ws.data_ptr(), ws.numel(), _stream(Q), grid)
+                         _dtype_code(Q), norm, eps, ws.data_ptr(), ws.numel(), _stream(Q), grid, _dwc_args(Q, dwc))
     if rc != LAPATTN_OK:
         raise LapattnError(rc, "lapattn_forward")
     return out
 
 
-def backward(Q, K, V, dO, m, lam, ns_iters, norm=LAPATTN_NORM_INLINE, eps=0.0, grads=None, ws=None, grid=None):
-    """(dQ, dK, dV) of sum(Out * dO) on torch's current stream."""
+def backward(Q, K, V, dO, m, lam, ns_iters, norm=LAPATTN_NORM_INLINE, eps=0.0, grads=None, ws=None, grid=None,
+             dwc=None, dwc_grads=None):
+    """(dQ, dK, dV) of sum(Out * dO) on torch's current stream; with dwc = (filters, bias) also the
+    filter and bias gradients: (dQ, dK, dV, dfilters, dbias)."""
     import torch
     _check(Q, K, V, dO)
     dQ, dK, dV = grads if grads is not None else (torch.empty_like(Q), torch.empty_like(Q), torch.empty_like(Q))
     _check(Q, dQ, dK, dV)
-    ws = workspace(Q, m, ns_iters, True) if ws is None else ws
+    if dwc is not None and dwc_grads is None:
+        dwc_grads = (torch.empty_like(dwc[0]), torch.empty((Q.shape[1], Q.shape[3]), dtype=torch.float32,
+                                                             device=Q.device))
+    ws = workspace(Q, m, ns_iters, True, dwc is not None) if ws is None else ws
     B, H, n, d = Q.shape
     rc = lapattn_backward(Q.data_ptr(), K.data_ptr(), V.data_ptr(), dO.data_ptr(), dQ.data_ptr(), dK.data_ptr(),
                           dV.data_ptr(), B, H, n, d, m, lam, ns_iters, _dtype_code(Q), norm, eps, ws.data_ptr(),
-                          ws.numel(), _stream(Q), grid)
+                          ws.numel(), _stream(Q), grid, _dwc_args(Q, dwc, dwc_grads))
     if rc != LAPATTN_OK:
         raise LapattnError(rc, "lapattn_backward")
-    return dQ, dK, dV
+    return (dQ, dK, dV) if dwc is None else (dQ, dK, dV) + tuple(dwc_grads)

@@ -115,9 +115,36 @@ def test_window_landmark_options_validated(call):
     assert call(grid=(3, 1), m=8) == L.LAPATTN_ERR_SHAPE       # 100 tokens are not a 3-wide map
     assert call(grid=(20, 3), m=8) == L.LAPATTN_ERR_SHAPE      # r does not divide W' = 20
     assert call(grid=(4, 4), m=8) == L.LAPATTN_ERR_SHAPE       # r does not divide H' = 25
-    assert call(grid=(10, 0), m=4) == L.LAPATTN_ERR_PARAM      # only one of the two set
-    assert call(grid=(0, 5), m=4) == L.LAPATTN_ERR_PARAM
+    assert call(grid=(0, 5), m=4) == L.LAPATTN_ERR_PARAM       # windows need the map
+    assert call(grid=(3, 0), m=4) == L.LAPATTN_ERR_SHAPE       # a map without windows must still fit n
     assert call(grid=(-10, 5), m=4) == L.LAPATTN_ERR_PARAM
     # valid geometry: the call gets as far as the workspace check
     assert call(grid=(10, 5), m=4) == L.LAPATTN_ERR_WORKSPACE
     assert call(grid=(20, 5), m=4) == L.LAPATTN_ERR_WORKSPACE  # 5 x 20 map, r = 5: 1 x 4 windows
+    assert call(grid=(10, 0), m=4) == L.LAPATTN_ERR_WORKSPACE  # a map with segment landmarks
+
+
+@pytest.mark.parametrize("call", [fwd, bwd])
+def test_convolution_options_validated(call):
+    """The convolution branch: an odd filter side up to 7, the token map, and the filters."""
+    for k in (2, 9, -1, 4):
+        assert call(grid=(10, 0), m=4, dwc=(k, FAKE, None, None, None)) == L.LAPATTN_ERR_PARAM
+    assert call(m=4, dwc=(3, FAKE, None, None, None)) == L.LAPATTN_ERR_PARAM          # no map
+    assert call(grid=(3, 0), m=4, dwc=(3, FAKE, None, None, None)) == L.LAPATTN_ERR_SHAPE
+    assert call(grid=(10, 0), m=4, dwc=(3, None, None, None, None)) == L.LAPATTN_ERR_NULL
+    for k in (1, 3, 5, 7):
+        assert call(grid=(10, 0), m=4, dwc=(k, FAKE, FAKE, FAKE, FAKE)) == L.LAPATTN_ERR_WORKSPACE
+        assert call(grid=(10, 5), m=4, dwc=(k, FAKE, None, None, None)) == L.LAPATTN_ERR_WORKSPACE
+
+
+def test_convolution_workspace():
+    """The branch needs one fp32 [B,H,n,d] buffer in the forward and filter-gradient partials in
+    the backward, both reported only with LAPATTN_WS_DWC; unknown flags give 0."""
+    for dt in (0, 1):
+        f0 = L.lapattn_workspace_size(2, 3, 3136, 64, 64, 8, dt, 0)
+        f1 = L.lapattn_workspace_size(2, 3, 3136, 64, 64, 8, dt, L.LAPATTN_WS_DWC)
+        assert f1 >= f0 + 2 * 3 * 3136 * 64 * 4
+        b0 = L.lapattn_workspace_size(2, 3, 3136, 64, 64, 8, dt, L.LAPATTN_WS_BACKWARD)
+        b1 = L.lapattn_workspace_size(2, 3, 3136, 64, 64, 8, dt, L.LAPATTN_WS_BACKWARD | L.LAPATTN_WS_DWC)
+        assert b1 > b0
+        assert L.lapattn_workspace_size(2, 3, 3136, 64, 64, 8, dt, 4) == 0

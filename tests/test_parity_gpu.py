@@ -50,19 +50,26 @@ def say(msg):
     print(msg, flush=True)
 
 
-def run_forward(L, x, w, norm=0, eps=0.0, grid=None):
+def dev_dwc(dwc):
+    """(filters, bias) numpy -> fp32 device tensors."""
+    if dwc is None:
+        return None
+    return tuple(None if a is None else torch.from_numpy(a).to("cuda") for a in dwc)
+
+
+def run_forward(L, x, w, norm=0, eps=0.0, grid=None, dwc=None):
     Q, K, V = (to_dev(x[k], w.dtype) for k in ("Q", "K", "V"))
-    out = L.forward(Q, K, V, w.m, w.lam, w.T, norm=norm, eps=eps, grid=grid)
+    out = L.forward(Q, K, V, w.m, w.lam, w.T, norm=norm, eps=eps, grid=grid, dwc=dev_dwc(dwc))
     torch.cuda.synchronize()
     return to_np(out)
 
 
-def check_forward(L, w, norm=0, eps=0.0, tol=None, grid=None):
-    say("forward %s B=%d H=%d n=%d d=%d m=%d T=%d %s norm=%d eps=%g grid=%s" %
-        (w.name, w.B, w.H, w.n, w.d, w.m, w.T, w.dtype, norm, eps, grid))
+def check_forward(L, w, norm=0, eps=0.0, tol=None, grid=None, dwc=None):
+    say("forward %s B=%d H=%d n=%d d=%d m=%d T=%d %s norm=%d eps=%g grid=%s dwc k=%s" %
+        (w.name, w.B, w.H, w.n, w.d, w.m, w.T, w.dtype, norm, eps, grid, None if dwc is None else dwc[0].shape[-1]))
     x = W.make_inputs(w, with_grad=False)
-    got = run_forward(L, x, w, norm, eps, grid)
-    ref = oracle.forward(x["Q"], x["K"], x["V"], w.m, w.lam, w.T, norm, eps, grid=grid)
+    got = run_forward(L, x, w, norm, eps, grid, dwc)
+    ref = oracle.forward(x["Q"], x["K"], x["V"], w.m, w.lam, w.T, norm, eps, grid=grid, dwc_branch=dwc)
     err = head_rel(got, ref)
     say("  max head rel err %.3e" % err)
     assert np.isfinite(got).all()
@@ -168,26 +175,35 @@ def test_forward_full_size_sampled_heads(L, name):
 
 # ------------------------------------------------------------------------------ backward
 
-def check_backward(L, w, norm=0, eps=0.0, heads=None, grid=None):
-    say("backward %s B=%d H=%d n=%d d=%d m=%d T=%d %s norm=%d eps=%g grid=%s" %
-        (w.name, w.B, w.H, w.n, w.d, w.m, w.T, w.dtype, norm, eps, grid))
+def check_backward(L, w, norm=0, eps=0.0, heads=None, grid=None, dwc=None):
+    say("backward %s B=%d H=%d n=%d d=%d m=%d T=%d %s norm=%d eps=%g grid=%s dwc k=%s" %
+        (w.name, w.B, w.H, w.n, w.d, w.m, w.T, w.dtype, norm, eps, grid, None if dwc is None else dwc[0].shape[-1]))
     x = W.make_inputs(w, with_grad=True)
     Q, K, V, dO = (to_dev(x[k], w.dtype) for k in ("Q", "K", "V", "dO"))
-    dQ, dK, dV = L.backward(Q, K, V, dO, w.m, w.lam, w.T, norm=norm, eps=eps, grid=grid)
+    res = L.backward(Q, K, V, dO, w.m, w.lam, w.T, norm=norm, eps=eps, grid=grid, dwc=dev_dwc(dwc))
     torch.cuda.synchronize()
-    got = [to_np(t) for t in (dQ, dK, dV)]
+    got = [to_np(t) for t in res[:3]]
     BH = w.BH
     if heads is None:
         sub, gsub = x, got
     else:
         sub = {k: np.ascontiguousarray(v.reshape(BH, w.n, w.d)[heads][None]) for k, v in x.items()}
         gsub = [g.reshape(BH, w.n, w.d)[heads][None] for g in got]
-    ref = oracle.backward(sub["Q"], sub["K"], sub["V"], sub["dO"], w.m, w.lam, w.T, norm, eps, grid=grid)
-    errs = [head_rel(g, r) for g, r in zip(gsub, ref)]
+    ref = oracle.backward(sub["Q"], sub["K"], sub["V"], sub["dO"], w.m, w.lam, w.T, norm, eps, grid=grid,
+                          dwc_branch=dwc)
+    errs = [head_rel(g, r) for g, r in zip(gsub, ref[:3])]
     say("  dQ %.3e dK %.3e dV %.3e" % tuple(errs))
     for g in got:
         assert np.isfinite(g).all()
     assert max(errs) <= TOL[w.dtype]
+    if dwc is not None:
+        assert heads is None, "the filter gradients sum over every head of the batch"
+        gw_, gb_ = (res[3].cpu().numpy().astype(np.float64), res[4].cpu().numpy().astype(np.float64))
+        e_w = head_rel(gw_[None], ref[3][None])
+        e_b = head_rel(gb_[None, :, :, None], ref[4][None, :, :, None])
+        say("  dfilters %.3e dbias %.3e" % (e_w, e_b))
+        assert np.isfinite(gw_).all() and np.isfinite(gb_).all()
+        assert max(e_w, e_b) <= TOL[w.dtype]
 
 
 @pytest.mark.parametrize("norm", [0, 1, 2])
@@ -248,3 +264,47 @@ def test_backward_window_landmarks(L, dtype):
     check_backward(L, w, grid=(20, 4))
     check_backward(L, w.with_(d=64, sigma=0.125, lam=8.0), norm=1, grid=(20, 4))
     check_backward(L, w.with_(n=15 * 15, m=25), grid=(15, 3))
+
+
+# ------------------------------------------------------------------------------ convolution branch of Eq. (7)
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_forward_convolution_branch(L, dtype):
+    """Out = Z V + DWC(V): 3 x 3 filters with bias over a 24 x 32 map with window landmarks, 5 x 5
+    without bias over the same map with segment landmarks, and 1 x 1 / 7 x 7 filters over a
+    7 x 9 map (the 7 x 7 filter is wider than the map's height)."""
+    w = W.Workload("conv", 1, 2, 24 * 32, 64, 48, 6, dtype, 0.125, 8.0, 41, False)
+    check_forward(L, w, grid=(32, 4), dwc=W.make_dwc(2, 64, 3, seed=1))
+    w2 = w.with_(d=32, sigma=1 / math.sqrt(32), lam=math.sqrt(32), m=20)
+    check_forward(L, w2, norm=1, grid=(32, 0), dwc=W.make_dwc(2, 32, 5, seed=2, bias=False))
+    w3 = W.Workload("conv3", 2, 1, 7 * 9, 64, 7, 4, dtype, 0.125, 8.0, 43, False)
+    for k in (1, 7):
+        check_forward(L, w3, norm=2, grid=(9, 0), dwc=W.make_dwc(1, 64, k, seed=3 + k))
+
+
+def test_forward_convolution_branch_full_size(L):
+    """The PVT stage-1 shape (B=32, n = 56 x 56, bf16) with 7 x 7 window landmarks and a 3 x 3
+    branch; sampled heads (each head's output depends on that head only)."""
+    w = W.WORKLOADS["pvt_stage1"]
+    dwc = W.make_dwc(w.H, w.d, 3, seed=7)
+    say("forward full %s with dwc" % w.name)
+    x = W.make_inputs(w, with_grad=False)
+    got = run_forward(L, x, w, grid=(56, 7), dwc=dwc)
+    heads = [0, 13, w.BH - 1]
+    sub = {k: np.ascontiguousarray(v.reshape(w.BH, w.n, w.d)[heads][None]) for k, v in x.items()}
+    dsub = (dwc[0][[0]], dwc[1][[0]])   # H = 1: every sampled head uses filter set 0
+    ref = oracle.forward(sub["Q"], sub["K"], sub["V"], w.m, w.lam, w.T, grid=(56, 7),
+                         dwc_branch=(np.repeat(dsub[0], len(heads), 0), np.repeat(dsub[1], len(heads), 0)))
+    err = head_rel(got.reshape(w.BH, w.n, w.d)[heads][None], ref)
+    say("  heads %s max rel err %.3e" % (heads, err))
+    assert err <= TOL[w.dtype]
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_backward_convolution_branch(L, dtype):
+    """dV gains DWC^T(dOut); the filter and bias gradients sum over a batch of two."""
+    w = W.Workload("convb", 2, 2, 16 * 20, 32, 20, 5, dtype, 1 / math.sqrt(32), math.sqrt(32), 45, True)
+    check_backward(L, w, grid=(20, 4), dwc=W.make_dwc(2, 32, 3, seed=5))
+    check_backward(L, w.with_(d=64, sigma=0.125, lam=8.0), norm=1, grid=(20, 0),
+                   dwc=W.make_dwc(2, 64, 5, seed=6, bias=False))
+    check_backward(L, w.with_(n=6 * 8, m=6, B=1), norm=2, grid=(8, 0), dwc=W.make_dwc(2, 32, 7, seed=8))

@@ -104,3 +104,12 @@ def small(w, n=None, B=1, H=2, m=None, seed=None):
     n = n if n is not None else w.n
     m = m if m is not None else min(w.m, n)
     return w.with_(name=w.name + "_small", B=B, H=H, n=n, m=m, seed=seed if seed is not None else w.seed + 1000)
+
+
+def make_dwc(H, d, k, seed, bias=True):
+    """Filters [H][d][k][k] ~ N(0, 1/k^2) and a bias [H][d] ~ N(0, 0.1^2) (fp32 numpy arrays;
+    bias None when not drawn) for the depth-wise convolution branch."""
+    rng = np.random.default_rng(seed)
+    w = (rng.standard_normal((H, d, k, k)) / k).astype(np.float32)
+    b = (0.1 * rng.standard_normal((H, d))).astype(np.float32) if bias else None
+    return w, b

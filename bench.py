@@ -120,6 +120,65 @@ def time_train_step(steps):
     return res
 
 
+def time_dwc_branch(steps):
+    """The depth-wise convolution branch of Eq. (7) (3 x 3 filters with bias over the 56 x 56 token
+    map): the bf16 PVT stage-1 forward (7 x 7 window landmarks) with and without the branch, and
+    the fp32 training backward with it.  The branch kernels are HBM-bound: dwc reads V once and
+    writes fp32 DWC(V), dwc_dv reads dOut and reads and writes dV, dwc_dw reads dOut and V (each
+    neighbour row comes back from cache); reported against the 8 TB/s HBM peak."""
+    import torch
+    from paper_2604_20368_amd import lapattn
+    dev = torch.device("cuda:0")
+    res = {}
+    for leg, wname, dt in (("forward", "pvt_stage1", torch.bfloat16), ("backward", "train", torch.float32)):
+        w = W.WORKLOADS[wname]
+        x = W.make_inputs(w, with_grad=True)
+        Q, K, V, dO = (torch.from_numpy(x[k]).to(dev).to(dt) for k in ("Q", "K", "V", "dO"))
+        fw, fb = W.make_dwc(w.H, w.d, 3, seed=11)
+        dwc = (torch.from_numpy(fw).to(dev), torch.from_numpy(fb).to(dev))
+        grid = (56, 7) if leg == "forward" else (56, 0)
+        s = 2 if dt == torch.bfloat16 else 4
+        nd = w.B * w.H * w.n * w.d
+        if leg == "forward":
+            out = torch.empty_like(Q)
+            ws0, ws1 = lapattn.workspace(Q, w.m, w.T), lapattn.workspace(Q, w.m, w.T, dwc=True)
+            plain = lambda: lapattn.forward(Q, K, V, w.m, w.lam, w.T, out=out, ws=ws0, grid=grid)
+            fn = lambda: lapattn.forward(Q, K, V, w.m, w.lam, w.T, out=out, ws=ws1, grid=grid, dwc=dwc)
+            nbytes = {"dwc": nd * (s + 4)}
+        else:
+            grads = tuple(torch.empty_like(Q) for _ in range(3))
+            dg = (torch.empty_like(dwc[0]), torch.empty_like(dwc[1]))
+            ws0 = lapattn.workspace(Q, w.m, w.T, for_backward=True)
+            ws1 = lapattn.workspace(Q, w.m, w.T, for_backward=True, dwc=True)
+            plain = lambda: lapattn.backward(Q, K, V, dO, w.m, w.lam, w.T, grads=grads, ws=ws0, grid=grid)
+            fn = lambda: lapattn.backward(Q, K, V, dO, w.m, w.lam, w.T, grads=grads, ws=ws1, grid=grid, dwc=dwc,
+                                          dwc_grads=dg)
+            nbytes = {"dwc_dv": nd * 4 * 3, "dwc_dw": nd * 4 * 2}
+        r = {"workload": wname, "k": 3, "map": "56x56", "inputs": w.dtype}
+        for tag, f in (("ms_without", plain), ("ms", fn)):
+            for _ in range(3):
+                f()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for _ in range(steps):
+                f()
+            torch.cuda.synchronize()
+            r[tag] = round((time.perf_counter() - t0) * 1e3 / steps, 4)
+        lapattn.lapattn_timing_enable(1)
+        for _ in range(steps):
+            fn()
+        torch.cuda.synchronize()
+        lapattn.lapattn_timing_enable(0)
+        per = {}
+        for k, t in lapattn.lapattn_timing_read(cap=64 * steps + 64):
+            per.setdefault(k, []).append(t)
+        avg = {k: sum(v) / len(v) for k, v in per.items()}
+        r["kernels_ms"] = {k: round(v, 4) for k, v in avg.items()}
+        r["hbm_frac"] = {k: round(b / (avg[k] * 1e-3) / 1e9 / PEAK_HBM_GBS, 3) for k, b in nbytes.items()}
+        res[leg] = r
+    return res
+
+
 KERNEL_SOURCES = ["paper_2604_20368_amd/csrc/fast.hip", "paper_2604_20368_amd/csrc/common.hpp",
                   "paper_2604_20368_amd/csrc/host.cpp"]
 COPY_BYTES = 512 * 1024 * 1024
@@ -177,9 +236,9 @@ def ingest_traffic(kernel, fetch_dir, write_dir, copy_fetch_dir, copy_write_dir,
            "bytes_per_launch": f_k * 1024.0 * ff + w_k * 1024.0 * fw,
            "sources": KERNEL_SOURCES, "sources_sha256": h.hexdigest(),
            "commands": ["rocprofv3 --pmc FETCH_SIZE --output-format csv -d FETCH_DIR -o run -- "
-                        "python3 bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-train-step",
+                        "python3 bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-train-step --no-dwc",
                         "rocprofv3 --pmc WRITE_SIZE --output-format csv -d WRITE_DIR -o run -- "
-                        "python3 bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-train-step",
+                        "python3 bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-train-step --no-dwc",
                         "rocprofv3 --pmc FETCH_SIZE --output-format csv -d COPY_FETCH_DIR -o run -- "
                         "python3 bench.py --calibrate-copy",
                         "rocprofv3 --pmc WRITE_SIZE --output-format csv -d COPY_WRITE_DIR -o run -- "
@@ -198,6 +257,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-train-step", action="store_true",
                     help="skip the training workload's forward and backward timing")
+    ap.add_argument("--no-dwc", action="store_true",
+                    help="skip the timing of the depth-wise convolution branch")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run only the plain copy used to scale the HBM byte counters")
     ap.add_argument("--ingest-traffic", nargs=5, metavar=("KERNEL", "FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR",
@@ -274,6 +335,8 @@ def main():
     }
     if not args.no_train_step:
         res["train_step"] = time_train_step(min(args.steps, 20))
+    if not args.no_dwc:
+        res["dwc_branch"] = time_dwc_branch(min(args.steps, 20))
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(w, x)
     print(json.dumps(res), flush=True)

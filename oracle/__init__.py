@@ -22,4 +22,5 @@ from .oracle import (  # noqa: F401
     NORM_INLINE,
     NORM_ROWSUM,
     NORM_NONE,
+    NORM_MSPACE,
 )

@@ -17,6 +17,8 @@
  *                      with c = ||W||_1 ||W||_inf                  (R2, R3, R9, R10)
  *   key summary        sum_j phi(k_j)^T v_j and sum_j phi(k_j)^T   Sec. 3.2, Eq. (3)
  *   normalisation      z_ij = g_ij - mean_j' g_ij' + 1/n           Eq. (4) with Sigma^{-1/2} = I (R4)
+ *   m-space option     z_il = w_l (a_il - mean_l' a_il') + 1/m,   Appendix B, Eq. (13) with the
+ *                      Out_i = z_i^T M[:, :d]                     offline diagonal w (R15)
  *   output             Z V                                        Eq. (7)
  *   DWC(V)             the depth-wise convolution term of Eq. (7)  (R14), a separate
  *                      function: the caller adds it to Z V
@@ -177,7 +179,7 @@ static void head_free(head_state* s) {
 
 /* One head of the forward: q, k, v are n x d; out is n x d. */
 static void head_forward(const double* q, const double* k, const double* v, double* out,
-                         double lambda, int norm, double eps, head_state* s) {
+                         double lambda, int norm, double eps, const double* wl, head_state* s) {
     const int n = s->n, d = s->d, m = s->m, T = s->T, dv = s->dv;
 
     /* Landmarks (R5): means of the balanced segments [floor(l n/m), floor((l+1) n/m)), or of
@@ -240,6 +242,22 @@ static void head_forward(const double* q, const double* k, const double* v, doub
             s->Y[(size_t)i * dv + c] = acc;
         }
         double si = s->Y[(size_t)i * dv + d];
+        if (norm == ORACLE_NORM_MSPACE) {
+            /* Appendix B: the query's landmark kernel vector a_i, centred by its mean over the
+             * landmarks, whitened by the diagonal w, plus 1/m; it weights the rows of M. */
+            double abar = 0.0;
+            for (int l = 0; l < m; ++l) abar += s->A[(size_t)i * m + l];
+            abar /= m;
+            for (int c = 0; c < d; ++c) {
+                double o = 0.0;
+                for (int l = 0; l < m; ++l) {
+                    const double z = (wl ? wl[l] : 1.0) * (s->A[(size_t)i * m + l] - abar) + 1.0 / m;
+                    o += z * s->M[l * dv + c];
+                }
+                out[(size_t)i * d + c] = o;
+            }
+            continue;
+        }
         for (int c = 0; c < d; ++c) {
             double y = s->Y[(size_t)i * dv + c];
             double o;
@@ -260,7 +278,7 @@ static int check_args(int B, int H, int n, int d, int m, double lambda, int T, i
     if (B < 1 || H < 1 || n < 1 || d < 1 || m < 1 || m > n) return 2;
     if (!(lambda > 0.0) || !isfinite(lambda)) return 3;
     if (T < 0) return 3;
-    if (norm < 0 || norm > 2) return 3;
+    if (norm < 0 || norm > 3) return 3;
     return 0;
 }
 
@@ -276,7 +294,7 @@ int lapattn_oracle_forward(const double* Q, const double* K, const double* V, do
                            int B, int H, int n, int d, int m, double lambda, int T,
                            int norm, double eps, int grid_w, int r,
                            double* Qt, double* Kt, double* Wk, double* Xs,
-                           double* U, double* M, double* Y, double* vbar) {
+                           double* U, double* M, double* Y, double* vbar, const double* whiten) {
     if (!Q || !K || !V || !Out) return 1;
     int rc = check_args(B, H, n, d, m, lambda, T, norm);
     if (rc) return rc;
@@ -286,7 +304,8 @@ int lapattn_oracle_forward(const double* Q, const double* K, const double* V, do
     for (int h = 0; h < BH; ++h) {
         head_state s;
         head_alloc(&s, n, d, m, T, grid_w, r);
-        head_forward(Q + h * hs, K + h * hs, V + h * hs, Out + h * hs, lambda, norm, eps, &s);
+        const double* wl = whiten ? whiten + (size_t)(h % H) * m : NULL;
+        head_forward(Q + h * hs, K + h * hs, V + h * hs, Out + h * hs, lambda, norm, eps, wl, &s);
         if (Qt) memcpy(Qt + (size_t)h * m * d, s.qt, (size_t)m * d * sizeof(double));
         if (Kt) memcpy(Kt + (size_t)h * m * d, s.kt, (size_t)m * d * sizeof(double));
         if (Wk) memcpy(Wk + (size_t)h * m * m, s.Wk, (size_t)m * m * sizeof(double));
@@ -354,10 +373,10 @@ static void ns_backward(const head_state* s, const double* Gin, double* dW) {
 
 static void head_backward(const double* q, const double* k, const double* v, const double* dO,
                           double* dq, double* dk, double* dvv,
-                          double lambda, int norm, double eps, head_state* s) {
+                          double lambda, int norm, double eps, const double* wl, head_state* s) {
     const int n = s->n, d = s->d, m = s->m, T = s->T, dv = s->dv;
     double* outbuf = (double*)malloc((size_t)n * d * sizeof(double));
-    head_forward(q, k, v, outbuf, lambda, norm, eps, s);
+    head_forward(q, k, v, outbuf, lambda, norm, eps, wl, s);
     free(outbuf);
 
     double* dY = (double*)malloc((size_t)n * dv * sizeof(double));
@@ -397,21 +416,62 @@ static void head_backward(const double* q, const double* k, const double* v, con
             dvbar[c] = t;
         }
 
-    /* Y = A M:  dA = dY M^T,  dM = A^T dY;  A = exp(-D/lambda): dD = -A dA / lambda. */
+    if (norm == ORACLE_NORM_MSPACE) {
+        /* Out_i = sum_l z_il M_l[:d], z_il = w_l (a_il - abar_i) + 1/m:
+         *   dz_il = dO_i . M_l[:d],   da_il = w_l dz_il - (1/m) sum_l' w_l' dz_il',
+         *   dM_l[:d] = sum_i z_il dO_i,  dM_l[d] = 0 (the ones column does not enter). */
 #pragma omp parallel for schedule(static)
-    for (int i = 0; i < n; ++i)
-        for (int l = 0; l < m; ++l) {
-            double da = 0.0;
-            for (int c = 0; c < dv; ++c) da += dY[(size_t)i * dv + c] * s->M[l * dv + c];
-            dD[(size_t)i * m + l] = -s->A[(size_t)i * m + l] * da / lambda;
-        }
-#pragma omp parallel for schedule(static)
-    for (int l = 0; l < m; ++l)
-        for (int c = 0; c < dv; ++c) {
+        for (int i = 0; i < n; ++i) {
+            double* dz = (double*)malloc((size_t)m * sizeof(double));
             double t = 0.0;
-            for (int i = 0; i < n; ++i) t += s->A[(size_t)i * m + l] * dY[(size_t)i * dv + c];
-            dM[l * dv + c] = t;
+            for (int l = 0; l < m; ++l) {
+                double a = 0.0;
+                for (int c = 0; c < d; ++c) a += dO[(size_t)i * d + c] * s->M[l * dv + c];
+                dz[l] = a;
+                t += (wl ? wl[l] : 1.0) * a;
+            }
+            for (int l = 0; l < m; ++l) {
+                const double da = (wl ? wl[l] : 1.0) * dz[l] - t / m;
+                dD[(size_t)i * m + l] = -s->A[(size_t)i * m + l] * da / lambda;
+            }
+            free(dz);
         }
+        double* abar = (double*)malloc((size_t)n * sizeof(double));
+        for (int i = 0; i < n; ++i) {
+            double a = 0.0;
+            for (int l = 0; l < m; ++l) a += s->A[(size_t)i * m + l];
+            abar[i] = a / m;
+        }
+#pragma omp parallel for schedule(static)
+        for (int l = 0; l < m; ++l) {
+            for (int c = 0; c < d; ++c) {
+                double t = 0.0;
+                for (int i = 0; i < n; ++i) {
+                    const double z = (wl ? wl[l] : 1.0) * (s->A[(size_t)i * m + l] - abar[i]) + 1.0 / m;
+                    t += z * dO[(size_t)i * d + c];
+                }
+                dM[l * dv + c] = t;
+            }
+            dM[l * dv + d] = 0.0;
+        }
+        free(abar);
+    } else {
+        /* Y = A M:  dA = dY M^T,  dM = A^T dY;  A = exp(-D/lambda): dD = -A dA / lambda. */
+#pragma omp parallel for schedule(static)
+        for (int i = 0; i < n; ++i)
+            for (int l = 0; l < m; ++l) {
+                double da = 0.0;
+                for (int c = 0; c < dv; ++c) da += dY[(size_t)i * dv + c] * s->M[l * dv + c];
+                dD[(size_t)i * m + l] = -s->A[(size_t)i * m + l] * da / lambda;
+            }
+#pragma omp parallel for schedule(static)
+        for (int l = 0; l < m; ++l)
+            for (int c = 0; c < dv; ++c) {
+                double t = 0.0;
+                for (int i = 0; i < n; ++i) t += s->A[(size_t)i * m + l] * dY[(size_t)i * dv + c];
+                dM[l * dv + c] = t;
+            }
+    }
     /* D[i][l] = sum_c |q_ic - kt_lc|  ->  dq_ic += dD sign(.),  dkt_lc -= dD sign(.) */
 #pragma omp parallel for schedule(static)
     for (int i = 0; i < n; ++i)
@@ -508,7 +568,7 @@ static void head_backward(const double* q, const double* k, const double* v, con
 int lapattn_oracle_backward(const double* Q, const double* K, const double* V,
                             const double* dOut, double* dQ, double* dK, double* dV,
                             int B, int H, int n, int d, int m, double lambda, int T,
-                            int norm, double eps, int grid_w, int r) {
+                            int norm, double eps, int grid_w, int r, const double* whiten) {
     if (!Q || !K || !V || !dOut || !dQ || !dK || !dV) return 1;
     int rc = check_args(B, H, n, d, m, lambda, T, norm);
     if (rc) return rc;
@@ -518,8 +578,9 @@ int lapattn_oracle_backward(const double* Q, const double* K, const double* V,
     for (int h = 0; h < BH; ++h) {
         head_state s;
         head_alloc(&s, n, d, m, T, grid_w, r);
+        const double* wl = whiten ? whiten + (size_t)(h % H) * m : NULL;
         head_backward(Q + h * hs, K + h * hs, V + h * hs, dOut + h * hs,
-                      dQ + h * hs, dK + h * hs, dV + h * hs, lambda, norm, eps, &s);
+                      dQ + h * hs, dK + h * hs, dV + h * hs, lambda, norm, eps, wl, &s);
         head_free(&s);
     }
     return 0;

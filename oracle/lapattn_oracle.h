@@ -24,6 +24,9 @@
  *   R9  T counts NS updates; T = 0 returns X0
  *   R10 if the X0 scale is 0, X_t := 0 for every t
  *   R14 the depth-wise convolution branch of Eq. (7): k x k filters, stride 1, zero padding
+ *   R15 ORACLE_NORM_MSPACE: the landmark-space normalised embedding of Appendix B with its
+ *       diagonal whitening w (per head, given; NULL = ones) in place of the query's landmark
+ *       kernel vector: z_il = w_l (a_il - mean_l' a_il') + 1/m, Out_i = sum_l z_il M[l][:d]
  */
 #ifndef LAPATTN_ORACLE_H
 #define LAPATTN_ORACLE_H
@@ -32,7 +35,7 @@
 extern "C" {
 #endif
 
-enum { ORACLE_NORM_INLINE = 0, ORACLE_NORM_ROWSUM = 1, ORACLE_NORM_NONE = 2 };
+enum { ORACLE_NORM_INLINE = 0, ORACLE_NORM_ROWSUM = 1, ORACLE_NORM_NONE = 2, ORACLE_NORM_MSPACE = 3 };
 
 /* Laplacian kernel k(x, y) = exp(-||x - y||_1 / lambda)  (Sec. 1; Sec. 4.1). */
 double lapattn_oracle_kernel(const double* x, const double* y, int d, double lambda);
@@ -63,19 +66,20 @@ double lapattn_oracle_ns(const double* W, int m, int T, double eps, double* Xs);
  *   Y       [BH][n][d+1]   K_QL * M   (column d is the row sum s_i of G^)
  *   vbar    [BH][d]        mean of the values
  * grid_w, r select the landmark windows (lapattn_oracle_windows; 0, 0 = segments).
- * Returns 0 on success, nonzero on a bad argument. */
+ * whiten [H][m] is the diagonal of ORACLE_NORM_MSPACE (NULL: ones; ignored by the other
+ * normalisations).  Returns 0 on success, nonzero on a bad argument. */
 int lapattn_oracle_forward(const double* Q, const double* K, const double* V, double* Out,
                            int B, int H, int n, int d, int m, double lambda, int T,
                            int norm, double eps, int grid_w, int r,
                            double* Qt, double* Kt, double* Wk, double* Xs,
-                           double* U, double* M, double* Y, double* vbar);
+                           double* U, double* M, double* Y, double* vbar, const double* whiten);
 
 /* Backward pass: gradients of sum(Out * dOut) with respect to Q, K, V.
  * dQ, dK, dV are [B][H][n][d] and are overwritten.  Returns 0 on success. */
 int lapattn_oracle_backward(const double* Q, const double* K, const double* V,
                             const double* dOut, double* dQ, double* dK, double* dV,
                             int B, int H, int n, int d, int m, double lambda, int T,
-                            int norm, double eps, int grid_w, int r);
+                            int norm, double eps, int grid_w, int r, const double* whiten);
 
 /* Depth-wise convolution branch of Eq. (7), DWC(V) (reading R14): the n tokens of each head
  * form an H' x W' map in row-major order (W' = grid_w, H' = n / W'), and each value channel c

@@ -14,7 +14,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "lapattn_oracle.c")
 _LIB = os.path.join(_HERE, "liblapattn_oracle.so")
 
-NORM_INLINE, NORM_ROWSUM, NORM_NONE = 0, 1, 2
+NORM_INLINE, NORM_ROWSUM, NORM_NONE, NORM_MSPACE = 0, 1, 2, 3
 
 _lib = None
 _dp = ctypes.POINTER(ctypes.c_double)
@@ -71,10 +71,10 @@ def _configure(lib):
     lib.lapattn_oracle_windows.restype = ctypes.c_int
     lib.lapattn_oracle_windows.argtypes = [ctypes.c_int] * 4 + [ctypes.POINTER(ctypes.c_int)] * 2
     lib.lapattn_oracle_forward.argtypes = ([_dp] * 4 + [ctypes.c_int] * 5 + [ctypes.c_double, ctypes.c_int,
-                                           ctypes.c_int, ctypes.c_double, ctypes.c_int, ctypes.c_int] + [_dp] * 8)
+                                           ctypes.c_int, ctypes.c_double, ctypes.c_int, ctypes.c_int] + [_dp] * 9)
     lib.lapattn_oracle_backward.restype = ctypes.c_int
     lib.lapattn_oracle_backward.argtypes = ([_dp] * 7 + [ctypes.c_int] * 5 + [ctypes.c_double, ctypes.c_int,
-                                            ctypes.c_int, ctypes.c_double, ctypes.c_int, ctypes.c_int])
+                                            ctypes.c_int, ctypes.c_double, ctypes.c_int, ctypes.c_int, _dp])
     lib.lapattn_oracle_dwc.restype = ctypes.c_int
     lib.lapattn_oracle_dwc.argtypes = [_dp] * 4 + [ctypes.c_int] * 6
     lib.lapattn_oracle_dwc_backward.restype = ctypes.c_int
@@ -166,9 +166,19 @@ def dwc_backward(V, weight, dE, grid_w):
     return dV, dW, db
 
 
-def forward(Q, K, V, m, lam, T, norm=NORM_INLINE, eps=0.0, intermediates=False, grid=None, dwc_branch=None):
+def _whiten(whiten, H, m):
+    if whiten is None:
+        return None
+    w = _f64(whiten)
+    assert w.shape == (H, m)
+    return w
+
+
+def forward(Q, K, V, m, lam, T, norm=NORM_INLINE, eps=0.0, intermediates=False, grid=None, dwc_branch=None,
+            whiten=None):
     """Out = Z V (+ DWC(V) when dwc_branch = (weight, bias) is given, over the token map of width
-    grid[0]); grid = (W', r) selects r x r landmark windows when r > 0."""
+    grid[0]); grid = (W', r) selects r x r landmark windows when r > 0; whiten [H][m] is the
+    diagonal of NORM_MSPACE (None: ones)."""
     Q, K, V = _f64(Q), _f64(K), _f64(V)
     B, H, n, d = Q.shape
     assert K.shape == Q.shape and V.shape == Q.shape
@@ -183,7 +193,8 @@ def forward(Q, K, V, m, lam, T, norm=NORM_INLINE, eps=0.0, intermediates=False, 
         ptrs = [inter[k] for k in ("Qt", "Kt", "W", "Xs", "U", "M", "Y", "vbar")]
     gw, r = _attention_grid(grid)
     rc = load().lapattn_oracle_forward(_p(Q), _p(K), _p(V), _p(out), B, H, n, d, int(m), float(lam),
-                                       int(T), int(norm), float(eps), int(gw), int(r), *[_p(a) for a in ptrs])
+                                       int(T), int(norm), float(eps), int(gw), int(r), *[_p(a) for a in ptrs],
+                                       _p(_whiten(whiten, H, m)))
     if rc:
         raise ValueError("oracle forward rejected its arguments (code %d)" % rc)
     if dwc_branch is not None:
@@ -193,7 +204,7 @@ def forward(Q, K, V, m, lam, T, norm=NORM_INLINE, eps=0.0, intermediates=False, 
     return (out, inter) if intermediates else out
 
 
-def backward(Q, K, V, dO, m, lam, T, norm=NORM_INLINE, eps=0.0, grid=None, dwc_branch=None):
+def backward(Q, K, V, dO, m, lam, T, norm=NORM_INLINE, eps=0.0, grid=None, dwc_branch=None, whiten=None):
     """(dQ, dK, dV), and with dwc_branch = (weight, bias) also (dweight, dbias)."""
     Q, K, V, dO = _f64(Q), _f64(K), _f64(V), _f64(dO)
     B, H, n, d = Q.shape
@@ -201,7 +212,7 @@ def backward(Q, K, V, dO, m, lam, T, norm=NORM_INLINE, eps=0.0, grid=None, dwc_b
     gw, r = _attention_grid(grid)
     rc = load().lapattn_oracle_backward(_p(Q), _p(K), _p(V), _p(dO), _p(dQ), _p(dK), _p(dV),
                                         B, H, n, d, int(m), float(lam), int(T), int(norm), float(eps),
-                                        int(gw), int(r))
+                                        int(gw), int(r), _p(_whiten(whiten, H, m)))
     if rc:
         raise ValueError("oracle backward rejected its arguments (code %d)" % rc)
     if dwc_branch is None:

@@ -364,8 +364,8 @@ def test_forward_factored_equals_explicit_nystrom(oracle_lib):
 
 # ----------------------------------------------------------------------------- backward
 
-def fd_check(Q, K, V, dO, m, lam, T, norm, eps=0.0, h=1e-6):
-    dQ, dK, dV = oracle.backward(Q, K, V, dO, m, lam, T, norm, eps)
+def fd_check(Q, K, V, dO, m, lam, T, norm, eps=0.0, h=1e-6, whiten=None):
+    dQ, dK, dV = oracle.backward(Q, K, V, dO, m, lam, T, norm, eps, whiten=whiten)
     grads = {"Q": dQ, "K": dK, "V": dV}
     base = {"Q": Q, "K": K, "V": V}
     worst = 0.0
@@ -374,9 +374,9 @@ def fd_check(Q, K, V, dO, m, lam, T, norm, eps=0.0, h=1e-6):
         for idx in np.ndindex(Q.shape):
             args = {k: v.copy() for k, v in base.items()}
             args[name][idx] += h
-            lp = (oracle.forward(args["Q"], args["K"], args["V"], m, lam, T, norm, eps) * dO).sum()
+            lp = (oracle.forward(args["Q"], args["K"], args["V"], m, lam, T, norm, eps, whiten=whiten) * dO).sum()
             args[name][idx] -= 2 * h
-            lm = (oracle.forward(args["Q"], args["K"], args["V"], m, lam, T, norm, eps) * dO).sum()
+            lm = (oracle.forward(args["Q"], args["K"], args["V"], m, lam, T, norm, eps, whiten=whiten) * dO).sum()
             g[idx] = (lp - lm) / (2 * h)
         scale = max(np.abs(g).max(), 1e-12)
         worst = max(worst, np.abs(g - grads[name]).max() / scale)
@@ -583,3 +583,52 @@ def test_dwc_rejections(oracle_lib):
         w = np.zeros((1, 2, max(k, 1), max(k, 1))) if k > 0 else np.zeros((1, 2, 0, 0))
         with pytest.raises(ValueError):
             oracle.dwc(V, w, None, gw)
+
+
+# ----------------------------------------------------------------------------- m-space normalisation (R15)
+
+def dense_whitened_attention(Q, K, V, lam, w):
+    """Eq. (4) written out densely with a diagonal whitening over the keys:
+    z_ij = w_j (g_ij - mean_j' g_ij') + 1/n, out = Z V."""
+    G = np.exp(-np.abs(Q[:, None, :] - K[None, :, :]).sum(-1) / lam)
+    n = K.shape[0]
+    Z = (G - G.mean(axis=1, keepdims=True)) * w[None, :] + 1.0 / n
+    return Z @ V
+
+
+@pytest.mark.parametrize("n,d,lam", [(16, 8, math.sqrt(8)), (24, 4, 4.0)])
+def test_mspace_landmarks_equal_tokens_is_dense_whitened_attention(oracle_lib, n, d, lam):
+    """With m = n the landmarks are the keys, M = K_LL^-1 K_LK V = V once Newton-Schulz has
+    converged, and the landmark-space embedding of Appendix B with diagonal w is Eq. (4) with
+    the whitening diag(w) over the keys; w = 1 gives the inline normalisation."""
+    rng = np.random.default_rng(n + d)
+    Q, K, V = rand_qkv(rng, 1, 2, n, d)
+    w = rng.uniform(0.5, 1.5, size=(2, n))
+    out, it = oracle.forward(Q, K, V, n, lam, 60, oracle.NORM_MSPACE, intermediates=True, whiten=w)
+    ones = oracle.forward(Q, K, V, n, lam, 60, oracle.NORM_MSPACE)
+    inline = oracle.forward(Q, K, V, n, lam, 60, oracle.NORM_INLINE)
+    for h in range(2):
+        floor = 1e-15 * np.linalg.cond(it["W"][0, h]) * n
+        assert rel(out[0, h], dense_whitened_attention(Q[0, h], K[0, h], V[0, h], lam, w[h])) < max(floor, 1e-12)
+        assert rel(ones[0, h], dense_laplacian_attention(Q[0, h], K[0, h], V[0, h], lam, oracle.NORM_INLINE)) < max(floor, 1e-12)
+        assert rel(ones[0, h], inline[0, h]) < max(floor, 1e-12)
+
+
+def test_mspace_zero_whitening_gives_the_mean_landmark_row(oracle_lib):
+    """w = 0 leaves only the 1/m offset: every output row is the mean of the rows of M[:, :d]."""
+    rng = np.random.default_rng(31)
+    n, d, m = 30, 3, 7
+    Q, K, V = rand_qkv(rng, 2, 1, n, d)
+    out, it = oracle.forward(Q, K, V, m, 1.5, 5, oracle.NORM_MSPACE, intermediates=True, whiten=np.zeros((1, m)))
+    for b in range(2):
+        mean_row = it["M"][b, 0, :, :d].mean(axis=0)
+        np.testing.assert_allclose(out[b, 0], np.broadcast_to(mean_row, (n, d)), rtol=1e-13, atol=1e-15)
+
+
+@pytest.mark.parametrize("n,d,m,T,lam", [(13, 3, 5, 4, 1.5), (9, 5, 1, 2, 3.0), (12, 2, 12, 3, 2.0)])
+def test_mspace_backward_matches_finite_differences(oracle_lib, n, d, m, T, lam):
+    rng = np.random.default_rng(n * 7 + m)
+    Q, K, V = rand_qkv(rng, 1, 2, n, d, 0.7)
+    dO = rng.standard_normal(Q.shape)
+    w = rng.uniform(0.3, 1.7, size=(2, m))
+    assert fd_check(Q, K, V, dO, m, lam, T, oracle.NORM_MSPACE, whiten=w) < 1e-7

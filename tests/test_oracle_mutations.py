@@ -27,7 +27,8 @@ MUTANTS = {
     "row norm used twice": ("double c = n1 * ninf;", "double c = ninf * ninf;"),
     "mean-value gradient dropped": ("tv + dvbar[c] / n", "tv"),
     "NS factors swapped": ("matmul(X, WX, Xn, m, m, m);", "matmul(WX, X, Xn, m, m, m);"),
-    "kernel gradient sign": ("dD[(size_t)i * m + l] = -s->A", "dD[(size_t)i * m + l] = s->A"),
+    "kernel gradient sign": ("s->M[l * dv + c];\n                dD[(size_t)i * m + l] = -s->A",
+                             "s->M[l * dv + c];\n                dD[(size_t)i * m + l] = s->A"),
     "K_LL backward dropped": ("dqt[a * d + c] += g * sg;", "dqt[a * d + c] += 0 * g * sg;"),
     "rowsum backward power": ("dYi[d] = -t / (si * si);", "dYi[d] = -t / si;"),
     "ones column wrong": ("(c < d ? v[(size_t)j * d + c] : 1.0)", "(c < d ? v[(size_t)j * d + c] : 0.5)"),
@@ -48,6 +49,19 @@ MUTANTS = {
     "DWC bias gradient misses the batch": ("dbias[h * d + c] += gi;", "dbias[h * d + c] = gi;"),
     "DWC filter gradient misses the batch": ("for (size_t e = 0; e < (size_t)H * d * k * k; ++e) dWt[e] = 0.0;\n    for (size_t e = 0; e < (size_t)H * d; ++e) dbias[e] = 0.0;\n    for (int b = 0; b < B; ++b)\n        for (int h = 0; h < H; ++h) {",
         "for (size_t e = 0; e < (size_t)H * d; ++e) dbias[e] = 0.0;\n    for (int b = 0; b < B; ++b)\n        for (int h = 0; h < H; ++h) {\n            for (size_t e = (size_t)h * d * k * k; e < (size_t)(h + 1) * d * k * k; ++e) dWt[e] = 0.0;"),
+    "m-space centring dropped": (
+        "const double z = (wl ? wl[l] : 1.0) * (s->A[(size_t)i * m + l] - abar) + 1.0 / m;\n                    o += z",
+        "const double z = (wl ? wl[l] : 1.0) * (s->A[(size_t)i * m + l]) + 1.0 / m;\n                    o += z"),
+    "m-space offset 1/n": (
+        "const double z = (wl ? wl[l] : 1.0) * (s->A[(size_t)i * m + l] - abar) + 1.0 / m;\n                    o += z",
+        "const double z = (wl ? wl[l] : 1.0) * (s->A[(size_t)i * m + l] - abar) + 1.0 / n;\n                    o += z"),
+    "m-space whitening misses the mean": (
+        "const double z = (wl ? wl[l] : 1.0) * (s->A[(size_t)i * m + l] - abar) + 1.0 / m;\n                    o += z",
+        "const double z = (wl ? wl[l] : 1.0) * s->A[(size_t)i * m + l] - abar + 1.0 / m;\n                    o += z"),
+    "m-space backward mean term dropped": ("const double da = (wl ? wl[l] : 1.0) * dz[l] - t / m;",
+                                           "const double da = (wl ? wl[l] : 1.0) * dz[l];"),
+    "m-space dM from the kernel values": ("t += z * dO[(size_t)i * d + c];",
+                                          "t += s->A[(size_t)i * m + l] * dO[(size_t)i * d + c];"),
     "query/key landmarks swapped in K_LL": (
         "s->Wk[a * m + b] = lapattn_oracle_kernel(s->qt + a * d, s->kt + b * d, d, lambda);",
         "s->Wk[a * m + b] = lapattn_oracle_kernel(s->kt + a * d, s->qt + b * d, d, lambda);"),
@@ -76,6 +90,9 @@ PIN_CALLS = [
     lambda: pins.test_dwc_is_library_cross_correlation(None, 5, 7, 3),
     lambda: pins.test_dwc_one_hot_filters_shift_the_map(None),
     lambda: pins.test_dwc_backward_matches_finite_differences(None),
+    lambda: pins.test_mspace_landmarks_equal_tokens_is_dense_whitened_attention(None, 16, 8, 8 ** 0.5),
+    lambda: pins.test_mspace_zero_whitening_gives_the_mean_landmark_row(None),
+    lambda: pins.test_mspace_backward_matches_finite_differences(None, 13, 3, 5, 4, 1.5),
 ]
 
 

@@ -19,6 +19,10 @@
  *                 of Eq. (4) with the whitening taken as the identity
  *               LAPATTN_NORM_ROWSUM:  (G^ V)_i / s_i       (Eq. (3))
  *               LAPATTN_NORM_NONE:    (G^ V)_i
+ *               LAPATTN_NORM_MSPACE:  sum_l z_il M[l][:d],  M = X_T (K_LK V),
+ *                 z_il = w_l (a_il - mean_l' a_il') + 1/m with a_il = K_QL[i][l]: the
+ *                 landmark-space normalised embedding of Appendix B, whose m x m diagonal
+ *                 whitening w is given per head (lapattn_opts.whiten)
  * Optional depth-wise convolution branch of Eq. (7), off by default (lapattn_opts.dwc_k):
  *   Out_i += DWC(V)_i, each value channel of each head cross-correlated over the token map
  *   with its own k x k filter (stride 1, zero padding (k-1)/2) plus a per-channel bias.
@@ -62,7 +66,8 @@ typedef enum { LAPATTN_FP32 = 0, LAPATTN_BF16 = 1 } lapattn_dtype;
 typedef enum {
     LAPATTN_NORM_INLINE = 0,
     LAPATTN_NORM_ROWSUM = 1,
-    LAPATTN_NORM_NONE = 2
+    LAPATTN_NORM_NONE = 2,
+    LAPATTN_NORM_MSPACE = 3
 } lapattn_norm;
 
 enum {
@@ -82,7 +87,7 @@ enum {
                                      workspace is not 256-byte aligned */
 };
 
-/* Options; a NULL pointer means all fields zero: {LAPATTN_NORM_INLINE, 0.0f, 0, 0, 0, NULL...}.
+/* Options; a NULL pointer means all fields zero: {LAPATTN_NORM_INLINE, 0.0f, 0, 0, 0, NULL, ...}.
  * eps is the diagonal perturbation W <- W + eps I of Algorithm 2 (>= 0).
  * Token map: with grid_w > 0 the n tokens form a row-major H' x W' map (W' = grid_w,
  * H' = n / W'; n must be a multiple of W', LAPATTN_ERR_SHAPE otherwise).
@@ -100,7 +105,9 @@ enum {
  * [H][d][k][k] of fp32 and dwc_b [H][d] fp32 or NULL (no bias), shared by the batch, for
  * either dtype.  lapattn_backward adds the branch's part to dV and, when the pointers are
  * not NULL, writes the filter gradient dwc_dw [H][d][k][k] and the bias gradient dwc_db [H][d]
- * (fp32, summed over the batch, overwritten); lapattn_forward ignores those two. */
+ * (fp32, summed over the batch, overwritten); lapattn_forward ignores those two.
+ * whiten: with LAPATTN_NORM_MSPACE, the diagonal whitening w as a device array [H][m] of fp32
+ * shared by the batch (NULL: all ones); ignored by the other normalisations. */
 typedef struct {
     int norm;            /* lapattn_norm */
     float eps;
@@ -111,6 +118,7 @@ typedef struct {
     const float* dwc_b;  /* device [H][d] bias, or NULL */
     float* dwc_dw;       /* backward: device [H][d][k][k] filter gradient, or NULL */
     float* dwc_db;       /* backward: device [H][d] bias gradient, or NULL */
+    const float* whiten; /* LAPATTN_NORM_MSPACE: device [H][m] diagonal whitening, or NULL */
 } lapattn_opts;
 
 /* Workspace flags. */

@@ -31,14 +31,20 @@ static inline float kscale_of(float lambda) { return (float)(-1.4426950408889634
 //   Pass 2: dq_i += dD_il sign(q_i - kt_l).
 //   dvbar partial (inline normalisation): sum over the block's queries of (1 - s_i) dO_i,
 //   per wave through the tile, then over the waves in order.
+//   Landmark-space normalisation (Appendix B): the same as inline with M's rows scaled by the
+//   whitening, its ones column replaced by 1/m and vbar by sum_l w_l M_l (mvec); the partial
+//   sums of (1 - s_i) dO_i and of dO_i (into p0_part) give the gradient of the two vectors.
 template <int D, int NORM>
 __global__ __launch_bounds__(256) void bwd_query_kernel(const float* __restrict__ Q, const float* __restrict__ dO,
                                                         float* __restrict__ dQ, const float* __restrict__ kt,
                                                         const float* __restrict__ M, const float* __restrict__ vbar,
                                                         float* __restrict__ Aq, float* __restrict__ dDq,
                                                         float* __restrict__ rs, float* __restrict__ dYd,
-                                                        float* __restrict__ dvbar_part, int n, int m,
+                                                        float* __restrict__ dvbar_part, float* __restrict__ p0_part,
+                                                        const float* __restrict__ whiten,
+                                                        const float* __restrict__ mvec, int H, int n, int m,
                                                         float kscale, float inv_lambda, int nqb) {
+    constexpr bool CENTRED = NORM == NORM_INLINE || NORM == NORM_MSPACE;
     constexpr int D1 = D + 1;
     constexpr int NCH = D / 32;
     constexpr int TP = 65;                 // tile pitch: lane-strided accesses are conflict-free
@@ -47,8 +53,19 @@ __global__ __launch_bounds__(256) void bwd_query_kernel(const float* __restrict_
     __shared__ float sT[4 * 64 * TP];
     __shared__ float sred[4 * D];
     const int h = blockIdx.y, tid = threadIdx.x, w = tid >> 6, l = tid & 63;
-    for (int e = tid; e < 64 * D1; e += 256) sM[e] = (e < m * D1) ? M[(size_t)h * m * D1 + e] : 0.f;
-    if (tid < D) sVb[tid] = vbar[(size_t)h * D + tid];
+    if (NORM == NORM_MSPACE) {
+        const float* wl = whiten ? whiten + (size_t)(h % H) * m : nullptr;
+        for (int e = tid; e < 64 * D1; e += 256) {
+            const int a = e / D1, cc = e % D1;
+            float v = 0.f;
+            if (a < m) v = cc < D ? (wl ? wl[a] : 1.f) * M[(size_t)h * m * D1 + e] : 1.f / (float)m;
+            sM[e] = v;
+        }
+        if (tid < D) sVb[tid] = mvec[(size_t)h * 2 * D + tid];
+    } else {
+        for (int e = tid; e < 64 * D1; e += 256) sM[e] = (e < m * D1) ? M[(size_t)h * m * D1 + e] : 0.f;
+        if (tid < D) sVb[tid] = vbar[(size_t)h * D + tid];
+    }
     float* tile = sT + w * 64 * TP;
     const int i0 = blockIdx.x * 256 + w * 64;
     const int i = i0 + l;
@@ -105,7 +122,7 @@ __global__ __launch_bounds__(256) void bwd_query_kernel(const float* __restrict_
         }
     }
     float rsc = 1.f, dyd = 0.f;
-    if (NORM == NORM_INLINE) {
+    if (CENTRED) {
         float t = 0.f;
 #pragma unroll
         for (int c = 0; c < D; ++c) t = fmaf(g[c], sVb[c], t);
@@ -169,8 +186,8 @@ __global__ __launch_bounds__(256) void bwd_query_kernel(const float* __restrict_
         for (int c4 = 0; c4 < D / 4; ++c4)
             reinterpret_cast<float4*>(dQ + row)[c4] = make_float4(dq[4 * c4], dq[4 * c4 + 1], dq[4 * c4 + 2], dq[4 * c4 + 3]);
     }
-    // dvbar partial
-    if (NORM == NORM_INLINE) {
+    // dvbar partial (and for the landmark-space form the plain sum of dO)
+    if (CENTRED) {
         __builtin_amdgcn_wave_barrier();
         const float wt = live ? 1.f - s : 0.f;
 #pragma unroll
@@ -185,6 +202,22 @@ __global__ __launch_bounds__(256) void bwd_query_kernel(const float* __restrict_
         if (tid < D)
             dvbar_part[((size_t)h * nqb + blockIdx.x) * D + tid] =
                 ((sred[tid] + sred[D + tid]) + sred[2 * D + tid]) + sred[3 * D + tid];
+        if (NORM == NORM_MSPACE) {
+            __syncthreads();   // sred is reused
+            const float wg = live ? 1.f : 0.f;
+#pragma unroll
+            for (int c = 0; c < D; ++c) tile[l * TP + c] = wg * g[c];
+            __builtin_amdgcn_wave_barrier();
+            if (l < D) {
+                float t = 0.f;
+                for (int r = 0; r < 64; ++r) t += tile[r * TP + l];
+                sred[w * D + l] = t;
+            }
+            __syncthreads();
+            if (tid < D)
+                p0_part[((size_t)h * nqb + blockIdx.x) * D + tid] =
+                    ((sred[tid] + sred[D + tid]) + sred[2 * D + tid]) + sred[3 * D + tid];
+        }
     } else if (tid < D) {
         dvbar_part[((size_t)h * nqb + blockIdx.x) * D + tid] = 0.f;
     }
@@ -334,8 +367,9 @@ __global__ __launch_bounds__(256) void bwd_ns_kernel(const float* __restrict__ q
                                                      const float* __restrict__ U, const float* __restrict__ dM_part,
                                                      const float* __restrict__ dvbar_part, float* __restrict__ dU,
                                                      float* __restrict__ dvbar, float* __restrict__ dqtW,
-                                                     float* __restrict__ dktW, int n, int m, int T, double lambda,
-                                                     double eps, int nlc, int nqb) {
+                                                     float* __restrict__ dktW, const float* __restrict__ p0_part,
+                                                     const float* __restrict__ whiten, int mspace, int H, int n,
+                                                     int m, int T, double lambda, double eps, int nlc, int nqb) {
     using SQ = ns_tiles<MP, MP>;
     using SU = ns_tiles<MP, D>;
     constexpr int D1 = D + 1;
@@ -348,6 +382,7 @@ __global__ __launch_bounds__(256) void bwd_ns_kernel(const float* __restrict__ q
     __shared__ double lds[LDSN];
     __shared__ double su1[MP], sdm1[MP];
     __shared__ double svb[256];
+    __shared__ double sp1[D], sp0[D];   // landmark-space form: sums of (1 - s_i) dO_i and of dO_i
     double* sW = lds;
     double* sX = lds + MP * P;
     double* sG = lds + 2 * MP * P;
@@ -361,7 +396,8 @@ __global__ __launch_bounds__(256) void bwd_ns_kernel(const float* __restrict__ q
     const int code = (int)cinfo[h * 4 + 3];
 
     // dvbar (inline normalisation; zeros otherwise because the partials are zero): 256 / D
-    // partial sums per column over the query blocks, then in order
+    // partial sums per column over the query blocks, then in order.  The landmark-space form
+    // keeps that sum (sp1) and the sum of dO (sp0) for the gradient of M, and has no dvbar.
     {
         constexpr int G = 256 / D;
         const int g = tid / D, cc = tid % D;
@@ -374,8 +410,23 @@ __global__ __launch_bounds__(256) void bwd_ns_kernel(const float* __restrict__ q
             double t = 0.0;
 #pragma unroll
             for (int gg = 0; gg < G; ++gg) t += svb[gg * D + tid];
-            dvbar[(size_t)h * D + tid] = (float)t;
+            sp1[tid] = t;
+            dvbar[(size_t)h * D + tid] = mspace ? 0.f : (float)t;
         }
+        if (mspace) {
+            __syncthreads();
+            double s0 = 0.0;
+            for (int b = g; b < nqb; b += G) s0 += p0_part[((size_t)h * nqb + b) * D + cc];
+            svb[tid] = s0;
+            __syncthreads();
+            if (tid < D) {
+                double t = 0.0;
+#pragma unroll
+                for (int gg = 0; gg < G; ++gg) t += svb[gg * D + tid];
+                sp0[tid] = t;
+            }
+        }
+        __syncthreads();
     }
     {
         double* sU = lds;
@@ -396,6 +447,21 @@ __global__ __launch_bounds__(256) void bwd_ns_kernel(const float* __restrict__ q
                 const int e = tid + 256 * r;
                 const float v = dp[min(e, lim)];
                 dm[r] += (e <= lim) ? (double)v : 0.0;
+            }
+        }
+        if (mspace) {
+            // the partials hold the gradient of M~ = diag(w) M with the ones column 1/m; with
+            // mw = sum_l w_l M_l and mb = (1/m) sum_l M_l entering as - s_i mw + mb:
+            // dM_l[:d] = w_l (dM~_l + sp1 - sp0) + sp0 / m, and no gradient for the ones column
+            const float* wl = whiten ? whiten + (size_t)(h % H) * m : nullptr;
+#pragma unroll
+            for (int r = 0; r < NE; ++r) {
+                const int e = tid + 256 * r;
+                const int a = e / D1, cc = e % D1;
+                if (e <= lim) {
+                    const double wa = wl ? (double)wl[a] : 1.0;
+                    dm[r] = cc < D ? wa * (dm[r] + sp1[cc] - sp0[cc]) + sp0[cc] / m : 0.0;
+                }
             }
         }
         float uv[NE];
@@ -893,19 +959,22 @@ hipError_t launch_narrow_bf16(const float* gQ, const float* gK, const float* gV,
 
 hipError_t launch_bwd_query(int norm, const float* Q, const float* dO, float* dQ, const float* kt, const float* M,
                             const float* vbar, float* Aq, float* dDq, float* rs, float* dYd, float* dvbar_part,
-                            int BH, int n, int d, int m, float lambda, int nqb, hipStream_t st) {
+                            float* p0_part, const float* whiten, const float* mvec, int BH, int H, int n, int d,
+                            int m, float lambda, int nqb, hipStream_t st) {
     const float ks = kscale_of(lambda), il = 1.f / lambda;
     dim3 grid(nqb, BH);
 #define LAPATTN_BQ(Dv, Nv)                                                                                  \
     hipLaunchKernelGGL((bwd_query_kernel<Dv, Nv>), grid, dim3(256), 0, st, Q, dO, dQ, kt, M, vbar, Aq, dDq, rs, \
-                       dYd, dvbar_part, n, m, ks, il, nqb)
+                       dYd, dvbar_part, p0_part, whiten, mvec, H, n, m, ks, il, nqb)
     if (d == 32) {
         if (norm == NORM_INLINE) LAPATTN_BQ(32, NORM_INLINE);
         else if (norm == NORM_ROWSUM) LAPATTN_BQ(32, NORM_ROWSUM);
+        else if (norm == NORM_MSPACE) LAPATTN_BQ(32, NORM_MSPACE);
         else LAPATTN_BQ(32, NORM_NONE);
     } else {
         if (norm == NORM_INLINE) LAPATTN_BQ(64, NORM_INLINE);
         else if (norm == NORM_ROWSUM) LAPATTN_BQ(64, NORM_ROWSUM);
+        else if (norm == NORM_MSPACE) LAPATTN_BQ(64, NORM_MSPACE);
         else LAPATTN_BQ(64, NORM_NONE);
     }
 #undef LAPATTN_BQ
@@ -927,11 +996,11 @@ hipError_t launch_bwd_query_lm(const float* Q, const float* dO, const float* kt,
 
 hipError_t launch_bwd_ns(const float* qt, const float* kt, const double* Xs, const double* cinfo, const float* U,
                          const float* dM_part, const float* dvbar_part, float* dU, float* dvbar, float* dqtW,
-                         float* dktW, int BH, int n, int d, int m, int T, double lambda, double eps, int nlc,
-                         int nqb, int MP, hipStream_t st) {
+                         float* dktW, const float* p0_part, const float* whiten, int mspace, int BH, int H, int n,
+                         int d, int m, int T, double lambda, double eps, int nlc, int nqb, int MP, hipStream_t st) {
 #define LAPATTN_BNS(MPv, Dv)                                                                                      \
     hipLaunchKernelGGL((bwd_ns_kernel<MPv, Dv>), dim3(BH), dim3(256), 0, st, qt, kt, Xs, cinfo, U, dM_part,       \
-                       dvbar_part, dU, dvbar, dqtW, dktW, n, m, T, lambda, eps, nlc, nqb)
+                       dvbar_part, dU, dvbar, dqtW, dktW, p0_part, whiten, mspace, H, n, m, T, lambda, eps, nlc, nqb)
     if (MP == 32 && d == 32) LAPATTN_BNS(32, 32);
     else if (MP == 32) LAPATTN_BNS(32, 64);
     else if (d == 32) LAPATTN_BNS(64, 32);

@@ -7,7 +7,7 @@
 namespace lapattn {
 
 enum { DT_F32 = 0, DT_BF16 = 1 };
-enum { NORM_INLINE = 0, NORM_ROWSUM = 1, NORM_NONE = 2 };
+enum { NORM_INLINE = 0, NORM_ROWSUM = 1, NORM_NONE = 2, NORM_MSPACE = 3 };
 
 // Element access for the two storage types.  bf16 is carried as raw 16-bit
 // patterns; widening is exact, narrowing rounds to nearest even.

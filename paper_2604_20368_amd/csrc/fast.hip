@@ -852,7 +852,8 @@ template <int D>
 __global__ __launch_bounds__(512) void mfinal_kernel(const float* __restrict__ Upart, const float* __restrict__ XT,
                                                      _Float16* __restrict__ Mt, float* __restrict__ mscale,
                                                      float* __restrict__ Mones, float* __restrict__ Mout, int m,
-                                                     int nkb) {
+                                                     int nkb, const float* __restrict__ whiten, int mspace, int H,
+                                                     float* __restrict__ mvec) {
     constexpr int D1 = D + 1;
     constexpr int CB = D / 32;
     constexpr int NG = D / 8 + 1;
@@ -892,13 +893,32 @@ __global__ __launch_bounds__(512) void mfinal_kernel(const float* __restrict__ U
     }
     __syncthreads();
     // M[a][c0 + cc] = sum_b X_T[a][b] U[b][c0 + cc]: thread (cc = tid/64, a = tid%64)
+    // landmark-space normalisation: the operand rows are w_l M[l] (whitening w, ones when
+    // whiten is NULL), and each value column also gives sum_l w_l M[l][c] and (1/m) sum_l M[l][c]
     float mv = 0.f;
     if (w < nc) {
         float t = 0.f;
 #pragma unroll 16
         for (int b = 0; b < 64; ++b) t = fmaf(sX[l * 65 + b], sU[w * 64 + b], t);
-        sM[w * 64 + l] = t;
         if (l < m) Mout[((size_t)h * m + l) * D1 + c0 + w] = t;
+        if (mspace && !ones) {
+            const float tv = l < m ? t : 0.f;
+            float tw = whiten && l < m ? whiten[(size_t)(h % H) * m + l] * tv : tv;
+            sM[w * 64 + l] = tw;
+            float s1 = tw, s0 = tv;
+#pragma unroll
+            for (int off = 32; off >= 1; off >>= 1) {
+                s1 += __shfl_xor(s1, off, 64);
+                s0 += __shfl_xor(s0, off, 64);
+            }
+            if (l == 0) {
+                mvec[(size_t)h * 2 * D + c0 + w] = s1;
+                mvec[(size_t)h * 2 * D + D + c0 + w] = s0 / (float)m;
+            }
+            t = tw;
+        } else {
+            sM[w * 64 + l] = t;
+        }
         mv = fabsf(t);
     }
     mv = wave_max_dpp(mv);
@@ -909,8 +929,8 @@ __global__ __launch_bounds__(512) void mfinal_kernel(const float* __restrict__ U
     for (int i = 1; i < 8; ++i) mxg = fmaxf(mxg, smx[i]);
     const int e = pow2_exp(mxg);
     if (tid == 0) mscale[h * NG + g] = ldexpf(1.f, e);
-    if (ones) {
-        if (tid < 64) Mones[(size_t)h * 64 + tid] = sM[tid];   // rows >= m are zero
+    if (ones) {   // rows >= m are zero; the landmark-space form weights every landmark by 1/m
+        if (tid < 64) Mones[(size_t)h * 64 + tid] = mspace ? (tid < m ? 1.f / (float)m : 0.f) : sM[tid];
         return;
     }
     // operand tiles: one 16-byte chunk (i = 0..7) per (column, s, lane half)
@@ -940,13 +960,15 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
                                                      const float* __restrict__ frame, const _Float16* __restrict__ Mt,
                                                      const float* __restrict__ mscale,
                                                      const float* __restrict__ Mones, const float* __restrict__ vbar,
-                                                     const float* __restrict__ extra, int n, int m, int nqb, int BH) {
+                                                     const float* __restrict__ extra,
+                                                     const float* __restrict__ mvec, int n, int m, int nqb, int BH) {
     constexpr int D2 = D / 2;
     constexpr int D8 = D / 8;
     constexpr int CB = D / 32;
     __shared__ __attribute__((aligned(16))) _Float16 sM[4 * CB * 512];
     __shared__ __attribute__((aligned(16))) float sVb[D];
     __shared__ __attribute__((aligned(16))) float sMo[64];
+    __shared__ __attribute__((aligned(16))) float sMb[NORM == NORM_MSPACE ? D : 4];
     // per wave: the bf16 output rows of one 32-query half, staged so that they leave as whole
     // rows (pitch D + 8 halves)
     constexpr int OP = D + 8;
@@ -958,7 +980,14 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
         const uint4* src = reinterpret_cast<const uint4*>(Mt + (size_t)h * 4 * CB * 512);
         uint4* dst = reinterpret_cast<uint4*>(sM);
         for (int e = tid; e < 4 * CB * 64; e += 256) dst[e] = src[e];
-        if (tid < D) sVb[tid] = vbar[(size_t)h * D + tid];
+        if (tid < D) {
+            if (NORM == NORM_MSPACE) {
+                sVb[tid] = mvec[(size_t)h * 2 * D + tid];
+                sMb[tid] = mvec[(size_t)h * 2 * D + D + tid];
+            } else {
+                sVb[tid] = vbar[(size_t)h * D + tid];
+            }
+        }
         if (tid < 64) sMo[tid] = Mones[(size_t)h * 64 + tid];
     }
     const float R = frame[h * 4 + 0], inv2R = frame[h * 4 + 1], esc = frame[h * 4 + 2];
@@ -1034,9 +1063,10 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
             A[s4] = __builtin_bit_cast(h8_t, (uint4){ah[8 * s4 + 4 * qb], ah[8 * s4 + 4 * qb + 1],
                                                      ah[8 * s4 + 4 * qb + 2], ah[8 * s4 + 4 * qb + 3]});
         const float si = __uint_as_float(sw[qb]);
-        float tmul, tadd;   // o = y * tmul * scv[group] + tadd * vbar
+        float tmul, tadd;   // o = y * tmul * scv[group] + tadd * vbar (+ mb, landmark-space form)
         if (NORM == NORM_INLINE) { tmul = 1.f; tadd = 1.f - si; }
         else if (NORM == NORM_ROWSUM) { tmul = 1.f / si; tadd = 0.f; }
+        else if (NORM == NORM_MSPACE) { tmul = 1.f; tadd = -si; }
         else { tmul = 1.f; tadd = 0.f; }
         uint16_t* stage = sOut + w * 32 * OP + (l & 31) * OP;
 #pragma unroll
@@ -1058,6 +1088,13 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
                 float o1 = fmaf(y[4 * g + 1], tm, tadd * vb.y);
                 float o2 = fmaf(y[4 * g + 2], tm, tadd * vb.z);
                 float o3 = fmaf(y[4 * g + 3], tm, tadd * vb.w);
+                if (NORM == NORM_MSPACE) {
+                    const float4 mb = *reinterpret_cast<const float4*>(&sMb[c0]);
+                    o0 += mb.x;
+                    o1 += mb.y;
+                    o2 += mb.z;
+                    o3 += mb.w;
+                }
                 if (extra) {   // the convolution branch of Eq. (7); rows past n read row n - 1
                     const int iq = min(i0 + 32 * qb + (l & 31), n - 1);
                     const float4 ex = *reinterpret_cast<const float4*>(extra + ((size_t)h * n + iq) * D + c0);
@@ -1134,31 +1171,34 @@ hipError_t launch_fast_key(const void* K, const void* V, const uint32_t* qfix, c
 }
 
 hipError_t launch_fast_mfinal(const float* Upart, const float* XT, _Float16* Mt, float* mscale, float* Mones,
-                              float* M, int BH, int d, int m, int nkb, hipStream_t st) {
+                              float* M, int BH, int d, int m, int nkb, const float* whiten, int mspace, int H,
+                              float* mvec, hipStream_t st) {
     if (d == 32)
         hipLaunchKernelGGL(mfinal_kernel<32>, dim3(32 / 8 + 1, BH), dim3(512), 0, st, Upart, XT, Mt, mscale, Mones, M, m,
-                           nkb);
+                           nkb, whiten, mspace, H, mvec);
     else
         hipLaunchKernelGGL(mfinal_kernel<64>, dim3(64 / 8 + 1, BH), dim3(512), 0, st, Upart, XT, Mt, mscale, Mones, M, m,
-                           nkb);
+                           nkb, whiten, mspace, H, mvec);
     return hipGetLastError();
 }
 
 hipError_t launch_fast_query(int norm, const void* Q, void* Out, const uint32_t* kfix, const float* frame,
                              const _Float16* Mt, const float* mscale, const float* Mones, const float* vbar,
-                             const float* extra, int BH, int n, int d, int m, hipStream_t st) {
+                             const float* extra, const float* mvec, int BH, int n, int d, int m, hipStream_t st) {
     const int nqb = (n + 255) / 256;
     dim3 grid(nqb * BH);
 #define LAPATTN_Q2(Dv, Nv)                                                                                        \
     hipLaunchKernelGGL((query2_kernel<Dv, Nv>), grid, dim3(256), 0, st, (const uint16_t*)Q, (uint16_t*)Out, kfix, \
-                       frame, Mt, mscale, Mones, vbar, extra, n, m, nqb, BH)
+                       frame, Mt, mscale, Mones, vbar, extra, mvec, n, m, nqb, BH)
     if (d == 32) {
         if (norm == NORM_INLINE) LAPATTN_Q2(32, NORM_INLINE);
         else if (norm == NORM_ROWSUM) LAPATTN_Q2(32, NORM_ROWSUM);
+        else if (norm == NORM_MSPACE) LAPATTN_Q2(32, NORM_MSPACE);
         else LAPATTN_Q2(32, NORM_NONE);
     } else {
         if (norm == NORM_INLINE) LAPATTN_Q2(64, NORM_INLINE);
         else if (norm == NORM_ROWSUM) LAPATTN_Q2(64, NORM_ROWSUM);
+        else if (norm == NORM_MSPACE) LAPATTN_Q2(64, NORM_MSPACE);
         else LAPATTN_Q2(64, NORM_NONE);
     }
 #undef LAPATTN_Q2

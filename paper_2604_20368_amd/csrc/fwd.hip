@@ -4,7 +4,9 @@
 //   key_summary_kernel  U = K_LK [V | 1], split over key chunks (Sec. 3.2, Eq. (3) key summaries;
 //                       K_LK of Algorithm 1 in the orientation K_QL X K_LK)
 //   ns_solve_kernel     K_LL, Algorithm 2 in fp64 on the matrix cores, then M = X_T U
-//   query_out_kernel    Y = K_QL M and the normalisation (Eq. (8), Eq. (4))
+//   query_out_kernel    Y = K_QL M and the normalisation (Eq. (8), Eq. (4), or the landmark-space
+//                       form of Appendix B)
+//   mspace_vec_kernel   the two per-head vectors of the landmark-space normalisation
 #include "common.hpp"
 #include "kernels.hpp"
 #include "ns_mfma.hpp"
@@ -370,7 +372,10 @@ template <int D, int NORM>
 __global__ __launch_bounds__(256) void query_out_kernel(const float* __restrict__ Q, float* __restrict__ Out,
                                                         const float* __restrict__ kt, const float* __restrict__ M,
                                                         const float* __restrict__ vbar,
-                                                        const float* __restrict__ extra, int n, int m, float kscale) {
+                                                        const float* __restrict__ extra,
+                                                        const float* __restrict__ whiten,
+                                                        const float* __restrict__ mvec, int H, int n, int m,
+                                                        float kscale) {
     constexpr int D1 = D + 1;
     constexpr int NCH = D / 32;
     constexpr int CB = D / 32;             // 32-column blocks of the output
@@ -379,15 +384,31 @@ __global__ __launch_bounds__(256) void query_out_kernel(const float* __restrict_
     __shared__ __attribute__((aligned(16))) float sMT[32 * CB * 64];
     __shared__ float sMo[64];
     __shared__ float sVb[D];
+    __shared__ float sMb[NORM == NORM_MSPACE ? D : 1];
     __shared__ float sT[4 * 64 * TP];
     const int h = blockIdx.y, tid = threadIdx.x, w = tid >> 6, l = tid & 63;
+    // landmark-space normalisation: the rows of M scaled by the whitening w, the ones column
+    // replaced by 1/m (so that s_i becomes the landmark mean of a_i), and the vectors
+    // sum_l w_l M_l and (1/m) sum_l M_l from mvec
+    const float* wl = (NORM == NORM_MSPACE && whiten) ? whiten + (size_t)(h % H) * m : nullptr;
     for (int e = tid; e < 32 * CB * 64; e += 256) {
         const int s = e / (CB * 64), cb = (e / 64) % CB, ln = e % 64;
         const int lm = 2 * s + ln / 32;
-        sMT[e] = (lm < m) ? M[((size_t)h * m + lm) * D1 + 32 * cb + ln % 32] : 0.f;
+        const float wv = wl && lm < m ? wl[lm] : 1.f;
+        sMT[e] = (lm < m) ? wv * M[((size_t)h * m + lm) * D1 + 32 * cb + ln % 32] : 0.f;
     }
-    if (tid < 64) sMo[tid] = (tid < m) ? M[((size_t)h * m + tid) * D1 + D] : 0.f;
-    if (tid < D) sVb[tid] = vbar[(size_t)h * D + tid];
+    if (tid < 64) {
+        if (NORM == NORM_MSPACE) sMo[tid] = (tid < m) ? 1.f / (float)m : 0.f;
+        else sMo[tid] = (tid < m) ? M[((size_t)h * m + tid) * D1 + D] : 0.f;
+    }
+    if (NORM == NORM_MSPACE) {
+        if (tid < D) {
+            sVb[tid] = mvec[(size_t)h * 2 * D + tid];
+            sMb[tid] = mvec[(size_t)h * 2 * D + D + tid];
+        }
+    } else if (tid < D) {
+        sVb[tid] = vbar[(size_t)h * D + tid];
+    }
     float* tile = sT + w * 64 * TP;
     const int i0 = blockIdx.x * 256 + w * 64;
     const int i = i0 + l;
@@ -468,6 +489,7 @@ __global__ __launch_bounds__(256) void query_out_kernel(const float* __restrict_
                         const float y = acc[qb][cb][4 * g + t];
                         if (NORM == NORM_INLINE) o[t] = fmaf(1.f - si, sVb[c0 + t], y);
                         else if (NORM == NORM_ROWSUM) o[t] = y / si;
+                        else if (NORM == NORM_MSPACE) o[t] = fmaf(-si, sVb[c0 + t], y) + sMb[c0 + t];
                         else o[t] = y;
                     }
                     if (extra) {   // the convolution branch of Eq. (7)
@@ -529,28 +551,51 @@ hipError_t launch_ns_solve(const float* qt, const float* kt, const float* Upart,
 
 template <int D>
 static void query_out_launch(int norm, const void* Q, void* Out, const float* kt, const float* M, const float* vbar,
-                             const float* extra, int BH, int n, int m, float kscale, hipStream_t st) {
+                             const float* extra, const float* whiten, const float* mvec, int BH, int H, int n, int m,
+                             float kscale, hipStream_t st) {
     dim3 grid((n + 255) / 256, BH);
     const float* q = (const float*)Q;
     float* o = (float*)Out;
-    if (norm == NORM_INLINE)
-        hipLaunchKernelGGL((query_out_kernel<D, NORM_INLINE>), grid, dim3(256), 0, st, q, o, kt, M, vbar, extra, n, m,
-                           kscale);
-    else if (norm == NORM_ROWSUM)
-        hipLaunchKernelGGL((query_out_kernel<D, NORM_ROWSUM>), grid, dim3(256), 0, st, q, o, kt, M, vbar, extra, n, m,
-                           kscale);
-    else
-        hipLaunchKernelGGL((query_out_kernel<D, NORM_NONE>), grid, dim3(256), 0, st, q, o, kt, M, vbar, extra, n, m,
-                           kscale);
+#define LAPATTN_QO(Nv)                                                                                             \
+    hipLaunchKernelGGL((query_out_kernel<D, Nv>), grid, dim3(256), 0, st, q, o, kt, M, vbar, extra, whiten, mvec, H, \
+                       n, m, kscale)
+    if (norm == NORM_INLINE) LAPATTN_QO(NORM_INLINE);
+    else if (norm == NORM_ROWSUM) LAPATTN_QO(NORM_ROWSUM);
+    else if (norm == NORM_MSPACE) LAPATTN_QO(NORM_MSPACE);
+    else LAPATTN_QO(NORM_NONE);
+#undef LAPATTN_QO
 }
 
 hipError_t launch_query_out(int dt, int norm, const void* Q, void* Out, const float* kt, const float* M,
-                            const float* vbar, const float* extra, int BH, int n, int d, int m, float lambda,
-                            hipStream_t st) {
+                            const float* vbar, const float* extra, const float* whiten, const float* mvec, int BH,
+                            int H, int n, int d, int m, float lambda, hipStream_t st) {
     if (dt != DT_F32) return hipErrorInvalidValue;   // bf16 inputs take the fast path
     const float ks = kscale_of(lambda);
-    if (d == 32) query_out_launch<32>(norm, Q, Out, kt, M, vbar, extra, BH, n, m, ks, st);
-    else query_out_launch<64>(norm, Q, Out, kt, M, vbar, extra, BH, n, m, ks, st);
+    if (d == 32) query_out_launch<32>(norm, Q, Out, kt, M, vbar, extra, whiten, mvec, BH, H, n, m, ks, st);
+    else query_out_launch<64>(norm, Q, Out, kt, M, vbar, extra, whiten, mvec, BH, H, n, m, ks, st);
+    return hipGetLastError();
+}
+
+// Landmark-space normalisation vectors: mvec[h] = {sum_l w_l M_l[:d], (1/m) sum_l M_l[:d]}
+// (w = ones when whiten is NULL), summed in landmark order.  grid (BH), D threads.
+__global__ void mspace_vec_kernel(const float* __restrict__ M, const float* __restrict__ whiten,
+                                  float* __restrict__ mvec, int H, int m, int D) {
+    const int h = blockIdx.x, c = threadIdx.x;
+    if (c >= D) return;
+    const float* wl = whiten ? whiten + (size_t)(h % H) * m : nullptr;
+    float sw = 0.f, sb = 0.f;
+    for (int l = 0; l < m; ++l) {
+        const float v = M[((size_t)h * m + l) * (D + 1) + c];
+        sw = fmaf(wl ? wl[l] : 1.f, v, sw);
+        sb += v;
+    }
+    mvec[(size_t)h * 2 * D + c] = sw;
+    mvec[(size_t)h * 2 * D + D + c] = sb / (float)m;
+}
+
+hipError_t launch_mspace_vec(const float* M, const float* whiten, float* mvec, int BH, int H, int d, int m,
+                             hipStream_t st) {
+    hipLaunchKernelGGL(mspace_vec_kernel, dim3(BH), dim3(64), 0, st, M, whiten, mvec, H, m, d);
     return hipGetLastError();
 }
 

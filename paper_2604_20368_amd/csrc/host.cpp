@@ -28,7 +28,8 @@ int check_shape(int B, int H, int n, int d, int m, float lambda, int T, int dtyp
     if (!(std::isfinite(lambda) && lambda > 0.f)) return LAPATTN_ERR_PARAM;
     if (T < 0 || T > kMaxT) return LAPATTN_ERR_PARAM;
     if (dtype != LAPATTN_FP32 && dtype != LAPATTN_BF16) return LAPATTN_ERR_PARAM;
-    if (norm != LAPATTN_NORM_INLINE && norm != LAPATTN_NORM_ROWSUM && norm != LAPATTN_NORM_NONE)
+    if (norm != LAPATTN_NORM_INLINE && norm != LAPATTN_NORM_ROWSUM && norm != LAPATTN_NORM_NONE &&
+        norm != LAPATTN_NORM_MSPACE)
         return LAPATTN_ERR_PARAM;
     if (!(std::isfinite(eps) && eps >= 0.f)) return LAPATTN_ERR_PARAM;
     if (d != 32 && d != 64) return LAPATTN_ERR_UNSUPPORTED;
@@ -50,7 +51,8 @@ int check_align(std::initializer_list<const void*> tensors, const void* workspac
 
 struct FastPlan {
     size_t qt, kt, vseg, segmax, vsegmax, frame, qfix, kfix, vbar, XT, cinfo, Upart, Mt, mscale, Mones, M;
-    size_t E;   // convolution branch: DWC(V) + bias, fp32 [BH][n][d]
+    size_t E;      // convolution branch: DWC(V) + bias, fp32 [BH][n][d]
+    size_t mvec;   // landmark-space normalisation: [BH][2][d]
     size_t total;
     int kpb, nkb;
 };
@@ -61,6 +63,8 @@ struct Plan {
         dqtW, dktW, dDk, dqt_part;
     size_t wQ, wK, wV, wG, gQ, gK, gV;   // bf16 backward: fp32 copies of the inputs, fp32 gradients
     size_t E;                            // convolution branch, forward: DWC(V) + bias [BH][n][d]
+    size_t mvec;                         // landmark-space normalisation: [BH][2][d]
+    size_t p0_part;                      // landmark-space normalisation: per-block sums of dOut
     size_t dwc_part;                     // convolution branch, backward: filter-gradient partials
     size_t total;
     int MP, nkc, nqb, nlc;
@@ -94,12 +98,14 @@ Plan make_plan(int BH, int n, int d, int m, int T, bool bwd, bool bf16 = false, 
     p.U = c.take(bh * m * d1 * f);
     p.M = c.take(bh * m * d1 * f);
     p.vbar = c.take(bh * d * f);
+    p.mvec = c.take(bh * 2 * d * f);
     if (bwd) {
         p.Aq = c.take(bh * n * 64 * f);    // rows of pitch 64 (16-byte aligned for the LDS copies)
         p.dDq = c.take(bh * n * 64 * f);
         p.rs = c.take(bh * n * f);
         p.dYd = c.take(bh * n * f);
         p.dvbar_part = c.take(bh * p.nqb * d * f);
+        p.p0_part = c.take(bh * p.nqb * d * f);
         p.dM_part = c.take(bh * p.nlc * m * d1 * f);
         p.dkt_part = c.take(bh * p.nlc * m * d * f);
         p.dU = c.take(bh * m * d1 * f);
@@ -153,6 +159,7 @@ FastPlan make_fast_plan(int BH, int n, int d, int m, bool dwc = false) {
     p.mscale = c.take(bh * ((size_t)d / 8 + 1) * f);
     p.Mones = c.take(bh * 64 * f);
     p.M = c.take(bh * m * d1 * f);
+    p.mvec = c.take(bh * 2 * d * f);
     if (dwc) p.E = c.take(bh * n * d * f);
     p.total = (c.off + 255) & ~size_t(255);
     return p;
@@ -221,6 +228,7 @@ hipError_t run_named(Recorder& rec, const char* name, F&& f) {
 
 int norm_of(const lapattn_opts* o) { return o ? o->norm : LAPATTN_NORM_INLINE; }
 float eps_of(const lapattn_opts* o) { return o ? o->eps : 0.f; }
+const float* whiten_of(const lapattn_opts* o) { return o ? o->whiten : nullptr; }
 lapattn::LmPool pool_of(const lapattn_opts* o) { return o ? lapattn::LmPool{o->grid_w, o->pool_r} : lapattn::LmPool{0, 0}; }
 
 // Token map and landmark geometry: no map (gw = 0) or a row-major map of width gw dividing n;
@@ -276,7 +284,8 @@ hipError_t forward_internals(Recorder& rec, const Plan& p, const void* Q, const 
 
 hipError_t forward_fast(Recorder& rec, const FastPlan& p, const void* Q, const void* K, const void* V, void* Out,
                         void* ws, int BH, int H, int n, int d, int m, float lambda, int T, int norm, float eps,
-                        lapattn::LmPool pl, const Dwc& dwc, hipStream_t st) {
+                        lapattn::LmPool pl, const Dwc& dwc, const float* whiten, hipStream_t st) {
+    const bool mspace = norm == LAPATTN_NORM_MSPACE;
     hipError_t e;
     float* E = dwc.k ? at<float>(ws, p.E) : nullptr;
     if (E) {
@@ -306,13 +315,13 @@ hipError_t forward_fast(Recorder& rec, const FastPlan& p, const void* Q, const v
     e = run_named(rec, "m_final", [&] {
         return lapattn::launch_fast_mfinal(at<float>(ws, p.Upart), at<float>(ws, p.XT), at<_Float16>(ws, p.Mt),
                                            at<float>(ws, p.mscale), at<float>(ws, p.Mones), at<float>(ws, p.M), BH, d, m,
-                                           p.nkb, st);
+                                           p.nkb, whiten, mspace ? 1 : 0, H, at<float>(ws, p.mvec), st);
     });
     if (e != hipSuccess) return e;
     e = run_named(rec, "query", [&] {
         return lapattn::launch_fast_query(norm, Q, Out, at<uint32_t>(ws, p.kfix), at<float>(ws, p.frame),
                                           at<_Float16>(ws, p.Mt), at<float>(ws, p.mscale), at<float>(ws, p.Mones),
-                                          at<float>(ws, p.vbar), E, BH, n, d, m, st);
+                                          at<float>(ws, p.vbar), E, at<float>(ws, p.mvec), BH, n, d, m, st);
     });
     return e;
 }
@@ -351,7 +360,7 @@ int lapattn_forward(const void* Q, const void* K, const void* V, void* Out, int 
             if (!workspace || workspace_bytes < fp.total) return LAPATTN_ERR_WORKSPACE;
             Recorder rec(st);
             hipError_t e = forward_fast(rec, fp, Q, K, V, Out, workspace, BH, H, n, d, m, lambda, ns_iters, norm, eps,
-                                        pl, dwc, st);
+                                        pl, dwc, whiten_of(opts), st);
             return e == hipSuccess ? LAPATTN_OK : LAPATTN_ERR_HIP;
         }
         const Plan p = make_plan(BH, n, d, m, ns_iters, false, false, dwc.k != 0);
@@ -367,10 +376,17 @@ int lapattn_forward(const void* Q, const void* K, const void* V, void* Out, int 
             });
             if (e != hipSuccess) return LAPATTN_ERR_HIP;
         }
+        if (norm == LAPATTN_NORM_MSPACE) {
+            e = run_named(rec, "mspace_vec", [&] {
+                return lapattn::launch_mspace_vec(at<float>(workspace, p.M), whiten_of(opts),
+                                                  at<float>(workspace, p.mvec), BH, H, d, m, st);
+            });
+            if (e != hipSuccess) return LAPATTN_ERR_HIP;
+        }
         e = run_named(rec, "query_out", [&] {
             return lapattn::launch_query_out(dtype, norm, Q, Out, at<float>(workspace, p.kt),
-                                             at<float>(workspace, p.M), at<float>(workspace, p.vbar), E, BH, n, d, m,
-                                             lambda, st);
+                                             at<float>(workspace, p.M), at<float>(workspace, p.vbar), E,
+                                             whiten_of(opts), at<float>(workspace, p.mvec), BH, H, n, d, m, lambda, st);
         });
         return e == hipSuccess ? LAPATTN_OK : LAPATTN_ERR_HIP;
     } catch (...) {
@@ -422,11 +438,20 @@ int lapattn_backward(const void* Q, const void* K, const void* V, const void* dO
         }
         e = forward_internals(rec, p, q, k, v, ws, BH, n, d, m, lambda, ns_iters, LAPATTN_FP32, eps, true, pl, st);
         if (e != hipSuccess) return LAPATTN_ERR_HIP;
+        const bool mspace = norm == LAPATTN_NORM_MSPACE;
+        const float* whiten = whiten_of(opts);
+        if (mspace) {
+            e = run_named(rec, "mspace_vec", [&] {
+                return lapattn::launch_mspace_vec(at<float>(ws, p.M), whiten, at<float>(ws, p.mvec), BH, H, d, m, st);
+            });
+            if (e != hipSuccess) return LAPATTN_ERR_HIP;
+        }
         e = run_named(rec, "bwd_query", [&] {
             return lapattn::launch_bwd_query(norm, q, g, dq, at<float>(ws, p.kt), at<float>(ws, p.M),
                                              at<float>(ws, p.vbar), at<float>(ws, p.Aq), at<float>(ws, p.dDq),
                                              at<float>(ws, p.rs), at<float>(ws, p.dYd), at<float>(ws, p.dvbar_part),
-                                             BH, n, d, m, lambda, p.nqb, st);
+                                             at<float>(ws, p.p0_part), whiten, at<float>(ws, p.mvec), BH, H, n, d, m,
+                                             lambda, p.nqb, st);
         });
         if (e != hipSuccess) return LAPATTN_ERR_HIP;
         e = run_named(rec, "bwd_query_lm", [&] {
@@ -439,8 +464,9 @@ int lapattn_backward(const void* Q, const void* K, const void* V, const void* dO
             return lapattn::launch_bwd_ns(at<float>(ws, p.qt), at<float>(ws, p.kt), at<double>(ws, p.Xs),
                                           at<double>(ws, p.cinfo), at<float>(ws, p.U), at<float>(ws, p.dM_part),
                                           at<float>(ws, p.dvbar_part), at<float>(ws, p.dU), at<float>(ws, p.dvbar),
-                                          at<float>(ws, p.dqtW), at<float>(ws, p.dktW), BH, n, d, m, ns_iters,
-                                          (double)lambda, (double)eps, p.nlc, p.nqb, p.MP, st);
+                                          at<float>(ws, p.dqtW), at<float>(ws, p.dktW), at<float>(ws, p.p0_part),
+                                          whiten, mspace ? 1 : 0, BH, H, n, d, m, ns_iters, (double)lambda,
+                                          (double)eps, p.nlc, p.nqb, p.MP, st);
         });
         if (e != hipSuccess) return LAPATTN_ERR_HIP;
         e = run_named(rec, "bwd_key", [&] {
@@ -488,7 +514,8 @@ const char* lapattn_status_str(int status) {
         case LAPATTN_OK: return "ok";
         case LAPATTN_ERR_NULL: return "null pointer argument";
         case LAPATTN_ERR_SHAPE: return "invalid shape (B, H, n >= 1, 1 <= m <= n, B*H*n*d < 2^31)";
-        case LAPATTN_ERR_PARAM: return "invalid parameter (lambda, ns_iters, eps, norm, dtype, map or convolution options)";
+        case LAPATTN_ERR_PARAM:
+            return "invalid parameter (lambda, ns_iters, eps, norm, dtype, map or convolution options)";
         case LAPATTN_ERR_UNSUPPORTED: return "unsupported configuration (d in {32, 64}, m <= 64)";
         case LAPATTN_ERR_WORKSPACE: return "workspace missing or too small";
         case LAPATTN_ERR_HIP: return "HIP launch failed";

@@ -35,19 +35,26 @@ hipError_t launch_ns_solve(const float* qt, const float* kt, const float* Upart,
                            int store_all, int MP, hipStream_t st);
 
 // Query side: Out_i = normalise(sum_l k(q_i, kt_l) M_l) (+ extra_i when extra, [BH][n][d], is given).
+// The landmark-space normalisation takes the whitening [H][m] (NULL: ones) and mvec below.
 hipError_t launch_query_out(int dt, int norm, const void* Q, void* Out, const float* kt, const float* M,
-                            const float* vbar, const float* extra, int BH, int n, int d, int m, float lambda,
-                            hipStream_t st);
+                            const float* vbar, const float* extra, const float* whiten, const float* mvec, int BH,
+                            int H, int n, int d, int m, float lambda, hipStream_t st);
+
+// Landmark-space normalisation: mvec[BH][2][d] = {sum_l w_l M_l[:d], (1/m) sum_l M_l[:d]}.
+hipError_t launch_mspace_vec(const float* M, const float* whiten, float* mvec, int BH, int H, int d, int m,
+                             hipStream_t st);
 
 // Backward (fp32 inputs) --------------------------------------------------------
 
 // Query-major pass: writes the direct dQ term, the kernel values Aq and dDq = -A dA / lambda
 // ([BH][n][m]), per-query dY scale rs and last column dYd ([BH][n]), and per-block
-// partial sums of dvbar ([BH][nqb][d]).
+// partial sums of dvbar ([BH][nqb][d]; for the landmark-space normalisation also the sums of
+// dO into p0_part, with the whitening and mvec of the forward).
 hipError_t launch_bwd_query(int norm, const float* Q, const float* dO, float* dQ,
                             const float* kt, const float* M, const float* vbar,
                             float* Aq, float* dDq, float* rs, float* dYd, float* dvbar_part,
-                            int BH, int n, int d, int m, float lambda, int nqb, hipStream_t st);
+                            float* p0_part, const float* whiten, const float* mvec,
+                            int BH, int H, int n, int d, int m, float lambda, int nqb, hipStream_t st);
 
 // Landmark-major pass over queries: partial dM [BH][nlc][m][d+1] and dkt [BH][nlc][m][d].
 hipError_t launch_bwd_query_lm(const float* Q, const float* dO, const float* kt,
@@ -60,7 +67,8 @@ hipError_t launch_bwd_query_lm(const float* Q, const float* dO, const float* kt,
 hipError_t launch_bwd_ns(const float* qt, const float* kt, const double* Xs, const double* cinfo,
                          const float* U, const float* dM_part, const float* dvbar_part,
                          float* dU, float* dvbar, float* dqtW, float* dktW,
-                         int BH, int n, int d, int m, int T, double lambda, double eps,
+                         const float* p0_part, const float* whiten, int mspace,
+                         int BH, int H, int n, int d, int m, int T, double lambda, double eps,
                          int nlc, int nqb, int MP, hipStream_t st);
 
 // Key-major pass: direct dK, final dV, and dDk = -B dB / lambda ([BH][n][m]).
@@ -95,11 +103,14 @@ hipError_t launch_fast_frame_ns(const float* qt, const float* kt, const double* 
                                 hipStream_t st);
 hipError_t launch_fast_key(const void* K, const void* V, const uint32_t* qfix, const float* frame, float* Upart,
                            int BH, int n, int d, int m, int kpb, int nkb, hipStream_t st);
+// mspace: the landmark-space normalisation (operand rows scaled by the whitening [H][m], NULL:
+// ones; the ones column 1/m; mvec[BH][2][d] written as for launch_mspace_vec).
 hipError_t launch_fast_mfinal(const float* Upart, const float* XT, _Float16* Mt, float* mscale, float* Mones,
-                              float* M, int BH, int d, int m, int nkb, hipStream_t st);
+                              float* M, int BH, int d, int m, int nkb, const float* whiten, int mspace, int H,
+                              float* mvec, hipStream_t st);
 hipError_t launch_fast_query(int norm, const void* Q, void* Out, const uint32_t* kfix, const float* frame,
                              const _Float16* Mt, const float* mscale, const float* Mones, const float* vbar,
-                             const float* extra, int BH, int n, int d, int m, hipStream_t st);
+                             const float* extra, const float* mvec, int BH, int n, int d, int m, hipStream_t st);
 
 // Depth-wise convolution branch of Eq. (7) (dwc.hip) ------------------------------------------
 // Filters W [H][d][k][k], bias [H][d] (may be NULL), over the row-major token map of width gw;

@@ -68,7 +68,7 @@ def test_argument_validation(call):
     assert call(ns_iters=-1) == L.LAPATTN_ERR_PARAM
     assert call(ns_iters=65) == L.LAPATTN_ERR_PARAM
     assert call(dtype=2) == L.LAPATTN_ERR_PARAM
-    assert call(norm=3) == L.LAPATTN_ERR_PARAM
+    assert call(norm=4) == L.LAPATTN_ERR_PARAM
     assert call(eps=-0.1) == L.LAPATTN_ERR_PARAM
     assert call(eps=float("nan")) == L.LAPATTN_ERR_PARAM
     assert call(d=48) == L.LAPATTN_ERR_UNSUPPORTED

@@ -57,19 +57,25 @@ def dev_dwc(dwc):
     return tuple(None if a is None else torch.from_numpy(a).to("cuda") for a in dwc)
 
 
-def run_forward(L, x, w, norm=0, eps=0.0, grid=None, dwc=None):
+def dev_f32(a):
+    return None if a is None else torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to("cuda")
+
+
+def run_forward(L, x, w, norm=0, eps=0.0, grid=None, dwc=None, whiten=None):
     Q, K, V = (to_dev(x[k], w.dtype) for k in ("Q", "K", "V"))
-    out = L.forward(Q, K, V, w.m, w.lam, w.T, norm=norm, eps=eps, grid=grid, dwc=dev_dwc(dwc))
+    out = L.forward(Q, K, V, w.m, w.lam, w.T, norm=norm, eps=eps, grid=grid, dwc=dev_dwc(dwc), whiten=dev_f32(whiten))
     torch.cuda.synchronize()
     return to_np(out)
 
 
-def check_forward(L, w, norm=0, eps=0.0, tol=None, grid=None, dwc=None):
-    say("forward %s B=%d H=%d n=%d d=%d m=%d T=%d %s norm=%d eps=%g grid=%s dwc k=%s" %
-        (w.name, w.B, w.H, w.n, w.d, w.m, w.T, w.dtype, norm, eps, grid, None if dwc is None else dwc[0].shape[-1]))
+def check_forward(L, w, norm=0, eps=0.0, tol=None, grid=None, dwc=None, whiten=None):
+    say("forward %s B=%d H=%d n=%d d=%d m=%d T=%d %s norm=%d eps=%g grid=%s dwc k=%s whiten=%s" %
+        (w.name, w.B, w.H, w.n, w.d, w.m, w.T, w.dtype, norm, eps, grid, None if dwc is None else dwc[0].shape[-1],
+         whiten is not None))
     x = W.make_inputs(w, with_grad=False)
-    got = run_forward(L, x, w, norm, eps, grid, dwc)
-    ref = oracle.forward(x["Q"], x["K"], x["V"], w.m, w.lam, w.T, norm, eps, grid=grid, dwc_branch=dwc)
+    got = run_forward(L, x, w, norm, eps, grid, dwc, whiten)
+    ref = oracle.forward(x["Q"], x["K"], x["V"], w.m, w.lam, w.T, norm, eps, grid=grid, dwc_branch=dwc,
+                         whiten=None if whiten is None else np.asarray(whiten, dtype=np.float32).astype(np.float64))
     err = head_rel(got, ref)
     say("  max head rel err %.3e" % err)
     assert np.isfinite(got).all()
@@ -175,12 +181,14 @@ def test_forward_full_size_sampled_heads(L, name):
 
 # ------------------------------------------------------------------------------ backward
 
-def check_backward(L, w, norm=0, eps=0.0, heads=None, grid=None, dwc=None):
-    say("backward %s B=%d H=%d n=%d d=%d m=%d T=%d %s norm=%d eps=%g grid=%s dwc k=%s" %
-        (w.name, w.B, w.H, w.n, w.d, w.m, w.T, w.dtype, norm, eps, grid, None if dwc is None else dwc[0].shape[-1]))
+def check_backward(L, w, norm=0, eps=0.0, heads=None, grid=None, dwc=None, whiten=None):
+    say("backward %s B=%d H=%d n=%d d=%d m=%d T=%d %s norm=%d eps=%g grid=%s dwc k=%s whiten=%s" %
+        (w.name, w.B, w.H, w.n, w.d, w.m, w.T, w.dtype, norm, eps, grid, None if dwc is None else dwc[0].shape[-1],
+         whiten is not None))
     x = W.make_inputs(w, with_grad=True)
     Q, K, V, dO = (to_dev(x[k], w.dtype) for k in ("Q", "K", "V", "dO"))
-    res = L.backward(Q, K, V, dO, w.m, w.lam, w.T, norm=norm, eps=eps, grid=grid, dwc=dev_dwc(dwc))
+    res = L.backward(Q, K, V, dO, w.m, w.lam, w.T, norm=norm, eps=eps, grid=grid, dwc=dev_dwc(dwc),
+                     whiten=dev_f32(whiten))
     torch.cuda.synchronize()
     got = [to_np(t) for t in res[:3]]
     BH = w.BH
@@ -189,8 +197,12 @@ def check_backward(L, w, norm=0, eps=0.0, heads=None, grid=None, dwc=None):
     else:
         sub = {k: np.ascontiguousarray(v.reshape(BH, w.n, w.d)[heads][None]) for k, v in x.items()}
         gsub = [g.reshape(BH, w.n, w.d)[heads][None] for g in got]
+    wsub = None
+    if whiten is not None:
+        wf = np.asarray(whiten, dtype=np.float32).astype(np.float64)
+        wsub = wf if heads is None else wf[[hh % w.H for hh in heads]]
     ref = oracle.backward(sub["Q"], sub["K"], sub["V"], sub["dO"], w.m, w.lam, w.T, norm, eps, grid=grid,
-                          dwc_branch=dwc)
+                          dwc_branch=dwc, whiten=wsub)
     errs = [head_rel(g, r) for g, r in zip(gsub, ref[:3])]
     say("  dQ %.3e dK %.3e dV %.3e" % tuple(errs))
     for g in got:
@@ -308,3 +320,52 @@ def test_backward_convolution_branch(L, dtype):
     check_backward(L, w.with_(d=64, sigma=0.125, lam=8.0), norm=1, grid=(20, 0),
                    dwc=W.make_dwc(2, 64, 5, seed=6, bias=False))
     check_backward(L, w.with_(n=6 * 8, m=6, B=1), norm=2, grid=(8, 0), dwc=W.make_dwc(2, 32, 7, seed=8))
+
+
+# ------------------------------------------------------------------------------ landmark-space normalisation
+
+MSPACE = 3
+
+
+def rand_whiten(H, m, seed):
+    return np.random.default_rng(seed).uniform(0.5, 1.5, size=(H, m)).astype(np.float32)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_forward_mspace(L, dtype):
+    """Appendix B's landmark-space embedding with a per-head diagonal whitening: every landmark
+    tile of the n = 16384 shape with a ragged tail, an odd m, and the all-ones default."""
+    w = W.small(W.WORKLOADS["highres"], n=3000, B=1, H=2).with_(dtype=dtype)
+    check_forward(L, w, norm=MSPACE, whiten=rand_whiten(2, 64, 1))
+    check_forward(L, w.with_(n=333, m=37), norm=MSPACE, whiten=rand_whiten(2, 37, 2))
+    w2 = W.small(W.WORKLOADS["train"], n=700, B=2, H=2).with_(dtype=dtype, m=20)
+    check_forward(L, w2, norm=MSPACE)
+    check_forward(L, w2, norm=MSPACE, whiten=np.zeros((2, 20), np.float32))
+
+
+def test_forward_mspace_full_size_sampled_heads(L):
+    w = W.WORKLOADS["highres"]
+    wh = rand_whiten(w.H, w.m, 3)
+    say("forward full %s mspace" % w.name)
+    x = W.make_inputs(w, with_grad=False)
+    got = run_forward(L, x, w, norm=MSPACE, whiten=wh)
+    heads = [0, 5, w.BH - 1]
+    sub = {k: np.ascontiguousarray(v.reshape(w.BH, w.n, w.d)[heads][None]) for k, v in x.items()}
+    ref = oracle.forward(sub["Q"], sub["K"], sub["V"], w.m, w.lam, w.T, MSPACE,
+                         whiten=wh.astype(np.float64)[[hh % w.H for hh in heads]])
+    err = head_rel(got.reshape(w.BH, w.n, w.d)[heads][None], ref)
+    say("  heads %s max rel err %.3e" % (heads, err))
+    assert err <= TOL[w.dtype]
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_backward_mspace(L, dtype):
+    w = W.small(W.WORKLOADS["train"], n=700, B=1, H=2).with_(dtype=dtype)
+    check_backward(L, w, norm=MSPACE, whiten=rand_whiten(2, 64, 4))
+    check_backward(L, w.with_(d=64, sigma=0.125, lam=8.0, n=333, m=37, B=2), norm=MSPACE, whiten=rand_whiten(2, 37, 5))
+    check_backward(L, w.with_(m=9, n=64), norm=MSPACE)
+
+
+def test_backward_mspace_full_size_sampled_heads(L):
+    w = W.WORKLOADS["train"]
+    check_backward(L, w, norm=MSPACE, heads=[0, 37, w.BH - 1], whiten=rand_whiten(w.H, w.m, 6))

@@ -83,7 +83,9 @@ def time_train_step(steps):
     """The training workload's forward and backward (fp32 path; B=32, H=4, n=3136, d=32, m=64,
     T=6), reported beside the headline: wall-clock ms per call, per-kernel ms from the library's
     HIP events, and the fraction of the VALU peak for the pairwise work (2nm pairs per head of
-    (2d+1) operations for the forward, about 2.5 times that for the backward)."""
+    (2d+1) operations for the forward, about 2.5 times that for the backward).  step_saved is a
+    whole training step (forward then backward) in which the backward reuses the forward's
+    internals through the save option instead of recomputing them."""
     import torch
     from paper_2604_20368_amd import lapattn
     w = W.WORKLOADS["train"]
@@ -93,12 +95,19 @@ def time_train_step(steps):
     out = torch.empty_like(Q)
     wsf = lapattn.workspace(Q, w.m, w.T)
     wsb = lapattn.workspace(Q, w.m, w.T, for_backward=True)
+    wss = lapattn.workspace(Q, w.m, w.T, for_backward=True)
     grads = tuple(torch.empty_like(Q) for _ in range(3))
     res = {"workload": w.name, "B": w.B, "H": w.H, "n": w.n, "d": w.d, "m": w.m, "T": w.T, "inputs": w.dtype}
     pair_ops = w.B * w.H * 2 * w.n * w.m * (2 * w.d + 1)
+
+    def step_saved():   # the backward reuses the forward's internals (save option)
+        lapattn.forward(Q, K, V, w.m, w.lam, w.T, out=out, ws=wss, save=True)
+        lapattn.backward(Q, K, V, dO, w.m, w.lam, w.T, grads=grads, ws=wss, save=True)
+
     for name, fn, ops in (("forward", lambda: lapattn.forward(Q, K, V, w.m, w.lam, w.T, out=out, ws=wsf), pair_ops),
                           ("backward", lambda: lapattn.backward(Q, K, V, dO, w.m, w.lam, w.T, grads=grads, ws=wsb),
-                           2.5 * pair_ops)):
+                           2.5 * pair_ops),
+                          ("step_saved", step_saved, 3.5 * pair_ops)):
         for _ in range(3):
             fn()
         torch.cuda.synchronize()

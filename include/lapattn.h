@@ -107,7 +107,12 @@ enum {
  * not NULL, writes the filter gradient dwc_dw [H][d][k][k] and the bias gradient dwc_db [H][d]
  * (fp32, summed over the batch, overwritten); lapattn_forward ignores those two.
  * whiten: with LAPATTN_NORM_MSPACE, the diagonal whitening w as a device array [H][m] of fp32
- * shared by the batch (NULL: all ones); ignored by the other normalisations. */
+ * shared by the batch (NULL: all ones); ignored by the other normalisations.
+ * save (fp32 inputs; ignored for bf16): lapattn_forward keeps the landmark means, the key-side
+ * summary and every Newton-Schulz iterate in the workspace, which must then be sized with
+ * LAPATTN_WS_BACKWARD; a following lapattn_backward with save set and the same inputs, sizes,
+ * options and workspace (the caller orders the two calls) reuses them instead of recomputing
+ * them.  Results are bitwise those of the calls without save. */
 typedef struct {
     int norm;            /* lapattn_norm */
     float eps;
@@ -119,6 +124,7 @@ typedef struct {
     float* dwc_dw;       /* backward: device [H][d][k][k] filter gradient, or NULL */
     float* dwc_db;       /* backward: device [H][d] bias gradient, or NULL */
     const float* whiten; /* LAPATTN_NORM_MSPACE: device [H][m] diagonal whitening, or NULL */
+    int save;            /* 1: forward leaves its internals for the backward (see above) */
 } lapattn_opts;
 
 /* Workspace flags. */

@@ -126,9 +126,8 @@ Plan make_plan(int BH, int n, int d, int m, int T, bool bwd, bool bf16 = false, 
         }
         if (dwc)
             p.dwc_part = c.take(bh * ((n + kDwcChunk - 1) / kDwcChunk) * d * (kDwcMaxK * kDwcMaxK + 1) * f);
-    } else if (dwc) {
-        p.E = c.take(bh * n * d * f);
     }
+    if (dwc) p.E = c.take(bh * n * d * f);
     p.total = (c.off + 255) & ~size_t(255);
     return p;
 }
@@ -229,6 +228,7 @@ hipError_t run_named(Recorder& rec, const char* name, F&& f) {
 int norm_of(const lapattn_opts* o) { return o ? o->norm : LAPATTN_NORM_INLINE; }
 float eps_of(const lapattn_opts* o) { return o ? o->eps : 0.f; }
 const float* whiten_of(const lapattn_opts* o) { return o ? o->whiten : nullptr; }
+bool save_of(const lapattn_opts* o) { return o && o->save; }
 lapattn::LmPool pool_of(const lapattn_opts* o) { return o ? lapattn::LmPool{o->grid_w, o->pool_r} : lapattn::LmPool{0, 0}; }
 
 // Token map and landmark geometry: no map (gw = 0) or a row-major map of width gw dividing n;
@@ -363,11 +363,14 @@ int lapattn_forward(const void* Q, const void* K, const void* V, void* Out, int 
                                         pl, dwc, whiten_of(opts), st);
             return e == hipSuccess ? LAPATTN_OK : LAPATTN_ERR_HIP;
         }
-        const Plan p = make_plan(BH, n, d, m, ns_iters, false, false, dwc.k != 0);
+        // save: the backward's layout, with every Newton-Schulz iterate kept, so that a following
+        // lapattn_backward (save set, same arguments and workspace) can skip the recomputation
+        const bool save = save_of(opts);
+        const Plan p = make_plan(BH, n, d, m, ns_iters, save, false, dwc.k != 0);
         if (!workspace || workspace_bytes < p.total) return LAPATTN_ERR_WORKSPACE;
         Recorder rec(st);
         hipError_t e = forward_internals(rec, p, Q, K, V, workspace, BH, n, d, m, lambda, ns_iters, dtype, eps,
-                                         false, pl, st);
+                                         save, pl, st);
         if (e != hipSuccess) return LAPATTN_ERR_HIP;
         float* E = dwc.k ? at<float>(workspace, p.E) : nullptr;
         if (E) {
@@ -436,8 +439,13 @@ int lapattn_backward(const void* Q, const void* K, const void* V, const void* dO
             });
             if (e != hipSuccess) return LAPATTN_ERR_HIP;
         }
-        e = forward_internals(rec, p, q, k, v, ws, BH, n, d, m, lambda, ns_iters, LAPATTN_FP32, eps, true, pl, st);
-        if (e != hipSuccess) return LAPATTN_ERR_HIP;
+        // fp32 inputs with save: the forward left pool, key-side summary and solve (with every
+        // iterate) in this workspace; otherwise they are recomputed here
+        if (bf16 || !save_of(opts)) {
+            e = forward_internals(rec, p, q, k, v, ws, BH, n, d, m, lambda, ns_iters, LAPATTN_FP32, eps, true, pl,
+                                  st);
+            if (e != hipSuccess) return LAPATTN_ERR_HIP;
+        }
         const bool mspace = norm == LAPATTN_NORM_MSPACE;
         const float* whiten = whiten_of(opts);
         if (mspace) {

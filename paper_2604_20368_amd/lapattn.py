@@ -22,7 +22,8 @@ EXPORTS = ("lapattn_workspace_size", "lapattn_forward", "lapattn_backward", "lap
 class lapattn_opts(ctypes.Structure):
     _fields_ = [("norm", ctypes.c_int), ("eps", ctypes.c_float), ("grid_w", ctypes.c_int), ("pool_r", ctypes.c_int),
                 ("dwc_k", ctypes.c_int), ("dwc_w", ctypes.c_void_p), ("dwc_b", ctypes.c_void_p),
-                ("dwc_dw", ctypes.c_void_p), ("dwc_db", ctypes.c_void_p), ("whiten", ctypes.c_void_p)]
+                ("dwc_dw", ctypes.c_void_p), ("dwc_db", ctypes.c_void_p), ("whiten", ctypes.c_void_p),
+                ("save", ctypes.c_int)]
 
 
 class LapattnError(RuntimeError):
@@ -73,26 +74,28 @@ def lapattn_workspace_size(B, H, n, d, m, ns_iters, dtype, flags):
     return int(library().lapattn_workspace_size(B, H, n, d, m, ns_iters, dtype, int(flags)))
 
 
-def _opts(norm, eps, grid=None, dwc=None, whiten=None):
+def _opts(norm, eps, grid=None, dwc=None, whiten=None, save=False):
     gw, r = grid if grid is not None else (0, 0)
     k, w, b, dw, db = dwc if dwc is not None else (0, None, None, None, None)
-    return ctypes.byref(lapattn_opts(int(norm), float(eps), int(gw), int(r), int(k), w, b, dw, db, whiten))
+    return ctypes.byref(lapattn_opts(int(norm), float(eps), int(gw), int(r), int(k), w, b, dw, db, whiten,
+                                     int(bool(save))))
 
 
 def lapattn_forward(Q, K, V, Out, B, H, n, d, m, lam, ns_iters, dtype, norm=LAPATTN_NORM_INLINE, eps=0.0,
-                    workspace=0, workspace_bytes=0, stream=0, grid=None, dwc=None, whiten=None):
+                    workspace=0, workspace_bytes=0, stream=0, grid=None, dwc=None, whiten=None, save=False):
     """Raw call with integer device addresses; returns the status code.  grid = (W', r): the
     W'-wide token map, with r x r window landmarks when r > 0 (None: no map, balanced
     segments).  dwc = (k, filters, bias, dfilters, dbias) addresses of the convolution branch;
     whiten the address of the landmark-space whitening."""
     return library().lapattn_forward(Q, K, V, Out, B, H, n, d, m, float(lam), ns_iters, dtype,
-                                     _opts(norm, eps, grid, dwc, whiten), workspace, workspace_bytes, stream)
+                                     _opts(norm, eps, grid, dwc, whiten, save), workspace, workspace_bytes, stream)
 
 
 def lapattn_backward(Q, K, V, dO, dQ, dK, dV, B, H, n, d, m, lam, ns_iters, dtype, norm=LAPATTN_NORM_INLINE,
-                     eps=0.0, workspace=0, workspace_bytes=0, stream=0, grid=None, dwc=None, whiten=None):
+                     eps=0.0, workspace=0, workspace_bytes=0, stream=0, grid=None, dwc=None, whiten=None,
+                     save=False):
     return library().lapattn_backward(Q, K, V, dO, dQ, dK, dV, B, H, n, d, m, float(lam), ns_iters, dtype,
-                                      _opts(norm, eps, grid, dwc, whiten), workspace, workspace_bytes, stream)
+                                      _opts(norm, eps, grid, dwc, whiten, save), workspace, workspace_bytes, stream)
 
 
 def lapattn_timing_enable(on):
@@ -177,26 +180,27 @@ def _whiten_arg(Q, m, whiten):
 
 
 def forward(Q, K, V, m, lam, ns_iters, norm=LAPATTN_NORM_INLINE, eps=0.0, out=None, ws=None, grid=None, dwc=None,
-            whiten=None):
+            whiten=None, save=False):
     """Out = lapattn(Q, K, V) on torch's current stream; grid = (W', r) the token map (r > 0: window
     landmarks), dwc = (filters, bias) adds the convolution branch over that map, whiten [H][m]
-    is the diagonal of LAPATTN_NORM_MSPACE."""
+    is the diagonal of LAPATTN_NORM_MSPACE; save keeps the internals in ws (a backward-sized
+    workspace) for backward(..., save=True, ws=ws)."""
     import torch
     _check(Q, K, V)
     out = torch.empty_like(Q) if out is None else out
     _check(Q, out)
-    ws = workspace(Q, m, ns_iters, False, dwc is not None) if ws is None else ws
+    ws = workspace(Q, m, ns_iters, save, dwc is not None) if ws is None else ws
     B, H, n, d = Q.shape
     rc = lapattn_forward(Q.data_ptr(), K.data_ptr(), V.data_ptr(), out.data_ptr(), B, H, n, d, m, lam, ns_iters,
                          _dtype_code(Q), norm, eps, ws.data_ptr(), ws.numel(), _stream(Q), grid, _dwc_args(Q, dwc),
-                         _whiten_arg(Q, m, whiten))
+                         _whiten_arg(Q, m, whiten), save)
     if rc != LAPATTN_OK:
         raise LapattnError(rc, "lapattn_forward")
     return out
 
 
 def backward(Q, K, V, dO, m, lam, ns_iters, norm=LAPATTN_NORM_INLINE, eps=0.0, grads=None, ws=None, grid=None,
-             dwc=None, dwc_grads=None, whiten=None):
+             dwc=None, dwc_grads=None, whiten=None, save=False):
     """(dQ, dK, dV) of sum(Out * dO) on torch's current stream; with dwc = (filters, bias) also the
     filter and bias gradients: (dQ, dK, dV, dfilters, dbias)."""
     import torch
@@ -210,7 +214,8 @@ def backward(Q, K, V, dO, m, lam, ns_iters, norm=LAPATTN_NORM_INLINE, eps=0.0, g
     B, H, n, d = Q.shape
     rc = lapattn_backward(Q.data_ptr(), K.data_ptr(), V.data_ptr(), dO.data_ptr(), dQ.data_ptr(), dK.data_ptr(),
                           dV.data_ptr(), B, H, n, d, m, lam, ns_iters, _dtype_code(Q), norm, eps, ws.data_ptr(),
-                          ws.numel(), _stream(Q), grid, _dwc_args(Q, dwc, dwc_grads), _whiten_arg(Q, m, whiten))
+                          ws.numel(), _stream(Q), grid, _dwc_args(Q, dwc, dwc_grads), _whiten_arg(Q, m, whiten),
+                          save)
     if rc != LAPATTN_OK:
         raise LapattnError(rc, "lapattn_backward")
     return (dQ, dK, dV) if dwc is None else (dQ, dK, dV) + tuple(dwc_grads)

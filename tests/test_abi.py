@@ -148,3 +148,14 @@ def test_convolution_workspace():
         b1 = L.lapattn_workspace_size(2, 3, 3136, 64, 64, 8, dt, L.LAPATTN_WS_BACKWARD | L.LAPATTN_WS_DWC)
         assert b1 > b0
         assert L.lapattn_workspace_size(2, 3, 3136, 64, 64, 8, dt, 4) == 0
+
+
+def test_saved_forward_needs_the_backward_workspace():
+    """With save, the forward keeps the backward's internals: a forward-sized workspace is
+    rejected (fp32); bf16 ignores save."""
+    fsz = L.lapattn_workspace_size(1, 2, 100, 32, 8, 4, 0, 0)
+    bsz = L.lapattn_workspace_size(1, 2, 100, 32, 8, 4, 0, L.LAPATTN_WS_BACKWARD)
+    assert bsz > fsz
+    assert fwd(save=True, workspace_bytes=fsz) == L.LAPATTN_ERR_WORKSPACE
+    assert fwd(save=True, workspace_bytes=bsz - 256) == L.LAPATTN_ERR_WORKSPACE
+    assert fwd(save=False, workspace_bytes=fsz - 256) == L.LAPATTN_ERR_WORKSPACE

@@ -369,3 +369,26 @@ def test_backward_mspace(L, dtype):
 def test_backward_mspace_full_size_sampled_heads(L):
     w = W.WORKLOADS["train"]
     check_backward(L, w, norm=MSPACE, heads=[0, 37, w.BH - 1], whiten=rand_whiten(w.H, w.m, 6))
+
+
+# ------------------------------------------------------------------------------ saved forward state
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_backward_reuses_saved_forward_state(L, dtype):
+    """forward(save) then backward(save) on one workspace equals, bit for bit, the calls that
+    recompute (the backward skips pool, key-side summary and solve for fp32 inputs; bf16 ignores
+    save), for the inline and landmark-space forms and with the convolution branch."""
+    w = W.small(W.WORKLOADS["train"], n=56 * 14, B=2, H=2).with_(dtype=dtype)
+    x = W.make_inputs(w, with_grad=True)
+    Q, K, V, dO = (to_dev(x[k], w.dtype) for k in ("Q", "K", "V", "dO"))
+    for kw in (dict(), dict(norm=MSPACE, whiten=dev_f32(rand_whiten(2, w.m, 9))),
+               dict(grid=(56, 0), dwc=dev_dwc(W.make_dwc(2, w.d, 3, seed=10)))):
+        say("saved state %s %s" % (dtype, sorted(kw)))
+        ws = L.workspace(Q, w.m, w.T, True, "dwc" in kw)
+        out_s = L.forward(Q, K, V, w.m, w.lam, w.T, ws=ws, save=True, **kw)
+        g_s = L.backward(Q, K, V, dO, w.m, w.lam, w.T, ws=ws, save=True, **kw)
+        out_r = L.forward(Q, K, V, w.m, w.lam, w.T, **kw)
+        g_r = L.backward(Q, K, V, dO, w.m, w.lam, w.T, **kw)
+        torch.cuda.synchronize()
+        assert torch.equal(out_s, out_r)
+        assert all(torch.equal(a, b) for a, b in zip(g_s, g_r))

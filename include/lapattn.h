@@ -109,7 +109,8 @@ enum {
  * whiten: with LAPATTN_NORM_MSPACE, the diagonal whitening w as a device array [H][m] of fp32
  * shared by the batch (NULL: all ones); ignored by the other normalisations.
  * save (fp32 inputs; ignored for bf16): lapattn_forward keeps the landmark means, the key-side
- * summary and every Newton-Schulz iterate in the workspace, which must then be sized with
+ * summary, every Newton-Schulz iterate and the n x m kernel values of both sides (K_QL and
+ * K_LK^T, 64 floats per token) in the workspace, which must then be sized with
  * LAPATTN_WS_BACKWARD; a following lapattn_backward with save set and the same inputs, sizes,
  * options and workspace (the caller orders the two calls) reuses them instead of recomputing
  * them.  Results are bitwise those of the calls without save. */

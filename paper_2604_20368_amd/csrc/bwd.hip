@@ -42,8 +42,8 @@ __global__ __launch_bounds__(256) void bwd_query_kernel(const float* __restrict_
                                                         float* __restrict__ rs, float* __restrict__ dYd,
                                                         float* __restrict__ dvbar_part, float* __restrict__ p0_part,
                                                         const float* __restrict__ whiten,
-                                                        const float* __restrict__ mvec, int H, int n, int m,
-                                                        float kscale, float inv_lambda, int nqb) {
+                                                        const float* __restrict__ mvec, int saved, int H, int n,
+                                                        int m, float kscale, float inv_lambda, int nqb) {
     constexpr bool CENTRED = NORM == NORM_INLINE || NORM == NORM_MSPACE;
     constexpr int D1 = D + 1;
     constexpr int NCH = D / 32;
@@ -89,7 +89,9 @@ __global__ __launch_bounds__(256) void bwd_query_kernel(const float* __restrict_
     auto emit = [&](int a, float dist) {
         tile[l * TP + a] = (live && a < m) ? __builtin_amdgcn_exp2f(dist * kscale) : 0.f;
     };
-    {
+    if (saved) {   // the forward left the rows of A in Aq: copy them into the tile
+        load_rows64(tile, Aq + (size_t)h * n * 64, i0, n, m);
+    } else {
         float ta[32], tb[32];
         srow32(ta, tab);
         float dist = 0.f;
@@ -138,8 +140,7 @@ __global__ __launch_bounds__(256) void bwd_query_kernel(const float* __restrict_
         rs[(size_t)h * n + i] = rsc;
         dYd[(size_t)h * n + i] = dyd;
     }
-    for (int r = 0; r < 64 && i0 + r < n; ++r)
-        if (l < m) Aq[((size_t)h * n + i0 + r) * 64 + l] = tile[r * TP + l];
+    if (!saved) store_rows64(Aq + (size_t)h * n * 64, tile, i0, n, m);
     __builtin_amdgcn_wave_barrier();
 
     // dA_il and dD_il into the tile (LDS only), then whole rows of dDq
@@ -158,8 +159,7 @@ __global__ __launch_bounds__(256) void bwd_query_kernel(const float* __restrict_
         tile[l * TP + a] = -tile[l * TP + a] * da * inv_lambda;
     }
     __builtin_amdgcn_wave_barrier();
-    for (int r = 0; r < 64 && i0 + r < n; ++r)
-        if (l < m) dDq[((size_t)h * n + i0 + r) * 64 + l] = tile[r * TP + l];
+    store_rows64(dDq + (size_t)h * n * 64, tile, i0, n, m);
 
     // pass 2: dq_i += dD_il sign(q_i - kt_l); each unit's dD is read before the unit's first
     // wait (which covers it); landmarks past m have dD = 0 (a zero column when m is odd)
@@ -641,7 +641,7 @@ __global__ __launch_bounds__(256) void bwd_key_kernel(const float* __restrict__ 
                                                       float* __restrict__ dK, float* __restrict__ dV,
                                                       const float* __restrict__ qt, const float* __restrict__ dU,
                                                       const float* __restrict__ dvbar, float* __restrict__ dDk,
-                                                      int n, int m, float kscale, float inv_lambda) {
+                                                      int saved, int n, int m, float kscale, float inv_lambda) {
     constexpr int D1 = D + 1;
     constexpr int NCH = D / 32;
     constexpr int TP = 65;
@@ -674,7 +674,10 @@ __global__ __launch_bounds__(256) void bwd_key_kernel(const float* __restrict__ 
     auto emit = [&](int a, float dist) {
         tile[l * TP + a] = (live && a < m) ? __builtin_amdgcn_exp2f(dist * kscale) : 0.f;
     };
-    {
+    if (saved) {   // the forward's key-side summary left the rows of B in dDk: copy them (each
+                   // wave reads only its own rows, which it overwrites with dD further down)
+        load_rows64(tile, dDk + (size_t)h * n * 64, j0, n, m);
+    } else {
         float ta[32], tb[32];
         srow32(ta, tab);
         float dist = 0.f;
@@ -779,8 +782,7 @@ __global__ __launch_bounds__(256) void bwd_key_kernel(const float* __restrict__ 
         asm volatile("" ::"s"(ta[0]), "s"(ta[16]));
     }
     __builtin_amdgcn_wave_barrier();
-    for (int r = 0; r < 64 && j0 + r < n; ++r)
-        if (l < m) dDk[((size_t)h * n + j0 + r) * 64 + l] = tile[r * TP + l];
+    store_rows64(dDk + (size_t)h * n * 64, tile, j0, n, m);
     if (live) {
 #pragma unroll
         for (int c4 = 0; c4 < D / 4; ++c4)
@@ -959,13 +961,13 @@ hipError_t launch_narrow_bf16(const float* gQ, const float* gK, const float* gV,
 
 hipError_t launch_bwd_query(int norm, const float* Q, const float* dO, float* dQ, const float* kt, const float* M,
                             const float* vbar, float* Aq, float* dDq, float* rs, float* dYd, float* dvbar_part,
-                            float* p0_part, const float* whiten, const float* mvec, int BH, int H, int n, int d,
-                            int m, float lambda, int nqb, hipStream_t st) {
+                            float* p0_part, const float* whiten, const float* mvec, int saved, int BH, int H, int n,
+                            int d, int m, float lambda, int nqb, hipStream_t st) {
     const float ks = kscale_of(lambda), il = 1.f / lambda;
     dim3 grid(nqb, BH);
 #define LAPATTN_BQ(Dv, Nv)                                                                                  \
     hipLaunchKernelGGL((bwd_query_kernel<Dv, Nv>), grid, dim3(256), 0, st, Q, dO, dQ, kt, M, vbar, Aq, dDq, rs, \
-                       dYd, dvbar_part, p0_part, whiten, mvec, H, n, m, ks, il, nqb)
+                       dYd, dvbar_part, p0_part, whiten, mvec, saved, H, n, m, ks, il, nqb)
     if (d == 32) {
         if (norm == NORM_INLINE) LAPATTN_BQ(32, NORM_INLINE);
         else if (norm == NORM_ROWSUM) LAPATTN_BQ(32, NORM_ROWSUM);
@@ -1010,15 +1012,16 @@ hipError_t launch_bwd_ns(const float* qt, const float* kt, const double* Xs, con
 }
 
 hipError_t launch_bwd_key(const float* K, const float* V, float* dK, float* dV, const float* qt, const float* dU,
-                          const float* dvbar, float* dDk, int BH, int n, int d, int m, float lambda, hipStream_t st) {
+                          const float* dvbar, float* dDk, int saved, int BH, int n, int d, int m, float lambda,
+                          hipStream_t st) {
     const float ks = kscale_of(lambda), il = 1.f / lambda;
     dim3 grid((n + 255) / 256, BH);
     if (d == 32)
-        hipLaunchKernelGGL((bwd_key_kernel<32>), grid, dim3(256), 0, st, K, V, dK, dV, qt, dU, dvbar, dDk, n, m, ks,
-                           il);
+        hipLaunchKernelGGL((bwd_key_kernel<32>), grid, dim3(256), 0, st, K, V, dK, dV, qt, dU, dvbar, dDk, saved, n, m,
+                           ks, il);
     else
-        hipLaunchKernelGGL((bwd_key_kernel<64>), grid, dim3(256), 0, st, K, V, dK, dV, qt, dU, dvbar, dDk, n, m, ks,
-                           il);
+        hipLaunchKernelGGL((bwd_key_kernel<64>), grid, dim3(256), 0, st, K, V, dK, dV, qt, dU, dvbar, dDk, saved, n, m,
+                           ks, il);
     return hipGetLastError();
 }
 

@@ -72,7 +72,8 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 template <int D>
 __global__ __launch_bounds__(256) void key_summary_kernel(const float* __restrict__ K, const float* __restrict__ V,
                                                           const float* __restrict__ qt, float* __restrict__ Upart,
-                                                          int n, int m, float kscale, int chunk_keys, int nkc) {
+                                                          float* __restrict__ Bsave, int n, int m, float kscale,
+                                                          int chunk_keys, int nkc) {
     constexpr int D1 = D + 1;
     constexpr int NCH = D / 32;            // 32-coordinate units per landmark row
     constexpr int CT = D / 16 + 1;         // MFMA column tiles: the values, then the ones column
@@ -153,6 +154,13 @@ __global__ __launch_bounds__(256) void key_summary_kernel(const float* __restric
                                                                              0, 0, 0);
                 }
             }
+        }
+        if (Bsave && live) {   // the key's row of B for the backward ([BH][n][64], zeros past m)
+            float4* dst = reinterpret_cast<float4*>(Bsave + ((size_t)h * n + j) * 64);
+#pragma unroll 4
+            for (int a4 = 0; a4 < 16; ++a4)
+                dst[a4] = make_float4(sB[(4 * a4) * BP + l], sB[(4 * a4 + 1) * BP + l], sB[(4 * a4 + 2) * BP + l],
+                                      sB[(4 * a4 + 3) * BP + l]);
         }
         __builtin_amdgcn_wave_barrier();
     }
@@ -374,8 +382,8 @@ __global__ __launch_bounds__(256) void query_out_kernel(const float* __restrict_
                                                         const float* __restrict__ vbar,
                                                         const float* __restrict__ extra,
                                                         const float* __restrict__ whiten,
-                                                        const float* __restrict__ mvec, int H, int n, int m,
-                                                        float kscale) {
+                                                        const float* __restrict__ mvec, float* __restrict__ Asave,
+                                                        int H, int n, int m, float kscale) {
     constexpr int D1 = D + 1;
     constexpr int NCH = D / 32;
     constexpr int CB = D / 32;             // 32-column blocks of the output
@@ -447,6 +455,7 @@ __global__ __launch_bounds__(256) void query_out_kernel(const float* __restrict_
     }
     if (m & 1) tile[l * TP + m] = 0.f;   // the pair loops read column m (unwritten when d = 64)
     __builtin_amdgcn_wave_barrier();
+    if (Asave) store_rows64(Asave + (size_t)h * n * 64, tile, i0, n, m);   // A's rows for the backward
     f32x16_t acc[2][CB];
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb)
@@ -522,16 +531,16 @@ hipError_t launch_pool(int dt, const void* Q, const void* K, const void* V, floa
     return hipGetLastError();
 }
 
-hipError_t launch_key_summary(int dt, const void* K, const void* V, const float* qt, float* Upart, int BH, int n,
-                              int d, int m, float lambda, int chunk_keys, int nkc, hipStream_t st) {
+hipError_t launch_key_summary(int dt, const void* K, const void* V, const float* qt, float* Upart, float* Bsave,
+                              int BH, int n, int d, int m, float lambda, int chunk_keys, int nkc, hipStream_t st) {
     if (dt != DT_F32) return hipErrorInvalidValue;   // bf16 inputs take the fast path
     const float ks = kscale_of(lambda);
     if (d == 32)
         hipLaunchKernelGGL((key_summary_kernel<32>), dim3(nkc, BH), dim3(256), 0, st, (const float*)K,
-                           (const float*)V, qt, Upart, n, m, ks, chunk_keys, nkc);
+                           (const float*)V, qt, Upart, Bsave, n, m, ks, chunk_keys, nkc);
     else
         hipLaunchKernelGGL((key_summary_kernel<64>), dim3(nkc, BH), dim3(256), 0, st, (const float*)K,
-                           (const float*)V, qt, Upart, n, m, ks, chunk_keys, nkc);
+                           (const float*)V, qt, Upart, Bsave, n, m, ks, chunk_keys, nkc);
     return hipGetLastError();
 }
 
@@ -551,14 +560,14 @@ hipError_t launch_ns_solve(const float* qt, const float* kt, const float* Upart,
 
 template <int D>
 static void query_out_launch(int norm, const void* Q, void* Out, const float* kt, const float* M, const float* vbar,
-                             const float* extra, const float* whiten, const float* mvec, int BH, int H, int n, int m,
-                             float kscale, hipStream_t st) {
+                             const float* extra, const float* whiten, const float* mvec, float* Asave, int BH, int H,
+                             int n, int m, float kscale, hipStream_t st) {
     dim3 grid((n + 255) / 256, BH);
     const float* q = (const float*)Q;
     float* o = (float*)Out;
 #define LAPATTN_QO(Nv)                                                                                             \
-    hipLaunchKernelGGL((query_out_kernel<D, Nv>), grid, dim3(256), 0, st, q, o, kt, M, vbar, extra, whiten, mvec, H, \
-                       n, m, kscale)
+    hipLaunchKernelGGL((query_out_kernel<D, Nv>), grid, dim3(256), 0, st, q, o, kt, M, vbar, extra, whiten, mvec,     \
+                       Asave, H, n, m, kscale)
     if (norm == NORM_INLINE) LAPATTN_QO(NORM_INLINE);
     else if (norm == NORM_ROWSUM) LAPATTN_QO(NORM_ROWSUM);
     else if (norm == NORM_MSPACE) LAPATTN_QO(NORM_MSPACE);
@@ -567,12 +576,12 @@ static void query_out_launch(int norm, const void* Q, void* Out, const float* kt
 }
 
 hipError_t launch_query_out(int dt, int norm, const void* Q, void* Out, const float* kt, const float* M,
-                            const float* vbar, const float* extra, const float* whiten, const float* mvec, int BH,
-                            int H, int n, int d, int m, float lambda, hipStream_t st) {
+                            const float* vbar, const float* extra, const float* whiten, const float* mvec,
+                            float* Asave, int BH, int H, int n, int d, int m, float lambda, hipStream_t st) {
     if (dt != DT_F32) return hipErrorInvalidValue;   // bf16 inputs take the fast path
     const float ks = kscale_of(lambda);
-    if (d == 32) query_out_launch<32>(norm, Q, Out, kt, M, vbar, extra, whiten, mvec, BH, H, n, m, ks, st);
-    else query_out_launch<64>(norm, Q, Out, kt, M, vbar, extra, whiten, mvec, BH, H, n, m, ks, st);
+    if (d == 32) query_out_launch<32>(norm, Q, Out, kt, M, vbar, extra, whiten, mvec, Asave, BH, H, n, m, ks, st);
+    else query_out_launch<64>(norm, Q, Out, kt, M, vbar, extra, whiten, mvec, Asave, BH, H, n, m, ks, st);
     return hipGetLastError();
 }
 

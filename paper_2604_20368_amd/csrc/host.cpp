@@ -262,7 +262,7 @@ int check_dwc(const Dwc& c, lapattn::LmPool pl) {
 // The forward stages shared by lapattn_forward and lapattn_backward (which recomputes them).
 hipError_t forward_internals(Recorder& rec, const Plan& p, const void* Q, const void* K, const void* V, void* ws,
                              int BH, int n, int d, int m, float lambda, int T, int dtype, float eps, bool store_all,
-                             lapattn::LmPool pl, hipStream_t st) {
+                             lapattn::LmPool pl, hipStream_t st, float* Bsave = nullptr) {
     float* qt = at<float>(ws, p.qt);
     float* kt = at<float>(ws, p.kt);
     double* vseg = at<double>(ws, p.vseg);
@@ -271,7 +271,7 @@ hipError_t forward_internals(Recorder& rec, const Plan& p, const void* Q, const 
     e = run_named(rec, "pool", [&] { return lapattn::launch_pool(dtype, Q, K, V, qt, kt, vseg, BH, n, d, m, pl, st); });
     if (e != hipSuccess) return e;
     e = run_named(rec, "key_summary", [&] {
-        return lapattn::launch_key_summary(dtype, K, V, qt, Upart, BH, n, d, m, lambda, kKeyChunk, p.nkc, st);
+        return lapattn::launch_key_summary(dtype, K, V, qt, Upart, Bsave, BH, n, d, m, lambda, kKeyChunk, p.nkc, st);
     });
     if (e != hipSuccess) return e;
     e = run_named(rec, "ns_solve", [&] {
@@ -369,8 +369,10 @@ int lapattn_forward(const void* Q, const void* K, const void* V, void* Out, int 
         const Plan p = make_plan(BH, n, d, m, ns_iters, save, false, dwc.k != 0);
         if (!workspace || workspace_bytes < p.total) return LAPATTN_ERR_WORKSPACE;
         Recorder rec(st);
+        // with save the key side also leaves B's rows (in the backward's dDk slice) and the query
+        // side A's rows (Aq), so that the backward skips its two distance passes as well
         hipError_t e = forward_internals(rec, p, Q, K, V, workspace, BH, n, d, m, lambda, ns_iters, dtype, eps,
-                                         save, pl, st);
+                                         save, pl, st, save ? at<float>(workspace, p.dDk) : nullptr);
         if (e != hipSuccess) return LAPATTN_ERR_HIP;
         float* E = dwc.k ? at<float>(workspace, p.E) : nullptr;
         if (E) {
@@ -389,7 +391,8 @@ int lapattn_forward(const void* Q, const void* K, const void* V, void* Out, int 
         e = run_named(rec, "query_out", [&] {
             return lapattn::launch_query_out(dtype, norm, Q, Out, at<float>(workspace, p.kt),
                                              at<float>(workspace, p.M), at<float>(workspace, p.vbar), E,
-                                             whiten_of(opts), at<float>(workspace, p.mvec), BH, H, n, d, m, lambda, st);
+                                             whiten_of(opts), at<float>(workspace, p.mvec),
+                                             save ? at<float>(workspace, p.Aq) : nullptr, BH, H, n, d, m, lambda, st);
         });
         return e == hipSuccess ? LAPATTN_OK : LAPATTN_ERR_HIP;
     } catch (...) {
@@ -441,7 +444,8 @@ int lapattn_backward(const void* Q, const void* K, const void* V, const void* dO
         }
         // fp32 inputs with save: the forward left pool, key-side summary and solve (with every
         // iterate) in this workspace; otherwise they are recomputed here
-        if (bf16 || !save_of(opts)) {
+        const bool saved = !bf16 && save_of(opts);
+        if (!saved) {
             e = forward_internals(rec, p, q, k, v, ws, BH, n, d, m, lambda, ns_iters, LAPATTN_FP32, eps, true, pl,
                                   st);
             if (e != hipSuccess) return LAPATTN_ERR_HIP;
@@ -458,8 +462,8 @@ int lapattn_backward(const void* Q, const void* K, const void* V, const void* dO
             return lapattn::launch_bwd_query(norm, q, g, dq, at<float>(ws, p.kt), at<float>(ws, p.M),
                                              at<float>(ws, p.vbar), at<float>(ws, p.Aq), at<float>(ws, p.dDq),
                                              at<float>(ws, p.rs), at<float>(ws, p.dYd), at<float>(ws, p.dvbar_part),
-                                             at<float>(ws, p.p0_part), whiten, at<float>(ws, p.mvec), BH, H, n, d, m,
-                                             lambda, p.nqb, st);
+                                             at<float>(ws, p.p0_part), whiten, at<float>(ws, p.mvec), saved ? 1 : 0, BH,
+                                             H, n, d, m, lambda, p.nqb, st);
         });
         if (e != hipSuccess) return LAPATTN_ERR_HIP;
         e = run_named(rec, "bwd_query_lm", [&] {
@@ -479,7 +483,8 @@ int lapattn_backward(const void* Q, const void* K, const void* V, const void* dO
         if (e != hipSuccess) return LAPATTN_ERR_HIP;
         e = run_named(rec, "bwd_key", [&] {
             return lapattn::launch_bwd_key(k, v, dk, dv, at<float>(ws, p.qt), at<float>(ws, p.dU),
-                                           at<float>(ws, p.dvbar), at<float>(ws, p.dDk), BH, n, d, m, lambda, st);
+                                           at<float>(ws, p.dvbar), at<float>(ws, p.dDk), saved ? 1 : 0, BH, n, d, m,
+                                           lambda, st);
         });
         if (e != hipSuccess) return LAPATTN_ERR_HIP;
         e = run_named(rec, "bwd_key_lm", [&] {

@@ -20,8 +20,9 @@ hipError_t launch_pool(int dt, const void* Q, const void* K, const void* V,
                        float* qt, float* kt, double* vseg,
                        int BH, int n, int d, int m, LmPool pl, hipStream_t st);
 
-// Key-side summary: per key chunk, Upart[h][chunk][a][c] = sum_j k(qt_a, k_j) [v_j | 1]_c.
-hipError_t launch_key_summary(int dt, const void* K, const void* V, const float* qt, float* Upart,
+// Key-side summary: per key chunk, Upart[h][chunk][a][c] = sum_j k(qt_a, k_j) [v_j | 1]_c;
+// with Bsave, also the rows B[j][a] = k(qt_a, k_j) ([BH][n][64], zeros past m) for the backward.
+hipError_t launch_key_summary(int dt, const void* K, const void* V, const float* qt, float* Upart, float* Bsave,
                               int BH, int n, int d, int m, float lambda, int chunk_keys, int nkc,
                               hipStream_t st);
 
@@ -36,9 +37,10 @@ hipError_t launch_ns_solve(const float* qt, const float* kt, const float* Upart,
 
 // Query side: Out_i = normalise(sum_l k(q_i, kt_l) M_l) (+ extra_i when extra, [BH][n][d], is given).
 // The landmark-space normalisation takes the whitening [H][m] (NULL: ones) and mvec below.
+// With Asave, also the rows A[i][l] = k(q_i, kt_l) ([BH][n][64], columns below m) for the backward.
 hipError_t launch_query_out(int dt, int norm, const void* Q, void* Out, const float* kt, const float* M,
-                            const float* vbar, const float* extra, const float* whiten, const float* mvec, int BH,
-                            int H, int n, int d, int m, float lambda, hipStream_t st);
+                            const float* vbar, const float* extra, const float* whiten, const float* mvec,
+                            float* Asave, int BH, int H, int n, int d, int m, float lambda, hipStream_t st);
 
 // Landmark-space normalisation: mvec[BH][2][d] = {sum_l w_l M_l[:d], (1/m) sum_l M_l[:d]}.
 hipError_t launch_mspace_vec(const float* M, const float* whiten, float* mvec, int BH, int H, int d, int m,
@@ -46,14 +48,15 @@ hipError_t launch_mspace_vec(const float* M, const float* whiten, float* mvec, i
 
 // Backward (fp32 inputs) --------------------------------------------------------
 
-// Query-major pass: writes the direct dQ term, the kernel values Aq and dDq = -A dA / lambda
+// Query-major pass: writes the direct dQ term, the kernel values Aq (read instead when saved: the
+// forward's launch_query_out left them there) and dDq = -A dA / lambda
 // ([BH][n][m]), per-query dY scale rs and last column dYd ([BH][n]), and per-block
 // partial sums of dvbar ([BH][nqb][d]; for the landmark-space normalisation also the sums of
 // dO into p0_part, with the whitening and mvec of the forward).
 hipError_t launch_bwd_query(int norm, const float* Q, const float* dO, float* dQ,
                             const float* kt, const float* M, const float* vbar,
                             float* Aq, float* dDq, float* rs, float* dYd, float* dvbar_part,
-                            float* p0_part, const float* whiten, const float* mvec,
+                            float* p0_part, const float* whiten, const float* mvec, int saved,
                             int BH, int H, int n, int d, int m, float lambda, int nqb, hipStream_t st);
 
 // Landmark-major pass over queries: partial dM [BH][nlc][m][d+1] and dkt [BH][nlc][m][d].
@@ -71,9 +74,10 @@ hipError_t launch_bwd_ns(const float* qt, const float* kt, const double* Xs, con
                          int BH, int H, int n, int d, int m, int T, double lambda, double eps,
                          int nlc, int nqb, int MP, hipStream_t st);
 
-// Key-major pass: direct dK, final dV, and dDk = -B dB / lambda ([BH][n][m]).
+// Key-major pass: direct dK, final dV, and dDk = -B dB / lambda ([BH][n][m]).  saved: dDk holds
+// B's rows from the forward on entry (launch_key_summary's Bsave) instead of being recomputed.
 hipError_t launch_bwd_key(const float* K, const float* V, float* dK, float* dV,
-                          const float* qt, const float* dU, const float* dvbar, float* dDk,
+                          const float* qt, const float* dU, const float* dvbar, float* dDk, int saved,
                           int BH, int n, int d, int m, float lambda, hipStream_t st);
 
 // Landmark-major pass over keys: partial dqt [BH][nlc][m][d].

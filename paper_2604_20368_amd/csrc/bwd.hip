@@ -20,6 +20,8 @@ namespace lapattn {
 
 static inline float kscale_of(float lambda) { return (float)(-1.4426950408889634 / (double)lambda); }
 
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
 // ------------------------------------------------------------------------------------------
 // Query-major pass.  grid (nqb, BH), 256 threads, lane = query (wave w of block b covers
 // queries 256 b + 64 w ..).  Landmark rows of kt come through scalar registers (srows.hpp),
@@ -143,21 +145,44 @@ __global__ __launch_bounds__(256) void bwd_query_kernel(const float* __restrict_
     if (!saved) store_rows64(Aq + (size_t)h * n * 64, tile, i0, n, m);
     __builtin_amdgcn_wave_barrier();
 
-    // dA_il and dD_il into the tile (LDS only), then whole rows of dDq
-    float dq[D], gs[D];
+    // dA_il = sum_c M[l][c] dY_i[c] (dY_i = [rs_i dO_i | dYd_i]) on fp32 MFMA 32x32x2 as
+    // dA^T = M dY^T, per 32-landmark block lb and 32-query half qb, k = a coordinate pair (the
+    // ones column is coordinate D, coordinate D + 1 is zero).  A operand: lane l holds
+    // M[32 lb + l % 32][2 s + l / 32]; B operand: one permlane32 swap of the lane's own pair of
+    // coordinates gives both halves (queries 0..31 keep theirs and receive coordinate 2s+1 of
+    // 32..63, and vice versa).  Result register r at lane l: landmark 32 lb + 8 (r / 4) +
+    // 4 (l / 32) + r % 4, query 32 qb + l % 32; dD = -a dA / lambda replaces a in the tile.
+    {
+        constexpr int KS = D / 2 + 1;   // coordinate pairs, the last one (dYd, 0)
+        const int nlb = (m + 31) / 32;
+        const int hk = l >> 5, lr = l & 31;
+        // one 32 x 32 block at a time (16 accumulator registers); the swaps are redone per block
+        for (int blk = 0; blk < 2 * nlb; ++blk) {
+            const int lb = blk >> 1, qb = blk & 1;
+            f32x16_t acc;
 #pragma unroll
-    for (int c = 0; c < D; ++c) {
-        dq[c] = 0.f;
-        gs[c] = g[c] * rsc;
-    }
-#pragma unroll 2
-    for (int a = 0; a < m; ++a) {
-        const float* mr = sM + a * D1;
-        float da = dyd * mr[D];
+            for (int r = 0; r < 16; ++r) acc[r] = 0.f;
 #pragma unroll
-        for (int c = 0; c < D; ++c) da = fmaf(gs[c], mr[c], da);
-        tile[l * TP + a] = -tile[l * TP + a] * da * inv_lambda;
+            for (int s = 0; s < KS; ++s) {
+                const float x0 = (2 * s < D) ? g[2 * s] * rsc : dyd;
+                const float x1 = (2 * s + 1 < D) ? g[2 * s + 1] * rsc : 0.f;
+                const auto bsw =
+                    __builtin_amdgcn_permlane32_swap(__float_as_uint(x0), __float_as_uint(x1), false, false);
+                const int c = 2 * s + hk;
+                const float av = c <= D ? sM[(32 * lb + lr) * D1 + c] : 0.f;
+                acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av, __uint_as_float(qb ? bsw[1] : bsw[0]), acc, 0, 0, 0);
+            }
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int a = 32 * lb + 8 * (r >> 2) + 4 * hk + (r & 3);
+                float* t = tile + (32 * qb + lr) * TP + a;
+                *t = -*t * acc[r] * inv_lambda;
+            }
+        }
     }
+    float dq[D];
+#pragma unroll
+    for (int c = 0; c < D; ++c) dq[c] = 0.f;
     __builtin_amdgcn_wave_barrier();
     store_rows64(dDq + (size_t)h * n * 64, tile, i0, n, m);
 
@@ -262,7 +287,6 @@ __device__ __forceinline__ void stage_rows(float* dst, const float* base, int t0
 //   dkt_l -= dD_il sign(q_i - kt_l).
 // Queries past the chunk contribute zeros.
 typedef float f32x32_t __attribute__((ext_vector_type(32)));
-typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 template <int D>
 __global__ __launch_bounds__(64) void bwd_query_lm_kernel(const float* __restrict__ Q, const float* __restrict__ dO,

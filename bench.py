@@ -129,6 +129,43 @@ def time_train_step(steps):
     return res
 
 
+def time_other_forwards(steps, names=("pvt_stage1", "deit_small")):
+    """Forward throughput of the other forward-only workloads (reported beside the headline, which
+    they do not enter): tokens/s = B n per call, wall-clock ms per call and per-kernel ms."""
+    import torch
+    from paper_2604_20368_amd import lapattn
+    dev = torch.device("cuda:0")
+    res = {}
+    for name in names:
+        w = W.WORKLOADS[name]
+        x = W.make_inputs(w, with_grad=False)
+        dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+        Q, K, V = (torch.from_numpy(x[k]).to(dev).to(dt) for k in ("Q", "K", "V"))
+        out = torch.empty_like(Q)
+        ws = lapattn.workspace(Q, w.m, w.T)
+        fn = lambda: lapattn.forward(Q, K, V, w.m, w.lam, w.T, out=out, ws=ws)
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            fn()
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / steps
+        lapattn.lapattn_timing_enable(1)
+        for _ in range(steps):
+            fn()
+        torch.cuda.synchronize()
+        lapattn.lapattn_timing_enable(0)
+        per = {}
+        for k, t in lapattn.lapattn_timing_read(cap=64 * steps + 64):
+            per.setdefault(k, []).append(t)
+        res[name] = {"B": w.B, "H": w.H, "n": w.n, "d": w.d, "m": w.m, "T": w.T, "inputs": w.dtype,
+                     "tokens_per_s": round(w.B * w.n / (ms * 1e-3), 1), "ms": round(ms, 4),
+                     "kernels_ms": {k: round(sum(v) / len(v), 4) for k, v in per.items()}}
+    return res
+
+
 def time_dwc_branch(steps):
     """The depth-wise convolution branch of Eq. (7) (3 x 3 filters with bias over the 56 x 56 token
     map): the bf16 PVT stage-1 forward (7 x 7 window landmarks) with and without the branch, and
@@ -245,9 +282,9 @@ def ingest_traffic(kernel, fetch_dir, write_dir, copy_fetch_dir, copy_write_dir,
            "bytes_per_launch": f_k * 1024.0 * ff + w_k * 1024.0 * fw,
            "sources": KERNEL_SOURCES, "sources_sha256": h.hexdigest(),
            "commands": ["rocprofv3 --pmc FETCH_SIZE --output-format csv -d FETCH_DIR -o run -- "
-                        "python3 bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-train-step --no-dwc",
+                        "python3 bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-train-step --no-dwc --no-other",
                         "rocprofv3 --pmc WRITE_SIZE --output-format csv -d WRITE_DIR -o run -- "
-                        "python3 bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-train-step --no-dwc",
+                        "python3 bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-train-step --no-dwc --no-other",
                         "rocprofv3 --pmc FETCH_SIZE --output-format csv -d COPY_FETCH_DIR -o run -- "
                         "python3 bench.py --calibrate-copy",
                         "rocprofv3 --pmc WRITE_SIZE --output-format csv -d COPY_WRITE_DIR -o run -- "
@@ -258,6 +295,40 @@ def ingest_traffic(kernel, fetch_dir, write_dir, copy_fetch_dir, copy_write_dir,
     print(json.dumps(rec), flush=True)
 
 
+def summarize_trace(trace_dir):
+    """Per-kernel statistics (calls, average, min, max in us) of a rocprofv3 kernel trace of
+    `bench.py --steps 20 --warmup 5 --no-cpu-baseline --no-other --no-dwc`, split into the
+    headline forward (the bf16 kernels) and the training legs by launch order: 43 forwards
+    (4 kernels each), 43 backwards (9) and 43 saved steps (10) of 3 warmup + 20 timed + 20
+    event-timed calls."""
+    import csv
+    import re
+    import statistics as st
+    rows = list(csv.DictReader(open(os.path.join(trace_dir, "run_kernel_trace.csv"))))
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    seq = []
+    for r in rows:
+        mm = re.search(r"lapattn::(\w+)", r["Kernel_Name"]) or re.search(r"_ZN7lapattn\d+(\w+?)I", r["Kernel_Name"])
+        if mm:
+            seq.append((mm.group(1), (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3))
+    fast = {"pool2_kernel", "frame_ns_kernel", "key_kernel", "mfinal_kernel", "query2_kernel"}
+    head = [x for x in seq if x[0] in fast]
+    fp32 = [x for x in seq if x[0] not in fast]
+    nf, nb, ns = 43 * 4, 43 * 9, 43 * 10
+    if len(fp32) != nf + nb + ns:
+        raise SystemExit("unexpected launch count %d" % len(fp32))
+    out = {}
+    for leg, lst in (("headline", head), ("train_forward", fp32[:nf]), ("train_backward", fp32[nf:nf + nb]),
+                     ("train_step_saved", fp32[nf + nb:])):
+        d = {}
+        for k, t in lst:
+            d.setdefault(k, []).append(t)
+        out[leg] = {k: {"calls": len(v), "avg_us": round(st.mean(v), 1), "min_us": round(min(v), 1),
+                        "max_us": round(max(v), 1)} for k, v in d.items()}
+        out[leg]["sum_avg_us"] = round(sum(st.mean(v) for v in d.values()), 1)
+    print(json.dumps(out, indent=1))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -266,8 +337,12 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-train-step", action="store_true",
                     help="skip the training workload's forward and backward timing")
+    ap.add_argument("--no-other", action="store_true",
+                    help="skip the forward timing of the other forward-only workloads")
     ap.add_argument("--no-dwc", action="store_true",
                     help="skip the timing of the depth-wise convolution branch")
+    ap.add_argument("--summarize-trace", metavar="TRACE_DIR",
+                    help="per-leg kernel statistics of a rocprofv3 --kernel-trace CSV directory")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run only the plain copy used to scale the HBM byte counters")
     ap.add_argument("--ingest-traffic", nargs=5, metavar=("KERNEL", "FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR",
@@ -278,6 +353,9 @@ def main():
         k = args.ingest_traffic[0]
         ingest_traffic(k, *args.ingest_traffic[1:], out_path=os.path.join(
             ROOT, "profiles", "traffic_%s_%s.txt" % (k, WORKLOAD)))
+        return
+    if args.summarize_trace:
+        summarize_trace(args.summarize_trace)
         return
     if args.calibrate_copy:
         calibrate_copy()
@@ -344,6 +422,8 @@ def main():
     }
     if not args.no_train_step:
         res["train_step"] = time_train_step(min(args.steps, 20))
+    if not args.no_other:
+        res["other_forwards"] = time_other_forwards(min(args.steps, 20))
     if not args.no_dwc:
         res["dwc_branch"] = time_dwc_branch(min(args.steps, 20))
     if not args.no_cpu_baseline:

@@ -28,20 +28,20 @@ def to_dev(x, dtype):
     return t.to(torch.bfloat16) if dtype == "bf16" else t
 
 
-def replay_case(L, w, backward):
+def replay_case(L, w, backward, **kw):
     print("graph %s B=%d H=%d n=%d d=%d m=%d %s backward=%s" % (w.name, w.B, w.H, w.n, w.d, w.m, w.dtype, backward),
           flush=True)
     names = ("Q", "K", "V", "dO") if backward else ("Q", "K", "V")
     x = W.make_inputs(w, with_grad=backward)
     bufs = [to_dev(x[k], w.dtype) for k in names]
-    ws = L.workspace(bufs[0], w.m, w.T, for_backward=backward)
+    ws = L.workspace(bufs[0], w.m, w.T, backward, "dwc" in kw)
     outs = [torch.empty_like(bufs[0]) for _ in range(3 if backward else 1)]
 
     def run():
         if backward:
-            L.backward(*bufs, w.m, w.lam, w.T, grads=outs, ws=ws)
+            L.backward(*bufs, w.m, w.lam, w.T, grads=outs, ws=ws, **kw)
         else:
-            L.forward(*bufs, w.m, w.lam, w.T, out=outs[0], ws=ws)
+            L.forward(*bufs, w.m, w.lam, w.T, out=outs[0], ws=ws, **kw)
 
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
@@ -63,9 +63,9 @@ def replay_case(L, w, backward):
         torch.cuda.synchronize()
         got = [o.clone() for o in outs]
         if backward:
-            ref = L.backward(*bufs, w.m, w.lam, w.T)
+            ref = L.backward(*bufs, w.m, w.lam, w.T, **kw)
         else:
-            ref = (L.forward(*bufs, w.m, w.lam, w.T),)
+            ref = (L.forward(*bufs, w.m, w.lam, w.T, **kw),)
         torch.cuda.synchronize()
         same = [torch.equal(a, b) for a, b in zip(got, ref)]
         print("  replay %d bitwise equal to eager: %s" % (r, same), flush=True)
@@ -80,3 +80,14 @@ def test_forward_graph_replay(L, dtype):
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
 def test_backward_graph_replay(L, dtype):
     replay_case(L, W.small(W.WORKLOADS["train"], n=900, B=1, H=2).with_(dtype=dtype), backward=True)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_forward_graph_replay_with_options(L, dtype):
+    """The convolution branch and the landmark-space normalisation under capture."""
+    import numpy as np
+    w = W.small(W.WORKLOADS["train"], n=24 * 20, B=1, H=2).with_(dtype=dtype, m=30)
+    fw, fb = W.make_dwc(2, w.d, 3, seed=21)
+    wh = np.random.default_rng(22).uniform(0.5, 1.5, size=(2, 30)).astype(np.float32)
+    dev = lambda a: torch.from_numpy(a).to("cuda")
+    replay_case(L, w, backward=False, norm=3, grid=(20, 4), dwc=(dev(fw), dev(fb)), whiten=dev(wh))

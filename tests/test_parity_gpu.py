@@ -392,3 +392,17 @@ def test_backward_reuses_saved_forward_state(L, dtype):
         torch.cuda.synchronize()
         assert torch.equal(out_s, out_r)
         assert all(torch.equal(a, b) for a, b in zip(g_s, g_r))
+
+
+# ------------------------------------------------------------------------------ options together
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_all_options_together(L, dtype):
+    """Window landmarks, the landmark-space normalisation with a whitening, eps > 0, lambda = 4 and
+    a 5 x 5 convolution branch at once, forward and backward, against the oracle."""
+    w = W.Workload("combo", 2, 2, 24 * 20, 32, 30, 5, dtype, 1 / math.sqrt(32), 4.0, 47, True)
+    grid = (20, 4)   # 24 x 20 map, 4 x 4 windows: 6 x 5 = 30 landmarks
+    dwc = W.make_dwc(2, 32, 5, seed=12)
+    wh = rand_whiten(2, 30, 13)
+    check_forward(L, w, norm=MSPACE, eps=0.05, grid=grid, dwc=dwc, whiten=wh)
+    check_backward(L, w, norm=MSPACE, eps=0.05, grid=grid, dwc=dwc, whiten=wh)

@@ -23,6 +23,34 @@ static inline float kscale_of(float lambda) { return (float)(-1.4426950408889634
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 // ------------------------------------------------------------------------------------------
+// Direct global -> LDS copies (global_load_lds_dwordx4): each instruction moves 64 lanes x 16
+// bytes to consecutive LDS addresses.  Their completion is tracked by vmcnt alone -- the
+// compiler does not order later LDS reads after them -- so a reader waits with lds_dma_wait().
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+__device__ __forceinline__ void lds_dma16(float* lds_dst, const float* src_lane) {
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(src_lane), (lds_void_t*)(lds_dst),
+                                     16, 0, 0);
+}
+__device__ __forceinline__ void lds_dma4(float* lds_dst, const float* src_lane) {
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(src_lane), (lds_void_t*)(lds_dst),
+                                     4, 0, 0);
+}
+__device__ __forceinline__ void lds_dma_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Rows r0 .. r0+63 of a [n][64] array into a wave's [row][column] tile of pitch 65 by direct
+// copies (one row per instruction, all 64 in flight, no registers); rows past n are zero.
+// Columns at or past m hold whatever the array holds there: the callers never read them.
+__device__ __forceinline__ void load_rows64_dma(float* tile, const float* __restrict__ src, int r0, int n) {
+    const int l = (int)(threadIdx.x & 63);
+#pragma unroll
+    for (int r = 0; r < 64; ++r) lds_dma4(tile + r * 65, src + (size_t)min(r0 + r, n - 1) * 64 + l);
+    lds_dma_wait();
+    for (int r = max(0, n - r0); r < 64; ++r) tile[r * 65 + l] = 0.f;
+    __builtin_amdgcn_wave_barrier();
+}
+
+// ------------------------------------------------------------------------------------------
 // Query-major pass.  grid (nqb, BH), 256 threads, lane = query (wave w of block b covers
 // queries 256 b + 64 w ..).  Landmark rows of kt come through scalar registers (srows.hpp),
 // the rows of M are LDS broadcasts; loops that stream rows read no LDS (see pass 1).
@@ -92,7 +120,7 @@ __global__ __launch_bounds__(256) void bwd_query_kernel(const float* __restrict_
         tile[l * TP + a] = (live && a < m) ? __builtin_amdgcn_exp2f(dist * kscale) : 0.f;
     };
     if (saved) {   // the forward left the rows of A in Aq: copy them into the tile
-        load_rows64(tile, Aq + (size_t)h * n * 64, i0, n, m);
+        load_rows64_dma(tile, Aq + (size_t)h * n * 64, i0, n);
     } else {
         float ta[32], tb[32];
         srow32(ta, tab);
@@ -247,22 +275,6 @@ __global__ __launch_bounds__(256) void bwd_query_kernel(const float* __restrict_
         dvbar_part[((size_t)h * nqb + blockIdx.x) * D + tid] = 0.f;
     }
 }
-
-// ------------------------------------------------------------------------------------------
-// Direct global -> LDS copies (global_load_lds_dwordx4): each instruction moves 64 lanes x 16
-// bytes to consecutive LDS addresses.  Their completion is tracked by vmcnt alone -- the
-// compiler does not order later LDS reads after them -- so a reader waits with lds_dma_wait().
-typedef __attribute__((address_space(3))) void lds_void_t;
-
-__device__ __forceinline__ void lds_dma16(float* lds_dst, const float* src_lane) {
-    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(src_lane), (lds_void_t*)(lds_dst),
-                                     16, 0, 0);
-}
-__device__ __forceinline__ void lds_dma4(float* lds_dst, const float* src_lane) {
-    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(src_lane), (lds_void_t*)(lds_dst),
-                                     4, 0, 0);
-}
-__device__ __forceinline__ void lds_dma_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // The rows of a [token][W] array (W floats per row, W a multiple of 4) for tokens t0 .. t0 + R - 1
 // (clamped to the last token) into dst[R][W]; R W must be a multiple of 256.
@@ -700,7 +712,7 @@ __global__ __launch_bounds__(256) void bwd_key_kernel(const float* __restrict__ 
     };
     if (saved) {   // the forward's key-side summary left the rows of B in dDk: copy them (each
                    // wave reads only its own rows, which it overwrites with dD further down)
-        load_rows64(tile, dDk + (size_t)h * n * 64, j0, n, m);
+        load_rows64_dma(tile, dDk + (size_t)h * n * 64, j0, n);
     } else {
         float ta[32], tb[32];
         srow32(ta, tab);

@@ -73,10 +73,9 @@ __device__ __host__ __forceinline__ LmTokens lm_tokens(LmPool p, int l, int n, i
     return k;
 }
 
-// A wave's [row][column] tile of pitch 65 (rows r0 .. r0+63, columns below 64) and a [n][64]
-// row array: lane l moves column l of 16 rows at a time, so that 16 accesses are in flight.
-// Stores skip rows past n and columns past m; loads give zeros there (rows clamped into the
-// array, so that the loads are unconditional).
+// A wave's [row][column] tile of pitch 65 (rows r0 .. r0+63) into a [n][64] row array: lane l
+// moves column l of 16 rows at a time, so that 16 accesses are in flight; rows past n and
+// columns past m are skipped.
 __device__ __forceinline__ void store_rows64(float* __restrict__ dst, const float* __restrict__ tile, int r0, int n,
                                              int m) {
     const int l = (int)(threadIdx.x & 63);
@@ -88,18 +87,6 @@ __device__ __forceinline__ void store_rows64(float* __restrict__ dst, const floa
 #pragma unroll
         for (int t = 0; t < 16; ++t)
             if (l < m && r0 + b + t < n) dst[(size_t)(r0 + b + t) * 64 + l] = v[t];
-    }
-}
-__device__ __forceinline__ void load_rows64(float* __restrict__ tile, const float* __restrict__ src, int r0, int n,
-                                            int m) {
-    const int l = (int)(threadIdx.x & 63);
-#pragma unroll 1
-    for (int b = 0; b < 64; b += 16) {
-        float v[16];
-#pragma unroll
-        for (int t = 0; t < 16; ++t) v[t] = src[(size_t)min(r0 + b + t, n - 1) * 64 + l];
-#pragma unroll
-        for (int t = 0; t < 16; ++t) tile[(b + t) * 65 + l] = (l < m && r0 + b + t < n) ? v[t] : 0.f;
     }
 }
 

@@ -90,6 +90,15 @@ __device__ __forceinline__ void store_rows64(float* __restrict__ dst, const floa
     }
 }
 
+// Blocks are dispatched to the 8 XCDs round-robin (block i to XCD i % 8).  xcd_order maps block i
+// of n to a logical index such that each XCD's blocks get a contiguous range: a bijection of [0, n).
+__device__ __forceinline__ int xcd_order(int i, int n) {
+    const int x = i & 7, y = i >> 3;
+    int off = 0;
+    for (int xp = 0; xp < x; ++xp) off += xp < n ? (n - xp + 7) >> 3 : 0;
+    return off + y;
+}
+
 __device__ __forceinline__ float sgnf(float x) { return (float)((x > 0.f) - (x < 0.f)); }
 __device__ __forceinline__ double sgnd(double x) { return (double)((x > 0.0) - (x < 0.0)); }
 

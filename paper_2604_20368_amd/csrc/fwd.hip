@@ -80,7 +80,10 @@ __global__ __launch_bounds__(256) void key_summary_kernel(const float* __restric
     constexpr int BP = 68;                 // LDS pitch of a wave's B tile (conflict-free reads)
     constexpr int RP = 16 * CT;            // pitch of the partial being reduced
     __shared__ __attribute__((aligned(16))) float lds[4 * 64 * BP];
-    const int chunk = blockIdx.x, h = blockIdx.y;
+    // blocks in XCD-contiguous order: the blocks that one XCD runs take consecutive (head, chunk)
+    // pairs, so that a CU's scalar cache serves few landmark tables
+    const int G = (int)(gridDim.x * gridDim.y), lin = xcd_order(blockIdx.y * gridDim.x + blockIdx.x, G);
+    const int chunk = lin % (int)gridDim.x, h = lin / (int)gridDim.x;
     const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, li = l & 15, lk = l >> 4;
     float* sB = lds + w * 64 * BP;
     const float* tab = qt + __builtin_amdgcn_readfirstlane(h * m * D);   // wave-uniform: scalar loads

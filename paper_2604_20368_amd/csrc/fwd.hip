@@ -370,14 +370,33 @@ __global__ __launch_bounds__(256) void ns_solve_kernel(const float* __restrict__
 // Query side (fp32 inputs).  grid (ceil(n/256), BH), 256 threads, lane = query (wave w of block
 // b covers queries 256 b + 64 w ..).
 //   Landmark pass: a_il = k(q_i, kt_l) into the wave's [query][landmark] LDS tile (the landmark
-//   rows of kt through scalar registers).  s_i = sum_l a_il M[l][d] in fp32 is formed with the
-//   contraction, which reads the tile anyway.
+//   rows of kt through scalar registers), 32 landmarks at a time: the tile is 64 x 33 floats per
+//   wave, so that three blocks share a compute unit.  s_i = sum_l a_il M[l][d] in fp32 is formed
+//   with the contraction, which reads the tile anyway.
 //   Contraction: for each 32-query half, Y^T = M^T A^T on fp32 MFMA 32x32x2 (k = a pair of
 //   landmarks).  The B operands of a pair for both halves come from one permlane32 swap of the
 //   pair's two tile columns (queries 0..31 keep theirs and receive the other landmark of 32..63
 //   and vice versa).  The result holds, per lane, 16 output columns of one query: normalised
 //   (Eq. (4) / Eq. (3)) and stored four columns at a time.
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+// Rows r0 .. r0 + 63 of a 64 x 32 half tile (pitch 33) into columns c0 .. c0 + mh - 1 of dst
+// ([n][64]); rows past n are skipped.  Lanes 0..31 and 32..63 take two rows per store.
+__device__ __forceinline__ void store_half_rows(float* __restrict__ dst, const float* __restrict__ tile, int r0,
+                                                int n, int c0, int mh) {
+    const int l = (int)(threadIdx.x & 63), c = l & 31, rh = l >> 5;
+#pragma unroll 1
+    for (int b = 0; b < 64; b += 32) {
+        float v[16];
+#pragma unroll
+        for (int t = 0; t < 16; ++t) v[t] = tile[(b + 2 * t + rh) * 33 + c];
+#pragma unroll
+        for (int t = 0; t < 16; ++t) {
+            const int r = r0 + b + 2 * t + rh;
+            if (c < mh && r < n) dst[(size_t)r * 64 + c0 + c] = v[t];
+        }
+    }
+}
 
 template <int D, int NORM>
 __global__ __launch_bounds__(256) void query_out_kernel(const float* __restrict__ Q, float* __restrict__ Out,
@@ -390,7 +409,7 @@ __global__ __launch_bounds__(256) void query_out_kernel(const float* __restrict_
     constexpr int D1 = D + 1;
     constexpr int NCH = D / 32;
     constexpr int CB = D / 32;             // 32-column blocks of the output
-    constexpr int TP = 65;
+    constexpr int TP = 33;   // one half (32 landmarks) of the tile and a zero column
     // MFMA A operand of landmark pair s, column block cb: lane j + 32 k holds M[2s + k][32 cb + j]
     __shared__ __attribute__((aligned(16))) float sMT[32 * CB * 64];
     __shared__ float sMo[64];
@@ -434,31 +453,6 @@ __global__ __launch_bounds__(256) void query_out_kernel(const float* __restrict_
         }
     }
     __syncthreads();   // sMT, sMo, sVb
-    const float* tab = kt + __builtin_amdgcn_readfirstlane(h * m * D);   // wave-uniform: scalar loads
-    const int units = m * NCH;
-    // no LDS reads in this loop: a wait for one would also wait for the row prefetch
-    auto emit = [&](int a, float dist) {   // a == m only past the table: a zero column
-        tile[l * TP + a] = (live && a < m) ? __builtin_amdgcn_exp2f(dist * kscale) : 0.f;
-    };
-    {
-        float ta[32], tb[32];
-        srow32(ta, tab);
-        float dist = 0.f;
-        for (int u = 0; u < units; u += 2) {
-            dist = l1_unit(q + 32 * (u % NCH), ta, tb, tab + 32 * min(u + 1, units - 1), dist);
-            if (NCH == 1) {
-                emit(u, dist);
-                dist = 0.f;
-            }
-            dist = l1_unit(q + 32 * ((u + 1) % NCH), tb, ta, tab + 32 * min(u + 2, units - 1), dist);
-            emit((u + 1) / NCH, dist);
-            dist = 0.f;
-        }
-        asm volatile("" ::"s"(ta[0]), "s"(ta[16]));
-    }
-    if (m & 1) tile[l * TP + m] = 0.f;   // the pair loops read column m (unwritten when d = 64)
-    __builtin_amdgcn_wave_barrier();
-    if (Asave) store_rows64(Asave + (size_t)h * n * 64, tile, i0, n, m);   // A's rows for the backward
     f32x16_t acc[2][CB];
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb)
@@ -466,20 +460,51 @@ __global__ __launch_bounds__(256) void query_out_kernel(const float* __restrict_
         for (int cb = 0; cb < CB; ++cb)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[qb][cb][r] = 0.f;
-    const int npair = (m + 1) / 2;
     float s = 0.f;   // s_i = sum_l a_il M[l][d], in landmark order
-#pragma unroll 2
-    for (int p = 0; p < npair; ++p) {
-        const float x0 = tile[l * TP + 2 * p], x1 = tile[l * TP + 2 * p + 1];
-        s = fmaf(x1, sMo[2 * p + 1], fmaf(x0, sMo[2 * p], s));
-        const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x0), __float_as_uint(x1), false, false);
-#pragma unroll
-        for (int cb = 0; cb < CB; ++cb) {
-            const float av = sMT[(p * CB + cb) * 64 + l];
-#pragma unroll
-            for (int qb = 0; qb < 2; ++qb)
-                acc[qb][cb] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, __uint_as_float(b[qb]), acc[qb][cb], 0, 0, 0);
+    for (int hh = 0; 32 * hh < m; ++hh) {
+        const int mh = min(32, m - 32 * hh);   // landmarks 32 hh .. 32 hh + mh - 1
+        const float* tab = kt + __builtin_amdgcn_readfirstlane((h * m + 32 * hh) * D);   // wave-uniform: scalar loads
+        const int units = mh * NCH;
+        // no LDS reads in this loop: a wait for one would also wait for the row prefetch
+        auto emit = [&](int a, float dist) {   // a == mh only past the table: a zero column
+            tile[l * TP + a] = (live && a < mh) ? __builtin_amdgcn_exp2f(dist * kscale) : 0.f;
+        };
+        {
+            float ta[32], tb[32];
+            srow32(ta, tab);
+            float dist = 0.f;
+            for (int u = 0; u < units; u += 2) {
+                dist = l1_unit(q + 32 * (u % NCH), ta, tb, tab + 32 * min(u + 1, units - 1), dist);
+                if (NCH == 1) {
+                    emit(u, dist);
+                    dist = 0.f;
+                }
+                dist = l1_unit(q + 32 * ((u + 1) % NCH), tb, ta, tab + 32 * min(u + 2, units - 1), dist);
+                emit((u + 1) / NCH, dist);
+                dist = 0.f;
+            }
+            asm volatile("" ::"s"(ta[0]), "s"(ta[16]));
         }
+        if (mh & 1) tile[l * TP + mh] = 0.f;   // the pair loop reads column mh (unwritten when d = 64)
+        __builtin_amdgcn_wave_barrier();
+        if (Asave) store_half_rows(Asave + (size_t)h * n * 64, tile, i0, n, 32 * hh, mh);   // A's rows for the backward
+        const int npair = (mh + 1) / 2;
+#pragma unroll 2
+        for (int pl = 0; pl < npair; ++pl) {
+            const int p = 16 * hh + pl;   // landmark pair of the whole tile
+            const float x0 = tile[l * TP + 2 * pl], x1 = tile[l * TP + 2 * pl + 1];
+            s = fmaf(x1, sMo[2 * p + 1], fmaf(x0, sMo[2 * p], s));
+            const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x0), __float_as_uint(x1), false, false);
+#pragma unroll
+            for (int cb = 0; cb < CB; ++cb) {
+                const float av = sMT[(p * CB + cb) * 64 + l];
+#pragma unroll
+                for (int qb = 0; qb < 2; ++qb)
+                    acc[qb][cb] =
+                        __builtin_amdgcn_mfma_f32_32x32x2f32(av, __uint_as_float(b[qb]), acc[qb][cb], 0, 0, 0);
+            }
+        }
+        __builtin_amdgcn_wave_barrier();   // the next half overwrites the tile
     }
     // result register r at lane l: column 8 (r / 4) + 4 (l / 32) + r % 4 of the block, query l % 32
     // of the half; s_i of that query from the same swap

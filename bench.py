@@ -225,6 +225,167 @@ def time_dwc_branch(steps):
     return res
 
 
+SWEEP_N = (256, 1024, 4096, 16384)
+SWEEP_M = (16, 32, 64)
+# kernels that evaluate the Laplacian kernel (with the contractions fused into them) and the
+# Newton-Schulz kernels, forward and backward
+SWEEP_GROUPS = (("lap_fwd", ("key_summary", "query_out")),
+                ("lap_bwd", ("bwd_query", "bwd_query_lm", "bwd_key", "bwd_key_lm")),
+                ("ns_fwd", ("ns_solve",)), ("ns_bwd", ("bwd_ns",)))
+
+
+def _eager_lap(Q, K, V1, qt, kt, M, lam):
+    """The two Laplacian kernel evaluations and their contractions as plain PyTorch operations:
+    U = B [V | 1] with B_aj = k(qt_a, k_j), Y = A M with A_il = k(q_i, kt_l)."""
+    import torch
+    A = torch.exp(-torch.cdist(Q, kt, p=1) / lam)
+    Bt = torch.exp(-torch.cdist(K, qt, p=1) / lam)
+    return torch.matmul(Bt.transpose(1, 2).contiguous(), V1), torch.matmul(A, M)
+
+
+def _eager_ns(qt, kt, U, lam, T):
+    """K_LL, the Newton-Schulz iterates of Algorithm 2 from X_0 = K_LL^T / (||K_LL||_1 ||K_LL||_inf)
+    and M = X_T U as plain PyTorch operations."""
+    import torch
+    Wm = torch.exp(-torch.cdist(qt, kt, p=1) / lam)
+    c = Wm.abs().sum(1).amax(-1) * Wm.abs().sum(2).amax(-1)
+    X = Wm.transpose(1, 2).contiguous() / c[:, None, None]
+    I2 = 2.0 * torch.eye(Wm.shape[-1], device=Wm.device, dtype=Wm.dtype)
+    for _ in range(T):
+        X = torch.matmul(X, I2 - torch.matmul(Wm, X))
+    return torch.matmul(X, U)
+
+
+def time_sweep(steps):
+    """Execution time of the Laplacian kernel evaluation and of the Newton-Schulz solve, forward and
+    backward, over sequence lengths n and landmark counts m at batch 1, 2 heads, 32 channels (fp32,
+    lambda = sqrt(32), T = 6, inline normalisation): the setting of the paper's kernel timing
+    (Sec. 3, CUDA acceleration).  Ours: per-kernel HIP events around the library's launches in a
+    forward and backward with the save option (the backward reuses the forward's kernel values).
+    Beside them the same computations written as plain PyTorch operations (autograd for their
+    backward), timed with events on the same GPU.  out_rel and grad_rel compare the two: the
+    largest per-head relative Frobenius difference of the output and of dQ, dK, dV (the
+    PyTorch gradients from autograd through the whole composition, pooling included)."""
+    import torch
+    from paper_2604_20368_amd import lapattn
+    dev = torch.device("cuda:0")
+    d, T, lam = 32, 6, math.sqrt(32)
+    rows = []
+
+    def ev_time(fn, pre=None):   # mean ms of fn over steps calls, events on torch's stream
+        tot = 0.0
+        for r in range(steps + 2):
+            args = pre() if pre else ()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn(*args)
+            b.record()
+            torch.cuda.synchronize()
+            if r >= 2:
+                tot += a.elapsed_time(b)
+        return tot / steps
+
+    def rel(a, b):
+        a, b = a.reshape(a.shape[0], -1).double(), b.reshape(b.shape[0], -1).double()
+        return float(((a - b).norm(dim=1) / b.norm(dim=1)).max())
+
+    for n in SWEEP_N:
+        for m in SWEEP_M:
+            wl = W.Workload("sweep", 1, 2, n, d, m, T, "fp32", 1 / math.sqrt(d), lam, 7 + n + m, True)
+            x = W.make_inputs(wl)
+            Q, K, V, dO = (torch.from_numpy(x[k]).to(dev) for k in ("Q", "K", "V", "dO"))
+            out = torch.empty_like(Q)
+            grads = tuple(torch.empty_like(Q) for _ in range(3))
+            ws = lapattn.workspace(Q, m, T, for_backward=True)
+
+            def step():
+                lapattn.forward(Q, K, V, m, lam, T, out=out, ws=ws, save=True)
+                lapattn.backward(Q, K, V, dO, m, lam, T, grads=grads, ws=ws, save=True)
+
+            for _ in range(3):
+                step()
+            torch.cuda.synchronize()
+            lapattn.lapattn_timing_enable(1)
+            for _ in range(steps):
+                step()
+            torch.cuda.synchronize()
+            lapattn.lapattn_timing_enable(0)
+            per = {}
+            for k, t in lapattn.lapattn_timing_read(cap=64 * steps + 64):
+                per[k] = per.get(k, 0.0) + t / steps
+            row = {"n": n, "m": m}
+            for g, names in SWEEP_GROUPS:
+                row["ours_" + g] = sum(per.get(k, 0.0) for k in names)
+            row["ours_other"] = sum(per.values()) - sum(row["ours_" + g] for g, _ in SWEEP_GROUPS)
+            row["ours_kernels"] = {k: round(v, 5) for k, v in per.items()}
+
+            # the same function in plain PyTorch (Q, K, V as [BH, n, d]; segments of n / m tokens)
+            BH = 2
+            Qf, Kf, Vf, dOf = (t.reshape(BH, n, d) for t in (Q, K, V, dO))
+            V1 = torch.cat([Vf, torch.ones(BH, n, 1, device=dev)], dim=2)
+            qt = Qf.reshape(BH, m, n // m, d).mean(2)
+            kt = Kf.reshape(BH, m, n // m, d).mean(2)
+            with torch.no_grad():
+                U0, _ = _eager_lap(Qf, Kf, V1, qt, kt, torch.zeros(BH, m, d + 1, device=dev), lam)
+                M0 = _eager_ns(qt, kt, U0, lam, T)
+            gU, gY = torch.randn(BH, m, d + 1, device=dev), torch.randn(BH, n, d + 1, device=dev)
+            gM = torch.randn(BH, m, d + 1, device=dev)
+            with torch.no_grad():
+                row["eager_lap_fwd"] = ev_time(lambda: _eager_lap(Qf, Kf, V1, qt, kt, M0, lam))
+                row["eager_ns_fwd"] = ev_time(lambda: _eager_ns(qt, kt, U0, lam, T))
+
+            def lap_graph():
+                ins = [t.detach().requires_grad_() for t in (Qf, Kf, V1, qt, kt, M0)]
+                return ins, _eager_lap(*ins, lam)
+
+            def ns_graph():
+                ins = [t.detach().requires_grad_() for t in (qt, kt, U0)]
+                return ins, (_eager_ns(*ins, lam, T),)
+
+            row["eager_lap_bwd"] = ev_time(lambda ins, o: torch.autograd.grad(o, ins, (gU, gY)), pre=lap_graph)
+            row["eager_ns_bwd"] = ev_time(lambda ins, o: torch.autograd.grad(o, ins, (gM,)), pre=ns_graph)
+
+            # whole composition once, untimed: the output and the gradients against ours
+            Qr, Kr, Vr = (t.detach().clone().requires_grad_() for t in (Qf, Kf, Vf))
+            qtr = Qr.reshape(BH, m, n // m, d).mean(2)
+            ktr = Kr.reshape(BH, m, n // m, d).mean(2)
+            V1r = torch.cat([Vr, torch.ones(BH, n, 1, device=dev)], dim=2)
+            Ur, _ = _eager_lap(Qr, Kr, V1r, qtr, ktr, torch.zeros(BH, m, d + 1, device=dev), lam)
+            _, Yr = _eager_lap(Qr, Kr, V1r, qtr, ktr, _eager_ns(qtr, ktr, Ur, lam, T), lam)
+            outr = Yr[:, :, :d] + (1.0 - Yr[:, :, d:]) * Vr.mean(1, keepdim=True)
+            gr = torch.autograd.grad(outr, (Qr, Kr, Vr), dOf)
+            step()
+            torch.cuda.synchronize()
+            row["out_rel"] = rel(out.reshape(BH, n, d), outr.detach())
+            row["grad_rel"] = max(rel(a.reshape(BH, n, d), b) for a, b in zip(grads, gr))
+            rows.append({k: (round(v, 5) if isinstance(v, float) and not k.endswith("_rel") else v)
+                         for k, v in row.items()})
+            print("sweep n=%d m=%d done" % (n, m), file=sys.stderr, flush=True)
+    return rows
+
+
+def print_sweep(rows):
+    cols = [("n", "n"), ("m", "m"), ("lap fwd: ours", "ours_lap_fwd"), ("PyTorch", "eager_lap_fwd"),
+            ("lap bwd: ours", "ours_lap_bwd"), ("PyTorch", "eager_lap_bwd"), ("NS fwd: ours", "ours_ns_fwd"),
+            ("PyTorch", "eager_ns_fwd"), ("NS bwd: ours", "ours_ns_bwd"), ("PyTorch", "eager_ns_bwd"),
+            ("ours other", "ours_other"), ("out_rel", "out_rel"), ("grad_rel", "grad_rel")]
+    print("| " + " | ".join(c for c, _ in cols) + " |")
+    print("|" + "---|" * len(cols))
+    for r in rows:
+        cells = []
+        for _, k in cols:
+            v = r[k]
+            cells.append(str(v) if isinstance(v, int) else ("%.1e" % v if k.endswith("_rel") else "%.1f" % (v * 1e3)))
+        print("| " + " | ".join(cells) + " |")
+    names = list(rows[0]["ours_kernels"])
+    print()
+    print("| n | m | " + " | ".join(names) + " |")
+    print("|" + "---|" * (len(names) + 2))
+    for r in rows:
+        print("| %d | %d | " % (r["n"], r["m"]) +
+              " | ".join("%.1f" % (r["ours_kernels"].get(k, 0.0) * 1e3) for k in names) + " |")
+
+
 KERNEL_SOURCES = ["paper_2604_20368_amd/csrc/fast.hip", "paper_2604_20368_amd/csrc/common.hpp",
                   "paper_2604_20368_amd/csrc/host.cpp"]
 COPY_BYTES = 512 * 1024 * 1024
@@ -341,6 +502,9 @@ def main():
                     help="skip the forward timing of the other forward-only workloads")
     ap.add_argument("--no-dwc", action="store_true",
                     help="skip the timing of the depth-wise convolution branch")
+    ap.add_argument("--sweep", action="store_true",
+                    help="only the (n, m) timing sweep of the Laplacian kernel and Newton-Schulz kernels "
+                         "(batch 1, 2 heads, d=32) beside plain PyTorch; prints a markdown table in us")
     ap.add_argument("--summarize-trace", metavar="TRACE_DIR",
                     help="per-leg kernel statistics of a rocprofv3 --kernel-trace CSV directory")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -359,6 +523,9 @@ def main():
         return
     if args.calibrate_copy:
         calibrate_copy()
+        return
+    if args.sweep:
+        print_sweep(time_sweep(min(args.steps, 20)))
         return
     if args.gpus != 1:
         print("bench.py measures one GPU: this build runs on a single MI355X and has no multi-GPU path "

@@ -58,7 +58,8 @@ __global__ __launch_bounds__(256) void pool_kernel(const typename elem<DT>::type
 
 // ------------------------------------------------------------------------------------------
 // Key-side summary (fp32 inputs).  grid (nkc, BH), 256 threads; block `chunk` covers keys
-// [chunk * chunk_keys, ...) in tiles of 64, one tile per wave at a time (lane = key j).
+// [chunk * chunk_keys, ...) (chunk_keys a multiple of 256) in tiles of 64, one tile per wave at a
+// time (lane = key j).
 //   Per tile: the key row in registers; for every landmark a, the L1 distance to qt_a -- the
 //   landmark row is wave-uniform and comes through scalar registers, 32 coordinates at a time,
 //   each unit's loads issued right after the first use of the previous one -- and

@@ -15,8 +15,13 @@ namespace {
 
 constexpr int kMaxM = 64;
 constexpr int kMaxT = 64;
-constexpr int kKeyChunk = 1024;  // keys per block of the key-summary kernel (four 64-key tiles per wave)
-constexpr int kLmChunk = 256;    // tokens per block of the landmark-major backward passes
+constexpr int kKeyChunk = 1024;  // keys per block of the key-summary kernel (four 64-key tiles per wave), at most
+constexpr int kKeyMinChunk = 256;  // ... and at least (one tile per wave: the kernel needs a multiple of 256)
+constexpr int kCUs = 256;
+constexpr int kLmChunk = 256;    // tokens per block of the landmark-major backward passes (at most)
+constexpr int kLmMinChunk = 32;  // ... and at least
+constexpr int kMaxParts = 64;    // partial sums per head that a shorter chunk may create
+constexpr int kLmWaves = 1024;   // one wave per SIMD of the chip
 constexpr int kDwcChunk = 256;   // tokens per block of the convolution filter gradient
 constexpr int kDwcMaxK = 7;      // largest convolution filter side
 
@@ -67,8 +72,28 @@ struct Plan {
     size_t p0_part;                      // landmark-space normalisation: per-block sums of dOut
     size_t dwc_part;                     // convolution branch, backward: filter-gradient partials
     size_t total;
-    int MP, nkc, nqb, nlc;
+    int MP, nkc, nqb, nlc, lmc, kc;
 };
+
+// Keys per block of the fp32 key-side summary: 1024, halved while the grid has fewer blocks than
+// the chip has compute units and the per-head partial sums stay within kMaxParts.
+int key_chunk(int BH, int n) {
+    int c = kKeyChunk;
+    while (c > kKeyMinChunk && (long long)BH * ((n + c - 1) / c) < kCUs && (n + c / 2 - 1) / (c / 2) <= kMaxParts)
+        c /= 2;
+    return c;
+}
+
+// Tokens per block of the landmark-major backward passes (one wave each, walking its tokens in
+// order): 256, halved while the grid holds fewer waves than the chip has SIMDs and the number of
+// per-head partial sums stays within kMaxParts, so that a few heads still spread over the chip.
+int lm_chunk(int BH, int n) {
+    int c = kLmChunk;
+    while (c > kLmMinChunk && (long long)BH * ((n + c - 1) / c) < kLmWaves &&
+           (n + c / 2 - 1) / (c / 2) <= kMaxParts)
+        c /= 2;
+    return c;
+}
 
 struct Carver {
     size_t off = 0;
@@ -83,9 +108,11 @@ struct Carver {
 Plan make_plan(int BH, int n, int d, int m, int T, bool bwd, bool bf16 = false, bool dwc = false) {
     Plan p{};
     p.MP = m <= 32 ? 32 : 64;
-    p.nkc = (n + kKeyChunk - 1) / kKeyChunk;
+    p.kc = key_chunk(BH, n);
+    p.nkc = (n + p.kc - 1) / p.kc;
     p.nqb = (n + 255) / 256;
-    p.nlc = (n + kLmChunk - 1) / kLmChunk;
+    p.lmc = lm_chunk(BH, n);
+    p.nlc = (n + p.lmc - 1) / p.lmc;
     const size_t bh = (size_t)BH, d1 = (size_t)d + 1, f = sizeof(float), g = sizeof(double);
     const size_t mpp = (size_t)p.MP * p.MP;
     Carver c;
@@ -271,7 +298,7 @@ hipError_t forward_internals(Recorder& rec, const Plan& p, const void* Q, const 
     e = run_named(rec, "pool", [&] { return lapattn::launch_pool(dtype, Q, K, V, qt, kt, vseg, BH, n, d, m, pl, st); });
     if (e != hipSuccess) return e;
     e = run_named(rec, "key_summary", [&] {
-        return lapattn::launch_key_summary(dtype, K, V, qt, Upart, Bsave, BH, n, d, m, lambda, kKeyChunk, p.nkc, st);
+        return lapattn::launch_key_summary(dtype, K, V, qt, Upart, Bsave, BH, n, d, m, lambda, p.kc, p.nkc, st);
     });
     if (e != hipSuccess) return e;
     e = run_named(rec, "ns_solve", [&] {
@@ -469,7 +496,7 @@ int lapattn_backward(const void* Q, const void* K, const void* V, const void* dO
         e = run_named(rec, "bwd_query_lm", [&] {
             return lapattn::launch_bwd_query_lm(q, g, at<float>(ws, p.kt), at<float>(ws, p.Aq), at<float>(ws, p.dDq),
                                                 at<float>(ws, p.rs), at<float>(ws, p.dYd), at<float>(ws, p.dM_part),
-                                                at<float>(ws, p.dkt_part), BH, n, d, m, kLmChunk, p.nlc, st);
+                                                at<float>(ws, p.dkt_part), BH, n, d, m, p.lmc, p.nlc, st);
         });
         if (e != hipSuccess) return LAPATTN_ERR_HIP;
         e = run_named(rec, "bwd_ns", [&] {
@@ -489,7 +516,7 @@ int lapattn_backward(const void* Q, const void* K, const void* V, const void* dO
         if (e != hipSuccess) return LAPATTN_ERR_HIP;
         e = run_named(rec, "bwd_key_lm", [&] {
             return lapattn::launch_bwd_key_lm(k, at<float>(ws, p.qt), at<float>(ws, p.dDk), at<float>(ws, p.dqt_part),
-                                              BH, n, d, m, kLmChunk, p.nlc, st);
+                                              BH, n, d, m, p.lmc, p.nlc, st);
         });
         if (e != hipSuccess) return LAPATTN_ERR_HIP;
         e = run_named(rec, "bwd_pool", [&] {

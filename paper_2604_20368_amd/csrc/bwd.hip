@@ -39,14 +39,32 @@ __device__ __forceinline__ void lds_dma4(float* lds_dst, const float* src_lane) 
 __device__ __forceinline__ void lds_dma_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // Rows r0 .. r0+63 of a [n][64] array into a wave's [row][column] tile of pitch 65 by direct
-// copies (one row per instruction, all 64 in flight, no registers); rows past n are zero.
+// copies (one row per instruction, all 64 in flight, no data registers); rows past n are zero.
+// The row addresses are formed in the loop (partly unrolled): fully unrolled, a caller's loop
+// would hoist all 64 of them and keep them in registers.
 // Columns at or past m hold whatever the array holds there: the callers never read them.
 __device__ __forceinline__ void load_rows64_dma(float* tile, const float* __restrict__ src, int r0, int n) {
     const int l = (int)(threadIdx.x & 63);
-#pragma unroll
-    for (int r = 0; r < 64; ++r) lds_dma4(tile + r * 65, src + (size_t)min(r0 + r, n - 1) * 64 + l);
+    const float* col = src + l;
+#pragma unroll 8
+    for (int r = 0; r < 64; ++r) lds_dma4(tile + r * 65, col + (size_t)min(r0 + r, n - 1) * 64);
     lds_dma_wait();
     for (int r = max(0, n - r0); r < 64; ++r) tile[r * 65 + l] = 0.f;
+    __builtin_amdgcn_wave_barrier();
+}
+
+// Columns c0 .. c0 + 31 of the same rows into a 64 x 32 tile of pitch 33: one row per copy, on
+// lanes 0..31 (a copy writes consecutive LDS words, and consecutive rows are 33 words apart).
+__device__ __forceinline__ void load_half_rows_dma(float* tile, const float* __restrict__ src, int r0, int n, int c0) {
+    const int l = (int)(threadIdx.x & 63);
+    if (l < 32) {
+        const float* col = src + c0 + l;
+#pragma unroll 8
+        for (int r = 0; r < 64; ++r) lds_dma4(tile + r * 33, col + (size_t)min(r0 + r, n - 1) * 64);
+    }
+    lds_dma_wait();
+    if (l < 32)
+        for (int r = max(0, n - r0); r < 64; ++r) tile[r * 33 + l] = 0.f;
     __builtin_amdgcn_wave_barrier();
 }
 
@@ -65,7 +83,7 @@ __device__ __forceinline__ void load_rows64_dma(float* tile, const float* __rest
 //   whitening, its ones column replaced by 1/m and vbar by sum_l w_l M_l (mvec); the partial
 //   sums of (1 - s_i) dO_i and of dO_i (into p0_part) give the gradient of the two vectors.
 template <int D, int NORM>
-__global__ __launch_bounds__(256) void bwd_query_kernel(const float* __restrict__ Q, const float* __restrict__ dO,
+__global__ __launch_bounds__(256, D == 32 ? 3 : 2) void bwd_query_kernel(const float* __restrict__ Q, const float* __restrict__ dO,
                                                         float* __restrict__ dQ, const float* __restrict__ kt,
                                                         const float* __restrict__ M, const float* __restrict__ vbar,
                                                         float* __restrict__ Aq, float* __restrict__ dDq,
@@ -77,7 +95,11 @@ __global__ __launch_bounds__(256) void bwd_query_kernel(const float* __restrict_
     constexpr bool CENTRED = NORM == NORM_INLINE || NORM == NORM_MSPACE;
     constexpr int D1 = D + 1;
     constexpr int NCH = D / 32;
-    constexpr int TP = 65;                 // tile pitch: lane-strided accesses are conflict-free
+    // Landmarks in ranges of LW: 32 (a 64 x 33 tile per wave, which lets three blocks share a
+    // compute unit), except for the row-sum normalisation, which needs s_i and y_i over all
+    // landmarks before dA and takes them in one range of 64.  Every sum keeps landmark order.
+    constexpr int LW = NORM == NORM_ROWSUM ? 64 : 32;
+    constexpr int TP = LW + 1;             // tile pitch: lane-strided accesses are conflict-free
     __shared__ __attribute__((aligned(16))) float sM[64 * D1];
     __shared__ float sVb[D];
     __shared__ float sT[4 * 64 * TP];
@@ -110,166 +132,170 @@ __global__ __launch_bounds__(256) void bwd_query_kernel(const float* __restrict_
         g[4 * c4 + 0] = b.x; g[4 * c4 + 1] = b.y; g[4 * c4 + 2] = b.z; g[4 * c4 + 3] = b.w;
     }
     __syncthreads();   // sM, sVb
-    const float* tab = kt + __builtin_amdgcn_readfirstlane(h * m * D);   // wave-uniform: scalar loads
-    const int units = m * NCH;
-
-    // pass 1: a_il into the tile (a landmark column a == m, reached only past the table, holds
-    // zeros).  The streaming loops read no LDS: a wait for an LDS read would also wait for the
-    // row prefetch.
-    auto emit = [&](int a, float dist) {
-        tile[l * TP + a] = (live && a < m) ? __builtin_amdgcn_exp2f(dist * kscale) : 0.f;
-    };
-    if (saved) {   // the forward left the rows of A in Aq: copy them into the tile
-        load_rows64_dma(tile, Aq + (size_t)h * n * 64, i0, n);
-    } else {
-        float ta[32], tb[32];
-        srow32(ta, tab);
-        float dist = 0.f;
-        for (int u = 0; u < units; u += 2) {
-            dist = l1_unit(q + 32 * (u % NCH), ta, tb, tab + 32 * min(u + 1, units - 1), dist);
-            if (NCH == 1) {
-                emit(u, dist);
-                dist = 0.f;
-            }
-            dist = l1_unit(q + 32 * ((u + 1) % NCH), tb, ta, tab + 32 * min(u + 2, units - 1), dist);
-            emit((u + 1) / NCH, dist);
-            dist = 0.f;
-        }
-        asm volatile("" ::"s"(ta[0]), "s"(ta[16]));
-    }
-    if (m & 1) tile[l * TP + m] = 0.f;   // the pair loops read column m (unwritten when d = 64)
-    __builtin_amdgcn_wave_barrier();
-    // s_i (and y_i for the row-sum normalisation) from the tile, in landmark order
-    float s = 0.f;
-    float y[NORM == NORM_ROWSUM ? D : 1];
-#pragma unroll
-    for (int c = 0; c < (NORM == NORM_ROWSUM ? D : 1); ++c) y[c] = 0.f;
-    for (int a = 0; a < m; ++a) {
-        const float av = tile[l * TP + a];
-        const float* mr = sM + a * D1;
-        s = fmaf(av, mr[D], s);
-        if (NORM == NORM_ROWSUM) {
-#pragma unroll
-            for (int c = 0; c < D; ++c) y[c] = fmaf(av, mr[c], y[c]);
-        }
-    }
     float rsc = 1.f, dyd = 0.f;
     if (CENTRED) {
         float t = 0.f;
 #pragma unroll
         for (int c = 0; c < D; ++c) t = fmaf(g[c], sVb[c], t);
         dyd = -t;
-    } else if (NORM == NORM_ROWSUM) {
-        float t = 0.f;
+    }
+    float s = 0.f;   // s_i (and y_i for the row-sum normalisation), in landmark order
+    float y[NORM == NORM_ROWSUM ? D : 1];
 #pragma unroll
-        for (int c = 0; c < D; ++c) t = fmaf(g[c], y[c], t);
-        rsc = 1.f / s;
-        dyd = -t / (s * s);
+    for (int c = 0; c < (NORM == NORM_ROWSUM ? D : 1); ++c) y[c] = 0.f;
+    float dq[D];
+#pragma unroll
+    for (int c = 0; c < D; ++c) dq[c] = 0.f;
+    const int nrange = LW == 64 ? 1 : (m + LW - 1) / LW;   // m <= 64
+    for (int ri = 0; ri < nrange; ++ri) {
+        const int lo = LW * ri, mh = min(LW, m - lo);   // landmarks lo .. lo + mh - 1: tile columns 0 .. mh - 1
+        const float* tab = kt + __builtin_amdgcn_readfirstlane((h * m + lo) * D);   // wave-uniform: scalar loads
+        const int units = mh * NCH;
+
+        // pass 1: a_il into the tile (a column mh, reached only past the table, holds zeros).
+        // The streaming loops read no LDS: a wait for an LDS read would also wait for the row
+        // prefetch.
+        auto emit = [&](int a, float dist) {
+            tile[l * TP + a] = (live && a < mh) ? __builtin_amdgcn_exp2f(dist * kscale) : 0.f;
+        };
+        if (saved) {   // the forward left the rows of A in Aq: copy them into the tile
+            if (LW == 64) load_rows64_dma(tile, Aq + (size_t)h * n * 64, i0, n);
+            else load_half_rows_dma(tile, Aq + (size_t)h * n * 64, i0, n, lo);
+        } else {
+            float ta[32], tb[32];
+            srow32(ta, tab);
+            float dist = 0.f;
+            for (int u = 0; u < units; u += 2) {
+                dist = l1_unit(q + 32 * (u % NCH), ta, tb, tab + 32 * min(u + 1, units - 1), dist);
+                if (NCH == 1) {
+                    emit(u, dist);
+                    dist = 0.f;
+                }
+                dist = l1_unit(q + 32 * ((u + 1) % NCH), tb, ta, tab + 32 * min(u + 2, units - 1), dist);
+                emit((u + 1) / NCH, dist);
+                dist = 0.f;
+            }
+            asm volatile("" ::"s"(ta[0]), "s"(ta[16]));
+        }
+        if (mh & 1) tile[l * TP + mh] = 0.f;   // the pair loops read column mh (unwritten when d = 64)
+        __builtin_amdgcn_wave_barrier();
+        for (int a = 0; a < mh; ++a) {
+            const float av = tile[l * TP + a];
+            const float* mr = sM + (lo + a) * D1;
+            s = fmaf(av, mr[D], s);
+            if (NORM == NORM_ROWSUM) {
+#pragma unroll
+                for (int c = 0; c < D; ++c) y[c] = fmaf(av, mr[c], y[c]);
+            }
+        }
+        if (NORM == NORM_ROWSUM) {   // one range: s and y are complete
+            float t = 0.f;
+#pragma unroll
+            for (int c = 0; c < D; ++c) t = fmaf(g[c], y[c], t);
+            rsc = 1.f / s;
+            dyd = -t / (s * s);
+        }
+        if (!saved) {
+            if (LW == 64) store_rows64(Aq + (size_t)h * n * 64, tile, i0, n, m);
+            else store_half_rows(Aq + (size_t)h * n * 64, tile, i0, n, lo, mh);
+        }
+        __builtin_amdgcn_wave_barrier();
+
+        // dA_il = sum_c M[l][c] dY_i[c] (dY_i = [rs_i dO_i | dYd_i]) on fp32 MFMA 32x32x2 as
+        // dA^T = M dY^T, per 32-landmark block lb of the range and 32-query half qb, k = a
+        // coordinate pair (the ones column is coordinate D, coordinate D + 1 is zero).  A operand:
+        // lane l holds M[32 lb + l % 32][2 s + l / 32]; B operand: one permlane32 swap of the
+        // lane's own pair of coordinates gives both halves (queries 0..31 keep theirs and receive
+        // coordinate 2s+1 of 32..63, and vice versa).  Result register r at lane l: landmark
+        // 32 lb + 8 (r / 4) + 4 (l / 32) + r % 4, query 32 qb + l % 32; dD = -a dA / lambda
+        // replaces a in the tile.
+        {
+            constexpr int KS = D / 2 + 1;   // coordinate pairs, the last one (dYd, 0)
+            const int nlb = (mh + 31) / 32, lb0 = lo / 32;
+            const int hk = l >> 5, lr = l & 31;
+            // one 32 x 32 block at a time (16 accumulator registers); the swaps are redone per block
+            for (int blk = 0; blk < 2 * nlb; ++blk) {
+                const int lb = blk >> 1, qb = blk & 1;
+                f32x16_t acc;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) {
+                    const float x0 = (2 * ks < D) ? g[2 * ks] * rsc : dyd;
+                    const float x1 = (2 * ks + 1 < D) ? g[2 * ks + 1] * rsc : 0.f;
+                    const auto bsw =
+                        __builtin_amdgcn_permlane32_swap(__float_as_uint(x0), __float_as_uint(x1), false, false);
+                    const int c = 2 * ks + hk;
+                    const float av = c <= D ? sM[(32 * (lb0 + lb) + lr) * D1 + c] : 0.f;
+                    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av, __uint_as_float(qb ? bsw[1] : bsw[0]), acc, 0, 0,
+                                                               0);
+                }
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int a = 32 * lb + 8 * (r >> 2) + 4 * hk + (r & 3);
+                    float* t = tile + (32 * qb + lr) * TP + a;
+                    *t = -*t * acc[r] * inv_lambda;
+                }
+            }
+        }
+        __builtin_amdgcn_wave_barrier();
+        if (LW == 64) store_rows64(dDq + (size_t)h * n * 64, tile, i0, n, m);
+        else store_half_rows(dDq + (size_t)h * n * 64, tile, i0, n, lo, mh);
+
+        // pass 2: dq_i += dD_il sign(q_i - kt_l); each unit's dD is read before the unit's
+        // first wait (which covers it); landmarks past m have dD = 0 (a zero column when mh is odd)
+        {
+            float ta[32], tb[32];
+            srow32(ta, tab);
+            for (int u = 0; u < units; u += 2) {
+                if (NCH == 1) {
+                    const float d0 = tile[l * TP + u], d1 = tile[l * TP + u + 1];
+                    __builtin_amdgcn_sched_barrier(0);
+                    sgn_unit(dq, q, ta, tb, tab + 32 * min(u + 1, units - 1), d0);
+                    sgn_unit(dq, q, tb, ta, tab + 32 * min(u + 2, units - 1), d1);
+                } else {
+                    const float d0 = tile[l * TP + u / NCH];
+                    __builtin_amdgcn_sched_barrier(0);
+                    sgn_unit(dq, q, ta, tb, tab + 32 * min(u + 1, units - 1), d0);
+                    sgn_unit(dq + 32, q + 32, tb, ta, tab + 32 * min(u + 2, units - 1), d0);
+                }
+            }
+            asm volatile("" ::"s"(ta[0]), "s"(ta[16]));
+        }
+        __builtin_amdgcn_wave_barrier();   // the next range overwrites the tile
     }
     if (live) {
         rs[(size_t)h * n + i] = rsc;
         dYd[(size_t)h * n + i] = dyd;
-    }
-    if (!saved) store_rows64(Aq + (size_t)h * n * 64, tile, i0, n, m);
-    __builtin_amdgcn_wave_barrier();
-
-    // dA_il = sum_c M[l][c] dY_i[c] (dY_i = [rs_i dO_i | dYd_i]) on fp32 MFMA 32x32x2 as
-    // dA^T = M dY^T, per 32-landmark block lb and 32-query half qb, k = a coordinate pair (the
-    // ones column is coordinate D, coordinate D + 1 is zero).  A operand: lane l holds
-    // M[32 lb + l % 32][2 s + l / 32]; B operand: one permlane32 swap of the lane's own pair of
-    // coordinates gives both halves (queries 0..31 keep theirs and receive coordinate 2s+1 of
-    // 32..63, and vice versa).  Result register r at lane l: landmark 32 lb + 8 (r / 4) +
-    // 4 (l / 32) + r % 4, query 32 qb + l % 32; dD = -a dA / lambda replaces a in the tile.
-    {
-        constexpr int KS = D / 2 + 1;   // coordinate pairs, the last one (dYd, 0)
-        const int nlb = (m + 31) / 32;
-        const int hk = l >> 5, lr = l & 31;
-        // one 32 x 32 block at a time (16 accumulator registers); the swaps are redone per block
-        for (int blk = 0; blk < 2 * nlb; ++blk) {
-            const int lb = blk >> 1, qb = blk & 1;
-            f32x16_t acc;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) acc[r] = 0.f;
-#pragma unroll
-            for (int s = 0; s < KS; ++s) {
-                const float x0 = (2 * s < D) ? g[2 * s] * rsc : dyd;
-                const float x1 = (2 * s + 1 < D) ? g[2 * s + 1] * rsc : 0.f;
-                const auto bsw =
-                    __builtin_amdgcn_permlane32_swap(__float_as_uint(x0), __float_as_uint(x1), false, false);
-                const int c = 2 * s + hk;
-                const float av = c <= D ? sM[(32 * lb + lr) * D1 + c] : 0.f;
-                acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av, __uint_as_float(qb ? bsw[1] : bsw[0]), acc, 0, 0, 0);
-            }
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int a = 32 * lb + 8 * (r >> 2) + 4 * hk + (r & 3);
-                float* t = tile + (32 * qb + lr) * TP + a;
-                *t = -*t * acc[r] * inv_lambda;
-            }
-        }
-    }
-    float dq[D];
-#pragma unroll
-    for (int c = 0; c < D; ++c) dq[c] = 0.f;
-    __builtin_amdgcn_wave_barrier();
-    store_rows64(dDq + (size_t)h * n * 64, tile, i0, n, m);
-
-    // pass 2: dq_i += dD_il sign(q_i - kt_l); each unit's dD is read before the unit's first
-    // wait (which covers it); landmarks past m have dD = 0 (a zero column when m is odd)
-    {
-        float ta[32], tb[32];
-        srow32(ta, tab);
-        for (int u = 0; u < units; u += 2) {
-            if (NCH == 1) {
-                const float d0 = tile[l * TP + u], d1 = tile[l * TP + u + 1];
-                __builtin_amdgcn_sched_barrier(0);
-                sgn_unit(dq, q, ta, tb, tab + 32 * min(u + 1, units - 1), d0);
-                sgn_unit(dq, q, tb, ta, tab + 32 * min(u + 2, units - 1), d1);
-            } else {
-                const float d0 = tile[l * TP + u / NCH];
-                __builtin_amdgcn_sched_barrier(0);
-                sgn_unit(dq, q, ta, tb, tab + 32 * min(u + 1, units - 1), d0);
-                sgn_unit(dq + 32, q + 32, tb, ta, tab + 32 * min(u + 2, units - 1), d0);
-            }
-        }
-        asm volatile("" ::"s"(ta[0]), "s"(ta[16]));
-    }
-    if (live) {
 #pragma unroll
         for (int c4 = 0; c4 < D / 4; ++c4)
             reinterpret_cast<float4*>(dQ + row)[c4] = make_float4(dq[4 * c4], dq[4 * c4 + 1], dq[4 * c4 + 2], dq[4 * c4 + 3]);
     }
-    // dvbar partial (and for the landmark-space form the plain sum of dO)
+    // dvbar partial (and for the landmark-space form the plain sum of dO): per wave through the
+    // tile, 32 columns at a time (rows in order), then over the waves in order
     if (CENTRED) {
-        __builtin_amdgcn_wave_barrier();
-        const float wt = live ? 1.f - s : 0.f;
+        auto block_sum = [&](float wt, float* part) {
 #pragma unroll
-        for (int c = 0; c < D; ++c) tile[l * TP + c] = wt * g[c];
-        __builtin_amdgcn_wave_barrier();
-        if (l < D) {
-            float t = 0.f;
-            for (int r = 0; r < 64; ++r) t += tile[r * TP + l];
-            sred[w * D + l] = t;
-        }
-        __syncthreads();
-        if (tid < D)
-            dvbar_part[((size_t)h * nqb + blockIdx.x) * D + tid] =
-                ((sred[tid] + sred[D + tid]) + sred[2 * D + tid]) + sred[3 * D + tid];
-        if (NORM == NORM_MSPACE) {
-            __syncthreads();   // sred is reused
-            const float wg = live ? 1.f : 0.f;
+            for (int c0 = 0; c0 < D; c0 += 32) {
+                __builtin_amdgcn_wave_barrier();
 #pragma unroll
-            for (int c = 0; c < D; ++c) tile[l * TP + c] = wg * g[c];
-            __builtin_amdgcn_wave_barrier();
-            if (l < D) {
-                float t = 0.f;
-                for (int r = 0; r < 64; ++r) t += tile[r * TP + l];
-                sred[w * D + l] = t;
+                for (int c = 0; c < 32; ++c) tile[l * TP + c] = wt * g[c0 + c];
+                __builtin_amdgcn_wave_barrier();
+                if (l < 32) {
+                    float t = 0.f;
+                    for (int r = 0; r < 64; ++r) t += tile[r * TP + l];
+                    sred[w * D + c0 + l] = t;
+                }
             }
             __syncthreads();
             if (tid < D)
-                p0_part[((size_t)h * nqb + blockIdx.x) * D + tid] =
+                part[((size_t)h * nqb + blockIdx.x) * D + tid] =
                     ((sred[tid] + sred[D + tid]) + sred[2 * D + tid]) + sred[3 * D + tid];
+        };
+        block_sum(live ? 1.f - s : 0.f, dvbar_part);
+        if (NORM == NORM_MSPACE) {
+            __syncthreads();   // sred is reused
+            block_sum(live ? 1.f : 0.f, p0_part);
         }
     } else if (tid < D) {
         dvbar_part[((size_t)h * nqb + blockIdx.x) * D + tid] = 0.f;

@@ -79,6 +79,7 @@ __device__ __host__ __forceinline__ LmTokens lm_tokens(LmPool p, int l, int n, i
 __device__ __forceinline__ void store_rows64(float* __restrict__ dst, const float* __restrict__ tile, int r0, int n,
                                              int m) {
     const int l = (int)(threadIdx.x & 63);
+    float* col = dst + (size_t)r0 * 64 + l;   // rows at constant offsets from one address
 #pragma unroll 1
     for (int b = 0; b < 64; b += 16) {
         float v[16];
@@ -86,7 +87,24 @@ __device__ __forceinline__ void store_rows64(float* __restrict__ dst, const floa
         for (int t = 0; t < 16; ++t) v[t] = tile[(b + t) * 65 + l];
 #pragma unroll
         for (int t = 0; t < 16; ++t)
-            if (l < m && r0 + b + t < n) dst[(size_t)(r0 + b + t) * 64 + l] = v[t];
+            if (l < m && r0 + b + t < n) col[(b + t) * 64] = v[t];
+    }
+}
+
+// Rows r0 .. r0 + 63 of a 64 x 32 half tile (pitch 33) into columns c0 .. c0 + mh - 1 of dst
+// ([n][64]); rows past n are skipped.  Lanes 0..31 and 32..63 take two rows per store.
+__device__ __forceinline__ void store_half_rows(float* __restrict__ dst, const float* __restrict__ tile, int r0,
+                                                int n, int c0, int mh) {
+    const int l = (int)(threadIdx.x & 63), c = l & 31, rh = l >> 5;
+    float* col = dst + (size_t)(r0 + rh) * 64 + c0 + c;   // rows at constant offsets from one address
+#pragma unroll 1
+    for (int b = 0; b < 64; b += 32) {
+        float v[16];
+#pragma unroll
+        for (int t = 0; t < 16; ++t) v[t] = tile[(b + 2 * t + rh) * 33 + c];
+#pragma unroll
+        for (int t = 0; t < 16; ++t)
+            if (c < mh && r0 + rh + b + 2 * t < n) col[(b + 2 * t) * 64] = v[t];
     }
 }
 

@@ -381,24 +381,6 @@ __global__ __launch_bounds__(256) void ns_solve_kernel(const float* __restrict__
 //   (Eq. (4) / Eq. (3)) and stored four columns at a time.
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
-// Rows r0 .. r0 + 63 of a 64 x 32 half tile (pitch 33) into columns c0 .. c0 + mh - 1 of dst
-// ([n][64]); rows past n are skipped.  Lanes 0..31 and 32..63 take two rows per store.
-__device__ __forceinline__ void store_half_rows(float* __restrict__ dst, const float* __restrict__ tile, int r0,
-                                                int n, int c0, int mh) {
-    const int l = (int)(threadIdx.x & 63), c = l & 31, rh = l >> 5;
-#pragma unroll 1
-    for (int b = 0; b < 64; b += 32) {
-        float v[16];
-#pragma unroll
-        for (int t = 0; t < 16; ++t) v[t] = tile[(b + 2 * t + rh) * 33 + c];
-#pragma unroll
-        for (int t = 0; t < 16; ++t) {
-            const int r = r0 + b + 2 * t + rh;
-            if (c < mh && r < n) dst[(size_t)r * 64 + c0 + c] = v[t];
-        }
-    }
-}
-
 template <int D, int NORM>
 __global__ __launch_bounds__(256) void query_out_kernel(const float* __restrict__ Q, float* __restrict__ Out,
                                                         const float* __restrict__ kt, const float* __restrict__ M,

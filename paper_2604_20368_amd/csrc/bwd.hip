@@ -699,14 +699,18 @@ __global__ __launch_bounds__(256) void bwd_ns_kernel(const float* __restrict__ q
 // The landmark rows are streamed twice (the table is small and stays in cache).  dV_j gets
 // dvbar / n at the end.
 template <int D>
-__global__ __launch_bounds__(256) void bwd_key_kernel(const float* __restrict__ K, const float* __restrict__ V,
+__global__ __launch_bounds__(256, D == 32 ? 3 : 2) void bwd_key_kernel(const float* __restrict__ K, const float* __restrict__ V,
                                                       float* __restrict__ dK, float* __restrict__ dV,
                                                       const float* __restrict__ qt, const float* __restrict__ dU,
                                                       const float* __restrict__ dvbar, float* __restrict__ dDk,
                                                       int saved, int n, int m, float kscale, float inv_lambda) {
     constexpr int D1 = D + 1;
     constexpr int NCH = D / 32;
-    constexpr int TP = 65;
+    // Landmarks in ranges of LW: 32 at d = 32 (a 64 x 33 tile per wave, which lets three blocks
+    // share a compute unit), one range of 64 at d = 64 (whose registers allow two blocks either
+    // way).  dV accumulates over the ranges; every sum keeps landmark order.
+    constexpr int LW = D == 32 ? 32 : 64;
+    constexpr int TP = LW + 1;
     __shared__ __attribute__((aligned(16))) float sdU[64 * D1];
     __shared__ float sdv[D];
     __shared__ float sT[4 * 64 * TP];
@@ -718,133 +722,159 @@ __global__ __launch_bounds__(256) void bwd_key_kernel(const float* __restrict__ 
     const int j = j0 + l;
     const bool live = j < n;
     const size_t row = ((size_t)h * n + (live ? j : n - 1)) * D;
-    float kk[D], v[D], dk[D];
+    float v[D], dk[D];
 #pragma unroll
     for (int c4 = 0; c4 < D / 4; ++c4) {
-        const float4 a = reinterpret_cast<const float4*>(K + row)[c4];
         const float4 b = reinterpret_cast<const float4*>(V + row)[c4];
-        kk[4 * c4 + 0] = a.x; kk[4 * c4 + 1] = a.y; kk[4 * c4 + 2] = a.z; kk[4 * c4 + 3] = a.w;
         v[4 * c4 + 0] = b.x; v[4 * c4 + 1] = b.y; v[4 * c4 + 2] = b.z; v[4 * c4 + 3] = b.w;
     }
+    // the key row, read where a pass needs it (a cache hit after the first time): held across the
+    // dV and dB products it would push the kernel past three blocks per compute unit
+    float kk[D];
+    auto load_key = [&]() {
+        const float* kr = K + row;
+        asm volatile("" : "+v"(kr));   // a fresh load each time, not a value kept from the last one
+#pragma unroll
+        for (int c4 = 0; c4 < D / 4; ++c4) {
+            const float4 a = reinterpret_cast<const float4*>(kr)[c4];
+            kk[4 * c4 + 0] = a.x; kk[4 * c4 + 1] = a.y; kk[4 * c4 + 2] = a.z; kk[4 * c4 + 3] = a.w;
+        }
+    };
 #pragma unroll
     for (int c = 0; c < D; ++c) dk[c] = 0.f;
     __syncthreads();   // sdU, sdv
-    const float* tab = qt + __builtin_amdgcn_readfirstlane(h * m * D);   // wave-uniform: scalar loads
-    const int units = m * NCH;
-    // distance pass: B_aj into the tile (a column a == m, reached only past the table, holds
-    // zeros); the streaming loops read no LDS
-    auto emit = [&](int a, float dist) {
-        tile[l * TP + a] = (live && a < m) ? __builtin_amdgcn_exp2f(dist * kscale) : 0.f;
-    };
-    if (saved) {   // the forward's key-side summary left the rows of B in dDk: copy them (each
-                   // wave reads only its own rows, which it overwrites with dD further down)
-        load_rows64_dma(tile, dDk + (size_t)h * n * 64, j0, n);
-    } else {
-        float ta[32], tb[32];
-        srow32(ta, tab);
-        float dist = 0.f;
-        for (int u = 0; u < units; u += 2) {
-            dist = l1_unit(kk + 32 * (u % NCH), ta, tb, tab + 32 * min(u + 1, units - 1), dist);
-            if (NCH == 1) {
-                emit(u, dist);
-                dist = 0.f;
-            }
-            dist = l1_unit(kk + 32 * ((u + 1) % NCH), tb, ta, tab + 32 * min(u + 2, units - 1), dist);
-            emit((u + 1) / NCH, dist);
-            dist = 0.f;
-        }
-        asm volatile("" ::"s"(ta[0]), "s"(ta[16]));
-    }
-    if (m & 1) tile[l * TP + m] = 0.f;   // the pair loops read column m (unwritten when d = 64)
-    __builtin_amdgcn_wave_barrier();
-    // dV = B^T dU[:, :d] (k = a landmark pair; A operand straight from the tile), stored at once
-    // with dvbar / n; then dB = [v | 1] dU^T on the same instruction (k = a coordinate pair; the A
-    // operands of both 32-key halves from one permlane32 swap of the lane's own values) and
-    // dD = -B dB / lambda in place in the tile.  Result register r at lane l: row 8 (r / 4) +
-    // 4 (l / 32) + r % 4, column l % 32 of the 32 x 32 block.
-    const int npair = (m + 1) / 2;
-    const float invn = 1.f / (float)n;
+    // dV_j = sum_a B_aj dU_a[:d] on fp32 MFMA 32x32x2 (k = a landmark pair; A operand straight
+    // from the tile), per 32-key half kh and 32-column block cb, accumulated over the ranges
+    f32x16_t accv[2][D / 32];
 #pragma unroll
     for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
-        for (int cb = 0; cb < D / 32; ++cb) {
-            f32x16_t acc;
+        for (int cb = 0; cb < D / 32; ++cb)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) acc[r] = 0.f;
-#pragma unroll 4
-            for (int p = 0; p < npair; ++p) {
-                const float av = tile[(32 * kh + (l & 31)) * TP + 2 * p + (l >> 5)];
-                const float bv = sdU[(2 * p + (l >> 5)) * D1 + 32 * cb + (l & 31)];
-                acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc, 0, 0, 0);
-            }
-            const int c = 32 * cb + (l & 31);
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int key = 32 * kh + 8 * (r / 4) + 4 * (l >> 5) + r % 4;
-                if (j0 + key < n) dV[((size_t)h * n + j0 + key) * D + c] = acc[r] + sdv[c] * invn;
-            }
-        }
-    {
-        f32x16_t acc[2][2];
+            for (int r = 0; r < 16; ++r) accv[kh][cb][r] = 0.f;
+    // dV with dvbar / n; result register r at lane l: key 32 kh + 8 (r / 4) + 4 (l / 32) + r % 4,
+    // column 32 cb + l % 32
+    auto store_dv = [&]() {
+        const float invn = 1.f / (float)n;
 #pragma unroll
         for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
-            for (int lb = 0; lb < 2; ++lb)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) acc[kh][lb][r] = 0.f;
-        const bool two = m > 32;
-#pragma unroll
-        for (int sp = 0; sp < D / 2; ++sp) {
-            const auto a2 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v[2 * sp]), __float_as_uint(v[2 * sp + 1]),
-                                                             false, false);
-#pragma unroll
-            for (int lb = 0; lb < 2; ++lb) {
-                if (lb == 1 && !two) break;
-                const float bv = sdU[(32 * lb + (l & 31)) * D1 + 2 * sp + (l >> 5)];
-#pragma unroll
-                for (int kh = 0; kh < 2; ++kh)
-                    acc[kh][lb] = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a2[kh]), bv, acc[kh][lb], 0, 0, 0);
-            }
-        }
-#pragma unroll
-        for (int lb = 0; lb < 2; ++lb) {
-            if (lb == 1 && !two) break;
-            const int a = 32 * lb + (l & 31);
-            const float u1 = sdU[a * D1 + D];
-#pragma unroll
-            for (int kh = 0; kh < 2; ++kh)
+            for (int cb = 0; cb < D / 32; ++cb) {
+                const int c = 32 * cb + (l & 31);
+                const float add = sdv[c] * invn;
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const int key = 32 * kh + 8 * (r / 4) + 4 * (l >> 5) + r % 4;
-                    float* tp = tile + key * TP + a;
-                    const float dd = -(*tp) * (acc[kh][lb][r] + u1) * inv_lambda;
-                    if (a < m) *tp = dd;
+                    if (j0 + key < n) dV[((size_t)h * n + j0 + key) * D + c] = accv[kh][cb][r] + add;
                 }
+            }
+    };
+    const int nrange = LW == 64 ? 1 : (m + LW - 1) / LW;   // m <= 64
+    for (int ri = 0; ri < nrange; ++ri) {
+        const int lo = LW * ri, mh = min(LW, m - lo);   // landmarks lo .. lo + mh - 1: tile columns 0 .. mh - 1
+        const float* tab = qt + __builtin_amdgcn_readfirstlane((h * m + lo) * D);   // wave-uniform: scalar loads
+        const int units = mh * NCH;
+        // distance pass: B_aj into the tile (a column mh, reached only past the table, holds
+        // zeros); the streaming loops read no LDS
+        auto emit = [&](int a, float dist) {
+            tile[l * TP + a] = (live && a < mh) ? __builtin_amdgcn_exp2f(dist * kscale) : 0.f;
+        };
+        if (saved) {   // the forward's key-side summary left the rows of B in dDk: copy the range's
+                       // columns (each wave reads only its own rows, whose columns it overwrites
+                       // with dD further down)
+            if (LW == 64) load_rows64_dma(tile, dDk + (size_t)h * n * 64, j0, n);
+            else load_half_rows_dma(tile, dDk + (size_t)h * n * 64, j0, n, lo);
+        } else {
+            load_key();
+            float ta[32], tb[32];
+            srow32(ta, tab);
+            float dist = 0.f;
+            for (int u = 0; u < units; u += 2) {
+                dist = l1_unit(kk + 32 * (u % NCH), ta, tb, tab + 32 * min(u + 1, units - 1), dist);
+                if (NCH == 1) {
+                    emit(u, dist);
+                    dist = 0.f;
+                }
+                dist = l1_unit(kk + 32 * ((u + 1) % NCH), tb, ta, tab + 32 * min(u + 2, units - 1), dist);
+                emit((u + 1) / NCH, dist);
+                dist = 0.f;
+            }
+            asm volatile("" ::"s"(ta[0]), "s"(ta[16]));
         }
-    }
-    __builtin_amdgcn_wave_barrier();
-    // sign pass: dK_j -= dD_aj sign(qt_a - k_j), accumulated as dD sign(k_j - qt_a); each unit's
-    // dD is read before the unit's first wait
-    {
-        float ta[32], tb[32];
-        srow32(ta, tab);
-        for (int u = 0; u < units; u += 2) {
-            if (NCH == 1) {
-                const float d0 = tile[l * TP + u], d1 = tile[l * TP + u + 1];
-                __builtin_amdgcn_sched_barrier(0);
-                sgn_unit(dk, kk, ta, tb, tab + 32 * min(u + 1, units - 1), d0);
-                sgn_unit(dk, kk, tb, ta, tab + 32 * min(u + 2, units - 1), d1);
-            } else {
-                const float d0 = tile[l * TP + u / NCH];
-                __builtin_amdgcn_sched_barrier(0);
-                sgn_unit(dk, kk, ta, tb, tab + 32 * min(u + 1, units - 1), d0);
-                sgn_unit(dk + 32, kk + 32, tb, ta, tab + 32 * min(u + 2, units - 1), d0);
+        if (mh & 1) tile[l * TP + mh] = 0.f;   // the pair loops read column mh (unwritten when d = 64)
+        __builtin_amdgcn_wave_barrier();
+        {
+            const int npair = (mh + 1) / 2;
+#pragma unroll
+            for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+                for (int cb = 0; cb < D / 32; ++cb)
+#pragma unroll 4
+                    for (int p = 0; p < npair; ++p) {
+                        const float av = tile[(32 * kh + (l & 31)) * TP + 2 * p + (l >> 5)];
+                        const float bv = sdU[(lo + 2 * p + (l >> 5)) * D1 + 32 * cb + (l & 31)];
+                        accv[kh][cb] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, accv[kh][cb], 0, 0, 0);
+                    }
+        }
+        if (LW == 64) store_dv();   // one range: dV is complete (its accumulators free for dB)
+        // dB = [v | 1] dU^T on the same instruction (k = a coordinate pair; the A operands of both
+        // 32-key halves from one permlane32 swap of the lane's own values), per 32-landmark block
+        // and key half, and dD = -B dB / lambda in place in the tile.  Result register r at lane
+        // l: key 32 kh + 8 (r / 4) + 4 (l / 32) + r % 4, landmark l % 32 of the block.
+        {
+            const int nlb = (mh + 31) / 32;
+            for (int lb = 0; lb < nlb; ++lb) {
+                const int ac = 32 * lb + (l & 31);   // tile column; landmark lo + ac
+                const float u1 = sdU[(lo + ac) * D1 + D];
+#pragma unroll 1
+                for (int kh = 0; kh < 2; ++kh) {   // rolled: the swaps are redone, not held, per half
+                    f32x16_t acc;
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+#pragma unroll
+                    for (int sp = 0; sp < D / 2; ++sp) {
+                        const auto a2 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v[2 * sp]),
+                                                                         __float_as_uint(v[2 * sp + 1]), false, false);
+                        const float bv = sdU[(lo + ac) * D1 + 2 * sp + (l >> 5)];
+                        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a2[kh]), bv, acc, 0, 0, 0);
+                    }
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int key = 32 * kh + 8 * (r / 4) + 4 * (l >> 5) + r % 4;
+                        float* tp = tile + key * TP + ac;
+                        const float dd = -(*tp) * (acc[r] + u1) * inv_lambda;
+                        if (ac < mh) *tp = dd;
+                    }
+                }
             }
         }
-        asm volatile("" ::"s"(ta[0]), "s"(ta[16]));
+        __builtin_amdgcn_wave_barrier();
+        if (LW == 64) store_rows64(dDk + (size_t)h * n * 64, tile, j0, n, m);
+        else store_half_rows(dDk + (size_t)h * n * 64, tile, j0, n, lo, mh);
+        // sign pass: dK_j -= dD_aj sign(qt_a - k_j), accumulated as dD sign(k_j - qt_a); each
+        // unit's dD is read before the unit's first wait
+        {
+            load_key();
+            float ta[32], tb[32];
+            srow32(ta, tab);
+            for (int u = 0; u < units; u += 2) {
+                if (NCH == 1) {
+                    const float d0 = tile[l * TP + u], d1 = tile[l * TP + u + 1];
+                    __builtin_amdgcn_sched_barrier(0);
+                    sgn_unit(dk, kk, ta, tb, tab + 32 * min(u + 1, units - 1), d0);
+                    sgn_unit(dk, kk, tb, ta, tab + 32 * min(u + 2, units - 1), d1);
+                } else {
+                    const float d0 = tile[l * TP + u / NCH];
+                    __builtin_amdgcn_sched_barrier(0);
+                    sgn_unit(dk, kk, ta, tb, tab + 32 * min(u + 1, units - 1), d0);
+                    sgn_unit(dk + 32, kk + 32, tb, ta, tab + 32 * min(u + 2, units - 1), d0);
+                }
+            }
+            asm volatile("" ::"s"(ta[0]), "s"(ta[16]));
+        }
+        __builtin_amdgcn_wave_barrier();   // the next range overwrites the tile
     }
-    __builtin_amdgcn_wave_barrier();
-    store_rows64(dDk + (size_t)h * n * 64, tile, j0, n, m);
+    if (LW == 32) store_dv();
     if (live) {
 #pragma unroll
         for (int c4 = 0; c4 < D / 4; ++c4)

@@ -63,15 +63,17 @@ __global__ __launch_bounds__(256) void pool_kernel(const typename elem<DT>::type
 //   Per tile: the key row in registers; for every landmark a, the L1 distance to qt_a -- the
 //   landmark row is wave-uniform and comes through scalar registers, 32 coordinates at a time,
 //   each unit's loads issued right after the first use of the previous one -- and
-//   B_aj = exp2(dist * kscale) into the wave's LDS tile [a][j]; then U_part[a][c] +=
-//   sum_j B_aj [V_j | 1]_c on fp32 MFMA 16x16x4 (A = B from LDS, B = value rows straight from
-//   global memory, loaded before the landmark loop; the ones column is column 0 of the last
-//   column tile).  At the end the four waves' partials are added in a fixed order.
+//   B_aj = exp2(dist * kscale) into the wave's LDS tile [a][j], 32 landmarks at a time (a
+//   32 x 64 tile per wave: three blocks share a compute unit at d = 32); after each range,
+//   U_part[a][c] += sum_j B_aj [V_j | 1]_c for its landmarks on fp32 MFMA 16x16x4 (A = B from
+//   LDS, B = value rows straight from global memory, loaded before the landmark loop; the ones
+//   column is column 0 of the last column tile).  At the end the four waves' partials are added
+//   in a fixed order.
 // Writes Upart[h][chunk][a][c] for a < m, c <= d.
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 template <int D>
-__global__ __launch_bounds__(256) void key_summary_kernel(const float* __restrict__ K, const float* __restrict__ V,
+__global__ __launch_bounds__(256, D == 32 ? 3 : 2) void key_summary_kernel(const float* __restrict__ K, const float* __restrict__ V,
                                                           const float* __restrict__ qt, float* __restrict__ Upart,
                                                           float* __restrict__ Bsave, int n, int m, float kscale,
                                                           int chunk_keys, int nkc) {
@@ -80,16 +82,15 @@ __global__ __launch_bounds__(256) void key_summary_kernel(const float* __restric
     constexpr int CT = D / 16 + 1;         // MFMA column tiles: the values, then the ones column
     constexpr int BP = 68;                 // LDS pitch of a wave's B tile (conflict-free reads)
     constexpr int RP = 16 * CT;            // pitch of the partial being reduced
-    __shared__ __attribute__((aligned(16))) float lds[4 * 64 * BP];
+    __shared__ __attribute__((aligned(16))) float lds[4 * 32 * BP];
+    static_assert(64 * RP <= 4 * 32 * BP, "the partial being reduced fits the tiles");
     // blocks in XCD-contiguous order: the blocks that one XCD runs take consecutive (head, chunk)
     // pairs, so that a CU's scalar cache serves few landmark tables
     const int G = (int)(gridDim.x * gridDim.y), lin = xcd_order(blockIdx.y * gridDim.x + blockIdx.x, G);
     const int chunk = lin % (int)gridDim.x, h = lin / (int)gridDim.x;
     const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, li = l & 15, lk = l >> 4;
-    float* sB = lds + w * 64 * BP;
+    float* sB = lds + w * 32 * BP;
     const float* tab = qt + __builtin_amdgcn_readfirstlane(h * m * D);   // wave-uniform: scalar loads
-    const int units = m * NCH;
-    for (int a = m; a < 64; ++a) sB[a * BP + l] = 0.f;
     f32x4_t acc[4][CT];
 #pragma unroll
     for (int rt = 0; rt < 4; ++rt)
@@ -121,50 +122,65 @@ __global__ __launch_bounds__(256) void key_summary_kernel(const float* __restric
             for (int ct = 0; ct < CT - 1; ++ct)
                 bv[s][ct] = V[((size_t)h * n + r) * D + 16 * ct + li];
         }
-        // landmark loop: unit u = (a, 32-coordinate part) of the table, two units per pass in
-        // alternating buffers; both units of a pass always run (a surplus unit past the table
-        // repeats the last one and stores a zero row), so that each prefetch stays where it is
-        // issued
-        {
-            float ta[32], tb[32];
-            srow32(ta, tab);
-            float dist = 0.f;
-            for (int u = 0; u < units; u += 2) {
-                dist = l1_unit(x + 32 * (u % NCH), ta, tb, tab + 32 * min(u + 1, units - 1), dist);
-                if (NCH == 1) {
-                    sB[u * BP + l] = live ? __builtin_amdgcn_exp2f(dist * kscale) : 0.f;
+#pragma unroll
+        for (int ri = 0; ri < 2; ++ri) {   // unrolled: acc is indexed by the range
+            if (32 * ri >= m) break;
+            const int mh = min(32, m - 32 * ri);   // landmarks 32 ri .. 32 ri + mh - 1: tile rows 0 .. mh - 1
+            const float* tabr = tab + 32 * ri * D;
+            const int units = mh * NCH;
+            for (int a = mh; a < 32; ++a) sB[a * BP + l] = 0.f;   // rows past m (else the last range's)
+            // landmark loop: unit u = (a, 32-coordinate part) of the range, two units per pass in
+            // alternating buffers; both units of a pass always run (a surplus unit past the table
+            // repeats the last one and stores a zero row), so that each prefetch stays where it is
+            // issued
+            {
+                float ta[32], tb[32];
+                srow32(ta, tabr);
+                float dist = 0.f;
+                for (int u = 0; u < units; u += 2) {
+                    dist = l1_unit(x + 32 * (u % NCH), ta, tb, tabr + 32 * min(u + 1, units - 1), dist);
+                    if (NCH == 1) {
+                        sB[u * BP + l] = live ? __builtin_amdgcn_exp2f(dist * kscale) : 0.f;
+                        dist = 0.f;
+                    }
+                    dist = l1_unit(x + 32 * ((u + 1) % NCH), tb, ta, tabr + 32 * min(u + 2, units - 1), dist);
+                    const int a = (u + 1) / NCH;   // < 32; a == mh only past the table (zero row)
+                    sB[a * BP + l] = (live && a < mh) ? __builtin_amdgcn_exp2f(dist * kscale) : 0.f;
                     dist = 0.f;
                 }
-                dist = l1_unit(x + 32 * ((u + 1) % NCH), tb, ta, tab + 32 * min(u + 2, units - 1), dist);
-                const int a = (u + 1) / NCH;   // < 64; a == m only past the table (zero row)
-                sB[a * BP + l] = (live && a < m) ? __builtin_amdgcn_exp2f(dist * kscale) : 0.f;
-                dist = 0.f;
+                // the last prefetch is consumed here, so that no prefetch is moved next to its use
+                asm volatile("" ::"s"(ta[0]), "s"(ta[16]));
             }
-            // the last prefetch is consumed here, so that no prefetch is moved next to its use
-            asm volatile("" ::"s"(ta[0]), "s"(ta[16]));
-        }
-        __builtin_amdgcn_wave_barrier();
-        // U_part += B [V | 1] over the tile's 64 keys, one 16-row tile of landmarks at a time
+            __builtin_amdgcn_wave_barrier();
+            // U_part += B [V | 1] over the tile's 64 keys, one 16-row tile of landmarks at a time
 #pragma unroll
-        for (int rt = 0; rt < 4; ++rt) {
-            if (16 * rt < m) {
+            for (int rl = 0; rl < 2; ++rl) {
+                const int rt = 2 * ri + rl;
+                if (16 * rt < m) {
 #pragma unroll
-                for (int s = 0; s < 16; ++s) {
-                    const float av = sB[(16 * rt + li) * BP + 4 * s + lk];
+                    for (int s = 0; s < 16; ++s) {
+                        const float av = sB[(16 * rl + li) * BP + 4 * s + lk];
 #pragma unroll
-                    for (int ct = 0; ct < CT - 1; ++ct)
-                        acc[rt][ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv[s][ct], acc[rt][ct], 0, 0, 0);
-                    acc[rt][CT - 1] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, li == 0 ? 1.f : 0.f, acc[rt][CT - 1],
-                                                                             0, 0, 0);
+                        for (int ct = 0; ct < CT - 1; ++ct)
+                            acc[rt][ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv[s][ct], acc[rt][ct], 0, 0, 0);
+                        acc[rt][CT - 1] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, li == 0 ? 1.f : 0.f,
+                                                                                 acc[rt][CT - 1], 0, 0, 0);
+                    }
                 }
             }
-        }
-        if (Bsave && live) {   // the key's row of B for the backward ([BH][n][64], zeros past m)
-            float4* dst = reinterpret_cast<float4*>(Bsave + ((size_t)h * n + j) * 64);
+            if (Bsave && live) {   // the key's row of B for the backward ([BH][n][64], zeros past m)
+                float4* dst = reinterpret_cast<float4*>(Bsave + ((size_t)h * n + j) * 64 + 32 * ri);
 #pragma unroll 4
-            for (int a4 = 0; a4 < 16; ++a4)
-                dst[a4] = make_float4(sB[(4 * a4) * BP + l], sB[(4 * a4 + 1) * BP + l], sB[(4 * a4 + 2) * BP + l],
-                                      sB[(4 * a4 + 3) * BP + l]);
+                for (int a4 = 0; a4 < 8; ++a4)
+                    dst[a4] = make_float4(sB[(4 * a4) * BP + l], sB[(4 * a4 + 1) * BP + l],
+                                          sB[(4 * a4 + 2) * BP + l], sB[(4 * a4 + 3) * BP + l]);
+            }
+            __builtin_amdgcn_wave_barrier();   // the next range overwrites the tile
+        }
+        if (Bsave && live && m <= 32) {   // no second range: its columns are zeros
+            float4* dst = reinterpret_cast<float4*>(Bsave + ((size_t)h * n + j) * 64 + 32);
+#pragma unroll
+            for (int a4 = 0; a4 < 8; ++a4) dst[a4] = make_float4(0.f, 0.f, 0.f, 0.f);
         }
         __builtin_amdgcn_wave_barrier();
     }

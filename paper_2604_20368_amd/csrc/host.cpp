@@ -15,9 +15,8 @@ namespace {
 
 constexpr int kMaxM = 64;
 constexpr int kMaxT = 64;
-constexpr int kKeyChunk = 1024;  // keys per block of the key-summary kernel (four 64-key tiles per wave), at most
-constexpr int kKeyMinChunk = 256;  // ... and at least (one tile per wave: the kernel needs a multiple of 256)
-constexpr int kCUs = 256;
+constexpr int kKeyChunk = 256;   // keys per block of the fp32 key-summary kernel (one 64-key tile per wave) ...
+constexpr int kKeyMaxChunk = 1024;  // ... up to this many for long sequences (a multiple of 256)
 constexpr int kLmChunk = 256;    // tokens per block of the landmark-major backward passes (at most)
 constexpr int kLmMinChunk = 32;  // ... and at least
 constexpr int kMaxParts = 64;    // partial sums per head that a shorter chunk may create
@@ -75,12 +74,11 @@ struct Plan {
     int MP, nkc, nqb, nlc, lmc, kc;
 };
 
-// Keys per block of the fp32 key-side summary: 1024, halved while the grid has fewer blocks than
-// the chip has compute units and the per-head partial sums stay within kMaxParts.
-int key_chunk(int BH, int n) {
+// Keys per block of the fp32 key-side summary: 256 (many small blocks fill the three block slots
+// of every compute unit evenly), doubled while a head would have more than kMaxParts partial sums.
+int key_chunk(int n) {
     int c = kKeyChunk;
-    while (c > kKeyMinChunk && (long long)BH * ((n + c - 1) / c) < kCUs && (n + c / 2 - 1) / (c / 2) <= kMaxParts)
-        c /= 2;
+    while (c < kKeyMaxChunk && (n + c - 1) / c > kMaxParts) c *= 2;
     return c;
 }
 
@@ -108,7 +106,7 @@ struct Carver {
 Plan make_plan(int BH, int n, int d, int m, int T, bool bwd, bool bf16 = false, bool dwc = false) {
     Plan p{};
     p.MP = m <= 32 ? 32 : 64;
-    p.kc = key_chunk(BH, n);
+    p.kc = key_chunk(n);
     p.nkc = (n + p.kc - 1) / p.kc;
     p.nqb = (n + 255) / 256;
     p.lmc = lm_chunk(BH, n);

@@ -230,6 +230,16 @@ def test_backward_shapes(L, d, m, n):
     check_backward(L, w)
 
 
+@pytest.mark.parametrize("n,d", [(4096, 32), (16384, 64)])
+def test_long_sequence_few_heads(L, n, d):
+    """Batch 1, 2 heads, m = 64: the chunk lengths the library picks for a small grid at their
+    limit of 64 partial sums per head -- 64-token landmark-major chunks at n = 4096 (256 at
+    n = 16384) and 256-key blocks on the key side (16 and 64 partials)."""
+    w = W.Workload("long", 1, 2, n, d, 64, 6, "fp32", 1 / math.sqrt(d), math.sqrt(d), 16, True)
+    check_forward(L, w)
+    check_backward(L, w)
+
+
 def test_backward_eps(L):
     w = W.Workload("beps", 1, 2, 300, 32, 16, 5, "fp32", 0.2, 4.0, 15, True)
     check_backward(L, w, eps=0.1)

@@ -8,9 +8,9 @@
 //   bwd_query_kernel     query-major: dY, dA = dY M^T, dD = -A dA / lambda, direct dQ
 //   bwd_query_lm_kernel  landmark-major over queries: dM = A^T dY, dkt from K_QL
 //   bwd_ns_kernel        dX = dM U^T, dU = X_T^T dM, reverse Newton-Schulz, K_LL backward
-//   bwd_key_kernel       key-major: dB = dU [v|1]^T, dV, dD' = -B dB / lambda, direct dK
+//   bwd_key_kernel       key-major: dB = dU [v|1]^T, dV, dD' = -B dB / lambda, dK
 //   bwd_key_lm_kernel    landmark-major over keys: dqt from K_LK
-//   bwd_pool_kernel      landmark-mean backward into dQ, dK
+//   bwd_pool_kernel      landmark-mean backward into dQ
 #include "common.hpp"
 #include "kernels.hpp"
 #include "ns_mfma.hpp"
@@ -429,7 +429,8 @@ __global__ __launch_bounds__(256) void bwd_ns_kernel(const float* __restrict__ q
                                                      const float* __restrict__ U, const float* __restrict__ dM_part,
                                                      const float* __restrict__ dvbar_part, float* __restrict__ dU,
                                                      float* __restrict__ dvbar, float* __restrict__ dqtW,
-                                                     float* __restrict__ dktW, const float* __restrict__ p0_part,
+                                                     float* __restrict__ dkpool, const float* __restrict__ dkt_part,
+                                                     LmPool pl, const float* __restrict__ p0_part,
                                                      const float* __restrict__ whiten, int mspace, int H, int n,
                                                      int m, int T, double lambda, double eps, int nlc, int nqb) {
     using SQ = ns_tiles<MP, MP>;
@@ -684,7 +685,13 @@ __global__ __launch_bounds__(256) void bwd_ns_kernel(const float* __restrict__ q
             const float qa = sqf[a * D + cc], t = sTf[a * MP + b];
             s += (qa > kb) ? t : ((qa < kb) ? -t : 0.f);
         }
-        dktW[(size_t)h * m * D + e] = -s;
+        // dk~_b: this term plus the query-side partial sums (chunk order, fp64), over the
+        // landmark's token count: the pooling gradient the key-major pass adds to its dK rows
+        const float kw = -s;
+        double ak = kw;
+#pragma unroll 4
+        for (int ch = 0; ch < nlc; ++ch) ak += dkt_part[(((size_t)h * nlc + ch) * m + b) * D + cc];
+        dkpool[(size_t)h * m * D + e] = (float)ak * (1.f / (float)lm_tokens(pl, b, n, m).count);
     }
 }
 
@@ -703,7 +710,8 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void bwd_key_kernel(const flo
                                                       float* __restrict__ dK, float* __restrict__ dV,
                                                       const float* __restrict__ qt, const float* __restrict__ dU,
                                                       const float* __restrict__ dvbar, float* __restrict__ dDk,
-                                                      int saved, int n, int m, float kscale, float inv_lambda) {
+                                                      const float* __restrict__ dkpool, LmPool pl, int saved, int n,
+                                                      int m, float kscale, float inv_lambda) {
     constexpr int D1 = D + 1;
     constexpr int NCH = D / 32;
     // Landmarks in ranges of LW: 32 at d = 32 (a 64 x 33 tile per wave, which lets three blocks
@@ -875,10 +883,15 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void bwd_key_kernel(const flo
         __builtin_amdgcn_wave_barrier();   // the next range overwrites the tile
     }
     if (LW == 32) store_dv();
-    if (live) {
+    if (live) {   // with the pooling gradient of the key's landmark (window or segment)
+        const int lp = pl.r ? ((j / pl.gw) / pl.r) * (pl.gw / pl.r) + (j % pl.gw) / pl.r : seg_of(j, n, m);
+        const float4* kp = reinterpret_cast<const float4*>(dkpool + ((size_t)h * m + lp) * D);
 #pragma unroll
-        for (int c4 = 0; c4 < D / 4; ++c4)
-            reinterpret_cast<float4*>(dK + row)[c4] = make_float4(dk[4 * c4], dk[4 * c4 + 1], dk[4 * c4 + 2], dk[4 * c4 + 3]);
+        for (int c4 = 0; c4 < D / 4; ++c4) {
+            const float4 p = kp[c4];
+            reinterpret_cast<float4*>(dK + row)[c4] =
+                make_float4(dk[4 * c4] + p.x, dk[4 * c4 + 1] + p.y, dk[4 * c4 + 2] + p.z, dk[4 * c4 + 3] + p.w);
+        }
     }
 }
 
@@ -934,31 +947,25 @@ __global__ __launch_bounds__(64) void bwd_key_lm_kernel(const float* __restrict_
 }
 
 // ------------------------------------------------------------------------------------------
-// Landmark-mean backward.  grid (m, BH), 256 threads: dq_l = dqtW_l + sum of the key-side
-// partials, dk_l = dktW_l + sum of the query-side partials (chunk order, fp64), then
-// dQ_i += dq_l / |S_l| and dK_i += dk_l / |S_l| over the landmark's tokens: one contiguous run
-// for a segment, r runs of r tokens for a window; four floats at a time.
-__global__ __launch_bounds__(256) void bwd_pool_kernel(float* __restrict__ dQ, float* __restrict__ dK,
-                                                       const float* __restrict__ dqtW, const float* __restrict__ dktW,
-                                                       const float* __restrict__ dqt_part,
-                                                       const float* __restrict__ dkt_part, int n, int d, int m,
+// Landmark-mean backward of the queries.  grid (m, BH), 256 threads: dq_l = dqtW_l + sum of the
+// key-side partials (chunk order, fp64), then dQ_i += dq_l / |S_l| over the landmark's tokens:
+// one contiguous run for a segment, r runs of r tokens for a window; four floats at a time.  The
+// keys' share (dk_l, summed by the Newton-Schulz backward) is added by the key-major pass, which
+// writes each dK row once.
+__global__ __launch_bounds__(256) void bwd_pool_kernel(float* __restrict__ dQ, const float* __restrict__ dqtW,
+                                                       const float* __restrict__ dqt_part, int n, int d, int m,
                                                        int nlc, LmPool pl) {
     const int l = blockIdx.x, h = blockIdx.y, tid = threadIdx.x;
-    __shared__ float sq[64], sk[64];
+    __shared__ float sq[64];
     const LmTokens tok = lm_tokens(pl, l, n, m);
     const int cntl = tok.count;
     const float inv = 1.f / (float)cntl;
     if (tid < d) {
         const size_t o = ((size_t)h * m + l) * d + tid;
-        double aq = dqtW[o], ak = dktW[o];
+        double aq = dqtW[o];
 #pragma unroll 4
-        for (int ch = 0; ch < nlc; ++ch) {
-            const size_t p = (((size_t)h * nlc + ch) * m + l) * d + tid;
-            aq += dqt_part[p];
-            ak += dkt_part[p];
-        }
+        for (int ch = 0; ch < nlc; ++ch) aq += dqt_part[(((size_t)h * nlc + ch) * m + l) * d + tid];
         sq[tid] = (float)aq * inv;
-        sk[tid] = (float)ak * inv;
     }
     __syncthreads();
     const int runs = pl.r ? pl.r : 1, run_len = pl.r ? pl.r : cntl;
@@ -966,14 +973,11 @@ __global__ __launch_bounds__(256) void bwd_pool_kernel(float* __restrict__ dQ, f
         const size_t base = ((size_t)h * n + tok(k * run_len)) * d;
         const int cnt4 = run_len * d / 4;
         float4* q4 = reinterpret_cast<float4*>(dQ + base);
-        float4* k4 = reinterpret_cast<float4*>(dK + base);
         for (int e = tid; e < cnt4; e += 256) {
             const int c = (4 * e) % d;
-            float4 a = q4[e], b = k4[e];
+            float4 a = q4[e];
             a.x += sq[c]; a.y += sq[c + 1]; a.z += sq[c + 2]; a.w += sq[c + 3];
-            b.x += sk[c]; b.y += sk[c + 1]; b.z += sk[c + 2]; b.w += sk[c + 3];
             q4[e] = a;
-            k4[e] = b;
         }
     }
 }
@@ -1090,11 +1094,13 @@ hipError_t launch_bwd_query_lm(const float* Q, const float* dO, const float* kt,
 
 hipError_t launch_bwd_ns(const float* qt, const float* kt, const double* Xs, const double* cinfo, const float* U,
                          const float* dM_part, const float* dvbar_part, float* dU, float* dvbar, float* dqtW,
-                         float* dktW, const float* p0_part, const float* whiten, int mspace, int BH, int H, int n,
-                         int d, int m, int T, double lambda, double eps, int nlc, int nqb, int MP, hipStream_t st) {
+                         float* dkpool, const float* dkt_part, LmPool pl, const float* p0_part, const float* whiten,
+                         int mspace, int BH, int H, int n, int d, int m, int T, double lambda, double eps, int nlc,
+                         int nqb, int MP, hipStream_t st) {
 #define LAPATTN_BNS(MPv, Dv)                                                                                      \
     hipLaunchKernelGGL((bwd_ns_kernel<MPv, Dv>), dim3(BH), dim3(256), 0, st, qt, kt, Xs, cinfo, U, dM_part,       \
-                       dvbar_part, dU, dvbar, dqtW, dktW, p0_part, whiten, mspace, H, n, m, T, lambda, eps, nlc, nqb)
+                       dvbar_part, dU, dvbar, dqtW, dkpool, dkt_part, pl, p0_part, whiten, mspace, H, n, m, T, lambda, \
+                       eps, nlc, nqb)
     if (MP == 32 && d == 32) LAPATTN_BNS(32, 32);
     else if (MP == 32) LAPATTN_BNS(32, 64);
     else if (d == 32) LAPATTN_BNS(64, 32);
@@ -1104,16 +1110,16 @@ hipError_t launch_bwd_ns(const float* qt, const float* kt, const double* Xs, con
 }
 
 hipError_t launch_bwd_key(const float* K, const float* V, float* dK, float* dV, const float* qt, const float* dU,
-                          const float* dvbar, float* dDk, int saved, int BH, int n, int d, int m, float lambda,
-                          hipStream_t st) {
+                          const float* dvbar, float* dDk, const float* dkpool, LmPool pl, int saved, int BH, int n,
+                          int d, int m, float lambda, hipStream_t st) {
     const float ks = kscale_of(lambda), il = 1.f / lambda;
     dim3 grid((n + 255) / 256, BH);
     if (d == 32)
-        hipLaunchKernelGGL((bwd_key_kernel<32>), grid, dim3(256), 0, st, K, V, dK, dV, qt, dU, dvbar, dDk, saved, n, m,
-                           ks, il);
+        hipLaunchKernelGGL((bwd_key_kernel<32>), grid, dim3(256), 0, st, K, V, dK, dV, qt, dU, dvbar, dDk, dkpool, pl,
+                           saved, n, m, ks, il);
     else
-        hipLaunchKernelGGL((bwd_key_kernel<64>), grid, dim3(256), 0, st, K, V, dK, dV, qt, dU, dvbar, dDk, saved, n, m,
-                           ks, il);
+        hipLaunchKernelGGL((bwd_key_kernel<64>), grid, dim3(256), 0, st, K, V, dK, dV, qt, dU, dvbar, dDk, dkpool, pl,
+                           saved, n, m, ks, il);
     return hipGetLastError();
 }
 
@@ -1127,10 +1133,9 @@ hipError_t launch_bwd_key_lm(const float* K, const float* qt, const float* dDk, 
     return hipGetLastError();
 }
 
-hipError_t launch_bwd_pool(float* dQ, float* dK, const float* dqtW, const float* dktW, const float* dqt_part,
-                           const float* dkt_part, int BH, int n, int d, int m, int nlc, LmPool pl, hipStream_t st) {
-    hipLaunchKernelGGL(bwd_pool_kernel, dim3(m, BH), dim3(256), 0, st, dQ, dK, dqtW, dktW, dqt_part, dkt_part, n, d,
-                       m, nlc, pl);
+hipError_t launch_bwd_pool(float* dQ, const float* dqtW, const float* dqt_part, int BH, int n, int d, int m, int nlc,
+                           LmPool pl, hipStream_t st) {
+    hipLaunchKernelGGL(bwd_pool_kernel, dim3(m, BH), dim3(256), 0, st, dQ, dqtW, dqt_part, n, d, m, nlc, pl);
     return hipGetLastError();
 }
 

@@ -64,7 +64,7 @@ struct FastPlan {
 struct Plan {
     size_t qt, kt, vseg, Upart, Xs, cinfo, U, M, vbar;                   // forward
     size_t Aq, dDq, rs, dYd, dvbar_part, dM_part, dkt_part, dU, dvbar,   // backward
-        dqtW, dktW, dDk, dqt_part;
+        dqtW, dkpool, dDk, dqt_part;
     size_t wQ, wK, wV, wG, gQ, gK, gV;   // bf16 backward: fp32 copies of the inputs, fp32 gradients
     size_t E;                            // convolution branch, forward: DWC(V) + bias [BH][n][d]
     size_t mvec;                         // landmark-space normalisation: [BH][2][d]
@@ -136,7 +136,7 @@ Plan make_plan(int BH, int n, int d, int m, int T, bool bwd, bool bf16 = false, 
         p.dU = c.take(bh * m * d1 * f);
         p.dvbar = c.take(bh * d * f);
         p.dqtW = c.take(bh * m * d * f);
-        p.dktW = c.take(bh * m * d * f);
+        p.dkpool = c.take(bh * m * d * f);
         p.dDk = c.take(bh * n * 64 * f);
         p.dqt_part = c.take(bh * p.nlc * m * d * f);
         if (bf16) {
@@ -501,15 +501,16 @@ int lapattn_backward(const void* Q, const void* K, const void* V, const void* dO
             return lapattn::launch_bwd_ns(at<float>(ws, p.qt), at<float>(ws, p.kt), at<double>(ws, p.Xs),
                                           at<double>(ws, p.cinfo), at<float>(ws, p.U), at<float>(ws, p.dM_part),
                                           at<float>(ws, p.dvbar_part), at<float>(ws, p.dU), at<float>(ws, p.dvbar),
-                                          at<float>(ws, p.dqtW), at<float>(ws, p.dktW), at<float>(ws, p.p0_part),
-                                          whiten, mspace ? 1 : 0, BH, H, n, d, m, ns_iters, (double)lambda,
+                                          at<float>(ws, p.dqtW), at<float>(ws, p.dkpool), at<float>(ws, p.dkt_part), pl,
+                                          at<float>(ws, p.p0_part), whiten, mspace ? 1 : 0, BH, H, n, d, m, ns_iters,
+                                          (double)lambda,
                                           (double)eps, p.nlc, p.nqb, p.MP, st);
         });
         if (e != hipSuccess) return LAPATTN_ERR_HIP;
         e = run_named(rec, "bwd_key", [&] {
             return lapattn::launch_bwd_key(k, v, dk, dv, at<float>(ws, p.qt), at<float>(ws, p.dU),
-                                           at<float>(ws, p.dvbar), at<float>(ws, p.dDk), saved ? 1 : 0, BH, n, d, m,
-                                           lambda, st);
+                                           at<float>(ws, p.dvbar), at<float>(ws, p.dDk), at<float>(ws, p.dkpool), pl,
+                                           saved ? 1 : 0, BH, n, d, m, lambda, st);
         });
         if (e != hipSuccess) return LAPATTN_ERR_HIP;
         e = run_named(rec, "bwd_key_lm", [&] {
@@ -518,8 +519,7 @@ int lapattn_backward(const void* Q, const void* K, const void* V, const void* dO
         });
         if (e != hipSuccess) return LAPATTN_ERR_HIP;
         e = run_named(rec, "bwd_pool", [&] {
-            return lapattn::launch_bwd_pool(dq, dk, at<float>(ws, p.dqtW), at<float>(ws, p.dktW),
-                                            at<float>(ws, p.dqt_part), at<float>(ws, p.dkt_part), BH, n, d, m, p.nlc,
+            return lapattn::launch_bwd_pool(dq, at<float>(ws, p.dqtW), at<float>(ws, p.dqt_part), BH, n, d, m, p.nlc,
                                             pl, st);
         });
         if (e != hipSuccess) return LAPATTN_ERR_HIP;

@@ -65,28 +65,30 @@ hipError_t launch_bwd_query_lm(const float* Q, const float* dO, const float* kt,
                                float* dM_part, float* dkt_part,
                                int BH, int n, int d, int m, int chunk, int nlc, hipStream_t st);
 
-// Newton-Schulz backward: dU [BH][m][d+1], dvbar [BH][d], and the K_LL gradient
-// mapped to the landmarks, dqtW, dktW [BH][m][d].
+// Newton-Schulz backward: dU [BH][m][d+1], dvbar [BH][d], the K_LL gradient mapped to the
+// query landmarks, dqtW [BH][m][d], and the whole key-landmark gradient over each landmark's
+// token count, dkpool [BH][m][d] = (K_LL term + the query-side partials dkt_part) / |S_l|.
 hipError_t launch_bwd_ns(const float* qt, const float* kt, const double* Xs, const double* cinfo,
                          const float* U, const float* dM_part, const float* dvbar_part,
-                         float* dU, float* dvbar, float* dqtW, float* dktW,
+                         float* dU, float* dvbar, float* dqtW, float* dkpool, const float* dkt_part, LmPool pl,
                          const float* p0_part, const float* whiten, int mspace,
                          int BH, int H, int n, int d, int m, int T, double lambda, double eps,
                          int nlc, int nqb, int MP, hipStream_t st);
 
-// Key-major pass: direct dK, final dV, and dDk = -B dB / lambda ([BH][n][m]).  saved: dDk holds
-// B's rows from the forward on entry (launch_key_summary's Bsave) instead of being recomputed.
+// Key-major pass: final dK (the direct term plus dkpool of the key's landmark), final dV, and
+// dDk = -B dB / lambda ([BH][n][m]).  saved: dDk holds B's rows from the forward on entry
+// (launch_key_summary's Bsave) instead of being recomputed.
 hipError_t launch_bwd_key(const float* K, const float* V, float* dK, float* dV,
-                          const float* qt, const float* dU, const float* dvbar, float* dDk, int saved,
-                          int BH, int n, int d, int m, float lambda, hipStream_t st);
+                          const float* qt, const float* dU, const float* dvbar, float* dDk, const float* dkpool,
+                          LmPool pl, int saved, int BH, int n, int d, int m, float lambda, hipStream_t st);
 
 // Landmark-major pass over keys: partial dqt [BH][nlc][m][d].
 hipError_t launch_bwd_key_lm(const float* K, const float* qt, const float* dDk, float* dqt_part,
                              int BH, int n, int d, int m, int chunk, int nlc, hipStream_t st);
 
-// Landmark-mean backward: dQ_i += dqt_{l(i)} / |S_l|, dK_j += dkt_{l(j)} / |S_l|.
-hipError_t launch_bwd_pool(float* dQ, float* dK, const float* dqtW, const float* dktW,
-                           const float* dqt_part, const float* dkt_part,
+// Landmark-mean backward of the queries: dQ_i += dqt_{l(i)} / |S_l| (dqt = dqtW + the key-side
+// partials); the keys' share is added by launch_bwd_key.
+hipError_t launch_bwd_pool(float* dQ, const float* dqtW, const float* dqt_part,
                            int BH, int n, int d, int m, int nlc, LmPool pl, hipStream_t st);
 
 // bf16 backward: the four inputs widened to fp32 (exact), the three fp32 gradients rounded to

@@ -409,8 +409,10 @@ __global__ __launch_bounds__(256) void query_out_kernel(const float* __restrict_
     constexpr int NCH = D / 32;
     constexpr int CB = D / 32;             // 32-column blocks of the output
     constexpr int TP = 33;   // one half (32 landmarks) of the tile and a zero column
-    // MFMA A operand of landmark pair s, column block cb: lane j + 32 k holds M[2s + k][32 cb + j]
-    __shared__ __attribute__((aligned(16))) float sMT[32 * CB * 64];
+    // MFMA A operand of pair s of the current 32-landmark range (staged per range, 4 KB at d = 32,
+    // so that four blocks share a compute unit), column block cb: lane j + 32 k holds
+    // M[32 hh + 2s + k][32 cb + j]
+    __shared__ __attribute__((aligned(16))) float sMT[16 * CB * 64];
     __shared__ float sMo[64];
     __shared__ float sVb[D];
     __shared__ float sMb[NORM == NORM_MSPACE ? D : 1];
@@ -420,12 +422,14 @@ __global__ __launch_bounds__(256) void query_out_kernel(const float* __restrict_
     // replaced by 1/m (so that s_i becomes the landmark mean of a_i), and the vectors
     // sum_l w_l M_l and (1/m) sum_l M_l from mvec
     const float* wl = (NORM == NORM_MSPACE && whiten) ? whiten + (size_t)(h % H) * m : nullptr;
-    for (int e = tid; e < 32 * CB * 64; e += 256) {
-        const int s = e / (CB * 64), cb = (e / 64) % CB, ln = e % 64;
-        const int lm = 2 * s + ln / 32;
-        const float wv = wl && lm < m ? wl[lm] : 1.f;
-        sMT[e] = (lm < m) ? wv * M[((size_t)h * m + lm) * D1 + 32 * cb + ln % 32] : 0.f;
-    }
+    auto stage = [&](int hh) {
+        for (int e = tid; e < 16 * CB * 64; e += 256) {
+            const int s = 16 * hh + e / (CB * 64), cb = (e / 64) % CB, ln = e % 64;
+            const int lm = 2 * s + ln / 32;
+            const float wv = wl && lm < m ? wl[lm] : 1.f;
+            sMT[e] = (lm < m) ? wv * M[((size_t)h * m + lm) * D1 + 32 * cb + ln % 32] : 0.f;
+        }
+    };
     if (tid < 64) {
         if (NORM == NORM_MSPACE) sMo[tid] = (tid < m) ? 1.f / (float)m : 0.f;
         else sMo[tid] = (tid < m) ? M[((size_t)h * m + tid) * D1 + D] : 0.f;
@@ -488,6 +492,9 @@ __global__ __launch_bounds__(256) void query_out_kernel(const float* __restrict_
         __builtin_amdgcn_wave_barrier();
         if (Asave) store_half_rows(Asave + (size_t)h * n * 64, tile, i0, n, 32 * hh, mh);   // A's rows for the backward
         const int npair = (mh + 1) / 2;
+        __syncthreads();   // the last range's operands are read by every wave
+        stage(hh);
+        __syncthreads();
 #pragma unroll 2
         for (int pl = 0; pl < npair; ++pl) {
             const int p = 16 * hh + pl;   // landmark pair of the whole tile
@@ -496,7 +503,7 @@ __global__ __launch_bounds__(256) void query_out_kernel(const float* __restrict_
             const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x0), __float_as_uint(x1), false, false);
 #pragma unroll
             for (int cb = 0; cb < CB; ++cb) {
-                const float av = sMT[(p * CB + cb) * 64 + l];
+                const float av = sMT[(pl * CB + cb) * 64 + l];
 #pragma unroll
                 for (int qb = 0; qb < 2; ++qb)
                     acc[qb][cb] =

@@ -23,7 +23,8 @@
  *   DWC(V)             the depth-wise convolution term of Eq. (7)  (R14), a separate
  *                      function: the caller adds it to Z V
  *   backward           chain rule through all of the above; kernel gradient
- *                      dk/dx = -(1/lambda) sign(x-y) k            App. A (R8)
+ *                      dk/dx = -(1/lambda) sign(x-y) k            App. A (R8), the sign
+ *                      decided with the landmark mean y rounded to fp32 (R16)
  */
 #include "lapattn_oracle.h"
 
@@ -43,6 +44,13 @@ int lapattn_oracle_threads(void) {
 }
 
 static double sgn(double x) { return (double)((x > 0) - (x < 0)); }
+
+/* R16: the backward decides sign(x - y) of the kernel gradient (App. A) with the landmark
+ * mean y rounded to fp32, the precision in which the kernels hold the landmarks (the paper
+ * fixes none).  The sign is a decision taken by floating point: where a token coordinate lies
+ * within the rounding of a landmark mean, the two choices are the two one-sided derivatives,
+ * and both sides must take the same one.  Every other step stays in fp64. */
+static double lm32(double y) { return (double)(float)y; }
 
 double lapattn_oracle_kernel(const double* x, const double* y, int d, double lambda) {
     double dist = 0.0;
@@ -478,7 +486,7 @@ static void head_backward(const double* q, const double* k, const double* v, con
         for (int c = 0; c < d; ++c) {
             double t = 0.0;
             for (int l = 0; l < m; ++l)
-                t += dD[(size_t)i * m + l] * sgn(q[(size_t)i * d + c] - s->kt[l * d + c]);
+                t += dD[(size_t)i * m + l] * sgn(q[(size_t)i * d + c] - lm32(s->kt[l * d + c]));
             dq[(size_t)i * d + c] = t;
         }
 #pragma omp parallel for schedule(static)
@@ -486,7 +494,7 @@ static void head_backward(const double* q, const double* k, const double* v, con
         for (int c = 0; c < d; ++c) {
             double t = 0.0;
             for (int i = 0; i < n; ++i)
-                t += dD[(size_t)i * m + l] * sgn(q[(size_t)i * d + c] - s->kt[l * d + c]);
+                t += dD[(size_t)i * m + l] * sgn(q[(size_t)i * d + c] - lm32(s->kt[l * d + c]));
             dkt[l * d + c] -= t;
         }
 
@@ -523,7 +531,7 @@ static void head_backward(const double* q, const double* k, const double* v, con
             double tv = 0.0, tk = 0.0;
             for (int a = 0; a < m; ++a) {
                 tv += s->Bm[(size_t)a * n + j] * dU[a * dv + c];
-                tk += dDB[(size_t)a * n + j] * sgn(s->qt[a * d + c] - k[(size_t)j * d + c]);
+                tk += dDB[(size_t)a * n + j] * sgn(lm32(s->qt[a * d + c]) - k[(size_t)j * d + c]);
             }
             dvv[(size_t)j * d + c] = tv + dvbar[c] / n;   /* vbar = (1/n) sum_j v_j */
             dk[(size_t)j * d + c] = -tk;
@@ -533,7 +541,7 @@ static void head_backward(const double* q, const double* k, const double* v, con
         for (int c = 0; c < d; ++c) {
             double t = 0.0;
             for (int j = 0; j < n; ++j)
-                t += dDB[(size_t)a * n + j] * sgn(s->qt[a * d + c] - k[(size_t)j * d + c]);
+                t += dDB[(size_t)a * n + j] * sgn(lm32(s->qt[a * d + c]) - k[(size_t)j * d + c]);
             dqt[a * d + c] += t;
         }
 
@@ -543,7 +551,7 @@ static void head_backward(const double* q, const double* k, const double* v, con
             double kab = s->Wk[a * m + b] - (a == b ? eps : 0.0);
             double g = -kab * dW[a * m + b] / lambda;
             for (int c = 0; c < d; ++c) {
-                double sg = sgn(s->qt[a * d + c] - s->kt[b * d + c]);
+                double sg = sgn(lm32(s->qt[a * d + c]) - lm32(s->kt[b * d + c]));
                 dqt[a * d + c] += g * sg;
                 dkt[b * d + c] -= g * sg;
             }

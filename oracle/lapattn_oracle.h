@@ -27,6 +27,8 @@
  *   R15 ORACLE_NORM_MSPACE: the landmark-space normalised embedding of Appendix B with its
  *       diagonal whitening w (per head, given; NULL = ones) in place of the query's landmark
  *       kernel vector: z_il = w_l (a_il - mean_l' a_il') + 1/m, Out_i = sum_l z_il M[l][:d]
+ *   R16 the backward decides each sign(x - y) of the kernel gradient with the landmark mean
+ *       y rounded to fp32 (the precision the GPU kernels hold landmarks in); the rest stays fp64
  */
 #ifndef LAPATTN_ORACLE_H
 #define LAPATTN_ORACLE_H

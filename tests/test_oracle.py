@@ -427,6 +427,40 @@ def test_backward_scale_term_is_needed(oracle_lib):
     assert fd_check(Q, K, V, dO, 8, 1.0, 0, oracle.NORM_NONE) < 1e-7   # T = 0: output = A W^T/c B V
 
 
+def test_backward_sign_decided_on_fp32_landmark_means(oracle_lib):
+    """R16: a key coordinate equal to the fp32 rounding of a query-landmark mean is a tie of
+    sign(qt - k) for the kernels, which hold landmarks in fp32.  Input A: queries 1 and 1 + 2^-23
+    (fp32 neighbours), mean 1 + 2^-24, which rounds (to even) to 1.0; key coordinate 1.0.
+    Input B: the second query is 1.0, so the mean is exactly 1.0 and the tie is real.  At a kink
+    the central difference gives the average of the one-sided derivatives, i.e. sign(0) = 0
+    (R8); the oracle's gradient at A must equal it up to the smooth change of 2^-24, while the
+    fp64 decision sign(2^-24) = 1 would differ by a whole one-sided term."""
+    lam, T, m = 1.5, 4, 2
+    Q = np.array([[1.0, 0.3], [1.0 + 2.0 ** -23, -0.2], [0.5, 0.7], [-0.1, 0.2]])[None, None]
+    K = np.array([[0.3, -0.4], [-0.6, 0.1], [1.0, 0.4], [0.2, -0.3]])[None, None]
+    rng = np.random.default_rng(41)
+    V = rng.standard_normal(Q.shape)
+    dO = rng.standard_normal(Q.shape)
+    assert np.float32((Q[0, 0, 0, 0] + Q[0, 0, 1, 0]) / 2) == np.float32(1.0)
+    QB = Q.copy()
+    QB[0, 0, 1, 0] = 1.0
+    h = 1e-7
+    loss = lambda q, k: (oracle.forward(q, k, V, m, lam, T) * dO).sum()
+    kp, km = K.copy(), K.copy()
+    kp[0, 0, 2, 0] += h
+    km[0, 0, 2, 0] -= h
+    fd_b = (loss(QB, kp) - loss(QB, km)) / (2 * h)
+    dK_a = oracle.backward(Q, K, V, dO, m, lam, T)[1][0, 0, 2, 0]
+    dK_b = oracle.backward(QB, K, V, dO, m, lam, T)[1][0, 0, 2, 0]
+    assert abs(dK_b - fd_b) < 1e-6 * max(1.0, abs(fd_b))
+    assert abs(dK_a - fd_b) < 1e-5 * max(1.0, abs(fd_b))
+    # the one-sided derivatives (above and below the kink) differ from the tie value
+    kp2 = K.copy()
+    kp2[0, 0, 2, 0] += 2 * h
+    right = (loss(QB, kp2) - loss(QB, kp)) / h
+    assert abs(right - fd_b) > 1e-3
+
+
 # ----------------------------------------------------------------------------- 2-D windows
 
 def window_order(hp, wp, r):

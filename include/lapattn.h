@@ -150,8 +150,10 @@ int lapattn_forward(const void* Q, const void* K, const void* V, void* Out,
 /* Backward pass: dQ, dK, dV = gradients of sum(Out * dOut) with respect to
  * Q, K, V, through the landmark means, the three kernel blocks and every
  * Newton-Schulz update including the scale of X_0 (kernel gradient of App. A,
- * with sign(0) = 0; ties in the norm maxima go to the lowest index).  The
- * forward internals are recomputed; nothing is kept from a forward call.
+ * with sign(0) = 0 and each sign decided on the landmark means as held in fp32;
+ * ties in the norm maxima go to the lowest index).  Without opts->save the
+ * forward internals are recomputed here; with it (fp32 inputs) they are read from
+ * the workspace left by a lapattn_forward call with save set (see lapattn_opts).
  * dtype = LAPATTN_BF16 runs the fp32 computation on the exactly widened bf16
  * inputs (held in the workspace, which is correspondingly larger) and rounds the
  * three gradients to bf16 (nearest even); dQ, dK, dV are in the input dtype. */

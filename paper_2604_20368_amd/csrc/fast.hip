@@ -12,15 +12,22 @@
 //                    MFMA operand tiles with a power-of-two scale per column
 //   query2_kernel    Y = K_QL M (Eq. (8)) and the normalisation (Eq. (4) / Eq. (3))
 //
-// Distances.  Per head, with R = max(|Q|, |K|) over the head and S = 65535 / (2R), every
-// coordinate x becomes u(x) = rint((x + R) S) in [0, 65535] (v_cvt_pknorm_u16_f32 of
-// (x + R) / (2R), two coordinates per instruction).  Then
-// sum_c |u(x_c) - u(y_c)| = S ||x - y||_1 + e with |e| <= d (each rounding moves a
-// coordinate by at most 1/2 a step), so the distance error is at most d / S = 2 R d / 65535.
+// Distances.  Per head, a range R covering every landmark coordinate (below) and
+// S = 65535 / (2R): a coordinate x becomes u(x) = rint((clamp(x, -R, R) + R) S) in [0, 65535]
+// (v_cvt_pknorm_u16_f32 of (x + R) / (2R), which saturates, two coordinates per instruction).
+// For a token x and a landmark y (|y_c| <= R for every c),
+//   ||x - y||_1 = ||clamp(x) - y||_1 + E(x),  E(x) = sum_c max(|x_c| - R, 0),
+// exactly: a coordinate beyond R lies on the far side of every landmark coordinate.  So
+// sum_c |u(x_c) - u(y_c)| = S ||clamp(x) - y||_1 + e with |e| <= d (each rounding moves a
+// coordinate by at most 1/2 a step): the error of the clamped part is at most 2 R d / 65535,
+// and E(x) is formed in fp32 once per token and enters the exponent as a per-token bias.
+// R = max(landmark max, min(head max, 2 x the median over landmarks of their tokens' max));
+// a head without far tokens keeps R = its max |Q|, |K| and E = 0, and one or a few outlier
+// tokens no longer coarsen every distance of their head.
 // v_sad_u16 adds |a.lo - b.lo| + |a.hi - b.hi| to an accumulator: two coordinates per lane
 // and instruction, exact integer arithmetic.  The accumulator starts at the bit pattern of
 // 2^23, so after the sum it reads as the float 2^23 + D (D < 2^23 for d <= 64), and one fma
-// maps it to the exp2 argument -D log2(e) / (lambda S).
+// maps it to the exp2 argument -(D / S + E) log2(e) / lambda.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -46,6 +53,21 @@ __device__ __forceinline__ uint32_t fix2(float x0, float x1, float inv2R) {
 // A packed bf16 pair (one dword) to the fixed-point frame.
 __device__ __forceinline__ uint32_t fix2_bf16(uint32_t w, float inv2R) {
     return fix2(bf16_lo(w), bf16_hi(w), inv2R);
+}
+
+// exp2 bias of a token whose coordinates may lie beyond the range R: ebias + xscale E(x) with
+// E(x) = sum_c max(|x_c|, R) - d R = sum_c max(|x_c| - R, 0) (the row as D8 16-byte chunks of
+// bf16 pairs).
+template <int D8>
+__device__ __forceinline__ float excess_bias(const uint4 (&row)[D8], float R, float xscale, float ebias) {
+    float e = 0.f;
+#pragma unroll
+    for (int c8 = 0; c8 < D8; ++c8) {
+        const uint32_t wd[4] = {row[c8].x, row[c8].y, row[c8].z, row[c8].w};
+#pragma unroll
+        for (int t = 0; t < 4; ++t) e += fmaxf(fabsf(bf16_lo(wd[t])), R) + fmaxf(fabsf(bf16_hi(wd[t])), R);
+    }
+    return fmaf(e - (float)(8 * D8) * R, xscale, ebias);
 }
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
@@ -230,11 +252,11 @@ __device__ __forceinline__ void load_row(uint32_t (&t)[D2], const uint32_t* __re
     for (int c = 0; c < D2; ++c) t[c] = row[c];
 }
 
-// The kernel value of one (lane's key, landmark row) pair: two sad chains over the even and
-// odd coordinate pairs; the first sad (the wait point for `t`) is issued before the scalar
-// loads of the next row, which go into `nt`.
+// The exp2 argument (lap_arg) and the kernel value (lap_row) of one (lane's token, landmark
+// row) pair: two sad chains over the even and odd coordinate pairs; the first sad (the wait
+// point for `t`) is issued before the scalar loads of the next row, which go into `nt`.
 template <int D2>
-__device__ __forceinline__ float lap_row(const uint32_t (&kf)[D2], const uint32_t (&t)[D2], uint32_t (&nt)[D2],
+__device__ __forceinline__ float lap_arg(const uint32_t (&kf)[D2], const uint32_t (&t)[D2], uint32_t (&nt)[D2],
                                          const uint32_t* __restrict__ next_row, float esc, float ebias) {
     uint32_t u0 = __builtin_amdgcn_sad_u16(kf[0], t[0], 0x4B000000u);
     __builtin_amdgcn_sched_barrier(0);
@@ -246,16 +268,28 @@ __device__ __forceinline__ float lap_row(const uint32_t (&kf)[D2], const uint32_
         u0 = __builtin_amdgcn_sad_u16(kf[c], t[c], u0);
         u1 = __builtin_amdgcn_sad_u16(kf[c + 1], t[c + 1], u1);
     }
-    return __builtin_amdgcn_exp2f(fmaf(__uint_as_float(u0 + u1), esc, ebias));
+    return fmaf(__uint_as_float(u0 + u1), esc, ebias);
+}
+template <int D2>
+__device__ __forceinline__ float lap_row(const uint32_t (&kf)[D2], const uint32_t (&t)[D2], uint32_t (&nt)[D2],
+                                         const uint32_t* __restrict__ next_row, float esc, float ebias) {
+    return __builtin_amdgcn_exp2f(lap_arg<D2>(kf, t, nt, next_row, esc, ebias));
 }
 
 // ------------------------------------------------------------------------------------------
 // Per-head frame and Newton-Schulz solve.  grid (BH), 512 threads (8 waves).
 //
-// Frame: frame[h] = {R, 1/(2R), escale = -log2(e) / (lambda S), vscale}; R is NaN when Q, K or
-// V hold a non-finite value (the outputs of that head are then NaN, as the plain computation
-// gives).  qfix/kfix[h][a][c/2] = u(x_{a,c}) | u(x_{a,c+1}) << 16 for landmarks a < 64 (zero
-// rows >= m).  vbar[h] = mean of the values; vscale = 2^-e keeps fp16 copies of V below 2^14.
+// Frame: frame[h][0..7] = {R, 1/(2R), escale = -log2(e) / (lambda S), vscale,
+// xscale = -log2(e) / lambda, clamped, rho, 0}; R is NaN when Q, K or V hold a non-finite value
+// (the outputs of that head are then NaN, as the plain computation gives); clamped = 1 when
+// some |x| of Q or K exceeds R (the key and query sides then add the excess E(x) of each
+// token).  qfix/kfix[h][a][c/2] = u(x_{a,c}) | u(x_{a,c+1}) << 16 for landmarks a < 64 (zero
+// rows >= m); kcen[h][c/2] = the key-landmark codes' centre c (the rounded mean over the landmarks
+// of each coordinate), rho = max_l sum_c |u(kt_{l,c}) - c_c| (code units): by the triangle
+// inequality every query's code distance to landmark l is at least its distance to c minus rho.
+// vbar[h] = mean of the values; vscale = 2^e puts the largest |v| of the head in
+// [2^13, 2^14), so that the fp16 copies of V (exact for bf16 values in fp16's normal range)
+// neither overflow nor fall into fp16's subnormal range for small values.
 //
 // Solve (Algorithm 2): W = K_LL + eps I padded to 64 x 64 (lane = row a, eight columns b per
 // wave, v_sad_u16 against the key-landmark rows read by the whole wave at one LDS address);
@@ -367,8 +401,8 @@ template <int D>
 __global__ __launch_bounds__(kSolveThreads) void frame_ns_kernel(
     const float* __restrict__ qt, const float* __restrict__ kt, const double* __restrict__ vseg,
     const float* __restrict__ segmax, const float* __restrict__ vsegmax, float* __restrict__ frame,
-    uint32_t* __restrict__ qfix, uint32_t* __restrict__ kfix, float* __restrict__ vbar, float* __restrict__ XT,
-    float* __restrict__ cinfo, int n, int m, float lambda, int T, float eps) {
+    uint32_t* __restrict__ qfix, uint32_t* __restrict__ kfix, uint32_t* __restrict__ kcen, float* __restrict__ vbar,
+    float* __restrict__ XT, float* __restrict__ cinfo, int n, int m, float lambda, int T, float eps) {
     constexpr int NT = kSolveThreads;
     constexpr int NW = NT / 64;          // 8 waves
     constexpr int D2 = D / 2;
@@ -397,7 +431,7 @@ __global__ __launch_bounds__(kSolveThreads) void frame_ns_kernel(
     float* part = reinterpret_cast<float*>(ETh(0));          // 2 x NW x 64 floats
     double* vpart = reinterpret_cast<double*>(ETh(0)) + 512;  // G x D doubles, after part
     float* sWf = reinterpret_cast<float*>(ETh(1));
-    static_assert(2 * 64 * D2 * 4 <= 2 * 64 * kLP * 2, "landmark tables exceed Z^T[1]");
+    static_assert(2 * 64 * D2 * 4 + D2 * 4 <= 2 * 64 * kLP * 2, "landmark tables and centre exceed Z^T[1]");
     static_assert(2 * NW * 64 * 4 <= 512 * 8 && 512 * 8 + G * D * 8 <= 2 * 64 * kLP * 2, "partials exceed E^T[0]");
     static_assert(64 * WP * 4 <= 2 * 64 * kLP * 2, "fp32 W exceeds E^T[1]");
     static_assert(G * D == NT && G * LPG == 64, "value partials");
@@ -427,21 +461,47 @@ __global__ __launch_bounds__(kSolveThreads) void frame_ns_kernel(
     float sa = segmax[(size_t)h * m + tm], sb = vsegmax[(size_t)h * m + tm];
     if (tid >= m) sa = sb = 0.f;
     vpart[tid] = vs;   // [g][c]
+    {
+        // largest landmark coordinate (rows past m were loaded from row 0 and are left out)
+        float lmx = 0.f;
+#pragma unroll
+        for (int r = 0; r < WPT; ++r)
+            if ((tid + NT * r) / D2 < m)
+                lmx = fmaxf(lmx, fmaxf(fmaxf(fabsf(q0[r]), fabsf(q1[r])), fmaxf(fabsf(k0[r]), fabsf(k1[r]))));
+        lmx = wave_max_dpp(lmx);
+        if (l == 0) sred[48 + w] = lmx;
+    }
+    __syncthreads();
     if (w == 0) {
         const bool bad = __any(!(isfinite(sa) && isfinite(sb)));
-        float R = wave_max_dpp(sa);
+        const float xmax = wave_max_dpp(sa);
         const float vm = wave_max_dpp(sb);
+        // median of the landmarks' token maxima (lane l < m holds landmark l's): the value of
+        // rank (m - 1) / 2, ties ranked by landmark index
+        int rank = 0;
+        for (int j = 0; j < m; ++j) {
+            const float sj = __shfl(sa, j, 64);
+            rank += (sj < sa || (sj == sa && j < l)) ? 1 : 0;
+        }
+        const unsigned long long pick = __ballot(l < m && rank == (m - 1) / 2);
+        const float med = pick ? __shfl(sa, (int)__builtin_ctzll(pick), 64) : xmax;   // none: a NaN maximum
+        float lmax = sred[48];
+#pragma unroll
+        for (int i = 1; i < NW; ++i) lmax = fmaxf(lmax, sred[48 + i]);
         if (l == 0) {
-            if (R == 0.f) R = 1.f;
+            float R = fmaxf(lmax, fminf(xmax, 2.f * med));
+            if (!(R > 0.f)) R = 1.f;
             const float S = (float)(65535.0 / (2.0 * (double)R));
-            float vscale = 1.f;
-            if (vm > 16384.f) vscale = exp2f(-ceilf(log2f(vm / 16384.f)));
+            const float vscale = (vm > 0.f && isfinite(vm)) ? ldexpf(1.f, 13 - ilogbf(vm)) : 1.f;
             const float inv2R = (float)(0.5 / (double)R);
             const float escale = (float)(-1.4426950408889634 / ((double)lambda * (double)S));
-            frame[h * 4 + 0] = bad ? __builtin_nanf("") : R;
-            frame[h * 4 + 1] = inv2R;
-            frame[h * 4 + 2] = escale;
-            frame[h * 4 + 3] = vscale;
+            frame[h * 8 + 0] = bad ? __builtin_nanf("") : R;
+            frame[h * 8 + 1] = inv2R;
+            frame[h * 8 + 2] = escale;
+            frame[h * 8 + 3] = vscale;
+            frame[h * 8 + 4] = (float)(-1.4426950408889634 / (double)lambda);
+            frame[h * 8 + 5] = xmax > R ? 1.f : 0.f;
+            frame[h * 8 + 7] = 0.f;
             sred[0] = inv2R;
             sred[1] = escale;
         }
@@ -468,6 +528,31 @@ __global__ __launch_bounds__(kSolveThreads) void frame_ns_kernel(
         sK[e] = uk;
     }
     __syncthreads();
+    if (w == 0) {
+        // centre of the key-landmark codes (per coordinate, the rounded mean over the m
+        // landmarks) and rho = the largest code distance of a landmark from it, for the query
+        // side's bound on each query's largest kernel value
+        uint32_t* scen = sK + 64 * D2;
+        if (l < D2) {
+            uint32_t slo = 0, shi = 0;
+            for (int a = 0; a < m; ++a) {
+                const uint32_t u = sK[a * D2 + l];
+                slo += u & 0xffffu;
+                shi += u >> 16;
+            }
+            const uint32_t cen = ((slo + m / 2) / m) | (((shi + m / 2) / m) << 16);
+            scen[l] = cen;
+            kcen[(size_t)h * D2 + l] = cen;
+        }
+        __builtin_amdgcn_wave_barrier();   // the wave's LDS requests complete in order
+        uint32_t dist = 0;
+        if (l < m) {
+#pragma unroll
+            for (int c2 = 0; c2 < D2; ++c2) dist = __builtin_amdgcn_sad_u16(sK[l * D2 + c2], scen[c2], dist);
+        }
+        const float rho = (float)__float_as_uint(wave_max_dpp(__uint_as_float(dist)));
+        if (l == 0) frame[h * 8 + 6] = rho;
+    }
 
     // ---- W[a][b] = k(qt_a, kt_b) (+ eps on the diagonal): lane a, columns b = BPW w..+BPW
     uint32_t qa[D2];
@@ -682,7 +767,9 @@ __device__ void key_role(int h, int kb, char* lds_raw, const uint16_t* __restric
     _Float16* const tiles = reinterpret_cast<_Float16*>(lds_raw);
     _Float16* sB = tiles + w * (2 * 64 * kLP);   // this wave's [a][j]
     _Float16* sV = sB + 64 * kLP;                 // this wave's [c][j]
-    const float inv2R = frame[h * 4 + 1], esc = frame[h * 4 + 2], vsc = frame[h * 4 + 3];
+    const float inv2R = frame[h * 8 + 1], esc = frame[h * 8 + 2], vsc = frame[h * 8 + 3];
+    const float R = frame[h * 8 + 0], xsc = frame[h * 8 + 4];
+    const bool clamped = frame[h * 8 + 5] != 0.f;
     const uint32_t* tab = qfix + (size_t)h * 64 * D2;
     const float ebias = -kTwo23 * esc;
     const int j_begin = kb * kpb, j_end = min(n, j_begin + kpb);
@@ -737,6 +824,8 @@ __device__ void key_role(int h, int kb, char* lds_raw, const uint16_t* __restric
                 kf[4 * c8 + 2] = fix2_bf16(kr[c8].z, inv2R);
                 kf[4 * c8 + 3] = fix2_bf16(kr[c8].w, inv2R);
             }
+            // the key's excess beyond the range enters the exponent (head-uniform branch)
+            const float kbias = clamped ? excess_bias<D8>(kr, R, xsc, ebias) : ebias;
             // The next tile's keys are fetched in D/8 column groups spread over the landmark
             // loop, so that the key stream reaches memory as a steady flow rather than one
             // burst per tile from every wave at once; its values follow after this tile's
@@ -755,8 +844,8 @@ __device__ void key_role(int h, int kb, char* lds_raw, const uint16_t* __restric
 #pragma unroll 1
                 for (int i = c8 * npairs / D8; i < (c8 + 1) * npairs / D8; ++i) {
                     const int pn = p + 1 < npairs ? p + 1 : 0;
-                    const float b0 = lap_row<D2>(kf, ta, tb, tab + (2 * p + 1) * D2, esc, ebias);
-                    const float b1 = lap_row<D2>(kf, tb, ta, tab + (2 * pn) * D2, esc, ebias);
+                    const float b0 = lap_row<D2>(kf, ta, tb, tab + (2 * p + 1) * D2, esc, kbias);
+                    const float b1 = lap_row<D2>(kf, tb, ta, tab + (2 * pn) * D2, esc, kbias);
                     const uint32_t v = pk_f16(b0, 2 * p + 1 < m ? b1 : 0.f) & vmask;
                     brow[(2 * p) * kLP] = (uint16_t)(v & 0xffffu);
                     brow[(2 * p + 1) * kLP] = (uint16_t)(v >> 16);
@@ -841,36 +930,50 @@ __global__ __launch_bounds__(256, 2) void key_kernel(const uint16_t* __restrict_
 
 // ------------------------------------------------------------------------------------------
 // U = sum over key chunks, M = X_T U, and the query side's copy of M, by column groups:
-// grid (NG, BH) with NG = D/8 + 1, 512 threads.  Group g < D/8 holds value columns 8g..8g+7,
-// group D/8 the ones column D.  M = X_T U is separable by columns, so each block sums only its
-// columns of the chunk partials (Upart[h][kb][c][a], four quarters of the chunks combined in a
-// fixed order) and forms only its columns of M.
+// grid (NG, BH) with NG = D/8 + 1, 576 threads (nine waves).  Group g < D/8 holds value columns
+// 8g..8g+7, group D/8 the ones column D.  M = X_T U is separable by columns, so each block sums
+// only its columns of the chunk partials (Upart[h][kb][c][a], four quarters of the chunks
+// combined in a fixed order) and forms only its columns of M.  A value group also sums the
+// ones column and forms M[.][D] (its ninth wave), so that with `center` (the inline
+// normalisation) its operand columns are M'[a][c] = M[a][c] - M[a][D] vbar[c], formed in fp32:
+// Y'_i = sum_l a_il M'_l = Y_i[:d] - s_i vbar, and the output Y'_i + vbar no longer takes the
+// difference of Y_i[:d] and s_i vbar after the fp16 rounding of M (terms that grow with n when
+// the kernel values are flat).
 // Value columns: fp16 MFMA operand tiles Mt[h][s][cb][lane][i] = M[16s + 8(lane/32) + i]
 // [32cb + lane%32] * 2^-e_g with mscale[h][g] = 2^e_g putting the group's largest magnitude in
 // [2^14, 2^15).  Ones column: Mones[h][a] = M[a][D] in fp32.
+constexpr int kMfinalThreads = 576;
+
 template <int D>
-__global__ __launch_bounds__(512) void mfinal_kernel(const float* __restrict__ Upart, const float* __restrict__ XT,
-                                                     _Float16* __restrict__ Mt, float* __restrict__ mscale,
-                                                     float* __restrict__ Mones, float* __restrict__ Mout, int m,
-                                                     int nkb, const float* __restrict__ whiten, int mspace, int H,
-                                                     float* __restrict__ mvec) {
+__global__ __launch_bounds__(kMfinalThreads) void mfinal_kernel(const float* __restrict__ Upart,
+                                                                const float* __restrict__ XT,
+                                                                _Float16* __restrict__ Mt, float* __restrict__ mscale,
+                                                                float* __restrict__ Mones, float* __restrict__ Mout,
+                                                                int m, int nkb, const float* __restrict__ whiten,
+                                                                int mspace, int H, float* __restrict__ mvec,
+                                                                const float* __restrict__ vbar, int center) {
     constexpr int D1 = D + 1;
     constexpr int CB = D / 32;
     constexpr int NG = D / 8 + 1;
+    constexpr int NI = 9 * 16;   // float4 items per chunk: nine columns of 64 rows
     __shared__ float sX[64 * 65];
-    __shared__ __attribute__((aligned(16))) float sU[8 * 64];   // [c][b]
+    __shared__ __attribute__((aligned(16))) float sU[9 * 64];   // [column][b]
     __shared__ __attribute__((aligned(16))) float sM[8 * 64];   // [c][a]
-    __shared__ __attribute__((aligned(16))) float4 red[3 * 128];
-    __shared__ float smx[8];
-    const int g = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, w = tid >> 6, l = tid & 63;
+    __shared__ __attribute__((aligned(16))) float4 red[3 * NI];
+    __shared__ float sMd[64];
+    __shared__ float smx[9];
+    const int g = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, w = tid / 64, l = tid & 63;
     const bool ones = g == NG - 1;
-    const int c0 = 8 * g, nc = ones ? 1 : 8;
-    // the group's nc * 64 floats of every chunk partial, as nc * 16 float4; the chunks in four
-    // quarters, eight loads in flight per thread
-    const int f = tid & 127, qq = tid >> 7;
+    const int c0 = 8 * g, nc = ones ? 1 : 8;   // operand columns of this group
+    const int ncol = ones ? 1 : 9;             // columns summed: the operand columns and column D
+    // item f: local column f / 16 (column D for local column 8, and in the ones group), rows
+    // 4 (f % 16) .. +3 of every chunk partial; the chunks in four quarters, eight loads in flight
+    const int f = tid % NI, qq = tid / NI;
+    const int cl = f >> 4;
+    const int gc = (ones || cl == 8) ? D : c0 + cl;
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (f < nc * 16) {
-        const float4* src = reinterpret_cast<const float4*>(Upart + ((size_t)h * nkb * D1 + c0) * 64) + f;
+    if (cl < ncol) {
+        const float4* src = reinterpret_cast<const float4*>(Upart + ((size_t)h * nkb * D1 + gc) * 64) + (f & 15);
         const int k_lo = qq * nkb / 4, k_hi = (qq + 1) * nkb / 4;
         for (int k0 = k_lo; k0 < k_hi; k0 += 8) {
             float4 t[8];
@@ -883,23 +986,27 @@ __global__ __launch_bounds__(512) void mfinal_kernel(const float* __restrict__ U
             }
         }
     }
-    for (int e = tid; e < 4096; e += 512) sX[(e >> 6) * 65 + (e & 63)] = XT[(size_t)h * 4096 + e];
-    if (qq > 0 && f < nc * 16) red[(qq - 1) * 128 + f] = acc;
+    for (int e = tid; e < 4096; e += kMfinalThreads) sX[(e >> 6) * 65 + (e & 63)] = XT[(size_t)h * 4096 + e];
+    if (qq > 0 && cl < ncol) red[(qq - 1) * NI + f] = acc;
     __syncthreads();
-    if (qq == 0 && f < nc * 16) {
-        const float4 r1 = red[f], r2 = red[128 + f], r3 = red[256 + f];
+    if (qq == 0 && cl < ncol) {
+        const float4 r1 = red[f], r2 = red[NI + f], r3 = red[2 * NI + f];
         reinterpret_cast<float4*>(sU)[f] = make_float4(((acc.x + r1.x) + r2.x) + r3.x, ((acc.y + r1.y) + r2.y) + r3.y,
                                                        ((acc.z + r1.z) + r2.z) + r3.z, ((acc.w + r1.w) + r2.w) + r3.w);
     }
     __syncthreads();
-    // M[a][c0 + cc] = sum_b X_T[a][b] U[b][c0 + cc]: thread (cc = tid/64, a = tid%64)
+    // M[a][col] = sum_b X_T[a][b] U[b][col]: thread (column w, a = l)
+    float t = 0.f;
+    if (w < ncol) {
+#pragma unroll 16
+        for (int b = 0; b < 64; ++b) t = fmaf(sX[l * 65 + b], sU[w * 64 + b], t);
+        if (w == 8) sMd[l] = t;   // M[a][D] in a value group
+    }
+    __syncthreads();
     // landmark-space normalisation: the operand rows are w_l M[l] (whitening w, ones when
     // whiten is NULL), and each value column also gives sum_l w_l M[l][c] and (1/m) sum_l M[l][c]
     float mv = 0.f;
     if (w < nc) {
-        float t = 0.f;
-#pragma unroll 16
-        for (int b = 0; b < 64; ++b) t = fmaf(sX[l * 65 + b], sU[w * 64 + b], t);
         if (l < m) Mout[((size_t)h * m + l) * D1 + c0 + w] = t;
         if (mspace && !ones) {
             const float tv = l < m ? t : 0.f;
@@ -917,6 +1024,7 @@ __global__ __launch_bounds__(512) void mfinal_kernel(const float* __restrict__ U
             }
             t = tw;
         } else {
+            if (center && !ones) t = l < m ? fmaf(-sMd[l], vbar[(size_t)h * D + c0 + w], t) : 0.f;
             sM[w * 64 + l] = t;
         }
         mv = fabsf(t);
@@ -926,7 +1034,7 @@ __global__ __launch_bounds__(512) void mfinal_kernel(const float* __restrict__ U
     __syncthreads();
     float mxg = smx[0];
 #pragma unroll
-    for (int i = 1; i < 8; ++i) mxg = fmaxf(mxg, smx[i]);
+    for (int i = 1; i < 9; ++i) mxg = fmaxf(mxg, smx[i]);
     const int e = pow2_exp(mxg);
     if (tid == 0) mscale[h * NG + g] = ldexpf(1.f, e);
     if (ones) {   // rows >= m are zero; the landmark-space form weights every landmark by 1/m
@@ -953,10 +1061,13 @@ __global__ __launch_bounds__(512) void mfinal_kernel(const float* __restrict__ U
 // MFMA (M's value columns as fp16 with a power-of-two scale per column group): the result
 // holds, per lane, 16 output columns of one query, so the normalisation and the bf16 stores
 // happen straight from registers.  The row sum s_i = sum_l a_il M[l][d] (the ones column) is
-// accumulated in fp32 in the landmark loop from the unrounded kernel values.
+// accumulated in fp32 in the landmark loop from the unrounded kernel values where the
+// normalisation needs it (row sums, landmark space); the inline form reads M centred by
+// mfinal_kernel, out_i = Y'_i + vbar.
 template <int D, int NORM>
 __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict__ Q, uint16_t* __restrict__ Out,
                                                      const uint32_t* __restrict__ kfix,
+                                                     const uint32_t* __restrict__ kcen,
                                                      const float* __restrict__ frame, const _Float16* __restrict__ Mt,
                                                      const float* __restrict__ mscale,
                                                      const float* __restrict__ Mones, const float* __restrict__ vbar,
@@ -990,7 +1101,10 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
         }
         if (tid < 64) sMo[tid] = Mones[(size_t)h * 64 + tid];
     }
-    const float R = frame[h * 4 + 0], inv2R = frame[h * 4 + 1], esc = frame[h * 4 + 2];
+    const float R = frame[h * 8 + 0], inv2R = frame[h * 8 + 1], esc = frame[h * 8 + 2];
+    const float xsc = frame[h * 8 + 4];
+    const bool clamped = frame[h * 8 + 5] != 0.f;
+    const float rho = frame[h * 8 + 6];
     const float ebias = -kTwo23 * esc;
     constexpr int NG = D / 8 + 1;
     float scv[D / 8];
@@ -1001,6 +1115,7 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
     const int i0 = qblk * 256 + w * 64;
     const int i = i0 + l;
     uint32_t qf[D2];
+    float qbias = ebias;   // with the query's excess beyond the range when the head has far tokens
     if (i < n) {
         const uint4* qr = reinterpret_cast<const uint4*>(Q + ((size_t)h * n + i) * D);
         uint4 raw[D8];
@@ -1013,27 +1128,41 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
             qf[4 * c8 + 2] = fix2_bf16(raw[c8].z, inv2R);
             qf[4 * c8 + 3] = fix2_bf16(raw[c8].w, inv2R);
         }
+        if (clamped) qbias = excess_bias<D8>(raw, R, xsc, ebias);
     } else {
 #pragma unroll
         for (int c = 0; c < D2; ++c) qf[c] = 0u;
     }
     // kernel values, two landmarks per fp16 pair register (landmarks >= m give 0); the
     // landmark rows come through scalar registers, the loads of each row issued right after
-    // the first use of the previous one (the table has 64 rows, zero past m)
+    // the first use of the previous one (the table has 64 rows, zero past m).
+    // Row shift: with the exp2 argument g_c of the query's distance to the landmarks' centre,
+    // every landmark's argument is at most g_c + rho |escale| (triangle inequality in code
+    // space), so the values are formed as exp2(g_l - sh) with sh = min(g_c + rho |escale|, 0):
+    // at most 1, and a far query's values stay in fp16's range instead of underflowing.  The
+    // factor f = exp2(sh) of the row is applied in fp32 in the epilogue (it cancels under the
+    // row-sum normalisation).
     uint32_t ah[32];
-    float srow = 0.f;   // s_i of this lane's query
+    float srow = 0.f;   // s_i of this lane's query (of the shifted values)
+    float fsh;          // exp2(sh)
     __syncthreads();    // sM, sMo, sVb
     {
         uint32_t ta[D2], tb[D2];
-        load_row<D2>(ta, tab);
+        load_row<D2>(tb, kcen + (size_t)h * D2);
+        const float gc = lap_arg<D2>(qf, tb, ta, tab, esc, qbias);   // issues landmark row 0 into ta
+        const float sh = fminf(fmaf(-esc, rho, gc), 0.f);
+        qbias -= sh;
+        fsh = __builtin_amdgcn_exp2f(sh);
 #pragma unroll
         for (int p = 0; p < 32; ++p) {
             if (2 * p < m) {
-                const float a0 = lap_row<D2>(qf, ta, tb, tab + (2 * p + 1) * D2, esc, ebias);
-                float a1 = lap_row<D2>(qf, tb, ta, tab + (p < 31 ? 2 * p + 2 : 63) * D2, esc, ebias);
+                const float a0 = lap_row<D2>(qf, ta, tb, tab + (2 * p + 1) * D2, esc, qbias);
+                float a1 = lap_row<D2>(qf, tb, ta, tab + (p < 31 ? 2 * p + 2 : 63) * D2, esc, qbias);
                 if (2 * p + 1 >= m) a1 = 0.f;
-                const float2 mo = *reinterpret_cast<const float2*>(&sMo[2 * p]);
-                srow = fmaf(a1, mo.y, fmaf(a0, mo.x, srow));
+                if (NORM == NORM_ROWSUM || NORM == NORM_MSPACE) {
+                    const float2 mo = *reinterpret_cast<const float2*>(&sMo[2 * p]);
+                    srow = fmaf(a1, mo.y, fmaf(a0, mo.x, srow));
+                }
                 ah[p] = pk_f16(a0, a1);
             } else {
                 ah[p] = 0u;
@@ -1054,6 +1183,7 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
     const int NSTEP = (m + 15) / 16;
     // s_i for the two 32-query halves in the output layout (lane l: query 32 qb + l%32)
     const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(srow), __float_as_uint(srow), false, false);
+    const auto sf = __builtin_amdgcn_permlane32_swap(__float_as_uint(fsh), __float_as_uint(fsh), false, false);
     const bool nan_head = !isfinite(R);
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
@@ -1062,12 +1192,12 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
         for (int s4 = 0; s4 < 4; ++s4)
             A[s4] = __builtin_bit_cast(h8_t, (uint4){ah[8 * s4 + 4 * qb], ah[8 * s4 + 4 * qb + 1],
                                                      ah[8 * s4 + 4 * qb + 2], ah[8 * s4 + 4 * qb + 3]});
-        const float si = __uint_as_float(sw[qb]);
+        const float si = __uint_as_float(sw[qb]), fi = __uint_as_float(sf[qb]);
         float tmul, tadd;   // o = y * tmul * scv[group] + tadd * vbar (+ mb, landmark-space form)
-        if (NORM == NORM_INLINE) { tmul = 1.f; tadd = 1.f - si; }
+        if (NORM == NORM_INLINE) { tmul = fi; tadd = 1.f; }   // M centred: y = Y[:d] - s vbar
         else if (NORM == NORM_ROWSUM) { tmul = 1.f / si; tadd = 0.f; }
-        else if (NORM == NORM_MSPACE) { tmul = 1.f; tadd = -si; }
-        else { tmul = 1.f; tadd = 0.f; }
+        else if (NORM == NORM_MSPACE) { tmul = fi; tadd = -si * fi; }
+        else { tmul = fi; tadd = 0.f; }
         uint16_t* stage = sOut + w * 32 * OP + (l & 31) * OP;
 #pragma unroll
         for (int cb = 0; cb < CB; ++cb) {
@@ -1146,15 +1276,15 @@ hipError_t launch_fast_pool(const void* Q, const void* K, const void* V, float* 
 }
 
 hipError_t launch_fast_frame_ns(const float* qt, const float* kt, const double* vseg, const float* segmax,
-                                const float* vsegmax, float* frame, uint32_t* qfix, uint32_t* kfix, float* vbar,
-                                float* XT, float* cinfo, int BH, int n, int d, int m, float lambda, int T, float eps,
-                                hipStream_t st) {
+                                const float* vsegmax, float* frame, uint32_t* qfix, uint32_t* kfix, uint32_t* kcen,
+                                float* vbar, float* XT, float* cinfo, int BH, int n, int d, int m, float lambda, int T,
+                                float eps, hipStream_t st) {
     if (d == 32)
         hipLaunchKernelGGL(frame_ns_kernel<32>, dim3(BH), dim3(kSolveThreads), 0, st, qt, kt, vseg, segmax, vsegmax, frame,
-                           qfix, kfix, vbar, XT, cinfo, n, m, lambda, T, eps);
+                           qfix, kfix, kcen, vbar, XT, cinfo, n, m, lambda, T, eps);
     else
         hipLaunchKernelGGL(frame_ns_kernel<64>, dim3(BH), dim3(kSolveThreads), 0, st, qt, kt, vseg, segmax, vsegmax, frame,
-                           qfix, kfix, vbar, XT, cinfo, n, m, lambda, T, eps);
+                           qfix, kfix, kcen, vbar, XT, cinfo, n, m, lambda, T, eps);
     return hipGetLastError();
 }
 
@@ -1172,24 +1302,25 @@ hipError_t launch_fast_key(const void* K, const void* V, const uint32_t* qfix, c
 
 hipError_t launch_fast_mfinal(const float* Upart, const float* XT, _Float16* Mt, float* mscale, float* Mones,
                               float* M, int BH, int d, int m, int nkb, const float* whiten, int mspace, int H,
-                              float* mvec, hipStream_t st) {
+                              float* mvec, const float* vbar, int center, hipStream_t st) {
     if (d == 32)
-        hipLaunchKernelGGL(mfinal_kernel<32>, dim3(32 / 8 + 1, BH), dim3(512), 0, st, Upart, XT, Mt, mscale, Mones, M, m,
-                           nkb, whiten, mspace, H, mvec);
+        hipLaunchKernelGGL(mfinal_kernel<32>, dim3(32 / 8 + 1, BH), dim3(kMfinalThreads), 0, st, Upart, XT, Mt, mscale,
+                           Mones, M, m, nkb, whiten, mspace, H, mvec, vbar, center);
     else
-        hipLaunchKernelGGL(mfinal_kernel<64>, dim3(64 / 8 + 1, BH), dim3(512), 0, st, Upart, XT, Mt, mscale, Mones, M, m,
-                           nkb, whiten, mspace, H, mvec);
+        hipLaunchKernelGGL(mfinal_kernel<64>, dim3(64 / 8 + 1, BH), dim3(kMfinalThreads), 0, st, Upart, XT, Mt, mscale,
+                           Mones, M, m, nkb, whiten, mspace, H, mvec, vbar, center);
     return hipGetLastError();
 }
 
-hipError_t launch_fast_query(int norm, const void* Q, void* Out, const uint32_t* kfix, const float* frame,
+hipError_t launch_fast_query(int norm, const void* Q, void* Out, const uint32_t* kfix, const uint32_t* kcen,
+                             const float* frame,
                              const _Float16* Mt, const float* mscale, const float* Mones, const float* vbar,
                              const float* extra, const float* mvec, int BH, int n, int d, int m, hipStream_t st) {
     const int nqb = (n + 255) / 256;
     dim3 grid(nqb * BH);
 #define LAPATTN_Q2(Dv, Nv)                                                                                        \
     hipLaunchKernelGGL((query2_kernel<Dv, Nv>), grid, dim3(256), 0, st, (const uint16_t*)Q, (uint16_t*)Out, kfix, \
-                       frame, Mt, mscale, Mones, vbar, extra, mvec, n, m, nqb, BH)
+                       kcen, frame, Mt, mscale, Mones, vbar, extra, mvec, n, m, nqb, BH)
     if (d == 32) {
         if (norm == NORM_INLINE) LAPATTN_Q2(32, NORM_INLINE);
         else if (norm == NORM_ROWSUM) LAPATTN_Q2(32, NORM_ROWSUM);

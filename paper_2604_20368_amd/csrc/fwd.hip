@@ -212,7 +212,9 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void key_summary_kernel(const
 // Newton-Schulz solve, one block of 256 threads per head, fp64 in LDS, matrices padded to
 // MP x MP with zeros (the padding stays zero under every update):
 //   W = K_LL + eps I,  c = ||W||_1 ||W||_inf,  X0 = W^T / c (X := 0 if c = 0),
-//   X_{t+1} = X_t (2I - W X_t);  then U = sum of the key-chunk partials, M = X_T U.
+//   X_{t+1} = X_t (2I - W X_t);  then U = sum of the key-chunk partials, M = X_T U, and
+//   Mc = M[:, :d] - M[:, d] vbar^T (fp64, then rounded), the value part the inline form reads:
+//   sum_l a_il Mc_l = Y_i[:d] - s_i vbar without the difference of the two rounded terms.
 // With store_all, Xs[h] holds X_0 .. X_T and then W (T + 2 matrices, pitch MP) for the backward.
 // Products on the fp64 matrix cores (ns_mfma.hpp); U's value columns and the ones column are
 // kept apart so that the value part of M is one MFMA product and the ones column a matrix-vector
@@ -223,8 +225,9 @@ __global__ __launch_bounds__(256) void ns_solve_kernel(const float* __restrict__
                                                        const double* __restrict__ vseg,
                                                        double* __restrict__ Xs, double* __restrict__ cinfo,
                                                        float* __restrict__ U, float* __restrict__ M,
-                                                       float* __restrict__ vbar, int n, int m, int T,
-                                                       double lambda, double eps, int nkc, int store_all) {
+                                                       float* __restrict__ Mc, float* __restrict__ vbar, int n,
+                                                       int m, int T, double lambda, double eps, int nkc,
+                                                       int store_all) {
     using SQ = ns_tiles<MP, MP>;
     using SU = ns_tiles<MP, D>;
     constexpr int D1 = D + 1;
@@ -237,6 +240,8 @@ __global__ __launch_bounds__(256) void ns_solve_kernel(const float* __restrict__
     __shared__ double sred[4];
     __shared__ double su1[MP];
     __shared__ double svb[256];
+    __shared__ double sM1[MP];
+    __shared__ double svbar[D];
     __shared__ double sc;
     double* sX = lds;
     double* sW = lds + MP * P;
@@ -347,24 +352,6 @@ __global__ __launch_bounds__(256) void ns_solve_kernel(const float* __restrict__
             }
         }
     }
-    __syncthreads();
-    {
-        f64x4_t r[SU::NT];
-        ns_mm<MP, D, MP, false, false, P, PU>(sX, sU, r);     // X_T U (value columns)
-#pragma unroll
-        for (int i = 0; i < SU::NT; ++i)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int a = SU::row(i, j), cc = SU::col(i);
-                if (a < m) M[((size_t)h * m + a) * D1 + cc] = (float)r[i][j];
-            }
-    }
-    if (tid < m) {
-        double s = 0.0;
-#pragma unroll 16
-        for (int b = 0; b < MP; ++b) s += sX[tid * P + b] * su1[b];
-        M[((size_t)h * m + tid) * D1 + D] = (float)s;
-    }
     // vbar = (sum of the segment value sums) / n: 256 / D partial sums per column, then in order
     {
         constexpr int G = 256 / D;
@@ -373,13 +360,38 @@ __global__ __launch_bounds__(256) void ns_solve_kernel(const float* __restrict__
 #pragma unroll 4
         for (int l = g; l < m; l += G) s += vseg[((size_t)h * m + l) * D + cc];
         svb[tid] = s;
-        __syncthreads();
-        if (tid < D) {
-            double t = 0.0;
+    }
+    __syncthreads();   // sU, su1, svb
+    if (tid < m) {
+        double s = 0.0;
+#pragma unroll 16
+        for (int b = 0; b < MP; ++b) s += sX[tid * P + b] * su1[b];
+        M[((size_t)h * m + tid) * D1 + D] = (float)s;
+        sM1[tid] = s;
+    }
+    if (tid < D) {
+        constexpr int G = 256 / D;
+        double t = 0.0;
 #pragma unroll
-            for (int gg = 0; gg < G; ++gg) t += svb[gg * D + tid];
-            vbar[(size_t)h * D + tid] = (float)(t / n);
-        }
+        for (int gg = 0; gg < G; ++gg) t += svb[gg * D + tid];
+        vbar[(size_t)h * D + tid] = (float)(t / n);
+        svbar[tid] = t / n;
+    }
+    __syncthreads();
+    {
+        // X_T U (value columns); Mc = M[:, :d] - M[:, d] vbar^T in fp64 for the inline form
+        f64x4_t r[SU::NT];
+        ns_mm<MP, D, MP, false, false, P, PU>(sX, sU, r);
+#pragma unroll
+        for (int i = 0; i < SU::NT; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int a = SU::row(i, j), cc = SU::col(i);
+                if (a < m) {
+                    M[((size_t)h * m + a) * D1 + cc] = (float)r[i][j];
+                    Mc[((size_t)h * m + a) * D + cc] = (float)(r[i][j] - sM1[a] * svbar[cc]);
+                }
+            }
     }
 }
 
@@ -389,7 +401,8 @@ __global__ __launch_bounds__(256) void ns_solve_kernel(const float* __restrict__
 //   Landmark pass: a_il = k(q_i, kt_l) into the wave's [query][landmark] LDS tile (the landmark
 //   rows of kt through scalar registers), 32 landmarks at a time: the tile is 64 x 33 floats per
 //   wave, so that three blocks share a compute unit.  s_i = sum_l a_il M[l][d] in fp32 is formed
-//   with the contraction, which reads the tile anyway.
+//   with the contraction, which reads the tile anyway, where the normalisation needs it; the
+//   inline form contracts with Mc = M[:, :d] - M[:, d] vbar^T instead: out_i = (A Mc)_i + vbar.
 //   Contraction: for each 32-query half, Y^T = M^T A^T on fp32 MFMA 32x32x2 (k = a pair of
 //   landmarks).  The B operands of a pair for both halves come from one permlane32 swap of the
 //   pair's two tile columns (queries 0..31 keep theirs and receive the other landmark of 32..63
@@ -400,6 +413,7 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 template <int D, int NORM>
 __global__ __launch_bounds__(256) void query_out_kernel(const float* __restrict__ Q, float* __restrict__ Out,
                                                         const float* __restrict__ kt, const float* __restrict__ M,
+                                                        const float* __restrict__ Mc,
                                                         const float* __restrict__ vbar,
                                                         const float* __restrict__ extra,
                                                         const float* __restrict__ whiten,
@@ -427,7 +441,8 @@ __global__ __launch_bounds__(256) void query_out_kernel(const float* __restrict_
             const int s = 16 * hh + e / (CB * 64), cb = (e / 64) % CB, ln = e % 64;
             const int lm = 2 * s + ln / 32;
             const float wv = wl && lm < m ? wl[lm] : 1.f;
-            sMT[e] = (lm < m) ? wv * M[((size_t)h * m + lm) * D1 + 32 * cb + ln % 32] : 0.f;
+            const float* src = NORM == NORM_INLINE ? Mc + ((size_t)h * m + lm) * D : M + ((size_t)h * m + lm) * D1;
+            sMT[e] = (lm < m) ? wv * src[32 * cb + ln % 32] : 0.f;
         }
     };
     if (tid < 64) {
@@ -499,7 +514,7 @@ __global__ __launch_bounds__(256) void query_out_kernel(const float* __restrict_
         for (int pl = 0; pl < npair; ++pl) {
             const int p = 16 * hh + pl;   // landmark pair of the whole tile
             const float x0 = tile[l * TP + 2 * pl], x1 = tile[l * TP + 2 * pl + 1];
-            s = fmaf(x1, sMo[2 * p + 1], fmaf(x0, sMo[2 * p], s));
+            if (NORM == NORM_ROWSUM || NORM == NORM_MSPACE) s = fmaf(x1, sMo[2 * p + 1], fmaf(x0, sMo[2 * p], s));
             const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x0), __float_as_uint(x1), false, false);
 #pragma unroll
             for (int cb = 0; cb < CB; ++cb) {
@@ -530,7 +545,7 @@ __global__ __launch_bounds__(256) void query_out_kernel(const float* __restrict_
 #pragma unroll
                     for (int t = 0; t < 4; ++t) {
                         const float y = acc[qb][cb][4 * g + t];
-                        if (NORM == NORM_INLINE) o[t] = fmaf(1.f - si, sVb[c0 + t], y);
+                        if (NORM == NORM_INLINE) o[t] = y + sVb[c0 + t];   // y = Y[:d] - s vbar (Mc)
                         else if (NORM == NORM_ROWSUM) o[t] = y / si;
                         else if (NORM == NORM_MSPACE) o[t] = fmaf(-si, sVb[c0 + t], y) + sMb[c0 + t];
                         else o[t] = y;
@@ -579,11 +594,11 @@ hipError_t launch_key_summary(int dt, const void* K, const void* V, const float*
 }
 
 hipError_t launch_ns_solve(const float* qt, const float* kt, const float* Upart, const double* vseg, double* Xs,
-                           double* cinfo, float* U, float* M, float* vbar, int BH, int n, int d, int m, int T,
+                           double* cinfo, float* U, float* M, float* Mc, float* vbar, int BH, int n, int d, int m, int T,
                            double lambda, double eps, int nkc, int store_all, int MP, hipStream_t st) {
 #define LAPATTN_NS(MPv, Dv)                                                                                  \
     hipLaunchKernelGGL((ns_solve_kernel<MPv, Dv>), dim3(BH), dim3(256), 0, st, qt, kt, Upart, vseg, Xs, cinfo, \
-                       U, M, vbar, n, m, T, lambda, eps, nkc, store_all)
+                       U, M, Mc, vbar, n, m, T, lambda, eps, nkc, store_all)
     if (MP == 32 && d == 32) LAPATTN_NS(32, 32);
     else if (MP == 32) LAPATTN_NS(32, 64);
     else if (d == 32) LAPATTN_NS(64, 32);
@@ -593,14 +608,15 @@ hipError_t launch_ns_solve(const float* qt, const float* kt, const float* Upart,
 }
 
 template <int D>
-static void query_out_launch(int norm, const void* Q, void* Out, const float* kt, const float* M, const float* vbar,
+static void query_out_launch(int norm, const void* Q, void* Out, const float* kt, const float* M, const float* Mc,
+                             const float* vbar,
                              const float* extra, const float* whiten, const float* mvec, float* Asave, int BH, int H,
                              int n, int m, float kscale, hipStream_t st) {
     dim3 grid((n + 255) / 256, BH);
     const float* q = (const float*)Q;
     float* o = (float*)Out;
 #define LAPATTN_QO(Nv)                                                                                             \
-    hipLaunchKernelGGL((query_out_kernel<D, Nv>), grid, dim3(256), 0, st, q, o, kt, M, vbar, extra, whiten, mvec,     \
+    hipLaunchKernelGGL((query_out_kernel<D, Nv>), grid, dim3(256), 0, st, q, o, kt, M, Mc, vbar, extra, whiten, mvec, \
                        Asave, H, n, m, kscale)
     if (norm == NORM_INLINE) LAPATTN_QO(NORM_INLINE);
     else if (norm == NORM_ROWSUM) LAPATTN_QO(NORM_ROWSUM);
@@ -610,12 +626,12 @@ static void query_out_launch(int norm, const void* Q, void* Out, const float* kt
 }
 
 hipError_t launch_query_out(int dt, int norm, const void* Q, void* Out, const float* kt, const float* M,
-                            const float* vbar, const float* extra, const float* whiten, const float* mvec,
+                            const float* Mc, const float* vbar, const float* extra, const float* whiten, const float* mvec,
                             float* Asave, int BH, int H, int n, int d, int m, float lambda, hipStream_t st) {
     if (dt != DT_F32) return hipErrorInvalidValue;   // bf16 inputs take the fast path
     const float ks = kscale_of(lambda);
-    if (d == 32) query_out_launch<32>(norm, Q, Out, kt, M, vbar, extra, whiten, mvec, Asave, BH, H, n, m, ks, st);
-    else query_out_launch<64>(norm, Q, Out, kt, M, vbar, extra, whiten, mvec, Asave, BH, H, n, m, ks, st);
+    if (d == 32) query_out_launch<32>(norm, Q, Out, kt, M, Mc, vbar, extra, whiten, mvec, Asave, BH, H, n, m, ks, st);
+    else query_out_launch<64>(norm, Q, Out, kt, M, Mc, vbar, extra, whiten, mvec, Asave, BH, H, n, m, ks, st);
     return hipGetLastError();
 }
 

@@ -54,7 +54,7 @@ int check_align(std::initializer_list<const void*> tensors, const void* workspac
 // ------------------------------------------------------------------------------- workspace plan
 
 struct FastPlan {
-    size_t qt, kt, vseg, segmax, vsegmax, frame, qfix, kfix, vbar, XT, cinfo, Upart, Mt, mscale, Mones, M;
+    size_t qt, kt, vseg, segmax, vsegmax, frame, qfix, kfix, kcen, vbar, XT, cinfo, Upart, Mt, mscale, Mones, M;
     size_t E;      // convolution branch: DWC(V) + bias, fp32 [BH][n][d]
     size_t mvec;   // landmark-space normalisation: [BH][2][d]
     size_t total;
@@ -62,7 +62,7 @@ struct FastPlan {
 };
 
 struct Plan {
-    size_t qt, kt, vseg, Upart, Xs, cinfo, U, M, vbar;                   // forward
+    size_t qt, kt, vseg, Upart, Xs, cinfo, U, M, Mc, vbar;               // forward
     size_t Aq, dDq, rs, dYd, dvbar_part, dM_part, dkt_part, dU, dvbar,   // backward
         dqtW, dkpool, dDk, dqt_part;
     size_t wQ, wK, wV, wG, gQ, gK, gV;   // bf16 backward: fp32 copies of the inputs, fp32 gradients
@@ -122,6 +122,7 @@ Plan make_plan(int BH, int n, int d, int m, int T, bool bwd, bool bf16 = false, 
     p.cinfo = c.take(bh * 4 * g);
     p.U = c.take(bh * m * d1 * f);
     p.M = c.take(bh * m * d1 * f);
+    p.Mc = c.take(bh * m * d * f);
     p.vbar = c.take(bh * d * f);
     p.mvec = c.take(bh * 2 * d * f);
     if (bwd) {
@@ -172,9 +173,10 @@ FastPlan make_fast_plan(int BH, int n, int d, int m, bool dwc = false) {
     p.vseg = c.take(bh * m * d * g);
     p.segmax = c.take(bh * m * f);
     p.vsegmax = c.take(bh * m * f);
-    p.frame = c.take(bh * 4 * f);
+    p.frame = c.take(bh * 8 * f);
     p.qfix = c.take(bh * 64 * (d / 2) * 4);
     p.kfix = c.take(bh * 64 * (d / 2) * 4);
+    p.kcen = c.take(bh * (d / 2) * 4);
     p.vbar = c.take(bh * d * f);
     p.XT = c.take(bh * 64 * 64 * f);
     p.cinfo = c.take(bh * 4 * f);
@@ -301,7 +303,8 @@ hipError_t forward_internals(Recorder& rec, const Plan& p, const void* Q, const 
     if (e != hipSuccess) return e;
     e = run_named(rec, "ns_solve", [&] {
         return lapattn::launch_ns_solve(qt, kt, Upart, vseg, at<double>(ws, p.Xs), at<double>(ws, p.cinfo),
-                                        at<float>(ws, p.U), at<float>(ws, p.M), at<float>(ws, p.vbar), BH, n, d, m, T,
+                                        at<float>(ws, p.U), at<float>(ws, p.M), at<float>(ws, p.Mc),
+                                        at<float>(ws, p.vbar), BH, n, d, m, T,
                                         (double)lambda, (double)eps, p.nkc, store_all ? 1 : 0, p.MP, st);
     });
     return e;
@@ -327,7 +330,8 @@ hipError_t forward_fast(Recorder& rec, const FastPlan& p, const void* Q, const v
     e = run_named(rec, "frame_ns", [&] {
         return lapattn::launch_fast_frame_ns(at<float>(ws, p.qt), at<float>(ws, p.kt), at<double>(ws, p.vseg),
                                              at<float>(ws, p.segmax), at<float>(ws, p.vsegmax), at<float>(ws, p.frame),
-                                             at<uint32_t>(ws, p.qfix), at<uint32_t>(ws, p.kfix), at<float>(ws, p.vbar),
+                                             at<uint32_t>(ws, p.qfix), at<uint32_t>(ws, p.kfix),
+                                             at<uint32_t>(ws, p.kcen), at<float>(ws, p.vbar),
                                              at<float>(ws, p.XT), at<float>(ws, p.cinfo), BH, n, d, m, lambda, T, eps,
                                              st);
     });
@@ -340,11 +344,13 @@ hipError_t forward_fast(Recorder& rec, const FastPlan& p, const void* Q, const v
     e = run_named(rec, "m_final", [&] {
         return lapattn::launch_fast_mfinal(at<float>(ws, p.Upart), at<float>(ws, p.XT), at<_Float16>(ws, p.Mt),
                                            at<float>(ws, p.mscale), at<float>(ws, p.Mones), at<float>(ws, p.M), BH, d, m,
-                                           p.nkb, whiten, mspace ? 1 : 0, H, at<float>(ws, p.mvec), st);
+                                           p.nkb, whiten, mspace ? 1 : 0, H, at<float>(ws, p.mvec),
+                                           at<float>(ws, p.vbar), norm == LAPATTN_NORM_INLINE ? 1 : 0, st);
     });
     if (e != hipSuccess) return e;
     e = run_named(rec, "query", [&] {
-        return lapattn::launch_fast_query(norm, Q, Out, at<uint32_t>(ws, p.kfix), at<float>(ws, p.frame),
+        return lapattn::launch_fast_query(norm, Q, Out, at<uint32_t>(ws, p.kfix), at<uint32_t>(ws, p.kcen),
+                                          at<float>(ws, p.frame),
                                           at<_Float16>(ws, p.Mt), at<float>(ws, p.mscale), at<float>(ws, p.Mones),
                                           at<float>(ws, p.vbar), E, at<float>(ws, p.mvec), BH, n, d, m, st);
     });
@@ -415,7 +421,8 @@ int lapattn_forward(const void* Q, const void* K, const void* V, void* Out, int 
         }
         e = run_named(rec, "query_out", [&] {
             return lapattn::launch_query_out(dtype, norm, Q, Out, at<float>(workspace, p.kt),
-                                             at<float>(workspace, p.M), at<float>(workspace, p.vbar), E,
+                                             at<float>(workspace, p.M), at<float>(workspace, p.Mc),
+                                             at<float>(workspace, p.vbar), E,
                                              whiten_of(opts), at<float>(workspace, p.mvec),
                                              save ? at<float>(workspace, p.Aq) : nullptr, BH, H, n, d, m, lambda, st);
         });

@@ -29,17 +29,18 @@ hipError_t launch_key_summary(int dt, const void* K, const void* V, const float*
 // Newton-Schulz on K_LL and the solved matrix M = X_T U.
 //   Xs:    [BH][store_all ? T+1 : 1][MP][MP] fp64 iterates (padded to MP)
 //   cinfo: [BH][4] fp64: scale c, ||W||_1, ||W||_inf, (a* * 256 + b*)
-//   U, M:  [BH][m][d+1] fp32;  vbar: [BH][d] fp32
+//   U, M:  [BH][m][d+1] fp32;  Mc: [BH][m][d] fp32, M[:, :d] - M[:, d] vbar^T;  vbar: [BH][d] fp32
 hipError_t launch_ns_solve(const float* qt, const float* kt, const float* Upart, const double* vseg,
-                           double* Xs, double* cinfo, float* U, float* M, float* vbar,
+                           double* Xs, double* cinfo, float* U, float* M, float* Mc, float* vbar,
                            int BH, int n, int d, int m, int T, double lambda, double eps, int nkc,
                            int store_all, int MP, hipStream_t st);
 
-// Query side: Out_i = normalise(sum_l k(q_i, kt_l) M_l) (+ extra_i when extra, [BH][n][d], is given).
+// Query side: Out_i = normalise(sum_l k(q_i, kt_l) M_l) (+ extra_i when extra, [BH][n][d], is given);
+// the inline form reads Mc (launch_ns_solve).
 // The landmark-space normalisation takes the whitening [H][m] (NULL: ones) and mvec below.
 // With Asave, also the rows A[i][l] = k(q_i, kt_l) ([BH][n][64], columns below m) for the backward.
 hipError_t launch_query_out(int dt, int norm, const void* Q, void* Out, const float* kt, const float* M,
-                            const float* vbar, const float* extra, const float* whiten, const float* mvec,
+                            const float* Mc, const float* vbar, const float* extra, const float* whiten, const float* mvec,
                             float* Asave, int BH, int H, int n, int d, int m, float lambda, hipStream_t st);
 
 // Landmark-space normalisation: mvec[BH][2][d] = {sum_l w_l M_l[:d], (1/m) sum_l M_l[:d]}.
@@ -104,17 +105,19 @@ hipError_t launch_fast_pool(const void* Q, const void* K, const void* V, float* 
                             float* segmax, float* vsegmax, int BH, int n, int d, int m, LmPool pl,
                             hipStream_t st);
 hipError_t launch_fast_frame_ns(const float* qt, const float* kt, const double* vseg, const float* segmax,
-                                const float* vsegmax, float* frame, uint32_t* qfix, uint32_t* kfix, float* vbar,
-                                float* XT, float* cinfo, int BH, int n, int d, int m, float lambda, int T, float eps,
-                                hipStream_t st);
+                                const float* vsegmax, float* frame, uint32_t* qfix, uint32_t* kfix, uint32_t* kcen,
+                                float* vbar, float* XT, float* cinfo, int BH, int n, int d, int m, float lambda, int T,
+                                float eps, hipStream_t st);
 hipError_t launch_fast_key(const void* K, const void* V, const uint32_t* qfix, const float* frame, float* Upart,
                            int BH, int n, int d, int m, int kpb, int nkb, hipStream_t st);
 // mspace: the landmark-space normalisation (operand rows scaled by the whitening [H][m], NULL:
-// ones; the ones column 1/m; mvec[BH][2][d] written as for launch_mspace_vec).
+// ones; the ones column 1/m; mvec[BH][2][d] written as for launch_mspace_vec).  center (the
+// inline normalisation): the operand columns are M[a][c] - M[a][d] vbar[c] (vbar [BH][d]).
 hipError_t launch_fast_mfinal(const float* Upart, const float* XT, _Float16* Mt, float* mscale, float* Mones,
                               float* M, int BH, int d, int m, int nkb, const float* whiten, int mspace, int H,
-                              float* mvec, hipStream_t st);
-hipError_t launch_fast_query(int norm, const void* Q, void* Out, const uint32_t* kfix, const float* frame,
+                              float* mvec, const float* vbar, int center, hipStream_t st);
+hipError_t launch_fast_query(int norm, const void* Q, void* Out, const uint32_t* kfix, const uint32_t* kcen,
+                             const float* frame,
                              const _Float16* Mt, const float* mscale, const float* Mones, const float* vbar,
                              const float* extra, const float* mvec, int BH, int n, int d, int m, hipStream_t st);
 

@@ -12,8 +12,10 @@ the architectures it builds on -- 197 = 14x14 patches + a class token (DeiT at
 Recipe: numpy PCG64 ``default_rng(seed)``; draw ``standard_normal((B,H,n,d))`` for
 Q, then K, then V, then (training workload only) dOut; scale Q, K, V by sigma and
 dOut by 1; round to fp32 (round-to-nearest-even), then to bf16 (RNE) for the bf16
-workloads.  The fp32 arrays returned always hold the exact values the device
-receives, so the oracle sees the same numbers widened to fp64.
+workloads.  A heavy-tailed variant (``dist="t3"``, a robustness case, not one of the
+five workloads) draws Q and K from ``standard_t(3, ...)`` instead, in the same order.
+The fp32 arrays returned always hold the exact values the device receives, so the
+oracle sees the same numbers widened to fp64.
 """
 import math
 from dataclasses import dataclass
@@ -35,6 +37,7 @@ class Workload:
     lam: float        # Laplacian scale lambda
     seed: int
     backward: bool    # the workload also runs the backward pass
+    dist: str = "normal"   # Q and K entries: "normal", or "t3" (Student-t, 3 degrees of freedom)
 
     @property
     def BH(self):
@@ -87,7 +90,10 @@ def make_inputs(w, with_grad=None, heads=None):
     shape = (w.B, w.H, w.n, w.d)
     out = {}
     for name, scale in (("Q", w.sigma), ("K", w.sigma), ("V", w.sigma)) + ((("dO", 1.0),) if with_grad else ()):
-        x = (rng.standard_normal(shape) * scale).astype(np.float32)
+        if w.dist == "t3" and name in ("Q", "K"):
+            x = (rng.standard_t(3, shape) * scale).astype(np.float32)
+        else:
+            x = (rng.standard_normal(shape) * scale).astype(np.float32)
         if w.dtype == "bf16":
             x = round_bf16(x)
         out[name] = x

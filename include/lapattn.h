@@ -83,8 +83,10 @@ enum {
     LAPATTN_ERR_UNSUPPORTED = 4,  /* d not in {32, 64} or m > 64 */
     LAPATTN_ERR_WORKSPACE = 5,    /* workspace NULL or smaller than lapattn_workspace_size() */
     LAPATTN_ERR_HIP = 6,          /* a HIP launch failed */
-    LAPATTN_ERR_ALIGN = 7         /* a tensor pointer is not 16-byte aligned, or the
+    LAPATTN_ERR_ALIGN = 7,        /* a tensor pointer is not 16-byte aligned, or the
                                      workspace is not 256-byte aligned */
+    LAPATTN_ERR_SCRATCH = 8       /* lapattn_forward_noalloc: the call needs more workspace
+                                     than the library's static scratch array holds (32 MiB) */
 };
 
 /* Options; a NULL pointer means all fields zero: {LAPATTN_NORM_INLINE, 0.0f, 0, 0, 0, NULL, ...}.
@@ -162,6 +164,21 @@ int lapattn_backward(const void* Q, const void* K, const void* V, const void* dO
                      int B, int H, int n, int d, int m, float lambda, int ns_iters,
                      int dtype, const lapattn_opts* opts,
                      void* workspace, size_t workspace_bytes, lapattn_stream_t stream);
+
+/* Forward pass without a caller workspace, for callers that cannot allocate device memory:
+ * code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * Arguments, results and errors as lapattn_forward, whose kernels it runs on a static device
+ * array of the library (32 MiB per GPU, held by every GPU the library runs on until the process
+ * ends) in place of the workspace; it calls no allocating routine.  A call whose
+ * lapattn_workspace_size (with LAPATTN_WS_DWC when opts->dwc_k is set) exceeds 32 MiB returns
+ * LAPATTN_ERR_SCRATCH, and opts->save returns LAPATTN_ERR_PARAM (the saved state would sit in
+ * the shared array), both before anything is enqueued.  All calls on one GPU share its array:
+ * calls that overlap on one GPU (other streams, other threads) race and must be ordered by the
+ * caller.  The first call on each device looks up that device's array (with the device
+ * current). */
+int lapattn_forward_noalloc(const void* Q, const void* K, const void* V, void* Out,
+                            int B, int H, int n, int d, int m, float lambda, int ns_iters,
+                            int dtype, const lapattn_opts* opts, lapattn_stream_t stream);
 
 /* Human-readable name of a status code (static storage). */
 const char* lapattn_status_str(int status);

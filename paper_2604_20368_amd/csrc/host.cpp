@@ -565,6 +565,7 @@ const char* lapattn_status_str(int status) {
         case LAPATTN_ERR_WORKSPACE: return "workspace missing or too small";
         case LAPATTN_ERR_HIP: return "HIP launch failed";
         case LAPATTN_ERR_ALIGN: return "a tensor is not 16-byte aligned or the workspace not 256-byte aligned";
+        case LAPATTN_ERR_SCRATCH: return "the call needs more workspace than the static scratch array holds (32 MiB)";
         default: return "unknown status";
     }
 }

@@ -13,10 +13,11 @@ LAPATTN_FP32, LAPATTN_BF16 = 0, 1
 LAPATTN_NORM_INLINE, LAPATTN_NORM_ROWSUM, LAPATTN_NORM_NONE, LAPATTN_NORM_MSPACE = 0, 1, 2, 3
 LAPATTN_OK, LAPATTN_ERR_NULL, LAPATTN_ERR_SHAPE, LAPATTN_ERR_PARAM = 0, 1, 2, 3
 LAPATTN_ERR_UNSUPPORTED, LAPATTN_ERR_WORKSPACE, LAPATTN_ERR_HIP, LAPATTN_ERR_ALIGN = 4, 5, 6, 7
+LAPATTN_ERR_SCRATCH = 8
 LAPATTN_WS_BACKWARD, LAPATTN_WS_DWC = 1, 2
 
 EXPORTS = ("lapattn_workspace_size", "lapattn_forward", "lapattn_backward", "lapattn_status_str",
-           "lapattn_timing_enable", "lapattn_timing_read", "lapattn_timing_name")
+           "lapattn_timing_enable", "lapattn_timing_read", "lapattn_timing_name", "lapattn_forward_noalloc")
 
 
 class lapattn_opts(ctypes.Structure):
@@ -51,6 +52,8 @@ def library():
     lib.lapattn_forward.argtypes = [vp] * 4 + [ci] * 5 + [cf, ci, ci, ctypes.POINTER(lapattn_opts), vp, sz, vp]
     lib.lapattn_backward.restype = ci
     lib.lapattn_backward.argtypes = [vp] * 7 + [ci] * 5 + [cf, ci, ci, ctypes.POINTER(lapattn_opts), vp, sz, vp]
+    lib.lapattn_forward_noalloc.restype = ci
+    lib.lapattn_forward_noalloc.argtypes = [vp] * 4 + [ci] * 5 + [cf, ci, ci, ctypes.POINTER(lapattn_opts), vp]
     lib.lapattn_status_str.restype = ctypes.c_char_p
     lib.lapattn_status_str.argtypes = [ci]
     lib.lapattn_timing_enable.restype = ci
@@ -89,6 +92,13 @@ def lapattn_forward(Q, K, V, Out, B, H, n, d, m, lam, ns_iters, dtype, norm=LAPA
     whiten the address of the landmark-space whitening."""
     return library().lapattn_forward(Q, K, V, Out, B, H, n, d, m, float(lam), ns_iters, dtype,
                                      _opts(norm, eps, grid, dwc, whiten, save), workspace, workspace_bytes, stream)
+
+
+def lapattn_forward_noalloc(Q, K, V, Out, B, H, n, d, m, lam, ns_iters, dtype, norm=LAPATTN_NORM_INLINE, eps=0.0,
+                            stream=0, grid=None, dwc=None, whiten=None, save=False):
+    """Raw call of the forward on the library's static scratch array (no workspace argument)."""
+    return library().lapattn_forward_noalloc(Q, K, V, Out, B, H, n, d, m, float(lam), ns_iters, dtype,
+                                             _opts(norm, eps, grid, dwc, whiten, save), stream)
 
 
 def lapattn_backward(Q, K, V, dO, dQ, dK, dV, B, H, n, d, m, lam, ns_iters, dtype, norm=LAPATTN_NORM_INLINE,
@@ -196,6 +206,23 @@ def forward(Q, K, V, m, lam, ns_iters, norm=LAPATTN_NORM_INLINE, eps=0.0, out=No
                          _whiten_arg(Q, m, whiten), save)
     if rc != LAPATTN_OK:
         raise LapattnError(rc, "lapattn_forward")
+    return out
+
+
+def forward_noalloc(Q, K, V, m, lam, ns_iters, norm=LAPATTN_NORM_INLINE, eps=0.0, out=None, grid=None, dwc=None,
+                    whiten=None):
+    """Out = lapattn(Q, K, V) through lapattn_forward_noalloc: no workspace is allocated (out is
+    allocated here unless given)."""
+    import torch
+    _check(Q, K, V)
+    out = torch.empty_like(Q) if out is None else out
+    _check(Q, out)
+    B, H, n, d = Q.shape
+    rc = lapattn_forward_noalloc(Q.data_ptr(), K.data_ptr(), V.data_ptr(), out.data_ptr(), B, H, n, d, m, lam,
+                                 ns_iters, _dtype_code(Q), norm, eps, _stream(Q), grid, _dwc_args(Q, dwc),
+                                 _whiten_arg(Q, m, whiten))
+    if rc != LAPATTN_OK:
+        raise LapattnError(rc, "lapattn_forward_noalloc")
     return out
 
 

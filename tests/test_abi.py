@@ -28,7 +28,7 @@ def test_library_exports_every_declared_function():
 
 
 def test_status_strings():
-    for code in range(8):
+    for code in range(9):
         assert L.lapattn_status_str(code) and L.lapattn_status_str(code) != "unknown status"
     assert L.lapattn_status_str(99) == "unknown status"
 
@@ -159,3 +159,29 @@ def test_saved_forward_needs_the_backward_workspace():
     assert fwd(save=True, workspace_bytes=fsz) == L.LAPATTN_ERR_WORKSPACE
     assert fwd(save=True, workspace_bytes=bsz - 256) == L.LAPATTN_ERR_WORKSPACE
     assert fwd(save=False, workspace_bytes=fsz - 256) == L.LAPATTN_ERR_WORKSPACE
+
+
+def fwd_noalloc(**kw):
+    args = dict(Q=FAKE, K=FAKE, V=FAKE, Out=FAKE, B=1, H=2, n=100, d=32, m=8, lam=1.0, ns_iters=4, dtype=0,
+                norm=0, eps=0.0)
+    args.update(kw)
+    return L.lapattn_forward_noalloc(**args)
+
+
+def test_forward_noalloc_validation():
+    """The allocation-free forward applies the forward's checks, then rejects calls whose workspace
+    would exceed its 32 MiB scratch array, and the save option -- all before any HIP call."""
+    for p in ("Q", "K", "V", "Out"):
+        assert fwd_noalloc(**{p: 0}) == L.LAPATTN_ERR_NULL
+    assert fwd_noalloc(m=101) == L.LAPATTN_ERR_SHAPE
+    assert fwd_noalloc(lam=0.0) == L.LAPATTN_ERR_PARAM
+    assert fwd_noalloc(d=48) == L.LAPATTN_ERR_UNSUPPORTED
+    assert fwd_noalloc(Q=FAKE + 4) == L.LAPATTN_ERR_ALIGN
+    assert fwd_noalloc(save=True) == L.LAPATTN_ERR_PARAM
+    # the n = 16384 workload fits (10 MiB of workspace); the same shape with fp32 inputs at twice
+    # the batch (37 MiB), or with the convolution branch (74 MiB), does not
+    big = dict(B=8, H=2, n=16384, d=64, m=64, ns_iters=8, dtype=1)
+    assert L.lapattn_workspace_size(8, 2, 16384, 64, 64, 8, 1, 0) <= 32 << 20
+    assert L.lapattn_workspace_size(16, 2, 16384, 64, 64, 8, 0, 0) > 32 << 20
+    assert fwd_noalloc(**dict(big, B=16, dtype=0)) == L.LAPATTN_ERR_SCRATCH
+    assert fwd_noalloc(**big, grid=(128, 0), dwc=(3, FAKE, 0, 0, 0)) == L.LAPATTN_ERR_SCRATCH

@@ -55,20 +55,6 @@ __device__ __forceinline__ uint32_t fix2_bf16(uint32_t w, float inv2R) {
     return fix2(bf16_lo(w), bf16_hi(w), inv2R);
 }
 
-// exp2 bias of a token whose coordinates may lie beyond the range R: ebias + xscale E(x) with
-// E(x) = sum_c max(|x_c|, R) - d R = sum_c max(|x_c| - R, 0) (the row as D8 16-byte chunks of
-// bf16 pairs).
-template <int D8>
-__device__ __forceinline__ float excess_bias(const uint4 (&row)[D8], float R, float xscale, float ebias) {
-    float e = 0.f;
-#pragma unroll
-    for (int c8 = 0; c8 < D8; ++c8) {
-        const uint32_t wd[4] = {row[c8].x, row[c8].y, row[c8].z, row[c8].w};
-#pragma unroll
-        for (int t = 0; t < 4; ++t) e += fmaxf(fabsf(bf16_lo(wd[t])), R) + fmaxf(fabsf(bf16_hi(wd[t])), R);
-    }
-    return fmaf(e - (float)(8 * D8) * R, xscale, ebias);
-}
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
@@ -280,14 +266,12 @@ __device__ __forceinline__ float lap_row(const uint32_t (&kf)[D2], const uint32_
 // Per-head frame and Newton-Schulz solve.  grid (BH), 512 threads (8 waves).
 //
 // Frame: frame[h][0..7] = {R, 1/(2R), escale = -log2(e) / (lambda S), vscale,
-// xscale = -log2(e) / lambda, clamped, rho, 0}; R is NaN when Q, K or V hold a non-finite value
+// xscale = -log2(e) / lambda, clamped, rho (written by mfinal_kernel), 0}; R is NaN when Q, K or
+// V hold a non-finite value
 // (the outputs of that head are then NaN, as the plain computation gives); clamped = 1 when
 // some |x| of Q or K exceeds R (the key and query sides then add the excess E(x) of each
 // token).  qfix/kfix[h][a][c/2] = u(x_{a,c}) | u(x_{a,c+1}) << 16 for landmarks a < 64 (zero
-// rows >= m); kcen[h][c/2] = the key-landmark codes' centre c (the rounded mean over the landmarks
-// of each coordinate), rho = max_l sum_c |u(kt_{l,c}) - c_c| (code units): by the triangle
-// inequality every query's code distance to landmark l is at least its distance to c minus rho.
-// vbar[h] = mean of the values; vscale = 2^e puts the largest |v| of the head in
+// rows >= m).  vbar[h] = mean of the values; vscale = 2^e puts the largest |v| of the head in
 // [2^13, 2^14), so that the fp16 copies of V (exact for bf16 values in fp16's normal range)
 // neither overflow nor fall into fp16's subnormal range for small values.
 //
@@ -401,8 +385,8 @@ template <int D>
 __global__ __launch_bounds__(kSolveThreads) void frame_ns_kernel(
     const float* __restrict__ qt, const float* __restrict__ kt, const double* __restrict__ vseg,
     const float* __restrict__ segmax, const float* __restrict__ vsegmax, float* __restrict__ frame,
-    uint32_t* __restrict__ qfix, uint32_t* __restrict__ kfix, uint32_t* __restrict__ kcen, float* __restrict__ vbar,
-    float* __restrict__ XT, float* __restrict__ cinfo, int n, int m, float lambda, int T, float eps) {
+    uint32_t* __restrict__ qfix, uint32_t* __restrict__ kfix, float* __restrict__ vbar, float* __restrict__ XT,
+    float* __restrict__ cinfo, int n, int m, float lambda, int T, float eps) {
     constexpr int NT = kSolveThreads;
     constexpr int NW = NT / 64;          // 8 waves
     constexpr int D2 = D / 2;
@@ -431,7 +415,7 @@ __global__ __launch_bounds__(kSolveThreads) void frame_ns_kernel(
     float* part = reinterpret_cast<float*>(ETh(0));          // 2 x NW x 64 floats
     double* vpart = reinterpret_cast<double*>(ETh(0)) + 512;  // G x D doubles, after part
     float* sWf = reinterpret_cast<float*>(ETh(1));
-    static_assert(2 * 64 * D2 * 4 + D2 * 4 <= 2 * 64 * kLP * 2, "landmark tables and centre exceed Z^T[1]");
+    static_assert(2 * 64 * D2 * 4 <= 2 * 64 * kLP * 2, "landmark tables exceed Z^T[1]");
     static_assert(2 * NW * 64 * 4 <= 512 * 8 && 512 * 8 + G * D * 8 <= 2 * 64 * kLP * 2, "partials exceed E^T[0]");
     static_assert(64 * WP * 4 <= 2 * 64 * kLP * 2, "fp32 W exceeds E^T[1]");
     static_assert(G * D == NT && G * LPG == 64, "value partials");
@@ -477,14 +461,15 @@ __global__ __launch_bounds__(kSolveThreads) void frame_ns_kernel(
         const float xmax = wave_max_dpp(sa);
         const float vm = wave_max_dpp(sb);
         // median of the landmarks' token maxima (lane l < m holds landmark l's): the value of
-        // rank (m - 1) / 2, ties ranked by landmark index
+        // rank (m - 1) / 2, ties ranked by landmark index (landmark j's value read as a scalar)
         int rank = 0;
         for (int j = 0; j < m; ++j) {
-            const float sj = __shfl(sa, j, 64);
+            const float sj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sa), j));
             rank += (sj < sa || (sj == sa && j < l)) ? 1 : 0;
         }
         const unsigned long long pick = __ballot(l < m && rank == (m - 1) / 2);
-        const float med = pick ? __shfl(sa, (int)__builtin_ctzll(pick), 64) : xmax;   // none: a NaN maximum
+        const float med = pick ? __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sa), (int)__builtin_ctzll(pick)))
+                               : xmax;   // none: a NaN maximum
         float lmax = sred[48];
 #pragma unroll
         for (int i = 1; i < NW; ++i) lmax = fmaxf(lmax, sred[48 + i]);
@@ -528,32 +513,6 @@ __global__ __launch_bounds__(kSolveThreads) void frame_ns_kernel(
         sK[e] = uk;
     }
     __syncthreads();
-    if (w == 0) {
-        // centre of the key-landmark codes (per coordinate, the rounded mean over the m
-        // landmarks) and rho = the largest code distance of a landmark from it, for the query
-        // side's bound on each query's largest kernel value
-        uint32_t* scen = sK + 64 * D2;
-        if (l < D2) {
-            uint32_t slo = 0, shi = 0;
-            for (int a = 0; a < m; ++a) {
-                const uint32_t u = sK[a * D2 + l];
-                slo += u & 0xffffu;
-                shi += u >> 16;
-            }
-            const uint32_t cen = ((slo + m / 2) / m) | (((shi + m / 2) / m) << 16);
-            scen[l] = cen;
-            kcen[(size_t)h * D2 + l] = cen;
-        }
-        __builtin_amdgcn_wave_barrier();   // the wave's LDS requests complete in order
-        uint32_t dist = 0;
-        if (l < m) {
-#pragma unroll
-            for (int c2 = 0; c2 < D2; ++c2) dist = __builtin_amdgcn_sad_u16(sK[l * D2 + c2], scen[c2], dist);
-        }
-        const float rho = (float)__float_as_uint(wave_max_dpp(__uint_as_float(dist)));
-        if (l == 0) frame[h * 8 + 6] = rho;
-    }
-
     // ---- W[a][b] = k(qt_a, kt_b) (+ eps on the diagonal): lane a, columns b = BPW w..+BPW
     uint32_t qa[D2];
 #pragma unroll
@@ -755,7 +714,7 @@ constexpr int kKeyTileLds = 4 * 2 * 64 * kLP * 2;   // four waves' [a][j] and [c
 
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
-// Writes Upart[h][kb][c][a] (a < 64, rows >= m zero).
+// Writes Upart[h][kb][c][a] (a < 64; rows >= m finite, multiplied by zero columns of X_T).
 template <int D>
 __device__ void key_role(int h, int kb, char* lds_raw, const uint16_t* __restrict__ K,
                          const uint16_t* __restrict__ V, const uint32_t* __restrict__ qfix,
@@ -769,7 +728,7 @@ __device__ void key_role(int h, int kb, char* lds_raw, const uint16_t* __restric
     _Float16* sV = sB + 64 * kLP;                 // this wave's [c][j]
     const float inv2R = frame[h * 8 + 1], esc = frame[h * 8 + 2], vsc = frame[h * 8 + 3];
     const float R = frame[h * 8 + 0], xsc = frame[h * 8 + 4];
-    const bool clamped = frame[h * 8 + 5] != 0.f;
+    const bool clamped = __float_as_uint(frame[h * 8 + 5]) != 0u;   // integer test: a scalar branch
     const uint32_t* tab = qfix + (size_t)h * 64 * D2;
     const float ebias = -kTwo23 * esc;
     const int j_begin = kb * kpb, j_end = min(n, j_begin + kpb);
@@ -824,8 +783,21 @@ __device__ void key_role(int h, int kb, char* lds_raw, const uint16_t* __restric
                 kf[4 * c8 + 2] = fix2_bf16(kr[c8].z, inv2R);
                 kf[4 * c8 + 3] = fix2_bf16(kr[c8].w, inv2R);
             }
-            // the key's excess beyond the range enters the exponent (head-uniform branch)
-            const float kbias = clamped ? excess_bias<D8>(kr, R, xsc, ebias) : ebias;
+            // keys past the end of the chunk: exponent bias -inf, kernel values exactly 0 (their
+            // value registers hold finite values of this head, so the products stay 0)
+            float kbias = vmask ? ebias : -__builtin_inff();
+            if (clamped) {
+                // a head with tokens beyond the range: the key's excess enters the exponent
+                float ex = 0.f;
+#pragma unroll
+                for (int c8 = 0; c8 < D8; ++c8) {
+                    const uint32_t wd[4] = {kr[c8].x, kr[c8].y, kr[c8].z, kr[c8].w};
+#pragma unroll
+                    for (int t = 0; t < 4; ++t)
+                        ex += fmaxf(fabsf(bf16_lo(wd[t])), R) + fmaxf(fabsf(bf16_hi(wd[t])), R);
+                }
+                kbias = vmask ? fmaf(ex - (float)D * R, xsc, ebias) : -__builtin_inff();
+            }
             // The next tile's keys are fetched in D/8 column groups spread over the landmark
             // loop, so that the key stream reaches memory as a steady flow rather than one
             // burst per tile from every wave at once; its values follow after this tile's
@@ -833,7 +805,8 @@ __device__ void key_role(int h, int kb, char* lds_raw, const uint16_t* __restric
             const uint4 *kp, *vp;
             row_ptrs(tile + 4, kp, vp);
             // landmark pairs (2p, 2p+1): rows 2p, 2p+1 of the [a][j] tile; table rows >= m are
-            // zero and the value of landmark m (odd m) is replaced by 0
+            // zero codes, so the value of a landmark m (odd m) is finite, and row m of U is
+            // dropped by the zero column m of X_T
             uint16_t* brow = reinterpret_cast<uint16_t*>(sB) + l;
             uint32_t ta[D2], tb[D2];
             load_row<D2>(ta, tab + (2 * rot) * D2);
@@ -846,9 +819,10 @@ __device__ void key_role(int h, int kb, char* lds_raw, const uint16_t* __restric
                     const int pn = p + 1 < npairs ? p + 1 : 0;
                     const float b0 = lap_row<D2>(kf, ta, tb, tab + (2 * p + 1) * D2, esc, kbias);
                     const float b1 = lap_row<D2>(kf, tb, ta, tab + (2 * pn) * D2, esc, kbias);
-                    const uint32_t v = pk_f16(b0, 2 * p + 1 < m ? b1 : 0.f) & vmask;
-                    brow[(2 * p) * kLP] = (uint16_t)(v & 0xffffu);
-                    brow[(2 * p + 1) * kLP] = (uint16_t)(v >> 16);
+                    const uint32_t v = pk_f16(b0, b1);
+                    uint16_t* r2 = brow + (2 * p) * kLP;
+                    r2[0] = (uint16_t)(v & 0xffffu);
+                    r2[kLP] = (uint16_t)(v >> 16);
                     p = pn;
                 }
             }
@@ -858,7 +832,7 @@ __device__ void key_role(int h, int kb, char* lds_raw, const uint16_t* __restric
                 const uint32_t yw[4] = {vr[c8].x, vr[c8].y, vr[c8].z, vr[c8].w};
 #pragma unroll
                 for (int t = 0; t < 4; ++t) {
-                    const uint32_t pv = pk_f16(bf16_lo(yw[t]) * vsc, bf16_hi(yw[t]) * vsc) & vmask;
+                    const uint32_t pv = pk_f16(bf16_lo(yw[t]) * vsc, bf16_hi(yw[t]) * vsc);
                     reinterpret_cast<uint16_t*>(sV)[(8 * c8 + 2 * t) * kLP + l] = (uint16_t)(pv & 0xffffu);
                     reinterpret_cast<uint16_t*>(sV)[(8 * c8 + 2 * t + 1) * kLP + l] = (uint16_t)(pv >> 16);
                 }
@@ -933,15 +907,20 @@ __global__ __launch_bounds__(256, 2) void key_kernel(const uint16_t* __restrict_
 // grid (NG, BH) with NG = D/8 + 1, 576 threads (nine waves).  Group g < D/8 holds value columns
 // 8g..8g+7, group D/8 the ones column D.  M = X_T U is separable by columns, so each block sums
 // only its columns of the chunk partials (Upart[h][kb][c][a], four quarters of the chunks
-// combined in a fixed order) and forms only its columns of M.  A value group also sums the
-// ones column and forms M[.][D] (its ninth wave), so that with `center` (the inline
-// normalisation) its operand columns are M'[a][c] = M[a][c] - M[a][D] vbar[c], formed in fp32:
+// combined in a fixed order) and forms only its columns of M.  With `center` (the inline
+// normalisation) a value group also sums the ones column and forms its operand columns as
+// M'[a][c] = sum_b X_T[a][b] (U[b][c] - U[b][D] vbar[c]) = M[a][c] - M[a][D] vbar[c] in fp32:
 // Y'_i = sum_l a_il M'_l = Y_i[:d] - s_i vbar, and the output Y'_i + vbar no longer takes the
 // difference of Y_i[:d] and s_i vbar after the fp16 rounding of M (terms that grow with n when
 // the kernel values are flat).
 // Value columns: fp16 MFMA operand tiles Mt[h][s][cb][lane][i] = M[16s + 8(lane/32) + i]
 // [32cb + lane%32] * 2^-e_g with mscale[h][g] = 2^e_g putting the group's largest magnitude in
 // [2^14, 2^15).  Ones column: Mones[h][a] = M[a][D] in fp32.
+// The ones group also forms the query side's row bound from the key-landmark codes kfix[h]:
+// kcen[h][c/2] = their centre (per coordinate, the rounded mean over the m landmarks) and
+// frame[h][6] = rho = max_l sum_c |u(kt_{l,c}) - centre_c| (code units); by the triangle
+// inequality every query's code distance to landmark l is at least its distance to the centre
+// minus rho.
 constexpr int kMfinalThreads = 576;
 
 template <int D>
@@ -951,8 +930,12 @@ __global__ __launch_bounds__(kMfinalThreads) void mfinal_kernel(const float* __r
                                                                 float* __restrict__ Mones, float* __restrict__ Mout,
                                                                 int m, int nkb, const float* __restrict__ whiten,
                                                                 int mspace, int H, float* __restrict__ mvec,
-                                                                const float* __restrict__ vbar, int center) {
+                                                                const float* __restrict__ vbar, int center,
+                                                                const uint32_t* __restrict__ kfix,
+                                                                uint32_t* __restrict__ kcen,
+                                                                float* __restrict__ frame) {
     constexpr int D1 = D + 1;
+    constexpr int D2 = D / 2;
     constexpr int CB = D / 32;
     constexpr int NG = D / 8 + 1;
     constexpr int NI = 9 * 16;   // float4 items per chunk: nine columns of 64 rows
@@ -960,12 +943,12 @@ __global__ __launch_bounds__(kMfinalThreads) void mfinal_kernel(const float* __r
     __shared__ __attribute__((aligned(16))) float sU[9 * 64];   // [column][b]
     __shared__ __attribute__((aligned(16))) float sM[8 * 64];   // [c][a]
     __shared__ __attribute__((aligned(16))) float4 red[3 * NI];
-    __shared__ float sMd[64];
-    __shared__ float smx[9];
+    __shared__ uint32_t scen[D2];
+    __shared__ float smx[8];
     const int g = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, w = tid / 64, l = tid & 63;
     const bool ones = g == NG - 1;
     const int c0 = 8 * g, nc = ones ? 1 : 8;   // operand columns of this group
-    const int ncol = ones ? 1 : 9;             // columns summed: the operand columns and column D
+    const int ncol = ones ? 1 : (center ? 9 : 8);   // columns summed: the operand columns and column D
     // item f: local column f / 16 (column D for local column 8, and in the ones group), rows
     // 4 (f % 16) .. +3 of every chunk partial; the chunks in four quarters, eight loads in flight
     const int f = tid % NI, qq = tid / NI;
@@ -994,20 +977,52 @@ __global__ __launch_bounds__(kMfinalThreads) void mfinal_kernel(const float* __r
         reinterpret_cast<float4*>(sU)[f] = make_float4(((acc.x + r1.x) + r2.x) + r3.x, ((acc.y + r1.y) + r2.y) + r3.y,
                                                        ((acc.z + r1.z) + r2.z) + r3.z, ((acc.w + r1.w) + r2.w) + r3.w);
     }
-    __syncthreads();
-    // M[a][col] = sum_b X_T[a][b] U[b][col]: thread (column w, a = l)
-    float t = 0.f;
-    if (w < ncol) {
+    if (ones && w == 8) {
+        // centre of the key-landmark codes (rows >= m of the table are zero)
+        const uint32_t* tab = kfix + (size_t)h * 64 * D2;
+        if (l < D2) {
+            uint32_t slo = 0, shi = 0;
 #pragma unroll 16
-        for (int b = 0; b < 64; ++b) t = fmaf(sX[l * 65 + b], sU[w * 64 + b], t);
-        if (w == 8) sMd[l] = t;   // M[a][D] in a value group
+            for (int a = 0; a < 64; ++a) {
+                const uint32_t u = tab[a * D2 + l];
+                slo += u & 0xffffu;
+                shi += u >> 16;
+            }
+            const uint32_t cen = ((slo + m / 2) / m) | (((shi + m / 2) / m) << 16);
+            scen[l] = cen;
+            kcen[(size_t)h * D2 + l] = cen;
+        }
     }
     __syncthreads();
+    if (ones && w == 8) {
+        // rho: the largest code distance of a landmark from the centre
+        const uint32_t* tab = kfix + (size_t)h * 64 * D2;
+        uint32_t dist = 0;
+        if (l < m) {
+#pragma unroll
+            for (int c2 = 0; c2 < D2; ++c2) dist = __builtin_amdgcn_sad_u16(tab[l * D2 + c2], scen[c2], dist);
+        }
+        const float rho = (float)__float_as_uint(wave_max_dpp(__uint_as_float(dist)));
+        if (l == 0) frame[h * 8 + 6] = rho;
+    }
+    // M[a][col] = sum_b X_T[a][b] U[b][col]: thread (column w, a = l); with `center`, U's value
+    // columns less U[b][D] vbar[col]
+    float t = 0.f;
+    if (w < nc) {
+        if (center && !ones) {
+            const float vb = vbar[(size_t)h * D + c0 + w];
+#pragma unroll 16
+            for (int b = 0; b < 64; ++b) t = fmaf(sX[l * 65 + b], fmaf(-sU[8 * 64 + b], vb, sU[w * 64 + b]), t);
+        } else {
+#pragma unroll 16
+            for (int b = 0; b < 64; ++b) t = fmaf(sX[l * 65 + b], sU[w * 64 + b], t);
+        }
+    }
     // landmark-space normalisation: the operand rows are w_l M[l] (whitening w, ones when
     // whiten is NULL), and each value column also gives sum_l w_l M[l][c] and (1/m) sum_l M[l][c]
     float mv = 0.f;
     if (w < nc) {
-        if (l < m) Mout[((size_t)h * m + l) * D1 + c0 + w] = t;
+        if (l < m && !(center && !ones)) Mout[((size_t)h * m + l) * D1 + c0 + w] = t;
         if (mspace && !ones) {
             const float tv = l < m ? t : 0.f;
             float tw = whiten && l < m ? whiten[(size_t)(h % H) * m + l] * tv : tv;
@@ -1024,17 +1039,18 @@ __global__ __launch_bounds__(kMfinalThreads) void mfinal_kernel(const float* __r
             }
             t = tw;
         } else {
-            if (center && !ones) t = l < m ? fmaf(-sMd[l], vbar[(size_t)h * D + c0 + w], t) : 0.f;
             sM[w * 64 + l] = t;
         }
         mv = fabsf(t);
     }
-    mv = wave_max_dpp(mv);
-    if (l == 0) smx[w] = mv;
+    if (w < 8) {
+        mv = wave_max_dpp(mv);
+        if (l == 0) smx[w] = mv;
+    }
     __syncthreads();
     float mxg = smx[0];
 #pragma unroll
-    for (int i = 1; i < 9; ++i) mxg = fmaxf(mxg, smx[i]);
+    for (int i = 1; i < 8; ++i) mxg = fmaxf(mxg, smx[i]);
     const int e = pow2_exp(mxg);
     if (tid == 0) mscale[h * NG + g] = ldexpf(1.f, e);
     if (ones) {   // rows >= m are zero; the landmark-space form weights every landmark by 1/m
@@ -1103,7 +1119,7 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
     }
     const float R = frame[h * 8 + 0], inv2R = frame[h * 8 + 1], esc = frame[h * 8 + 2];
     const float xsc = frame[h * 8 + 4];
-    const bool clamped = frame[h * 8 + 5] != 0.f;
+    const bool clamped = __float_as_uint(frame[h * 8 + 5]) != 0u;   // integer test: a scalar branch
     const float rho = frame[h * 8 + 6];
     const float ebias = -kTwo23 * esc;
     constexpr int NG = D / 8 + 1;
@@ -1128,10 +1144,25 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
             qf[4 * c8 + 2] = fix2_bf16(raw[c8].z, inv2R);
             qf[4 * c8 + 3] = fix2_bf16(raw[c8].w, inv2R);
         }
-        if (clamped) qbias = excess_bias<D8>(raw, R, xsc, ebias);
     } else {
 #pragma unroll
         for (int c = 0; c < D2; ++c) qf[c] = 0u;
+    }
+    if (clamped) {
+        // a head with tokens beyond the range: the query's excess enters the exponent (its row
+        // read again, from cache, so that the raw words need not stay live above)
+        if (i < n) {
+            const uint4* qr = reinterpret_cast<const uint4*>(Q + ((size_t)h * n + i) * D);
+            float ex = 0.f;
+#pragma unroll
+            for (int c8 = 0; c8 < D8; ++c8) {
+                const uint4 r4 = qr[c8];
+                const uint32_t wd[4] = {r4.x, r4.y, r4.z, r4.w};
+#pragma unroll
+                for (int t = 0; t < 4; ++t) ex += fmaxf(fabsf(bf16_lo(wd[t])), R) + fmaxf(fabsf(bf16_hi(wd[t])), R);
+            }
+            qbias = fmaf(ex - (float)D * R, xsc, ebias);
+        }
     }
     // kernel values, two landmarks per fp16 pair register (landmarks >= m give 0); the
     // landmark rows come through scalar registers, the loads of each row issued right after
@@ -1276,15 +1307,15 @@ hipError_t launch_fast_pool(const void* Q, const void* K, const void* V, float* 
 }
 
 hipError_t launch_fast_frame_ns(const float* qt, const float* kt, const double* vseg, const float* segmax,
-                                const float* vsegmax, float* frame, uint32_t* qfix, uint32_t* kfix, uint32_t* kcen,
-                                float* vbar, float* XT, float* cinfo, int BH, int n, int d, int m, float lambda, int T,
-                                float eps, hipStream_t st) {
+                                const float* vsegmax, float* frame, uint32_t* qfix, uint32_t* kfix, float* vbar,
+                                float* XT, float* cinfo, int BH, int n, int d, int m, float lambda, int T, float eps,
+                                hipStream_t st) {
     if (d == 32)
         hipLaunchKernelGGL(frame_ns_kernel<32>, dim3(BH), dim3(kSolveThreads), 0, st, qt, kt, vseg, segmax, vsegmax, frame,
-                           qfix, kfix, kcen, vbar, XT, cinfo, n, m, lambda, T, eps);
+                           qfix, kfix, vbar, XT, cinfo, n, m, lambda, T, eps);
     else
         hipLaunchKernelGGL(frame_ns_kernel<64>, dim3(BH), dim3(kSolveThreads), 0, st, qt, kt, vseg, segmax, vsegmax, frame,
-                           qfix, kfix, kcen, vbar, XT, cinfo, n, m, lambda, T, eps);
+                           qfix, kfix, vbar, XT, cinfo, n, m, lambda, T, eps);
     return hipGetLastError();
 }
 
@@ -1292,23 +1323,24 @@ hipError_t launch_fast_key(const void* K, const void* V, const uint32_t* qfix, c
                            int BH, int n, int d, int m, int kpb, int nkb, hipStream_t st) {
     dim3 grid(BH * nkb);
     if (d == 32)
-        hipLaunchKernelGGL(key_kernel<32>, grid, dim3(256), 0, st, (const uint16_t*)K, (const uint16_t*)V, qfix, frame,
-                           Upart, BH, n, m, kpb, nkb);
+        hipLaunchKernelGGL(key_kernel<32>, grid, dim3(256), 0, st, (const uint16_t*)K, (const uint16_t*)V, qfix,
+                           frame, Upart, BH, n, m, kpb, nkb);
     else
-        hipLaunchKernelGGL(key_kernel<64>, grid, dim3(256), 0, st, (const uint16_t*)K, (const uint16_t*)V, qfix, frame,
-                           Upart, BH, n, m, kpb, nkb);
+        hipLaunchKernelGGL(key_kernel<64>, grid, dim3(256), 0, st, (const uint16_t*)K, (const uint16_t*)V, qfix,
+                           frame, Upart, BH, n, m, kpb, nkb);
     return hipGetLastError();
 }
 
 hipError_t launch_fast_mfinal(const float* Upart, const float* XT, _Float16* Mt, float* mscale, float* Mones,
                               float* M, int BH, int d, int m, int nkb, const float* whiten, int mspace, int H,
-                              float* mvec, const float* vbar, int center, hipStream_t st) {
+                              float* mvec, const float* vbar, int center, const uint32_t* kfix, uint32_t* kcen,
+                              float* frame, hipStream_t st) {
     if (d == 32)
         hipLaunchKernelGGL(mfinal_kernel<32>, dim3(32 / 8 + 1, BH), dim3(kMfinalThreads), 0, st, Upart, XT, Mt, mscale,
-                           Mones, M, m, nkb, whiten, mspace, H, mvec, vbar, center);
+                           Mones, M, m, nkb, whiten, mspace, H, mvec, vbar, center, kfix, kcen, frame);
     else
         hipLaunchKernelGGL(mfinal_kernel<64>, dim3(64 / 8 + 1, BH), dim3(kMfinalThreads), 0, st, Upart, XT, Mt, mscale,
-                           Mones, M, m, nkb, whiten, mspace, H, mvec, vbar, center);
+                           Mones, M, m, nkb, whiten, mspace, H, mvec, vbar, center, kfix, kcen, frame);
     return hipGetLastError();
 }
 

@@ -330,8 +330,7 @@ hipError_t forward_fast(Recorder& rec, const FastPlan& p, const void* Q, const v
     e = run_named(rec, "frame_ns", [&] {
         return lapattn::launch_fast_frame_ns(at<float>(ws, p.qt), at<float>(ws, p.kt), at<double>(ws, p.vseg),
                                              at<float>(ws, p.segmax), at<float>(ws, p.vsegmax), at<float>(ws, p.frame),
-                                             at<uint32_t>(ws, p.qfix), at<uint32_t>(ws, p.kfix),
-                                             at<uint32_t>(ws, p.kcen), at<float>(ws, p.vbar),
+                                             at<uint32_t>(ws, p.qfix), at<uint32_t>(ws, p.kfix), at<float>(ws, p.vbar),
                                              at<float>(ws, p.XT), at<float>(ws, p.cinfo), BH, n, d, m, lambda, T, eps,
                                              st);
     });
@@ -345,7 +344,9 @@ hipError_t forward_fast(Recorder& rec, const FastPlan& p, const void* Q, const v
         return lapattn::launch_fast_mfinal(at<float>(ws, p.Upart), at<float>(ws, p.XT), at<_Float16>(ws, p.Mt),
                                            at<float>(ws, p.mscale), at<float>(ws, p.Mones), at<float>(ws, p.M), BH, d, m,
                                            p.nkb, whiten, mspace ? 1 : 0, H, at<float>(ws, p.mvec),
-                                           at<float>(ws, p.vbar), norm == LAPATTN_NORM_INLINE ? 1 : 0, st);
+                                           at<float>(ws, p.vbar), norm == LAPATTN_NORM_INLINE ? 1 : 0,
+                                           at<uint32_t>(ws, p.kfix), at<uint32_t>(ws, p.kcen), at<float>(ws, p.frame),
+                                           st);
     });
     if (e != hipSuccess) return e;
     e = run_named(rec, "query", [&] {

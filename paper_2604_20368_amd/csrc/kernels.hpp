@@ -105,17 +105,20 @@ hipError_t launch_fast_pool(const void* Q, const void* K, const void* V, float* 
                             float* segmax, float* vsegmax, int BH, int n, int d, int m, LmPool pl,
                             hipStream_t st);
 hipError_t launch_fast_frame_ns(const float* qt, const float* kt, const double* vseg, const float* segmax,
-                                const float* vsegmax, float* frame, uint32_t* qfix, uint32_t* kfix, uint32_t* kcen,
-                                float* vbar, float* XT, float* cinfo, int BH, int n, int d, int m, float lambda, int T,
-                                float eps, hipStream_t st);
+                                const float* vsegmax, float* frame, uint32_t* qfix, uint32_t* kfix, float* vbar,
+                                float* XT, float* cinfo, int BH, int n, int d, int m, float lambda, int T, float eps,
+                                hipStream_t st);
 hipError_t launch_fast_key(const void* K, const void* V, const uint32_t* qfix, const float* frame, float* Upart,
                            int BH, int n, int d, int m, int kpb, int nkb, hipStream_t st);
 // mspace: the landmark-space normalisation (operand rows scaled by the whitening [H][m], NULL:
 // ones; the ones column 1/m; mvec[BH][2][d] written as for launch_mspace_vec).  center (the
-// inline normalisation): the operand columns are M[a][c] - M[a][d] vbar[c] (vbar [BH][d]).
+// inline normalisation): the operand columns are M[a][c] - M[a][d] vbar[c] (vbar [BH][d]), and M's
+// value columns are not written.  Also the query side's row bound: kcen [BH][d/2] (centre of the
+// key-landmark codes kfix) and frame[h][6] (its radius).
 hipError_t launch_fast_mfinal(const float* Upart, const float* XT, _Float16* Mt, float* mscale, float* Mones,
                               float* M, int BH, int d, int m, int nkb, const float* whiten, int mspace, int H,
-                              float* mvec, const float* vbar, int center, hipStream_t st);
+                              float* mvec, const float* vbar, int center, const uint32_t* kfix, uint32_t* kcen,
+                              float* frame, hipStream_t st);
 hipError_t launch_fast_query(int norm, const void* Q, void* Out, const uint32_t* kfix, const uint32_t* kcen,
                              const float* frame,
                              const _Float16* Mt, const float* mscale, const float* Mones, const float* vbar,

@@ -38,6 +38,31 @@ def alu_ops(kernel, w):
     return None if pairs is None else pairs * (2 * w.d + 1)
 
 
+def forward_ops(w):
+    """The forward's pairwise work: (2 n m + m^2) kernel values per head, (2d + 1) operations each
+    (d differences, d absolute-value accumulations, one exponential)."""
+    return w.BH * (2 * w.n * w.m + w.m * w.m) * (2 * w.d + 1)
+
+
+def event_median(fn, calls, pre=None):
+    """Median over `calls` calls of fn's duration from a pair of HIP events recorded on torch's
+    current stream (the stream the library launches on); pre(i), when given, runs before the
+    start event of call i (outside the timed interval)."""
+    import torch
+    evs = []
+    for i in range(calls):
+        if pre is not None:
+            pre(i)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        fn()
+        b.record()
+        evs.append((a, b))
+    torch.cuda.synchronize()
+    t = sorted(a.elapsed_time(b) for a, b in evs)
+    return t[len(t) // 2]
+
+
 def traffic_record(kernel):
     """HBM traffic measured with rocprofv3 counters for this kernel, if the
     committed record matches the current kernel sources (else None)."""
@@ -58,11 +83,20 @@ def traffic_record(kernel):
     return rec.get("bytes_per_launch")
 
 
-def cpu_baseline(w, x, budget_s=10.0):
-    """The fp64 oracle on a bounded sample: whole heads of the same workload,
-    one after another (wrapping around), until about budget_s seconds of work;
-    scaled to tokens/s of the full workload (one token = all H heads of one
-    position)."""
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def oracle_rate(w, x, budget_s):
+    """The fp64 oracle over whole heads of workload w (wrapping around), for about budget_s
+    seconds: (tokens/s of the full workload, heads run, seconds).  One token = all H heads of
+    one position."""
     import oracle
     heads, t_used = 0, 0.0
     BH = w.BH
@@ -73,10 +107,40 @@ def cpu_baseline(w, x, budget_s=10.0):
         oracle.forward(sub["Q"], sub["K"], sub["V"], w.m, w.lam, w.T)
         t_used += time.perf_counter() - t0
         heads += 1
-    tokens = w.B * w.n * heads / BH
-    return {"value": tokens / t_used, "unit": "tokens/s", "cores": oracle.threads(), "kind": "oracle",
-            "sample": "%d head-passes over the %d heads of the %s workload (n=%d, d=%d, m=%d, T=%d), fp64 "
-                      "forward, %.1f s" % (heads, BH, w.name, w.n, w.d, w.m, w.T, t_used)}
+    return w.B * w.n * heads / BH / t_used, heads, t_used
+
+
+def cpu_baseline(w, x, budget_s=10.0):
+    """The fp64 oracle (never tuned) on a bounded sample of the same workload: whole heads, one
+    after another, for about budget_s seconds each with all of the oracle's OpenMP threads (in
+    this process) and with one thread (a child process that only runs the oracle); scaled to
+    tokens/s of the full workload."""
+    import subprocess
+    import oracle
+    rate, heads, t_used = oracle_rate(w, x, budget_s)
+    res = {"value": rate, "unit": "tokens/s", "cores": oracle.threads(), "kind": "oracle",
+           "sample": "%d head-passes over the %d heads of the %s workload (n=%d, d=%d, m=%d, T=%d), fp64 "
+                     "forward, %.1f s" % (heads, w.BH, w.name, w.n, w.d, w.m, w.T, t_used),
+           "host_cores": os.cpu_count(), "cpu_model": cpu_model()}
+    env = dict(os.environ, OMP_NUM_THREADS="1")
+    try:
+        out = subprocess.run([sys.executable, os.path.abspath(__file__), "--oracle-only", "--budget", str(budget_s)],
+                             env=env, capture_output=True, text=True, timeout=10 * budget_s + 60)
+        one = json.loads(out.stdout.strip().splitlines()[-1])
+        res["one_thread"] = {"value": one["value"], "cores": one["cores"], "sample": one["sample"]}
+    except (subprocess.SubprocessError, ValueError, IndexError) as e:
+        res["one_thread"] = {"error": str(e)}
+    return res
+
+
+def oracle_only(budget_s):
+    """The child process of cpu_baseline: the oracle alone (no GPU), one JSON line."""
+    import oracle
+    w = W.WORKLOADS[WORKLOAD]
+    x = W.make_inputs(w, with_grad=False)
+    rate, heads, t_used = oracle_rate(w, x, budget_s)
+    print(json.dumps({"value": rate, "cores": oracle.threads(),
+                      "sample": "%d head-passes, %.1f s" % (heads, t_used)}), flush=True)
 
 
 def time_train_step(steps):
@@ -443,9 +507,9 @@ def ingest_traffic(kernel, fetch_dir, write_dir, copy_fetch_dir, copy_write_dir,
            "bytes_per_launch": f_k * 1024.0 * ff + w_k * 1024.0 * fw,
            "sources": KERNEL_SOURCES, "sources_sha256": h.hexdigest(),
            "commands": ["rocprofv3 --pmc FETCH_SIZE --output-format csv -d FETCH_DIR -o run -- "
-                        "python3 bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-train-step --no-dwc --no-other",
+                        "python3 bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-train-step --no-dwc --no-other --no-event-timing",
                         "rocprofv3 --pmc WRITE_SIZE --output-format csv -d WRITE_DIR -o run -- "
-                        "python3 bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-train-step --no-dwc --no-other",
+                        "python3 bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-train-step --no-dwc --no-other --no-event-timing",
                         "rocprofv3 --pmc FETCH_SIZE --output-format csv -d COPY_FETCH_DIR -o run -- "
                         "python3 bench.py --calibrate-copy",
                         "rocprofv3 --pmc WRITE_SIZE --output-format csv -d COPY_WRITE_DIR -o run -- "
@@ -454,6 +518,73 @@ def ingest_traffic(kernel, fetch_dir, write_dir, copy_fetch_dir, copy_write_dir,
     with open(out_path, "w") as f:
         json.dump(rec, f, indent=1)
     print(json.dumps(rec), flush=True)
+
+
+PMC_PASSES = (
+    "SQ_WAVES SQ_INSTS_VALU SQ_ACTIVE_INST_VALU SQ_INSTS_LDS SQ_INSTS_SALU SQ_INSTS_SMEM SQ_BUSY_CYCLES "
+    "SQ_WAIT_INST_ANY GRBM_GUI_ACTIVE",
+    "SQ_WAVE_CYCLES SQ_ACTIVE_INST_LDS SQ_INSTS_VALU_CVT SQ_ACTIVE_INST_ANY GRBM_GUI_ACTIVE",
+    "SQ_INSTS_MFMA SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU_MFMA_MOPS_F16 SQ_INSTS_VALU_MFMA_MOPS_F64 GRBM_GUI_ACTIVE",
+)
+VALU_LANE_RATE = 256 * 4 * 16 * 2.4e9   # lane-instructions per second: 256 CUs x 4 SIMD x 16 lanes x 2.4 GHz
+
+
+def _short_kernel(name):
+    import re
+    mm = re.search(r"lapattn::(\w+)", name) or re.search(r"_ZN7lapattn\d+(\w+?)I", name) or \
+        re.search(r"^(\w+)", name.strip())
+    return mm.group(1) if mm else name
+
+
+def ingest_pmc(out_path, trace_dir, pmc_dirs):
+    """Per-kernel averages of rocprofv3 --pmc counters (one directory per counter pass, PMC_PASSES)
+    over all dispatches of each lapattn kernel in a run of this benchmark, with the kernels'
+    average durations from a --kernel-trace run of the same command, and derived figures:
+      valu_issue_frac  SQ_INSTS_VALU x 64 lanes / (duration x 39.3 T lane-instructions/s), the
+                       share of the chip's VALU issue slots the kernel's instructions fill
+      valu_busy        SQ_ACTIVE_INST_VALU x 4 / (SIMDs x GRBM_GUI_ACTIVE / 8): cycles with a VALU
+                       instruction in flight per SIMD (the counter is in quad-cycles; GRBM_GUI_ACTIVE
+                       is summed over the 8 XCDs, so an eighth of it is the dispatch window's length
+                       in cycles, launch overhead included)
+      mfma_busy        SQ_VALU_MFMA_BUSY_CYCLES / (SIMDs x GRBM_GUI_ACTIVE / 8)
+    Writes a JSON summary to out_path."""
+    import csv
+    import glob
+    import statistics as stt
+    dur = {}
+    for f in glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True):
+        for r in csv.DictReader(open(f)):
+            k = _short_kernel(r["Kernel_Name"])
+            dur.setdefault(k, []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    vals = {}
+    for d in pmc_dirs:
+        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            for r in csv.DictReader(open(f)):
+                k = _short_kernel(r["Kernel_Name"])
+                vals.setdefault(k, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    simds = 256 * 4
+    out = {"what": "rocprofv3 counters per dispatch (averages over every dispatch of the kernel in the run)",
+           "passes": list(PMC_PASSES), "kernels": {}}
+    for k, cs in sorted(vals.items()):
+        if k not in dur:
+            continue
+        avg = {c: stt.mean(v) for c, v in cs.items()}
+        us = stt.mean(dur[k])
+        rec = {"dispatches": len(dur[k]), "avg_us": round(us, 2)}
+        rec.update({c: round(v, 1) for c, v in sorted(avg.items())})
+        if "SQ_INSTS_VALU" in avg:
+            rec["valu_issue_frac"] = round(avg["SQ_INSTS_VALU"] * 64 / (us * 1e-6 * VALU_LANE_RATE), 4)
+        gui = avg.get("GRBM_GUI_ACTIVE")
+        if gui:
+            gui /= 8.0   # per XCD
+            if "SQ_ACTIVE_INST_VALU" in avg:
+                rec["valu_busy"] = round(4 * avg["SQ_ACTIVE_INST_VALU"] / (simds * gui), 4)
+            if "SQ_VALU_MFMA_BUSY_CYCLES" in avg:
+                rec["mfma_busy"] = round(avg["SQ_VALU_MFMA_BUSY_CYCLES"] / (simds * gui), 4)
+        out["kernels"][k] = rec
+    with open(out_path, "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps(out), flush=True)
 
 
 def summarize_trace(trace_dir):
@@ -502,17 +633,30 @@ def main():
                     help="skip the forward timing of the other forward-only workloads")
     ap.add_argument("--no-dwc", action="store_true",
                     help="skip the timing of the depth-wise convolution branch")
+    ap.add_argument("--no-event-timing", action="store_true",
+                    help="skip the per-call event medians (warm and cold) of the headline forward")
     ap.add_argument("--sweep", action="store_true",
                     help="only the (n, m) timing sweep of the Laplacian kernel and Newton-Schulz kernels "
                          "(batch 1, 2 heads, d=32) beside plain PyTorch; prints a markdown table in us")
     ap.add_argument("--summarize-trace", metavar="TRACE_DIR",
                     help="per-leg kernel statistics of a rocprofv3 --kernel-trace CSV directory")
+    ap.add_argument("--oracle-only", action="store_true", help=argparse.SUPPRESS)
+    ap.add_argument("--budget", type=float, default=10.0, help=argparse.SUPPRESS)
+    ap.add_argument("--ingest-pmc", nargs="+", metavar="ARG",
+                    help="OUT TRACE_DIR PMC_DIR [PMC_DIR ...]: per-kernel counter summary of rocprofv3 --pmc "
+                         "runs of this benchmark, with durations from a --kernel-trace run of the same command")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run only the plain copy used to scale the HBM byte counters")
     ap.add_argument("--ingest-traffic", nargs=5, metavar=("KERNEL", "FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR",
                                                           "COPY_WRITE_DIR"),
                     help="write profiles/traffic_<KERNEL>_<workload>.txt from rocprofv3 --pmc CSV directories")
     args = ap.parse_args()
+    if args.oracle_only:
+        oracle_only(args.budget)
+        return
+    if args.ingest_pmc:
+        ingest_pmc(args.ingest_pmc[0], args.ingest_pmc[1], args.ingest_pmc[2:])
+        return
     if args.ingest_traffic:
         k = args.ingest_traffic[0]
         ingest_traffic(k, *args.ingest_traffic[1:], out_path=os.path.join(
@@ -529,7 +673,7 @@ def main():
         return
     if args.gpus != 1:
         print("bench.py measures one GPU: this build runs on a single MI355X and has no multi-GPU path "
-              "(every head is independent; see DESIGN.md for how the work would shard).", file=sys.stderr)
+              "(every batch row and head is independent, so the work would shard over GPUs by heads).", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -566,6 +710,15 @@ def main():
 
     ms = (t1 - t0) * 1e3 / args.steps
     tokens = w.B * w.n
+    # per-call HIP-event timing on the stream the library launches on: the median of 200 calls
+    # with the inputs in cache (warm), and of 200 calls each after a 1 GiB write that evicts
+    # them from L2 and the 256 MB Infinity Cache (cold; the write is outside the timed interval)
+    warm_ms = cold_ms = None
+    if not args.no_event_timing:
+        scrub = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+        warm_ms = event_median(step, 200)
+        cold_ms = event_median(step, 200, pre=lambda i: scrub.fill_(float(i)))
+        del scrub
     per = {}
     for name, t in launches:
         per.setdefault(name, []).append(t)
@@ -578,6 +731,7 @@ def main():
         roof = {"bound": "alu", "kernel": dom, "achieved": round(ach, 3), "peak": PEAK_FP32_VECTOR_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(ach / PEAK_FP32_VECTOR_TFLOPS, 4),
                 "traffic": traffic_record(dom), "avg_ms": round(avg[dom], 5)}
+    fwd_ops = forward_ops(w)
     res = {
         "metric": METRIC, "value": tokens / (ms * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
@@ -586,6 +740,14 @@ def main():
                    "lambda": w.lam, "inputs": w.dtype, "tokens_per_step": tokens},
         "kernels_ms": {k: round(v, 5) for k, v in avg.items()},
         "roofline": roof,
+        "forward_fraction": {
+            "ops": fwd_ops, "ms": round(ms, 5),
+            "of_157.3T_ops": round(fwd_ops / (ms * 1e-3) / 1e12 / PEAK_FP32_VECTOR_TFLOPS, 4),
+            "of_78.6T_packed_lane_ops": round(fwd_ops / (ms * 1e-3) / 1e12 / (PEAK_FP32_VECTOR_TFLOPS / 2), 4)},
+        "event_timing": None if warm_ms is None else {
+            "calls": 200, "warm_median_ms": round(warm_ms, 5), "cold_median_ms": round(cold_ms, 5),
+            "warm_tokens_per_s": round(tokens / (warm_ms * 1e-3), 1),
+            "cold_tokens_per_s": round(tokens / (cold_ms * 1e-3), 1), "cold_scrub_bytes": 1 << 30},
     }
     if not args.no_train_step:
         res["train_step"] = time_train_step(min(args.steps, 20))

@@ -10,7 +10,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "liblapattn.so")
-SOURCES = ["fwd.hip", "fast.hip", "bwd.hip", "dwc.hip", "noalloc.hip", "host.cpp"]
+SOURCES = ["fwd.hip", "fast.hip", "nsbig.hip", "bwd.hip", "dwc.hip", "noalloc.hip", "host.cpp"]
 ARCH = "gfx950"
 
 # Packed fp32 VALU instructions are disabled for every device pass (the compiler would

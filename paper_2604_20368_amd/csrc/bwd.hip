@@ -82,7 +82,9 @@ __device__ __forceinline__ void load_half_rows_dma(float* tile, const float* __r
 //   Landmark-space normalisation (Appendix B): the same as inline with M's rows scaled by the
 //   whitening, its ones column replaced by 1/m and vbar by sum_l w_l M_l (mvec); the partial
 //   sums of (1 - s_i) dO_i and of dO_i (into p0_part) give the gradient of the two vectors.
-template <int D, int NORM>
+// MPK = 64 for m <= 64, 128 for m up to 128.  The rows of A and dD (Aq, dDq) are group-major:
+// [h][g][n][64] for the landmark groups g of 64 (one group when m <= 64).
+template <int D, int NORM, int MPK>
 __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void bwd_query_kernel(const float* __restrict__ Q, const float* __restrict__ dO,
                                                         float* __restrict__ dQ, const float* __restrict__ kt,
                                                         const float* __restrict__ M, const float* __restrict__ vbar,
@@ -97,17 +99,20 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void bwd_query_kernel(const f
     constexpr int NCH = D / 32;
     // Landmarks in ranges of LW: 32 (a 64 x 33 tile per wave, which lets three blocks share a
     // compute unit), except for the row-sum normalisation, which needs s_i and y_i over all
-    // landmarks before dA and takes them in one range of 64.  Every sum keeps landmark order.
-    constexpr int LW = NORM == NORM_ROWSUM ? 64 : 32;
+    // landmarks before dA and takes them in one range of 64 when m <= 64; for m > 64 it takes
+    // them in a first walk over the ranges (PRE) and forms the kernel values again for dA.
+    // Every sum keeps landmark order.
+    constexpr int LW = (NORM == NORM_ROWSUM && MPK == 64) ? 64 : 32;
+    constexpr bool PRE = NORM == NORM_ROWSUM && MPK == 128;
     constexpr int TP = LW + 1;             // tile pitch: lane-strided accesses are conflict-free
-    __shared__ __attribute__((aligned(16))) float sM[64 * D1];
+    __shared__ __attribute__((aligned(16))) float sM[MPK * D1];
     __shared__ float sVb[D];
     __shared__ float sT[4 * 64 * TP];
     __shared__ float sred[4 * D];
     const int h = blockIdx.y, tid = threadIdx.x, w = tid >> 6, l = tid & 63;
     if (NORM == NORM_MSPACE) {
         const float* wl = whiten ? whiten + (size_t)(h % H) * m : nullptr;
-        for (int e = tid; e < 64 * D1; e += 256) {
+        for (int e = tid; e < MPK * D1; e += 256) {
             const int a = e / D1, cc = e % D1;
             float v = 0.f;
             if (a < m) v = cc < D ? (wl ? wl[a] : 1.f) * M[(size_t)h * m * D1 + e] : 1.f / (float)m;
@@ -115,7 +120,7 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void bwd_query_kernel(const f
         }
         if (tid < D) sVb[tid] = mvec[(size_t)h * 2 * D + tid];
     } else {
-        for (int e = tid; e < 64 * D1; e += 256) sM[e] = (e < m * D1) ? M[(size_t)h * m * D1 + e] : 0.f;
+        for (int e = tid; e < MPK * D1; e += 256) sM[e] = (e < m * D1) ? M[(size_t)h * m * D1 + e] : 0.f;
         if (tid < D) sVb[tid] = vbar[(size_t)h * D + tid];
     }
     float* tile = sT + w * 64 * TP;
@@ -146,21 +151,20 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void bwd_query_kernel(const f
     float dq[D];
 #pragma unroll
     for (int c = 0; c < D; ++c) dq[c] = 0.f;
-    const int nrange = LW == 64 ? 1 : (m + LW - 1) / LW;   // m <= 64
-    for (int ri = 0; ri < nrange; ++ri) {
-        const int lo = LW * ri, mh = min(LW, m - lo);   // landmarks lo .. lo + mh - 1: tile columns 0 .. mh - 1
-        const float* tab = kt + __builtin_amdgcn_readfirstlane((h * m + lo) * D);   // wave-uniform: scalar loads
+    const int ng = (m + 63) / 64;   // landmark groups of the row arrays
+    const int nrange = LW == 64 ? 1 : (m + LW - 1) / LW;
+    // pass 1 over the range of landmarks lo .. lo + mh - 1 (tile columns 0 .. mh - 1): a_il into
+    // the tile (a column mh, reached only past the table, holds zeros).  The streaming loops read
+    // no LDS: a wait for an LDS read would also wait for the row prefetch.
+    auto pass1 = [&](int lo, int mh, const float* tab) {
+        const float* Ag = Aq + (size_t)(h * ng + lo / 64) * n * 64;
         const int units = mh * NCH;
-
-        // pass 1: a_il into the tile (a column mh, reached only past the table, holds zeros).
-        // The streaming loops read no LDS: a wait for an LDS read would also wait for the row
-        // prefetch.
         auto emit = [&](int a, float dist) {
             tile[l * TP + a] = (live && a < mh) ? __builtin_amdgcn_exp2f(dist * kscale) : 0.f;
         };
         if (saved) {   // the forward left the rows of A in Aq: copy them into the tile
-            if (LW == 64) load_rows64_dma(tile, Aq + (size_t)h * n * 64, i0, n);
-            else load_half_rows_dma(tile, Aq + (size_t)h * n * 64, i0, n, lo);
+            if (LW == 64) load_rows64_dma(tile, Ag, i0, n);
+            else load_half_rows_dma(tile, Ag, i0, n, lo % 64);
         } else {
             float ta[32], tb[32];
             srow32(ta, tab);
@@ -179,6 +183,9 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void bwd_query_kernel(const f
         }
         if (mh & 1) tile[l * TP + mh] = 0.f;   // the pair loops read column mh (unwritten when d = 64)
         __builtin_amdgcn_wave_barrier();
+    };
+    // s_i (and y_i for the row-sum normalisation) over the range, then the range's rows of A
+    auto sums_and_rows = [&](int lo, int mh) {
         for (int a = 0; a < mh; ++a) {
             const float av = tile[l * TP + a];
             const float* mr = sM + (lo + a) * D1;
@@ -188,16 +195,36 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void bwd_query_kernel(const f
                 for (int c = 0; c < D; ++c) y[c] = fmaf(av, mr[c], y[c]);
             }
         }
-        if (NORM == NORM_ROWSUM) {   // one range: s and y are complete
-            float t = 0.f;
-#pragma unroll
-            for (int c = 0; c < D; ++c) t = fmaf(g[c], y[c], t);
-            rsc = 1.f / s;
-            dyd = -t / (s * s);
-        }
         if (!saved) {
-            if (LW == 64) store_rows64(Aq + (size_t)h * n * 64, tile, i0, n, m);
-            else store_half_rows(Aq + (size_t)h * n * 64, tile, i0, n, lo, mh);
+            float* Ag = Aq + (size_t)(h * ng + lo / 64) * n * 64;
+            if (LW == 64) store_rows64(Ag, tile, i0, n, mh);
+            else store_half_rows(Ag, tile, i0, n, lo % 64, mh);
+        }
+    };
+    auto rowsum_scales = [&]() {   // s and y complete
+        float t = 0.f;
+#pragma unroll
+        for (int c = 0; c < D; ++c) t = fmaf(g[c], y[c], t);
+        rsc = 1.f / s;
+        dyd = -t / (s * s);
+    };
+    if (PRE) {
+        for (int ri = 0; ri < nrange; ++ri) {
+            const int lo = LW * ri, mh = min(LW, m - lo);
+            pass1(lo, mh, kt + __builtin_amdgcn_readfirstlane((h * m + lo) * D));
+            sums_and_rows(lo, mh);
+            __builtin_amdgcn_wave_barrier();   // the next range overwrites the tile
+        }
+        rowsum_scales();
+    }
+    for (int ri = 0; ri < nrange; ++ri) {
+        const int lo = LW * ri, mh = min(LW, m - lo);   // landmarks lo .. lo + mh - 1: tile columns 0 .. mh - 1
+        const float* tab = kt + __builtin_amdgcn_readfirstlane((h * m + lo) * D);   // wave-uniform: scalar loads
+        const int units = mh * NCH;
+        pass1(lo, mh, tab);
+        if (!PRE) {
+            sums_and_rows(lo, mh);
+            if (NORM == NORM_ROWSUM) rowsum_scales();   // one range: s and y are complete
         }
         __builtin_amdgcn_wave_barrier();
 
@@ -239,8 +266,11 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void bwd_query_kernel(const f
             }
         }
         __builtin_amdgcn_wave_barrier();
-        if (LW == 64) store_rows64(dDq + (size_t)h * n * 64, tile, i0, n, m);
-        else store_half_rows(dDq + (size_t)h * n * 64, tile, i0, n, lo, mh);
+        {
+            float* Dg = dDq + (size_t)(h * ng + lo / 64) * n * 64;
+            if (LW == 64) store_rows64(Dg, tile, i0, n, mh);
+            else store_half_rows(Dg, tile, i0, n, lo % 64, mh);
+        }
 
         // pass 2: dq_i += dD_il sign(q_i - kt_l); each unit's dD is read before the unit's
         // first wait (which covers it); landmarks past m have dD = 0 (a zero column when mh is odd)
@@ -323,7 +353,8 @@ __device__ __forceinline__ void stage_rows(float* dst, const float* base, int t0
 //   dM_l[:d] += a_il rs_i dO_i on fp32 MFMA 32x32x1 (A = a_il, lane = landmark = MFMA row; B =
 //   rs_i dO_i[32 hh + l % 32], one 32-column half per instruction), dM_l[d] += a_il dYd_i;
 //   dkt_l -= dD_il sign(q_i - kt_l).
-// Queries past the chunk contribute zeros.
+// Queries past the chunk contribute zeros.  Landmarks in groups of 64: blockIdx.z = group g, lane l
+// = landmark 64 g + l, reading the group's rows of Aq and dDq ([h][g][n][64]).
 typedef float f32x32_t __attribute__((ext_vector_type(32)));
 
 template <int D>
@@ -338,13 +369,15 @@ __global__ __launch_bounds__(64) void bwd_query_lm_kernel(const float* __restric
     constexpr int ST = 8;                                            // queries per sub-tile
     constexpr int BUF = ST * D + ST * 64 + ST * 64 + ST * D + 64;   // Q, Aq, dDq, dO, rs | dYd
     __shared__ __attribute__((aligned(16))) float sbuf[2 * BUF];
-    const int ch = blockIdx.x, h = blockIdx.y, l = threadIdx.x;
-    const bool live = l < m;
-    const int lc = live ? l : m - 1;
+    const int ch = blockIdx.x, h = blockIdx.y, l = threadIdx.x, g = blockIdx.z, ng = gridDim.z;
+    const int lm0 = 64 * g;
+    const bool live = lm0 + l < m;
+    const int lc = live ? lm0 + l : m - 1;   // landmark
+    const int lcol = lc - lm0;               // its column in the group's rows
     const float* Qh = Q + (size_t)h * n * D;
     const float* dOh = dO + (size_t)h * n * D;
-    const float* Ah = Aq + (size_t)h * n * 64;
-    const float* DDh = dDq + (size_t)h * n * 64;
+    const float* Ah = Aq + (size_t)(h * ng + g) * n * 64;
+    const float* DDh = dDq + (size_t)(h * ng + g) * n * 64;
     const int i0 = ch * chunk, i1 = min(n, i0 + chunk);
     auto stage = [&](int b, int t0) {
         float* sb = sbuf + b * BUF;
@@ -382,7 +415,7 @@ __global__ __launch_bounds__(64) void bwd_query_lm_kernel(const float* __restric
 #pragma unroll 4
         for (int r = 0; r < ST; ++r) {
             const bool in = live && t0 + r < i1;
-            const float av = sA[r * 64 + lc], ddv = sDD[r * 64 + lc];   // unconditional reads
+            const float av = sA[r * 64 + lcol], ddv = sDD[r * 64 + lcol];   // unconditional reads
             const float a = in ? av : 0.f;
             const float dd = in ? ddv : 0.f;
             const float rsi = sRY[r], ydi = sRY[ST + r];
@@ -404,13 +437,13 @@ __global__ __launch_bounds__(64) void bwd_query_lm_kernel(const float* __restric
     for (int hh = 0; hh < NH; ++hh)
 #pragma unroll
         for (int r = 0; r < 32; ++r) {
-            const int lm = 32 * (r / 16) + 8 * ((r % 16) / 4) + 4 * (l / 32) + r % 4;
+            const int lm = lm0 + 32 * (r / 16) + 8 * ((r % 16) / 4) + 4 * (l / 32) + r % 4;
             if (lm < m) dM_part[(o + lm) * D1 + 32 * hh + (l & 31)] = acc[hh][r];
         }
     if (!live) return;
-    dM_part[(o + l) * D1 + D] = dml;
+    dM_part[(o + lc) * D1 + D] = dml;
 #pragma unroll
-    for (int c = 0; c < D; ++c) dkt_part[(o + l) * D + c] = dk[c];
+    for (int c = 0; c < D; ++c) dkt_part[(o + lc) * D + c] = dk[c];
 }
 
 // ------------------------------------------------------------------------------------------
@@ -704,8 +737,9 @@ __global__ __launch_bounds__(256) void bwd_ns_kernel(const float* __restrict__ q
 //   dD_aj = -B_aj dB_aj / lambda back into the tile (then whole rows of dDk);
 //   sign pass: dK_j -= dD_aj sign(qt_a - k_j).
 // The landmark rows are streamed twice (the table is small and stays in cache).  dV_j gets
-// dvbar / n at the end.
-template <int D>
+// dvbar / n at the end.  MPK = 64 for m <= 64, 128 for m up to 128; the rows of B and dD (dDk)
+// are group-major, [h][g][n][64] for the landmark groups g of 64.
+template <int D, int MPK>
 __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void bwd_key_kernel(const float* __restrict__ K, const float* __restrict__ V,
                                                       float* __restrict__ dK, float* __restrict__ dV,
                                                       const float* __restrict__ qt, const float* __restrict__ dU,
@@ -715,15 +749,17 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void bwd_key_kernel(const flo
     constexpr int D1 = D + 1;
     constexpr int NCH = D / 32;
     // Landmarks in ranges of LW: 32 at d = 32 (a 64 x 33 tile per wave, which lets three blocks
-    // share a compute unit), one range of 64 at d = 64 (whose registers allow two blocks either
-    // way).  dV accumulates over the ranges; every sum keeps landmark order.
+    // share a compute unit), ranges of 64 at d = 64 (whose registers allow two blocks either
+    // way).  dV accumulates over the ranges (at d = 64 through its rows in memory, each range
+    // adding to what the previous one stored); every sum keeps landmark order.
     constexpr int LW = D == 32 ? 32 : 64;
     constexpr int TP = LW + 1;
-    __shared__ __attribute__((aligned(16))) float sdU[64 * D1];
+    __shared__ __attribute__((aligned(16))) float sdU[MPK * D1];
     __shared__ float sdv[D];
     __shared__ float sT[4 * 64 * TP];
     const int h = blockIdx.y, tid = threadIdx.x, w = tid >> 6, l = tid & 63;
-    for (int e = tid; e < 64 * D1; e += 256) sdU[e] = (e < m * D1) ? dU[(size_t)h * m * D1 + e] : 0.f;
+    for (int e = tid; e < MPK * D1; e += 256) sdU[e] = (e < m * D1) ? dU[(size_t)h * m * D1 + e] : 0.f;
+    const int ng = (m + 63) / 64;   // landmark groups of the row arrays
     if (tid < D) sdv[tid] = dvbar[(size_t)h * D + tid];
     float* tile = sT + w * 64 * TP;
     const int j0 = blockIdx.x * 256 + w * 64;
@@ -760,9 +796,10 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void bwd_key_kernel(const flo
         for (int cb = 0; cb < D / 32; ++cb)
 #pragma unroll
             for (int r = 0; r < 16; ++r) accv[kh][cb][r] = 0.f;
-    // dV with dvbar / n; result register r at lane l: key 32 kh + 8 (r / 4) + 4 (l / 32) + r % 4,
+    // dV with dvbar / n (first: the first contribution, else added to the stored rows, which this
+    // lane wrote); result register r at lane l: key 32 kh + 8 (r / 4) + 4 (l / 32) + r % 4,
     // column 32 cb + l % 32
-    auto store_dv = [&]() {
+    auto store_dv = [&](bool first) {
         const float invn = 1.f / (float)n;
 #pragma unroll
         for (int kh = 0; kh < 2; ++kh)
@@ -773,11 +810,14 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void bwd_key_kernel(const flo
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const int key = 32 * kh + 8 * (r / 4) + 4 * (l >> 5) + r % 4;
-                    if (j0 + key < n) dV[((size_t)h * n + j0 + key) * D + c] = accv[kh][cb][r] + add;
+                    if (j0 + key < n) {
+                        float* p = dV + ((size_t)h * n + j0 + key) * D + c;
+                        *p = accv[kh][cb][r] + (first ? add : *p);
+                    }
                 }
             }
     };
-    const int nrange = LW == 64 ? 1 : (m + LW - 1) / LW;   // m <= 64
+    const int nrange = (MPK == 64 && LW == 64) ? 1 : (m + LW - 1) / LW;
     for (int ri = 0; ri < nrange; ++ri) {
         const int lo = LW * ri, mh = min(LW, m - lo);   // landmarks lo .. lo + mh - 1: tile columns 0 .. mh - 1
         const float* tab = qt + __builtin_amdgcn_readfirstlane((h * m + lo) * D);   // wave-uniform: scalar loads
@@ -787,11 +827,12 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void bwd_key_kernel(const flo
         auto emit = [&](int a, float dist) {
             tile[l * TP + a] = (live && a < mh) ? __builtin_amdgcn_exp2f(dist * kscale) : 0.f;
         };
+        float* Dg = dDk + (size_t)(h * ng + lo / 64) * n * 64;   // the range's group of rows
         if (saved) {   // the forward's key-side summary left the rows of B in dDk: copy the range's
                        // columns (each wave reads only its own rows, whose columns it overwrites
                        // with dD further down)
-            if (LW == 64) load_rows64_dma(tile, dDk + (size_t)h * n * 64, j0, n);
-            else load_half_rows_dma(tile, dDk + (size_t)h * n * 64, j0, n, lo);
+            if (LW == 64) load_rows64_dma(tile, Dg, j0, n);
+            else load_half_rows_dma(tile, Dg, j0, n, lo % 64);
         } else {
             load_key();
             float ta[32], tb[32];
@@ -824,7 +865,15 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void bwd_key_kernel(const flo
                         accv[kh][cb] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, accv[kh][cb], 0, 0, 0);
                     }
         }
-        if (LW == 64) store_dv();   // one range: dV is complete (its accumulators free for dB)
+        if (LW == 64) {   // the range's share of dV is complete (its accumulators free for dB)
+            store_dv(ri == 0);
+#pragma unroll
+            for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+                for (int cb = 0; cb < D / 32; ++cb)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) accv[kh][cb][r] = 0.f;
+        }
         // dB = [v | 1] dU^T on the same instruction (k = a coordinate pair; the A operands of both
         // 32-key halves from one permlane32 swap of the lane's own values), per 32-landmark block
         // and key half, and dD = -B dB / lambda in place in the tile.  Result register r at lane
@@ -857,8 +906,8 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void bwd_key_kernel(const flo
             }
         }
         __builtin_amdgcn_wave_barrier();
-        if (LW == 64) store_rows64(dDk + (size_t)h * n * 64, tile, j0, n, m);
-        else store_half_rows(dDk + (size_t)h * n * 64, tile, j0, n, lo, mh);
+        if (LW == 64) store_rows64(Dg, tile, j0, n, mh);
+        else store_half_rows(Dg, tile, j0, n, lo % 64, mh);
         // sign pass: dK_j -= dD_aj sign(qt_a - k_j), accumulated as dD sign(k_j - qt_a); each
         // unit's dD is read before the unit's first wait
         {
@@ -882,7 +931,7 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void bwd_key_kernel(const flo
         }
         __builtin_amdgcn_wave_barrier();   // the next range overwrites the tile
     }
-    if (LW == 32) store_dv();
+    if (LW == 32) store_dv(true);
     if (live) {   // with the pooling gradient of the key's landmark (window or segment)
         const int lp = pl.r ? ((j / pl.gw) / pl.r) * (pl.gw / pl.r) + (j % pl.gw) / pl.r : seg_of(j, n, m);
         const float4* kp = reinterpret_cast<const float4*>(dkpool + ((size_t)h * m + lp) * D);
@@ -898,18 +947,21 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void bwd_key_kernel(const flo
 // ------------------------------------------------------------------------------------------
 // Landmark-major pass over keys.  grid (nlc, BH), 64 threads (lane = landmark a); block ch covers
 // keys [ch * chunk, ...) in sub-tiles of 16 whose rows of K and of dDk (pitch 64) are copied to
-// LDS one sub-tile ahead:  dqt_a += sum_j dD_aj sign(qt_a - k_j).
+// LDS one sub-tile ahead:  dqt_a += sum_j dD_aj sign(qt_a - k_j).  Landmarks in groups of 64:
+// blockIdx.z = group g, lane = landmark 64 g + lane, reading the group's rows of dDk.
 template <int D>
 __global__ __launch_bounds__(64) void bwd_key_lm_kernel(const float* __restrict__ K, const float* __restrict__ qt,
                                                         const float* __restrict__ dDk, float* __restrict__ dqt_part,
                                                         int n, int m, int chunk, int nlc) {
     constexpr int BUF = 16 * D + 16 * 64;
     __shared__ __attribute__((aligned(16))) float sbuf[2 * BUF];
-    const int ch = blockIdx.x, h = blockIdx.y, a = threadIdx.x;
+    const int ch = blockIdx.x, h = blockIdx.y, g = blockIdx.z, ng = gridDim.z;
+    const int a = 64 * g + (int)threadIdx.x;   // landmark
     const bool live = a < m;
     const int ac = live ? a : m - 1;
+    const int acol = ac - 64 * g;              // its column in the group's rows
     const float* Kh = K + (size_t)h * n * D;
-    const float* DDh = dDk + (size_t)h * n * 64;
+    const float* DDh = dDk + (size_t)(h * ng + g) * n * 64;
     float q[D], acc[D];
 #pragma unroll
     for (int c = 0; c < D; ++c) {
@@ -931,7 +983,7 @@ __global__ __launch_bounds__(64) void bwd_key_lm_kernel(const float* __restrict_
         const float* sDD = sK + 16 * D;
 #pragma unroll 4
         for (int r = 0; r < 16; ++r) {
-            const float ddv = sDD[r * 64 + ac];
+            const float ddv = sDD[r * 64 + acol];
             const float dd = (live && t0 + r < j1) ? ddv : 0.f;
             const float dds = dd * 0x1p64f;
             const float* kr = sK + r * D;
@@ -984,16 +1036,19 @@ __global__ __launch_bounds__(256) void bwd_pool_kernel(float* __restrict__ dQ, c
 
 // ------------------------------------------------------------------------------------------
 // bf16 backward: widening of the inputs (exact) and rounding of the gradients (nearest even,
-// NaN kept NaN), eight elements per thread and array.  grid-stride over count / 8 groups.
+// NaN kept NaN), eight elements per thread and array, the first na of the arrays given.
+// grid-stride over count / 8 groups.
 __global__ __launch_bounds__(256) void widen_bf16_kernel(const uint16_t* __restrict__ a0, const uint16_t* __restrict__ a1,
                                                          const uint16_t* __restrict__ a2, const uint16_t* __restrict__ a3,
                                                          float* __restrict__ b0, float* __restrict__ b1,
-                                                         float* __restrict__ b2, float* __restrict__ b3, size_t groups) {
+                                                         float* __restrict__ b2, float* __restrict__ b3, size_t groups,
+                                                         int na) {
     const uint16_t* src[4] = {a0, a1, a2, a3};
     float* dst[4] = {b0, b1, b2, b3};
     for (size_t gi = (size_t)blockIdx.x * 256 + threadIdx.x; gi < groups; gi += (size_t)gridDim.x * 256) {
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
+            if (t >= na) break;
             const uint4 v = reinterpret_cast<const uint4*>(src[t])[gi];
             const uint32_t w[4] = {v.x, v.y, v.z, v.w};
             float o[8];
@@ -1018,12 +1073,13 @@ __device__ __forceinline__ uint32_t bf16_rne(float x) {
 __global__ __launch_bounds__(256) void narrow_bf16_kernel(const float* __restrict__ a0, const float* __restrict__ a1,
                                                           const float* __restrict__ a2, uint16_t* __restrict__ b0,
                                                           uint16_t* __restrict__ b1, uint16_t* __restrict__ b2,
-                                                          size_t groups) {
+                                                          size_t groups, int na) {
     const float* src[3] = {a0, a1, a2};
     uint16_t* dst[3] = {b0, b1, b2};
     for (size_t gi = (size_t)blockIdx.x * 256 + threadIdx.x; gi < groups; gi += (size_t)gridDim.x * 256) {
 #pragma unroll
         for (int t = 0; t < 3; ++t) {
+            if (t >= na) break;
             const float4 x = reinterpret_cast<const float4*>(src[t])[2 * gi];
             const float4 y = reinterpret_cast<const float4*>(src[t])[2 * gi + 1];
             uint4 o;
@@ -1040,7 +1096,8 @@ hipError_t launch_widen_bf16(const uint16_t* Q, const uint16_t* K, const uint16_
                              float* wK, float* wV, float* wG, size_t count, hipStream_t st) {
     const size_t groups = count / 8;
     const unsigned blocks = (unsigned)min((groups + 255) / 256, (size_t)4096);
-    hipLaunchKernelGGL(widen_bf16_kernel, dim3(blocks), dim3(256), 0, st, Q, K, V, G, wQ, wK, wV, wG, groups);
+    hipLaunchKernelGGL(widen_bf16_kernel, dim3(blocks), dim3(256), 0, st, Q, K, V, G, wQ, wK, wV, wG, groups,
+                       G ? 4 : 3);
     return hipGetLastError();
 }
 
@@ -1048,7 +1105,8 @@ hipError_t launch_narrow_bf16(const float* gQ, const float* gK, const float* gV,
                               uint16_t* dV, size_t count, hipStream_t st) {
     const size_t groups = count / 8;
     const unsigned blocks = (unsigned)min((groups + 255) / 256, (size_t)4096);
-    hipLaunchKernelGGL(narrow_bf16_kernel, dim3(blocks), dim3(256), 0, st, gQ, gK, gV, dQ, dK, dV, groups);
+    hipLaunchKernelGGL(narrow_bf16_kernel, dim3(blocks), dim3(256), 0, st, gQ, gK, gV, dQ, dK, dV, groups,
+                       gK ? 3 : 1);
     return hipGetLastError();
 }
 
@@ -1061,20 +1119,24 @@ hipError_t launch_bwd_query(int norm, const float* Q, const float* dO, float* dQ
                             int d, int m, float lambda, int nqb, hipStream_t st) {
     const float ks = kscale_of(lambda), il = 1.f / lambda;
     dim3 grid(nqb, BH);
-#define LAPATTN_BQ(Dv, Nv)                                                                                  \
-    hipLaunchKernelGGL((bwd_query_kernel<Dv, Nv>), grid, dim3(256), 0, st, Q, dO, dQ, kt, M, vbar, Aq, dDq, rs, \
+#define LAPATTN_BQ(Dv, Nv, MPv)                                                                                  \
+    hipLaunchKernelGGL((bwd_query_kernel<Dv, Nv, MPv>), grid, dim3(256), 0, st, Q, dO, dQ, kt, M, vbar, Aq, dDq, rs, \
                        dYd, dvbar_part, p0_part, whiten, mvec, saved, H, n, m, ks, il, nqb)
-    if (d == 32) {
-        if (norm == NORM_INLINE) LAPATTN_BQ(32, NORM_INLINE);
-        else if (norm == NORM_ROWSUM) LAPATTN_BQ(32, NORM_ROWSUM);
-        else if (norm == NORM_MSPACE) LAPATTN_BQ(32, NORM_MSPACE);
-        else LAPATTN_BQ(32, NORM_NONE);
+#define LAPATTN_BQN(Dv, MPv)                                        \
+    do {                                                            \
+        if (norm == NORM_INLINE) LAPATTN_BQ(Dv, NORM_INLINE, MPv);   \
+        else if (norm == NORM_ROWSUM) LAPATTN_BQ(Dv, NORM_ROWSUM, MPv); \
+        else if (norm == NORM_MSPACE) LAPATTN_BQ(Dv, NORM_MSPACE, MPv); \
+        else LAPATTN_BQ(Dv, NORM_NONE, MPv);                         \
+    } while (0)
+    if (m <= 64) {
+        if (d == 32) LAPATTN_BQN(32, 64);
+        else LAPATTN_BQN(64, 64);
     } else {
-        if (norm == NORM_INLINE) LAPATTN_BQ(64, NORM_INLINE);
-        else if (norm == NORM_ROWSUM) LAPATTN_BQ(64, NORM_ROWSUM);
-        else if (norm == NORM_MSPACE) LAPATTN_BQ(64, NORM_MSPACE);
-        else LAPATTN_BQ(64, NORM_NONE);
+        if (d == 32) LAPATTN_BQN(32, 128);
+        else LAPATTN_BQN(64, 128);
     }
+#undef LAPATTN_BQN
 #undef LAPATTN_BQ
     return hipGetLastError();
 }
@@ -1082,7 +1144,7 @@ hipError_t launch_bwd_query(int norm, const float* Q, const float* dO, float* dQ
 hipError_t launch_bwd_query_lm(const float* Q, const float* dO, const float* kt, const float* Aq, const float* dDq,
                                const float* rs, const float* dYd, float* dM_part, float* dkt_part, int BH, int n,
                                int d, int m, int chunk, int nlc, hipStream_t st) {
-    dim3 grid(nlc, BH);
+    dim3 grid(nlc, BH, (m + 63) / 64);
     if (d == 32)
         hipLaunchKernelGGL((bwd_query_lm_kernel<32>), grid, dim3(64), 0, st, Q, dO, kt, Aq, dDq, rs, dYd, dM_part,
                            dkt_part, n, m, chunk, nlc);
@@ -1114,18 +1176,23 @@ hipError_t launch_bwd_key(const float* K, const float* V, float* dK, float* dV, 
                           int d, int m, float lambda, hipStream_t st) {
     const float ks = kscale_of(lambda), il = 1.f / lambda;
     dim3 grid((n + 255) / 256, BH);
-    if (d == 32)
-        hipLaunchKernelGGL((bwd_key_kernel<32>), grid, dim3(256), 0, st, K, V, dK, dV, qt, dU, dvbar, dDk, dkpool, pl,
-                           saved, n, m, ks, il);
-    else
-        hipLaunchKernelGGL((bwd_key_kernel<64>), grid, dim3(256), 0, st, K, V, dK, dV, qt, dU, dvbar, dDk, dkpool, pl,
-                           saved, n, m, ks, il);
+#define LAPATTN_BK(Dv, MPv)                                                                                      \
+    hipLaunchKernelGGL((bwd_key_kernel<Dv, MPv>), grid, dim3(256), 0, st, K, V, dK, dV, qt, dU, dvbar, dDk, dkpool, \
+                       pl, saved, n, m, ks, il)
+    if (m <= 64) {
+        if (d == 32) LAPATTN_BK(32, 64);
+        else LAPATTN_BK(64, 64);
+    } else {
+        if (d == 32) LAPATTN_BK(32, 128);
+        else LAPATTN_BK(64, 128);
+    }
+#undef LAPATTN_BK
     return hipGetLastError();
 }
 
 hipError_t launch_bwd_key_lm(const float* K, const float* qt, const float* dDk, float* dqt_part, int BH, int n, int d,
                              int m, int chunk, int nlc, hipStream_t st) {
-    dim3 grid(nlc, BH);
+    dim3 grid(nlc, BH, (m + 63) / 64);
     if (d == 32)
         hipLaunchKernelGGL((bwd_key_lm_kernel<32>), grid, dim3(64), 0, st, K, qt, dDk, dqt_part, n, m, chunk, nlc);
     else

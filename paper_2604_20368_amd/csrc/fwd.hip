@@ -69,7 +69,10 @@ __global__ __launch_bounds__(256) void pool_kernel(const typename elem<DT>::type
 //   LDS, B = value rows straight from global memory, loaded before the landmark loop; the ones
 //   column is column 0 of the last column tile).  At the end the four waves' partials are added
 //   in a fixed order.
-// Writes Upart[h][chunk][a][c] for a < m, c <= d.
+// Landmarks in groups of 64 (blockIdx.z = group g: landmarks 64 g .. 64 g + 63), so that m up to
+// 128 takes two blocks per key chunk, each reading the chunk's keys.
+// Writes Upart[h][chunk][a][c] for the group's landmarks a < m, c <= d; with Bsave, the keys' rows
+// of B into Bsave[h][g][n][64] (group-major rows of 64 landmarks, zeros past m).
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 template <int D>
@@ -88,9 +91,12 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void key_summary_kernel(const
     // pairs, so that a CU's scalar cache serves few landmark tables
     const int G = (int)(gridDim.x * gridDim.y), lin = xcd_order(blockIdx.y * gridDim.x + blockIdx.x, G);
     const int chunk = lin % (int)gridDim.x, h = lin / (int)gridDim.x;
+    const int g = blockIdx.z, ng = gridDim.z, lm0 = 64 * g;
+    const int mg = min(64, m - lm0);   // landmarks of the group
     const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, li = l & 15, lk = l >> 4;
     float* sB = lds + w * 32 * BP;
-    const float* tab = qt + __builtin_amdgcn_readfirstlane(h * m * D);   // wave-uniform: scalar loads
+    const float* tab = qt + __builtin_amdgcn_readfirstlane((h * m + lm0) * D);   // wave-uniform: scalar loads
+    float* Bg = Bsave ? Bsave + (size_t)(h * ng + g) * n * 64 : nullptr;
     f32x4_t acc[4][CT];
 #pragma unroll
     for (int rt = 0; rt < 4; ++rt)
@@ -124,8 +130,8 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void key_summary_kernel(const
         }
 #pragma unroll
         for (int ri = 0; ri < 2; ++ri) {   // unrolled: acc is indexed by the range
-            if (32 * ri >= m) break;
-            const int mh = min(32, m - 32 * ri);   // landmarks 32 ri .. 32 ri + mh - 1: tile rows 0 .. mh - 1
+            if (32 * ri >= mg) break;
+            const int mh = min(32, mg - 32 * ri);   // landmarks lm0 + 32 ri .. + mh - 1: tile rows 0 .. mh - 1
             const float* tabr = tab + 32 * ri * D;
             const int units = mh * NCH;
             for (int a = mh; a < 32; ++a) sB[a * BP + l] = 0.f;   // rows past m (else the last range's)
@@ -156,7 +162,7 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void key_summary_kernel(const
 #pragma unroll
             for (int rl = 0; rl < 2; ++rl) {
                 const int rt = 2 * ri + rl;
-                if (16 * rt < m) {
+                if (16 * rt < mg) {
 #pragma unroll
                     for (int s = 0; s < 16; ++s) {
                         const float av = sB[(16 * rl + li) * BP + 4 * s + lk];
@@ -168,8 +174,8 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void key_summary_kernel(const
                     }
                 }
             }
-            if (Bsave && live) {   // the key's row of B for the backward ([BH][n][64], zeros past m)
-                float4* dst = reinterpret_cast<float4*>(Bsave + ((size_t)h * n + j) * 64 + 32 * ri);
+            if (Bg && live) {   // the key's row of B for the backward (zeros past m)
+                float4* dst = reinterpret_cast<float4*>(Bg + (size_t)j * 64 + 32 * ri);
 #pragma unroll 4
                 for (int a4 = 0; a4 < 8; ++a4)
                     dst[a4] = make_float4(sB[(4 * a4) * BP + l], sB[(4 * a4 + 1) * BP + l],
@@ -177,8 +183,8 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void key_summary_kernel(const
             }
             __builtin_amdgcn_wave_barrier();   // the next range overwrites the tile
         }
-        if (Bsave && live && m <= 32) {   // no second range: its columns are zeros
-            float4* dst = reinterpret_cast<float4*>(Bsave + ((size_t)h * n + j) * 64 + 32);
+        if (Bg && live && mg <= 32) {   // no second range: its columns are zeros
+            float4* dst = reinterpret_cast<float4*>(Bg + (size_t)j * 64 + 32);
 #pragma unroll
             for (int a4 = 0; a4 < 8; ++a4) dst[a4] = make_float4(0.f, 0.f, 0.f, 0.f);
         }
@@ -202,9 +208,9 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void key_summary_kernel(const
         }
     }
     __syncthreads();
-    for (int e = tid; e < m * D1; e += 256) {
+    for (int e = tid; e < mg * D1; e += 256) {
         const int a = e / D1, c = e % D1;
-        Upart[(((size_t)h * nkc + chunk) * m + a) * D1 + c] = red[a * RP + c];
+        Upart[(((size_t)h * nkc + chunk) * m + lm0 + a) * D1 + c] = red[a * RP + c];
     }
 }
 
@@ -408,6 +414,8 @@ __global__ __launch_bounds__(256) void ns_solve_kernel(const float* __restrict__
 //   pair's two tile columns (queries 0..31 keep theirs and receive the other landmark of 32..63
 //   and vice versa).  The result holds, per lane, 16 output columns of one query: normalised
 //   (Eq. (4) / Eq. (3)) and stored four columns at a time.
+// Any m up to 128 (up to four ranges); with Asave, A's rows go to Asave[h][g][n][64] for the
+// landmark groups g of 64.
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 template <int D, int NORM>
@@ -427,11 +435,12 @@ __global__ __launch_bounds__(256) void query_out_kernel(const float* __restrict_
     // so that four blocks share a compute unit), column block cb: lane j + 32 k holds
     // M[32 hh + 2s + k][32 cb + j]
     __shared__ __attribute__((aligned(16))) float sMT[16 * CB * 64];
-    __shared__ float sMo[64];
+    __shared__ float sMo[128];
     __shared__ float sVb[D];
     __shared__ float sMb[NORM == NORM_MSPACE ? D : 1];
     __shared__ float sT[4 * 64 * TP];
     const int h = blockIdx.y, tid = threadIdx.x, w = tid >> 6, l = tid & 63;
+    const int ng = (m + 63) / 64;   // landmark groups of the saved rows
     // landmark-space normalisation: the rows of M scaled by the whitening w, the ones column
     // replaced by 1/m (so that s_i becomes the landmark mean of a_i), and the vectors
     // sum_l w_l M_l and (1/m) sum_l M_l from mvec
@@ -445,7 +454,7 @@ __global__ __launch_bounds__(256) void query_out_kernel(const float* __restrict_
             sMT[e] = (lm < m) ? wv * src[32 * cb + ln % 32] : 0.f;
         }
     };
-    if (tid < 64) {
+    if (tid < 128) {
         if (NORM == NORM_MSPACE) sMo[tid] = (tid < m) ? 1.f / (float)m : 0.f;
         else sMo[tid] = (tid < m) ? M[((size_t)h * m + tid) * D1 + D] : 0.f;
     }
@@ -505,7 +514,8 @@ __global__ __launch_bounds__(256) void query_out_kernel(const float* __restrict_
         }
         if (mh & 1) tile[l * TP + mh] = 0.f;   // the pair loop reads column mh (unwritten when d = 64)
         __builtin_amdgcn_wave_barrier();
-        if (Asave) store_half_rows(Asave + (size_t)h * n * 64, tile, i0, n, 32 * hh, mh);   // A's rows for the backward
+        if (Asave)   // A's rows for the backward, group-major: Asave[h][g][n][64], g = landmark / 64
+            store_half_rows(Asave + (size_t)(h * ng + (hh >> 1)) * n * 64, tile, i0, n, 32 * (hh & 1), mh);
         const int npair = (mh + 1) / 2;
         __syncthreads();   // the last range's operands are read by every wave
         stage(hh);
@@ -585,10 +595,10 @@ hipError_t launch_key_summary(int dt, const void* K, const void* V, const float*
     if (dt != DT_F32) return hipErrorInvalidValue;   // bf16 inputs take the fast path
     const float ks = kscale_of(lambda);
     if (d == 32)
-        hipLaunchKernelGGL((key_summary_kernel<32>), dim3(nkc, BH), dim3(256), 0, st, (const float*)K,
+        hipLaunchKernelGGL((key_summary_kernel<32>), dim3(nkc, BH, (m + 63) / 64), dim3(256), 0, st, (const float*)K,
                            (const float*)V, qt, Upart, Bsave, n, m, ks, chunk_keys, nkc);
     else
-        hipLaunchKernelGGL((key_summary_kernel<64>), dim3(nkc, BH), dim3(256), 0, st, (const float*)K,
+        hipLaunchKernelGGL((key_summary_kernel<64>), dim3(nkc, BH, (m + 63) / 64), dim3(256), 0, st, (const float*)K,
                            (const float*)V, qt, Upart, Bsave, n, m, ks, chunk_keys, nkc);
     return hipGetLastError();
 }

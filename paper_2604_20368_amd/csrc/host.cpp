@@ -13,7 +13,7 @@
 
 namespace {
 
-constexpr int kMaxM = 64;
+constexpr int kMaxM = 128;
 constexpr int kMaxT = 64;
 constexpr int kKeyChunk = 256;   // keys per block of the fp32 key-summary kernel (one 64-key tile per wave) ...
 constexpr int kKeyMaxChunk = 1024;  // ... up to this many for long sequences (a multiple of 256)
@@ -63,6 +63,8 @@ struct FastPlan {
 
 struct Plan {
     size_t qt, kt, vseg, Upart, Xs, cinfo, U, M, Mc, vbar;               // forward
+    size_t Ebuf, Ud, nsbs, dDW;          // m > 64: solve and its backward spread over workgroups
+    size_t oF;                           // bf16 forward with m > 64: the fp32 output
     size_t Aq, dDq, rs, dYd, dvbar_part, dM_part, dkt_part, dU, dvbar,   // backward
         dqtW, dkpool, dDk, dqt_part;
     size_t wQ, wK, wV, wG, gQ, gK, gV;   // bf16 backward: fp32 copies of the inputs, fp32 gradients
@@ -71,7 +73,7 @@ struct Plan {
     size_t p0_part;                      // landmark-space normalisation: per-block sums of dOut
     size_t dwc_part;                     // convolution branch, backward: filter-gradient partials
     size_t total;
-    int MP, nkc, nqb, nlc, lmc, kc;
+    int MP, ng, nkc, nqb, nlc, lmc, kc;
 };
 
 // Keys per block of the fp32 key-side summary: 256 (many small blocks fill the three block slots
@@ -105,7 +107,9 @@ struct Carver {
 
 Plan make_plan(int BH, int n, int d, int m, int T, bool bwd, bool bf16 = false, bool dwc = false) {
     Plan p{};
-    p.MP = m <= 32 ? 32 : 64;
+    p.MP = m <= 32 ? 32 : (m <= 64 ? 64 : 128);
+    p.ng = (m + 63) / 64;   // landmark groups of 64 (the row arrays below are group-major)
+    const bool big = p.MP == 128;
     p.kc = key_chunk(n);
     p.nkc = (n + p.kc - 1) / p.kc;
     p.nqb = (n + 255) / 256;
@@ -118,16 +122,22 @@ Plan make_plan(int BH, int n, int d, int m, int T, bool bwd, bool bf16 = false, 
     p.kt = c.take(bh * m * d * f);
     p.vseg = c.take(bh * m * d * g);
     p.Upart = c.take(bh * p.nkc * m * d1 * f);
-    p.Xs = c.take(bh * (bwd ? (size_t)T + 2 : 1) * mpp * g);   // X_0..X_T and W for the backward
+    // X_0..X_T and W for the backward (always, for m > 64)
+    p.Xs = c.take(bh * ((bwd || big) ? (size_t)T + 2 : 1) * mpp * g);
     p.cinfo = c.take(bh * 4 * g);
     p.U = c.take(bh * m * d1 * f);
     p.M = c.take(bh * m * d1 * f);
     p.Mc = c.take(bh * m * d * f);
     p.vbar = c.take(bh * d * f);
     p.mvec = c.take(bh * 2 * d * f);
+    if (big) {
+        p.Ebuf = c.take(bh * 2 * mpp * g);
+        p.Ud = c.take(bh * m * d1 * g);
+    }
+    const size_t rows = bh * p.ng * n * 64 * f;   // [BH][ng][n][64]: rows of pitch 64 (16-byte aligned)
     if (bwd) {
-        p.Aq = c.take(bh * n * 64 * f);    // rows of pitch 64 (16-byte aligned for the LDS copies)
-        p.dDq = c.take(bh * n * 64 * f);
+        p.Aq = c.take(rows);
+        p.dDq = c.take(rows);
         p.rs = c.take(bh * n * f);
         p.dYd = c.take(bh * n * f);
         p.dvbar_part = c.take(bh * p.nqb * d * f);
@@ -138,7 +148,11 @@ Plan make_plan(int BH, int n, int d, int m, int T, bool bwd, bool bf16 = false, 
         p.dvbar = c.take(bh * d * f);
         p.dqtW = c.take(bh * m * d * f);
         p.dkpool = c.take(bh * m * d * f);
-        p.dDk = c.take(bh * n * 64 * f);
+        p.dDk = c.take(rows);
+        if (big) {
+            p.nsbs = c.take(lapattn::nsb_backward_scratch(BH, d) * g);
+            p.dDW = c.take(bh * mpp * f);
+        }
         p.dqt_part = c.take(bh * p.nlc * m * d * f);
         if (bf16) {
             const size_t t = bh * n * d * f;
@@ -152,6 +166,13 @@ Plan make_plan(int BH, int n, int d, int m, int T, bool bwd, bool bf16 = false, 
         }
         if (dwc)
             p.dwc_part = c.take(bh * ((n + kDwcChunk - 1) / kDwcChunk) * d * (kDwcMaxK * kDwcMaxK + 1) * f);
+    }
+    if (bf16 && !bwd) {   // the bf16 forward with m > 64: fp32 copies of the inputs, fp32 output
+        const size_t t = bh * n * d * f;
+        p.wQ = c.take(t);
+        p.wK = c.take(t);
+        p.wV = c.take(t);
+        p.oF = c.take(t);
     }
     if (dwc) p.E = c.take(bh * n * d * f);
     p.total = (c.off + 255) & ~size_t(255);
@@ -301,6 +322,13 @@ hipError_t forward_internals(Recorder& rec, const Plan& p, const void* Q, const 
         return lapattn::launch_key_summary(dtype, K, V, qt, Upart, Bsave, BH, n, d, m, lambda, p.kc, p.nkc, st);
     });
     if (e != hipSuccess) return e;
+    if (p.MP == 128)
+        return run_named(rec, "ns_solve", [&] {
+            return lapattn::launch_nsb_forward(qt, kt, Upart, vseg, at<double>(ws, p.Xs), at<double>(ws, p.Ebuf),
+                                               at<double>(ws, p.Ud), at<double>(ws, p.cinfo), at<float>(ws, p.U),
+                                               at<float>(ws, p.M), at<float>(ws, p.Mc), at<float>(ws, p.vbar), BH, n,
+                                               d, m, T, (double)lambda, (double)eps, p.nkc, st);
+        });
     e = run_named(rec, "ns_solve", [&] {
         return lapattn::launch_ns_solve(qt, kt, Upart, vseg, at<double>(ws, p.Xs), at<double>(ws, p.cinfo),
                                         at<float>(ws, p.U), at<float>(ws, p.M), at<float>(ws, p.Mc),
@@ -366,7 +394,7 @@ size_t lapattn_workspace_size(int B, int H, int n, int d, int m, int ns_iters, i
     if (check_shape(B, H, n, d, m, 1.f, ns_iters, dtype, LAPATTN_NORM_INLINE, 0.f) != LAPATTN_OK) return 0;
     if (flags & ~(LAPATTN_WS_BACKWARD | LAPATTN_WS_DWC)) return 0;
     const bool bwd = (flags & LAPATTN_WS_BACKWARD) != 0, dwc = (flags & LAPATTN_WS_DWC) != 0;
-    if (dtype == LAPATTN_BF16 && !bwd) return make_fast_plan(B * H, n, d, m, dwc).total;
+    if (dtype == LAPATTN_BF16 && !bwd && m <= 64) return make_fast_plan(B * H, n, d, m, dwc).total;
     return make_plan(B * H, n, d, m, ns_iters, bwd, dtype == LAPATTN_BF16, dwc).total;
 }
 
@@ -387,7 +415,7 @@ int lapattn_forward(const void* Q, const void* K, const void* V, void* Out, int 
         if (rc) return rc;
         const int BH = B * H;
         hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-        if (dtype == LAPATTN_BF16) {
+        if (dtype == LAPATTN_BF16 && m <= 64) {
             const FastPlan fp = make_fast_plan(BH, n, d, m, dwc.k != 0);
             if (!workspace || workspace_bytes < fp.total) return LAPATTN_ERR_WORKSPACE;
             Recorder rec(st);
@@ -395,21 +423,41 @@ int lapattn_forward(const void* Q, const void* K, const void* V, void* Out, int 
                                         pl, dwc, whiten_of(opts), st);
             return e == hipSuccess ? LAPATTN_OK : LAPATTN_ERR_HIP;
         }
+        // bf16 inputs with m > 64: widened to fp32 (exact), the fp32 path, the output rounded to bf16
+        const bool bf16 = dtype == LAPATTN_BF16;
         // save: the backward's layout, with every Newton-Schulz iterate kept, so that a following
         // lapattn_backward (save set, same arguments and workspace) can skip the recomputation
-        const bool save = save_of(opts);
-        const Plan p = make_plan(BH, n, d, m, ns_iters, save, false, dwc.k != 0);
+        const bool save = !bf16 && save_of(opts);
+        const Plan p = make_plan(BH, n, d, m, ns_iters, save, bf16, dwc.k != 0);
         if (!workspace || workspace_bytes < p.total) return LAPATTN_ERR_WORKSPACE;
         Recorder rec(st);
+        hipError_t e;
+        const void* q = Q;
+        const void* k = K;
+        const void* v = V;
+        void* out = Out;
+        if (bf16) {
+            e = run_named(rec, "widen", [&] {
+                return lapattn::launch_widen_bf16(static_cast<const uint16_t*>(Q), static_cast<const uint16_t*>(K),
+                                                  static_cast<const uint16_t*>(V), nullptr, at<float>(workspace, p.wQ),
+                                                  at<float>(workspace, p.wK), at<float>(workspace, p.wV), nullptr,
+                                                  (size_t)BH * n * d, st);
+            });
+            if (e != hipSuccess) return LAPATTN_ERR_HIP;
+            q = at<float>(workspace, p.wQ);
+            k = at<float>(workspace, p.wK);
+            v = at<float>(workspace, p.wV);
+            out = at<float>(workspace, p.oF);
+        }
         // with save the key side also leaves B's rows (in the backward's dDk slice) and the query
         // side A's rows (Aq), so that the backward skips its two distance passes as well
-        hipError_t e = forward_internals(rec, p, Q, K, V, workspace, BH, n, d, m, lambda, ns_iters, dtype, eps,
-                                         save, pl, st, save ? at<float>(workspace, p.dDk) : nullptr);
+        e = forward_internals(rec, p, q, k, v, workspace, BH, n, d, m, lambda, ns_iters, LAPATTN_FP32, eps, save, pl,
+                              st, save ? at<float>(workspace, p.dDk) : nullptr);
         if (e != hipSuccess) return LAPATTN_ERR_HIP;
         float* E = dwc.k ? at<float>(workspace, p.E) : nullptr;
         if (E) {
             e = run_named(rec, "dwc", [&] {
-                return lapattn::launch_dwc_fwd(lapattn::DT_F32, V, dwc.w, dwc.b, E, BH, H, n, d, pl.gw, dwc.k, st);
+                return lapattn::launch_dwc_fwd(lapattn::DT_F32, v, dwc.w, dwc.b, E, BH, H, n, d, pl.gw, dwc.k, st);
             });
             if (e != hipSuccess) return LAPATTN_ERR_HIP;
         }
@@ -421,12 +469,20 @@ int lapattn_forward(const void* Q, const void* K, const void* V, void* Out, int 
             if (e != hipSuccess) return LAPATTN_ERR_HIP;
         }
         e = run_named(rec, "query_out", [&] {
-            return lapattn::launch_query_out(dtype, norm, Q, Out, at<float>(workspace, p.kt),
+            return lapattn::launch_query_out(LAPATTN_FP32, norm, q, out, at<float>(workspace, p.kt),
                                              at<float>(workspace, p.M), at<float>(workspace, p.Mc),
                                              at<float>(workspace, p.vbar), E,
                                              whiten_of(opts), at<float>(workspace, p.mvec),
                                              save ? at<float>(workspace, p.Aq) : nullptr, BH, H, n, d, m, lambda, st);
         });
+        if (e != hipSuccess) return LAPATTN_ERR_HIP;
+        if (bf16) {
+            e = run_named(rec, "narrow", [&] {
+                return lapattn::launch_narrow_bf16(at<float>(workspace, p.oF), nullptr, nullptr,
+                                                   static_cast<uint16_t*>(Out), nullptr, nullptr, (size_t)BH * n * d,
+                                                   st);
+            });
+        }
         return e == hipSuccess ? LAPATTN_OK : LAPATTN_ERR_HIP;
     } catch (...) {
         return LAPATTN_ERR_HIP;
@@ -505,6 +561,16 @@ int lapattn_backward(const void* Q, const void* K, const void* V, const void* dO
                                                 at<float>(ws, p.dkt_part), BH, n, d, m, p.lmc, p.nlc, st);
         });
         if (e != hipSuccess) return LAPATTN_ERR_HIP;
+        if (p.MP == 128)
+            e = run_named(rec, "bwd_ns", [&] {
+                return lapattn::launch_nsb_backward(
+                    at<float>(ws, p.qt), at<float>(ws, p.kt), at<double>(ws, p.Xs), at<double>(ws, p.cinfo),
+                    at<float>(ws, p.U), at<float>(ws, p.dM_part), at<float>(ws, p.dvbar_part), at<float>(ws, p.p0_part),
+                    whiten, mspace ? 1 : 0, at<float>(ws, p.dU), at<float>(ws, p.dvbar), at<float>(ws, p.dqtW),
+                    at<float>(ws, p.dkpool), at<float>(ws, p.dkt_part), pl, at<double>(ws, p.nsbs), at<float>(ws, p.dDW),
+                    BH, H, n, d, m, ns_iters, (double)lambda, (double)eps, p.nlc, p.nqb, st);
+            });
+        else
         e = run_named(rec, "bwd_ns", [&] {
             return lapattn::launch_bwd_ns(at<float>(ws, p.qt), at<float>(ws, p.kt), at<double>(ws, p.Xs),
                                           at<double>(ws, p.cinfo), at<float>(ws, p.U), at<float>(ws, p.dM_part),
@@ -562,7 +628,7 @@ const char* lapattn_status_str(int status) {
         case LAPATTN_ERR_SHAPE: return "invalid shape (B, H, n >= 1, 1 <= m <= n, B*H*n*d < 2^31)";
         case LAPATTN_ERR_PARAM:
             return "invalid parameter (lambda, ns_iters, eps, norm, dtype, map or convolution options)";
-        case LAPATTN_ERR_UNSUPPORTED: return "unsupported configuration (d in {32, 64}, m <= 64)";
+        case LAPATTN_ERR_UNSUPPORTED: return "unsupported configuration (d in {32, 64}, m <= 128)";
         case LAPATTN_ERR_WORKSPACE: return "workspace missing or too small";
         case LAPATTN_ERR_HIP: return "HIP launch failed";
         case LAPATTN_ERR_ALIGN: return "a tensor is not 16-byte aligned or the workspace not 256-byte aligned";

@@ -21,13 +21,14 @@ hipError_t launch_pool(int dt, const void* Q, const void* K, const void* V,
                        int BH, int n, int d, int m, LmPool pl, hipStream_t st);
 
 // Key-side summary: per key chunk, Upart[h][chunk][a][c] = sum_j k(qt_a, k_j) [v_j | 1]_c;
-// with Bsave, also the rows B[j][a] = k(qt_a, k_j) ([BH][n][64], zeros past m) for the backward.
+// with Bsave, also the rows B[j][a] = k(qt_a, k_j) for the backward, group-major
+// ([BH][G][n][64] for the G = ceil(m / 64) landmark groups, zeros past m).
 hipError_t launch_key_summary(int dt, const void* K, const void* V, const float* qt, float* Upart, float* Bsave,
                               int BH, int n, int d, int m, float lambda, int chunk_keys, int nkc,
                               hipStream_t st);
 
-// Newton-Schulz on K_LL and the solved matrix M = X_T U.
-//   Xs:    [BH][store_all ? T+1 : 1][MP][MP] fp64 iterates (padded to MP)
+// Newton-Schulz on K_LL and the solved matrix M = X_T U, m <= 64.
+//   Xs:    [BH][store_all ? T+2 : 1][MP][MP] fp64 iterates (padded to MP), then W
 //   cinfo: [BH][4] fp64: scale c, ||W||_1, ||W||_inf, (a* * 256 + b*)
 //   U, M:  [BH][m][d+1] fp32;  Mc: [BH][m][d] fp32, M[:, :d] - M[:, d] vbar^T;  vbar: [BH][d] fp32
 hipError_t launch_ns_solve(const float* qt, const float* kt, const float* Upart, const double* vseg,
@@ -38,10 +39,37 @@ hipError_t launch_ns_solve(const float* qt, const float* kt, const float* Upart,
 // Query side: Out_i = normalise(sum_l k(q_i, kt_l) M_l) (+ extra_i when extra, [BH][n][d], is given);
 // the inline form reads Mc (launch_ns_solve).
 // The landmark-space normalisation takes the whitening [H][m] (NULL: ones) and mvec below.
-// With Asave, also the rows A[i][l] = k(q_i, kt_l) ([BH][n][64], columns below m) for the backward.
+// With Asave, also the rows A[i][l] = k(q_i, kt_l) for the backward, group-major ([BH][G][n][64],
+// columns below m).
 hipError_t launch_query_out(int dt, int norm, const void* Q, void* Out, const float* kt, const float* M,
                             const float* Mc, const float* vbar, const float* extra, const float* whiten, const float* mvec,
                             float* Asave, int BH, int H, int n, int d, int m, float lambda, hipStream_t st);
+
+// The same for 64 < m <= 128 (nsbig.hip), products spread over many workgroups:
+//   Xs:    [BH][T+2][128][128] fp64: X_0 .. X_T, then W (always all of them)
+//   Ebuf:  [BH][2][128][128] fp64 scratch;  Ud: [BH][m][d+1] fp64 scratch
+struct NsbJob {   // Out = alpha op(A) op(B) + beta1 C1 + beta2 C2 + gamma I (diagonal below idm)
+    const double *A, *B, *C1, *C2;
+    double* Out;
+    long long sA, sB, sC1, sC2, sOut;   // per-head strides (doubles)
+    int pa, pb, pc1, pc2, pout;          // row pitches (doubles)
+    int ta, tb;                          // op(X) = X^T
+    int M, N, K, idm;                    // Out is M x N; K <= 128
+    double alpha, beta1, beta2, gamma;
+};
+struct NsbJobs {
+    NsbJob j[3];
+};
+NsbJob nsb_job(const double* A, long long sA, int pa, bool ta, const double* B, long long sB, int pb, bool tb,
+               double* Out, long long sOut, int pout, int M, int N, int K, double alpha);
+hipError_t launch_nsb_mm(const NsbJobs& js, int njobs, int BH, hipStream_t st);
+hipError_t launch_nsb_forward(const float* qt, const float* kt, const float* Upart, const double* vseg, double* Xs,
+                              double* Ebuf, double* Ud, double* cinfo, float* U, float* M, float* Mc, float* vbar,
+                              int BH, int n, int d, int m, int T, double lambda, double eps, int nkc, hipStream_t st);
+// Scratch doubles of launch_nsb_backward.
+inline size_t nsb_backward_scratch(int BH, int d) {
+    return (size_t)BH * (7 * 128 * 128 + 3 * 128 * (size_t)(d + 1) + 2 * (size_t)d);
+}
 
 // Landmark-space normalisation: mvec[BH][2][d] = {sum_l w_l M_l[:d], (1/m) sum_l M_l[:d]}.
 hipError_t launch_mspace_vec(const float* M, const float* whiten, float* mvec, int BH, int H, int d, int m,
@@ -51,7 +79,7 @@ hipError_t launch_mspace_vec(const float* M, const float* whiten, float* mvec, i
 
 // Query-major pass: writes the direct dQ term, the kernel values Aq (read instead when saved: the
 // forward's launch_query_out left them there) and dDq = -A dA / lambda
-// ([BH][n][m]), per-query dY scale rs and last column dYd ([BH][n]), and per-block
+// ([BH][G][n][64], group-major for the G = ceil(m / 64) landmark groups), per-query dY scale rs and last column dYd ([BH][n]), and per-block
 // partial sums of dvbar ([BH][nqb][d]; for the landmark-space normalisation also the sums of
 // dO into p0_part, with the whitening and mvec of the forward).
 hipError_t launch_bwd_query(int norm, const float* Q, const float* dO, float* dQ,
@@ -75,9 +103,17 @@ hipError_t launch_bwd_ns(const float* qt, const float* kt, const double* Xs, con
                          const float* p0_part, const float* whiten, int mspace,
                          int BH, int H, int n, int d, int m, int T, double lambda, double eps,
                          int nlc, int nqb, int MP, hipStream_t st);
+// The same for 64 < m <= 128 (nsbig.hip), with nsb_backward_scratch(BH, d) doubles of scratch and
+// dDW [BH][128][128] fp32; Xs as launch_nsb_forward left it.
+hipError_t launch_nsb_backward(const float* qt, const float* kt, const double* Xs, const double* cinfo,
+                               const float* U, const float* dM_part, const float* dvbar_part,
+                               const float* p0_part, const float* whiten, int mspace, float* dU, float* dvbar,
+                               float* dqtW, float* dkpool, const float* dkt_part, LmPool pl, double* scratch,
+                               float* dDW, int BH, int H, int n, int d, int m, int T, double lambda, double eps,
+                               int nlc, int nqb, hipStream_t st);
 
 // Key-major pass: final dK (the direct term plus dkpool of the key's landmark), final dV, and
-// dDk = -B dB / lambda ([BH][n][m]).  saved: dDk holds B's rows from the forward on entry
+// dDk = -B dB / lambda ([BH][G][n][64], group-major).  saved: dDk holds B's rows from the forward on entry
 // (launch_key_summary's Bsave) instead of being recomputed.
 hipError_t launch_bwd_key(const float* K, const float* V, float* dK, float* dV,
                           const float* qt, const float* dU, const float* dvbar, float* dDk, const float* dkpool,
@@ -93,7 +129,8 @@ hipError_t launch_bwd_pool(float* dQ, const float* dqtW, const float* dqt_part,
                            int BH, int n, int d, int m, int nlc, LmPool pl, hipStream_t st);
 
 // bf16 backward: the four inputs widened to fp32 (exact), the three fp32 gradients rounded to
-// bf16 (nearest even); count elements each, a multiple of 8, 16-byte aligned arrays.
+// bf16 (nearest even); count elements each, a multiple of 8, 16-byte aligned arrays.  With G
+// NULL only Q, K, V are widened (the forward for m > 64); with gK NULL only gQ is rounded.
 hipError_t launch_widen_bf16(const uint16_t* Q, const uint16_t* K, const uint16_t* V, const uint16_t* G, float* wQ,
                              float* wK, float* wV, float* wG, size_t count, hipStream_t st);
 hipError_t launch_narrow_bf16(const float* gQ, const float* gK, const float* gV, uint16_t* dQ, uint16_t* dK,

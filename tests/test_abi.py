@@ -72,7 +72,8 @@ def test_argument_validation(call):
     assert call(eps=-0.1) == L.LAPATTN_ERR_PARAM
     assert call(eps=float("nan")) == L.LAPATTN_ERR_PARAM
     assert call(d=48) == L.LAPATTN_ERR_UNSUPPORTED
-    assert call(m=65) == L.LAPATTN_ERR_UNSUPPORTED
+    assert call(n=200, m=129) == L.LAPATTN_ERR_UNSUPPORTED      # m up to 128
+    assert call(n=200, m=128, workspace_bytes=0) == L.LAPATTN_ERR_WORKSPACE   # a valid m > 64
     assert call(workspace_bytes=0) == L.LAPATTN_ERR_WORKSPACE    # valid sizes, workspace too small
     need = L.lapattn_workspace_size(1, 2, 100, 32, 8, 4, 0, call is bwd)
     assert call(workspace_bytes=need - 1) == L.LAPATTN_ERR_WORKSPACE

@@ -567,3 +567,71 @@ def test_backward_saved_state_shapes(L, d, m):
         torch.cuda.synchronize()
         assert torch.equal(out_s, out_r)
         assert all(torch.equal(a, b) for a, b in zip(g_s, g_r))
+
+
+# ------------------------------------------------------------------------------ m up to 128 (64 < m: the
+# landmark groups of 64, the Newton-Schulz solve and its backward over many workgroups)
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("d,m,n", [(32, 96, 1000), (64, 128, 1111), (64, 65, 300), (32, 128, 128), (64, 100, 777)])
+def test_forward_many_landmarks(L, dtype, d, m, n):
+    """m past one group of 64 landmarks, each normalisation, ragged n, m = n at 128."""
+    w = W.Workload("bigm", 1, 2, n, d, m, 6, dtype, 1 / math.sqrt(d), math.sqrt(d), 41, False)
+    for norm in (0, 1, 2):
+        check_forward(L, w, norm=norm)
+    check_forward(L, w, norm=MSPACE, whiten=rand_whiten(2, m, 7))
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_forward_many_landmarks_windows_and_options(L, dtype):
+    """4 x 4 windows of a 32 x 64 token map (m = 128) with eps and the convolution branch;
+    Algorithm 2's X0 alone (T = 0), one update, and a kernel that underflows (the c = 0 guard)."""
+    w = W.Workload("bigw", 1, 2, 32 * 64, 64, 128, 8, dtype, 1 / 8, 8.0, 43, False)
+    check_forward(L, w, grid=(64, 4))
+    check_forward(L, w, norm=1, eps=0.05, grid=(64, 4), dwc=W.make_dwc(2, 64, 3, seed=44))
+    for T in (0, 1):
+        check_forward(L, w.with_(T=T, n=500, m=120))
+    check_forward(L, w.with_(n=300, m=99, lam=1e-6))
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("d,m,n", [(32, 96, 700), (64, 128, 600), (64, 73, 333)])
+def test_backward_many_landmarks(L, dtype, d, m, n):
+    """Gradients at m past 64: each normalisation, eps, the landmark-space form."""
+    w = W.Workload("bigmb", 1, 2, n, d, m, 5, dtype, 1 / math.sqrt(d), math.sqrt(d), 45, True)
+    for norm in (0, 1, 2):
+        check_backward(L, w, norm=norm)
+    check_backward(L, w, eps=0.1)
+    check_backward(L, w, norm=MSPACE, whiten=rand_whiten(2, m, 46))
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_backward_many_landmarks_windows(L, dtype):
+    """4 x 4 windows of a 32 x 64 map (m = 128), with the convolution branch; T = 0 and T = 1."""
+    w = W.Workload("bigwb", 1, 2, 32 * 64, 32, 128, 4, dtype, 1 / math.sqrt(32), math.sqrt(32), 47, True)
+    check_backward(L, w, grid=(64, 4))
+    check_backward(L, w, norm=1, grid=(64, 4), dwc=W.make_dwc(2, 32, 3, seed=48))
+    for T in (0, 1):
+        check_backward(L, w.with_(T=T, n=400, m=110))
+
+
+@pytest.mark.parametrize("d,m", [(32, 96), (64, 128), (64, 81)])
+def test_backward_saved_state_many_landmarks(L, d, m):
+    """forward(save) + backward(save) equal the recomputing calls bit for bit past 64 landmarks
+    (the saved rows of A and B in groups of 64), inline and row-sum forms; windows too."""
+    w = W.Workload("savedbig", 2, 2, 700, d, m, 5, "fp32", 1 / math.sqrt(d), math.sqrt(d), 49, True)
+    cases = [(w, dict()), (w, dict(norm=1))]
+    if m == 128:
+        cases.append((w.with_(n=32 * 64), dict(grid=(64, 4))))
+    for wc, kw in cases:
+        say("saved state d=%d m=%d n=%d %s" % (wc.d, wc.m, wc.n, sorted(kw.items())))
+        x = W.make_inputs(wc, with_grad=True)
+        Q, K, V, dO = (to_dev(x[k], wc.dtype) for k in ("Q", "K", "V", "dO"))
+        ws = L.workspace(Q, wc.m, wc.T, True)
+        out_s = L.forward(Q, K, V, wc.m, wc.lam, wc.T, ws=ws, save=True, **kw)
+        g_s = L.backward(Q, K, V, dO, wc.m, wc.lam, wc.T, ws=ws, save=True, **kw)
+        out_r = L.forward(Q, K, V, wc.m, wc.lam, wc.T, **kw)
+        g_r = L.backward(Q, K, V, dO, wc.m, wc.lam, wc.T, **kw)
+        torch.cuda.synchronize()
+        assert torch.equal(out_s, out_r)
+        assert all(torch.equal(a, b) for a, b in zip(g_s, g_r))

@@ -80,7 +80,7 @@ enum {
                                      eps not finite or < 0, unknown norm or dtype,
                                      window options negative or pool_r without grid_w,
                                      dwc_k not 0, 1, 3, 5 or 7, or dwc_k without grid_w */
-    LAPATTN_ERR_UNSUPPORTED = 4,  /* d not in {32, 64} or m > 64 */
+    LAPATTN_ERR_UNSUPPORTED = 4,  /* d not in {32, 64} or m > 128 */
     LAPATTN_ERR_WORKSPACE = 5,    /* workspace NULL or smaller than lapattn_workspace_size() */
     LAPATTN_ERR_HIP = 6,          /* a HIP launch failed */
     LAPATTN_ERR_ALIGN = 7,        /* a tensor pointer is not 16-byte aligned, or the
@@ -112,8 +112,8 @@ enum {
  * shared by the batch (NULL: all ones); ignored by the other normalisations.
  * save (fp32 inputs; ignored for bf16): lapattn_forward keeps the landmark means, the key-side
  * summary, every Newton-Schulz iterate and the n x m kernel values of both sides (K_QL and
- * K_LK^T, 64 floats per token) in the workspace, which must then be sized with
- * LAPATTN_WS_BACKWARD; a following lapattn_backward with save set and the same inputs, sizes,
+ * K_LK^T, 64 floats per token for each group of 64 landmarks) in the workspace, which must
+ * then be sized with LAPATTN_WS_BACKWARD; a following lapattn_backward with save set and the same inputs, sizes,
  * options and workspace (the caller orders the two calls) reuses them instead of recomputing
  * them.  Results are bitwise those of the calls without save. */
 typedef struct {
@@ -142,8 +142,11 @@ size_t lapattn_workspace_size(int B, int H, int n, int d, int m, int ns_iters,
 
 /* Forward pass (Algorithm 1 with Algorithm 2 as the pseudoinverse, the
  * key-summary reordering of Sec. 3.2, and the normalisation chosen in opts).
- * lambda > 0 is the kernel scale, m the number of landmarks (1 <= m <= min(n, 64)),
- * ns_iters the number T of Newton-Schulz updates (T = 0 uses X_0). */
+ * lambda > 0 is the kernel scale, m the number of landmarks (1 <= m <= min(n, 128)),
+ * ns_iters the number T of Newton-Schulz updates (T = 0 uses X_0).  dtype = LAPATTN_BF16
+ * computes from the bf16 inputs directly for m <= 64 (fixed-point L1 distances, fp16 matrix
+ * cores, fp32 accumulation); for m > 64 it runs the fp32 computation on the exactly widened
+ * inputs and rounds the output to bf16 (nearest even). */
 int lapattn_forward(const void* Q, const void* K, const void* V, void* Out,
                     int B, int H, int n, int d, int m, float lambda, int ns_iters,
                     int dtype, const lapattn_opts* opts,

@@ -77,11 +77,16 @@ __global__ __launch_bounds__(256) void nsb_norm_kernel(const double* __restrict_
     const int h = blockIdx.x, tid = threadIdx.x, w = tid >> 6;
     const double* Wh = W + (size_t)h * wstride;
     const int idx = tid % kBig;
+    // 16 loads in flight per batch, summed in index order
+    const int step = tid < kBig ? kBig : 1;
+    const double* p = tid < kBig ? Wh + idx : Wh + (size_t)idx * kBig;
     double s = 0.0;
-    if (tid < kBig) {
-        for (int a = 0; a < kBig; ++a) s += fabs(Wh[a * kBig + idx]);
-    } else {
-        for (int b = 0; b < kBig; ++b) s += fabs(Wh[idx * kBig + b]);
+    for (int i0 = 0; i0 < kBig; i0 += 16) {
+        double v[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) v[i] = p[(size_t)(i0 + i) * step];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) s += fabs(v[i]);
     }
     double v = isnan(s) ? -1.0 : s;
     int arg = idx;
@@ -117,9 +122,15 @@ __global__ __launch_bounds__(256) void nsb_norm_kernel(const double* __restrict_
     __syncthreads();
     const double c = sc;
     double* Xh = X0 + (size_t)h * xstride;
-    for (int e = tid; e < kBig * kBig; e += 256) {
-        const int a = e / kBig, b = e % kBig;
-        Xh[e] = (c > 0.0) ? Wh[b * kBig + a] / c : 0.0;
+    for (int e0 = 0; e0 < kBig * kBig; e0 += 256 * 8) {
+        double v[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int e = e0 + 256 * i + tid, a = e / kBig, b = e % kBig;
+            v[i] = Wh[b * kBig + a];
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) Xh[e0 + 256 * i + tid] = (c > 0.0) ? v[i] / c : 0.0;
     }
 }
 
@@ -136,36 +147,42 @@ __global__ __launch_bounds__(256) void nsb_mm_kernel(NsbJobs js) {
     const int tcn = (J.N + 31) / 32;
     if ((int)blockIdx.x >= ((J.M + 31) / 32) * tcn) return;   // the whole block: no barrier reached
     const int r0 = (blockIdx.x / tcn) * 32, c0 = (blockIdx.x % tcn) * 32;
-    constexpr int SP = 33;
-    __shared__ double sA[kBig * SP];
-    __shared__ double sB[kBig * SP];
+    constexpr int SP = 34;   // even: a lane's two rows (columns) are one 16-byte read
+    __shared__ __attribute__((aligned(16))) double sA[kBig * SP];
+    __shared__ __attribute__((aligned(16))) double sB[kBig * SP];
     const double* A = J.A + (size_t)h * J.sA;
     const double* B = J.B + (size_t)h * J.sB;
     const int K = J.K;
-    for (int e = tid; e < 32 * kBig; e += 256) {
-        int r, k;
-        if (J.ta) { k = e / 32; r = e % 32; } else { r = e / kBig; k = e % kBig; }
-        const int rr = r0 + r;
-        double v = 0.0;
-        if (k < K && rr < J.M) v = J.ta ? A[(size_t)k * J.pa + rr] : A[(size_t)rr * J.pa + k];
-        sA[k * SP + r] = v;
-        int c;
-        if (J.tb) { c = e / kBig; k = e % kBig; } else { k = e / 32; c = e % 32; }
-        const int cc = c0 + c;
-        double u = 0.0;
-        if (k < K && cc < J.N) u = J.tb ? B[(size_t)cc * J.pb + k] : B[(size_t)k * J.pb + cc];
-        sB[k * SP + c] = u;
+    constexpr int NE = 32 * kBig / 256;   // staged elements per thread and operand
+    double va[NE], vb[NE];   // every load issued before the first LDS write
+#pragma unroll
+    for (int i = 0; i < NE; ++i) {
+        const int e = tid + 256 * i;
+        const int kA = J.ta ? e / 32 : e % kBig, rA = J.ta ? e % 32 : e / kBig;
+        const int kB = J.tb ? e % kBig : e / 32, cB = J.tb ? e / kBig : e % 32;
+        const int rr = r0 + rA, cc = c0 + cB;
+        va[i] = (kA < K && rr < J.M) ? (J.ta ? A[(size_t)kA * J.pa + rr] : A[(size_t)rr * J.pa + kA]) : 0.0;
+        vb[i] = (kB < K && cc < J.N) ? (J.tb ? B[(size_t)cc * J.pb + kB] : B[(size_t)kB * J.pb + cc]) : 0.0;
+    }
+#pragma unroll
+    for (int i = 0; i < NE; ++i) {
+        const int e = tid + 256 * i;
+        const int kA = J.ta ? e / 32 : e % kBig, rA = J.ta ? e % 32 : e / kBig;
+        const int kB = J.tb ? e % kBig : e / 32, cB = J.tb ? e / kBig : e % 32;
+        sA[kA * SP + rA] = va[i];
+        sB[kB * SP + cB] = vb[i];
     }
     __syncthreads();
     const int tr = tid >> 4, tc = tid & 15;
     double a00 = 0.0, a01 = 0.0, a10 = 0.0, a11 = 0.0;
+#pragma unroll 8
     for (int k = 0; k < K; ++k) {
-        const double x0 = sA[k * SP + 2 * tr], x1 = sA[k * SP + 2 * tr + 1];
-        const double y0 = sB[k * SP + 2 * tc], y1 = sB[k * SP + 2 * tc + 1];
-        a00 = fma(x0, y0, a00);
-        a01 = fma(x0, y1, a01);
-        a10 = fma(x1, y0, a10);
-        a11 = fma(x1, y1, a11);
+        const double2 x = *reinterpret_cast<const double2*>(sA + k * SP + 2 * tr);
+        const double2 y = *reinterpret_cast<const double2*>(sB + k * SP + 2 * tc);
+        a00 = fma(x.x, y.x, a00);
+        a01 = fma(x.x, y.y, a01);
+        a10 = fma(x.y, y.x, a10);
+        a11 = fma(x.y, y.y, a11);
     }
     const double acc[2][2] = {{a00, a01}, {a10, a11}};
     double* O = J.Out + (size_t)h * J.sOut;
@@ -194,7 +211,16 @@ __global__ __launch_bounds__(256) void nsb_usum_kernel(const float* __restrict__
     const int h = blockIdx.y, e = blockIdx.x * 256 + threadIdx.x;
     if (e >= m * D1) return;
     double u = 0.0;
-    for (int ch = 0; ch < nkc; ++ch) u += (double)Upart[((size_t)h * nkc + ch) * m * D1 + e];
+    const float* p = Upart + (size_t)h * nkc * m * D1 + e;
+    int ch = 0;
+    for (; ch + 8 <= nkc; ch += 8) {   // 8 loads in flight, added in chunk order
+        float v[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = p[(size_t)(ch + i) * m * D1];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) u += (double)v[i];
+    }
+    for (; ch < nkc; ++ch) u += (double)p[(size_t)ch * m * D1];
     Ud[(size_t)h * m * D1 + e] = u;
     U[(size_t)h * m * D1 + e] = (float)u;
 }
@@ -214,12 +240,32 @@ __global__ __launch_bounds__(256) void nsb_final_kernel(const double* __restrict
     __shared__ double sM1[32];
     __shared__ double svb[D];
     const int h = blockIdx.y, r0 = 32 * blockIdx.x, tid = threadIdx.x;
-    for (int e = tid; e < kBig * D1; e += 256) sU[e] = e < m * D1 ? Ud[(size_t)h * m * D1 + e] : 0.0;
-    const double* Xh = XT + (size_t)h * xstride;
-    for (int e = tid; e < 32 * kBig; e += 256) sX[e] = Xh[(size_t)r0 * kBig + e];
+    {
+        constexpr int NU = (kBig * D1 + 255) / 256, NX = 32 * kBig / 256;
+        double u[NU], x[NX];   // every load issued before the first LDS write
+        const double* Xh = XT + (size_t)h * xstride + (size_t)r0 * kBig;
+#pragma unroll
+        for (int i = 0; i < NU; ++i) {
+            const int e = tid + 256 * i;
+            u[i] = e < m * D1 ? Ud[(size_t)h * m * D1 + e] : 0.0;
+        }
+#pragma unroll
+        for (int i = 0; i < NX; ++i) x[i] = Xh[tid + 256 * i];
+#pragma unroll
+        for (int i = 0; i < NU; ++i)
+            if (tid + 256 * i < kBig * D1) sU[tid + 256 * i] = u[i];
+#pragma unroll
+        for (int i = 0; i < NX; ++i) sX[tid + 256 * i] = x[i];
+    }
     if (tid < D) {
         double t = 0.0;
-        for (int l = 0; l < m; ++l) t += vseg[((size_t)h * m + l) * D + tid];
+        for (int l0 = 0; l0 < m; l0 += 16) {   // 16 loads in flight, added in landmark order
+            double v[16];
+#pragma unroll
+            for (int i = 0; i < 16; ++i) v[i] = l0 + i < m ? vseg[((size_t)h * m + l0 + i) * D + tid] : 0.0;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) t += v[i];
+        }
         svb[tid] = t / n;
         if (blockIdx.x == 0) vbar[(size_t)h * D + tid] = (float)(t / n);
     }
@@ -253,9 +299,20 @@ __global__ __launch_bounds__(256) void nsb_bwd_vbar_kernel(const float* __restri
     constexpr int G = 256 / D;
     __shared__ double svb[256];
     const int h = blockIdx.x, tid = threadIdx.x, g = tid / D, cc = tid % D;
-    double s = 0.0;
-    for (int b = g; b < nqb; b += G) s += dvbar_part[((size_t)h * nqb + b) * D + cc];
-    svb[tid] = s;
+    auto colsum = [&](const float* part) {   // blocks g, g + G, ... in order, 8 loads in flight
+        double t = 0.0;
+        int b = g;
+        for (; b + 7 * G < nqb; b += 8 * G) {
+            float v[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) v[i] = part[((size_t)h * nqb + b + i * G) * D + cc];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) t += v[i];
+        }
+        for (; b < nqb; b += G) t += part[((size_t)h * nqb + b) * D + cc];
+        return t;
+    };
+    svb[tid] = colsum(dvbar_part);
     __syncthreads();
     if (tid < D) {
         double t = 0.0;
@@ -266,9 +323,7 @@ __global__ __launch_bounds__(256) void nsb_bwd_vbar_kernel(const float* __restri
     }
     if (mspace) {
         __syncthreads();
-        double s0 = 0.0;
-        for (int b = g; b < nqb; b += G) s0 += p0_part[((size_t)h * nqb + b) * D + cc];
-        svb[tid] = s0;
+        svb[tid] = colsum(p0_part);
         __syncthreads();
         if (tid < D) {
             double t = 0.0;
@@ -293,7 +348,16 @@ __global__ __launch_bounds__(256) void nsb_bwd_dm_kernel(const float* __restrict
     const int a = e / D1, cc = e % D1;
     double dm = 0.0, u = 0.0;
     if (a < m) {
-        for (int ch = 0; ch < nlc; ++ch) dm += (double)dM_part[((size_t)h * nlc + ch) * m * D1 + e];
+        const float* pp = dM_part + (size_t)h * nlc * m * D1 + e;
+        int ch = 0;
+        for (; ch + 8 <= nlc; ch += 8) {   // 8 loads in flight, added in chunk order
+            float v[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) v[i] = pp[(size_t)(ch + i) * m * D1];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) dm += (double)v[i];
+        }
+        for (; ch < nlc; ++ch) dm += (double)pp[(size_t)ch * m * D1];
         if (mspace) {
             const double wa = whiten ? (double)whiten[(size_t)(h % H) * m + a] : 1.0;
             const double* sp = spv + (size_t)h * 2 * D;
@@ -324,54 +388,113 @@ __global__ __launch_bounds__(256) void nsb_bwd_x0_kernel(const double* __restric
     const double c = cinfo[h * 4 + 0], n1 = cinfo[h * 4 + 1], ninf = cinfo[h * 4 + 2];
     const int code = (int)cinfo[h * 4 + 3], as = code / 256, bs = code % 256;
     double part = 0.0;
-    for (int e = tid; e < kBig * kBig; e += 256) part += Gh[e] * Wh[(e % kBig) * kBig + e / kBig];
+    for (int e0 = 0; e0 < kBig * kBig; e0 += 256 * 8) {   // 8 pairs of loads in flight
+        double g[8], wt[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int e = e0 + 256 * i + tid;
+            g[i] = Gh[e];
+            wt[i] = Wh[(e % kBig) * kBig + e / kBig];
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) part += g[i] * wt[i];
+    }
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) part += __shfl_xor(part, off, 64);
     if ((tid & 63) == 0) sp[tid >> 6] = part;
     __syncthreads();
     const double dc = c > 0.0 ? -(((sp[0] + sp[1]) + sp[2]) + sp[3]) / (c * c) : 0.0;
-    for (int e = tid; e < kBig * kBig; e += 256) {
-        const int a = e / kBig, b = e % kBig;
-        const double wab = Wh[e];
-        double v = have_dw ? dW[(size_t)h * mm + e] : 0.0;
-        if (c > 0.0) {
-            v += Gh[b * kBig + a] / c;
-            if (b == bs) v += dc * ninf * sgnd(wab);
-            if (a == as) v += dc * n1 * sgnd(wab);
+    for (int e0 = 0; e0 < kBig * kBig; e0 += 256 * 8) {
+        double wv[8], dv[8], gt[8];   // all loads of the batch in flight together
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int e = e0 + 256 * i + tid, a = e / kBig, b = e % kBig;
+            wv[i] = Wh[e];
+            dv[i] = have_dw ? dW[(size_t)h * mm + e] : 0.0;
+            gt[i] = Gh[b * kBig + a];
         }
-        const double kab = wab - (a == b && a < m ? eps : 0.0);
-        dDW[(size_t)h * mm + e] = (float)(-kab * v / lambda);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int e = e0 + 256 * i + tid, a = e / kBig, b = e % kBig;
+            const double wab = wv[i];
+            double v = dv[i];
+            if (c > 0.0) {
+                v += gt[i] / c;
+                if (b == bs) v += dc * ninf * sgnd(wab);
+                if (a == as) v += dc * n1 * sgnd(wab);
+            }
+            const double kab = wab - (a == b && a < m ? eps : 0.0);
+            dDW[(size_t)h * mm + e] = (float)(-kab * v / lambda);
+        }
     }
     for (int e = tid; e < m * D1; e += 256) dU[(size_t)h * m * D1 + e] = (float)dUd[(size_t)h * kBig * D1 + e];
 }
 
-// K_LL backward: dqtW_a += sum_b dDW_ab sign(qt_a - kt_b) (blockIdx.z = 0, row a = blockIdx.x)
-// and dk~_b = -sum_a dDW_ab sign(qt_a - kt_b) plus the query-side partials (chunk order, fp64),
-// over the landmark's token count (blockIdx.z = 1, b = blockIdx.x): the pooling gradient the
-// key-major pass adds to its dK rows.  grid (m, BH, 2), D threads (one coordinate each).
-__global__ void nsb_bwd_kll_kernel(const float* __restrict__ qt, const float* __restrict__ kt,
-                                   const float* __restrict__ dDW, float* __restrict__ dqtW,
-                                   float* __restrict__ dkpool, const float* __restrict__ dkt_part, LmPool pl, int n,
-                                   int m, int D, int nlc) {
-    const int x = blockIdx.x, h = blockIdx.y, cc = threadIdx.x;
-    if (cc >= D) return;
+// K_LL backward: dqtW_a += sum_b dDW_ab sign(qt_a - kt_b) (blockIdx.z = 0, rows a) and
+// dk~_b = -sum_a dDW_ab sign(qt_a - kt_b) plus the query-side partials (chunk order, fp64), over
+// the landmark's token count (blockIdx.z = 1, columns b): the pooling gradient the key-major pass
+// adds to its dK rows.  grid (ceil(m / R), BH, 2), R = 256 / D landmarks per block, thread (landmark
+// x0 + tid / D, coordinate tid % D); the other side's landmark rows and the block's rows (columns)
+// of dDW are staged in LDS.  Sums in index order.
+template <int D>
+__global__ __launch_bounds__(256) void nsb_bwd_kll_kernel(const float* __restrict__ qt, const float* __restrict__ kt,
+                                                          const float* __restrict__ dDW, float* __restrict__ dqtW,
+                                                          float* __restrict__ dkpool,
+                                                          const float* __restrict__ dkt_part, LmPool pl, int n,
+                                                          int m, int nlc) {
+    constexpr int R = 256 / D;
+    __shared__ float so[kBig * D];
+    __shared__ float st[R * kBig];
+    const int h = blockIdx.y, z = blockIdx.z, tid = threadIdx.x;
+    const int r = tid / D, cc = tid % D, x0 = blockIdx.x * R, x = x0 + r;
+    const float* other = (z == 0 ? kt : qt) + (size_t)h * m * D;
     const float* Th = dDW + (size_t)h * kBig * kBig;
+    {
+        constexpr int NO = kBig * D / 256, NT = R * kBig / 256;
+        float vo[NO], vt[NT];   // every load issued before the first LDS write
+#pragma unroll
+        for (int i = 0; i < NO; ++i) {
+            const int e = tid + 256 * i;
+            vo[i] = e < m * D ? other[e] : 0.f;
+        }
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            const int e = tid + 256 * i, xr = x0 + e / kBig, jj = e % kBig;
+            vt[i] = xr < m ? (z == 0 ? Th[xr * kBig + jj] : Th[jj * kBig + xr]) : 0.f;
+        }
+#pragma unroll
+        for (int i = 0; i < NO; ++i) so[tid + 256 * i] = vo[i];
+#pragma unroll
+        for (int i = 0; i < NT; ++i) st[tid + 256 * i] = vt[i];
+    }
+    __syncthreads();
+    if (x >= m) return;
+    const float* trow = st + r * kBig;
     float s = 0.f;
-    if (blockIdx.z == 0) {
+    if (z == 0) {
         const float qa = qt[((size_t)h * m + x) * D + cc];
         for (int b = 0; b < m; ++b) {
-            const float kb = kt[((size_t)h * m + b) * D + cc], t = Th[x * kBig + b];
+            const float kb = so[b * D + cc], t = trow[b];
             s += (qa > kb) ? t : ((qa < kb) ? -t : 0.f);
         }
         dqtW[((size_t)h * m + x) * D + cc] = s;
     } else {
         const float kb = kt[((size_t)h * m + x) * D + cc];
         for (int a = 0; a < m; ++a) {
-            const float qa = qt[((size_t)h * m + a) * D + cc], t = Th[a * kBig + x];
+            const float qa = so[a * D + cc], t = trow[a];
             s += (qa > kb) ? t : ((qa < kb) ? -t : 0.f);
         }
         double ak = -s;
-        for (int ch = 0; ch < nlc; ++ch) ak += dkt_part[(((size_t)h * nlc + ch) * m + x) * D + cc];
+        const float* pp = dkt_part + ((size_t)h * nlc * m + x) * D + cc;
+        int ch = 0;
+        for (; ch + 8 <= nlc; ch += 8) {   // 8 loads in flight, added in chunk order
+            float v[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) v[i] = pp[(size_t)(ch + i) * m * D];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) ak += v[i];
+        }
+        for (; ch < nlc; ++ch) ak += pp[(size_t)ch * m * D];
         dkpool[((size_t)h * m + x) * D + cc] = (float)ak * (1.f / (float)lm_tokens(pl, x, n, m).count);
     }
 }
@@ -532,8 +655,12 @@ hipError_t launch_nsb_backward(const float* qt, const float* kt, const double* X
     hipLaunchKernelGGL(nsb_bwd_x0_kernel, dim3(BH), dim3(256), 0, st, Gb[T & 1], W, xs, dW, T > 0 ? 1 : 0, cinfo, dDW,
                        dUd, dU, m, D1, lambda, eps);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(nsb_bwd_kll_kernel, dim3(m, BH, 2), dim3(64), 0, st, qt, kt, dDW, dqtW, dkpool, dkt_part, pl, n,
-                       m, d, nlc);
+    if (d == 32)
+        hipLaunchKernelGGL(nsb_bwd_kll_kernel<32>, dim3((m + 7) / 8, BH, 2), dim3(256), 0, st, qt, kt, dDW, dqtW, dkpool,
+                           dkt_part, pl, n, m, nlc);
+    else
+        hipLaunchKernelGGL(nsb_bwd_kll_kernel<64>, dim3((m + 3) / 4, BH, 2), dim3(256), 0, st, qt, kt, dDW, dqtW, dkpool,
+                           dkt_part, pl, n, m, nlc);
     return hipGetLastError();
 }
 

@@ -635,3 +635,20 @@ def test_backward_saved_state_many_landmarks(L, d, m):
         torch.cuda.synchronize()
         assert torch.equal(out_s, out_r)
         assert all(torch.equal(a, b) for a, b in zip(g_s, g_r))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_forward_many_landmarks_full_size_sampled_heads(L, dtype):
+    """The n = 16384 workload (B=8, H=2, d=64) with m = 128 landmarks, as bench.py times it:
+    every output checked finite, four sampled heads against the oracle."""
+    w = W.WORKLOADS["highres"].with_(name="highres_m128", m=128, dtype=dtype)
+    say("forward full %s %s" % (w.name, dtype))
+    x = W.make_inputs(w, with_grad=False)
+    got = run_forward(L, x, w)
+    BH = w.BH
+    heads = sorted(set([0, BH - 1, BH // 2, (7 * BH) // 11]))
+    sub = {k: np.ascontiguousarray(v.reshape(BH, w.n, w.d)[heads][None]) for k, v in x.items()}
+    ref = oracle.forward(sub["Q"], sub["K"], sub["V"], w.m, w.lam, w.T)
+    say("  heads %s" % heads)
+    assert np.isfinite(got).all()
+    assert_parity(got.reshape(BH, w.n, w.d)[heads][None], ref, w.dtype)

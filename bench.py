@@ -328,7 +328,7 @@ def time_sweep(steps):
     """Execution time of the Laplacian kernel evaluation and of the Newton-Schulz solve, forward and
     backward, over sequence lengths n and landmark counts m at batch 1, 2 heads, 32 channels (fp32,
     lambda = sqrt(32), T = 6, inline normalisation): the setting of the paper's kernel timing
-    (Sec. 3, CUDA acceleration).  Ours: per-kernel HIP events around the library's launches in a
+    (Sec. 4.3, CUDA acceleration).  Ours: per-kernel HIP events around the library's launches in a
     forward and backward with the save option (the backward reuses the forward's kernel values).
     Beside them the same computations written as plain PyTorch operations (autograd for their
     backward), timed with events on the same GPU.  out_rel and grad_rel compare the two: the

@@ -285,6 +285,25 @@ def test_long_sequence_few_heads(L, n, d):
     check_backward(L, w)
 
 
+@pytest.mark.parametrize("m", [16, 32, 64])
+def test_sweep_shape_saved_path(L, m):
+    """The kernel-timing sweep's longest shape (B=1, H=2, d=32, n=16384, fp32, lambda = sqrt(32),
+    T = 6, the same seeds) on the path the sweep times -- forward and backward with save on one
+    workspace -- against the oracle, output and gradients."""
+    w = W.Workload("sweep", 1, 2, 16384, 32, m, 6, "fp32", 1 / math.sqrt(32), math.sqrt(32), 7 + 16384 + m, True)
+    say("sweep shape n=%d m=%d, save path" % (w.n, m))
+    x = W.make_inputs(w, with_grad=True)
+    Q, K, V, dO = (to_dev(x[k], w.dtype) for k in ("Q", "K", "V", "dO"))
+    ws = L.workspace(Q, m, w.T, True)
+    out = L.forward(Q, K, V, m, w.lam, w.T, ws=ws, save=True)
+    g = L.backward(Q, K, V, dO, m, w.lam, w.T, ws=ws, save=True)
+    torch.cuda.synchronize()
+    assert_parity(to_np(out), oracle.forward(x["Q"], x["K"], x["V"], m, w.lam, w.T), w.dtype)
+    ref = oracle.backward(x["Q"], x["K"], x["V"], x["dO"], m, w.lam, w.T)
+    for gg, r, what in zip(g[:3], ref[:3], ("dQ", "dK", "dV")):
+        assert_parity(to_np(gg), r, w.dtype, what)
+
+
 def test_backward_eps(L):
     w = W.Workload("beps", 1, 2, 300, 32, 16, 5, "fp32", 0.2, 4.0, 15, True)
     check_backward(L, w, eps=0.1)

@@ -7,7 +7,8 @@ library.  If the library is missing the calls raise; there is no fallback.
 import ctypes
 import os
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblapattn.so")
+# LAPATTN_LIB: another build of the same library (the CPU sanitizer run loads an instrumented one)
+LIB_PATH = os.environ.get("LAPATTN_LIB") or os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblapattn.so")
 
 LAPATTN_FP32, LAPATTN_BF16 = 0, 1
 LAPATTN_NORM_INLINE, LAPATTN_NORM_ROWSUM, LAPATTN_NORM_NONE, LAPATTN_NORM_MSPACE = 0, 1, 2, 3

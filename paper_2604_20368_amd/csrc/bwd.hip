@@ -709,6 +709,9 @@ __global__ __launch_bounds__(256) void bwd_ns_kernel(const float* __restrict__ q
         }
         dqtW[(size_t)h * m * D + e] = s;
     }
+    // dk~_b's K_LL term; dkpool_kernel adds the query-side partial sums and divides by the
+    // landmark's token count (here, at this kernel's register use, their loads would go one at a
+    // time)
     for (int e = tid; e < m * D; e += 256) {
         const int b = e / D, cc = e % D;
         const float kb = skf[e];
@@ -718,14 +721,30 @@ __global__ __launch_bounds__(256) void bwd_ns_kernel(const float* __restrict__ q
             const float qa = sqf[a * D + cc], t = sTf[a * MP + b];
             s += (qa > kb) ? t : ((qa < kb) ? -t : 0.f);
         }
-        // dk~_b: this term plus the query-side partial sums (chunk order, fp64), over the
-        // landmark's token count: the pooling gradient the key-major pass adds to its dK rows
-        const float kw = -s;
-        double ak = kw;
-#pragma unroll 4
-        for (int ch = 0; ch < nlc; ++ch) ak += dkt_part[(((size_t)h * nlc + ch) * m + b) * D + cc];
-        dkpool[(size_t)h * m * D + e] = (float)ak * (1.f / (float)lm_tokens(pl, b, n, m).count);
+        dkpool[(size_t)h * m * D + e] = -s;
     }
+}
+
+// dk~_b = (K_LL term + the query-side partial sums in chunk order, fp64) / |S_b|: the pooling
+// gradient the key-major pass adds to its dK rows.  grid (ceil(m d / 256), BH); the partials of
+// 16 chunks are loaded at a time.
+__global__ __launch_bounds__(256) void dkpool_kernel(float* __restrict__ dkpool, const float* __restrict__ dkt_part,
+                                                     LmPool pl, int n, int m, int D, int nlc) {
+    const int h = blockIdx.y, e = blockIdx.x * 256 + threadIdx.x;
+    if (e >= m * D) return;
+    const size_t md = (size_t)m * D;
+    double ak = dkpool[(size_t)h * md + e];
+    const float* pp = dkt_part + (size_t)h * nlc * md + e;
+    int ch = 0;
+    for (; ch + 16 <= nlc; ch += 16) {
+        float v[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) v[i] = pp[(size_t)(ch + i) * md];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) ak += v[i];
+    }
+    for (; ch < nlc; ++ch) ak += pp[(size_t)ch * md];
+    dkpool[(size_t)h * md + e] = (float)ak * (1.f / (float)lm_tokens(pl, e / D, n, m).count);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -1168,6 +1187,10 @@ hipError_t launch_bwd_ns(const float* qt, const float* kt, const double* Xs, con
     else if (d == 32) LAPATTN_BNS(64, 32);
     else LAPATTN_BNS(64, 64);
 #undef LAPATTN_BNS
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(dkpool_kernel, dim3((m * d + 255) / 256, BH), dim3(256), 0, st, dkpool, dkt_part, pl, n, m, d,
+                       nlc);
     return hipGetLastError();
 }
 

@@ -15,22 +15,44 @@
 namespace lapattn {
 
 // ------------------------------------------------------------------------------------------
-// Landmark means.  grid (m, BH), 256 threads: thread (r, c) sums the landmark's tokens
-// r, r+R, ... (segment or window, lm_tokens) in column c; the R partial sums are added in a
-// fixed order (deterministic).
+// Landmark means.  grid (m S, BH), 256 threads: block (l, s) = (x / S, x % S) sums part s of
+// landmark l's tokens (segment or window, lm_tokens; S contiguous parts, S > 1 when m BH alone
+// would leave most compute units idle); thread (r, c) sums the part's tokens r, r + R, ... in
+// column c, four rows' loads in flight at a time, and the R partial sums are added in a fixed
+// order (deterministic).  S = 1 writes the results; otherwise part[h][l][s][3][d] (fp64) for
+// pool_combine_kernel, which adds the S parts in order.
 template <int DT>
 __global__ __launch_bounds__(256) void pool_kernel(const typename elem<DT>::type* __restrict__ Q,
                                                    const typename elem<DT>::type* __restrict__ K,
                                                    const typename elem<DT>::type* __restrict__ V,
                                                    float* __restrict__ qt, float* __restrict__ kt,
-                                                   double* __restrict__ vseg, int n, int d, int m, LmPool pl) {
-    const int l = blockIdx.x, h = blockIdx.y;
+                                                   double* __restrict__ vseg, double* __restrict__ part, int n, int d,
+                                                   int m, int S, LmPool pl) {
+    const int l = blockIdx.x / S, sp = blockIdx.x % S, h = blockIdx.y;
     const LmTokens tok = lm_tokens(pl, l, n, m);
     const int cntl = tok.count;
+    const int t0 = (int)((long long)cntl * sp / S), t1 = (int)((long long)cntl * (sp + 1) / S);
     const int c = threadIdx.x % d, r = threadIdx.x / d, R = blockDim.x / d;
     const size_t base = (size_t)h * n * d;
     double sq = 0.0, sk = 0.0, sv = 0.0;
-    for (int t = r; t < cntl; t += R) {
+    int t = t0 + r;
+    for (; t + 3 * R < t1; t += 4 * R) {
+        float a[4], b[4], e[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const size_t idx = base + (size_t)tok(t + u * R) * d + c;
+            a[u] = elem<DT>::load(Q, idx);
+            b[u] = elem<DT>::load(K, idx);
+            e[u] = elem<DT>::load(V, idx);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            sq += a[u];
+            sk += b[u];
+            sv += e[u];
+        }
+    }
+    for (; t < t1; t += R) {
         const size_t idx = base + (size_t)tok(t) * d + c;
         sq += elem<DT>::load(Q, idx);
         sk += elem<DT>::load(K, idx);
@@ -48,12 +70,38 @@ __global__ __launch_bounds__(256) void pool_kernel(const typename elem<DT>::type
             b += red[1][rr * d + c];
             e += red[2][rr * d + c];
         }
-        const double cnt = (double)cntl;
-        const size_t o = ((size_t)h * m + l) * d + c;
-        qt[o] = (float)(a / cnt);
-        kt[o] = (float)(b / cnt);
-        vseg[o] = e;
+        if (S == 1) {
+            const double cnt = (double)cntl;
+            const size_t o = ((size_t)h * m + l) * d + c;
+            qt[o] = (float)(a / cnt);
+            kt[o] = (float)(b / cnt);
+            vseg[o] = e;
+        } else {
+            double* pp = part + (((size_t)h * m + l) * S + sp) * 3 * d + c;
+            pp[0] = a;
+            pp[d] = b;
+            pp[2 * d] = e;
+        }
     }
+}
+
+// The S parts of each landmark's sums, added in order.  grid (m, BH), d threads.
+__global__ void pool_combine_kernel(const double* __restrict__ part, float* __restrict__ qt, float* __restrict__ kt,
+                                    double* __restrict__ vseg, int n, int d, int m, int S, LmPool pl) {
+    const int l = blockIdx.x, h = blockIdx.y, c = threadIdx.x;
+    if (c >= d) return;
+    const double* pp = part + ((size_t)h * m + l) * S * 3 * d + c;
+    double a = 0.0, b = 0.0, e = 0.0;
+    for (int sp = 0; sp < S; ++sp) {
+        a += pp[(size_t)sp * 3 * d];
+        b += pp[(size_t)sp * 3 * d + d];
+        e += pp[(size_t)sp * 3 * d + 2 * d];
+    }
+    const double cnt = (double)lm_tokens(pl, l, n, m).count;
+    const size_t o = ((size_t)h * m + l) * d + c;
+    qt[o] = (float)(a / cnt);
+    kt[o] = (float)(b / cnt);
+    vseg[o] = e;
 }
 
 // ------------------------------------------------------------------------------------------
@@ -578,15 +626,26 @@ __global__ __launch_bounds__(256) void query_out_kernel(const float* __restrict_
 
 static inline float kscale_of(float lambda) { return (float)(-1.4426950408889634 / (double)lambda); }
 
+int pool_split(int BH, int n, int m) {
+    const int per = n / m;   // tokens per landmark (segments: this or one more; windows: exactly)
+    int S = 1;
+    while (S < 16 && (long long)m * BH * S < 512 && per / (2 * S) >= 64) S *= 2;
+    return S;
+}
+
 hipError_t launch_pool(int dt, const void* Q, const void* K, const void* V, float* qt, float* kt, double* vseg,
-                       int BH, int n, int d, int m, LmPool pl, hipStream_t st) {
-    dim3 grid(m, BH);
+                       double* part, int BH, int n, int d, int m, LmPool pl, hipStream_t st) {
+    const int S = pool_split(BH, n, m);
+    dim3 grid(m * S, BH);
     if (dt == DT_F32)
         hipLaunchKernelGGL(pool_kernel<DT_F32>, grid, dim3(256), 0, st, (const float*)Q, (const float*)K,
-                           (const float*)V, qt, kt, vseg, n, d, m, pl);
+                           (const float*)V, qt, kt, vseg, part, n, d, m, S, pl);
     else
         hipLaunchKernelGGL(pool_kernel<DT_BF16>, grid, dim3(256), 0, st, (const uint16_t*)Q, (const uint16_t*)K,
-                           (const uint16_t*)V, qt, kt, vseg, n, d, m, pl);
+                           (const uint16_t*)V, qt, kt, vseg, part, n, d, m, S, pl);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || S == 1) return e;
+    hipLaunchKernelGGL(pool_combine_kernel, dim3(m, BH), dim3(64), 0, st, part, qt, kt, vseg, n, d, m, S, pl);
     return hipGetLastError();
 }
 

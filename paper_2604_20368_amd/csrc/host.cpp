@@ -64,6 +64,7 @@ struct FastPlan {
 struct Plan {
     size_t qt, kt, vseg, Upart, Xs, cinfo, U, M, Mc, vbar;               // forward
     size_t Ebuf, Ud, nsbs, dDW;          // m > 64: solve and its backward spread over workgroups
+    size_t pool_part;                    // landmark sums split over blocks (small m BH)
     size_t oF;                           // bf16 forward with m > 64: the fp32 output
     size_t Aq, dDq, rs, dYd, dvbar_part, dM_part, dkt_part, dU, dvbar,   // backward
         dqtW, dkpool, dDk, dqt_part;
@@ -121,6 +122,7 @@ Plan make_plan(int BH, int n, int d, int m, int T, bool bwd, bool bf16 = false, 
     p.qt = c.take(bh * m * d * f);
     p.kt = c.take(bh * m * d * f);
     p.vseg = c.take(bh * m * d * g);
+    p.pool_part = c.take(bh * m * (size_t)lapattn::pool_split(BH, n, m) * 3 * d * g);
     p.Upart = c.take(bh * p.nkc * m * d1 * f);
     // X_0..X_T and W for the backward (always, for m > 64)
     p.Xs = c.take(bh * ((bwd || big) ? (size_t)T + 2 : 1) * mpp * g);
@@ -316,7 +318,9 @@ hipError_t forward_internals(Recorder& rec, const Plan& p, const void* Q, const 
     double* vseg = at<double>(ws, p.vseg);
     float* Upart = at<float>(ws, p.Upart);
     hipError_t e;
-    e = run_named(rec, "pool", [&] { return lapattn::launch_pool(dtype, Q, K, V, qt, kt, vseg, BH, n, d, m, pl, st); });
+    e = run_named(rec, "pool", [&] {
+        return lapattn::launch_pool(dtype, Q, K, V, qt, kt, vseg, at<double>(ws, p.pool_part), BH, n, d, m, pl, st);
+    });
     if (e != hipSuccess) return e;
     e = run_named(rec, "key_summary", [&] {
         return lapattn::launch_key_summary(dtype, K, V, qt, Upart, Bsave, BH, n, d, m, lambda, p.kc, p.nkc, st);

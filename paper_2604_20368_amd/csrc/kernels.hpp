@@ -15,9 +15,12 @@ namespace lapattn {
 // Forward ---------------------------------------------------------------------
 
 // Landmark means qt, kt [BH][m][d] (fp32) and per-landmark value sums vseg [BH][m][d] (fp64);
-// pl selects segments or r x r windows (common.hpp).
+// pl selects segments or r x r windows (common.hpp).  When m BH is small each landmark's tokens
+// are split over pool_split(BH, n, m) blocks whose fp64 sums go to part ([BH][m][S][3][d]) and
+// are added in order by a second launch.
+int pool_split(int BH, int n, int m);
 hipError_t launch_pool(int dt, const void* Q, const void* K, const void* V,
-                       float* qt, float* kt, double* vseg,
+                       float* qt, float* kt, double* vseg, double* part,
                        int BH, int n, int d, int m, LmPool pl, hipStream_t st);
 
 // Key-side summary: per key chunk, Upart[h][chunk][a][c] = sum_j k(qt_a, k_j) [v_j | 1]_c;

@@ -231,11 +231,17 @@ __device__ __forceinline__ int pow2_exp(float mx) { return (mx > 0.f && isfinite
 typedef short s4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s4_t lds_s4_t;
 
-// Scalar loads of one landmark row (D/2 words) into `t`.
+// Scalar loads of one landmark row (D/2 words) into `t`.  The row is read through the
+// constant address space: the tables are written by earlier launches and never within the
+// reading kernel, and this keeps the loads scalar (s_load) wherever the compiler cannot prove
+// the pointer free of the kernel's own stores.
+typedef const __attribute__((address_space(4))) uint32_t cu32_t;
+
 template <int D2>
 __device__ __forceinline__ void load_row(uint32_t (&t)[D2], const uint32_t* __restrict__ row) {
+    cu32_t* q = (cu32_t*)row;
 #pragma unroll
-    for (int c = 0; c < D2; ++c) t[c] = row[c];
+    for (int c = 0; c < D2; ++c) t[c] = q[c];
 }
 
 // The exp2 argument (lap_arg) and the kernel value (lap_row) of one (lane's token, landmark
@@ -260,6 +266,31 @@ template <int D2>
 __device__ __forceinline__ float lap_row(const uint32_t (&kf)[D2], const uint32_t (&t)[D2], uint32_t (&nt)[D2],
                                          const uint32_t* __restrict__ next_row, float esc, float ebias) {
     return __builtin_amdgcn_exp2f(lap_arg<D2>(kf, t, nt, next_row, esc, ebias));
+}
+
+// The exp2 arguments of two tokens (x, y) against one landmark row: four sad chains, the loads
+// of the next row into `nt` issued after the first sad (the wait point for `t`).  Each row
+// fetched through the scalar cache feeds twice the VALU work of lap_arg.
+template <int D2>
+__device__ __forceinline__ void lap_arg2(const uint32_t (&xf)[D2], const uint32_t (&yf)[D2], const uint32_t (&t)[D2],
+                                         uint32_t (&nt)[D2], const uint32_t* __restrict__ next_row, float esc,
+                                         float xbias, float ybias, float& gx, float& gy) {
+    uint32_t u0 = __builtin_amdgcn_sad_u16(xf[0], t[0], 0x4B000000u);
+    __builtin_amdgcn_sched_barrier(0);
+    load_row<D2>(nt, next_row);
+    __builtin_amdgcn_sched_barrier(0);
+    uint32_t u1 = __builtin_amdgcn_sad_u16(xf[1], t[1], 0u);
+    uint32_t v0 = __builtin_amdgcn_sad_u16(yf[0], t[0], 0x4B000000u);
+    uint32_t v1 = __builtin_amdgcn_sad_u16(yf[1], t[1], 0u);
+#pragma unroll
+    for (int c = 2; c < D2; c += 2) {
+        u0 = __builtin_amdgcn_sad_u16(xf[c], t[c], u0);
+        u1 = __builtin_amdgcn_sad_u16(xf[c + 1], t[c + 1], u1);
+        v0 = __builtin_amdgcn_sad_u16(yf[c], t[c], v0);
+        v1 = __builtin_amdgcn_sad_u16(yf[c + 1], t[c + 1], v1);
+    }
+    gx = fmaf(__uint_as_float(u0 + u1), esc, xbias);
+    gy = fmaf(__uint_as_float(v0 + v1), esc, ybias);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -903,6 +934,194 @@ __global__ __launch_bounds__(256, 2) void key_kernel(const uint16_t* __restrict_
 }
 
 // ------------------------------------------------------------------------------------------
+// Key-side partial sums with the landmarks split over the waves (m > 48).  A landmark row in
+// scalar registers feeds one VALU instruction per lane and coordinate pair; in key_kernel each
+// row serves the 64 keys of one wave, and the scalar cache that delivers the rows, not the VALU,
+// sets the pace.  Here a block takes tiles of 128 keys; every wave takes all of them (two per
+// lane: keys l and 64 + l) against its own 16 landmarks 16w..16w+15, so each row serves 128
+// keys, and contracts its rows of U over the tile on fp16 MFMA 16x16x32.  Per tile:
+//   staging: wave w converts its quarter of each key row (coordinates 16w'.. of the codes, u as
+//     in key_kernel) and its quarter of the value columns (fp16 times the value prescale,
+//     transposed to [c][j]) into LDS; one block barrier;
+//   each lane reads its two keys' codes back (rows of pitch D/2 + 4 words: conflict-free
+//   16-byte reads), forms the 2 x 16 kernel values and writes them to the wave's rows of the
+//   [a][j] tile;
+//   MFMA: U[16w + r][c] += sum_j B[16w + r][j] V[j][c] (and the ones column) over the 4 steps
+//   of 32 keys; one block barrier before the next tile's staging.
+// The raw rows of the next tile (each wave its quarters) are loaded behind the landmark loop.
+// Block (h, kb) takes tiles [kb T / nkb, (kb + 1) T / nkb) of the head's T = ceil(n / 128).
+// Writes Upart[h][kb][c][a] as key_kernel does.
+constexpr int kK2Keys = 128;
+constexpr int kK2VP = kK2Keys + 8;   // pitch (halves) of the [c][j] value and [a][j] kernel-value tiles
+
+template <int D>
+__global__ __launch_bounds__(256, D == 32 ? 4 : 3) void key2_kernel(const uint16_t* __restrict__ K,
+                                                                    const uint16_t* __restrict__ V,
+                                                                    const uint32_t* __restrict__ qfix,
+                                                                    const float* __restrict__ frame,
+                                                                    float* __restrict__ Upart, int BH, int n, int m,
+                                                                    int T, int nkb) {
+    constexpr int D2 = D / 2;
+    constexpr int D8 = D / 8;
+    constexpr int C16 = D / 16;
+    constexpr int CP = D2 + 4;      // code row pitch (words)
+    constexpr int QW = D8 / 4;      // 16-byte chunks of a row per wave (a quarter)
+    constexpr int VP = kK2VP;
+    __shared__ __attribute__((aligned(16))) uint32_t sC[kK2Keys * CP];
+    __shared__ __attribute__((aligned(16))) _Float16 sV[D * VP];
+    __shared__ __attribute__((aligned(16))) _Float16 sBt[4 * 16 * VP];
+    const int nblk = BH * nkb;
+    const int kbb = xcd_rank(blockIdx.x, nblk, 0);
+    const int h = kbb / nkb, kb = kbb % nkb;
+    const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
+    const float inv2R = frame[h * 8 + 1], esc = frame[h * 8 + 2], vsc = frame[h * 8 + 3];
+    const float R = frame[h * 8 + 0], xsc = frame[h * 8 + 4];
+    const bool clamped = __float_as_uint(frame[h * 8 + 5]) != 0u;   // integer test: a scalar branch
+    const float ebias = -kTwo23 * esc;
+    const uint32_t* tabw = qfix + ((size_t)h * 64 + 16 * __builtin_amdgcn_readfirstlane(w)) * D2;
+    const int t0 = (int)((long long)kb * T / nkb), t1 = (int)((long long)(kb + 1) * T / nkb);
+    _Float16* const brow = sBt + w * 16 * VP;
+    f32x4_t acc[C16 + 1];
+#pragma unroll
+    for (int cc = 0; cc <= C16; ++cc) acc[cc] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+    h8_t ones;   // B operand of the ones column: 1 in column 0
+#pragma unroll
+    for (int i = 0; i < 8; ++i) ones[i] = (l & 15) == 0 ? (_Float16)1.f : (_Float16)0.f;
+
+    // raw quarters of the lane's two key and value rows (keys past n keep the last values
+    // loaded, finite values of this head: their kernel values are exactly 0)
+    uint4 kq[2][QW] = {}, vq[2][QW] = {};
+    auto fetch = [&](int tile) {
+#pragma unroll
+        for (int s2 = 0; s2 < 2; ++s2) {
+            const int j = tile * kK2Keys + 64 * s2 + l;
+            if (j < n) {
+                const uint4* kp = reinterpret_cast<const uint4*>(K + ((size_t)h * n + j) * D) + QW * w;
+                const uint4* vp = reinterpret_cast<const uint4*>(V + ((size_t)h * n + j) * D) + QW * w;
+#pragma unroll
+                for (int i = 0; i < QW; ++i) kq[s2][i] = kp[i];
+#pragma unroll
+                for (int i = 0; i < QW; ++i) vq[s2][i] = vp[i];
+            }
+        }
+    };
+    if (t0 < t1) fetch(t0);
+    for (int tile = t0; tile < t1; ++tile) {
+        // staging: this wave's quarter of the codes and of the value columns of the 128 keys
+#pragma unroll
+        for (int s2 = 0; s2 < 2; ++s2) {
+            const int r = 64 * s2 + l;   // key row in the tile
+#pragma unroll
+            for (int i = 0; i < QW; ++i) {
+                const uint4 x = kq[s2][i];
+                *reinterpret_cast<uint4*>(sC + r * CP + 4 * (QW * w + i)) =
+                    make_uint4(fix2_bf16(x.x, inv2R), fix2_bf16(x.y, inv2R), fix2_bf16(x.z, inv2R),
+                               fix2_bf16(x.w, inv2R));
+                const uint4 y = vq[s2][i];
+                const uint32_t yw[4] = {y.x, y.y, y.z, y.w};
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const int c = 8 * (QW * w + i) + 2 * t;
+                    const uint32_t pv = pk_f16(bf16_lo(yw[t]) * vsc, bf16_hi(yw[t]) * vsc);
+                    reinterpret_cast<uint16_t*>(sV)[c * VP + r] = (uint16_t)(pv & 0xffffu);
+                    reinterpret_cast<uint16_t*>(sV)[(c + 1) * VP + r] = (uint16_t)(pv >> 16);
+                }
+            }
+        }
+        __syncthreads();   // the tile's codes and values are complete
+        if (tile + 1 < t1) fetch(tile + 1);
+        // the lane's two keys: codes, and the exponent bias (-inf past n: kernel values 0)
+        uint32_t kf0[D2], kf1[D2];
+#pragma unroll
+        for (int c4 = 0; c4 < D2 / 4; ++c4) {
+            const uint4 a0 = *reinterpret_cast<const uint4*>(sC + l * CP + 4 * c4);
+            const uint4 a1 = *reinterpret_cast<const uint4*>(sC + (64 + l) * CP + 4 * c4);
+            kf0[4 * c4] = a0.x; kf0[4 * c4 + 1] = a0.y; kf0[4 * c4 + 2] = a0.z; kf0[4 * c4 + 3] = a0.w;
+            kf1[4 * c4] = a1.x; kf1[4 * c4 + 1] = a1.y; kf1[4 * c4 + 2] = a1.z; kf1[4 * c4 + 3] = a1.w;
+        }
+        const int j0 = tile * kK2Keys + l, j1 = j0 + 64;
+        float kb0 = j0 < n ? ebias : -__builtin_inff(), kb1 = j1 < n ? ebias : -__builtin_inff();
+        if (clamped) {
+            // a head with tokens beyond the range: each key's excess enters its exponent (the
+            // whole rows read again, from cache)
+#pragma unroll
+            for (int s2 = 0; s2 < 2; ++s2) {
+                const int j = s2 ? j1 : j0;
+                if (j < n) {
+                    const uint4* kp = reinterpret_cast<const uint4*>(K + ((size_t)h * n + j) * D);
+                    float ex = 0.f;
+#pragma unroll
+                    for (int c8 = 0; c8 < D8; ++c8) {
+                        const uint4 r4 = kp[c8];
+                        const uint32_t wd[4] = {r4.x, r4.y, r4.z, r4.w};
+#pragma unroll
+                        for (int t = 0; t < 4; ++t)
+                            ex += fmaxf(fabsf(bf16_lo(wd[t])), R) + fmaxf(fabsf(bf16_hi(wd[t])), R);
+                    }
+                    const float bias = fmaf(ex - (float)D * R, xsc, ebias);
+                    if (s2) kb1 = bias;
+                    else kb0 = bias;
+                }
+            }
+        }
+        // kernel values of the wave's 16 landmarks (table rows past m are zero codes: finite
+        // values, in rows of U that the zero columns of X_T drop) for both keys, into the
+        // wave's rows of the [a][j] tile
+        {
+            uint16_t* bw = reinterpret_cast<uint16_t*>(brow);
+            // the rows are the same every tile: an opaque copy of the table pointer keeps the
+            // compiler from hoisting all 16 rows' loads out of the tile loop (they would not fit
+            // the scalar registers)
+            const uint32_t* tabt = tabw;
+            asm volatile("" : "+s"(tabt));
+            uint32_t ta[D2], tb[D2];
+            load_row<D2>(ta, tabt);
+#pragma unroll
+            for (int p = 0; p < 8; ++p) {
+                float x0, y0, x1, y1;   // x: key l, y: key 64 + l; landmarks 16w + 2p, 16w + 2p + 1
+                lap_arg2<D2>(kf0, kf1, ta, tb, tabt + (2 * p + 1) * D2, esc, kb0, kb1, x0, y0);
+                lap_arg2<D2>(kf0, kf1, tb, ta, tabt + (p < 7 ? 2 * p + 2 : 15) * D2, esc, kb0, kb1, x1, y1);
+                const uint32_t v0 = pk_f16(__builtin_amdgcn_exp2f(x0), __builtin_amdgcn_exp2f(y0));
+                const uint32_t v1 = pk_f16(__builtin_amdgcn_exp2f(x1), __builtin_amdgcn_exp2f(y1));
+                bw[(2 * p) * VP + l] = (uint16_t)(v0 & 0xffffu);
+                bw[(2 * p) * VP + 64 + l] = (uint16_t)(v0 >> 16);
+                bw[(2 * p + 1) * VP + l] = (uint16_t)(v1 & 0xffffu);
+                bw[(2 * p + 1) * VP + 64 + l] = (uint16_t)(v1 >> 16);
+            }
+        }
+        // the wave's LDS requests complete in order; the barrier keeps the compiler from moving
+        // the reads of other lanes' values above the writes
+        __builtin_amdgcn_wave_barrier();
+        {
+            const int ao = (l & 15) * VP + 8 * (l >> 4);
+#pragma unroll
+            for (int s4 = 0; s4 < 4; ++s4) {
+                const h8_t A = *reinterpret_cast<const h8_t*>(brow + ao + 32 * s4);
+#pragma unroll
+                for (int cc = 0; cc < C16; ++cc) {
+                    const h8_t Bv = *reinterpret_cast<const h8_t*>(sV + 16 * cc * VP + ao + 32 * s4);
+                    acc[cc] = __builtin_amdgcn_mfma_f32_16x16x32_f16(A, Bv, acc[cc], 0, 0, 0);
+                }
+                acc[C16] = __builtin_amdgcn_mfma_f32_16x16x32_f16(A, ones, acc[C16], 0, 0, 0);
+            }
+        }
+        __syncthreads();   // every wave is done with the codes and values before the next staging
+    }
+    // rows a = 16w + 4(l/16) + r, column 16cc + l%16 (the value columns were formed from
+    // V * vscale); the ones column from column 0 of its block
+    const float inv_vsc = 1.f / vsc;
+    float* dst = Upart + ((size_t)h * nkb + kb) * (D + 1) * 64;
+#pragma unroll
+    for (int cc = 0; cc < C16; ++cc)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) dst[(16 * cc + (l & 15)) * 64 + 16 * w + 4 * (l >> 4) + r] = acc[cc][r] * inv_vsc;
+    if ((l & 15) == 0) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) dst[D * 64 + 16 * w + 4 * (l >> 4) + r] = acc[C16][r];
+    }
+}
+
+// ------------------------------------------------------------------------------------------
 // U = sum over key chunks, M = X_T U, and the query side's copy of M, by column groups:
 // grid (NG, BH) with NG = D/8 + 1, 576 threads (nine waves).  Group g < D/8 holds value columns
 // 8g..8g+7, group D/8 the ones column D.  M = X_T U is separable by columns, so each block sums
@@ -1316,6 +1535,18 @@ hipError_t launch_fast_frame_ns(const float* qt, const float* kt, const double* 
     else
         hipLaunchKernelGGL(frame_ns_kernel<64>, dim3(BH), dim3(kSolveThreads), 0, st, qt, kt, vseg, segmax, vsegmax, frame,
                            qfix, kfix, vbar, XT, cinfo, n, m, lambda, T, eps);
+    return hipGetLastError();
+}
+
+hipError_t launch_fast_key2(const void* K, const void* V, const uint32_t* qfix, const float* frame, float* Upart,
+                            int BH, int n, int d, int m, int T, int nkb, hipStream_t st) {
+    dim3 grid(BH * nkb);
+    if (d == 32)
+        hipLaunchKernelGGL(key2_kernel<32>, grid, dim3(256), 0, st, (const uint16_t*)K, (const uint16_t*)V, qfix,
+                           frame, Upart, BH, n, m, T, nkb);
+    else
+        hipLaunchKernelGGL(key2_kernel<64>, grid, dim3(256), 0, st, (const uint16_t*)K, (const uint16_t*)V, qfix,
+                           frame, Upart, BH, n, m, T, nkb);
     return hipGetLastError();
 }
 

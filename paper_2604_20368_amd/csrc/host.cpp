@@ -59,6 +59,8 @@ struct FastPlan {
     size_t mvec;   // landmark-space normalisation: [BH][2][d]
     size_t total;
     int kpb, nkb;
+    bool split;    // key side with the landmarks split over the waves (key2_kernel), T tiles per head
+    int T;
 };
 
 struct Plan {
@@ -185,10 +187,30 @@ Plan make_plan(int BH, int n, int d, int m, int T, bool bwd, bool bf16 = false, 
 // has about two 64-key tiles per wave when the work allows it.
 FastPlan make_fast_plan(int BH, int n, int d, int m, bool dwc = false) {
     FastPlan p{};
-    const long long tiles = (long long)BH * ((n + 63) / 64);
-    const long long per_wave = tiles / 2048 > 1 ? tiles / 2048 : 1;
-    p.kpb = (int)(256 * per_wave);
-    p.nkb = (n + p.kpb - 1) / p.kpb;
+    p.split = m > 48;
+    if (p.split) {
+        // chunks per head: the fewest (rounds of blocks over the chip's block slots) x (tiles per
+        // block), three blocks per CU at d = 64, four at d = 32; on a tie the fewest rounds, then
+        // the most blocks
+        p.T = (n + 127) / 128;
+        const long long slots = 256LL * (d == 32 ? 4 : 3);
+        long long best = -1, best_rounds = 0;
+        for (int c = 1; c <= p.T; ++c) {
+            const long long rounds = ((long long)BH * c + slots - 1) / slots;
+            const long long cost = rounds * ((p.T + c - 1) / c);
+            if (best < 0 || cost < best || (cost == best && rounds <= best_rounds)) {
+                best = cost;
+                best_rounds = rounds;
+                p.nkb = c;
+            }
+        }
+        p.kpb = 0;
+    } else {
+        const long long tiles = (long long)BH * ((n + 63) / 64);
+        const long long per_wave = tiles / 2048 > 1 ? tiles / 2048 : 1;
+        p.kpb = (int)(256 * per_wave);
+        p.nkb = (n + p.kpb - 1) / p.kpb;
+    }
     const size_t bh = (size_t)BH, d1 = (size_t)d + 1, f = sizeof(float), g = sizeof(double);
     Carver c;
     p.qt = c.take(bh * m * d * f);
@@ -368,6 +390,9 @@ hipError_t forward_fast(Recorder& rec, const FastPlan& p, const void* Q, const v
     });
     if (e != hipSuccess) return e;
     e = run_named(rec, "key", [&] {
+        if (p.split)
+            return lapattn::launch_fast_key2(K, V, at<uint32_t>(ws, p.qfix), at<float>(ws, p.frame),
+                                             at<float>(ws, p.Upart), BH, n, d, m, p.T, p.nkb, st);
         return lapattn::launch_fast_key(K, V, at<uint32_t>(ws, p.qfix), at<float>(ws, p.frame), at<float>(ws, p.Upart),
                                         BH, n, d, m, p.kpb, p.nkb, st);
     });

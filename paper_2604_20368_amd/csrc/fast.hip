@@ -412,7 +412,9 @@ __device__ __forceinline__ void wave_argmax_dpp(float& v, int& idx) {
     idx = 63 - __builtin_amdgcn_readlane(lo, 63);
 }
 
-template <int D>
+// SOLVE = false: the frame and the code tables only (the solve then runs beside the key side,
+// ns_role in key2_kernel).
+template <int D, bool SOLVE>
 __global__ __launch_bounds__(kSolveThreads) void frame_ns_kernel(
     const float* __restrict__ qt, const float* __restrict__ kt, const double* __restrict__ vseg,
     const float* __restrict__ segmax, const float* __restrict__ vsegmax, float* __restrict__ frame,
@@ -543,6 +545,7 @@ __global__ __launch_bounds__(kSolveThreads) void frame_ns_kernel(
         sQ[e] = uq;
         sK[e] = uk;
     }
+    if (!SOLVE) return;
     __syncthreads();
     // ---- W[a][b] = k(qt_a, kt_b) (+ eps on the diagonal): lane a, columns b = BPW w..+BPW
     uint32_t qa[D2];
@@ -934,6 +937,226 @@ __global__ __launch_bounds__(256, 2) void key_kernel(const uint16_t* __restrict_
 }
 
 // ------------------------------------------------------------------------------------------
+// Newton-Schulz of one head by the four waves of a key2_kernel block (m > 48), so that the solve
+// runs beside the key side instead of before it: the same computation as frame_ns_kernel's
+// solve (W from the landmark code tables, c, X0 = W^T / c, the T updates in product form,
+// fp16-pair MFMA 32x32x16), with each wave owning the 32 x 32 block (rb, cb) = (w / 2, w % 2)
+// of both chains, and the transposed copies of Z and E in one buffer each (a second barrier per
+// step instead of a second buffer) to fit the key blocks' LDS: kNsRoleLds bytes.
+constexpr int kNsRoleLds = 4 * 64 * kLP * 2 + 2 * 4 * 64 * 4 + 64 * 4;
+
+template <int D>
+__device__ void ns_role(int h, char* lds, const uint32_t* __restrict__ qfix, const uint32_t* __restrict__ kfix,
+                        const float* __restrict__ frame, float* __restrict__ XT, float* __restrict__ cinfo, int m,
+                        int T, float eps) {
+    constexpr int NW = 4;
+    constexpr int D2 = D / 2;
+    constexpr int BPW = 64 / NW;   // columns b of W per wave
+    constexpr int WP = 68;         // fp32 pitch of the set-up copy of W
+    constexpr int TB = 64 * kLP;
+    _Float16* const ZTh = reinterpret_cast<_Float16*>(lds);
+    _Float16* const ZTl = ZTh + TB;
+    _Float16* const ETh = ZTh + 2 * TB;
+    _Float16* const ETl = ZTh + 3 * TB;
+    float* const part = reinterpret_cast<float*>(ZTh + 4 * TB);   // 2 x NW x 64
+    float* const sred = part + 2 * NW * 64;                        // 64
+    // set-up aliases in the E^T region, each dead before its successor is written: the code
+    // tables, then W in fp32 (read until the barrier that precedes the first store of E^T)
+    uint32_t* const sQ = reinterpret_cast<uint32_t*>(ETh);
+    uint32_t* const sK = sQ + 64 * D2;
+    float* const sWf = reinterpret_cast<float*>(ETh);
+    static_assert(2 * 64 * D2 * 4 <= 2 * TB * 2 && 64 * WP * 4 <= 2 * TB * 2, "set-up copies exceed E^T");
+    const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
+    const float esc = frame[h * 8 + 2];
+    const float ebias = -kTwo23 * esc;
+    {
+        constexpr int NE = 64 * D2 / 256;
+        uint32_t a[NE], b[NE];   // every load issued before the first LDS write
+#pragma unroll
+        for (int r = 0; r < NE; ++r) {
+            a[r] = qfix[(size_t)h * 64 * D2 + tid + 256 * r];
+            b[r] = kfix[(size_t)h * 64 * D2 + tid + 256 * r];
+        }
+#pragma unroll
+        for (int r = 0; r < NE; ++r) {
+            sQ[tid + 256 * r] = a[r];
+            sK[tid + 256 * r] = b[r];
+        }
+    }
+    __syncthreads();
+    // ---- W[a][b] = k(qt_a, kt_b) (+ eps on the diagonal): lane a, columns b = BPW w..+BPW
+    uint32_t qa[D2];
+#pragma unroll
+    for (int c4 = 0; c4 < D2 / 4; ++c4) {
+        const uint4 x = reinterpret_cast<const uint4*>(sQ + l * D2)[c4];
+        qa[4 * c4] = x.x; qa[4 * c4 + 1] = x.y; qa[4 * c4 + 2] = x.z; qa[4 * c4 + 3] = x.w;
+    }
+    float wv[BPW];
+    const uint4* krow = reinterpret_cast<const uint4*>(sK + BPW * w * D2);
+#pragma unroll
+    for (int bb = 0; bb < BPW; bb += 2) {
+        uint4 t0[D2 / 4], t1[D2 / 4];
+#pragma unroll
+        for (int c4 = 0; c4 < D2 / 4; ++c4) {
+            t0[c4] = krow[bb * (D2 / 4) + c4];
+            t1[c4] = krow[(bb + 1) * (D2 / 4) + c4];
+        }
+        uint32_t u0 = 0x4B000000u, u1 = 0u, v0 = 0x4B000000u, v1 = 0u;
+#pragma unroll
+        for (int c4 = 0; c4 < D2 / 4; ++c4) {
+            u0 = __builtin_amdgcn_sad_u16(qa[4 * c4 + 0], t0[c4].x, u0);
+            u1 = __builtin_amdgcn_sad_u16(qa[4 * c4 + 1], t0[c4].y, u1);
+            v0 = __builtin_amdgcn_sad_u16(qa[4 * c4 + 0], t1[c4].x, v0);
+            v1 = __builtin_amdgcn_sad_u16(qa[4 * c4 + 1], t1[c4].y, v1);
+            u0 = __builtin_amdgcn_sad_u16(qa[4 * c4 + 2], t0[c4].z, u0);
+            u1 = __builtin_amdgcn_sad_u16(qa[4 * c4 + 3], t0[c4].w, u1);
+            v0 = __builtin_amdgcn_sad_u16(qa[4 * c4 + 2], t1[c4].z, v0);
+            v1 = __builtin_amdgcn_sad_u16(qa[4 * c4 + 3], t1[c4].w, v1);
+        }
+        wv[bb] = __builtin_amdgcn_exp2f(fmaf(__uint_as_float(u0 + u1), esc, ebias));
+        wv[bb + 1] = __builtin_amdgcn_exp2f(fmaf(__uint_as_float(v0 + v1), esc, ebias));
+    }
+#pragma unroll
+    for (int bb = 0; bb < BPW; ++bb) {
+        const int b = BPW * w + bb;
+        if (l == b) wv[bb] += eps;
+        wv[bb] = (l < m && b < m) ? wv[bb] : 0.f;
+    }
+    float rsum = 0.f, wmax = 0.f;
+#pragma unroll
+    for (int bb = 0; bb < BPW; ++bb) {
+        rsum += fabsf(wv[bb]);
+        wmax = fmaxf(wmax, fabsf(wv[bb]));
+    }
+    wmax = wave_max_dpp(wmax);
+    __syncthreads();   // every wave is done with the code tables, which W replaces
+#pragma unroll
+    for (int q = 0; q < BPW / 4; ++q)
+        *reinterpret_cast<float4*>(sWf + l * WP + BPW * w + 4 * q) =
+            make_float4(wv[4 * q], wv[4 * q + 1], wv[4 * q + 2], wv[4 * q + 3]);
+    if (l == 0) sred[16 + w] = wmax;
+    __syncthreads();
+    {
+        float csum = 0.f;   // column l, rows BPW w..+BPW
+#pragma unroll
+        for (int i = 0; i < BPW; ++i) csum += fabsf(sWf[(BPW * w + i) * WP + l]);
+        part[w * 64 + l] = csum;
+        part[NW * 64 + w * 64 + l] = rsum;   // row l, columns BPW w..+BPW
+    }
+    __syncthreads();
+    if (w == 0) {
+        // column and row sums in a fixed order, then the first maximising column / row
+        float n1 = 0.f, ninf = 0.f, mx = 0.f;
+#pragma unroll
+        for (int g = 0; g < NW; ++g) {
+            n1 += part[g * 64 + l];
+            ninf += part[NW * 64 + g * 64 + l];
+            mx = fmaxf(mx, sred[16 + g]);
+        }
+        int bs, as;
+        wave_argmax_dpp(n1, bs);
+        wave_argmax_dpp(ninf, as);
+        if (l == 0) {
+            const float c = n1 * ninf;
+            sred[2] = c;
+            sred[3] = mx;
+            cinfo[h * 4 + 0] = c;
+            cinfo[h * 4 + 1] = n1;
+            cinfo[h * 4 + 2] = ninf;
+            cinfo[h * 4 + 3] = (float)(as * 256 + bs);
+        }
+    }
+    __syncthreads();
+    const float c = sred[2];
+    const float inv_c = c > 0.f ? 1.f / c : 0.f;
+    float mx = sred[3] * inv_c;             // max |X0| = max |Z_0|
+    float zs = ldexpf(1.f, pow2_exp(mx));   // Z_true = Z_stored * zs
+    {
+        // Z_0^T = X0^T = W / c: BPW consecutive b of row a
+        const float x0s = inv_c / zs;
+        uint32_t xh[BPW / 2], xl[BPW / 2];
+#pragma unroll
+        for (int q = 0; q < BPW / 2; ++q) split_pk(wv[2 * q] * x0s, wv[2 * q + 1] * x0s, xh[q], xl[q]);
+        const int o = l * kLP + BPW * w;
+#pragma unroll
+        for (int q = 0; q < BPW / 8; ++q) {
+            *reinterpret_cast<uint4*>(ZTh + o + 8 * q) = make_uint4(xh[4 * q], xh[4 * q + 1], xh[4 * q + 2], xh[4 * q + 3]);
+            *reinterpret_cast<uint4*>(ZTl + o + 8 * q) = make_uint4(xl[4 * q], xl[4 * q + 1], xl[4 * q + 2], xl[4 * q + 3]);
+        }
+        if (T == 0) {
+#pragma unroll
+            for (int bb = 0; bb < BPW; ++bb) XT[(size_t)h * 4096 + (BPW * w + bb) * 64 + l] = wv[bb] * inv_c;
+        }
+    }
+    __syncthreads();
+    if (T == 0) return;
+    const int rb = w >> 1, cb = w & 1;
+    // Z_0 = X0 (this wave's block, fp32): X0[row][col] = W[col][row] / c
+    f32x16_t zreg;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) zreg[r] = sWf[(32 * cb + (l & 31)) * WP + 32 * rb + c_row(r, l)] * inv_c;
+    // E_0 = I - W X0 (A = W from the fp32 copy, B = X0 through Z^T)
+    f32x16_t e0;
+    {
+        h8_t wah[4], wal[4];
+#pragma unroll
+        for (int s4 = 0; s4 < 4; ++s4) {
+            const float* src = sWf + (32 * rb + (l & 31)) * WP + 16 * s4 + 8 * (l >> 5);
+            uint32_t hq[4], lq[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) split_pk(src[2 * q], src[2 * q + 1], hq[q], lq[q]);
+            wah[s4] = __builtin_bit_cast(h8_t, make_uint4(hq[0], hq[1], hq[2], hq[3]));
+            wal[s4] = __builtin_bit_cast(h8_t, make_uint4(lq[0], lq[1], lq[2], lq[3]));
+        }
+        e0 = mm32_split(wah, wal, ZTh, ZTl, cb);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int row = 32 * rb + c_row(r, l), col = 32 * cb + (l & 31);
+            e0[r] = (row == col ? 1.f : 0.f) - e0[r] * zs;
+        }
+    }
+    __syncthreads();   // every wave has read W before E_0 takes its place
+    store32_t(e0, 1.f, rb, cb, ETh, ETl);
+    __syncthreads();
+    for (int k = 0; k < T; ++k) {
+        // Z_{k+1} = Z_k + Z_k E_k and, but for the last step, E_{k+1} = E_k E_k
+        h8_t ah[4], al[4];
+#pragma unroll
+        for (int s4 = 0; s4 < 4; ++s4) {
+            ah[s4] = a_from_transposed(ZTh, rb, 16 * s4);
+            al[s4] = a_from_transposed(ZTl, rb, 16 * s4);
+        }
+        const f32x16_t dz = mm32_split(ah, al, ETh, ETl, cb);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) zreg[r] = fmaf(dz[r], zs, zreg[r]);
+        if (k + 1 < T) {
+#pragma unroll
+            for (int s4 = 0; s4 < 4; ++s4) {
+                ah[s4] = a_from_transposed(ETh, rb, 16 * s4);
+                al[s4] = a_from_transposed(ETl, rb, 16 * s4);
+            }
+            const f32x16_t e = mm32_split(ah, al, ETh, ETl, cb);
+            // scale of Z_{k+1} from the maximum of Z_k (mx)
+            zs = ldexpf(1.f, (mx > 0.f && isfinite(mx)) ? ilogbf(mx) - 7 : 0);
+            float lm = 0.f;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) lm = fmaxf(lm, fabsf(zreg[r]));
+            lm = wave_max_dpp(lm);
+            __syncthreads();   // every wave's reads of step k are done
+            store32_t(zreg, 1.f / zs, rb, cb, ZTh, ZTl);
+            store32_t(e, 1.f, rb, cb, ETh, ETl);
+            if (l == 0) sred[32 + w] = lm;
+            __syncthreads();
+            mx = fmaxf(fmaxf(sred[32], sred[33]), fmaxf(sred[34], sred[35]));
+        } else {
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                XT[(size_t)h * 4096 + (32 * rb + c_row(r, l)) * 64 + 32 * cb + (l & 31)] = zreg[r];
+        }
+    }
+}
+
+// ------------------------------------------------------------------------------------------
 // Key-side partial sums with the landmarks split over the waves (m > 48).  A landmark row in
 // scalar registers feeds one VALU instruction per lane and coordinate pair; in key_kernel each
 // row serves the 64 keys of one wave, and the scalar cache that delivers the rows, not the VALU,
@@ -951,27 +1174,46 @@ __global__ __launch_bounds__(256, 2) void key_kernel(const uint16_t* __restrict_
 // The raw rows of the next tile (each wave its quarters) are loaded behind the landmark loop.
 // Block (h, kb) takes tiles [kb T / nkb, (kb + 1) T / nkb) of the head's T = ceil(n / 128).
 // Writes Upart[h][kb][c][a] as key_kernel does.
+// The first nns blocks of the launch solve Newton-Schulz for heads 0 .. nns - 1 (ns_role) while
+// the key blocks run: mfinal_kernel, the next launch, is the first to need X_T.
 constexpr int kK2Keys = 128;
 constexpr int kK2VP = kK2Keys + 8;   // pitch (halves) of the [c][j] value and [a][j] kernel-value tiles
+
+template <int D>
+struct K2Lds {
+    static constexpr int CP = D / 2 + 4;   // code row pitch (words)
+    static constexpr int C_BYTES = kK2Keys * CP * 4;
+    static constexpr int V_BYTES = D * kK2VP * 2;
+    static constexpr int B_BYTES = 4 * 16 * kK2VP * 2;
+    static constexpr int KEY = C_BYTES + V_BYTES + B_BYTES;
+    static constexpr int BYTES = KEY > kNsRoleLds ? KEY : kNsRoleLds;
+};
 
 template <int D>
 __global__ __launch_bounds__(256, D == 32 ? 4 : 3) void key2_kernel(const uint16_t* __restrict__ K,
                                                                     const uint16_t* __restrict__ V,
                                                                     const uint32_t* __restrict__ qfix,
+                                                                    const uint32_t* __restrict__ kfix,
                                                                     const float* __restrict__ frame,
-                                                                    float* __restrict__ Upart, int BH, int n, int m,
-                                                                    int T, int nkb) {
+                                                                    float* __restrict__ Upart, float* __restrict__ XT,
+                                                                    float* __restrict__ cinfo, int BH, int n, int m,
+                                                                    int ntile, int nkb, int T, float eps, int nns) {
     constexpr int D2 = D / 2;
     constexpr int D8 = D / 8;
     constexpr int C16 = D / 16;
-    constexpr int CP = D2 + 4;      // code row pitch (words)
+    constexpr int CP = K2Lds<D>::CP;
     constexpr int QW = D8 / 4;      // 16-byte chunks of a row per wave (a quarter)
     constexpr int VP = kK2VP;
-    __shared__ __attribute__((aligned(16))) uint32_t sC[kK2Keys * CP];
-    __shared__ __attribute__((aligned(16))) _Float16 sV[D * VP];
-    __shared__ __attribute__((aligned(16))) _Float16 sBt[4 * 16 * VP];
+    __shared__ __attribute__((aligned(16))) char lds[K2Lds<D>::BYTES];
+    if ((int)blockIdx.x < nns) {
+        ns_role<D>(blockIdx.x, lds, qfix, kfix, frame, XT, cinfo, m, T, eps);
+        return;
+    }
+    uint32_t* const sC = reinterpret_cast<uint32_t*>(lds);
+    _Float16* const sV = reinterpret_cast<_Float16*>(lds + K2Lds<D>::C_BYTES);
+    _Float16* const sBt = reinterpret_cast<_Float16*>(lds + K2Lds<D>::C_BYTES + K2Lds<D>::V_BYTES);
     const int nblk = BH * nkb;
-    const int kbb = xcd_rank(blockIdx.x, nblk, 0);
+    const int kbb = xcd_rank((int)blockIdx.x - nns, nblk, nns);
     const int h = kbb / nkb, kb = kbb % nkb;
     const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
     const float inv2R = frame[h * 8 + 1], esc = frame[h * 8 + 2], vsc = frame[h * 8 + 3];
@@ -979,7 +1221,7 @@ __global__ __launch_bounds__(256, D == 32 ? 4 : 3) void key2_kernel(const uint16
     const bool clamped = __float_as_uint(frame[h * 8 + 5]) != 0u;   // integer test: a scalar branch
     const float ebias = -kTwo23 * esc;
     const uint32_t* tabw = qfix + ((size_t)h * 64 + 16 * __builtin_amdgcn_readfirstlane(w)) * D2;
-    const int t0 = (int)((long long)kb * T / nkb), t1 = (int)((long long)(kb + 1) * T / nkb);
+    const int t0 = (int)((long long)kb * ntile / nkb), t1 = (int)((long long)(kb + 1) * ntile / nkb);
     _Float16* const brow = sBt + w * 16 * VP;
     f32x4_t acc[C16 + 1];
 #pragma unroll
@@ -1529,24 +1771,32 @@ hipError_t launch_fast_frame_ns(const float* qt, const float* kt, const double* 
                                 const float* vsegmax, float* frame, uint32_t* qfix, uint32_t* kfix, float* vbar,
                                 float* XT, float* cinfo, int BH, int n, int d, int m, float lambda, int T, float eps,
                                 hipStream_t st) {
-    if (d == 32)
-        hipLaunchKernelGGL(frame_ns_kernel<32>, dim3(BH), dim3(kSolveThreads), 0, st, qt, kt, vseg, segmax, vsegmax, frame,
-                           qfix, kfix, vbar, XT, cinfo, n, m, lambda, T, eps);
+    // m > 48: the frame alone; the solve runs in the key-side launch (key2_kernel)
+    if (d == 32 && m > 48)
+        hipLaunchKernelGGL((frame_ns_kernel<32, false>), dim3(BH), dim3(kSolveThreads), 0, st, qt, kt, vseg, segmax,
+                           vsegmax, frame, qfix, kfix, vbar, XT, cinfo, n, m, lambda, T, eps);
+    else if (m > 48)
+        hipLaunchKernelGGL((frame_ns_kernel<64, false>), dim3(BH), dim3(kSolveThreads), 0, st, qt, kt, vseg, segmax,
+                           vsegmax, frame, qfix, kfix, vbar, XT, cinfo, n, m, lambda, T, eps);
+    else if (d == 32)
+        hipLaunchKernelGGL((frame_ns_kernel<32, true>), dim3(BH), dim3(kSolveThreads), 0, st, qt, kt, vseg, segmax,
+                           vsegmax, frame, qfix, kfix, vbar, XT, cinfo, n, m, lambda, T, eps);
     else
-        hipLaunchKernelGGL(frame_ns_kernel<64>, dim3(BH), dim3(kSolveThreads), 0, st, qt, kt, vseg, segmax, vsegmax, frame,
-                           qfix, kfix, vbar, XT, cinfo, n, m, lambda, T, eps);
+        hipLaunchKernelGGL((frame_ns_kernel<64, true>), dim3(BH), dim3(kSolveThreads), 0, st, qt, kt, vseg, segmax,
+                           vsegmax, frame, qfix, kfix, vbar, XT, cinfo, n, m, lambda, T, eps);
     return hipGetLastError();
 }
 
-hipError_t launch_fast_key2(const void* K, const void* V, const uint32_t* qfix, const float* frame, float* Upart,
-                            int BH, int n, int d, int m, int T, int nkb, hipStream_t st) {
-    dim3 grid(BH * nkb);
+hipError_t launch_fast_key2(const void* K, const void* V, const uint32_t* qfix, const uint32_t* kfix,
+                            const float* frame, float* Upart, float* XT, float* cinfo, int BH, int n, int d, int m,
+                            int ntile, int nkb, int T, float eps, hipStream_t st) {
+    dim3 grid(BH + BH * nkb);   // BH solve blocks first, then the key blocks
     if (d == 32)
-        hipLaunchKernelGGL(key2_kernel<32>, grid, dim3(256), 0, st, (const uint16_t*)K, (const uint16_t*)V, qfix,
-                           frame, Upart, BH, n, m, T, nkb);
+        hipLaunchKernelGGL(key2_kernel<32>, grid, dim3(256), 0, st, (const uint16_t*)K, (const uint16_t*)V, qfix, kfix,
+                           frame, Upart, XT, cinfo, BH, n, m, ntile, nkb, T, eps, BH);
     else
-        hipLaunchKernelGGL(key2_kernel<64>, grid, dim3(256), 0, st, (const uint16_t*)K, (const uint16_t*)V, qfix,
-                           frame, Upart, BH, n, m, T, nkb);
+        hipLaunchKernelGGL(key2_kernel<64>, grid, dim3(256), 0, st, (const uint16_t*)K, (const uint16_t*)V, qfix, kfix,
+                           frame, Upart, XT, cinfo, BH, n, m, ntile, nkb, T, eps, BH);
     return hipGetLastError();
 }
 

@@ -2,6 +2,7 @@
 // planning, launch sequencing on the caller's stream, optional per-kernel timing.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <initializer_list>
 #include <mutex>
@@ -190,10 +191,11 @@ FastPlan make_fast_plan(int BH, int n, int d, int m, bool dwc = false) {
     p.split = m > 48;
     if (p.split) {
         // chunks per head: the fewest (rounds of blocks over the chip's block slots) x (tiles per
-        // block), three blocks per CU at d = 64, four at d = 32; on a tie the fewest rounds, then
-        // the most blocks
+        // block), three blocks per CU at d = 64, four at d = 32, less the BH slots of the blocks
+        // that solve Newton-Schulz in the same launch; on a tie the fewest rounds, then the most
+        // blocks
         p.T = (n + 127) / 128;
-        const long long slots = 256LL * (d == 32 ? 4 : 3);
+        const long long slots = std::max(256LL, 256LL * (d == 32 ? 4 : 3) - BH);
         long long best = -1, best_rounds = 0;
         for (int c = 1; c <= p.T; ++c) {
             const long long rounds = ((long long)BH * c + slots - 1) / slots;
@@ -391,8 +393,9 @@ hipError_t forward_fast(Recorder& rec, const FastPlan& p, const void* Q, const v
     if (e != hipSuccess) return e;
     e = run_named(rec, "key", [&] {
         if (p.split)
-            return lapattn::launch_fast_key2(K, V, at<uint32_t>(ws, p.qfix), at<float>(ws, p.frame),
-                                             at<float>(ws, p.Upart), BH, n, d, m, p.T, p.nkb, st);
+            return lapattn::launch_fast_key2(K, V, at<uint32_t>(ws, p.qfix), at<uint32_t>(ws, p.kfix),
+                                             at<float>(ws, p.frame), at<float>(ws, p.Upart), at<float>(ws, p.XT),
+                                             at<float>(ws, p.cinfo), BH, n, d, m, p.T, p.nkb, T, eps, st);
         return lapattn::launch_fast_key(K, V, at<uint32_t>(ws, p.qfix), at<float>(ws, p.frame), at<float>(ws, p.Upart),
                                         BH, n, d, m, p.kpb, p.nkb, st);
     });

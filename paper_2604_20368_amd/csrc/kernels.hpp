@@ -149,9 +149,12 @@ hipError_t launch_fast_frame_ns(const float* qt, const float* kt, const double* 
                                 float* XT, float* cinfo, int BH, int n, int d, int m, float lambda, int T, float eps,
                                 hipStream_t st);
 // The same with the landmarks split over the waves (m > 48): blocks (h, kb) of the head's
-// T = ceil(n / 128) tiles of 128 keys, tiles [kb T / nkb, (kb + 1) T / nkb).
-hipError_t launch_fast_key2(const void* K, const void* V, const uint32_t* qfix, const float* frame, float* Upart,
-                            int BH, int n, int d, int m, int T, int nkb, hipStream_t st);
+// ntile = ceil(n / 128) tiles of 128 keys, tiles [kb ntile / nkb, (kb + 1) ntile / nkb); the
+// launch also holds BH blocks that solve Newton-Schulz (T updates, eps) into XT and cinfo, from
+// the code tables qfix, kfix (launch_fast_frame_ns writes only the frame when m > 48).
+hipError_t launch_fast_key2(const void* K, const void* V, const uint32_t* qfix, const uint32_t* kfix,
+                            const float* frame, float* Upart, float* XT, float* cinfo, int BH, int n, int d, int m,
+                            int ntile, int nkb, int T, float eps, hipStream_t st);
 hipError_t launch_fast_key(const void* K, const void* V, const uint32_t* qfix, const float* frame, float* Upart,
                            int BH, int n, int d, int m, int kpb, int nkb, hipStream_t st);
 // mspace: the landmark-space normalisation (operand rows scaled by the whitening [H][m], NULL:

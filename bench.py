@@ -237,9 +237,10 @@ def time_other_forwards(steps, names=("pvt_stage1", "deit_small", "highres_m128"
 def time_dwc_branch(steps):
     """The depth-wise convolution branch of Eq. (7) (3 x 3 filters with bias over the 56 x 56 token
     map): the bf16 PVT stage-1 forward (7 x 7 window landmarks) with and without the branch, and
-    the fp32 training backward with it.  The branch kernels are HBM-bound: dwc reads V once and
-    writes fp32 DWC(V), dwc_dv reads dOut and reads and writes dV, dwc_dw reads dOut and V (each
-    neighbour row comes back from cache); reported against the 8 TB/s HBM peak."""
+    the fp32 training backward with it.  In the bf16 forward the 3 x 3 branch is formed in the
+    query kernel's epilogue (no kernel of its own: "ms" - "ms_without" is its cost).  The backward
+    branch kernels are HBM-bound: dwc_dv reads dOut and reads and writes dV, dwc_dw reads dOut and
+    V (each neighbour row comes back from cache); reported against the 8 TB/s HBM peak."""
     import torch
     from paper_2604_20368_amd import lapattn
     dev = torch.device("cuda:0")
@@ -258,7 +259,7 @@ def time_dwc_branch(steps):
             ws0, ws1 = lapattn.workspace(Q, w.m, w.T), lapattn.workspace(Q, w.m, w.T, dwc=True)
             plain = lambda: lapattn.forward(Q, K, V, w.m, w.lam, w.T, out=out, ws=ws0, grid=grid)
             fn = lambda: lapattn.forward(Q, K, V, w.m, w.lam, w.T, out=out, ws=ws1, grid=grid, dwc=dwc)
-            nbytes = {"dwc": nd * (s + 4)}
+            nbytes = {}
         else:
             grads = tuple(torch.empty_like(Q) for _ in range(3))
             dg = (torch.empty_like(dwc[0]), torch.empty_like(dwc[1]))
@@ -288,7 +289,8 @@ def time_dwc_branch(steps):
             per.setdefault(k, []).append(t)
         avg = {k: sum(v) / len(v) for k, v in per.items()}
         r["kernels_ms"] = {k: round(v, 4) for k, v in avg.items()}
-        r["hbm_frac"] = {k: round(b / (avg[k] * 1e-3) / 1e9 / PEAK_HBM_GBS, 3) for k, b in nbytes.items()}
+        r["hbm_frac"] = {k: round(b / (avg[k] * 1e-3) / 1e9 / PEAK_HBM_GBS, 3) for k, b in nbytes.items() if k in avg}
+        r["branch_ms"] = round(r["ms"] - r["ms_without"], 4)
         res[leg] = r
     return res
 

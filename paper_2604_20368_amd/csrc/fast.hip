@@ -38,6 +38,9 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 constexpr int kLP = 72;            // LDS row pitch (halves) of the 64 x 64 fp16 tiles
 constexpr float kTwo23 = 8388608.f;
+// Word 3 of a raw (unswizzled, stride 0) buffer resource on CDNA: 32-bit data format, so that
+// loads are range-checked against the byte count in word 2 and return 0 past it.
+constexpr int kRawBufferWord3 = 0x00020000;
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
@@ -1541,7 +1544,14 @@ __global__ __launch_bounds__(kMfinalThreads) void mfinal_kernel(const float* __r
 // accumulated in fp32 in the landmark loop from the unrounded kernel values where the
 // normalisation needs it (row sums, landmark space); the inline form reads M centred by
 // mfinal_kernel, out_i = Y'_i + vbar.
-template <int D, int NORM>
+// DWC = 1: the 3 x 3 convolution branch of Eq. (7) is formed here from the value rows of the
+// queries' map neighbours (V, bf16; filters dwc_w [H][d][3][3] and bias dwc_b [H][d] or NULL;
+// map width gw) instead of being read from `extra`.  The wave's 64 rows are convolved in D/8
+// passes between the landmark pairs, lane l taking channels 8 (l % (D/8)) .. +7 of one row, so
+// that each neighbour load reads whole rows and its latency hides behind the kernel
+// evaluations; the sums wait in LDS (fp32) for the epilogue, which adds the attention part there
+// and converts the row once.
+template <int D, int NORM, int DWC = 0>
 __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict__ Q, uint16_t* __restrict__ Out,
                                                      const uint32_t* __restrict__ kfix,
                                                      const uint32_t* __restrict__ kcen,
@@ -1549,7 +1559,9 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
                                                      const float* __restrict__ mscale,
                                                      const float* __restrict__ Mones, const float* __restrict__ vbar,
                                                      const float* __restrict__ extra,
-                                                     const float* __restrict__ mvec, int n, int m, int nqb, int BH) {
+                                                     const float* __restrict__ mvec, int n, int m, int nqb, int BH,
+                                                     const uint16_t* __restrict__ V, const float* __restrict__ dwc_w,
+                                                     const float* __restrict__ dwc_b, int gw, int H) {
     constexpr int D2 = D / 2;
     constexpr int D8 = D / 8;
     constexpr int CB = D / 32;
@@ -1560,7 +1572,11 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
     // per wave: the bf16 output rows of one 32-query half, staged so that they leave as whole
     // rows (pitch D + 8 halves)
     constexpr int OP = D + 8;
-    __shared__ __attribute__((aligned(16))) uint16_t sOut[4 * 32 * OP];
+    __shared__ __attribute__((aligned(16))) uint16_t sOut[DWC ? 8 : 4 * 32 * OP];
+    // convolution branch: per wave, its 64 rows in fp32 (pitch D + 4 floats), first the
+    // branch's sums and then the finished output rows
+    constexpr int SP = D + 4;
+    __shared__ __attribute__((aligned(16))) float sSt[DWC ? 4 * 64 * SP : 4];
     const int lin = xcd_rank(blockIdx.x, nqb * BH, 0);
     const int h = lin / nqb, qblk = lin % nqb;
     const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
@@ -1634,6 +1650,83 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
     // at most 1, and a far query's values stay in fp16's range instead of underflowing.  The
     // factor f = exp2(sh) of the row is applied in fp32 in the epilogue (it cancels under the
     // row-sum normalisation).
+    // convolution passes: pass k covers rows k RPP + l / CPR of the wave, channels cw .. cw + 7
+    constexpr int CPR = D / 8, RPP = 64 / CPR, NP = 64 / RPP, PI = 32 / NP;
+    const int cw = (l % CPR) * 8;
+    float dw[9][8], db[8];   // this lane's filter taps and bias
+    uint4 nv[9];             // the pass's neighbour rows, loaded a pass ahead
+    // V rows of this head through a raw buffer resource: a tap off the map reads at the
+    // resource's end, where the load returns zeros (its product adds nothing)
+    const uint32_t vbytes = (uint32_t)n * (uint32_t)(2 * D);   // < 2^32: B H n d < 2^31
+    const uint64_t vbase = (uint64_t)(V + (size_t)h * n * D);   // the block's head: one value per block
+    const uint64_t vbase_s = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(vbase >> 32)) << 32) |
+                             (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)vbase);
+    const __amdgpu_buffer_rsrc_t vres = __builtin_amdgcn_make_buffer_rsrc((void*)vbase_s, 0, (int)vbytes, kRawBufferWord3);
+    // map position (xq, yq) of the lane's row in the next pass, advanced by RPP tokens a pass;
+    // rows past n are not clamped: their loads stay range-checked and their sums are not stored
+    const int gh = DWC ? n / gw : 1;
+    const int qy = DWC ? RPP / gw : 0, rx = RPP - qy * gw;
+    int yq = 0, xq = 0;
+    if (DWC) {
+        const int iq = i0 + l / CPR;
+        yq = iq / gw;
+        xq = iq - yq * gw;
+    }
+    const uint32_t oc0 = (uint32_t)((i0 + l / CPR) * D + cw) * 2u;
+    auto dwc_issue = [&](int k) {
+        const bool yu = yq > 0, yd = yq < gh - 1, xl = xq > 0, xr = xq < gw - 1;
+#pragma unroll
+        for (int tp = 0; tp < 9; ++tp) {
+            const int dy = tp / 3 - 1, dx = tp % 3 - 1;
+            const bool in = (dy < 0 ? yu : (dy > 0 ? yd : true)) & (dx < 0 ? xl : (dx > 0 ? xr : true));
+            // in-map offsets are exact under the unsigned wrap
+            const uint32_t o = in ? oc0 + (uint32_t)((k * RPP + dy * gw + dx) * 2 * D) : vbytes;
+            nv[tp] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(vres, (int)o, 0, 0));
+        }
+        xq += rx;
+        yq += qy;
+        if (xq >= gw) {
+            xq -= gw;
+            ++yq;
+        }
+    };
+    auto dwc_pass = [&](int k) {
+        float a[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) a[e] = db[e];
+#pragma unroll
+        for (int tp = 0; tp < 9; ++tp) {
+            const uint32_t wd[4] = {nv[tp].x, nv[tp].y, nv[tp].z, nv[tp].w};
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                a[2 * t] = fmaf(dw[tp][2 * t], __uint_as_float(wd[t] << 16), a[2 * t]);
+                a[2 * t + 1] = fmaf(dw[tp][2 * t + 1], __uint_as_float(wd[t] & 0xffff0000u), a[2 * t + 1]);
+            }
+        }
+        float* dst = sSt + (w * 64 + k * RPP + l / CPR) * SP + cw;
+        *reinterpret_cast<float4*>(dst) = make_float4(a[0], a[1], a[2], a[3]);
+        *reinterpret_cast<float4*>(dst + 4) = make_float4(a[4], a[5], a[6], a[7]);
+    };
+    if (DWC) {
+        // filters [H][d][3][3]: the lane's eight channels are 72 consecutive floats
+        const float4* fw = reinterpret_cast<const float4*>(dwc_w + ((size_t)(h % H) * D + cw) * 9);
+        float f[72];
+#pragma unroll
+        for (int e = 0; e < 18; ++e) {
+            const float4 v4 = fw[e];
+            f[4 * e] = v4.x;
+            f[4 * e + 1] = v4.y;
+            f[4 * e + 2] = v4.z;
+            f[4 * e + 3] = v4.w;
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+#pragma unroll
+            for (int tp = 0; tp < 9; ++tp) dw[tp][e] = f[9 * e + tp];
+            db[e] = dwc_b ? dwc_b[(size_t)(h % H) * D + cw + e] : 0.f;
+        }
+        dwc_issue(0);
+    }
     uint32_t ah[32];
     float srow = 0.f;   // s_i of this lane's query (of the shifted values)
     float fsh;          // exp2(sh)
@@ -1659,8 +1752,13 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
             } else {
                 ah[p] = 0u;
             }
+            if (DWC && p % PI == PI - 1) {
+                dwc_pass(p / PI);
+                if (p / PI + 1 < NP) dwc_issue(p / PI + 1);
+            }
         }
     }
+    if (DWC) __builtin_amdgcn_wave_barrier();   // the passes' rows are read by other lanes below
     // lower half keeps ah[8s+t] (queries 0..31, landmarks 16s..16s+7) and receives queries
     // 32..63 / landmarks 16s..16s+7; the upper half receives queries 0..31 / 16s+8..16s+15
     // and keeps queries 32..63 / 16s+8..16s+15.
@@ -1717,7 +1815,19 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
                     o2 += mb.z;
                     o3 += mb.w;
                 }
-                if (extra) {   // the convolution branch of Eq. (7); rows past n read row n - 1
+                if (DWC) {
+                    // the convolution branch of Eq. (7), summed by the passes above: the row
+                    // finishes in fp32 where the sums were and is converted once, below
+                    float* so = sSt + (w * 64 + 32 * qb + (l & 31)) * SP + c0;
+                    const float4 cv = *reinterpret_cast<const float4*>(so);
+                    o0 += cv.x;
+                    o1 += cv.y;
+                    o2 += cv.z;
+                    o3 += cv.w;
+                    if (nan_head) o0 = o1 = o2 = o3 = __builtin_nanf("");
+                    *reinterpret_cast<float4*>(so) = make_float4(o0, o1, o2, o3);
+                    continue;
+                } else if (extra) {   // the convolution branch of Eq. (7); rows past n read row n - 1
                     const int iq = min(i0 + 32 * qb + (l & 31), n - 1);
                     const float4 ex = *reinterpret_cast<const float4*>(extra + ((size_t)h * n + iq) * D + c0);
                     o0 += ex.x;
@@ -1738,11 +1848,22 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
         // the reads of other lanes' rows above the writes.  Rows leave as 16-byte chunks, D/8
         // lanes per row, with non-temporal stores (the output is not read again here).
         __builtin_amdgcn_wave_barrier();
-        constexpr int CPR = D / 8, RPP = 64 / CPR;
 #pragma unroll
         for (int r0 = 0; r0 < 32; r0 += RPP) {
             const int r = r0 + l / CPR, c = (l % CPR) * 8;
-            const uint4 v = *reinterpret_cast<const uint4*>(sOut + (w * 32 + r) * OP + c);
+            uint4 v;
+            if (DWC) {
+                typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+                const float* src = sSt + (w * 64 + 32 * qb + r) * SP + c;
+                const float4 u0 = *reinterpret_cast<const float4*>(src);
+                const float4 u1 = *reinterpret_cast<const float4*>(src + 4);
+                const bf16x2_t p0 = {(__bf16)u0.x, (__bf16)u0.y}, p1 = {(__bf16)u0.z, (__bf16)u0.w};
+                const bf16x2_t p2 = {(__bf16)u1.x, (__bf16)u1.y}, p3 = {(__bf16)u1.z, (__bf16)u1.w};
+                v = {__builtin_bit_cast(uint32_t, p0), __builtin_bit_cast(uint32_t, p1),
+                     __builtin_bit_cast(uint32_t, p2), __builtin_bit_cast(uint32_t, p3)};
+            } else {
+                v = *reinterpret_cast<const uint4*>(sOut + (w * 32 + r) * OP + c);
+            }
             const int iq = i0 + 32 * qb + r;
             if (iq < n)
                 __builtin_nontemporal_store(__builtin_bit_cast(u32x4_t, v),
@@ -1828,23 +1949,30 @@ hipError_t launch_fast_mfinal(const float* Upart, const float* XT, _Float16* Mt,
 hipError_t launch_fast_query(int norm, const void* Q, void* Out, const uint32_t* kfix, const uint32_t* kcen,
                              const float* frame,
                              const _Float16* Mt, const float* mscale, const float* Mones, const float* vbar,
-                             const float* extra, const float* mvec, int BH, int n, int d, int m, hipStream_t st) {
+                             const float* extra, const float* mvec, int BH, int n, int d, int m, const void* V,
+                             const float* dwc_w, const float* dwc_b, int gw, int H, hipStream_t st) {
     const int nqb = (n + 255) / 256;
     dim3 grid(nqb * BH);
-#define LAPATTN_Q2(Dv, Nv)                                                                                        \
-    hipLaunchKernelGGL((query2_kernel<Dv, Nv>), grid, dim3(256), 0, st, (const uint16_t*)Q, (uint16_t*)Out, kfix, \
-                       kcen, frame, Mt, mscale, Mones, vbar, extra, mvec, n, m, nqb, BH)
+    const bool fused = dwc_w != nullptr;   // the 3 x 3 branch in the epilogue
+#define LAPATTN_Q2(Dv, Nv, Fv)                                                                                        \
+    hipLaunchKernelGGL((query2_kernel<Dv, Nv, Fv>), grid, dim3(256), 0, st, (const uint16_t*)Q, (uint16_t*)Out, kfix, \
+                       kcen, frame, Mt, mscale, Mones, vbar, extra, mvec, n, m, nqb, BH, (const uint16_t*)V, dwc_w,   \
+                       dwc_b, gw, H)
+#define LAPATTN_Q2N(Dv, Fv)                                              \
+    do {                                                                 \
+        if (norm == NORM_INLINE) LAPATTN_Q2(Dv, NORM_INLINE, Fv);        \
+        else if (norm == NORM_ROWSUM) LAPATTN_Q2(Dv, NORM_ROWSUM, Fv);   \
+        else if (norm == NORM_MSPACE) LAPATTN_Q2(Dv, NORM_MSPACE, Fv);   \
+        else LAPATTN_Q2(Dv, NORM_NONE, Fv);                              \
+    } while (0)
     if (d == 32) {
-        if (norm == NORM_INLINE) LAPATTN_Q2(32, NORM_INLINE);
-        else if (norm == NORM_ROWSUM) LAPATTN_Q2(32, NORM_ROWSUM);
-        else if (norm == NORM_MSPACE) LAPATTN_Q2(32, NORM_MSPACE);
-        else LAPATTN_Q2(32, NORM_NONE);
+        if (fused) LAPATTN_Q2N(32, 1);
+        else LAPATTN_Q2N(32, 0);
     } else {
-        if (norm == NORM_INLINE) LAPATTN_Q2(64, NORM_INLINE);
-        else if (norm == NORM_ROWSUM) LAPATTN_Q2(64, NORM_ROWSUM);
-        else if (norm == NORM_MSPACE) LAPATTN_Q2(64, NORM_MSPACE);
-        else LAPATTN_Q2(64, NORM_NONE);
+        if (fused) LAPATTN_Q2N(64, 1);
+        else LAPATTN_Q2N(64, 0);
     }
+#undef LAPATTN_Q2N
 #undef LAPATTN_Q2
     return hipGetLastError();
 }

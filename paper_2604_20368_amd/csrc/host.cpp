@@ -371,7 +371,10 @@ hipError_t forward_fast(Recorder& rec, const FastPlan& p, const void* Q, const v
                         lapattn::LmPool pl, const Dwc& dwc, const float* whiten, hipStream_t st) {
     const bool mspace = norm == LAPATTN_NORM_MSPACE;
     hipError_t e;
-    float* E = dwc.k ? at<float>(ws, p.E) : nullptr;
+    // the convolution branch: 3 x 3 filters are formed in the query kernel's epilogue; other
+    // sizes by the separate stencil kernel into E, which the query kernel adds
+    const bool dwc_fused = dwc.k == 3;
+    float* E = (dwc.k && !dwc_fused) ? at<float>(ws, p.E) : nullptr;
     if (E) {
         e = run_named(rec, "dwc", [&] {
             return lapattn::launch_dwc_fwd(lapattn::DT_BF16, V, dwc.w, dwc.b, E, BH, H, n, d, pl.gw, dwc.k, st);
@@ -411,9 +414,10 @@ hipError_t forward_fast(Recorder& rec, const FastPlan& p, const void* Q, const v
     if (e != hipSuccess) return e;
     e = run_named(rec, "query", [&] {
         return lapattn::launch_fast_query(norm, Q, Out, at<uint32_t>(ws, p.kfix), at<uint32_t>(ws, p.kcen),
-                                          at<float>(ws, p.frame),
-                                          at<_Float16>(ws, p.Mt), at<float>(ws, p.mscale), at<float>(ws, p.Mones),
-                                          at<float>(ws, p.vbar), E, at<float>(ws, p.mvec), BH, n, d, m, st);
+                                          at<float>(ws, p.frame), at<_Float16>(ws, p.Mt), at<float>(ws, p.mscale),
+                                          at<float>(ws, p.Mones), at<float>(ws, p.vbar), E, at<float>(ws, p.mvec), BH,
+                                          n, d, m, V, dwc_fused ? dwc.w : nullptr, dwc_fused ? dwc.b : nullptr, pl.gw,
+                                          H, st);
     });
     return e;
 }

@@ -166,10 +166,13 @@ hipError_t launch_fast_mfinal(const float* Upart, const float* XT, _Float16* Mt,
                               float* M, int BH, int d, int m, int nkb, const float* whiten, int mspace, int H,
                               float* mvec, const float* vbar, int center, const uint32_t* kfix, uint32_t* kcen,
                               float* frame, hipStream_t st);
+// Query side: Out = normalise(K_QL M) (+ extra [BH][n][d] fp32 when given); with dwc_w, the 3 x 3
+// convolution branch (filters [H][d][3][3], bias [H][d] or NULL, map width gw) formed from V in
+// the epilogue instead.
 hipError_t launch_fast_query(int norm, const void* Q, void* Out, const uint32_t* kfix, const uint32_t* kcen,
-                             const float* frame,
-                             const _Float16* Mt, const float* mscale, const float* Mones, const float* vbar,
-                             const float* extra, const float* mvec, int BH, int n, int d, int m, hipStream_t st);
+                             const float* frame, const _Float16* Mt, const float* mscale, const float* Mones,
+                             const float* vbar, const float* extra, const float* mvec, int BH, int n, int d, int m,
+                             const void* V, const float* dwc_w, const float* dwc_b, int gw, int H, hipStream_t st);
 
 // Depth-wise convolution branch of Eq. (7) (dwc.hip) ------------------------------------------
 // Filters W [H][d][k][k], bias [H][d] (may be NULL), over the row-major token map of width gw;

@@ -497,7 +497,7 @@ def ingest_traffic(kernel, fetch_dir, write_dir, copy_fetch_dir, copy_write_dir,
     `kernel`, stamped with a hash of the kernel sources (bench.py reports null once the
     sources change)."""
     import hashlib
-    symbol = {"key": "key_kernel", "query": "query2_kernel", "pool": "pool2_kernel", "frame_ns": "frame_ns_kernel",
+    symbol = {"key": "key2_kernel", "query": "query2_kernel", "pool": "pool2_kernel", "frame_ns": "frame_ns_kernel",
               "m_final": "mfinal_kernel"}[kernel]
     f_k = _pmc_per_dispatch(fetch_dir, "FETCH_SIZE", symbol)
     w_k = _pmc_per_dispatch(write_dir, "WRITE_SIZE", symbol)
@@ -597,7 +597,7 @@ def summarize_trace(trace_dir):
     """Per-kernel statistics (calls, average, min, max in us) of a rocprofv3 kernel trace of
     `bench.py --steps 20 --warmup 5 --no-cpu-baseline --no-other --no-dwc`, split into the
     headline forward (the bf16 kernels) and the training legs by launch order: 43 forwards
-    (4 kernels each), 43 backwards (9) and 43 saved steps (10) of 3 warmup + 20 timed + 20
+    (4 kernels each), 43 backwards (10) and 43 saved steps (11) of 3 warmup + 20 timed + 20
     event-timed calls."""
     import csv
     import re
@@ -609,10 +609,10 @@ def summarize_trace(trace_dir):
         mm = re.search(r"lapattn::(\w+)", r["Kernel_Name"]) or re.search(r"_ZN7lapattn\d+(\w+?)I", r["Kernel_Name"])
         if mm:
             seq.append((mm.group(1), (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3))
-    fast = {"pool2_kernel", "frame_ns_kernel", "key_kernel", "mfinal_kernel", "query2_kernel"}
+    fast = {"pool2_kernel", "frame_ns_kernel", "key_kernel", "key2_kernel", "mfinal_kernel", "query2_kernel"}
     head = [x for x in seq if x[0] in fast]
     fp32 = [x for x in seq if x[0] not in fast]
-    nf, nb, ns = 43 * 4, 43 * 9, 43 * 10
+    nf, nb, ns = 43 * 4, 43 * 10, 43 * 11
     if len(fp32) != nf + nb + ns:
         raise SystemExit("unexpected launch count %d" % len(fp32))
     out = {}

@@ -7,7 +7,8 @@
 //
 //   bwd_query_kernel     query-major: dY, dA = dY M^T, dD = -A dA / lambda, direct dQ
 //   bwd_query_lm_kernel  landmark-major over queries: dM = A^T dY, dkt from K_QL
-//   bwd_ns_kernel        dX = dM U^T, dU = X_T^T dM, reverse Newton-Schulz, K_LL backward
+//   bwd_ns_kernel        dX = dM U^T, dU = X_T^T dM, reverse Newton-Schulz, dDW (the K_LL
+//                        backward itself runs in kll_bwd_kernel, nsbig.hip)
 //   bwd_key_kernel       key-major: dB = dU [v|1]^T, dV, dD' = -B dB / lambda, dK
 //   bwd_key_lm_kernel    landmark-major over keys: dqt from K_LK
 //   bwd_pool_kernel      landmark-mean backward into dQ
@@ -447,11 +448,13 @@ __global__ __launch_bounds__(64) void bwd_query_lm_kernel(const float* __restric
 }
 
 // ------------------------------------------------------------------------------------------
-// Newton-Schulz backward, one block of 256 threads per head, fp64, products on the fp64 matrix
-// cores (ns_mfma.hpp).
-//   dM = sum of partials;  dX_T = dM U^T;  dU = X_T^T dM.
+// Newton-Schulz backward, one block of 256 threads per head (ns_mfma.hpp).
+//   dM = sum of partials;  dX_T = dM U^T;  dU = X_T^T dM  (fp64, fp64 matrix cores).
 //   For t = T-1..0, with G = dL/dX_{t+1} and X_{t+1} = 2 X_t - X_t W X_t:
-//     dW -= X_t^T G X_t^T;   G <- 2G - G X_t^T W^T - W^T X_t^T G.
+//     dW -= X_t^T G X_t^T;   G <- 2G - G X_t^T W^T - W^T X_t^T G,
+//   five fp32 products per step (fp32 matrix cores, ns32_mm): P = X^T G, P X^T, W^T P (the
+//   last term, reusing P), G X^T and (G X^T) W^T; G, X, W and P are held both ways in LDS
+//   (row-major as left factors, transposed as right ones), X_{t-1} is loaded while step t runs.
 //   X0 = W^T / c:  dW += G^T / c + dc (||W||_inf [b = b*] + ||W||_1 [a = a*]) sign(W),
 //     dc = -<G, W^T> / c^2.
 //   K_LL: dDW = -k dW / lambda;  dqt_a += sum_b dDW_ab sign(qt_a - kt_b);  dkt_b -= same.
@@ -464,30 +467,40 @@ __global__ __launch_bounds__(256) void bwd_ns_kernel(const float* __restrict__ q
                                                      float* __restrict__ dvbar, float* __restrict__ dqtW,
                                                      float* __restrict__ dkpool, const float* __restrict__ dkt_part,
                                                      LmPool pl, const float* __restrict__ p0_part,
-                                                     const float* __restrict__ whiten, int mspace, int H, int n,
+                                                     const float* __restrict__ whiten, int mspace,
+                                                     float* __restrict__ dDW, int H, int n,
                                                      int m, int T, double lambda, double eps, int nlc, int nqb) {
     using SQ = ns_tiles<MP, MP>;
     using SU = ns_tiles<MP, D>;
     constexpr int D1 = D + 1;
     constexpr int P = ns_pitch(MP);
     constexpr int PU = ns_pitch(D);
-    // W, X, G, T (MP x MP each, pitch P); before the reverse iteration the same space holds the
-    // value columns of U and dM (MP x D each, pitch PU) and X_T (pitch P).
-    constexpr int PRE = 2 * MP * PU + MP * P;
-    constexpr int LDSN = (4 * MP * P > PRE) ? 4 * MP * P : PRE;
-    __shared__ double lds[LDSN];
+    using L = ns32_tiles<MP>;
+    constexpr int PF = L::P;              // pitch (floats) of the fp32 matrices
+    constexpr int MSZ = MP * PF;
+    // fp32 reverse iteration: W, W^T, X, X^T, G, G^T, P (later G X^T), P^T.  Before it the same
+    // space holds the fp64 value columns of U and dM (MP x D each, pitch PU) and X_T (pitch P).
+    constexpr int PRE = (2 * MP * PU + MP * P) * 8;
+    constexpr int F32 = 8 * MSZ * 4;
+    __shared__ __attribute__((aligned(16))) char lds[F32 > PRE ? F32 : PRE];
     __shared__ double su1[MP], sdm1[MP];
     __shared__ double svb[256];
+    __shared__ double sred4[4];
     __shared__ double sp1[D], sp0[D];   // landmark-space form: sums of (1 - s_i) dO_i and of dO_i
-    double* sW = lds;
-    double* sX = lds + MP * P;
-    double* sG = lds + 2 * MP * P;
-    double* sT = lds + 3 * MP * P;
+    float* const fW = reinterpret_cast<float*>(lds);
+    float* const fWT = fW + MSZ;
+    float* const fX = fW + 2 * MSZ;
+    float* const fXT = fW + 3 * MSZ;
+    float* const fG = fW + 4 * MSZ;
+    float* const fGT = fW + 5 * MSZ;
+    float* const fP = fW + 6 * MSZ;
+    float* const fPT = fW + 7 * MSZ;
     const int h = blockIdx.x, tid = threadIdx.x;
-    const float* q = qt + (size_t)h * m * D;
-    const float* k = kt + (size_t)h * m * D;
     const size_t mm = (size_t)MP * MP;
     const double* Xh = Xs + (size_t)h * (T + 2) * mm;   // X_0 .. X_T, then W
+    // W's loads go first: they are waited for only when the reverse iteration begins
+    double wr[MP * MP / 256];
+    ns_fetch<MP>(wr, Xh + (size_t)(T + 1) * mm);
     const double c = cinfo[h * 4 + 0], n1 = cinfo[h * 4 + 1], ninf = cinfo[h * 4 + 2];
     const int code = (int)cinfo[h * 4 + 3];
 
@@ -524,10 +537,11 @@ __global__ __launch_bounds__(256) void bwd_ns_kernel(const float* __restrict__ q
         }
         __syncthreads();
     }
+    f64x4_t dX[SQ::NT];
     {
-        double* sU = lds;
-        double* sdM = lds + MP * PU;
-        double* sXT = lds + 2 * MP * PU;
+        double* sU = reinterpret_cast<double*>(lds);
+        double* sdM = sU + MP * PU;
+        double* sXT = sU + 2 * MP * PU;
         // dM = sum of the landmark-chunk partials (in chunk order); each thread's entries are
         // loaded together, chunk by chunk
         constexpr int NE = (MP * D1 + 255) / 256;
@@ -535,15 +549,21 @@ __global__ __launch_bounds__(256) void bwd_ns_kernel(const float* __restrict__ q
 #pragma unroll
         for (int r = 0; r < NE; ++r) dm[r] = 0.0;
         const int lim = m * D1 - 1;
-#pragma unroll 4
-        for (int ch = 0; ch < nlc; ++ch) {
-            const float* dp = dM_part + ((size_t)h * nlc + ch) * m * D1;
+        // CB chunks' loads in flight at a time, added in chunk order
+        constexpr int CB = NE > 9 ? 4 : 8;
+        for (int c0 = 0; c0 < nlc; c0 += CB) {
+            float v[CB][NE];
 #pragma unroll
-            for (int r = 0; r < NE; ++r) {
-                const int e = tid + 256 * r;
-                const float v = dp[min(e, lim)];
-                dm[r] += (e <= lim) ? (double)v : 0.0;
+            for (int cc = 0; cc < CB; ++cc) {
+                const float* dp = dM_part + ((size_t)h * nlc + min(c0 + cc, nlc - 1)) * m * D1;
+#pragma unroll
+                for (int r = 0; r < NE; ++r) v[cc][r] = dp[min(tid + 256 * r, lim)];
             }
+#pragma unroll
+            for (int cc = 0; cc < CB; ++cc)
+#pragma unroll
+                for (int r = 0; r < NE; ++r)
+                    if (c0 + cc < nlc && tid + 256 * r <= lim) dm[r] += (double)v[cc][r];
         }
         if (mspace) {
             // the partials hold the gradient of M~ = diag(w) M with the ones column 1/m; with
@@ -581,7 +601,6 @@ __global__ __launch_bounds__(256) void bwd_ns_kernel(const float* __restrict__ q
         ns_load<MP, P>(sXT, Xh + (size_t)T * mm);
         __syncthreads();
         // dX = dM U^T (registers, kept until G is stored) and dU = X_T^T dM (global)
-        f64x4_t dX[SQ::NT];
         ns_mm<MP, MP, D, false, true, PU, PU>(sdM, sU, dX);
 #pragma unroll
         for (int i = 0; i < SQ::NT; ++i)
@@ -603,148 +622,127 @@ __global__ __launch_bounds__(256) void bwd_ns_kernel(const float* __restrict__ q
             for (int a = 0; a < MP; ++a) s += sXT[a * P + tid] * sdm1[a];
             dU[((size_t)h * m + tid) * D1 + D] = (float)s;
         }
-        __syncthreads();
-        // W (kernel + eps I, as the forward solve stored it) and G = dX
-        ns_load<MP, P>(sW, Xh + (size_t)(T + 1) * mm);
-        ns_store<MP, MP, P>(sG, dX);
+        __syncthreads();   // the fp64 operands are dead: the fp32 matrices take the space
     }
-    f64x4_t dW[SQ::NT];
+    // W (kernel + eps I as the forward solve stored it: fp64 copies of fp32 values) both ways,
+    // and G = dX both ways
+    {
 #pragma unroll
-    for (int i = 0; i < SQ::NT; ++i) dW[i] = f64x4_t{0.0, 0.0, 0.0, 0.0};
+        for (int r = 0; r < MP * MP / 256; ++r) {
+            const int e = tid + 256 * r, a = e / MP, b = e % MP;
+            const float wv = (float)wr[r];
+            fW[a * PF + b] = wv;
+            fWT[b * PF + a] = wv;
+        }
+#pragma unroll
+        for (int i = 0; i < SQ::NT; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int a = SQ::row(i, j), b = SQ::col(i);
+                const float gv = (float)dX[i][j];
+                fG[a * PF + b] = gv;
+                fGT[b * PF + a] = gv;
+            }
+    }
+    const int row0 = 4 * ((tid & 63) >> 4), col = ns32_col<MP>();   // this lane's tile rows: 16 tr + row0 + j
+    f32x4_t dW[L::NT];
+#pragma unroll
+    for (int i = 0; i < L::NT; ++i) dW[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     if (c > 0.0) {
-        // X_t comes through registers: the loads of X_{t-1} are issued before step t's products
+        // X_t comes through registers: the loads of X_{t-1} are issued while step t runs
         double xr[MP * MP / 256];
         if (T > 0) ns_fetch<MP>(xr, Xh + (size_t)(T - 1) * mm);
-        __syncthreads();
         for (int t = T - 1; t >= 0; --t) {
-            ns_put<MP, P>(sX, xr);
-            __syncthreads();
+#pragma unroll
+            for (int r = 0; r < MP * MP / 256; ++r) {
+                const int e = tid + 256 * r, a = e / MP, b = e % MP;
+                const float xv = (float)xr[r];
+                fX[a * PF + b] = xv;
+                fXT[b * PF + a] = xv;
+            }
+            __syncthreads();   // X_t, and G from the previous step
             if (t > 0) ns_fetch<MP>(xr, Xh + (size_t)(t - 1) * mm);
-            f64x4_t r[SQ::NT], r2[SQ::NT];
-            // dW -= X^T G X^T
-            ns_mm<MP, MP, MP, true, false, P, P>(sX, sG, r);       // X^T G
-            ns_store<MP, MP, P>(sT, r);
-            __syncthreads();
-            ns_mm<MP, MP, MP, false, true, P, P>(sT, sX, r);       // (X^T G) X^T
+            f32x4_t r1[L::NT], r3[L::NT], r4[L::NT];
+            ns32_mm<MP>(fXT, fGT, r1);   // P = X^T G
 #pragma unroll
-            for (int i = 0; i < SQ::NT; ++i) dW[i] -= r[i];
-            __syncthreads();
-            // G X^T W^T
-            ns_mm<MP, MP, MP, false, true, P, P>(sG, sX, r);       // G X^T
-            ns_store<MP, MP, P>(sT, r);
-            __syncthreads();
-            ns_mm<MP, MP, MP, false, true, P, P>(sT, sW, r2);      // (G X^T) W^T
-            __syncthreads();
-            // W^T X^T G = (X W)^T G
-            ns_mm<MP, MP, MP, true, true, P, P>(sW, sX, r);        // W^T X^T
-            ns_store<MP, MP, P>(sT, r);
-            __syncthreads();
-            ns_mm<MP, MP, MP, false, false, P, P>(sT, sG, r);      // (W^T X^T) G
-            __syncthreads();
+            for (int i = 0; i < L::NT; ++i) {
+                const int ra = 16 * L::tr(i) + row0;
 #pragma unroll
-            for (int i = 0; i < SQ::NT; ++i)
+                for (int j = 0; j < 4; ++j) fP[(ra + j) * PF + col] = r1[i][j];
+                *reinterpret_cast<float4*>(fPT + col * PF + ra) = make_float4(r1[i][0], r1[i][1], r1[i][2], r1[i][3]);
+            }
+            __syncthreads();
+            ns32_mm<MP>(fP, fX, r1);     // P X^T
+#pragma unroll
+            for (int i = 0; i < L::NT; ++i) dW[i] -= r1[i];
+            ns32_mm<MP>(fWT, fPT, r3);   // W^T P = W^T X^T G
+            ns32_mm<MP>(fG, fX, r4);     // G X^T
+            __syncthreads();   // P, X and X^T are read: G X^T takes P's buffer
+#pragma unroll
+            for (int i = 0; i < L::NT; ++i) {
+                const int ra = 16 * L::tr(i) + row0;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) fP[(ra + j) * PF + col] = r4[i][j];
+            }
+            __syncthreads();
+            ns32_mm<MP>(fP, fW, r1);     // (G X^T) W^T
+            // G <- 2G - G X^T W^T - W^T X^T G (each lane rewrites its own entries; G is not
+            // read again in this step)
+#pragma unroll
+            for (int i = 0; i < L::NT; ++i) {
+                const int ra = 16 * L::tr(i) + row0;
+                float gn[4];
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
-                    const int a = SQ::row(i, j), b = SQ::col(i);
-                    sG[a * P + b] = 2.0 * sG[a * P + b] - r2[i][j] - r[i][j];
+                    gn[j] = 2.f * fG[(ra + j) * PF + col] - r1[i][j] - r3[i][j];
+                    fG[(ra + j) * PF + col] = gn[j];
                 }
-            __syncthreads();
+                *reinterpret_cast<float4*>(fGT + col * PF + ra) = make_float4(gn[0], gn[1], gn[2], gn[3]);
+            }
         }
+        __syncthreads();   // G = dL/dX_0
         // X0 = W^T / c
         const int as = code / 256, bs = code % 256;
         // <G, W^T>: block reduction in fixed order
         double part = 0.0;
 #pragma unroll
-        for (int i = 0; i < SQ::NT; ++i)
+        for (int i = 0; i < L::NT; ++i)
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                const int a = SQ::row(i, j), b = SQ::col(i);
-                part += sG[a * P + b] * sW[b * P + a];
+                const int a = 16 * L::tr(i) + row0 + j;
+                part += (double)fG[a * PF + col] * (double)fW[col * PF + a];
             }
 #pragma unroll
         for (int off = 32; off >= 1; off >>= 1) part += __shfl_xor(part, off, 64);
-        if ((tid & 63) == 0) sT[tid >> 6] = part;
+        if ((tid & 63) == 0) sred4[tid >> 6] = part;
         __syncthreads();
-        const double dc = -(((sT[0] + sT[1]) + sT[2]) + sT[3]) / (c * c);
+        const double dc = -(((sred4[0] + sred4[1]) + sred4[2]) + sred4[3]) / (c * c);
 #pragma unroll
-        for (int i = 0; i < SQ::NT; ++i)
+        for (int i = 0; i < L::NT; ++i)
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                const int a = SQ::row(i, j), b = SQ::col(i);
-                double v = sG[b * P + a] / c;
-                if (b == bs) v += dc * ninf * sgnd(sW[a * P + b]);
-                if (a == as) v += dc * n1 * sgnd(sW[a * P + b]);
-                dW[i][j] += v;
+                const int a = 16 * L::tr(i) + row0 + j, b = col;
+                const double wab = (double)fW[a * PF + b];
+                double v = (double)fG[b * PF + a] / c;
+                if (b == bs) v += dc * ninf * sgnd(wab);
+                if (a == as) v += dc * n1 * sgnd(wab);
+                dW[i][j] += (float)v;
             }
         __syncthreads();
     } else {
         __syncthreads();
     }
-    // dDW = -k dW / lambda (k = W - eps on the diagonal), fp32, into the T region; the landmark
-    // rows (zero past m) into the X and G regions.  Entries past m are zero, so the sums below
-    // run over all MP rows.
-    float* sTf = reinterpret_cast<float*>(sT);
-    float* sqf = reinterpret_cast<float*>(sX);
-    float* skf = sqf + MP * D;
+    // dDW = -k dW / lambda (k = W - eps on the diagonal), fp32, [MP][MP] (zero past m: W and the
+    // gradient vanish there); launch_kll_backward maps it to the landmarks over the whole chip
+    float* Dh = dDW + (size_t)h * MP * MP;
 #pragma unroll
-    for (int i = 0; i < SQ::NT; ++i)
+    for (int i = 0; i < L::NT; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const int a = SQ::row(i, j), b = SQ::col(i);
-            const double kab = sW[a * P + b] - (a == b && a < m ? eps : 0.0);
-            sTf[a * MP + b] = (float)(-kab * dW[i][j] / lambda);
+            const int a = 16 * L::tr(i) + row0 + j, b = col;
+            const double kab = (double)fW[a * PF + b] - (a == b && a < m ? eps : 0.0);
+            Dh[a * MP + b] = (float)(-kab * (double)dW[i][j] / lambda);
         }
-    ns_stage_rows<MP, D>(sqf, q, m * D);
-    ns_stage_rows<MP, D>(skf, k, m * D);
-    __syncthreads();
-    // dqt_a += sum_b dDW_ab sign(qt_a - kt_b);  dkt_b -= sum_a dDW_ab sign(qt_a - kt_b)
-    for (int e = tid; e < m * D; e += 256) {
-        const int a = e / D, cc = e % D;
-        const float qa = sqf[e];
-        float s = 0.f;
-#pragma unroll 8
-        for (int b = 0; b < MP; ++b) {
-            const float kb = skf[b * D + cc], t = sTf[a * MP + b];
-            s += (qa > kb) ? t : ((qa < kb) ? -t : 0.f);
-        }
-        dqtW[(size_t)h * m * D + e] = s;
-    }
-    // dk~_b's K_LL term; dkpool_kernel adds the query-side partial sums and divides by the
-    // landmark's token count (here, at this kernel's register use, their loads would go one at a
-    // time)
-    for (int e = tid; e < m * D; e += 256) {
-        const int b = e / D, cc = e % D;
-        const float kb = skf[e];
-        float s = 0.f;
-#pragma unroll 8
-        for (int a = 0; a < MP; ++a) {
-            const float qa = sqf[a * D + cc], t = sTf[a * MP + b];
-            s += (qa > kb) ? t : ((qa < kb) ? -t : 0.f);
-        }
-        dkpool[(size_t)h * m * D + e] = -s;
-    }
-}
-
-// dk~_b = (K_LL term + the query-side partial sums in chunk order, fp64) / |S_b|: the pooling
-// gradient the key-major pass adds to its dK rows.  grid (ceil(m d / 256), BH); the partials of
-// 16 chunks are loaded at a time.
-__global__ __launch_bounds__(256) void dkpool_kernel(float* __restrict__ dkpool, const float* __restrict__ dkt_part,
-                                                     LmPool pl, int n, int m, int D, int nlc) {
-    const int h = blockIdx.y, e = blockIdx.x * 256 + threadIdx.x;
-    if (e >= m * D) return;
-    const size_t md = (size_t)m * D;
-    double ak = dkpool[(size_t)h * md + e];
-    const float* pp = dkt_part + (size_t)h * nlc * md + e;
-    int ch = 0;
-    for (; ch + 16 <= nlc; ch += 16) {
-        float v[16];
-#pragma unroll
-        for (int i = 0; i < 16; ++i) v[i] = pp[(size_t)(ch + i) * md];
-#pragma unroll
-        for (int i = 0; i < 16; ++i) ak += v[i];
-    }
-    for (; ch < nlc; ++ch) ak += pp[(size_t)ch * md];
-    dkpool[(size_t)h * md + e] = (float)ak * (1.f / (float)lm_tokens(pl, e / D, n, m).count);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -1176,12 +1174,12 @@ hipError_t launch_bwd_query_lm(const float* Q, const float* dO, const float* kt,
 hipError_t launch_bwd_ns(const float* qt, const float* kt, const double* Xs, const double* cinfo, const float* U,
                          const float* dM_part, const float* dvbar_part, float* dU, float* dvbar, float* dqtW,
                          float* dkpool, const float* dkt_part, LmPool pl, const float* p0_part, const float* whiten,
-                         int mspace, int BH, int H, int n, int d, int m, int T, double lambda, double eps, int nlc,
-                         int nqb, int MP, hipStream_t st) {
+                         int mspace, float* dDW, int BH, int H, int n, int d, int m, int T, double lambda, double eps,
+                         int nlc, int nqb, int MP, hipStream_t st) {
 #define LAPATTN_BNS(MPv, Dv)                                                                                      \
     hipLaunchKernelGGL((bwd_ns_kernel<MPv, Dv>), dim3(BH), dim3(256), 0, st, qt, kt, Xs, cinfo, U, dM_part,       \
-                       dvbar_part, dU, dvbar, dqtW, dkpool, dkt_part, pl, p0_part, whiten, mspace, H, n, m, T, lambda, \
-                       eps, nlc, nqb)
+                       dvbar_part, dU, dvbar, dqtW, dkpool, dkt_part, pl, p0_part, whiten, mspace, dDW, H, n, m, T,  \
+                       lambda, eps, nlc, nqb)
     if (MP == 32 && d == 32) LAPATTN_BNS(32, 32);
     else if (MP == 32) LAPATTN_BNS(32, 64);
     else if (d == 32) LAPATTN_BNS(64, 32);
@@ -1189,9 +1187,7 @@ hipError_t launch_bwd_ns(const float* qt, const float* kt, const double* Xs, con
 #undef LAPATTN_BNS
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(dkpool_kernel, dim3((m * d + 255) / 256, BH), dim3(256), 0, st, dkpool, dkt_part, pl, n, m, d,
-                       nlc);
-    return hipGetLastError();
+    return launch_kll_backward(qt, kt, dDW, dqtW, dkpool, dkt_part, pl, BH, n, d, m, MP, nlc, st);
 }
 
 hipError_t launch_bwd_key(const float* K, const float* V, float* dK, float* dV, const float* qt, const float* dU,

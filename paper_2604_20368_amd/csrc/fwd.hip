@@ -263,16 +263,21 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void key_summary_kernel(const
 }
 
 // ------------------------------------------------------------------------------------------
-// Newton-Schulz solve, one block of 256 threads per head, fp64 in LDS, matrices padded to
-// MP x MP with zeros (the padding stays zero under every update):
+// Newton-Schulz solve, one block of 256 threads per head, matrices padded to MP x MP with zeros
+// (the padding stays zero under every update):
 //   W = K_LL + eps I,  c = ||W||_1 ||W||_inf,  X0 = W^T / c (X := 0 if c = 0),
 //   X_{t+1} = X_t (2I - W X_t);  then U = sum of the key-chunk partials, M = X_T U, and
 //   Mc = M[:, :d] - M[:, d] vbar^T (fp64, then rounded), the value part the inline form reads:
 //   sum_l a_il Mc_l = Y_i[:d] - s_i vbar without the difference of the two rounded terms.
-// With store_all, Xs[h] holds X_0 .. X_T and then W (T + 2 matrices, pitch MP) for the backward.
-// Products on the fp64 matrix cores (ns_mfma.hpp); U's value columns and the ones column are
-// kept apart so that the value part of M is one MFMA product and the ones column a matrix-vector
-// product.
+// Precision: K_LL in fp32 as the key side forms K_LK (exp2 of the code distance times
+// -log2(e)/lambda, the distance summed in four fp32 chains); the norms in fp64 (sums of the fp32
+// entries, exact up to the spread of their exponents, so the first maximising column and row
+// do not depend on the order); the iteration on the fp32 matrix cores; U, M and Mc in fp64.
+// With store_all, Xs[h] holds X_0 .. X_T and then W (T + 2 matrices, pitch MP, fp64 copies of the
+// fp32 iterates) for the backward.
+// Products on the fp32 matrix cores (ns32_mm, ns_mfma.hpp).  X is kept both ways (row-major as A
+// of X T, transposed as B of W X) in two alternating buffers, and 2I - W X is written transposed
+// (as B of X T): two block barriers per step.
 template <int MP, int D>
 __global__ __launch_bounds__(256) void ns_solve_kernel(const float* __restrict__ qt, const float* __restrict__ kt,
                                                        const float* __restrict__ Upart,
@@ -282,46 +287,131 @@ __global__ __launch_bounds__(256) void ns_solve_kernel(const float* __restrict__
                                                        float* __restrict__ Mc, float* __restrict__ vbar, int n,
                                                        int m, int T, double lambda, double eps, int nkc,
                                                        int store_all) {
-    using SQ = ns_tiles<MP, MP>;
+    using L = ns32_tiles<MP>;
     using SU = ns_tiles<MP, D>;
     constexpr int D1 = D + 1;
-    constexpr int P = ns_pitch(MP);
+    constexpr int P = L::P;
+    constexpr int MSZ = MP * P;                  // floats per LDS matrix
+    constexpr int P64 = ns_pitch(MP);
     constexpr int PU = ns_pitch(D);
-    // X, W, T (MP x MP each, pitch P); after the iteration U's value columns (MP x D, pitch PU)
-    // reuse the space from W on.
-    constexpr int LDSN = (3 * MP * P > MP * P + MP * PU) ? 3 * MP * P : MP * P + MP * PU;
-    __shared__ double lds[LDSN];
+    // fp32 phase: W, X (two buffers), X^T (two buffers), (2I - W X)^T; the query landmark rows
+    // are staged after W while W is formed.  fp64 phase (after the iteration): X_T
+    // and U's value columns from the start of the same space.
+    constexpr int F32 = 6 * MSZ * 4;
+    constexpr int F64 = (MP * P64 + MP * PU) * 8;
+    __shared__ __attribute__((aligned(16))) char lds[F32 > F64 ? F32 : F64];
     __shared__ double sred[4];
+    __shared__ double spart[256];
     __shared__ double su1[MP];
     __shared__ double svb[256];
     __shared__ double sM1[MP];
     __shared__ double svbar[D];
     __shared__ double sc;
-    double* sX = lds;
-    double* sW = lds + MP * P;
-    double* sT = lds + 2 * MP * P;
-    const int h = blockIdx.x, tid = threadIdx.x;
+    float* const sW = reinterpret_cast<float*>(lds);
+    float* const sX0 = sW + MSZ;    // X buffers i = 0, 1 at sX0 + i MSZ
+    float* const sXT0 = sW + 3 * MSZ;   // X^T buffers at sXT0 + i MSZ
+    float* const sTT = sW + 5 * MSZ;
+    const int h = blockIdx.x, tid = threadIdx.x, l = tid & 63, li = l & 15, g = l >> 4;
     const float* q = qt + (size_t)h * m * D;
     const float* k = kt + (size_t)h * m * D;
-
     const size_t mm = (size_t)MP * MP;
     double* Xh = Xs + (size_t)h * (store_all ? (T + 2) : 1) * mm;
-    ns_kll<MP, D, P>(q, k, sW, reinterpret_cast<float*>(sT), m, lambda, eps);
+
+    // The first CB key chunks of U's partial sums and the segment value sums behind vbar are
+    // loaded here and added after the iteration: their latency hides behind it.
+    constexpr int NE = (MP * D1 + 255) / 256;
+    // (MP = 64 runs one block per CU, so registers are plentiful; MP = 32 keeps them few)
+    constexpr int CB = MP == 64 ? (NE > 9 ? 4 : 8) : 2;
+    const int ulim = m * D1 - 1;
+    float ub[CB][NE];
+#pragma unroll
+    for (int cc = 0; cc < CB; ++cc) {
+        const float* up = Upart + ((size_t)h * nkc + min(cc, nkc - 1)) * m * D1;
+#pragma unroll
+        for (int r = 0; r < NE; ++r) ub[cc][r] = up[min(tid + 256 * r, ulim)];
+    }
+    constexpr int G = 256 / D;   // vbar: 256 / D partial sums per column
+    double vsg[MP / G];
+    {
+        const int gq = tid / D, cc = tid % D;
+#pragma unroll
+        for (int i = 0; i < MP / G; ++i) vsg[i] = vseg[((size_t)h * m + min(gq + G * i, m - 1)) * D + cc];
+    }
+
+    // ---- W = K_LL + eps I: thread (a-group, b = tid % MP) keeps the key landmark row b in
+    // registers; both landmark tables are staged in LDS first (coalesced loads; the key rows
+    // with a pitch of D + 4 floats, so that each lane's 16-byte reads of its own row are free of
+    // bank conflicts), the query rows a are read by one or two rows per wave.
+    {
+        constexpr int KP = D + 4;
+        float* sQ = sX0;            // MP x D floats (in the five matrices after W), zero rows past m
+        float* sK = sX0 + MP * D;   // MP x KP
+        static_assert(MP * (2 * D + 4) <= 5 * MSZ, "the landmark rows fit");
+        ns_stage_rows<MP, D>(sQ, q, m * D);
+        {
+            constexpr int NK = (MP * D / 4 + 255) / 256;
+            const int cnt4 = m * D / 4;
+            float4 kv[NK];
+#pragma unroll
+            for (int r = 0; r < NK; ++r)
+                kv[r] = reinterpret_cast<const float4*>(k)[min((int)tid + 256 * r, cnt4 - 1)];
+#pragma unroll
+            for (int r = 0; r < NK; ++r) {
+                const int e = tid + 256 * r;
+                if (e < MP * D / 4)
+                    *reinterpret_cast<float4*>(sK + (e / (D / 4)) * KP + 4 * (e % (D / 4))) =
+                        e < cnt4 ? kv[r] : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+        }
+        const float ks = (float)(-1.4426950408889634 / lambda);
+        __syncthreads();
+        const int b = tid % MP;
+        float kb[D];
+#pragma unroll
+        for (int c4 = 0; c4 < D / 4; ++c4) {
+            const float4 v = *reinterpret_cast<const float4*>(sK + b * KP + 4 * c4);
+            kb[4 * c4] = v.x; kb[4 * c4 + 1] = v.y; kb[4 * c4 + 2] = v.z; kb[4 * c4 + 3] = v.w;
+        }
+        for (int a = tid / MP; a < MP; a += 256 / MP) {
+            const float4* qa = reinterpret_cast<const float4*>(sQ + a * D);
+            float d4[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int c4 = 0; c4 < D / 4; ++c4) {
+                const float4 v = qa[c4];
+                d4[0] += fabsf(v.x - kb[4 * c4]);
+                d4[1] += fabsf(v.y - kb[4 * c4 + 1]);
+                d4[2] += fabsf(v.z - kb[4 * c4 + 2]);
+                d4[3] += fabsf(v.w - kb[4 * c4 + 3]);
+            }
+            float wv = 0.f;
+            if (a < m && b < m) {
+                wv = __builtin_amdgcn_exp2f(((d4[0] + d4[1]) + (d4[2] + d4[3])) * ks);
+                if (a == b) wv = (float)((double)wv + eps);
+            }
+            sW[a * P + b] = wv;
+        }
+    }
     __syncthreads();
-    if (store_all)
-        for (int e = tid; e < MP * MP; e += 256) Xh[(size_t)(T + 1) * mm + e] = sW[(e / MP) * P + e % MP];
-    // column sums (threads 0..MP-1) and row sums (MP..2MP-1) of |W|, each in index order, then
-    // the first maximising column b* and row a* by a lane butterfly
+    // ---- norms: column sums (s < MP) and row sums (s >= MP) of |W| in fp64, each over 256 / (2 MP)
+    // parts of the index range, then the first maximising column b* and row a* by a lane butterfly
+    {
+        constexpr int NPART = 256 / (2 * MP), LEN = MP / NPART;
+        const int s = tid % (2 * MP), part = tid / (2 * MP), idx = s % MP;
+        double acc[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+        for (int i = 0; i < LEN; ++i) {
+            const int ii = part * LEN + i;
+            acc[i & 3] += fabs((double)(s < MP ? sW[ii * P + idx] : sW[idx * P + ii]));
+        }
+        spart[tid] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+    }
+    __syncthreads();
     if (tid < 2 * MP) {
+        constexpr int NPART = 256 / (2 * MP);
         const int idx = tid % MP;
         double s = 0.0;
-        if (tid < MP) {
-#pragma unroll 16
-            for (int a = 0; a < MP; ++a) s += fabs(sW[a * P + idx]);
-        } else {
-#pragma unroll 16
-            for (int b = 0; b < MP; ++b) s += fabs(sW[idx * P + b]);
-        }
+#pragma unroll
+        for (int p = 0; p < NPART; ++p) s += spart[p * 2 * MP + tid];
         double v = isnan(s) ? -1.0 : s;
         int arg = idx;
         ns_group_argmax<MP>(v, arg);
@@ -342,89 +432,123 @@ __global__ __launch_bounds__(256) void ns_solve_kernel(const float* __restrict__
         cinfo[h * 4 + 3] = (double)(as * 256 + bs);
     }
     __syncthreads();
-    const double c = sc;
-    for (int e = tid; e < MP * MP; e += 256) {
-        const int a = e / MP, b = e % MP;
-        const double x = (c > 0.0) ? sW[b * P + a] / c : 0.0;
-        sX[a * P + b] = x;
-        if (store_all) Xh[e] = x;
-    }
-    __syncthreads();
-    for (int t = 0; t < T; ++t) {
-        f64x4_t r[SQ::NT];
-        ns_mm<MP, MP, MP, false, false, P, P>(sW, sX, r);      // W X
-#pragma unroll
-        for (int i = 0; i < SQ::NT; ++i)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int a = SQ::row(i, j), b = SQ::col(i);
-                sT[a * P + b] = (a == b ? 2.0 : 0.0) - r[i][j];
-            }
-        __syncthreads();
-        ns_mm<MP, MP, MP, false, false, P, P>(sX, sT, r);      // X (2I - W X)
-        __syncthreads();
-#pragma unroll
-        for (int i = 0; i < SQ::NT; ++i)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int a = SQ::row(i, j), b = SQ::col(i);
-                sX[a * P + b] = r[i][j];
-                if (store_all) Xh[(size_t)(t + 1) * mm + a * MP + b] = r[i][j];
-            }
-        __syncthreads();
-    }
-    if (!store_all)
-        for (int e = tid; e < MP * MP; e += 256) Xh[e] = sX[(e / MP) * P + e % MP];
-
-    // U = sum over key chunks (in chunk order) in fp64: value columns from the W region on, the
-    // ones column in su1.  Each thread's entries are loaded together, chunk by chunk.
-    double* sU = sW;
+    // ---- X0 = W^T / c: row-major into X buffer 0, and X0^T = W / c into its transposed buffer
     {
-        constexpr int NE = (MP * D1 + 255) / 256;
-        double u[NE];
-#pragma unroll
-        for (int r = 0; r < NE; ++r) u[r] = 0.0;
-        const int lim = m * D1 - 1;
-#pragma unroll 4
-        for (int ch = 0; ch < nkc; ++ch) {
-            const float* up = Upart + ((size_t)h * nkc + ch) * m * D1;
-#pragma unroll
-            for (int r = 0; r < NE; ++r) {
-                const int e = tid + 256 * r;
-                const float v = up[min(e, lim)];
-                u[r] += (e <= lim) ? (double)v : 0.0;
+        const double c = sc;
+        const double ic = c > 0.0 ? 1.0 / c : 0.0;
+        for (int e = tid; e < MP * MP; e += 256) {
+            const int a = e / MP, b = e % MP;
+            const float wab = sW[a * P + b];
+            const float x = (float)((double)wab * ic);   // X0[b][a]
+            sX0[b * P + a] = x;
+            sXT0[a * P + b] = x;
+            if (store_all) {
+                Xh[(size_t)b * MP + a] = (double)x;
+                Xh[(size_t)(T + 1) * mm + e] = (double)wab;
             }
         }
+    }
+    __syncthreads();
+    // ---- T steps of X <- X (2I - W X)
+    for (int t = 0; t < T; ++t) {
+        const int cur = t & 1;
+        f32x4_t r[L::NT];
+        ns32_mm<MP>(sW, sXT0 + cur * MSZ, r);   // W X
 #pragma unroll
-        for (int r = 0; r < NE; ++r) {
-            const int e = tid + 256 * r;
-            if (e < MP * D1) {
-                const int a = e / D1, cc = e % D1;
-                if (cc < D) sU[a * PU + cc] = u[r];
-                else su1[a] = u[r];
-                if (a < m) U[(size_t)h * m * D1 + e] = (float)u[r];
-            }
+        for (int i = 0; i < L::NT; ++i) {
+            const int row0 = 16 * L::tr(i) + 4 * g, col = 16 * L::tc() + li;
+            float4 tv;
+            tv.x = (row0 + 0 == col ? 2.f : 0.f) - r[i][0];
+            tv.y = (row0 + 1 == col ? 2.f : 0.f) - r[i][1];
+            tv.z = (row0 + 2 == col ? 2.f : 0.f) - r[i][2];
+            tv.w = (row0 + 3 == col ? 2.f : 0.f) - r[i][3];
+            *reinterpret_cast<float4*>(sTT + col * P + row0) = tv;   // (2I - W X)^T
+        }
+        __syncthreads();
+        ns32_mm<MP>(sX0 + cur * MSZ, sTT, r);   // X (2I - W X)
+        float* nX = sX0 + (cur ^ 1) * MSZ;
+        float* nXT = sXT0 + (cur ^ 1) * MSZ;
+#pragma unroll
+        for (int i = 0; i < L::NT; ++i) {
+            const int row0 = 16 * L::tr(i) + 4 * g, col = 16 * L::tc() + li;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) nX[(row0 + j) * P + col] = r[i][j];
+            *reinterpret_cast<float4*>(nXT + col * P + row0) = make_float4(r[i][0], r[i][1], r[i][2], r[i][3]);
+            if (store_all)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) Xh[(size_t)(t + 1) * mm + (row0 + j) * MP + col] = (double)r[i][j];
+        }
+        __syncthreads();
+    }
+    const float* sXf = sX0 + (T & 1) * MSZ;   // X_T
+    // ---- U = sum over key chunks (in chunk order) in fp64: the first CB chunks from the early
+    // loads, then CB chunks' loads in flight at a time
+    double u[NE];
+#pragma unroll
+    for (int r = 0; r < NE; ++r) u[r] = 0.0;
+#pragma unroll
+    for (int cc = 0; cc < CB; ++cc)
+#pragma unroll
+        for (int r = 0; r < NE; ++r)
+            if (cc < nkc && tid + 256 * r <= ulim) u[r] += (double)ub[cc][r];
+    for (int c0 = CB; c0 < nkc; c0 += CB) {
+#pragma unroll
+        for (int cc = 0; cc < CB; ++cc) {
+            const float* up = Upart + ((size_t)h * nkc + min(c0 + cc, nkc - 1)) * m * D1;
+#pragma unroll
+            for (int r = 0; r < NE; ++r) ub[cc][r] = up[min(tid + 256 * r, ulim)];
+        }
+#pragma unroll
+        for (int cc = 0; cc < CB; ++cc)
+#pragma unroll
+            for (int r = 0; r < NE; ++r)
+                if (c0 + cc < nkc && tid + 256 * r <= ulim) u[r] += (double)ub[cc][r];
+    }
+    // X_T to fp64 (registers first: the fp64 copy overwrites the fp32 buffers)
+    constexpr int NX = MP * MP / 256;
+    double xv[NX];
+#pragma unroll
+    for (int r = 0; r < NX; ++r) {
+        const int e = tid + 256 * r;
+        xv[r] = (double)sXf[(e / MP) * P + e % MP];
+        if (!store_all) Xh[e] = xv[r];
+    }
+    __syncthreads();   // every read of the fp32 buffers is done
+    double* sX = reinterpret_cast<double*>(lds);
+    double* sU = sX + MP * P64;
+#pragma unroll
+    for (int r = 0; r < NX; ++r) {
+        const int e = tid + 256 * r;
+        sX[(e / MP) * P64 + e % MP] = xv[r];
+    }
+#pragma unroll
+    for (int r = 0; r < NE; ++r) {
+        const int e = tid + 256 * r;
+        if (e < MP * D1) {
+            const int a = e / D1, cc = e % D1;
+            if (cc < D) sU[a * PU + cc] = u[r];
+            else su1[a] = u[r];
+            if (a < m) U[(size_t)h * m * D1 + e] = (float)u[r];
         }
     }
     // vbar = (sum of the segment value sums) / n: 256 / D partial sums per column, then in order
     {
-        constexpr int G = 256 / D;
-        const int g = tid / D, cc = tid % D;
+        const int gq = tid / D;
         double s = 0.0;
-#pragma unroll 4
-        for (int l = g; l < m; l += G) s += vseg[((size_t)h * m + l) * D + cc];
+#pragma unroll
+        for (int i = 0; i < MP / G; ++i)
+            if (gq + G * i < m) s += vsg[i];
         svb[tid] = s;
     }
-    __syncthreads();   // sU, su1, svb
+    __syncthreads();   // sX, sU, su1, svb
     if (tid < m) {
         double s = 0.0;
 #pragma unroll 16
-        for (int b = 0; b < MP; ++b) s += sX[tid * P + b] * su1[b];
+        for (int b = 0; b < MP; ++b) s += sX[tid * P64 + b] * su1[b];
         M[((size_t)h * m + tid) * D1 + D] = (float)s;
         sM1[tid] = s;
     }
     if (tid < D) {
-        constexpr int G = 256 / D;
         double t = 0.0;
 #pragma unroll
         for (int gg = 0; gg < G; ++gg) t += svb[gg * D + tid];
@@ -435,7 +559,7 @@ __global__ __launch_bounds__(256) void ns_solve_kernel(const float* __restrict__
     {
         // X_T U (value columns); Mc = M[:, :d] - M[:, d] vbar^T in fp64 for the inline form
         f64x4_t r[SU::NT];
-        ns_mm<MP, D, MP, false, false, P, PU>(sX, sU, r);
+        ns_mm<MP, D, MP, false, false, P64, PU>(sX, sU, r);
 #pragma unroll
         for (int i = 0; i < SU::NT; ++i)
 #pragma unroll

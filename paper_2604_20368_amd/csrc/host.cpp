@@ -154,10 +154,8 @@ Plan make_plan(int BH, int n, int d, int m, int T, bool bwd, bool bf16 = false, 
         p.dqtW = c.take(bh * m * d * f);
         p.dkpool = c.take(bh * m * d * f);
         p.dDk = c.take(rows);
-        if (big) {
-            p.nsbs = c.take(lapattn::nsb_backward_scratch(BH, d) * g);
-            p.dDW = c.take(bh * mpp * f);
-        }
+        if (big) p.nsbs = c.take(lapattn::nsb_backward_scratch(BH, d) * g);
+        p.dDW = c.take(bh * mpp * f);
         p.dqt_part = c.take(bh * p.nlc * m * d * f);
         if (bf16) {
             const size_t t = bh * n * d * f;
@@ -612,7 +610,8 @@ int lapattn_backward(const void* Q, const void* K, const void* V, const void* dO
                                           at<double>(ws, p.cinfo), at<float>(ws, p.U), at<float>(ws, p.dM_part),
                                           at<float>(ws, p.dvbar_part), at<float>(ws, p.dU), at<float>(ws, p.dvbar),
                                           at<float>(ws, p.dqtW), at<float>(ws, p.dkpool), at<float>(ws, p.dkt_part), pl,
-                                          at<float>(ws, p.p0_part), whiten, mspace ? 1 : 0, BH, H, n, d, m, ns_iters,
+                                          at<float>(ws, p.p0_part), whiten, mspace ? 1 : 0, at<float>(ws, p.dDW), BH,
+                                          H, n, d, m, ns_iters,
                                           (double)lambda,
                                           (double)eps, p.nlc, p.nqb, p.MP, st);
         });

@@ -99,13 +99,19 @@ hipError_t launch_bwd_query_lm(const float* Q, const float* dO, const float* kt,
 
 // Newton-Schulz backward: dU [BH][m][d+1], dvbar [BH][d], the K_LL gradient mapped to the
 // query landmarks, dqtW [BH][m][d], and the whole key-landmark gradient over each landmark's
-// token count, dkpool [BH][m][d] = (K_LL term + the query-side partials dkt_part) / |S_l|.
+// token count, dkpool [BH][m][d] = (K_LL term + the query-side partials dkt_part) / |S_l|;
+// dDW [BH][MP][MP] fp32 is scratch (the gradient of the kernel distances, between the solve's
+// backward and launch_kll_backward).
 hipError_t launch_bwd_ns(const float* qt, const float* kt, const double* Xs, const double* cinfo,
                          const float* U, const float* dM_part, const float* dvbar_part,
                          float* dU, float* dvbar, float* dqtW, float* dkpool, const float* dkt_part, LmPool pl,
-                         const float* p0_part, const float* whiten, int mspace,
+                         const float* p0_part, const float* whiten, int mspace, float* dDW,
                          int BH, int H, int n, int d, int m, int T, double lambda, double eps,
                          int nlc, int nqb, int MP, hipStream_t st);
+// K_LL backward from dDW [BH][MPW][MPW] (zero past m): dqtW and dkpool as above (nsbig.hip).
+hipError_t launch_kll_backward(const float* qt, const float* kt, const float* dDW, float* dqtW, float* dkpool,
+                               const float* dkt_part, LmPool pl, int BH, int n, int d, int m, int MPW, int nlc,
+                               hipStream_t st);
 // The same for 64 < m <= 128 (nsbig.hip), with nsb_backward_scratch(BH, d) doubles of scratch and
 // dDW [BH][128][128] fp32; Xs as launch_nsb_forward left it.
 hipError_t launch_nsb_backward(const float* qt, const float* kt, const double* Xs, const double* cinfo,

@@ -1,6 +1,7 @@
-// ns_mfma.hpp -- fp64 building blocks of the Newton-Schulz solve (Algorithm 2) and of its
-// backward, for one workgroup of 256 threads (four waves) per head: the kernel matrix K_LL and
-// block products on the fp64 matrix cores (v_mfma_f64_16x16x4_f64).
+// ns_mfma.hpp -- building blocks of the Newton-Schulz solve (Algorithm 2) and of its backward,
+// for one workgroup of 256 threads (four waves) per head: the kernel matrix K_LL, block products
+// on the fp64 matrix cores (v_mfma_f64_16x16x4_f64) and MP x MP products on the fp32 ones
+// (v_mfma_f32_16x16x4f32, ns32_mm at the end).
 //
 // Product layout.  A product C = op(A) op(B) of R x N (R, N multiples of 16, (R/16)(N/16) a
 // multiple of 4) is cut into 16 x 16 tiles numbered row-major; wave w owns tiles w, w + 4,
@@ -21,6 +22,7 @@
 namespace lapattn {
 
 typedef double f64x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 // Row pitch (doubles) of an LDS matrix with `cols` columns: cols rounded up to 4 mod 32.
 __host__ __device__ constexpr int ns_pitch(int cols) { return cols + ((36 - cols % 32) % 32); }
@@ -156,6 +158,71 @@ __device__ __forceinline__ void ns_group_argmax(double& v, int& idx) {
             idx = oi;
         }
     }
+}
+
+
+// fp32 products C = A B of MP x MP matrices (MP = 32 or 64) on v_mfma_f32_16x16x4f32 (ns32_mm),
+// for the Newton-Schulz iterations and their backward: 16 x 16 tiles, wave w owns column block w
+// (MP = 64: all four row blocks) or tile (w / 2, w % 2) (MP = 32).  The contraction is split over
+// the four lane groups (group g takes k = g MP/4 .. g MP/4 + MP/4 - 1, one per MFMA), so that a
+// lane's operands are contiguous runs of A's row and of B's column: B is passed transposed.
+// LDS matrices have a row pitch of MP + 4 floats (16-byte reads of 16 rows fall on distinct
+// banks).
+template <int MP>
+struct ns32_tiles {
+    static constexpr int KS = MP / 4;               // k values per lane group
+    static constexpr int NT = MP == 64 ? 4 : 1;     // tiles per wave
+    static constexpr int P = MP + 4;                // row pitch (floats) of the LDS matrices
+    static __device__ __forceinline__ int tc() {
+        const int w = (int)(threadIdx.x >> 6);
+        return MP == 64 ? w : (w & 1);
+    }
+    static __device__ __forceinline__ int tr(int t) {
+        const int w = (int)(threadIdx.x >> 6);
+        return MP == 64 ? t : (w >> 1);
+    }
+};
+
+// acc[t] = tile t of A B, A row-major and BT = B^T row-major (pitch P each).  Register r of tile t
+// at lane l holds row 16 tr(t) + 4 (l / 16) + r, column 16 tc + l % 16.
+template <int MP>
+__device__ __forceinline__ void ns32_mm(const float* __restrict__ A, const float* __restrict__ BT,
+                                        f32x4_t (&acc)[ns32_tiles<MP>::NT]) {
+    using L = ns32_tiles<MP>;
+    const int l = (int)(threadIdx.x & 63), li = l & 15, g = l >> 4;
+    float b[L::KS];
+    const float* bp = BT + (16 * L::tc() + li) * L::P + g * L::KS;
+#pragma unroll
+    for (int s4 = 0; s4 < L::KS / 4; ++s4) {
+        const float4 v = reinterpret_cast<const float4*>(bp)[s4];
+        b[4 * s4] = v.x; b[4 * s4 + 1] = v.y; b[4 * s4 + 2] = v.z; b[4 * s4 + 3] = v.w;
+    }
+    float a[L::NT][L::KS];
+#pragma unroll
+    for (int t = 0; t < L::NT; ++t) {
+        const float* ap = A + (16 * L::tr(t) + li) * L::P + g * L::KS;
+#pragma unroll
+        for (int s4 = 0; s4 < L::KS / 4; ++s4) {
+            const float4 v = reinterpret_cast<const float4*>(ap)[s4];
+            a[t][4 * s4] = v.x; a[t][4 * s4 + 1] = v.y; a[t][4 * s4 + 2] = v.z; a[t][4 * s4 + 3] = v.w;
+        }
+        acc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    }
+    // k outer, tiles inner: consecutive MFMAs are independent
+#pragma unroll
+    for (int s = 0; s < L::KS; ++s)
+#pragma unroll
+        for (int t = 0; t < L::NT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[t][s], b[s], acc[t], 0, 0, 0);
+}
+
+// Row and column of register j of tile t of an ns32_mm result at this lane.
+template <int MP>
+__device__ __forceinline__ int ns32_row(int t, int j) {
+    return 16 * ns32_tiles<MP>::tr(t) + 4 * (int)((threadIdx.x & 63) >> 4) + j;
+}
+template <int MP>
+__device__ __forceinline__ int ns32_col() {
+    return 16 * ns32_tiles<MP>::tc() + (int)(threadIdx.x & 15);
 }
 
 }  // namespace lapattn

@@ -15,7 +15,8 @@
 //   nsb_bwd_dm_kernel    dM = sum of the landmark-chunk partials, U in fp64
 //   (nsb_mm_kernel)      dX_T = dM U^T, dU = X_T^T dM, the reverse iteration
 //   nsb_bwd_x0_kernel    the gradient through X0 = W^T / c, dDW = -k dW / lambda, dU to fp32
-//   nsb_bwd_kll_kernel   the K_LL backward: dqt from the rows, the keys' pooling gradient
+//   kll_bwd_kernel       the K_LL backward: dqt from the rows, the keys' pooling gradient (also
+//                        for m <= 64, after bwd_ns_kernel)
 //
 // The iteration runs in product form: with E_0 = I - W X0, the updates X_{t+1} = X_t (2I - W X_t)
 // satisfy I - W X_t = E_0^(2^t), so X_{t+1} = X_t + X_t E_t with E_{t+1} = E_t E_t -- the same
@@ -433,24 +434,25 @@ __global__ __launch_bounds__(256) void nsb_bwd_x0_kernel(const double* __restric
 // K_LL backward: dqtW_a += sum_b dDW_ab sign(qt_a - kt_b) (blockIdx.z = 0, rows a) and
 // dk~_b = -sum_a dDW_ab sign(qt_a - kt_b) plus the query-side partials (chunk order, fp64), over
 // the landmark's token count (blockIdx.z = 1, columns b): the pooling gradient the key-major pass
-// adds to its dK rows.  grid (ceil(m / R), BH, 2), R = 256 / D landmarks per block, thread (landmark
-// x0 + tid / D, coordinate tid % D); the other side's landmark rows and the block's rows (columns)
-// of dDW are staged in LDS.  Sums in index order.
-template <int D>
-__global__ __launch_bounds__(256) void nsb_bwd_kll_kernel(const float* __restrict__ qt, const float* __restrict__ kt,
-                                                          const float* __restrict__ dDW, float* __restrict__ dqtW,
-                                                          float* __restrict__ dkpool,
-                                                          const float* __restrict__ dkt_part, LmPool pl, int n,
-                                                          int m, int nlc) {
+// adds to its dK rows.  dDW is MPW x MPW per head (MPW = 32, 64 or 128, zero past m).  grid
+// (ceil(m / R), BH, 2), R = 256 / D landmarks per block, thread (landmark x0 + tid / D,
+// coordinate tid % D); the other side's landmark rows and the block's rows (columns) of dDW are
+// staged in LDS.  Sums in index order.
+template <int D, int MPW>
+__global__ __launch_bounds__(256) void kll_bwd_kernel(const float* __restrict__ qt, const float* __restrict__ kt,
+                                                      const float* __restrict__ dDW, float* __restrict__ dqtW,
+                                                      float* __restrict__ dkpool,
+                                                      const float* __restrict__ dkt_part, LmPool pl, int n,
+                                                      int m, int nlc) {
     constexpr int R = 256 / D;
-    __shared__ float so[kBig * D];
-    __shared__ float st[R * kBig];
+    __shared__ float so[MPW * D];
+    __shared__ float st[R * MPW];
     const int h = blockIdx.y, z = blockIdx.z, tid = threadIdx.x;
     const int r = tid / D, cc = tid % D, x0 = blockIdx.x * R, x = x0 + r;
     const float* other = (z == 0 ? kt : qt) + (size_t)h * m * D;
-    const float* Th = dDW + (size_t)h * kBig * kBig;
+    const float* Th = dDW + (size_t)h * MPW * MPW;
     {
-        constexpr int NO = kBig * D / 256, NT = R * kBig / 256;
+        constexpr int NO = (MPW * D + 255) / 256, NT = (R * MPW + 255) / 256;
         float vo[NO], vt[NT];   // every load issued before the first LDS write
 #pragma unroll
         for (int i = 0; i < NO; ++i) {
@@ -459,17 +461,19 @@ __global__ __launch_bounds__(256) void nsb_bwd_kll_kernel(const float* __restric
         }
 #pragma unroll
         for (int i = 0; i < NT; ++i) {
-            const int e = tid + 256 * i, xr = x0 + e / kBig, jj = e % kBig;
-            vt[i] = xr < m ? (z == 0 ? Th[xr * kBig + jj] : Th[jj * kBig + xr]) : 0.f;
+            const int e = tid + 256 * i, xr = x0 + e / MPW, jj = e % MPW;
+            vt[i] = (xr < m && e < R * MPW) ? (z == 0 ? Th[xr * MPW + jj] : Th[jj * MPW + xr]) : 0.f;
         }
 #pragma unroll
-        for (int i = 0; i < NO; ++i) so[tid + 256 * i] = vo[i];
+        for (int i = 0; i < NO; ++i)
+            if (tid + 256 * i < MPW * D) so[tid + 256 * i] = vo[i];
 #pragma unroll
-        for (int i = 0; i < NT; ++i) st[tid + 256 * i] = vt[i];
+        for (int i = 0; i < NT; ++i)
+            if (tid + 256 * i < R * MPW) st[tid + 256 * i] = vt[i];
     }
     __syncthreads();
     if (x >= m) return;
-    const float* trow = st + r * kBig;
+    const float* trow = st + r * MPW;
     float s = 0.f;
     if (z == 0) {
         const float qa = qt[((size_t)h * m + x) * D + cc];
@@ -655,12 +659,26 @@ hipError_t launch_nsb_backward(const float* qt, const float* kt, const double* X
     hipLaunchKernelGGL(nsb_bwd_x0_kernel, dim3(BH), dim3(256), 0, st, Gb[T & 1], W, xs, dW, T > 0 ? 1 : 0, cinfo, dDW,
                        dUd, dU, m, D1, lambda, eps);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    if (d == 32)
-        hipLaunchKernelGGL(nsb_bwd_kll_kernel<32>, dim3((m + 7) / 8, BH, 2), dim3(256), 0, st, qt, kt, dDW, dqtW, dkpool,
-                           dkt_part, pl, n, m, nlc);
-    else
-        hipLaunchKernelGGL(nsb_bwd_kll_kernel<64>, dim3((m + 3) / 4, BH, 2), dim3(256), 0, st, qt, kt, dDW, dqtW, dkpool,
-                           dkt_part, pl, n, m, nlc);
+    return launch_kll_backward(qt, kt, dDW, dqtW, dkpool, dkt_part, pl, BH, n, d, m, kBig, nlc, st);
+}
+
+hipError_t launch_kll_backward(const float* qt, const float* kt, const float* dDW, float* dqtW, float* dkpool,
+                               const float* dkt_part, LmPool pl, int BH, int n, int d, int m, int MPW, int nlc,
+                               hipStream_t st) {
+    const int R = 256 / d;
+    const dim3 grid((m + R - 1) / R, BH, 2);
+#define LAPATTN_KB(Dv, Mv)                                                                                              hipLaunchKernelGGL((kll_bwd_kernel<Dv, Mv>), grid, dim3(256), 0, st, qt, kt, dDW, dqtW, dkpool, dkt_part, pl, n,                        m, nlc)
+    if (MPW == 32) {
+        if (d == 32) LAPATTN_KB(32, 32);
+        else LAPATTN_KB(64, 32);
+    } else if (MPW == 64) {
+        if (d == 32) LAPATTN_KB(32, 64);
+        else LAPATTN_KB(64, 64);
+    } else {
+        if (d == 32) LAPATTN_KB(32, 128);
+        else LAPATTN_KB(64, 128);
+    }
+#undef LAPATTN_KB
     return hipGetLastError();
 }
 

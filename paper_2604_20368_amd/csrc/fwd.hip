@@ -85,6 +85,55 @@ __global__ __launch_bounds__(256) void pool_kernel(const typename elem<DT>::type
     }
 }
 
+// Landmark means when every landmark has few tokens (at most kPoolSmall): grid
+// (ceil(m / (256 / d)), BH), 256 threads, thread (landmark x tid / d + blockIdx.x (256 / d),
+// column tid % d) sums its landmark's tokens in its column (fp64, in token order), four tokens'
+// loads in flight at a time.  The same outputs as pool_kernel with S = 1; at a handful of tokens
+// per landmark one block per landmark would be mostly launch overhead.
+constexpr int kPoolSmall = 16;
+
+template <int DT>
+__global__ __launch_bounds__(256) void pool_small_kernel(const typename elem<DT>::type* __restrict__ Q,
+                                                         const typename elem<DT>::type* __restrict__ K,
+                                                         const typename elem<DT>::type* __restrict__ V,
+                                                         float* __restrict__ qt, float* __restrict__ kt,
+                                                         double* __restrict__ vseg, int n, int d, int m, LmPool pl) {
+    const int lpb = 256 / d;
+    const int l = blockIdx.x * lpb + threadIdx.x / d, c = threadIdx.x % d, h = blockIdx.y;
+    if (l >= m) return;
+    const LmTokens tok = lm_tokens(pl, l, n, m);
+    const int cnt = tok.count;
+    const size_t base = (size_t)h * n * d + c;
+    double sq = 0.0, sk = 0.0, sv = 0.0;
+    int t = 0;
+    for (; t + 4 <= cnt; t += 4) {
+        float a[4], b[4], e[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const size_t idx = base + (size_t)tok(t + u) * d;
+            a[u] = elem<DT>::load(Q, idx);
+            b[u] = elem<DT>::load(K, idx);
+            e[u] = elem<DT>::load(V, idx);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            sq += a[u];
+            sk += b[u];
+            sv += e[u];
+        }
+    }
+    for (; t < cnt; ++t) {
+        const size_t idx = base + (size_t)tok(t) * d;
+        sq += elem<DT>::load(Q, idx);
+        sk += elem<DT>::load(K, idx);
+        sv += elem<DT>::load(V, idx);
+    }
+    const size_t o = ((size_t)h * m + l) * d + c;
+    qt[o] = (float)(sq / cnt);
+    kt[o] = (float)(sk / cnt);
+    vseg[o] = sv;
+}
+
 // The S parts of each landmark's sums, added in order.  grid (m, BH), d threads.
 __global__ void pool_combine_kernel(const double* __restrict__ part, float* __restrict__ qt, float* __restrict__ kt,
                                     double* __restrict__ vseg, int n, int d, int m, int S, LmPool pl) {
@@ -759,6 +808,17 @@ int pool_split(int BH, int n, int m) {
 
 hipError_t launch_pool(int dt, const void* Q, const void* K, const void* V, float* qt, float* kt, double* vseg,
                        double* part, int BH, int n, int d, int m, LmPool pl, hipStream_t st) {
+    const int most = pl.r > 0 ? pl.r * pl.r : (n + m - 1) / m;   // tokens of the largest landmark
+    if (most <= kPoolSmall) {
+        const dim3 grid((m + 256 / d - 1) / (256 / d), BH);
+        if (dt == DT_F32)
+            hipLaunchKernelGGL(pool_small_kernel<DT_F32>, grid, dim3(256), 0, st, (const float*)Q, (const float*)K,
+                               (const float*)V, qt, kt, vseg, n, d, m, pl);
+        else
+            hipLaunchKernelGGL(pool_small_kernel<DT_BF16>, grid, dim3(256), 0, st, (const uint16_t*)Q,
+                               (const uint16_t*)K, (const uint16_t*)V, qt, kt, vseg, n, d, m, pl);
+        return hipGetLastError();
+    }
     const int S = pool_split(BH, n, m);
     dim3 grid(m * S, BH);
     if (dt == DT_F32)

@@ -271,6 +271,29 @@ __device__ __forceinline__ float lap_row(const uint32_t (&kf)[D2], const uint32_
     return __builtin_amdgcn_exp2f(lap_arg<D2>(kf, t, nt, next_row, esc, ebias));
 }
 
+// As lap_arg, with the next row read from LDS (all lanes at one address) into registers: the
+// rows of one table alternate between the scalar cache and LDS, so that neither path alone has
+// to deliver a row per 32 v_sad_u16 of a wave.
+template <int D2>
+__device__ __forceinline__ float lap_arg_lds(const uint32_t (&kf)[D2], const uint32_t (&t)[D2], uint32_t (&nt)[D2],
+                                             const uint32_t* next_row, float esc, float ebias) {
+    uint32_t u0 = __builtin_amdgcn_sad_u16(kf[0], t[0], 0x4B000000u);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int c4 = 0; c4 < D2 / 4; ++c4) {
+        const uint4 r = reinterpret_cast<const uint4*>(next_row)[c4];
+        nt[4 * c4] = r.x; nt[4 * c4 + 1] = r.y; nt[4 * c4 + 2] = r.z; nt[4 * c4 + 3] = r.w;
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    uint32_t u1 = __builtin_amdgcn_sad_u16(kf[1], t[1], 0u);
+#pragma unroll
+    for (int c = 2; c < D2; c += 2) {
+        u0 = __builtin_amdgcn_sad_u16(kf[c], t[c], u0);
+        u1 = __builtin_amdgcn_sad_u16(kf[c + 1], t[c + 1], u1);
+    }
+    return fmaf(__uint_as_float(u0 + u1), esc, ebias);
+}
+
 // The exp2 arguments of two tokens (x, y) against one landmark row: four sad chains, the loads
 // of the next row into `nt` issued after the first sad (the wait point for `t`).  Each row
 // fetched through the scalar cache feeds twice the VALU work of lap_arg.
@@ -1577,6 +1600,9 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
     // branch's sums and then the finished output rows
     constexpr int SP = D + 4;
     __shared__ __attribute__((aligned(16))) float sSt[DWC ? 4 * 64 * SP : 4];
+    // without the branch: the odd landmark rows of the key-landmark table come from LDS
+    constexpr bool HYB = DWC == 0;
+    __shared__ __attribute__((aligned(16))) uint32_t sTab[HYB ? 64 * D2 : 4];
     const int lin = xcd_rank(blockIdx.x, nqb * BH, 0);
     const int h = lin / nqb, qblk = lin % nqb;
     const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
@@ -1593,6 +1619,10 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
             }
         }
         if (tid < 64) sMo[tid] = Mones[(size_t)h * 64 + tid];
+        if (HYB) {
+            const uint4* ts = reinterpret_cast<const uint4*>(kfix + (size_t)h * 64 * D2);
+            for (int e = tid; e < 64 * D2 / 4; e += 256) reinterpret_cast<uint4*>(sTab)[e] = ts[e];
+        }
     }
     const float R = frame[h * 8 + 0], inv2R = frame[h * 8 + 1], esc = frame[h * 8 + 2];
     const float xsc = frame[h * 8 + 4];
@@ -1741,8 +1771,14 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
 #pragma unroll
         for (int p = 0; p < 32; ++p) {
             if (2 * p < m) {
-                const float a0 = lap_row<D2>(qf, ta, tb, tab + (2 * p + 1) * D2, esc, qbias);
-                float a1 = lap_row<D2>(qf, tb, ta, tab + (p < 31 ? 2 * p + 2 : 63) * D2, esc, qbias);
+                float a0, a1;
+                if (HYB) {   // row 2p in scalar registers, row 2p + 1 from LDS
+                    a0 = __builtin_amdgcn_exp2f(lap_arg_lds<D2>(qf, ta, tb, sTab + (2 * p + 1) * D2, esc, qbias));
+                    a1 = lap_row<D2>(qf, tb, ta, tab + (p < 31 ? 2 * p + 2 : 63) * D2, esc, qbias);
+                } else {
+                    a0 = lap_row<D2>(qf, ta, tb, tab + (2 * p + 1) * D2, esc, qbias);
+                    a1 = lap_row<D2>(qf, tb, ta, tab + (p < 31 ? 2 * p + 2 : 63) * D2, esc, qbias);
+                }
                 if (2 * p + 1 >= m) a1 = 0.f;
                 if (NORM == NORM_ROWSUM || NORM == NORM_MSPACE) {
                     const float2 mo = *reinterpret_cast<const float2*>(&sMo[2 * p]);

@@ -30,13 +30,10 @@
 // maps it to the exp2 argument -(D / S + E) log2(e) / lambda.
 #include "common.hpp"
 #include "kernels.hpp"
+#include "ns_split.hpp"
 
 namespace lapattn {
 
-typedef _Float16 h8_t __attribute__((ext_vector_type(8)));
-typedef float f32x16_t __attribute__((ext_vector_type(16)));
-
-constexpr int kLP = 72;            // LDS row pitch (halves) of the 64 x 64 fp16 tiles
 constexpr float kTwo23 = 8388608.f;
 // Word 3 of a raw (unswizzled, stride 0) buffer resource on CDNA: 32-bit data format, so that
 // loads are range-checked against the byte count in word 2 and return 0 past it.
@@ -46,7 +43,6 @@ __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w 
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
 typedef unsigned short u16x2_t __attribute__((ext_vector_type(2)));
-typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
 
 // Two coordinates to the fixed-point frame: u = rint(clamp((x + R) / (2R)) * 65535), packed.
 __device__ __forceinline__ uint32_t fix2(float x0, float x1, float inv2R) {
@@ -64,19 +60,6 @@ __device__ __forceinline__ float wave_max(float v) {
     return v;
 }
 
-// Maximum of a non-negative value over the wave with DPP lane moves (no LDS round trips);
-// the result is wave-uniform.
-__device__ __forceinline__ float wave_max_dpp(float v) {
-    int x = __float_as_int(v);
-    x = max(x, __builtin_amdgcn_update_dpp(0, x, 0xB1, 0xF, 0xF, false));   // quad_perm [1,0,3,2]
-    x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x4E, 0xF, 0xF, false));   // quad_perm [2,3,0,1]
-    x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x141, 0xF, 0xF, false));  // row_half_mirror
-    x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x140, 0xF, 0xF, false));  // row_mirror
-    x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x142, 0xA, 0xF, false));  // row_bcast:15
-    x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x143, 0xC, 0xF, false));  // row_bcast:31
-    return __int_as_float(__builtin_amdgcn_readlane(x, 63));
-}
-
 // Maximum over the wave and the lowest lane index holding it.
 __device__ __forceinline__ void wave_argmax(float& v, int& idx) {
 #pragma unroll
@@ -90,13 +73,7 @@ __device__ __forceinline__ void wave_argmax(float& v, int& idx) {
     }
 }
 
-typedef float f32x2_t __attribute__((ext_vector_type(2)));
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
-
-// Two floats to a packed fp16 pair, round to nearest even (v_cvt_pk_f16_f32).
-__device__ __forceinline__ uint32_t pk_f16(float a, float b) {
-    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, f16x2_t));
-}
 
 // Workgroups are dispatched to the 8 XCDs round-robin (block id mod 8); each XCD has its own
 // L2 and its CUs share scalar caches.  xcd_rank maps the i-th of n consecutive blocks (first
@@ -221,19 +198,6 @@ __global__ __launch_bounds__(256) void pool2_kernel(const uint16_t* __restrict__
     }
 }
 
-__device__ __forceinline__ int c_row(int r, int l) { return 8 * (r >> 2) + 4 * (l >> 5) + (r & 3); }
-
-__device__ __forceinline__ void split_f16(float v, _Float16& hi, _Float16& lo) {
-    hi = (_Float16)v;
-    lo = (_Float16)(v - (float)hi);
-}
-
-// Power-of-two exponent that brings a maximum magnitude into [2^14, 2^15) (0 when mx is 0).
-__device__ __forceinline__ int pow2_exp(float mx) { return (mx > 0.f && isfinite(mx)) ? ilogbf(mx) - 14 : 0; }
-
-typedef short s4_t __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) s4_t lds_s4_t;
-
 // Scalar loads of one landmark row (D/2 words) into `t`.  The row is read through the
 // constant address space: the tables are written by earlier launches and never within the
 // reading kernel, and this keeps the loads scalar (s_load) wherever the compiler cannot prove
@@ -352,65 +316,6 @@ __device__ __forceinline__ void lap_arg2(const uint32_t (&xf)[D2], const uint32_
 //   Writes X_T (fp32, row-major [64][64]) and cinfo = {c, n1, ninf, a* 256 + b*}.
 constexpr int kSolveLds = 8 * 64 * kLP * 2 + 64 * 4;
 constexpr int kSolveThreads = 512;
-
-// The A operand of MFMA 32x32x16 (8 halves: row 32 rb + l%32, k = k0 + 8(l/32)..+8) of a
-// matrix held transposed in LDS (Mt[k][row], pitch kLP), via two ds_read_b64_tr_b16.  Within a
-// 16-lane group that instruction gives lane i element i%4 of the 4-element reads of lanes
-// 4q + i/4 (q = 0..3): when lane j of the group points at Mt[k1 + j/4][r0 + 4(j%4)], lane i
-// receives Mt[k1 + q][r0 + i], q = 0..3 -- row r0 + i of M over 4 consecutive k.
-__device__ __forceinline__ h8_t a_from_transposed(const _Float16* Mt, int rb, int k0) {
-    const int l = threadIdx.x & 63, g = l >> 4, i = l & 15;
-    const _Float16* p = Mt + (k0 + 8 * (g >> 1) + (i >> 2)) * kLP + 32 * rb + 16 * (g & 1) + 4 * (i & 3);
-    const s4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4_t*)p);
-    const s4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4_t*)(p + 4 * kLP));
-    typedef short s8_t __attribute__((ext_vector_type(8)));
-    return __builtin_bit_cast(h8_t, (s8_t)__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-}
-
-// One wave's 32 x 32 block of a 64 x 64 product, both factors fp16 pairs, B read from its
-// transposed copy (BT[col][k]); the A operands of the four k steps are given (hi, lo).
-// Result register r holds row 32 rb + c_row(r, l), column 32 cb + l%32.
-__device__ __forceinline__ f32x16_t mm32_split(const h8_t (&ah)[4], const h8_t (&al)[4],
-                                               const _Float16* __restrict__ BTh, const _Float16* __restrict__ BTl,
-                                               int cb) {
-    const int l = threadIdx.x & 63;
-    const int bo = (32 * cb + (l & 31)) * kLP + 8 * (l >> 5);
-    f32x16_t hh = {}, hl = {}, lh = {};
-#pragma unroll
-    for (int s4 = 0; s4 < 4; ++s4) {
-        const h8_t bh = *reinterpret_cast<const h8_t*>(BTh + bo + 16 * s4);
-        const h8_t bl = *reinterpret_cast<const h8_t*>(BTl + bo + 16 * s4);
-        hh = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah[s4], bh, hh, 0, 0, 0);
-        hl = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah[s4], bl, hl, 0, 0, 0);
-        lh = __builtin_amdgcn_mfma_f32_32x32x16_f16(al[s4], bh, lh, 0, 0, 0);
-    }
-    return hh + (hl + lh);
-}
-
-// Two floats as packed fp16 pairs: hi = rn(x), lo = rn(x - hi) (each one v_cvt_pk_f16_f32).
-__device__ __forceinline__ void split_pk(float x0, float x1, uint32_t& hi, uint32_t& lo) {
-    const f16x2_t h = __builtin_convertvector((f32x2_t){x0, x1}, f16x2_t);
-    const f32x2_t back = __builtin_convertvector(h, f32x2_t);
-    hi = __builtin_bit_cast(uint32_t, h);
-    lo = pk_f16(x0 - back[0], x1 - back[1]);
-}
-
-// Store a wave's 32 x 32 block (times `scale`) transposed as an fp16 pair: four consecutive
-// rows of one column per 8-byte write.
-__device__ __forceinline__ void store32_t(const f32x16_t& v, float scale, int rb, int cb, _Float16* MTh,
-                                          _Float16* MTl) {
-    const int l = threadIdx.x & 63;
-    const int col = 32 * cb + (l & 31);
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-        uint32_t h0, l0, h1, l1;
-        split_pk(v[4 * g] * scale, v[4 * g + 1] * scale, h0, l0);
-        split_pk(v[4 * g + 2] * scale, v[4 * g + 3] * scale, h1, l1);
-        const int o = col * kLP + 32 * rb + 8 * g + 4 * (l >> 5);
-        *reinterpret_cast<uint2*>(MTh + o) = make_uint2(h0, h1);
-        *reinterpret_cast<uint2*>(MTl + o) = make_uint2(l0, l1);
-    }
-}
 
 // One DPP step of wave_argmax_dpp: keep the larger (value bits, 63 - lane) key.
 template <int CTRL, int ROW_MASK>
@@ -966,25 +871,24 @@ __global__ __launch_bounds__(256, 2) void key_kernel(const uint16_t* __restrict_
 // Newton-Schulz of one head by the four waves of a key2_kernel block (m > 48), so that the solve
 // runs beside the key side instead of before it: the same computation as frame_ns_kernel's
 // solve (W from the landmark code tables, c, X0 = W^T / c, the T updates in product form,
-// fp16-pair MFMA 32x32x16), with each wave owning the 32 x 32 block (rb, cb) = (w / 2, w % 2)
-// of both chains, and the transposed copies of Z and E in one buffer each (a second barrier per
-// step instead of a second buffer) to fit the key blocks' LDS: kNsRoleLds bytes.
-constexpr int kNsRoleLds = 4 * 64 * kLP * 2 + 2 * 4 * 64 * 4 + 64 * 4;
+// fp16-pair MFMA 32x32x16, ns_iterate_split), with each wave owning the 32 x 32 block
+// (rb, cb) = (w / 2, w % 2) of both chains, and the transposed copies of Z and E in one buffer
+// each (a second barrier per step instead of a second buffer) to fit the key blocks' LDS:
+// kNsRoleLds bytes.
+constexpr int kNsRoleLds = kNsSplitLds + 2 * 4 * 64 * 4 + 64 * 4;
 
 template <int D>
 __device__ void ns_role(int h, char* lds, const uint32_t* __restrict__ qfix, const uint32_t* __restrict__ kfix,
-                        const float* __restrict__ frame, float* __restrict__ XT, float* __restrict__ cinfo, int m,
-                        int T, float eps) {
+                        float* __restrict__ frame, float* __restrict__ XT, float* __restrict__ cinfo,
+                        uint32_t* __restrict__ kcen, int m, int T, float eps) {
     constexpr int NW = 4;
     constexpr int D2 = D / 2;
     constexpr int BPW = 64 / NW;   // columns b of W per wave
-    constexpr int WP = 68;         // fp32 pitch of the set-up copy of W
+    constexpr int WP = kWP;        // fp32 pitch of the set-up copy of W
     constexpr int TB = 64 * kLP;
-    _Float16* const ZTh = reinterpret_cast<_Float16*>(lds);
-    _Float16* const ZTl = ZTh + TB;
-    _Float16* const ETh = ZTh + 2 * TB;
-    _Float16* const ETl = ZTh + 3 * TB;
-    float* const part = reinterpret_cast<float*>(ZTh + 4 * TB);   // 2 x NW x 64
+    // lds: the iteration's Z^T and E^T (kNsSplitLds bytes), then the partial sums
+    _Float16* const ETh = reinterpret_cast<_Float16*>(lds) + 2 * TB;
+    float* const part = reinterpret_cast<float*>(lds + kNsSplitLds);   // 2 x NW x 64
     float* const sred = part + 2 * NW * 64;                        // 64
     // set-up aliases in the E^T region, each dead before its successor is written: the code
     // tables, then W in fp32 (read until the barrier that precedes the first store of E^T)
@@ -1010,6 +914,34 @@ __device__ void ns_role(int h, char* lds, const uint32_t* __restrict__ qfix, con
         }
     }
     __syncthreads();
+    // ---- the query side's row bound from the key-landmark codes (rows >= m of the table are
+    // zero): kcen[h][c/2] = their centre (per coordinate, the rounded mean over the m landmarks)
+    // and frame[h][6] = rho = max_l sum_c |u(kt_{l,c}) - centre_c| (code units); by the triangle
+    // inequality every query's code distance to landmark l is at least its distance to the
+    // centre minus rho.
+    uint32_t* const scen = reinterpret_cast<uint32_t*>(part);   // D2 words, dead before the norms
+    if (tid < D2) {
+        uint32_t slo = 0, shi = 0;
+#pragma unroll 16
+        for (int a = 0; a < 64; ++a) {
+            const uint32_t u = sK[a * D2 + tid];
+            slo += u & 0xffffu;
+            shi += u >> 16;
+        }
+        const uint32_t cen = ((slo + m / 2) / m) | (((shi + m / 2) / m) << 16);
+        scen[tid] = cen;
+        kcen[(size_t)h * D2 + tid] = cen;
+    }
+    __syncthreads();
+    if (w == 0) {
+        uint32_t dist = 0;
+        if (l < m) {
+#pragma unroll
+            for (int c2 = 0; c2 < D2; ++c2) dist = __builtin_amdgcn_sad_u16(sK[l * D2 + c2], scen[c2], dist);
+        }
+        const float rho = (float)__float_as_uint(wave_max_dpp(__uint_as_float(dist)));
+        if (l == 0) frame[h * 8 + 6] = rho;
+    }
     // ---- W[a][b] = k(qt_a, kt_b) (+ eps on the diagonal): lane a, columns b = BPW w..+BPW
     uint32_t qa[D2];
 #pragma unroll
@@ -1095,91 +1027,14 @@ __device__ void ns_role(int h, char* lds, const uint32_t* __restrict__ qfix, con
     __syncthreads();
     const float c = sred[2];
     const float inv_c = c > 0.f ? 1.f / c : 0.f;
-    float mx = sred[3] * inv_c;             // max |X0| = max |Z_0|
-    float zs = ldexpf(1.f, pow2_exp(mx));   // Z_true = Z_stored * zs
-    {
-        // Z_0^T = X0^T = W / c: BPW consecutive b of row a
-        const float x0s = inv_c / zs;
-        uint32_t xh[BPW / 2], xl[BPW / 2];
+    // the iteration (product form, ns_split.hpp); W lies in the E^T region
+    float* const XTh = XT + (size_t)h * 4096;
+    ns_iterate_split<false, true>(sWf, inv_c, sred[3], lds, sred + 32, T,
+                                  [&](int, const f32x16_t& z, int rb, int cb) {
 #pragma unroll
-        for (int q = 0; q < BPW / 2; ++q) split_pk(wv[2 * q] * x0s, wv[2 * q + 1] * x0s, xh[q], xl[q]);
-        const int o = l * kLP + BPW * w;
-#pragma unroll
-        for (int q = 0; q < BPW / 8; ++q) {
-            *reinterpret_cast<uint4*>(ZTh + o + 8 * q) = make_uint4(xh[4 * q], xh[4 * q + 1], xh[4 * q + 2], xh[4 * q + 3]);
-            *reinterpret_cast<uint4*>(ZTl + o + 8 * q) = make_uint4(xl[4 * q], xl[4 * q + 1], xl[4 * q + 2], xl[4 * q + 3]);
-        }
-        if (T == 0) {
-#pragma unroll
-            for (int bb = 0; bb < BPW; ++bb) XT[(size_t)h * 4096 + (BPW * w + bb) * 64 + l] = wv[bb] * inv_c;
-        }
-    }
-    __syncthreads();
-    if (T == 0) return;
-    const int rb = w >> 1, cb = w & 1;
-    // Z_0 = X0 (this wave's block, fp32): X0[row][col] = W[col][row] / c
-    f32x16_t zreg;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) zreg[r] = sWf[(32 * cb + (l & 31)) * WP + 32 * rb + c_row(r, l)] * inv_c;
-    // E_0 = I - W X0 (A = W from the fp32 copy, B = X0 through Z^T)
-    f32x16_t e0;
-    {
-        h8_t wah[4], wal[4];
-#pragma unroll
-        for (int s4 = 0; s4 < 4; ++s4) {
-            const float* src = sWf + (32 * rb + (l & 31)) * WP + 16 * s4 + 8 * (l >> 5);
-            uint32_t hq[4], lq[4];
-#pragma unroll
-            for (int q = 0; q < 4; ++q) split_pk(src[2 * q], src[2 * q + 1], hq[q], lq[q]);
-            wah[s4] = __builtin_bit_cast(h8_t, make_uint4(hq[0], hq[1], hq[2], hq[3]));
-            wal[s4] = __builtin_bit_cast(h8_t, make_uint4(lq[0], lq[1], lq[2], lq[3]));
-        }
-        e0 = mm32_split(wah, wal, ZTh, ZTl, cb);
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int row = 32 * rb + c_row(r, l), col = 32 * cb + (l & 31);
-            e0[r] = (row == col ? 1.f : 0.f) - e0[r] * zs;
-        }
-    }
-    __syncthreads();   // every wave has read W before E_0 takes its place
-    store32_t(e0, 1.f, rb, cb, ETh, ETl);
-    __syncthreads();
-    for (int k = 0; k < T; ++k) {
-        // Z_{k+1} = Z_k + Z_k E_k and, but for the last step, E_{k+1} = E_k E_k
-        h8_t ah[4], al[4];
-#pragma unroll
-        for (int s4 = 0; s4 < 4; ++s4) {
-            ah[s4] = a_from_transposed(ZTh, rb, 16 * s4);
-            al[s4] = a_from_transposed(ZTl, rb, 16 * s4);
-        }
-        const f32x16_t dz = mm32_split(ah, al, ETh, ETl, cb);
-#pragma unroll
-        for (int r = 0; r < 16; ++r) zreg[r] = fmaf(dz[r], zs, zreg[r]);
-        if (k + 1 < T) {
-#pragma unroll
-            for (int s4 = 0; s4 < 4; ++s4) {
-                ah[s4] = a_from_transposed(ETh, rb, 16 * s4);
-                al[s4] = a_from_transposed(ETl, rb, 16 * s4);
-            }
-            const f32x16_t e = mm32_split(ah, al, ETh, ETl, cb);
-            // scale of Z_{k+1} from the maximum of Z_k (mx)
-            zs = ldexpf(1.f, (mx > 0.f && isfinite(mx)) ? ilogbf(mx) - 7 : 0);
-            float lm = 0.f;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) lm = fmaxf(lm, fabsf(zreg[r]));
-            lm = wave_max_dpp(lm);
-            __syncthreads();   // every wave's reads of step k are done
-            store32_t(zreg, 1.f / zs, rb, cb, ZTh, ZTl);
-            store32_t(e, 1.f, rb, cb, ETh, ETl);
-            if (l == 0) sred[32 + w] = lm;
-            __syncthreads();
-            mx = fmaxf(fmaxf(sred[32], sred[33]), fmaxf(sred[34], sred[35]));
-        } else {
-#pragma unroll
-            for (int r = 0; r < 16; ++r)
-                XT[(size_t)h * 4096 + (32 * rb + c_row(r, l)) * 64 + 32 * cb + (l & 31)] = zreg[r];
-        }
-    }
+                                      for (int r = 0; r < 16; ++r)
+                                          XTh[(32 * rb + c_row(r, l)) * 64 + 32 * cb + (l & 31)] = z[r];
+                                  });
 }
 
 // ------------------------------------------------------------------------------------------
@@ -1220,9 +1075,10 @@ __global__ __launch_bounds__(256, D == 32 ? 4 : 3) void key2_kernel(const uint16
                                                                     const uint16_t* __restrict__ V,
                                                                     const uint32_t* __restrict__ qfix,
                                                                     const uint32_t* __restrict__ kfix,
-                                                                    const float* __restrict__ frame,
+                                                                    float* __restrict__ frame,
                                                                     float* __restrict__ Upart, float* __restrict__ XT,
-                                                                    float* __restrict__ cinfo, int BH, int n, int m,
+                                                                    float* __restrict__ cinfo,
+                                                                    uint32_t* __restrict__ kcen, int BH, int n, int m,
                                                                     int ntile, int nkb, int T, float eps, int nns) {
     constexpr int D2 = D / 2;
     constexpr int D8 = D / 8;
@@ -1232,7 +1088,7 @@ __global__ __launch_bounds__(256, D == 32 ? 4 : 3) void key2_kernel(const uint16
     constexpr int VP = kK2VP;
     __shared__ __attribute__((aligned(16))) char lds[K2Lds<D>::BYTES];
     if ((int)blockIdx.x < nns) {
-        ns_role<D>(blockIdx.x, lds, qfix, kfix, frame, XT, cinfo, m, T, eps);
+        ns_role<D>(blockIdx.x, lds, qfix, kfix, frame, XT, cinfo, kcen, m, T, eps);
         return;
     }
     uint32_t* const sC = reinterpret_cast<uint32_t*>(lds);
@@ -1403,7 +1259,8 @@ __global__ __launch_bounds__(256, D == 32 ? 4 : 3) void key2_kernel(const uint16
 // Value columns: fp16 MFMA operand tiles Mt[h][s][cb][lane][i] = M[16s + 8(lane/32) + i]
 // [32cb + lane%32] * 2^-e_g with mscale[h][g] = 2^e_g putting the group's largest magnitude in
 // [2^14, 2^15).  Ones column: Mones[h][a] = M[a][D] in fp32.
-// The ones group also forms the query side's row bound from the key-landmark codes kfix[h]:
+// With kfix given (m <= 48; for m > 48 the solve blocks of key2_kernel form it), the ones group
+// also forms the query side's row bound from the key-landmark codes kfix[h]:
 // kcen[h][c/2] = their centre (per coordinate, the rounded mean over the m landmarks) and
 // frame[h][6] = rho = max_l sum_c |u(kt_{l,c}) - centre_c| (code units); by the triangle
 // inequality every query's code distance to landmark l is at least its distance to the centre
@@ -1464,7 +1321,7 @@ __global__ __launch_bounds__(kMfinalThreads) void mfinal_kernel(const float* __r
         reinterpret_cast<float4*>(sU)[f] = make_float4(((acc.x + r1.x) + r2.x) + r3.x, ((acc.y + r1.y) + r2.y) + r3.y,
                                                        ((acc.z + r1.z) + r2.z) + r3.z, ((acc.w + r1.w) + r2.w) + r3.w);
     }
-    if (ones && w == 8) {
+    if (ones && w == 8 && kfix) {
         // centre of the key-landmark codes (rows >= m of the table are zero)
         const uint32_t* tab = kfix + (size_t)h * 64 * D2;
         if (l < D2) {
@@ -1481,7 +1338,7 @@ __global__ __launch_bounds__(kMfinalThreads) void mfinal_kernel(const float* __r
         }
     }
     __syncthreads();
-    if (ones && w == 8) {
+    if (ones && w == 8 && kfix) {
         // rho: the largest code distance of a landmark from the centre
         const uint32_t* tab = kfix + (size_t)h * 64 * D2;
         uint32_t dist = 0;
@@ -1945,15 +1802,15 @@ hipError_t launch_fast_frame_ns(const float* qt, const float* kt, const double* 
 }
 
 hipError_t launch_fast_key2(const void* K, const void* V, const uint32_t* qfix, const uint32_t* kfix,
-                            const float* frame, float* Upart, float* XT, float* cinfo, int BH, int n, int d, int m,
-                            int ntile, int nkb, int T, float eps, hipStream_t st) {
+                            float* frame, float* Upart, float* XT, float* cinfo, uint32_t* kcen, int BH, int n, int d,
+                            int m, int ntile, int nkb, int T, float eps, hipStream_t st) {
     dim3 grid(BH + BH * nkb);   // BH solve blocks first, then the key blocks
     if (d == 32)
         hipLaunchKernelGGL(key2_kernel<32>, grid, dim3(256), 0, st, (const uint16_t*)K, (const uint16_t*)V, qfix, kfix,
-                           frame, Upart, XT, cinfo, BH, n, m, ntile, nkb, T, eps, BH);
+                           frame, Upart, XT, cinfo, kcen, BH, n, m, ntile, nkb, T, eps, BH);
     else
         hipLaunchKernelGGL(key2_kernel<64>, grid, dim3(256), 0, st, (const uint16_t*)K, (const uint16_t*)V, qfix, kfix,
-                           frame, Upart, XT, cinfo, BH, n, m, ntile, nkb, T, eps, BH);
+                           frame, Upart, XT, cinfo, kcen, BH, n, m, ntile, nkb, T, eps, BH);
     return hipGetLastError();
 }
 

@@ -396,7 +396,8 @@ hipError_t forward_fast(Recorder& rec, const FastPlan& p, const void* Q, const v
         if (p.split)
             return lapattn::launch_fast_key2(K, V, at<uint32_t>(ws, p.qfix), at<uint32_t>(ws, p.kfix),
                                              at<float>(ws, p.frame), at<float>(ws, p.Upart), at<float>(ws, p.XT),
-                                             at<float>(ws, p.cinfo), BH, n, d, m, p.T, p.nkb, T, eps, st);
+                                             at<float>(ws, p.cinfo), at<uint32_t>(ws, p.kcen), BH, n, d, m, p.T,
+                                             p.nkb, T, eps, st);
         return lapattn::launch_fast_key(K, V, at<uint32_t>(ws, p.qfix), at<float>(ws, p.frame), at<float>(ws, p.Upart),
                                         BH, n, d, m, p.kpb, p.nkb, st);
     });
@@ -406,7 +407,8 @@ hipError_t forward_fast(Recorder& rec, const FastPlan& p, const void* Q, const v
                                            at<float>(ws, p.mscale), at<float>(ws, p.Mones), at<float>(ws, p.M), BH, d, m,
                                            p.nkb, whiten, mspace ? 1 : 0, H, at<float>(ws, p.mvec),
                                            at<float>(ws, p.vbar), norm == LAPATTN_NORM_INLINE ? 1 : 0,
-                                           at<uint32_t>(ws, p.kfix), at<uint32_t>(ws, p.kcen), at<float>(ws, p.frame),
+                                           p.split ? nullptr : at<uint32_t>(ws, p.kfix), at<uint32_t>(ws, p.kcen),
+                                           at<float>(ws, p.frame),
                                            st);
     });
     if (e != hipSuccess) return e;

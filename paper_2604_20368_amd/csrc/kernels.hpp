@@ -157,17 +157,20 @@ hipError_t launch_fast_frame_ns(const float* qt, const float* kt, const double* 
 // The same with the landmarks split over the waves (m > 48): blocks (h, kb) of the head's
 // ntile = ceil(n / 128) tiles of 128 keys, tiles [kb ntile / nkb, (kb + 1) ntile / nkb); the
 // launch also holds BH blocks that solve Newton-Schulz (T updates, eps) into XT and cinfo, from
-// the code tables qfix, kfix (launch_fast_frame_ns writes only the frame when m > 48).
+// the code tables qfix, kfix (launch_fast_frame_ns writes only the frame when m > 48), and the
+// query side's row bound: kcen [BH][d/2] (centre of the key-landmark codes) and frame[h][6] (its
+// radius).
 hipError_t launch_fast_key2(const void* K, const void* V, const uint32_t* qfix, const uint32_t* kfix,
-                            const float* frame, float* Upart, float* XT, float* cinfo, int BH, int n, int d, int m,
-                            int ntile, int nkb, int T, float eps, hipStream_t st);
+                            float* frame, float* Upart, float* XT, float* cinfo, uint32_t* kcen, int BH, int n, int d,
+                            int m, int ntile, int nkb, int T, float eps, hipStream_t st);
 hipError_t launch_fast_key(const void* K, const void* V, const uint32_t* qfix, const float* frame, float* Upart,
                            int BH, int n, int d, int m, int kpb, int nkb, hipStream_t st);
 // mspace: the landmark-space normalisation (operand rows scaled by the whitening [H][m], NULL:
 // ones; the ones column 1/m; mvec[BH][2][d] written as for launch_mspace_vec).  center (the
 // inline normalisation): the operand columns are M[a][c] - M[a][d] vbar[c] (vbar [BH][d]), and M's
-// value columns are not written.  Also the query side's row bound: kcen [BH][d/2] (centre of the
-// key-landmark codes kfix) and frame[h][6] (its radius).
+// value columns are not written.  With kfix (m <= 48) also the query side's row bound: kcen
+// [BH][d/2] (centre of the key-landmark codes kfix) and frame[h][6] (its radius); NULL: formed by
+// launch_fast_key2.
 hipError_t launch_fast_mfinal(const float* Upart, const float* XT, _Float16* Mt, float* mscale, float* Mones,
                               float* M, int BH, int d, int m, int nkb, const float* whiten, int mspace, int H,
                               float* mvec, const float* vbar, int center, const uint32_t* kfix, uint32_t* kcen,

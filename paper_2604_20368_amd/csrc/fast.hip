@@ -211,13 +211,22 @@ __device__ __forceinline__ void load_row(uint32_t (&t)[D2], const uint32_t* __re
     for (int c = 0; c < D2; ++c) t[c] = q[c];
 }
 
+// The sad chains start at 0 (an inline operand beside the scalar row word) and meet the 2^23
+// bias in their final add, through an operand held in a scalar register: a literal start value
+// would cost a move per row.
+__device__ __forceinline__ uint32_t bias23() {
+    uint32_t b;
+    asm("s_mov_b32 %0, 0x4b000000" : "=s"(b));
+    return b;
+}
+
 // The exp2 argument (lap_arg) and the kernel value (lap_row) of one (lane's token, landmark
 // row) pair: two sad chains over the even and odd coordinate pairs; the first sad (the wait
 // point for `t`) is issued before the scalar loads of the next row, which go into `nt`.
 template <int D2>
 __device__ __forceinline__ float lap_arg(const uint32_t (&kf)[D2], const uint32_t (&t)[D2], uint32_t (&nt)[D2],
                                          const uint32_t* __restrict__ next_row, float esc, float ebias) {
-    uint32_t u0 = __builtin_amdgcn_sad_u16(kf[0], t[0], 0x4B000000u);
+    uint32_t u0 = __builtin_amdgcn_sad_u16(kf[0], t[0], 0u);
     __builtin_amdgcn_sched_barrier(0);
     load_row<D2>(nt, next_row);
     __builtin_amdgcn_sched_barrier(0);
@@ -227,7 +236,7 @@ __device__ __forceinline__ float lap_arg(const uint32_t (&kf)[D2], const uint32_
         u0 = __builtin_amdgcn_sad_u16(kf[c], t[c], u0);
         u1 = __builtin_amdgcn_sad_u16(kf[c + 1], t[c + 1], u1);
     }
-    return fmaf(__uint_as_float(u0 + u1), esc, ebias);
+    return fmaf(__uint_as_float(u0 + u1 + bias23()), esc, ebias);
 }
 template <int D2>
 __device__ __forceinline__ float lap_row(const uint32_t (&kf)[D2], const uint32_t (&t)[D2], uint32_t (&nt)[D2],
@@ -241,7 +250,7 @@ __device__ __forceinline__ float lap_row(const uint32_t (&kf)[D2], const uint32_
 template <int D2>
 __device__ __forceinline__ float lap_arg_lds(const uint32_t (&kf)[D2], const uint32_t (&t)[D2], uint32_t (&nt)[D2],
                                              const uint32_t* next_row, float esc, float ebias) {
-    uint32_t u0 = __builtin_amdgcn_sad_u16(kf[0], t[0], 0x4B000000u);
+    uint32_t u0 = __builtin_amdgcn_sad_u16(kf[0], t[0], 0u);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int c4 = 0; c4 < D2 / 4; ++c4) {
@@ -255,7 +264,7 @@ __device__ __forceinline__ float lap_arg_lds(const uint32_t (&kf)[D2], const uin
         u0 = __builtin_amdgcn_sad_u16(kf[c], t[c], u0);
         u1 = __builtin_amdgcn_sad_u16(kf[c + 1], t[c + 1], u1);
     }
-    return fmaf(__uint_as_float(u0 + u1), esc, ebias);
+    return fmaf(__uint_as_float(u0 + u1 + bias23()), esc, ebias);
 }
 
 // The exp2 arguments of two tokens (x, y) against one landmark row: four sad chains, the loads
@@ -265,12 +274,12 @@ template <int D2>
 __device__ __forceinline__ void lap_arg2(const uint32_t (&xf)[D2], const uint32_t (&yf)[D2], const uint32_t (&t)[D2],
                                          uint32_t (&nt)[D2], const uint32_t* __restrict__ next_row, float esc,
                                          float xbias, float ybias, float& gx, float& gy) {
-    uint32_t u0 = __builtin_amdgcn_sad_u16(xf[0], t[0], 0x4B000000u);
+    uint32_t u0 = __builtin_amdgcn_sad_u16(xf[0], t[0], 0u);
     __builtin_amdgcn_sched_barrier(0);
     load_row<D2>(nt, next_row);
     __builtin_amdgcn_sched_barrier(0);
     uint32_t u1 = __builtin_amdgcn_sad_u16(xf[1], t[1], 0u);
-    uint32_t v0 = __builtin_amdgcn_sad_u16(yf[0], t[0], 0x4B000000u);
+    uint32_t v0 = __builtin_amdgcn_sad_u16(yf[0], t[0], 0u);
     uint32_t v1 = __builtin_amdgcn_sad_u16(yf[1], t[1], 0u);
 #pragma unroll
     for (int c = 2; c < D2; c += 2) {
@@ -279,8 +288,9 @@ __device__ __forceinline__ void lap_arg2(const uint32_t (&xf)[D2], const uint32_
         v0 = __builtin_amdgcn_sad_u16(yf[c], t[c], v0);
         v1 = __builtin_amdgcn_sad_u16(yf[c + 1], t[c + 1], v1);
     }
-    gx = fmaf(__uint_as_float(u0 + u1), esc, xbias);
-    gy = fmaf(__uint_as_float(v0 + v1), esc, ybias);
+    const uint32_t b23 = bias23();
+    gx = fmaf(__uint_as_float(u0 + u1 + b23), esc, xbias);
+    gy = fmaf(__uint_as_float(v0 + v1 + b23), esc, ybias);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -1681,6 +1691,7 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
         else if (NORM == NORM_ROWSUM) { tmul = 1.f / si; tadd = 0.f; }
         else if (NORM == NORM_MSPACE) { tmul = fi; tadd = -si * fi; }
         else { tmul = fi; tadd = 0.f; }
+        if (nan_head) tmul = __builtin_nanf("");   // every output of the head NaN
         uint16_t* stage = sOut + w * 32 * OP + (l & 31) * OP;
 #pragma unroll
         for (int cb = 0; cb < CB; ++cb) {
@@ -1717,7 +1728,6 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
                     o1 += cv.y;
                     o2 += cv.z;
                     o3 += cv.w;
-                    if (nan_head) o0 = o1 = o2 = o3 = __builtin_nanf("");
                     *reinterpret_cast<float4*>(so) = make_float4(o0, o1, o2, o3);
                     continue;
                 } else if (extra) {   // the convolution branch of Eq. (7); rows past n read row n - 1
@@ -1728,7 +1738,6 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
                     o2 += ex.z;
                     o3 += ex.w;
                 }
-                if (nan_head) o0 = o1 = o2 = o3 = __builtin_nanf("");
                 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
                 const bf16x2_t p0 = {(__bf16)o0, (__bf16)o1}, p1 = {(__bf16)o2, (__bf16)o3};
                 uint2 st;

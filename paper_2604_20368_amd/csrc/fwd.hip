@@ -327,6 +327,123 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void key_summary_kernel(const
 // Products on the fp32 matrix cores (ns32_mm, ns_mfma.hpp).  X is kept both ways (row-major as A
 // of X T, transposed as B of W X) in two alternating buffers, and 2I - W X is written transposed
 // (as B of X T): two block barriers per step.
+// ---- Pieces of the Newton-Schulz solve shared by ns_solve_kernel and small_forward_kernel, for
+// one workgroup of 256 threads and W (MP x MP, zero outside m x m) in LDS with pitch
+// ns32_tiles<MP>::P.
+//
+// Norms: column sums (s < MP) and row sums (s >= MP) of |W| in fp64, each over 256 / (2 MP) parts
+// of the index range, then the first maximising column b* and row a* by a lane butterfly; c =
+// ||W||_1 ||W||_inf into *sc (LDS) and, when cinfo is given, {c, ||W||_1, ||W||_inf, a* 256 + b*}.
+// spart is 256 doubles of LDS, sred 4.  Begins after a barrier that completes W; ends with one.
+template <int MP>
+__device__ __forceinline__ void ns_norms(const float* sW, double* spart, double* sred, double* sc, double* cinfo) {
+    constexpr int P = ns32_tiles<MP>::P;
+    const int tid = threadIdx.x;
+    {
+        constexpr int NPART = 256 / (2 * MP), LEN = MP / NPART;
+        const int s = tid % (2 * MP), part = tid / (2 * MP), idx = s % MP;
+        double acc[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+        for (int i = 0; i < LEN; ++i) {
+            const int ii = part * LEN + i;
+            acc[i & 3] += fabs((double)(s < MP ? sW[ii * P + idx] : sW[idx * P + ii]));
+        }
+        spart[tid] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+    }
+    __syncthreads();
+    if (tid < 2 * MP) {
+        constexpr int NPART = 256 / (2 * MP);
+        const int idx = tid % MP;
+        double s = 0.0;
+#pragma unroll
+        for (int p = 0; p < NPART; ++p) s += spart[p * 2 * MP + tid];
+        double v = isnan(s) ? -1.0 : s;
+        int arg = idx;
+        ns_group_argmax<MP>(v, arg);
+        if (idx == 0) {
+            sred[tid < MP ? 0 : 2] = v;
+            sred[tid < MP ? 1 : 3] = (double)arg;
+        }
+    }
+    __syncthreads();
+    if (tid == 0) {
+        const double n1 = sred[0], ninf = sred[2];
+        const int bs = (int)sred[1], as = (int)sred[3];
+        const double c = n1 * ninf;
+        *sc = c;
+        if (cinfo) {
+            cinfo[0] = c;
+            cinfo[1] = n1;
+            cinfo[2] = ninf;
+            cinfo[3] = (double)(as * 256 + bs);
+        }
+    }
+    __syncthreads();
+}
+
+// X0 = W^T / c (X := 0 if c = 0) and T updates X <- X (2I - W X) on the fp32 matrix cores: X is
+// kept both ways (row-major as A of X T, transposed as B of W X) in two alternating buffers each
+// (sX0 + i MSZ, sXT0 + i MSZ), and 2I - W X is written transposed (as B of X T) into sTT: two
+// block barriers per step.  With Xh, X_0 .. X_T and then W go there (fp64 copies, pitch MP).
+// Returns the buffer holding X_T; ends with a barrier.
+template <int MP>
+__device__ __forceinline__ const float* ns_direct_steps(const float* sW, float* sX0, float* sXT0, float* sTT, double c,
+                                                        int T, double* Xh) {
+    using L = ns32_tiles<MP>;
+    constexpr int P = L::P;
+    constexpr int MSZ = MP * P;
+    const size_t mm = (size_t)MP * MP;
+    const int tid = threadIdx.x, l = tid & 63, li = l & 15, g = l >> 4;
+    // ---- X0 = W^T / c: row-major into X buffer 0, and X0^T = W / c into its transposed buffer
+    {
+        const double ic = c > 0.0 ? 1.0 / c : 0.0;
+        for (int e = tid; e < MP * MP; e += 256) {
+            const int a = e / MP, b = e % MP;
+            const float wab = sW[a * P + b];
+            const float x = (float)((double)wab * ic);   // X0[b][a]
+            sX0[b * P + a] = x;
+            sXT0[a * P + b] = x;
+            if (Xh) {
+                Xh[(size_t)b * MP + a] = (double)x;
+                Xh[(size_t)(T + 1) * mm + e] = (double)wab;
+            }
+        }
+    }
+    __syncthreads();
+    // ---- T steps of X <- X (2I - W X)
+    for (int t = 0; t < T; ++t) {
+        const int cur = t & 1;
+        f32x4_t r[L::NT];
+        ns32_mm<MP>(sW, sXT0 + cur * MSZ, r);   // W X
+#pragma unroll
+        for (int i = 0; i < L::NT; ++i) {
+            const int row0 = 16 * L::tr(i) + 4 * g, col = 16 * L::tc() + li;
+            float4 tv;
+            tv.x = (row0 + 0 == col ? 2.f : 0.f) - r[i][0];
+            tv.y = (row0 + 1 == col ? 2.f : 0.f) - r[i][1];
+            tv.z = (row0 + 2 == col ? 2.f : 0.f) - r[i][2];
+            tv.w = (row0 + 3 == col ? 2.f : 0.f) - r[i][3];
+            *reinterpret_cast<float4*>(sTT + col * P + row0) = tv;   // (2I - W X)^T
+        }
+        __syncthreads();
+        ns32_mm<MP>(sX0 + cur * MSZ, sTT, r);   // X (2I - W X)
+        float* nX = sX0 + (cur ^ 1) * MSZ;
+        float* nXT = sXT0 + (cur ^ 1) * MSZ;
+#pragma unroll
+        for (int i = 0; i < L::NT; ++i) {
+            const int row0 = 16 * L::tr(i) + 4 * g, col = 16 * L::tc() + li;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) nX[(row0 + j) * P + col] = r[i][j];
+            *reinterpret_cast<float4*>(nXT + col * P + row0) = make_float4(r[i][0], r[i][1], r[i][2], r[i][3]);
+            if (Xh)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) Xh[(size_t)(t + 1) * mm + (row0 + j) * MP + col] = (double)r[i][j];
+        }
+        __syncthreads();
+    }
+    return sX0 + (T & 1) * MSZ;
+}
+
 template <int MP, int D>
 __global__ __launch_bounds__(256) void ns_solve_kernel(const float* __restrict__ qt, const float* __restrict__ kt,
                                                        const float* __restrict__ Upart,
@@ -360,7 +477,7 @@ __global__ __launch_bounds__(256) void ns_solve_kernel(const float* __restrict__
     float* const sX0 = sW + MSZ;    // X buffers i = 0, 1 at sX0 + i MSZ
     float* const sXT0 = sW + 3 * MSZ;   // X^T buffers at sXT0 + i MSZ
     float* const sTT = sW + 5 * MSZ;
-    const int h = blockIdx.x, tid = threadIdx.x, l = tid & 63, li = l & 15, g = l >> 4;
+    const int h = blockIdx.x, tid = threadIdx.x;
     const float* q = qt + (size_t)h * m * D;
     const float* k = kt + (size_t)h * m * D;
     const size_t mm = (size_t)MP * MP;
@@ -441,95 +558,8 @@ __global__ __launch_bounds__(256) void ns_solve_kernel(const float* __restrict__
         }
     }
     __syncthreads();
-    // ---- norms: column sums (s < MP) and row sums (s >= MP) of |W| in fp64, each over 256 / (2 MP)
-    // parts of the index range, then the first maximising column b* and row a* by a lane butterfly
-    {
-        constexpr int NPART = 256 / (2 * MP), LEN = MP / NPART;
-        const int s = tid % (2 * MP), part = tid / (2 * MP), idx = s % MP;
-        double acc[4] = {0.0, 0.0, 0.0, 0.0};
-#pragma unroll
-        for (int i = 0; i < LEN; ++i) {
-            const int ii = part * LEN + i;
-            acc[i & 3] += fabs((double)(s < MP ? sW[ii * P + idx] : sW[idx * P + ii]));
-        }
-        spart[tid] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
-    }
-    __syncthreads();
-    if (tid < 2 * MP) {
-        constexpr int NPART = 256 / (2 * MP);
-        const int idx = tid % MP;
-        double s = 0.0;
-#pragma unroll
-        for (int p = 0; p < NPART; ++p) s += spart[p * 2 * MP + tid];
-        double v = isnan(s) ? -1.0 : s;
-        int arg = idx;
-        ns_group_argmax<MP>(v, arg);
-        if (idx == 0) {
-            sred[tid < MP ? 0 : 2] = v;
-            sred[tid < MP ? 1 : 3] = (double)arg;
-        }
-    }
-    __syncthreads();
-    if (tid == 0) {
-        const double n1 = sred[0], ninf = sred[2];
-        const int bs = (int)sred[1], as = (int)sred[3];
-        const double c = n1 * ninf;
-        sc = c;
-        cinfo[h * 4 + 0] = c;
-        cinfo[h * 4 + 1] = n1;
-        cinfo[h * 4 + 2] = ninf;
-        cinfo[h * 4 + 3] = (double)(as * 256 + bs);
-    }
-    __syncthreads();
-    // ---- X0 = W^T / c: row-major into X buffer 0, and X0^T = W / c into its transposed buffer
-    {
-        const double c = sc;
-        const double ic = c > 0.0 ? 1.0 / c : 0.0;
-        for (int e = tid; e < MP * MP; e += 256) {
-            const int a = e / MP, b = e % MP;
-            const float wab = sW[a * P + b];
-            const float x = (float)((double)wab * ic);   // X0[b][a]
-            sX0[b * P + a] = x;
-            sXT0[a * P + b] = x;
-            if (store_all) {
-                Xh[(size_t)b * MP + a] = (double)x;
-                Xh[(size_t)(T + 1) * mm + e] = (double)wab;
-            }
-        }
-    }
-    __syncthreads();
-    // ---- T steps of X <- X (2I - W X)
-    for (int t = 0; t < T; ++t) {
-        const int cur = t & 1;
-        f32x4_t r[L::NT];
-        ns32_mm<MP>(sW, sXT0 + cur * MSZ, r);   // W X
-#pragma unroll
-        for (int i = 0; i < L::NT; ++i) {
-            const int row0 = 16 * L::tr(i) + 4 * g, col = 16 * L::tc() + li;
-            float4 tv;
-            tv.x = (row0 + 0 == col ? 2.f : 0.f) - r[i][0];
-            tv.y = (row0 + 1 == col ? 2.f : 0.f) - r[i][1];
-            tv.z = (row0 + 2 == col ? 2.f : 0.f) - r[i][2];
-            tv.w = (row0 + 3 == col ? 2.f : 0.f) - r[i][3];
-            *reinterpret_cast<float4*>(sTT + col * P + row0) = tv;   // (2I - W X)^T
-        }
-        __syncthreads();
-        ns32_mm<MP>(sX0 + cur * MSZ, sTT, r);   // X (2I - W X)
-        float* nX = sX0 + (cur ^ 1) * MSZ;
-        float* nXT = sXT0 + (cur ^ 1) * MSZ;
-#pragma unroll
-        for (int i = 0; i < L::NT; ++i) {
-            const int row0 = 16 * L::tr(i) + 4 * g, col = 16 * L::tc() + li;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) nX[(row0 + j) * P + col] = r[i][j];
-            *reinterpret_cast<float4*>(nXT + col * P + row0) = make_float4(r[i][0], r[i][1], r[i][2], r[i][3]);
-            if (store_all)
-#pragma unroll
-                for (int j = 0; j < 4; ++j) Xh[(size_t)(t + 1) * mm + (row0 + j) * MP + col] = (double)r[i][j];
-        }
-        __syncthreads();
-    }
-    const float* sXf = sX0 + (T & 1) * MSZ;   // X_T
+    ns_norms<MP>(sW, spart, sred, &sc, cinfo + h * 4);
+    const float* sXf = ns_direct_steps<MP>(sW, sX0, sXT0, sTT, sc, T, store_all ? Xh : nullptr);   // X_T
     // ---- U = sum over key chunks (in chunk order) in fp64: the first CB chunks from the early
     // loads, then CB chunks' loads in flight at a time
     double u[NE];
@@ -885,6 +915,473 @@ hipError_t launch_query_out(int dt, int norm, const void* Q, void* Out, const fl
     const float ks = kscale_of(lambda);
     if (d == 32) query_out_launch<32>(norm, Q, Out, kt, M, Mc, vbar, extra, whiten, mvec, Asave, BH, H, n, m, ks, st);
     else query_out_launch<64>(norm, Q, Out, kt, M, Mc, vbar, extra, whiten, mvec, Asave, BH, H, n, m, ks, st);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------------------
+// Small heads (fp32 inputs, n <= 256 tokens, m <= 32 landmarks): the whole forward of one head in
+// one workgroup of 256 threads, every intermediate in LDS -- one launch instead of four, where
+// each of those would run a few waves per head and wait on its own latency chains (the
+// DeiT-small shape: 197 tokens, 32 landmarks).
+//
+// L1 distances in fixed point.  Every kernel value of the head -- K_LL, B and A of Eqs. (5)-(6) --
+// is exp(-||x - y||_1 / lambda) with x, y rows of Q, K or their landmark means, all of magnitude
+// at most R = max |x| over the head's Q and K (a mean lies within its tokens).  With s = 2^(22 -
+// e), R < 2^e, each coordinate is coded as the bits of fmaf(x, s, 1.5 2^23): for |x s| <= 2^22
+// that float lies in [2^23, 2^24], where consecutive floats are the consecutive integers, so the
+// bits are 0x4B000000 + 2^22 + round(x s) and the difference of two codes is the difference of
+// the rounded scaled coordinates.  One v_sad_u32 per coordinate then adds |x_c - y_c| s exactly
+// (a row's sum stays below D 2^23 <= 2^29).  The rounding moves a coordinate by at most 2^-(23 -
+// e) <= R 2^-22, a distance by at most D times that (typically ~3 times); the fp32 sums they
+// replace carry errors of the same order.  Because all three matrices use the same codes and the
+// same exponential, a query equal to a landmark mean gives exactly that row of K_LL (m = n
+// reproduces dense attention through X = W^-1).  A non-finite value in Q or K makes every output
+// of the head NaN.
+//
+// Steps:
+//   pool     thread (landmark a = t / 8, columns (t % 8) D/8 ..): the landmark means in fp64,
+//            rounded once; R by a block maximum; the means coded into LDS;
+//   K_LL     thread (a = t / 8, b = 4 (t % 8) ..): four sad chains;
+//   solve    ns_norms, ns_direct_steps (MP = 32), X_T copied aside;
+//   key side thread t: keys t % 128 and t % 128 + 128 against the 16 landmarks of half t / 128
+//            (each LDS broadcast of a landmark word serves two keys), B[a][j] into a [32][256]
+//            tile; then wave w contracts keys 64 w .. 64 w + 63 with [V | 1] on fp32 MFMA 16x16x4
+//            (the V rows loaded together, their fp64 column sums giving vbar) and the four
+//            waves' partials are added in a fixed order;
+//   M        M = X_T U in fp64 (ns_mm), Mc = M[:, :d] - M[:, d] vbar^T for the inline form;
+//   query    thread t: queries t % 128, t % 128 + 128 against half t / 128 of the landmarks, A
+//            into a [256][33] tile (and the two halves of s_i for the row sums); then
+//            Y = A M on fp32 MFMA, normalised (Eq. (4) / Eq. (3)) and stored.
+
+// |x - y| + acc on unsigned 32-bit integers (v_sad_u32).
+__device__ __forceinline__ uint32_t sad32(uint32_t x, uint32_t y, uint32_t acc) {
+    uint32_t r;
+    asm("v_sad_u32 %0, %1, %2, %3" : "=v"(r) : "v"(x), "v"(y), "v"(acc));
+    return r;
+}
+// Code of x on the grid 1/s (the comment above).
+__device__ __forceinline__ uint32_t sf_code(float x, float s) { return __float_as_uint(fmaf(x, s, 12582912.f)); }
+// Kernel value from a coded distance: exp2(dist * kss), kss = -log2(e) / (lambda s).
+__device__ __forceinline__ float sf_kval(uint32_t dist, float kss) {
+    return __builtin_amdgcn_exp2f((float)dist * kss);
+}
+
+// Coded L1 distances of two tokens (codes x0, x1) to rows 0 .. na - 1 of an LDS code table
+// (pitch LP words); emit(aa, dist0, dist1) per row.  The rows are read as half rows of D / 8
+// 16-byte words into two buffers: the reads of the next half row are issued before the sads of
+// the current one, so that D / 8 reads are always in flight (one or two waves per SIMD leave
+// the LDS latency to the wave itself).  Each word serves both tokens.  na is wave-uniform.
+template <int D, int LP, class Emit>
+__device__ __forceinline__ void sf_dist2(const uint32_t* __restrict__ tab, int na, const uint32_t (&x0)[D],
+                                         const uint32_t (&x1)[D], Emit&& emit) {
+    constexpr int H = D / 8;
+    if (na <= 0) return;
+    uint4 cur[H], nxt[H];
+#pragma unroll
+    for (int q = 0; q < H; ++q) cur[q] = reinterpret_cast<const uint4*>(tab)[q];
+    for (int aa = 0; aa < na; ++aa) {
+        const uint4* r = reinterpret_cast<const uint4*>(tab + aa * LP);
+#pragma unroll
+        for (int q = 0; q < H; ++q) nxt[q] = r[H + q];
+        __builtin_amdgcn_sched_barrier(0);
+        uint32_t u0 = 0u, w0 = 0u, u1 = 0u, w1 = 0u;
+#pragma unroll
+        for (int q = 0; q < H; ++q) {
+            const uint4 v = cur[q];
+            u0 = sad32(x0[4 * q], v.x, u0); w0 = sad32(x0[4 * q + 1], v.y, w0);
+            u1 = sad32(x1[4 * q], v.x, u1); w1 = sad32(x1[4 * q + 1], v.y, w1);
+            u0 = sad32(x0[4 * q + 2], v.z, u0); w0 = sad32(x0[4 * q + 3], v.w, w0);
+            u1 = sad32(x1[4 * q + 2], v.z, u1); w1 = sad32(x1[4 * q + 3], v.w, w1);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        const uint4* rn = reinterpret_cast<const uint4*>(tab + min(aa + 1, na - 1) * LP);
+#pragma unroll
+        for (int q = 0; q < H; ++q) cur[q] = rn[q];
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int q = 0; q < H; ++q) {
+            const uint4 v = nxt[q];
+            const int c = 4 * (H + q);
+            u0 = sad32(x0[c], v.x, u0); w0 = sad32(x0[c + 1], v.y, w0);
+            u1 = sad32(x1[c], v.x, u1); w1 = sad32(x1[c + 1], v.y, w1);
+            u0 = sad32(x0[c + 2], v.z, u0); w0 = sad32(x0[c + 3], v.w, w0);
+            u1 = sad32(x1[c + 2], v.z, u1); w1 = sad32(x1[c + 3], v.w, w1);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        emit(aa, u0 + w0, u1 + w1);
+    }
+}
+
+template <int D, int NORM>
+__global__ __launch_bounds__(256, 2) void small_forward_kernel(const float* __restrict__ Q, const float* __restrict__ K,
+                                                               const float* __restrict__ V, float* __restrict__ Out,
+                                                               int n, int m, double lambda, int T, double eps,
+                                                               LmPool pl) {
+    constexpr int MP = 32;
+    using L = ns32_tiles<MP>;
+    using SU = ns_tiles<MP, D>;
+    constexpr int P = L::P;               // pitch of the solve's fp32 matrices
+    constexpr int MSZ = MP * P;
+    constexpr int LP = D + 4;             // pitch of the landmark code rows and of M
+    constexpr int BP = 256 + 4;           // pitch of the key tile [a][j]
+    constexpr int AP = 33;                // pitch of the query tile [i][l]
+    constexpr int P64 = ns_pitch(MP);
+    constexpr int PU = ns_pitch(D);
+    constexpr int CT = D / 16 + 1;        // key-side column tiles: the values, then the ones column
+    constexpr int RP = 16 * CT;           // pitch of the key-side partial being reduced
+    constexpr int R1 = 6 * MSZ * 4, R2 = MP * BP * 4, R3 = 256 * AP * 4, R4 = (MP * P64 + MP * PU) * 8;
+    constexpr int R5 = MP * RP * 4;
+    constexpr int RB = R1 > R2 ? (R1 > R3 ? (R1 > R4 ? R1 : R4) : (R3 > R4 ? R3 : R4))
+                               : (R2 > R3 ? (R2 > R4 ? R2 : R4) : (R3 > R4 ? R3 : R4));
+    static_assert(R5 <= RB, "the key-side partial fits the shared region");
+    __shared__ __attribute__((aligned(16))) uint32_t sQc[MP * LP];   // coded landmark means
+    __shared__ __attribute__((aligned(16))) uint32_t sKc[MP * LP];
+    __shared__ __attribute__((aligned(16))) char reg[RB];   // solve / key tile / partial / M / query tile
+    __shared__ __attribute__((aligned(16))) float sXT[MSZ];
+    __shared__ __attribute__((aligned(16))) float sMv[MP * LP];
+    __shared__ float sM1[MP];
+    __shared__ float sS[2][256];
+    __shared__ float smx[4];
+    __shared__ double spart[256];
+    __shared__ double sred[4];
+    __shared__ double sc;
+    __shared__ double svp[4][D];
+    __shared__ double svb[D];
+    __shared__ double su1[MP];
+    __shared__ double sM1d[MP];
+    const int h = blockIdx.x, tid = threadIdx.x, w = tid >> 6, l = tid & 63, li = l & 15, lk = l >> 4;
+    const int hf = tid >> 7, t0 = tid & 127;   // key / query sides: landmark half, first token
+    const float* Qh = Q + (size_t)h * n * D;
+    const float* Kh = K + (size_t)h * n * D;
+    const float* Vh = V + (size_t)h * n * D;
+
+    // ---- landmark means, R = max |x| (infinite when a mean is not finite), the codes
+    constexpr int CPT = D / 8;   // columns per thread
+    float qm[CPT], km[CPT];
+    {
+        const int a = tid >> 3, c0 = (tid & 7) * CPT;
+        double sq[CPT], sk[CPT];
+#pragma unroll
+        for (int c = 0; c < CPT; ++c) sq[c] = sk[c] = 0.0;
+        float mx = 0.f;
+        int cnt = 1;
+        if (a < m) {
+            const LmTokens tok = lm_tokens(pl, a, n, m);
+            cnt = tok.count;
+#pragma unroll 4
+            for (int t = 0; t < tok.count; ++t) {
+                const size_t o = (size_t)tok(t) * D + c0;
+#pragma unroll
+                for (int c4 = 0; c4 < CPT / 4; ++c4) {
+                    const float4 qv = *reinterpret_cast<const float4*>(Qh + o + 4 * c4);
+                    const float4 kv = *reinterpret_cast<const float4*>(Kh + o + 4 * c4);
+                    sq[4 * c4] += qv.x; sq[4 * c4 + 1] += qv.y; sq[4 * c4 + 2] += qv.z; sq[4 * c4 + 3] += qv.w;
+                    sk[4 * c4] += kv.x; sk[4 * c4 + 1] += kv.y; sk[4 * c4 + 2] += kv.z; sk[4 * c4 + 3] += kv.w;
+                    mx = fmaxf(mx, fmaxf(fmaxf(fabsf(qv.x), fabsf(qv.y)), fmaxf(fabsf(qv.z), fabsf(qv.w))));
+                    mx = fmaxf(mx, fmaxf(fmaxf(fabsf(kv.x), fabsf(kv.y)), fmaxf(fabsf(kv.z), fabsf(kv.w))));
+                }
+            }
+        }
+        bool fin = true;
+#pragma unroll
+        for (int c = 0; c < CPT; ++c) {
+            qm[c] = a < m ? (float)(sq[c] / (double)cnt) : 0.f;
+            km[c] = a < m ? (float)(sk[c] / (double)cnt) : 0.f;
+            fin = fin && isfinite(qm[c]) && isfinite(km[c]);
+        }
+        // a NaN or infinite input leaves its landmark mean non-finite (fmaxf alone would skip a NaN)
+        if (!fin) mx = __builtin_inff();
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+        if (l == 0) smx[w] = mx;
+    }
+    __syncthreads();
+    const float R = fmaxf(fmaxf(smx[0], smx[1]), fmaxf(smx[2], smx[3]));
+    const bool nan_head = !(R <= 3.4028234663852886e38f);
+    float s, kss;
+    {
+        int e = 0;
+        (void)frexpf(nan_head ? 1.f : R, &e);   // R < 2^e (e = 0 for R = 0)
+        e = max(e, -100);                         // tiny R: a coarser grid, distances below 2^-100
+        s = __uint_as_float((uint32_t)(127 + 22 - e) << 23);
+        kss = (float)(-1.4426950408889634 / lambda) * __uint_as_float((uint32_t)(127 - 22 + e) << 23);
+    }
+    {
+        const int a = tid >> 3, c0 = (tid & 7) * CPT;
+#pragma unroll
+        for (int c = 0; c < CPT; ++c) {
+            sQc[a * LP + c0 + c] = sf_code(qm[c], s);
+            sKc[a * LP + c0 + c] = sf_code(km[c], s);
+        }
+    }
+    __syncthreads();
+    // ---- W = K_LL + eps I (zero outside m x m)
+    float* const sW = reinterpret_cast<float*>(reg);
+    float* const sX0 = sW + MSZ;
+    float* const sXT0 = sW + 3 * MSZ;
+    float* const sTT = sW + 5 * MSZ;
+    {
+        const int a = tid >> 3, b0 = 4 * (tid & 7);
+        uint32_t u[4] = {0u, 0u, 0u, 0u};
+#pragma unroll 4
+        for (int c4 = 0; c4 < D / 4; ++c4) {
+            const uint4 v = *reinterpret_cast<const uint4*>(sQc + a * LP + 4 * c4);
+#pragma unroll
+            for (int bb = 0; bb < 4; ++bb) {
+                const uint4 kb = *reinterpret_cast<const uint4*>(sKc + (b0 + bb) * LP + 4 * c4);
+                u[bb] = sad32(v.x, kb.x, u[bb]);
+                u[bb] = sad32(v.y, kb.y, u[bb]);
+                u[bb] = sad32(v.z, kb.z, u[bb]);
+                u[bb] = sad32(v.w, kb.w, u[bb]);
+            }
+        }
+#pragma unroll
+        for (int bb = 0; bb < 4; ++bb) {
+            const int b = b0 + bb;
+            float wv = 0.f;
+            if (a < m && b < m) {
+                wv = sf_kval(u[bb], kss);
+                if (a == b) wv = (float)((double)wv + eps);
+            }
+            sW[a * P + b] = wv;
+        }
+    }
+    __syncthreads();
+    // ---- Algorithm 2
+    ns_norms<MP>(sW, spart, sred, &sc, nullptr);
+    {
+        const float* sXf = ns_direct_steps<MP>(sW, sX0, sXT0, sTT, sc, T, nullptr);
+        for (int e = tid; e < MSZ; e += 256) sXT[e] = sXf[e];
+    }
+    __syncthreads();   // the solve's buffers are free
+    // ---- key side: B[a][j] = k(qt_a, k_j), then U = B [V | 1]
+    float* const sB = reinterpret_cast<float*>(reg);
+    {
+        uint32_t x0[D], x1[D];
+        {
+            const float4* r0 = reinterpret_cast<const float4*>(Kh + (size_t)min(t0, n - 1) * D);
+            const float4* r1 = reinterpret_cast<const float4*>(Kh + (size_t)min(t0 + 128, n - 1) * D);
+#pragma unroll
+            for (int c4 = 0; c4 < D / 4; ++c4) {
+                const float4 v0 = r0[c4], v1 = r1[c4];
+                x0[4 * c4] = sf_code(v0.x, s); x0[4 * c4 + 1] = sf_code(v0.y, s);
+                x0[4 * c4 + 2] = sf_code(v0.z, s); x0[4 * c4 + 3] = sf_code(v0.w, s);
+                x1[4 * c4] = sf_code(v1.x, s); x1[4 * c4 + 1] = sf_code(v1.y, s);
+                x1[4 * c4 + 2] = sf_code(v1.z, s); x1[4 * c4 + 3] = sf_code(v1.w, s);
+            }
+        }
+        const bool live0 = t0 < n, live1 = t0 + 128 < n;
+        const int na = __builtin_amdgcn_readfirstlane(min(max(m - 16 * hf, 0), 16));
+        sf_dist2<D, LP>(sQc + 16 * hf * LP, na, x0, x1, [&](int aa, uint32_t d0, uint32_t d1) {
+            const int a = 16 * hf + aa;
+            sB[a * BP + t0] = live0 ? sf_kval(d0, kss) : 0.f;
+            sB[a * BP + t0 + 128] = live1 ? sf_kval(d1, kss) : 0.f;
+        });
+        for (int a = 16 * hf + na; a < 16 * hf + 16; ++a) {   // landmarks past m
+            sB[a * BP + t0] = 0.f;
+            sB[a * BP + t0 + 128] = 0.f;
+        }
+    }
+    // wave w's operands: V rows of keys 64 w + 4 s + lk (clamped past n: their B columns are 0)
+    float vv[16][CT - 1];
+#pragma unroll
+    for (int s4 = 0; s4 < 16; ++s4) {
+        const float* vr = Vh + (size_t)min(64 * w + 4 * s4 + lk, n - 1) * D;
+#pragma unroll
+        for (int ct = 0; ct < CT - 1; ++ct) vv[s4][ct] = vr[16 * ct + li];
+    }
+    // vbar: this lane's live keys in fp64, then the four key groups of the wave (a butterfly);
+    // the waves' sums are added in order 0..3 after the next barrier
+    {
+        double vs[CT - 1];
+#pragma unroll
+        for (int ct = 0; ct < CT - 1; ++ct) vs[ct] = 0.0;
+#pragma unroll
+        for (int s4 = 0; s4 < 16; ++s4)
+            if (64 * w + 4 * s4 + lk < n)
+#pragma unroll
+                for (int ct = 0; ct < CT - 1; ++ct) vs[ct] += (double)vv[s4][ct];
+#pragma unroll
+        for (int ct = 0; ct < CT - 1; ++ct) {
+            vs[ct] += __shfl_xor(vs[ct], 16, 64);
+            vs[ct] += __shfl_xor(vs[ct], 32, 64);
+            if (lk == 0) svp[w][16 * ct + li] = vs[ct];
+        }
+    }
+    __syncthreads();   // B complete (a wave's keys were formed by two waves)
+    f32x4_t acc[2][CT];
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) acc[rt][ct] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s4 = 0; s4 < 16; ++s4) {
+        const int jr = 64 * w + 4 * s4 + lk;
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt) {
+            const float av = sB[(16 * rt + li) * BP + jr];
+#pragma unroll
+            for (int ct = 0; ct < CT - 1; ++ct) acc[rt][ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, vv[s4][ct], acc[rt][ct], 0, 0, 0);
+            acc[rt][CT - 1] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, li == 0 ? 1.f : 0.f, acc[rt][CT - 1], 0, 0, 0);
+        }
+    }
+    if (tid < D) svb[tid] = (((svp[0][tid] + svp[1][tid]) + svp[2][tid]) + svp[3][tid]) / n;
+    // the four waves' partials added in the order 3, 2, 1, 0 (register r of a 16x16x4 tile at
+    // lane l: row 4 (l / 16) + r, column l % 16)
+    float* const red = reinterpret_cast<float*>(reg);
+    for (int ww = 3; ww >= 0; --ww) {
+        __syncthreads();   // (first pass: every wave is done with the key tile)
+        if (w == ww) {
+#pragma unroll
+            for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+                for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        float* p = red + (16 * rt + 4 * lk + r) * RP + 16 * ct + li;
+                        *p = (ww == 3) ? acc[rt][ct][r] : *p + acc[rt][ct][r];
+                    }
+        }
+    }
+    __syncthreads();
+    // ---- M = X_T U in fp64 (the partial and X_T through registers: fp64 copies replace them)
+    constexpr int NU = (MP * (D + 1) + 255) / 256;
+    double uv[NU];
+#pragma unroll
+    for (int r = 0; r < NU; ++r) {
+        const int e = tid + 256 * r;
+        uv[r] = e < MP * (D + 1) ? (double)red[(e / (D + 1)) * RP + e % (D + 1)] : 0.0;
+    }
+    __syncthreads();
+    double* const sX64 = reinterpret_cast<double*>(reg);
+    double* const sU64 = sX64 + MP * P64;
+#pragma unroll
+    for (int r = 0; r < NU; ++r) {
+        const int e = tid + 256 * r;
+        if (e < MP * (D + 1)) {
+            const int a = e / (D + 1), c = e % (D + 1);
+            if (c < D) sU64[a * PU + c] = uv[r];
+            else su1[a] = uv[r];
+        }
+    }
+    for (int e = tid; e < MP * MP; e += 256) sX64[(e / MP) * P64 + e % MP] = (double)sXT[(e / MP) * P + e % MP];
+    __syncthreads();
+    if (tid < MP) {
+        double sacc = 0.0;
+#pragma unroll 8
+        for (int b = 0; b < MP; ++b) sacc += sX64[tid * P64 + b] * su1[b];
+        sM1d[tid] = sacc;
+        sM1[tid] = (float)sacc;
+    }
+    __syncthreads();
+    {
+        f64x4_t r[SU::NT];
+        ns_mm<MP, D, MP, false, false, P64, PU>(sX64, sU64, r);
+#pragma unroll
+        for (int i = 0; i < SU::NT; ++i)
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+                const int a = SU::row(i, jj), cc = SU::col(i);
+                sMv[a * LP + cc] = NORM == NORM_INLINE ? (float)(r[i][jj] - sM1d[a] * svb[cc]) : (float)r[i][jj];
+            }
+    }
+    __syncthreads();   // sMv, sM1; the shared region is free
+    // ---- query side: A[i][l] = k(q_i, kt_l) and the halves of s_i, then Y = A M
+    float* const sA = reinterpret_cast<float*>(reg);
+    {
+        uint32_t x0[D], x1[D];
+        {
+            const float4* r0 = reinterpret_cast<const float4*>(Qh + (size_t)min(t0, n - 1) * D);
+            const float4* r1 = reinterpret_cast<const float4*>(Qh + (size_t)min(t0 + 128, n - 1) * D);
+#pragma unroll
+            for (int c4 = 0; c4 < D / 4; ++c4) {
+                const float4 v0 = r0[c4], v1 = r1[c4];
+                x0[4 * c4] = sf_code(v0.x, s); x0[4 * c4 + 1] = sf_code(v0.y, s);
+                x0[4 * c4 + 2] = sf_code(v0.z, s); x0[4 * c4 + 3] = sf_code(v0.w, s);
+                x1[4 * c4] = sf_code(v1.x, s); x1[4 * c4 + 1] = sf_code(v1.y, s);
+                x1[4 * c4 + 2] = sf_code(v1.z, s); x1[4 * c4 + 3] = sf_code(v1.w, s);
+            }
+        }
+        const bool live0 = t0 < n, live1 = t0 + 128 < n;
+        float sr0 = 0.f, sr1 = 0.f;
+        const int na = __builtin_amdgcn_readfirstlane(min(max(m - 16 * hf, 0), 16));
+        sf_dist2<D, LP>(sKc + 16 * hf * LP, na, x0, x1, [&](int aa, uint32_t d0, uint32_t d1) {
+            const int a = 16 * hf + aa;
+            const float a0 = live0 ? sf_kval(d0, kss) : 0.f;
+            const float a1 = live1 ? sf_kval(d1, kss) : 0.f;
+            if (NORM == NORM_ROWSUM) {
+                sr0 = fmaf(a0, sM1[a], sr0);
+                sr1 = fmaf(a1, sM1[a], sr1);
+            }
+            sA[t0 * AP + a] = a0;
+            sA[(t0 + 128) * AP + a] = a1;
+        });
+        for (int a = 16 * hf + na; a < 16 * hf + 16; ++a) {   // landmarks past m
+            sA[t0 * AP + a] = 0.f;
+            sA[(t0 + 128) * AP + a] = 0.f;
+        }
+        if (NORM == NORM_ROWSUM) {
+            sS[hf][t0] = sr0;
+            sS[hf][t0 + 128] = sr1;
+        }
+    }
+    __syncthreads();   // A complete (a query's landmarks were formed by two waves)
+    {
+        constexpr int NCT = D / 16;
+        f32x4_t y[4][NCT];
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct) y[rt][ct] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s4 = 0; s4 < MP / 4; ++s4) {
+            const int kl = 4 * s4 + lk;   // landmark
+            float bv[NCT];
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct) bv[ct] = sMv[kl * LP + 16 * ct + li];
+#pragma unroll
+            for (int rt = 0; rt < 4; ++rt) {
+                const float av = sA[(64 * w + 16 * rt + li) * AP + kl];
+#pragma unroll
+                for (int ct = 0; ct < NCT; ++ct) y[rt][ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv[ct], y[rt][ct], 0, 0, 0);
+            }
+        }
+        const float nanv = nan_head ? __builtin_nanf("") : 0.f;   // added: NaN for the whole head
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int i = 64 * w + 16 * rt + 4 * lk + r;
+                if (i < n) {
+                    const float inv_s = NORM == NORM_ROWSUM ? 1.f / (sS[0][i] + sS[1][i]) : 1.f;
+#pragma unroll
+                    for (int ct = 0; ct < NCT; ++ct) {
+                        const int c = 16 * ct + li;
+                        float o = y[rt][ct][r];
+                        if (NORM == NORM_INLINE) o += (float)svb[c];
+                        else if (NORM == NORM_ROWSUM) o *= inv_s;
+                        Out[((size_t)h * n + i) * D + c] = o + nanv;
+                    }
+                }
+            }
+    }
+}
+
+hipError_t launch_small_forward(int norm, const float* Q, const float* K, const float* V, float* Out, int BH, int n,
+                                int d, int m, float lambda, int T, float eps, LmPool pl, hipStream_t st) {
+#define LAPATTN_SF(Dv, Nv)                                                                                  \
+    hipLaunchKernelGGL((small_forward_kernel<Dv, Nv>), dim3(BH), dim3(256), 0, st, Q, K, V, Out, n, m,       \
+                       (double)lambda, T, (double)eps, pl)
+    if (d == 32) {
+        if (norm == NORM_INLINE) LAPATTN_SF(32, NORM_INLINE);
+        else if (norm == NORM_ROWSUM) LAPATTN_SF(32, NORM_ROWSUM);
+        else LAPATTN_SF(32, NORM_NONE);
+    } else {
+        if (norm == NORM_INLINE) LAPATTN_SF(64, NORM_INLINE);
+        else if (norm == NORM_ROWSUM) LAPATTN_SF(64, NORM_ROWSUM);
+        else LAPATTN_SF(64, NORM_NONE);
+    }
+#undef LAPATTN_SF
     return hipGetLastError();
 }
 

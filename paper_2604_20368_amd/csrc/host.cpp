@@ -459,6 +459,19 @@ int lapattn_forward(const void* Q, const void* K, const void* V, void* Out, int 
                                         pl, dwc, whiten_of(opts), st);
             return e == hipSuccess ? LAPATTN_OK : LAPATTN_ERR_HIP;
         }
+        // small heads (fp32): one launch per forward, every intermediate in LDS
+        if (dtype == LAPATTN_FP32 && n <= 256 && m <= 32 && (d == 32 || d == 64) && !save_of(opts) && dwc.k == 0 &&
+            norm != LAPATTN_NORM_MSPACE) {
+            const Plan p = make_plan(BH, n, d, m, ns_iters, false, false, false);
+            if (!workspace || workspace_bytes < p.total) return LAPATTN_ERR_WORKSPACE;
+            Recorder rec(st);
+            const hipError_t e = run_named(rec, "small_forward", [&] {
+                return lapattn::launch_small_forward(norm, static_cast<const float*>(Q), static_cast<const float*>(K),
+                                                     static_cast<const float*>(V), static_cast<float*>(Out), BH, n, d,
+                                                     m, lambda, ns_iters, eps, pl, st);
+            });
+            return e == hipSuccess ? LAPATTN_OK : LAPATTN_ERR_HIP;
+        }
         // bf16 inputs with m > 64: widened to fp32 (exact), the fp32 path, the output rounded to bf16
         const bool bf16 = dtype == LAPATTN_BF16;
         // save: the backward's layout, with every Newton-Schulz iterate kept, so that a following

@@ -671,3 +671,82 @@ def test_forward_many_landmarks_full_size_sampled_heads(L, dtype):
     say("  heads %s" % heads)
     assert np.isfinite(got).all()
     assert_parity(got.reshape(BH, w.n, w.d)[heads][None], ref, w.dtype)
+
+
+# ------------------------------------------------------------------------------ small heads: the one-launch forward
+# fp32 heads with n <= 256, m <= 32 and d in {32, 64} (the DeiT-small shape: 197 tokens, 32
+# landmarks) run pooling, K_LL, Algorithm 2, the key side and the query side in one workgroup
+# per head.  These cases pin that path against the oracle across its limits.
+
+def launch_names(L, fn):
+    """Names of the library launches made by fn() (the library's own launch recorder)."""
+    L.lapattn_timing_enable(1)
+    try:
+        fn()
+        torch.cuda.synchronize()
+    finally:
+        L.lapattn_timing_enable(0)
+    return [k for k, _ in L.lapattn_timing_read(cap=256)]
+
+
+def test_small_forward_is_one_launch(L):
+    """The small-head shapes take the one-launch path; one token more, a bf16 input, m past 32
+    or the saved-state forward take the others."""
+    def names(w, **kw):
+        x = W.make_inputs(w, with_grad=False)
+        return launch_names(L, lambda: run_forward(L, x, w, **kw))
+    w = W.WORKLOADS["deit_small"].with_(B=1, H=2)
+    assert names(w) == ["small_forward"]
+    assert names(w.with_(n=256, d=32)) == ["small_forward"]
+    for other in (w.with_(n=257), w.with_(m=33), w.with_(dtype="bf16")):
+        assert "small_forward" not in names(other), other
+
+
+@pytest.mark.parametrize("d", [32, 64])
+@pytest.mark.parametrize("norm", [0, 1, 2])
+@pytest.mark.parametrize("n,m", [(1, 1), (2, 2), (31, 7), (64, 17), (197, 32), (256, 32), (256, 1), (32, 32),
+                                 (100, 31)])
+def test_small_forward_shapes(L, d, norm, n, m):
+    """Every normalisation at d = 32 and 64: one token, n = m, a ragged n against the 64-key
+    waves, an odd m, m = 1 and m = 32, n = 256 (every thread a live token)."""
+    w = W.Workload("small", 2, 3, n, d, m, 6, "fp32", 1 / math.sqrt(d), math.sqrt(d), 51, False)
+    check_forward(L, w, norm=norm)
+
+
+@pytest.mark.parametrize("T", [0, 1, 12])
+def test_small_forward_ns_updates(L, T):
+    """Algorithm 2's X_0 alone (T = 0), one update and many (the iterate has converged)."""
+    for d in (32, 64):
+        w = W.Workload("smallT", 1, 2, 197, d, 29, T, "fp32", 1 / math.sqrt(d), math.sqrt(d), 52, False)
+        for norm in (0, 1):
+            check_forward(L, w, norm=norm)
+
+
+def test_small_forward_windows_eps_lambda(L):
+    """4 x 4 windows of a 16 x 16 map (m = 16) and of a 12 x 16 map (m = 12), eps on the
+    diagonal, lambda = 4 and a heavy-tailed input."""
+    w = W.Workload("smallw", 1, 2, 256, 64, 16, 6, "fp32", 0.125, 8.0, 53, False)
+    for norm in (0, 1, 2):
+        check_forward(L, w, norm=norm, grid=(16, 4))
+    check_forward(L, w.with_(n=192, m=12, d=32), norm=1, grid=(16, 4))
+    check_forward(L, w.with_(m=30, n=200), eps=0.05)
+    check_forward(L, w.with_(m=30, n=200, lam=4.0, dist="t3"))
+
+
+def test_small_forward_degenerate_kernels(L):
+    """lambda = 1e-6 (every kernel value underflows: X = 0, the inline form gives v-bar, the
+    plain form 0), lambda = 1e8 (every kernel value rounds to 1) and a NaN query entry (its head's
+    output NaN, the other head untouched)."""
+    w = W.Workload("smallu", 1, 2, 197, 64, 32, 6, "fp32", 0.125, 1e-6, 54, False)
+    check_forward(L, w, norm=0)
+    x = W.make_inputs(w, with_grad=False)
+    assert not np.any(run_forward(L, x, w, norm=2))
+    check_forward(L, w.with_(lam=1e8), norm=0)
+    check_forward(L, w.with_(lam=1e8), norm=1)
+    w = w.with_(lam=8.0)
+    x = W.make_inputs(w, with_grad=False)
+    x["Q"][0, 1, 17, 3] = np.nan
+    got = run_forward(L, x, w)
+    assert np.isnan(got[0, 1]).any()
+    ref = oracle.forward(x["Q"][:, :1], x["K"][:, :1], x["V"][:, :1], w.m, w.lam, w.T)
+    assert_parity(got[:, :1], ref, "fp32")

@@ -148,9 +148,9 @@ size_t lapattn_workspace_size(int B, int H, int n, int d, int m, int ns_iters,
  * cores, fp32 accumulation); for m > 64 it runs the fp32 computation on the exactly widened
  * inputs and rounds the output to bf16 (nearest even).  fp32 heads with n <= 256, m <= 32 and
  * no convolution branch, saved state or landmark-space form run in one workgroup per head,
- * with the L1 distances in 32-bit fixed point on one grid per head (step max|Q, K| 2^-22 or
- * finer).  On these two paths (bf16, and the fp32 small heads) a NaN or infinity in Q or K
- * makes every output of its head NaN. */
+ * with the L1 distances in 32-bit fixed point on one grid per head (grid step at most
+ * 2^-21 max|Q, K|).  On these two paths (bf16, and the fp32 small heads) a NaN or infinity in
+ * Q or K makes every output of its head NaN. */
 int lapattn_forward(const void* Q, const void* K, const void* V, void* Out,
                     int B, int H, int n, int d, int m, float lambda, int ns_iters,
                     int dtype, const lapattn_opts* opts,

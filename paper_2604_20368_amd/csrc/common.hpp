@@ -33,6 +33,34 @@ template <> struct elem<DT_BF16> {
     }
 };
 
+// Fixed-point L1 distances of the one-launch small-head forward.  Every kernel value of a head is
+// exp(-||x - y||_1 / lambda) with x, y rows of Q, K or their landmark means, all of magnitude at
+// most R = max |x| over the head's Q and K.  With s = 2^(22 - e), R < 2^e, a coordinate is coded as the bits of
+// fmaf(x, s, 1.5 2^23): for |x s| <= 2^22 that float lies in [2^23, 2^24], where consecutive
+// floats are consecutive integers, so the bits are 0x4B000000 + 2^22 + round(x s) and the
+// difference of two codes is the difference of the rounded scaled coordinates.  One v_sad_u32
+// per coordinate then adds |x_c - y_c| s exactly (a row's sum stays below 64 2^23 = 2^29).  The
+// rounding moves a coordinate by at most 2^(e - 23) <= R 2^-22, a distance by at most d times
+// that (typically a few times); the fp32 sums of differences carry errors of the same order.
+// fgrid: s and kss = -log2(e) / (lambda s) from R and ks = -log2(e) / lambda; e >= -100 (a tiny R
+// gets a coarser grid: its distances are below 2^-100).  R must be finite.
+__device__ __forceinline__ void fgrid(float R, float ks, float& s, float& kss) {
+    int e = 0;
+    (void)frexpf(R, &e);   // R < 2^e (e = 0 for R = 0)
+    e = e < -100 ? -100 : e;
+    s = __uint_as_float((uint32_t)(127 + 22 - e) << 23);
+    kss = ks * __uint_as_float((uint32_t)(127 - 22 + e) << 23);
+}
+__device__ __forceinline__ uint32_t fcode(float x, float s) { return __float_as_uint(fmaf(x, s, 12582912.f)); }
+// Kernel value from a coded distance.
+__device__ __forceinline__ float fkval(uint32_t dist, float kss) { return __builtin_amdgcn_exp2f((float)dist * kss); }
+// |x - y| + acc on unsigned 32-bit integers (v_sad_u32).
+__device__ __forceinline__ uint32_t sad32(uint32_t x, uint32_t y, uint32_t acc) {
+    uint32_t r;
+    asm("v_sad_u32 %0, %1, %2, %3" : "=v"(r) : "v"(x), "v"(y), "v"(acc));
+    return r;
+}
+
 // Landmark segments: segment l covers tokens [floor(l n/m), floor((l+1) n/m)).
 __device__ __host__ __forceinline__ int seg_start(int l, int n, int m) {
     return (int)(((long long)l * n) / m);

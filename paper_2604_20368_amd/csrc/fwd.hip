@@ -924,19 +924,10 @@ hipError_t launch_query_out(int dt, int norm, const void* Q, void* Out, const fl
 // each of those would run a few waves per head and wait on its own latency chains (the
 // DeiT-small shape: 197 tokens, 32 landmarks).
 //
-// L1 distances in fixed point.  Every kernel value of the head -- K_LL, B and A of Eqs. (5)-(6) --
-// is exp(-||x - y||_1 / lambda) with x, y rows of Q, K or their landmark means, all of magnitude
-// at most R = max |x| over the head's Q and K (a mean lies within its tokens).  With s = 2^(22 -
-// e), R < 2^e, each coordinate is coded as the bits of fmaf(x, s, 1.5 2^23): for |x s| <= 2^22
-// that float lies in [2^23, 2^24], where consecutive floats are the consecutive integers, so the
-// bits are 0x4B000000 + 2^22 + round(x s) and the difference of two codes is the difference of
-// the rounded scaled coordinates.  One v_sad_u32 per coordinate then adds |x_c - y_c| s exactly
-// (a row's sum stays below D 2^23 <= 2^29).  The rounding moves a coordinate by at most 2^-(23 -
-// e) <= R 2^-22, a distance by at most D times that (typically ~3 times); the fp32 sums they
-// replace carry errors of the same order.  Because all three matrices use the same codes and the
-// same exponential, a query equal to a landmark mean gives exactly that row of K_LL (m = n
-// reproduces dense attention through X = W^-1).  A non-finite value in Q or K makes every output
-// of the head NaN.
+// L1 distances in fixed point (fcode, common.hpp): K_LL (Eq. (9)), B and A (Eq. (8)) are all
+// formed from the head's codes with one v_sad_u32 per coordinate and the same exponential, so a
+// query equal to a landmark mean gives exactly that row of K_LL (m = n reproduces dense attention
+// through X = W^-1).  A non-finite value in Q or K makes every output of the head NaN.
 //
 // Steps:
 //   pool     thread (landmark a = t / 8, columns (t % 8) D/8 ..): the landmark means in fp64,
@@ -952,19 +943,6 @@ hipError_t launch_query_out(int dt, int norm, const void* Q, void* Out, const fl
 //   query    thread t: queries t % 128, t % 128 + 128 against half t / 128 of the landmarks, A
 //            into a [256][33] tile (and the two halves of s_i for the row sums); then
 //            Y = A M on fp32 MFMA, normalised (Eq. (4) / Eq. (3)) and stored.
-
-// |x - y| + acc on unsigned 32-bit integers (v_sad_u32).
-__device__ __forceinline__ uint32_t sad32(uint32_t x, uint32_t y, uint32_t acc) {
-    uint32_t r;
-    asm("v_sad_u32 %0, %1, %2, %3" : "=v"(r) : "v"(x), "v"(y), "v"(acc));
-    return r;
-}
-// Code of x on the grid 1/s (the comment above).
-__device__ __forceinline__ uint32_t sf_code(float x, float s) { return __float_as_uint(fmaf(x, s, 12582912.f)); }
-// Kernel value from a coded distance: exp2(dist * kss), kss = -log2(e) / (lambda s).
-__device__ __forceinline__ float sf_kval(uint32_t dist, float kss) {
-    return __builtin_amdgcn_exp2f((float)dist * kss);
-}
 
 // Coded L1 distances of two tokens (codes x0, x1) to rows 0 .. na - 1 of an LDS code table
 // (pitch LP words); emit(aa, dist0, dist1) per row.  The rows are read as half rows of D / 8
@@ -1099,19 +1077,13 @@ __global__ __launch_bounds__(256, 2) void small_forward_kernel(const float* __re
     const float R = fmaxf(fmaxf(smx[0], smx[1]), fmaxf(smx[2], smx[3]));
     const bool nan_head = !(R <= 3.4028234663852886e38f);
     float s, kss;
-    {
-        int e = 0;
-        (void)frexpf(nan_head ? 1.f : R, &e);   // R < 2^e (e = 0 for R = 0)
-        e = max(e, -100);                         // tiny R: a coarser grid, distances below 2^-100
-        s = __uint_as_float((uint32_t)(127 + 22 - e) << 23);
-        kss = (float)(-1.4426950408889634 / lambda) * __uint_as_float((uint32_t)(127 - 22 + e) << 23);
-    }
+    fgrid(nan_head ? 1.f : R, (float)(-1.4426950408889634 / lambda), s, kss);
     {
         const int a = tid >> 3, c0 = (tid & 7) * CPT;
 #pragma unroll
         for (int c = 0; c < CPT; ++c) {
-            sQc[a * LP + c0 + c] = sf_code(qm[c], s);
-            sKc[a * LP + c0 + c] = sf_code(km[c], s);
+            sQc[a * LP + c0 + c] = fcode(qm[c], s);
+            sKc[a * LP + c0 + c] = fcode(km[c], s);
         }
     }
     __syncthreads();
@@ -1140,7 +1112,7 @@ __global__ __launch_bounds__(256, 2) void small_forward_kernel(const float* __re
             const int b = b0 + bb;
             float wv = 0.f;
             if (a < m && b < m) {
-                wv = sf_kval(u[bb], kss);
+                wv = fkval(u[bb], kss);
                 if (a == b) wv = (float)((double)wv + eps);
             }
             sW[a * P + b] = wv;
@@ -1164,18 +1136,18 @@ __global__ __launch_bounds__(256, 2) void small_forward_kernel(const float* __re
 #pragma unroll
             for (int c4 = 0; c4 < D / 4; ++c4) {
                 const float4 v0 = r0[c4], v1 = r1[c4];
-                x0[4 * c4] = sf_code(v0.x, s); x0[4 * c4 + 1] = sf_code(v0.y, s);
-                x0[4 * c4 + 2] = sf_code(v0.z, s); x0[4 * c4 + 3] = sf_code(v0.w, s);
-                x1[4 * c4] = sf_code(v1.x, s); x1[4 * c4 + 1] = sf_code(v1.y, s);
-                x1[4 * c4 + 2] = sf_code(v1.z, s); x1[4 * c4 + 3] = sf_code(v1.w, s);
+                x0[4 * c4] = fcode(v0.x, s); x0[4 * c4 + 1] = fcode(v0.y, s);
+                x0[4 * c4 + 2] = fcode(v0.z, s); x0[4 * c4 + 3] = fcode(v0.w, s);
+                x1[4 * c4] = fcode(v1.x, s); x1[4 * c4 + 1] = fcode(v1.y, s);
+                x1[4 * c4 + 2] = fcode(v1.z, s); x1[4 * c4 + 3] = fcode(v1.w, s);
             }
         }
         const bool live0 = t0 < n, live1 = t0 + 128 < n;
         const int na = __builtin_amdgcn_readfirstlane(min(max(m - 16 * hf, 0), 16));
         sf_dist2<D, LP>(sQc + 16 * hf * LP, na, x0, x1, [&](int aa, uint32_t d0, uint32_t d1) {
             const int a = 16 * hf + aa;
-            sB[a * BP + t0] = live0 ? sf_kval(d0, kss) : 0.f;
-            sB[a * BP + t0 + 128] = live1 ? sf_kval(d1, kss) : 0.f;
+            sB[a * BP + t0] = live0 ? fkval(d0, kss) : 0.f;
+            sB[a * BP + t0 + 128] = live1 ? fkval(d1, kss) : 0.f;
         });
         for (int a = 16 * hf + na; a < 16 * hf + 16; ++a) {   // landmarks past m
             sB[a * BP + t0] = 0.f;
@@ -1296,10 +1268,10 @@ __global__ __launch_bounds__(256, 2) void small_forward_kernel(const float* __re
 #pragma unroll
             for (int c4 = 0; c4 < D / 4; ++c4) {
                 const float4 v0 = r0[c4], v1 = r1[c4];
-                x0[4 * c4] = sf_code(v0.x, s); x0[4 * c4 + 1] = sf_code(v0.y, s);
-                x0[4 * c4 + 2] = sf_code(v0.z, s); x0[4 * c4 + 3] = sf_code(v0.w, s);
-                x1[4 * c4] = sf_code(v1.x, s); x1[4 * c4 + 1] = sf_code(v1.y, s);
-                x1[4 * c4 + 2] = sf_code(v1.z, s); x1[4 * c4 + 3] = sf_code(v1.w, s);
+                x0[4 * c4] = fcode(v0.x, s); x0[4 * c4 + 1] = fcode(v0.y, s);
+                x0[4 * c4 + 2] = fcode(v0.z, s); x0[4 * c4 + 3] = fcode(v0.w, s);
+                x1[4 * c4] = fcode(v1.x, s); x1[4 * c4 + 1] = fcode(v1.y, s);
+                x1[4 * c4 + 2] = fcode(v1.z, s); x1[4 * c4 + 3] = fcode(v1.w, s);
             }
         }
         const bool live0 = t0 < n, live1 = t0 + 128 < n;
@@ -1307,8 +1279,8 @@ __global__ __launch_bounds__(256, 2) void small_forward_kernel(const float* __re
         const int na = __builtin_amdgcn_readfirstlane(min(max(m - 16 * hf, 0), 16));
         sf_dist2<D, LP>(sKc + 16 * hf * LP, na, x0, x1, [&](int aa, uint32_t d0, uint32_t d1) {
             const int a = 16 * hf + aa;
-            const float a0 = live0 ? sf_kval(d0, kss) : 0.f;
-            const float a1 = live1 ? sf_kval(d1, kss) : 0.f;
+            const float a0 = live0 ? fkval(d0, kss) : 0.f;
+            const float a1 = live1 ? fkval(d1, kss) : 0.f;
             if (NORM == NORM_ROWSUM) {
                 sr0 = fmaf(a0, sM1[a], sr0);
                 sr1 = fmaf(a1, sM1[a], sr1);

@@ -44,13 +44,14 @@ hipError_t launch_ns_solve(const float* qt, const float* kt, const float* Upart,
 // The landmark-space normalisation takes the whitening [H][m] (NULL: ones) and mvec below.
 // With Asave, also the rows A[i][l] = k(q_i, kt_l) for the backward, group-major ([BH][G][n][64],
 // columns below m).
+hipError_t launch_query_out(int dt, int norm, const void* Q, void* Out, const float* kt, const float* M,
+                            const float* Mc, const float* vbar, const float* extra, const float* whiten, const float* mvec,
+                            float* Asave, int BH, int H, int n, int d, int m, float lambda, hipStream_t st);
+
 // Small heads (fp32, n <= 256, m <= 32, d 32 or 64; norm inline, row sums or none): the whole
 // forward of a head in one workgroup, Out [BH][n][d]; no workspace.
 hipError_t launch_small_forward(int norm, const float* Q, const float* K, const float* V, float* Out, int BH, int n,
                                 int d, int m, float lambda, int T, float eps, LmPool pl, hipStream_t st);
-hipError_t launch_query_out(int dt, int norm, const void* Q, void* Out, const float* kt, const float* M,
-                            const float* Mc, const float* vbar, const float* extra, const float* whiten, const float* mvec,
-                            float* Asave, int BH, int H, int n, int d, int m, float lambda, hipStream_t st);
 
 // The same for 64 < m <= 128 (nsbig.hip), products spread over many workgroups:
 //   Xs:    [BH][T+2][128][128] fp64: X_0 .. X_T, then W (always all of them)

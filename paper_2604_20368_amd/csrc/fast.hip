@@ -96,8 +96,9 @@ __device__ __forceinline__ int xcd_rank(int i, int n, int base) {
 // reads the 8-column group t % (D/8) of its rows (the landmark's tokens t / (D/8) + (256 / (D/8)) i
 // of its segment or window, lm_tokens), four rows per thread in flight at a time.  Sums: per thread in fp32, then over the
 // lanes of a wave that share a column group (a butterfly), then over the four waves in a fixed
-// order in fp64.
-template <int D>
+// order in fp64.  RV = false (the key side with the landmarks split over its waves, which forms
+// the value statistics itself): Q and K only, vseg and vsegmax untouched.
+template <int D, bool RV>
 __global__ __launch_bounds__(256) void pool2_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
                                                     const uint16_t* __restrict__ V, float* __restrict__ qt,
                                                     float* __restrict__ kt, double* __restrict__ vseg,
@@ -124,7 +125,7 @@ __global__ __launch_bounds__(256) void pool2_kernel(const uint16_t* __restrict__
                 const size_t off = base + (size_t)tok(t) * D;
                 a[u] = *reinterpret_cast<const uint4*>(Q + off);
                 b[u] = *reinterpret_cast<const uint4*>(K + off);
-                c[u] = *reinterpret_cast<const uint4*>(V + off);
+                c[u] = RV ? *reinterpret_cast<const uint4*>(V + off) : make_uint4(0u, 0u, 0u, 0u);
             } else {
                 a[u] = b[u] = c[u] = make_uint4(0u, 0u, 0u, 0u);   // +0: no effect on sums or maxima
             }
@@ -140,9 +141,11 @@ __global__ __launch_bounds__(256) void pool2_kernel(const uint16_t* __restrict__
                 const float v0 = bf16_lo(cw[j]), v1 = bf16_hi(cw[j]);
                 sq[2 * j] += q0; sq[2 * j + 1] += q1;
                 sk[2 * j] += k0; sk[2 * j + 1] += k1;
-                sv[2 * j] += v0; sv[2 * j + 1] += v1;
                 mx = fmaxf(fmaxf(mx, fabsf(q0)), fmaxf(fabsf(q1), fmaxf(fabsf(k0), fabsf(k1))));
-                vmx = fmaxf(vmx, fmaxf(fabsf(v0), fabsf(v1)));
+                if (RV) {
+                    sv[2 * j] += v0; sv[2 * j + 1] += v1;
+                    vmx = fmaxf(vmx, fmaxf(fabsf(v0), fabsf(v1)));
+                }
             }
         }
     }
@@ -150,7 +153,7 @@ __global__ __launch_bounds__(256) void pool2_kernel(const uint16_t* __restrict__
     // other lane bits by a butterfly; lane cg's result (always the same order) is the one kept.
     float* sums[3] = {sq, sk, sv};
 #pragma unroll
-    for (int a3 = 0; a3 < 3; ++a3)
+    for (int a3 = 0; a3 < (RV ? 3 : 2); ++a3)
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
             float v = sums[a3][j];
@@ -169,7 +172,7 @@ __global__ __launch_bounds__(256) void pool2_kernel(const uint16_t* __restrict__
         for (int j = 0; j < 8; ++j) {
             red[0][w][lane * 8 + j] = (double)sq[j];
             red[1][w][lane * 8 + j] = (double)sk[j];
-            red[2][w][lane * 8 + j] = (double)sv[j];
+            if (RV) red[2][w][lane * 8 + j] = (double)sv[j];
         }
     }
     if (lane == 0) {
@@ -179,7 +182,7 @@ __global__ __launch_bounds__(256) void pool2_kernel(const uint16_t* __restrict__
     __syncthreads();
     const double cnt = (double)cntl;
     bool bad = false;
-    if (tid < 3 * D) {
+    if (tid < (RV ? 3 : 2) * D) {
         const int a3 = tid / D, col = tid % D;
         const double t = ((red[a3][0][col] + red[a3][1][col]) + red[a3][2][col]) + red[a3][3][col];
         const size_t o = ((size_t)h * m + l) * D + col;
@@ -194,7 +197,7 @@ __global__ __launch_bounds__(256) void pool2_kernel(const uint16_t* __restrict__
         const float a = fmaxf(fmaxf(smx[0], smx[1]), fmaxf(smx[2], smx[3]));
         const float b = fmaxf(fmaxf(svmx[0], svmx[1]), fmaxf(svmx[2], svmx[3]));
         segmax[(size_t)h * m + l] = anybad ? __builtin_nanf("") : a;
-        vsegmax[(size_t)h * m + l] = anybad ? __builtin_nanf("") : b;
+        if (RV) vsegmax[(size_t)h * m + l] = anybad ? __builtin_nanf("") : b;
     }
 }
 
@@ -354,7 +357,8 @@ __device__ __forceinline__ void wave_argmax_dpp(float& v, int& idx) {
 }
 
 // SOLVE = false: the frame and the code tables only (the solve then runs beside the key side,
-// ns_role in key2_kernel).
+// ns_role in key2_kernel, whose key blocks also form the value statistics: vseg, vsegmax, vbar
+// and vscale are then neither read nor written, and R reflects Q and K only).
 template <int D, bool SOLVE>
 __global__ __launch_bounds__(kSolveThreads) void frame_ns_kernel(
     const float* __restrict__ qt, const float* __restrict__ kt, const double* __restrict__ vseg,
@@ -403,7 +407,7 @@ __global__ __launch_bounds__(kSolveThreads) void frame_ns_kernel(
         q0[r] = qt[o]; q1[r] = qt[o + 1]; k0[r] = kt[o]; k1[r] = kt[o + 1];
     }
     double vs = 0.0;
-    {
+    if (SOLVE) {
         // all loads issued before the first add (landmarks past m read row 0 and are dropped)
         const int c = tid % D, g = tid / D;
         double vv[LPG];
@@ -416,7 +420,7 @@ __global__ __launch_bounds__(kSolveThreads) void frame_ns_kernel(
         for (int i = 0; i < LPG; ++i) vs += g * LPG + i < m ? vv[i] : 0.0;
     }
     const int tm = tid < m ? tid : 0;
-    float sa = segmax[(size_t)h * m + tm], sb = vsegmax[(size_t)h * m + tm];
+    float sa = segmax[(size_t)h * m + tm], sb = SOLVE ? vsegmax[(size_t)h * m + tm] : 0.f;
     if (tid >= m) sa = sb = 0.f;
     vpart[tid] = vs;   // [g][c]
     {
@@ -466,7 +470,7 @@ __global__ __launch_bounds__(kSolveThreads) void frame_ns_kernel(
         }
     }
     __syncthreads();
-    if (tid < D) {
+    if (SOLVE && tid < D) {
         double t = 0.0;
 #pragma unroll
         for (int g = 0; g < G; ++g) t += vpart[g * D + tid];
@@ -1067,6 +1071,7 @@ __device__ void ns_role(int h, char* lds, const uint32_t* __restrict__ qfix, con
 // Writes Upart[h][kb][c][a] as key_kernel does.
 // The first nns blocks of the launch solve Newton-Schulz for heads 0 .. nns - 1 (ns_role) while
 // the key blocks run: mfinal_kernel, the next launch, is the first to need X_T.
+typedef unsigned short u16x2_t __attribute__((ext_vector_type(2)));
 constexpr int kK2Keys = 128;
 constexpr int kK2VP = kK2Keys + 8;   // pitch (halves) of the [c][j] value and [a][j] kernel-value tiles
 
@@ -1076,8 +1081,8 @@ struct K2Lds {
     static constexpr int C_BYTES = kK2Keys * CP * 4;
     static constexpr int V_BYTES = D * kK2VP * 2;
     static constexpr int B_BYTES = 4 * 16 * kK2VP * 2;
-    static constexpr int KEY = C_BYTES + V_BYTES + B_BYTES;
-    static constexpr int BYTES = KEY > kNsRoleLds ? KEY : kNsRoleLds;
+    static constexpr int KEY = C_BYTES + V_BYTES + B_BYTES;   // then the four quarters' exponents (16 bytes)
+    static constexpr int BYTES = KEY + 16 > kNsRoleLds ? KEY + 16 : kNsRoleLds;
 };
 
 template <int D>
@@ -1086,7 +1091,8 @@ __global__ __launch_bounds__(256, D == 32 ? 4 : 3) void key2_kernel(const uint16
                                                                     const uint32_t* __restrict__ qfix,
                                                                     const uint32_t* __restrict__ kfix,
                                                                     float* __restrict__ frame,
-                                                                    float* __restrict__ Upart, float* __restrict__ XT,
+                                                                    float* __restrict__ Upart,
+                                                                    float* __restrict__ vpart, float* __restrict__ XT,
                                                                     float* __restrict__ cinfo,
                                                                     uint32_t* __restrict__ kcen, int BH, int n, int m,
                                                                     int ntile, int nkb, int T, float eps, int nns) {
@@ -1108,7 +1114,7 @@ __global__ __launch_bounds__(256, D == 32 ? 4 : 3) void key2_kernel(const uint16
     const int kbb = xcd_rank((int)blockIdx.x - nns, nblk, nns);
     const int h = kbb / nkb, kb = kbb % nkb;
     const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
-    const float inv2R = frame[h * 8 + 1], esc = frame[h * 8 + 2], vsc = frame[h * 8 + 3];
+    const float inv2R = frame[h * 8 + 1], esc = frame[h * 8 + 2];
     const float R = frame[h * 8 + 0], xsc = frame[h * 8 + 4];
     const bool clamped = __float_as_uint(frame[h * 8 + 5]) != 0u;   // integer test: a scalar branch
     const float ebias = -kTwo23 * esc;
@@ -1121,26 +1127,68 @@ __global__ __launch_bounds__(256, D == 32 ? 4 : 3) void key2_kernel(const uint16
     h8_t ones;   // B operand of the ones column: 1 in column 0
 #pragma unroll
     for (int i = 0; i < 8; ++i) ones[i] = (l & 15) == 0 ? (_Float16)1.f : (_Float16)0.f;
+    // Value statistics.  The fp16 copies of wave q's quarter of the value columns carry a
+    // power-of-two scale 2^sig[q], the running minimum over the tiles so far of the exponent that
+    // puts the tile quarter's largest |v| in [2^13, 2^14) (so no copy overflows and a quarter's
+    // large values keep fp16's precision); acc of a column is rescaled exactly when its quarter's
+    // exponent drops.  Wave w < C16 also sums the value columns 16w .. 16w + 15 over the keys
+    // (a row of ones as the A operand against the staged values), for vbar.
+    constexpr int QC = D / 4;   // value columns per quarter
+    int sig[4] = {100, 100, 100, 100};   // running exponents of the four quarters (wave-uniform)
+    int sigw = 100;                      // this wave's quarter's
+    int* const ssig = reinterpret_cast<int*>(lds + K2Lds<D>::KEY);
+    float vsum = 0.f;   // wave w < C16, lane l < 16: the sum of value column 16w + l so far
+    const int wu = __builtin_amdgcn_readfirstlane(w);
 
-    // raw quarters of the lane's two key and value rows (keys past n keep the last values
-    // loaded, finite values of this head: their kernel values are exactly 0)
+    // raw quarters of the lane's two key and value rows (keys past n keep the last key rows
+    // loaded, finite values of this head whose kernel values are exactly 0; their value rows are
+    // zero, for the value sums)
     uint4 kq[2][QW] = {}, vq[2][QW] = {};
+    // the head's rows from wave-uniform bases and a 32-bit lane offset (no 64-bit address per
+    // lane to keep live through the loop)
+    const uint4* const kh4 = reinterpret_cast<const uint4*>(K + (size_t)h * n * D);
+    const uint4* const vh4 = reinterpret_cast<const uint4*>(V + (size_t)h * n * D);
     auto fetch = [&](int tile) {
 #pragma unroll
         for (int s2 = 0; s2 < 2; ++s2) {
             const int j = tile * kK2Keys + 64 * s2 + l;
             if (j < n) {
-                const uint4* kp = reinterpret_cast<const uint4*>(K + ((size_t)h * n + j) * D) + QW * w;
-                const uint4* vp = reinterpret_cast<const uint4*>(V + ((size_t)h * n + j) * D) + QW * w;
+                const uint32_t o = (uint32_t)j * (uint32_t)D8 + (uint32_t)(QW * w);
 #pragma unroll
-                for (int i = 0; i < QW; ++i) kq[s2][i] = kp[i];
+                for (int i = 0; i < QW; ++i) kq[s2][i] = kh4[o + i];
 #pragma unroll
-                for (int i = 0; i < QW; ++i) vq[s2][i] = vp[i];
+                for (int i = 0; i < QW; ++i) vq[s2][i] = vh4[o + i];
+            } else {
+#pragma unroll
+                for (int i = 0; i < QW; ++i) vq[s2][i] = make_uint4(0u, 0u, 0u, 0u);
             }
         }
     };
     if (t0 < t1) fetch(t0);
     for (int tile = t0; tile < t1; ++tile) {
+        // this wave's quarter: the largest exponent field of its values in the tile, its running
+        // exponent, shared with the other waves through LDS
+        {
+            // |v| of a bf16 value orders as its low 15 bits: a packed 16-bit maximum of the
+            // magnitudes, one instruction per two values
+            u16x2_t e2 = {0, 0};
+#pragma unroll
+            for (int s2 = 0; s2 < 2; ++s2)
+#pragma unroll
+                for (int i = 0; i < QW; ++i) {
+                    const uint32_t wd[4] = {vq[s2][i].x, vq[s2][i].y, vq[s2][i].z, vq[s2][i].w};
+#pragma unroll
+                    for (int t = 0; t < 4; ++t)
+                        e2 = __builtin_elementwise_max(e2, __builtin_bit_cast(u16x2_t, wd[t] & 0x7fff7fffu));
+                }
+            // the wave's maximum by DPP (integer compares of the bits, wave_max_dpp)
+            const int em = __float_as_int(wave_max_dpp(__int_as_float((int)max((uint32_t)e2[0], (uint32_t)e2[1]))));
+            const int E = em >> 7;   // biased exponent of the largest |v| (0: zero or subnormal)
+            const int st = E == 0 ? 100 : max(140 - E, -115);
+            sigw = min(sigw, st);
+            if (l == 0) ssig[w] = sigw;
+        }
+        const float vsc = __uint_as_float((uint32_t)(127 + sigw) << 23);
         // staging: this wave's quarter of the codes and of the value columns of the 128 keys
 #pragma unroll
         for (int s2 = 0; s2 < 2; ++s2) {
@@ -1223,11 +1271,36 @@ __global__ __launch_bounds__(256, D == 32 ? 4 : 3) void key2_kernel(const uint16
                 bw[(2 * p + 1) * VP + 64 + l] = (uint16_t)(v1 >> 16);
             }
         }
+        {
+            // quarters whose exponent dropped (scalar branches, rare after a block's first tile):
+            // their accumulated columns to the new scale (exact); the first tile starts from zero
+            int sn[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) sn[q] = __builtin_amdgcn_readfirstlane(ssig[q]);
+            if (tile > t0) {
+#pragma unroll
+                for (int cc = 0; cc < C16; ++cc) {
+                    const int qa = (16 * cc) / QC, qb = (16 * cc + 15) / QC;   // the column tile's quarters
+                    const int sa = qa == 0 ? sig[0] : qa == 1 ? sig[1] : qa == 2 ? sig[2] : sig[3];
+                    const int sb = qb == 0 ? sig[0] : qb == 1 ? sig[1] : qb == 2 ? sig[2] : sig[3];
+                    const int na = qa == 0 ? sn[0] : qa == 1 ? sn[1] : qa == 2 ? sn[2] : sn[3];
+                    const int nb = qb == 0 ? sn[0] : qb == 1 ? sn[1] : qb == 2 ? sn[2] : sn[3];
+                    if (na != sa || nb != sb) {
+                        const float f = ldexpf(1.f, ((16 * cc + (l & 15)) / QC == qa) ? na - sa : nb - sb);
+                        acc[cc] *= f;
+                        if (cc == wu) vsum *= f;
+                    }
+                }
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) sig[q] = sn[q];
+        }
         // the wave's LDS requests complete in order; the barrier keeps the compiler from moving
         // the reads of other lanes' values above the writes
         __builtin_amdgcn_wave_barrier();
         {
             const int ao = (l & 15) * VP + 8 * (l >> 4);
+            f32x4_t accv = (f32x4_t){0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int s4 = 0; s4 < 4; ++s4) {
                 const h8_t A = *reinterpret_cast<const h8_t*>(brow + ao + 32 * s4);
@@ -1235,20 +1308,31 @@ __global__ __launch_bounds__(256, D == 32 ? 4 : 3) void key2_kernel(const uint16
                 for (int cc = 0; cc < C16; ++cc) {
                     const h8_t Bv = *reinterpret_cast<const h8_t*>(sV + 16 * cc * VP + ao + 32 * s4);
                     acc[cc] = __builtin_amdgcn_mfma_f32_16x16x32_f16(A, Bv, acc[cc], 0, 0, 0);
+                    // the value sums of column tile w: `ones` as the A operand is a row 0 of ones
+                    // (held by the lanes with l % 16 = 0), so row 0 of the product sums the tile's
+                    // keys.  A scalar branch: a matrix instruction under a zero lane mask would
+                    // still write accv.
+                    if (cc == wu) accv = __builtin_amdgcn_mfma_f32_16x16x32_f16(ones, Bv, accv, 0, 0, 0);
                 }
                 acc[C16] = __builtin_amdgcn_mfma_f32_16x16x32_f16(A, ones, acc[C16], 0, 0, 0);
             }
+            vsum += accv[0];   // row 0 (lanes l < 16: column 16w + l)
         }
         __syncthreads();   // every wave is done with the codes and values before the next staging
     }
     // rows a = 16w + 4(l/16) + r, column 16cc + l%16 (the value columns were formed from
-    // V * vscale); the ones column from column 0 of its block
-    const float inv_vsc = 1.f / vsc;
+    // V 2^sig of their quarter); the ones column from column 0 of its block; the value sums of
+    // wave w < C16 from row 0 (lanes l < 16, column 16w + l)
     float* dst = Upart + ((size_t)h * nkb + kb) * (D + 1) * 64;
 #pragma unroll
-    for (int cc = 0; cc < C16; ++cc)
+    for (int cc = 0; cc < C16; ++cc) {
+        const int q = (16 * cc + (l & 15)) / QC;
+        const int sq = q == 0 ? sig[0] : q == 1 ? sig[1] : q == 2 ? sig[2] : sig[3];
+        const float inv = ldexpf(1.f, -sq);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) dst[(16 * cc + (l & 15)) * 64 + 16 * w + 4 * (l >> 4) + r] = acc[cc][r] * inv_vsc;
+        for (int r = 0; r < 4; ++r) dst[(16 * cc + (l & 15)) * 64 + 16 * w + 4 * (l >> 4) + r] = acc[cc][r] * inv;
+        if (cc == wu && l < 16) vpart[((size_t)h * nkb + kb) * D + 16 * cc + l] = vsum * inv;
+    }
     if ((l & 15) == 0) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) dst[D * 64 + 16 * w + 4 * (l >> 4) + r] = acc[C16][r];
@@ -1269,6 +1353,10 @@ __global__ __launch_bounds__(256, D == 32 ? 4 : 3) void key2_kernel(const uint16
 // Value columns: fp16 MFMA operand tiles Mt[h][s][cb][lane][i] = M[16s + 8(lane/32) + i]
 // [32cb + lane%32] * 2^-e_g with mscale[h][g] = 2^e_g putting the group's largest magnitude in
 // [2^14, 2^15).  Ones column: Mones[h][a] = M[a][D] in fp32.
+// With vpart given (m > 48: the key blocks' value sums, [h][kb][d]), each value group forms vbar
+// for its columns (the sums over the key blocks in order, in fp64, over n) and writes it for the
+// query side; a non-finite sum (a NaN or infinite value) makes vbar and the frame's R NaN, so that
+// every output of the head is NaN.  Otherwise vbar is read.
 // With kfix given (m <= 48; for m > 48 the solve blocks of key2_kernel form it), the ones group
 // also forms the query side's row bound from the key-landmark codes kfix[h]:
 // kcen[h][c/2] = their centre (per coordinate, the rounded mean over the m landmarks) and
@@ -1284,7 +1372,8 @@ __global__ __launch_bounds__(kMfinalThreads) void mfinal_kernel(const float* __r
                                                                 float* __restrict__ Mones, float* __restrict__ Mout,
                                                                 int m, int nkb, const float* __restrict__ whiten,
                                                                 int mspace, int H, float* __restrict__ mvec,
-                                                                const float* __restrict__ vbar, int center,
+                                                                float* __restrict__ vbar,
+                                                                const float* __restrict__ vpart, int n, int center,
                                                                 const uint32_t* __restrict__ kfix,
                                                                 uint32_t* __restrict__ kcen,
                                                                 float* __restrict__ frame) {
@@ -1299,9 +1388,40 @@ __global__ __launch_bounds__(kMfinalThreads) void mfinal_kernel(const float* __r
     __shared__ __attribute__((aligned(16))) float4 red[3 * NI];
     __shared__ uint32_t scen[D2];
     __shared__ float smx[8];
+    __shared__ float svb[8];
     const int g = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, w = tid / 64, l = tid & 63;
     const bool ones = g == NG - 1;
     const int c0 = 8 * g, nc = ones ? 1 : 8;   // operand columns of this group
+    if (!ones && w == 0) {
+        // lane (column l % 8, part l / 8): the key blocks k = part, part + 8, ... (the first
+        // eight loads issued together), then the eight parts by a butterfly (the same order in
+        // every lane)
+        if (vpart) {
+            const int col = l & 7, part = l >> 3;
+            const float* src = vpart + (size_t)h * nkb * D + c0 + col;
+            double t = 0.0;
+            float a[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) a[i] = part + 8 * i < nkb ? src[(size_t)(part + 8 * i) * D] : 0.f;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) t += (double)a[i];
+            for (int k = part + 64; k < nkb; k += 8) t += (double)src[(size_t)k * D];
+            t += __shfl_xor(t, 8, 64);
+            t += __shfl_xor(t, 16, 64);
+            t += __shfl_xor(t, 32, 64);
+            if (l < 8) {
+                float vb = (float)(t / n);
+                if (!isfinite(vb)) {   // a non-finite value: every output of the head NaN
+                    vb = __builtin_nanf("");
+                    frame[h * 8 + 0] = vb;   // R, read by the query side
+                }
+                vbar[(size_t)h * D + c0 + l] = vb;
+                svb[l] = vb;
+            }
+        } else if (l < 8) {
+            svb[l] = vbar[(size_t)h * D + c0 + l];
+        }
+    }
     const int ncol = ones ? 1 : (center ? 9 : 8);   // columns summed: the operand columns and column D
     // item f: local column f / 16 (column D for local column 8, and in the ones group), rows
     // 4 (f % 16) .. +3 of every chunk partial; the chunks in four quarters, eight loads in flight
@@ -1364,7 +1484,7 @@ __global__ __launch_bounds__(kMfinalThreads) void mfinal_kernel(const float* __r
     float t = 0.f;
     if (w < nc) {
         if (center && !ones) {
-            const float vb = vbar[(size_t)h * D + c0 + w];
+            const float vb = svb[w];
 #pragma unroll 16
             for (int b = 0; b < 64; ++b) t = fmaf(sX[l * 65 + b], fmaf(-sU[8 * 64 + b], vb, sU[w * 64 + b]), t);
         } else {
@@ -1781,12 +1901,15 @@ __global__ __launch_bounds__(256) void query2_kernel(const uint16_t* __restrict_
 hipError_t launch_fast_pool(const void* Q, const void* K, const void* V, float* qt, float* kt, double* vseg,
                             float* segmax, float* vsegmax, int BH, int n, int d, int m, LmPool pl, hipStream_t st) {
     dim3 grid(m, BH);
-    if (d == 32)
-        hipLaunchKernelGGL(pool2_kernel<32>, grid, dim3(256), 0, st, (const uint16_t*)Q, (const uint16_t*)K,
-                           (const uint16_t*)V, qt, kt, vseg, segmax, vsegmax, n, m, pl);
-    else
-        hipLaunchKernelGGL(pool2_kernel<64>, grid, dim3(256), 0, st, (const uint16_t*)Q, (const uint16_t*)K,
-                           (const uint16_t*)V, qt, kt, vseg, segmax, vsegmax, n, m, pl);
+    // m > 48: the key side (key2_kernel) forms the value statistics, V is not read here
+#define LAPATTN_P2(Dv, RVv)                                                                            \
+    hipLaunchKernelGGL((pool2_kernel<Dv, RVv>), grid, dim3(256), 0, st, (const uint16_t*)Q, (const uint16_t*)K, \
+                       (const uint16_t*)V, qt, kt, vseg, segmax, vsegmax, n, m, pl)
+    if (d == 32 && m > 48) LAPATTN_P2(32, false);
+    else if (d == 32) LAPATTN_P2(32, true);
+    else if (m > 48) LAPATTN_P2(64, false);
+    else LAPATTN_P2(64, true);
+#undef LAPATTN_P2
     return hipGetLastError();
 }
 
@@ -1811,15 +1934,15 @@ hipError_t launch_fast_frame_ns(const float* qt, const float* kt, const double* 
 }
 
 hipError_t launch_fast_key2(const void* K, const void* V, const uint32_t* qfix, const uint32_t* kfix,
-                            float* frame, float* Upart, float* XT, float* cinfo, uint32_t* kcen, int BH, int n, int d,
-                            int m, int ntile, int nkb, int T, float eps, hipStream_t st) {
+                            float* frame, float* Upart, float* vpart, float* XT, float* cinfo, uint32_t* kcen, int BH,
+                            int n, int d, int m, int ntile, int nkb, int T, float eps, hipStream_t st) {
     dim3 grid(BH + BH * nkb);   // BH solve blocks first, then the key blocks
     if (d == 32)
         hipLaunchKernelGGL(key2_kernel<32>, grid, dim3(256), 0, st, (const uint16_t*)K, (const uint16_t*)V, qfix, kfix,
-                           frame, Upart, XT, cinfo, kcen, BH, n, m, ntile, nkb, T, eps, BH);
+                           frame, Upart, vpart, XT, cinfo, kcen, BH, n, m, ntile, nkb, T, eps, BH);
     else
         hipLaunchKernelGGL(key2_kernel<64>, grid, dim3(256), 0, st, (const uint16_t*)K, (const uint16_t*)V, qfix, kfix,
-                           frame, Upart, XT, cinfo, kcen, BH, n, m, ntile, nkb, T, eps, BH);
+                           frame, Upart, vpart, XT, cinfo, kcen, BH, n, m, ntile, nkb, T, eps, BH);
     return hipGetLastError();
 }
 
@@ -1837,14 +1960,14 @@ hipError_t launch_fast_key(const void* K, const void* V, const uint32_t* qfix, c
 
 hipError_t launch_fast_mfinal(const float* Upart, const float* XT, _Float16* Mt, float* mscale, float* Mones,
                               float* M, int BH, int d, int m, int nkb, const float* whiten, int mspace, int H,
-                              float* mvec, const float* vbar, int center, const uint32_t* kfix, uint32_t* kcen,
-                              float* frame, hipStream_t st) {
+                              float* mvec, float* vbar, const float* vpart, int n, int center, const uint32_t* kfix,
+                              uint32_t* kcen, float* frame, hipStream_t st) {
     if (d == 32)
         hipLaunchKernelGGL(mfinal_kernel<32>, dim3(32 / 8 + 1, BH), dim3(kMfinalThreads), 0, st, Upart, XT, Mt, mscale,
-                           Mones, M, m, nkb, whiten, mspace, H, mvec, vbar, center, kfix, kcen, frame);
+                           Mones, M, m, nkb, whiten, mspace, H, mvec, vbar, vpart, n, center, kfix, kcen, frame);
     else
         hipLaunchKernelGGL(mfinal_kernel<64>, dim3(64 / 8 + 1, BH), dim3(kMfinalThreads), 0, st, Upart, XT, Mt, mscale,
-                           Mones, M, m, nkb, whiten, mspace, H, mvec, vbar, center, kfix, kcen, frame);
+                           Mones, M, m, nkb, whiten, mspace, H, mvec, vbar, vpart, n, center, kfix, kcen, frame);
     return hipGetLastError();
 }
 

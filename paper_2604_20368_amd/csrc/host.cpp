@@ -56,6 +56,7 @@ int check_align(std::initializer_list<const void*> tensors, const void* workspac
 
 struct FastPlan {
     size_t qt, kt, vseg, segmax, vsegmax, frame, qfix, kfix, kcen, vbar, XT, cinfo, Upart, Mt, mscale, Mones, M;
+    size_t vpart;  // split key side: value sums per key block [BH][nkb][d]
     size_t E;      // convolution branch: DWC(V) + bias, fp32 [BH][n][d]
     size_t mvec;   // landmark-space normalisation: [BH][2][d]
     size_t total;
@@ -226,6 +227,7 @@ FastPlan make_fast_plan(int BH, int n, int d, int m, bool dwc = false) {
     p.XT = c.take(bh * 64 * 64 * f);
     p.cinfo = c.take(bh * 4 * f);
     p.Upart = c.take(bh * p.nkb * d1 * 64 * f);   // [h][kb][c][a], 64 rows a
+    p.vpart = c.take(bh * p.nkb * (size_t)d * f);
     p.Mt = c.take(bh * 4 * ((size_t)d / 32) * 512 * 2);
     p.mscale = c.take(bh * ((size_t)d / 8 + 1) * f);
     p.Mones = c.take(bh * 64 * f);
@@ -395,7 +397,8 @@ hipError_t forward_fast(Recorder& rec, const FastPlan& p, const void* Q, const v
     e = run_named(rec, "key", [&] {
         if (p.split)
             return lapattn::launch_fast_key2(K, V, at<uint32_t>(ws, p.qfix), at<uint32_t>(ws, p.kfix),
-                                             at<float>(ws, p.frame), at<float>(ws, p.Upart), at<float>(ws, p.XT),
+                                             at<float>(ws, p.frame), at<float>(ws, p.Upart), at<float>(ws, p.vpart),
+                                             at<float>(ws, p.XT),
                                              at<float>(ws, p.cinfo), at<uint32_t>(ws, p.kcen), BH, n, d, m, p.T,
                                              p.nkb, T, eps, st);
         return lapattn::launch_fast_key(K, V, at<uint32_t>(ws, p.qfix), at<float>(ws, p.frame), at<float>(ws, p.Upart),
@@ -406,7 +409,8 @@ hipError_t forward_fast(Recorder& rec, const FastPlan& p, const void* Q, const v
         return lapattn::launch_fast_mfinal(at<float>(ws, p.Upart), at<float>(ws, p.XT), at<_Float16>(ws, p.Mt),
                                            at<float>(ws, p.mscale), at<float>(ws, p.Mones), at<float>(ws, p.M), BH, d, m,
                                            p.nkb, whiten, mspace ? 1 : 0, H, at<float>(ws, p.mvec),
-                                           at<float>(ws, p.vbar), norm == LAPATTN_NORM_INLINE ? 1 : 0,
+                                           at<float>(ws, p.vbar), p.split ? at<float>(ws, p.vpart) : nullptr, n,
+                                           norm == LAPATTN_NORM_INLINE ? 1 : 0,
                                            p.split ? nullptr : at<uint32_t>(ws, p.kfix), at<uint32_t>(ws, p.kcen),
                                            at<float>(ws, p.frame),
                                            st);

@@ -165,9 +165,11 @@ hipError_t launch_fast_frame_ns(const float* qt, const float* kt, const double* 
 // the code tables qfix, kfix (launch_fast_frame_ns writes only the frame when m > 48), and the
 // query side's row bound: kcen [BH][d/2] (centre of the key-landmark codes) and frame[h][6] (its
 // radius).
+// The key blocks also form the value statistics (pool and frame leave them out for m > 48): the
+// value sums per key block, vpart [BH][nkb][d], for launch_fast_mfinal's vbar.
 hipError_t launch_fast_key2(const void* K, const void* V, const uint32_t* qfix, const uint32_t* kfix,
-                            float* frame, float* Upart, float* XT, float* cinfo, uint32_t* kcen, int BH, int n, int d,
-                            int m, int ntile, int nkb, int T, float eps, hipStream_t st);
+                            float* frame, float* Upart, float* vpart, float* XT, float* cinfo, uint32_t* kcen, int BH,
+                            int n, int d, int m, int ntile, int nkb, int T, float eps, hipStream_t st);
 hipError_t launch_fast_key(const void* K, const void* V, const uint32_t* qfix, const float* frame, float* Upart,
                            int BH, int n, int d, int m, int kpb, int nkb, hipStream_t st);
 // mspace: the landmark-space normalisation (operand rows scaled by the whitening [H][m], NULL:
@@ -175,11 +177,12 @@ hipError_t launch_fast_key(const void* K, const void* V, const uint32_t* qfix, c
 // inline normalisation): the operand columns are M[a][c] - M[a][d] vbar[c] (vbar [BH][d]), and M's
 // value columns are not written.  With kfix (m <= 48) also the query side's row bound: kcen
 // [BH][d/2] (centre of the key-landmark codes kfix) and frame[h][6] (its radius); NULL: formed by
-// launch_fast_key2.
+// launch_fast_key2.  With vpart (m > 48), vbar is formed here from the key blocks' value sums
+// (over n tokens) and written; otherwise it is read (launch_fast_frame_ns).
 hipError_t launch_fast_mfinal(const float* Upart, const float* XT, _Float16* Mt, float* mscale, float* Mones,
                               float* M, int BH, int d, int m, int nkb, const float* whiten, int mspace, int H,
-                              float* mvec, const float* vbar, int center, const uint32_t* kfix, uint32_t* kcen,
-                              float* frame, hipStream_t st);
+                              float* mvec, float* vbar, const float* vpart, int n, int center, const uint32_t* kfix,
+                              uint32_t* kcen, float* frame, hipStream_t st);
 // Query side: Out = normalise(K_QL M) (+ extra [BH][n][d] fp32 when given); with dwc_w, the 3 x 3
 // convolution branch (filters [H][d][3][3], bias [H][d] or NULL, map width gw) formed from V in
 // the epilogue instead.

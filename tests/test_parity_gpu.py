@@ -531,6 +531,23 @@ def test_forward_bf16_heavy_tailed(L, norm):
     check_forward(L, w.with_(d=32, sigma=1 / math.sqrt(32), lam=math.sqrt(32), m=37, n=777, seed=24), norm=norm)
 
 
+@pytest.mark.parametrize("m", [32, 64])
+def test_forward_bf16_nonfinite_inputs(L, m):
+    """A NaN or an infinity in V, or a NaN in Q, of head 1 makes every output of head 1 NaN under
+    each normalisation (for m > 48 the value statistics come from the key side, m <= 48 from the
+    pooling), and head 0 keeps its parity."""
+    w = W.Workload("nonfinite", 1, 2, 1000, 64, m, 6, "bf16", 0.125, 8.0, 27, False)
+    for where, val in (("V", np.nan), ("V", np.inf), ("V", -np.inf), ("Q", np.nan)):
+        x = W.make_inputs(w, with_grad=False)
+        x[where][0, 1, 500, 7] = val
+        for norm in (0, 1, 2, 3):
+            say("non-finite %s = %s, m = %d, norm %d" % (where, val, m, norm))
+            got = run_forward(L, x, w, norm=norm)
+            assert np.isnan(got[0, 1]).all(), "head 1 must be NaN everywhere"
+            ref = oracle.forward(x["Q"][:, :1], x["K"][:, :1], x["V"][:, :1], w.m, w.lam, w.T, norm)
+            assert_parity(got[:, :1], ref, "bf16")
+
+
 @pytest.mark.parametrize("norm", [0, 1])
 def test_forward_bf16_outlier_tokens(L, norm):
     """One query row and one key row of head 0 and one value row of head 1 scaled by 2^10 (exact

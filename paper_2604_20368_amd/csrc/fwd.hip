@@ -15,72 +15,64 @@
 namespace lapattn {
 
 // ------------------------------------------------------------------------------------------
-// Landmark means.  grid (m S, BH), 256 threads: block (l, s) = (x / S, x % S) sums part s of
+// Landmark means of Q and K (the key side forms the value sums).  grid (m S, BH), 256 threads:
+// block (l, s) = (x / S, x % S) sums part s of
 // landmark l's tokens (segment or window, lm_tokens; S contiguous parts, S > 1 when m BH alone
 // would leave most compute units idle); thread (r, c) sums the part's tokens r, r + R, ... in
 // column c, four rows' loads in flight at a time, and the R partial sums are added in a fixed
-// order (deterministic).  S = 1 writes the results; otherwise part[h][l][s][3][d] (fp64) for
+// order (deterministic).  S = 1 writes the results; otherwise part[h][l][s][2][d] (fp64) for
 // pool_combine_kernel, which adds the S parts in order.
 template <int DT>
 __global__ __launch_bounds__(256) void pool_kernel(const typename elem<DT>::type* __restrict__ Q,
                                                    const typename elem<DT>::type* __restrict__ K,
-                                                   const typename elem<DT>::type* __restrict__ V,
                                                    float* __restrict__ qt, float* __restrict__ kt,
-                                                   double* __restrict__ vseg, double* __restrict__ part, int n, int d,
-                                                   int m, int S, LmPool pl) {
+                                                   double* __restrict__ part, int n, int d, int m, int S, LmPool pl) {
     const int l = blockIdx.x / S, sp = blockIdx.x % S, h = blockIdx.y;
     const LmTokens tok = lm_tokens(pl, l, n, m);
     const int cntl = tok.count;
     const int t0 = (int)((long long)cntl * sp / S), t1 = (int)((long long)cntl * (sp + 1) / S);
     const int c = threadIdx.x % d, r = threadIdx.x / d, R = blockDim.x / d;
     const size_t base = (size_t)h * n * d;
-    double sq = 0.0, sk = 0.0, sv = 0.0;
+    double sq = 0.0, sk = 0.0;
     int t = t0 + r;
     for (; t + 3 * R < t1; t += 4 * R) {
-        float a[4], b[4], e[4];
+        float a[4], b[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
             const size_t idx = base + (size_t)tok(t + u * R) * d + c;
             a[u] = elem<DT>::load(Q, idx);
             b[u] = elem<DT>::load(K, idx);
-            e[u] = elem<DT>::load(V, idx);
         }
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
             sq += a[u];
             sk += b[u];
-            sv += e[u];
         }
     }
     for (; t < t1; t += R) {
         const size_t idx = base + (size_t)tok(t) * d + c;
         sq += elem<DT>::load(Q, idx);
         sk += elem<DT>::load(K, idx);
-        sv += elem<DT>::load(V, idx);
     }
-    __shared__ double red[3][256];
+    __shared__ double red[2][256];
     red[0][threadIdx.x] = sq;
     red[1][threadIdx.x] = sk;
-    red[2][threadIdx.x] = sv;
     __syncthreads();
     if (r == 0) {
-        double a = 0.0, b = 0.0, e = 0.0;
+        double a = 0.0, b = 0.0;
         for (int rr = 0; rr < R; ++rr) {
             a += red[0][rr * d + c];
             b += red[1][rr * d + c];
-            e += red[2][rr * d + c];
         }
         if (S == 1) {
             const double cnt = (double)cntl;
             const size_t o = ((size_t)h * m + l) * d + c;
             qt[o] = (float)(a / cnt);
             kt[o] = (float)(b / cnt);
-            vseg[o] = e;
         } else {
-            double* pp = part + (((size_t)h * m + l) * S + sp) * 3 * d + c;
+            double* pp = part + (((size_t)h * m + l) * S + sp) * 2 * d + c;
             pp[0] = a;
             pp[d] = b;
-            pp[2 * d] = e;
         }
     }
 }
@@ -95,62 +87,55 @@ constexpr int kPoolSmall = 16;
 template <int DT>
 __global__ __launch_bounds__(256) void pool_small_kernel(const typename elem<DT>::type* __restrict__ Q,
                                                          const typename elem<DT>::type* __restrict__ K,
-                                                         const typename elem<DT>::type* __restrict__ V,
-                                                         float* __restrict__ qt, float* __restrict__ kt,
-                                                         double* __restrict__ vseg, int n, int d, int m, LmPool pl) {
+                                                         float* __restrict__ qt, float* __restrict__ kt, int n, int d,
+                                                         int m, LmPool pl) {
     const int lpb = 256 / d;
     const int l = blockIdx.x * lpb + threadIdx.x / d, c = threadIdx.x % d, h = blockIdx.y;
     if (l >= m) return;
     const LmTokens tok = lm_tokens(pl, l, n, m);
     const int cnt = tok.count;
     const size_t base = (size_t)h * n * d + c;
-    double sq = 0.0, sk = 0.0, sv = 0.0;
+    double sq = 0.0, sk = 0.0;
     int t = 0;
     for (; t + 4 <= cnt; t += 4) {
-        float a[4], b[4], e[4];
+        float a[4], b[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
             const size_t idx = base + (size_t)tok(t + u) * d;
             a[u] = elem<DT>::load(Q, idx);
             b[u] = elem<DT>::load(K, idx);
-            e[u] = elem<DT>::load(V, idx);
         }
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
             sq += a[u];
             sk += b[u];
-            sv += e[u];
         }
     }
     for (; t < cnt; ++t) {
         const size_t idx = base + (size_t)tok(t) * d;
         sq += elem<DT>::load(Q, idx);
         sk += elem<DT>::load(K, idx);
-        sv += elem<DT>::load(V, idx);
     }
     const size_t o = ((size_t)h * m + l) * d + c;
     qt[o] = (float)(sq / cnt);
     kt[o] = (float)(sk / cnt);
-    vseg[o] = sv;
 }
 
 // The S parts of each landmark's sums, added in order.  grid (m, BH), d threads.
 __global__ void pool_combine_kernel(const double* __restrict__ part, float* __restrict__ qt, float* __restrict__ kt,
-                                    double* __restrict__ vseg, int n, int d, int m, int S, LmPool pl) {
+                                    int n, int d, int m, int S, LmPool pl) {
     const int l = blockIdx.x, h = blockIdx.y, c = threadIdx.x;
     if (c >= d) return;
-    const double* pp = part + ((size_t)h * m + l) * S * 3 * d + c;
-    double a = 0.0, b = 0.0, e = 0.0;
+    const double* pp = part + ((size_t)h * m + l) * S * 2 * d + c;
+    double a = 0.0, b = 0.0;
     for (int sp = 0; sp < S; ++sp) {
-        a += pp[(size_t)sp * 3 * d];
-        b += pp[(size_t)sp * 3 * d + d];
-        e += pp[(size_t)sp * 3 * d + 2 * d];
+        a += pp[(size_t)sp * 2 * d];
+        b += pp[(size_t)sp * 2 * d + d];
     }
     const double cnt = (double)lm_tokens(pl, l, n, m).count;
     const size_t o = ((size_t)h * m + l) * d + c;
     qt[o] = (float)(a / cnt);
     kt[o] = (float)(b / cnt);
-    vseg[o] = e;
 }
 
 // ------------------------------------------------------------------------------------------
@@ -168,13 +153,15 @@ __global__ void pool_combine_kernel(const double* __restrict__ part, float* __re
 //   in a fixed order.
 // Landmarks in groups of 64 (blockIdx.z = group g: landmarks 64 g .. 64 g + 63), so that m up to
 // 128 takes two blocks per key chunk, each reading the chunk's keys.
-// Writes Upart[h][chunk][a][c] for the group's landmarks a < m, c <= d; with Bsave, the keys' rows
+// Writes Upart[h][chunk][a][c] for the group's landmarks a < m, c <= d, and (group 0) the chunk's value
+// sums vpart[h][chunk][c] (c < d, for vbar); with Bsave, the keys' rows
 // of B into Bsave[h][g][n][64] (group-major rows of 64 landmarks, zeros past m).
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 template <int D>
 __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void key_summary_kernel(const float* __restrict__ K, const float* __restrict__ V,
                                                           const float* __restrict__ qt, float* __restrict__ Upart,
+                                                          float* __restrict__ vpart,
                                                           float* __restrict__ Bsave, int n, int m, float kscale,
                                                           int chunk_keys, int nkc) {
     constexpr int D1 = D + 1;
@@ -183,7 +170,7 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void key_summary_kernel(const
     constexpr int BP = 68;                 // LDS pitch of a wave's B tile (conflict-free reads)
     constexpr int RP = 16 * CT;            // pitch of the partial being reduced
     __shared__ __attribute__((aligned(16))) float lds[4 * 32 * BP];
-    static_assert(64 * RP <= 4 * 32 * BP, "the partial being reduced fits the tiles");
+    static_assert(65 * RP <= 4 * 32 * BP, "the partial being reduced and the value sums fit the tiles");
     // blocks in XCD-contiguous order: the blocks that one XCD runs take consecutive (head, chunk)
     // pairs, so that a CU's scalar cache serves few landmark tables
     const int G = (int)(gridDim.x * gridDim.y), lin = xcd_order(blockIdx.y * gridDim.x + blockIdx.x, G);
@@ -199,6 +186,9 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void key_summary_kernel(const
     for (int rt = 0; rt < 4; ++rt)
 #pragma unroll
         for (int ct = 0; ct < CT; ++ct) acc[rt][ct] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    float vsa[CT - 1];   // group 0: this lane's sums of value column 16 ct + li over its keys
+#pragma unroll
+    for (int ct = 0; ct < CT - 1; ++ct) vsa[ct] = 0.f;
     const int j0 = chunk * chunk_keys, j1 = min(n, j0 + chunk_keys);
     for (int jt = j0 + 64 * w; jt < j1; jt += 256) {
         const int j = jt + l;
@@ -224,6 +214,15 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void key_summary_kernel(const
 #pragma unroll
             for (int ct = 0; ct < CT - 1; ++ct)
                 bv[s][ct] = V[((size_t)h * n + r) * D + 16 * ct + li];
+        }
+        if (g == 0) {
+            // vbar's partial sums over the lane's live keys (rows past n repeat the last key)
+#pragma unroll
+            for (int s = 0; s < 16; ++s) {
+                const bool kl = jt + 4 * s + lk < n;
+#pragma unroll
+                for (int ct = 0; ct < CT - 1; ++ct) vsa[ct] += kl ? bv[s][ct] : 0.f;
+            }
         }
 #pragma unroll
         for (int ri = 0; ri < 2; ++ri) {   // unrolled: acc is indexed by the range
@@ -287,6 +286,14 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void key_summary_kernel(const
         }
         __builtin_amdgcn_wave_barrier();
     }
+    // the value sums over the wave's four key groups (lanes li + 16 lk), the same order in every lane
+    if (g == 0) {
+#pragma unroll
+        for (int ct = 0; ct < CT - 1; ++ct) {
+            vsa[ct] += __shfl_xor(vsa[ct], 16, 64);
+            vsa[ct] += __shfl_xor(vsa[ct], 32, 64);
+        }
+    }
     // partials of waves 3, 2, 1, 0 added in that order into one [64][RP] buffer; result register
     // r of a 16x16x4 tile at lane l is row 4 (l / 16) + r, column l % 16
     float* red = lds;
@@ -302,6 +309,13 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void key_summary_kernel(const
                         float* p = red + (16 * rt + 4 * lk + r) * RP + 16 * ct + li;
                         *p = (ww == 3) ? acc[rt][ct][r] : *p + acc[rt][ct][r];
                     }
+            if (g == 0 && l < 16) {   // the value sums: row 64 of the buffer
+#pragma unroll
+                for (int ct = 0; ct < CT - 1; ++ct) {
+                    float* p = red + 64 * RP + 16 * ct + li;
+                    *p = (ww == 3) ? vsa[ct] : *p + vsa[ct];
+                }
+            }
         }
     }
     __syncthreads();
@@ -309,6 +323,7 @@ __global__ __launch_bounds__(256, D == 32 ? 3 : 2) void key_summary_kernel(const
         const int a = e / D1, c = e % D1;
         Upart[(((size_t)h * nkc + chunk) * m + lm0 + a) * D1 + c] = red[a * RP + c];
     }
+    if (g == 0 && tid < D) vpart[((size_t)h * nkc + chunk) * D + tid] = red[64 * RP + tid];
 }
 
 // ------------------------------------------------------------------------------------------
@@ -447,7 +462,7 @@ __device__ __forceinline__ const float* ns_direct_steps(const float* sW, float* 
 template <int MP, int D>
 __global__ __launch_bounds__(256) void ns_solve_kernel(const float* __restrict__ qt, const float* __restrict__ kt,
                                                        const float* __restrict__ Upart,
-                                                       const double* __restrict__ vseg,
+                                                       const float* __restrict__ vpart,
                                                        double* __restrict__ Xs, double* __restrict__ cinfo,
                                                        float* __restrict__ U, float* __restrict__ M,
                                                        float* __restrict__ Mc, float* __restrict__ vbar, int n,
@@ -483,7 +498,7 @@ __global__ __launch_bounds__(256) void ns_solve_kernel(const float* __restrict__
     const size_t mm = (size_t)MP * MP;
     double* Xh = Xs + (size_t)h * (store_all ? (T + 2) : 1) * mm;
 
-    // The first CB key chunks of U's partial sums and the segment value sums behind vbar are
+    // The first CB key chunks of U's partial sums and the key chunks' value sums behind vbar are
     // loaded here and added after the iteration: their latency hides behind it.
     constexpr int NE = (MP * D1 + 255) / 256;
     // (MP = 64 runs one block per CU, so registers are plentiful; MP = 32 keeps them few)
@@ -496,12 +511,13 @@ __global__ __launch_bounds__(256) void ns_solve_kernel(const float* __restrict__
 #pragma unroll
         for (int r = 0; r < NE; ++r) ub[cc][r] = up[min(tid + 256 * r, ulim)];
     }
-    constexpr int G = 256 / D;   // vbar: 256 / D partial sums per column
-    double vsg[MP / G];
+    constexpr int G = 256 / D;   // vbar: 256 / D partial sums per column over the key chunks' value sums
+    constexpr int VK = 16;       // chunks per partial loaded up front
+    float vpv[VK];
     {
         const int gq = tid / D, cc = tid % D;
 #pragma unroll
-        for (int i = 0; i < MP / G; ++i) vsg[i] = vseg[((size_t)h * m + min(gq + G * i, m - 1)) * D + cc];
+        for (int i = 0; i < VK; ++i) vpv[i] = gq + G * i < nkc ? vpart[((size_t)h * nkc + gq + G * i) * D + cc] : 0.f;
     }
 
     // ---- W = K_LL + eps I: thread (a-group, b = tid % MP) keeps the key landmark row b in
@@ -610,13 +626,14 @@ __global__ __launch_bounds__(256) void ns_solve_kernel(const float* __restrict__
             if (a < m) U[(size_t)h * m * D1 + e] = (float)u[r];
         }
     }
-    // vbar = (sum of the segment value sums) / n: 256 / D partial sums per column, then in order
+    // vbar = (sum of the key chunks' value sums) / n: 256 / D partial sums per column (chunks
+    // gq, gq + G, ... in order), then over the partials in order
     {
-        const int gq = tid / D;
+        const int gq = tid / D, cc = tid % D;
         double s = 0.0;
 #pragma unroll
-        for (int i = 0; i < MP / G; ++i)
-            if (gq + G * i < m) s += vsg[i];
+        for (int i = 0; i < VK; ++i) s += (double)vpv[i];
+        for (int k = gq + G * VK; k < nkc; k += G) s += (double)vpart[((size_t)h * nkc + k) * D + cc];
         svb[tid] = s;
     }
     __syncthreads();   // sX, sU, su1, svb
@@ -836,51 +853,52 @@ int pool_split(int BH, int n, int m) {
     return S;
 }
 
-hipError_t launch_pool(int dt, const void* Q, const void* K, const void* V, float* qt, float* kt, double* vseg,
-                       double* part, int BH, int n, int d, int m, LmPool pl, hipStream_t st) {
+hipError_t launch_pool(int dt, const void* Q, const void* K, float* qt, float* kt, double* part, int BH, int n, int d,
+                       int m, LmPool pl, hipStream_t st) {
     const int most = pl.r > 0 ? pl.r * pl.r : (n + m - 1) / m;   // tokens of the largest landmark
     if (most <= kPoolSmall) {
         const dim3 grid((m + 256 / d - 1) / (256 / d), BH);
         if (dt == DT_F32)
             hipLaunchKernelGGL(pool_small_kernel<DT_F32>, grid, dim3(256), 0, st, (const float*)Q, (const float*)K,
-                               (const float*)V, qt, kt, vseg, n, d, m, pl);
+                               qt, kt, n, d, m, pl);
         else
             hipLaunchKernelGGL(pool_small_kernel<DT_BF16>, grid, dim3(256), 0, st, (const uint16_t*)Q,
-                               (const uint16_t*)K, (const uint16_t*)V, qt, kt, vseg, n, d, m, pl);
+                               (const uint16_t*)K, qt, kt, n, d, m, pl);
         return hipGetLastError();
     }
     const int S = pool_split(BH, n, m);
     dim3 grid(m * S, BH);
     if (dt == DT_F32)
-        hipLaunchKernelGGL(pool_kernel<DT_F32>, grid, dim3(256), 0, st, (const float*)Q, (const float*)K,
-                           (const float*)V, qt, kt, vseg, part, n, d, m, S, pl);
+        hipLaunchKernelGGL(pool_kernel<DT_F32>, grid, dim3(256), 0, st, (const float*)Q, (const float*)K, qt, kt,
+                           part, n, d, m, S, pl);
     else
-        hipLaunchKernelGGL(pool_kernel<DT_BF16>, grid, dim3(256), 0, st, (const uint16_t*)Q, (const uint16_t*)K,
-                           (const uint16_t*)V, qt, kt, vseg, part, n, d, m, S, pl);
+        hipLaunchKernelGGL(pool_kernel<DT_BF16>, grid, dim3(256), 0, st, (const uint16_t*)Q, (const uint16_t*)K, qt, kt,
+                           part, n, d, m, S, pl);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || S == 1) return e;
-    hipLaunchKernelGGL(pool_combine_kernel, dim3(m, BH), dim3(64), 0, st, part, qt, kt, vseg, n, d, m, S, pl);
+    hipLaunchKernelGGL(pool_combine_kernel, dim3(m, BH), dim3(64), 0, st, part, qt, kt, n, d, m, S, pl);
     return hipGetLastError();
 }
 
-hipError_t launch_key_summary(int dt, const void* K, const void* V, const float* qt, float* Upart, float* Bsave,
-                              int BH, int n, int d, int m, float lambda, int chunk_keys, int nkc, hipStream_t st) {
+hipError_t launch_key_summary(int dt, const void* K, const void* V, const float* qt, float* Upart, float* vpart,
+                              float* Bsave, int BH, int n, int d, int m, float lambda, int chunk_keys, int nkc,
+                              hipStream_t st) {
     if (dt != DT_F32) return hipErrorInvalidValue;   // bf16 inputs take the fast path
     const float ks = kscale_of(lambda);
     if (d == 32)
         hipLaunchKernelGGL((key_summary_kernel<32>), dim3(nkc, BH, (m + 63) / 64), dim3(256), 0, st, (const float*)K,
-                           (const float*)V, qt, Upart, Bsave, n, m, ks, chunk_keys, nkc);
+                           (const float*)V, qt, Upart, vpart, Bsave, n, m, ks, chunk_keys, nkc);
     else
         hipLaunchKernelGGL((key_summary_kernel<64>), dim3(nkc, BH, (m + 63) / 64), dim3(256), 0, st, (const float*)K,
-                           (const float*)V, qt, Upart, Bsave, n, m, ks, chunk_keys, nkc);
+                           (const float*)V, qt, Upart, vpart, Bsave, n, m, ks, chunk_keys, nkc);
     return hipGetLastError();
 }
 
-hipError_t launch_ns_solve(const float* qt, const float* kt, const float* Upart, const double* vseg, double* Xs,
+hipError_t launch_ns_solve(const float* qt, const float* kt, const float* Upart, const float* vpart, double* Xs,
                            double* cinfo, float* U, float* M, float* Mc, float* vbar, int BH, int n, int d, int m, int T,
                            double lambda, double eps, int nkc, int store_all, int MP, hipStream_t st) {
 #define LAPATTN_NS(MPv, Dv)                                                                                  \
-    hipLaunchKernelGGL((ns_solve_kernel<MPv, Dv>), dim3(BH), dim3(256), 0, st, qt, kt, Upart, vseg, Xs, cinfo, \
+    hipLaunchKernelGGL((ns_solve_kernel<MPv, Dv>), dim3(BH), dim3(256), 0, st, qt, kt, Upart, vpart, Xs, cinfo, \
                        U, M, Mc, vbar, n, m, T, lambda, eps, nkc, store_all)
     if (MP == 32 && d == 32) LAPATTN_NS(32, 32);
     else if (MP == 32) LAPATTN_NS(32, 64);

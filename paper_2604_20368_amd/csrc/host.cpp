@@ -66,7 +66,7 @@ struct FastPlan {
 };
 
 struct Plan {
-    size_t qt, kt, vseg, Upart, Xs, cinfo, U, M, Mc, vbar;               // forward
+    size_t qt, kt, Upart, vpart, Xs, cinfo, U, M, Mc, vbar;              // forward
     size_t Ebuf, Ud, nsbs, dDW;          // m > 64: solve and its backward spread over workgroups
     size_t pool_part;                    // landmark sums split over blocks (small m BH)
     size_t oF;                           // bf16 forward with m > 64: the fp32 output
@@ -125,9 +125,9 @@ Plan make_plan(int BH, int n, int d, int m, int T, bool bwd, bool bf16 = false, 
     Carver c;
     p.qt = c.take(bh * m * d * f);
     p.kt = c.take(bh * m * d * f);
-    p.vseg = c.take(bh * m * d * g);
-    p.pool_part = c.take(bh * m * (size_t)lapattn::pool_split(BH, n, m) * 3 * d * g);
+    p.pool_part = c.take(bh * m * (size_t)lapattn::pool_split(BH, n, m) * 2 * d * g);
     p.Upart = c.take(bh * p.nkc * m * d1 * f);
+    p.vpart = c.take(bh * p.nkc * (size_t)d * f);
     // X_0..X_T and W for the backward (always, for m > 64)
     p.Xs = c.take(bh * ((bwd || big) ? (size_t)T + 2 : 1) * mpp * g);
     p.cinfo = c.take(bh * 4 * g);
@@ -339,26 +339,27 @@ hipError_t forward_internals(Recorder& rec, const Plan& p, const void* Q, const 
                              lapattn::LmPool pl, hipStream_t st, float* Bsave = nullptr) {
     float* qt = at<float>(ws, p.qt);
     float* kt = at<float>(ws, p.kt);
-    double* vseg = at<double>(ws, p.vseg);
     float* Upart = at<float>(ws, p.Upart);
+    float* vpart = at<float>(ws, p.vpart);
     hipError_t e;
     e = run_named(rec, "pool", [&] {
-        return lapattn::launch_pool(dtype, Q, K, V, qt, kt, vseg, at<double>(ws, p.pool_part), BH, n, d, m, pl, st);
+        return lapattn::launch_pool(dtype, Q, K, qt, kt, at<double>(ws, p.pool_part), BH, n, d, m, pl, st);
     });
     if (e != hipSuccess) return e;
     e = run_named(rec, "key_summary", [&] {
-        return lapattn::launch_key_summary(dtype, K, V, qt, Upart, Bsave, BH, n, d, m, lambda, p.kc, p.nkc, st);
+        return lapattn::launch_key_summary(dtype, K, V, qt, Upart, vpart, Bsave, BH, n, d, m, lambda, p.kc, p.nkc,
+                                           st);
     });
     if (e != hipSuccess) return e;
     if (p.MP == 128)
         return run_named(rec, "ns_solve", [&] {
-            return lapattn::launch_nsb_forward(qt, kt, Upart, vseg, at<double>(ws, p.Xs), at<double>(ws, p.Ebuf),
+            return lapattn::launch_nsb_forward(qt, kt, Upart, vpart, at<double>(ws, p.Xs), at<double>(ws, p.Ebuf),
                                                at<double>(ws, p.Ud), at<double>(ws, p.cinfo), at<float>(ws, p.U),
                                                at<float>(ws, p.M), at<float>(ws, p.Mc), at<float>(ws, p.vbar), BH, n,
                                                d, m, T, (double)lambda, (double)eps, p.nkc, st);
         });
     e = run_named(rec, "ns_solve", [&] {
-        return lapattn::launch_ns_solve(qt, kt, Upart, vseg, at<double>(ws, p.Xs), at<double>(ws, p.cinfo),
+        return lapattn::launch_ns_solve(qt, kt, Upart, vpart, at<double>(ws, p.Xs), at<double>(ws, p.cinfo),
                                         at<float>(ws, p.U), at<float>(ws, p.M), at<float>(ws, p.Mc),
                                         at<float>(ws, p.vbar), BH, n, d, m, T,
                                         (double)lambda, (double)eps, p.nkc, store_all ? 1 : 0, p.MP, st);

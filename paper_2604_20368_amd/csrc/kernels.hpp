@@ -14,27 +14,28 @@ namespace lapattn {
 
 // Forward ---------------------------------------------------------------------
 
-// Landmark means qt, kt [BH][m][d] (fp32) and per-landmark value sums vseg [BH][m][d] (fp64);
-// pl selects segments or r x r windows (common.hpp).  When m BH is small each landmark's tokens
-// are split over pool_split(BH, n, m) blocks whose fp64 sums go to part ([BH][m][S][3][d]) and
+// Landmark means qt, kt [BH][m][d] (fp32; V is not read: the key side forms its sums); pl
+// selects segments or r x r windows (common.hpp).  When m BH is small each landmark's tokens
+// are split over pool_split(BH, n, m) blocks whose fp64 sums go to part ([BH][m][S][2][d]) and
 // are added in order by a second launch.
 int pool_split(int BH, int n, int m);
-hipError_t launch_pool(int dt, const void* Q, const void* K, const void* V,
-                       float* qt, float* kt, double* vseg, double* part,
+hipError_t launch_pool(int dt, const void* Q, const void* K, float* qt, float* kt, double* part,
                        int BH, int n, int d, int m, LmPool pl, hipStream_t st);
 
-// Key-side summary: per key chunk, Upart[h][chunk][a][c] = sum_j k(qt_a, k_j) [v_j | 1]_c;
-// with Bsave, also the rows B[j][a] = k(qt_a, k_j) for the backward, group-major
-// ([BH][G][n][64] for the G = ceil(m / 64) landmark groups, zeros past m).
-hipError_t launch_key_summary(int dt, const void* K, const void* V, const float* qt, float* Upart, float* Bsave,
-                              int BH, int n, int d, int m, float lambda, int chunk_keys, int nkc,
+// Key-side summary: per key chunk, Upart[h][chunk][a][c] = sum_j k(qt_a, k_j) [v_j | 1]_c and the
+// value sums vpart[h][chunk][c] = sum_j v_jc (for vbar); with Bsave, also the rows
+// B[j][a] = k(qt_a, k_j) for the backward, group-major ([BH][G][n][64] for the G = ceil(m / 64)
+// landmark groups, zeros past m).
+hipError_t launch_key_summary(int dt, const void* K, const void* V, const float* qt, float* Upart, float* vpart,
+                              float* Bsave, int BH, int n, int d, int m, float lambda, int chunk_keys, int nkc,
                               hipStream_t st);
 
 // Newton-Schulz on K_LL and the solved matrix M = X_T U, m <= 64.
 //   Xs:    [BH][store_all ? T+2 : 1][MP][MP] fp64 iterates (padded to MP), then W
 //   cinfo: [BH][4] fp64: scale c, ||W||_1, ||W||_inf, (a* * 256 + b*)
 //   U, M:  [BH][m][d+1] fp32;  Mc: [BH][m][d] fp32, M[:, :d] - M[:, d] vbar^T;  vbar: [BH][d] fp32
-hipError_t launch_ns_solve(const float* qt, const float* kt, const float* Upart, const double* vseg,
+//   (vbar from the key chunks' value sums vpart)
+hipError_t launch_ns_solve(const float* qt, const float* kt, const float* Upart, const float* vpart,
                            double* Xs, double* cinfo, float* U, float* M, float* Mc, float* vbar,
                            int BH, int n, int d, int m, int T, double lambda, double eps, int nkc,
                            int store_all, int MP, hipStream_t st);
@@ -71,7 +72,7 @@ struct NsbJobs {
 NsbJob nsb_job(const double* A, long long sA, int pa, bool ta, const double* B, long long sB, int pb, bool tb,
                double* Out, long long sOut, int pout, int M, int N, int K, double alpha);
 hipError_t launch_nsb_mm(const NsbJobs& js, int njobs, int BH, hipStream_t st);
-hipError_t launch_nsb_forward(const float* qt, const float* kt, const float* Upart, const double* vseg, double* Xs,
+hipError_t launch_nsb_forward(const float* qt, const float* kt, const float* Upart, const float* vpart, double* Xs,
                               double* Ebuf, double* Ud, double* cinfo, float* U, float* M, float* Mc, float* vbar,
                               int BH, int n, int d, int m, int T, double lambda, double eps, int nkc, hipStream_t st);
 // Scratch doubles of launch_nsb_backward.

@@ -232,9 +232,9 @@ __global__ __launch_bounds__(256) void nsb_usum_kernel(const float* __restrict__
 // U (all rows) and the block's rows of X_T in LDS.
 template <int D>
 __global__ __launch_bounds__(256) void nsb_final_kernel(const double* __restrict__ XT, long long xstride,
-                                                        const double* __restrict__ Ud, const double* __restrict__ vseg,
+                                                        const double* __restrict__ Ud, const float* __restrict__ vpart,
                                                         float* __restrict__ M, float* __restrict__ Mc,
-                                                        float* __restrict__ vbar, int n, int m) {
+                                                        float* __restrict__ vbar, int n, int m, int nkc) {
     constexpr int D1 = D + 1;
     __shared__ double sU[kBig * D1];
     __shared__ double sX[32 * kBig];
@@ -260,12 +260,12 @@ __global__ __launch_bounds__(256) void nsb_final_kernel(const double* __restrict
     }
     if (tid < D) {
         double t = 0.0;
-        for (int l0 = 0; l0 < m; l0 += 16) {   // 16 loads in flight, added in landmark order
-            double v[16];
+        for (int k0 = 0; k0 < nkc; k0 += 16) {   // the key chunks' value sums: 16 loads in flight, in order
+            float v[16];
 #pragma unroll
-            for (int i = 0; i < 16; ++i) v[i] = l0 + i < m ? vseg[((size_t)h * m + l0 + i) * D + tid] : 0.0;
+            for (int i = 0; i < 16; ++i) v[i] = k0 + i < nkc ? vpart[((size_t)h * nkc + k0 + i) * D + tid] : 0.f;
 #pragma unroll
-            for (int i = 0; i < 16; ++i) t += v[i];
+            for (int i = 0; i < 16; ++i) t += (double)v[i];
         }
         svb[tid] = t / n;
         if (blockIdx.x == 0) vbar[(size_t)h * D + tid] = (float)(t / n);
@@ -527,7 +527,7 @@ NsbJob nsb_job(const double* A, long long sA, int pa, bool ta, const double* B, 
     return j;
 }
 
-hipError_t launch_nsb_forward(const float* qt, const float* kt, const float* Upart, const double* vseg, double* Xs,
+hipError_t launch_nsb_forward(const float* qt, const float* kt, const float* Upart, const float* vpart, double* Xs,
                               double* Ebuf, double* Ud, double* cinfo, float* U, float* M, float* Mc, float* vbar,
                               int BH, int n, int d, int m, int T, double lambda, double eps, int nkc, hipStream_t st) {
     const long long mm = (long long)kBig * kBig, xs = (long long)(T + 2) * mm, es = 2 * mm;
@@ -572,11 +572,11 @@ hipError_t launch_nsb_forward(const float* qt, const float* kt, const float* Upa
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const double* XT = Xs + (size_t)T * mm;
     if (d == 32)
-        hipLaunchKernelGGL(nsb_final_kernel<32>, dim3(kBig / 32, BH), dim3(256), 0, st, XT, xs, Ud, vseg, M, Mc, vbar,
-                           n, m);
+        hipLaunchKernelGGL(nsb_final_kernel<32>, dim3(kBig / 32, BH), dim3(256), 0, st, XT, xs, Ud, vpart, M, Mc, vbar,
+                           n, m, nkc);
     else
-        hipLaunchKernelGGL(nsb_final_kernel<64>, dim3(kBig / 32, BH), dim3(256), 0, st, XT, xs, Ud, vseg, M, Mc, vbar,
-                           n, m);
+        hipLaunchKernelGGL(nsb_final_kernel<64>, dim3(kBig / 32, BH), dim3(256), 0, st, XT, xs, Ud, vpart, M, Mc, vbar,
+                           n, m, nkc);
     return hipGetLastError();
 }
 

@@ -627,6 +627,43 @@ def summarize_trace(trace_dir):
     print(json.dumps(out, indent=1))
 
 
+def summarize_sweep_trace(trace_dir, steps):
+    """Kernel-only durations of the sweep (`bench.py --sweep --steps STEPS` under rocprofv3
+    --kernel-trace): the library's launches in order, split into steps at each pooling launch
+    (3 warmup + STEPS timed + 1 comparison step per (n, m)); per case the median over the timed
+    steps of each group of SWEEP_GROUPS, in us.  HIP events around a launch (the sweep's own
+    figures) add the launch latency, a few us for these one- or two-workgroup kernels."""
+    import csv
+    import re
+    import statistics as st
+    rows = list(csv.DictReader(open(os.path.join(trace_dir, "run_kernel_trace.csv"))))
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    seq = []
+    for r in rows:
+        mm = re.search(r"lapattn::(\w+?)(?:_kernel)?[<(]", r["Kernel_Name"]) or \
+            re.search(r"_ZN7lapattn\d+(\w+?)(?:_kernel)?(?:I|E)", r["Kernel_Name"])
+        if mm:
+            seq.append((mm.group(1), (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3))
+    step_list, cur = [], None
+    for k, t in seq:
+        if k in ("pool", "pool_small"):
+            cur = {}
+            step_list.append(cur)
+        if cur is not None:
+            cur[k] = cur.get(k, 0.0) + t
+    per_case = 3 + steps + 1
+    cases = [(n, m) for n in SWEEP_N for m in SWEEP_M]
+    if len(step_list) != per_case * len(cases):
+        raise SystemExit("unexpected step count %d (expected %d)" % (len(step_list), per_case * len(cases)))
+    groups = SWEEP_GROUPS + (("ns_bwd_kll", ("bwd_ns", "kll_bwd")),)
+    print("| n | m | " + " | ".join(g for g, _ in groups) + " |")
+    print("|" + "---|" * (len(groups) + 2))
+    for ci, (n, m) in enumerate(cases):
+        timed = step_list[ci * per_case + 3: ci * per_case + 3 + steps]
+        cells = ["%.1f" % st.median(sum(s.get(k, 0.0) for k in names) for s in timed) for _, names in groups]
+        print("| %d | %d | " % (n, m) + " | ".join(cells) + " |")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -644,6 +681,8 @@ def main():
     ap.add_argument("--sweep", action="store_true",
                     help="only the (n, m) timing sweep of the Laplacian kernel and Newton-Schulz kernels "
                          "(batch 1, 2 heads, d=32) beside plain PyTorch; prints a markdown table in us")
+    ap.add_argument("--summarize-sweep-trace", nargs=2, metavar=("TRACE_DIR", "STEPS"),
+                    help="kernel-only durations per (n, m) from a rocprofv3 --kernel-trace run of --sweep --steps STEPS")
     ap.add_argument("--summarize-trace", metavar="TRACE_DIR",
                     help="per-leg kernel statistics of a rocprofv3 --kernel-trace CSV directory")
     ap.add_argument("--oracle-only", action="store_true", help=argparse.SUPPRESS)
@@ -670,6 +709,9 @@ def main():
         return
     if args.summarize_trace:
         summarize_trace(args.summarize_trace)
+        return
+    if args.summarize_sweep_trace:
+        summarize_sweep_trace(args.summarize_sweep_trace[0], int(args.summarize_sweep_trace[1]))
         return
     if args.calibrate_copy:
         calibrate_copy()

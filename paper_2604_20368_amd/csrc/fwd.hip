@@ -511,13 +511,21 @@ __global__ __launch_bounds__(256) void ns_solve_kernel(const float* __restrict__
 #pragma unroll
         for (int r = 0; r < NE; ++r) ub[cc][r] = up[min(tid + 256 * r, ulim)];
     }
-    constexpr int G = 256 / D;   // vbar: 256 / D partial sums per column over the key chunks' value sums
-    constexpr int VK = 16;       // chunks per partial loaded up front
-    float vpv[VK];
+    // vbar's 256 / D partial sums per column over the key chunks' value sums (chunks gq, gq + G,
+    // ... in order, eight loads in flight), formed here beside the landmark rows' loads and kept
+    // in LDS until the end
+    constexpr int G = 256 / D;
     {
         const int gq = tid / D, cc = tid % D;
+        double vs = 0.0;
+        for (int k0 = gq; k0 < nkc; k0 += 8 * G) {
+            float v[8];
 #pragma unroll
-        for (int i = 0; i < VK; ++i) vpv[i] = gq + G * i < nkc ? vpart[((size_t)h * nkc + gq + G * i) * D + cc] : 0.f;
+            for (int i = 0; i < 8; ++i) v[i] = k0 + G * i < nkc ? vpart[((size_t)h * nkc + k0 + G * i) * D + cc] : 0.f;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) vs += (double)v[i];
+        }
+        svb[tid] = vs;
     }
 
     // ---- W = K_LL + eps I: thread (a-group, b = tid % MP) keeps the key landmark row b in
@@ -554,7 +562,8 @@ __global__ __launch_bounds__(256) void ns_solve_kernel(const float* __restrict__
             const float4 v = *reinterpret_cast<const float4*>(sK + b * KP + 4 * c4);
             kb[4 * c4] = v.x; kb[4 * c4 + 1] = v.y; kb[4 * c4 + 2] = v.z; kb[4 * c4 + 3] = v.w;
         }
-        for (int a = tid / MP; a < MP; a += 256 / MP) {
+#pragma unroll 2
+        for (int a = tid / MP; a < MP; a += 256 / MP) {   // two rows per pass: the next row's reads overlap
             const float4* qa = reinterpret_cast<const float4*>(sQ + a * D);
             float d4[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -577,7 +586,7 @@ __global__ __launch_bounds__(256) void ns_solve_kernel(const float* __restrict__
     ns_norms<MP>(sW, spart, sred, &sc, cinfo + h * 4);
     const float* sXf = ns_direct_steps<MP>(sW, sX0, sXT0, sTT, sc, T, store_all ? Xh : nullptr);   // X_T
     // ---- U = sum over key chunks (in chunk order) in fp64: the first CB chunks from the early
-    // loads, then CB chunks' loads in flight at a time
+    // loads, then 2 CB chunks' loads in flight at a time
     double u[NE];
 #pragma unroll
     for (int r = 0; r < NE; ++r) u[r] = 0.0;
@@ -586,18 +595,21 @@ __global__ __launch_bounds__(256) void ns_solve_kernel(const float* __restrict__
 #pragma unroll
         for (int r = 0; r < NE; ++r)
             if (cc < nkc && tid + 256 * r <= ulim) u[r] += (double)ub[cc][r];
-    for (int c0 = CB; c0 < nkc; c0 += CB) {
+    // the remaining chunks CB2 at a time (registers are free again after the iteration)
+    constexpr int CB2 = 2 * CB;
+    for (int c0 = CB; c0 < nkc; c0 += CB2) {
+        float ub2[CB2][NE];
 #pragma unroll
-        for (int cc = 0; cc < CB; ++cc) {
+        for (int cc = 0; cc < CB2; ++cc) {
             const float* up = Upart + ((size_t)h * nkc + min(c0 + cc, nkc - 1)) * m * D1;
 #pragma unroll
-            for (int r = 0; r < NE; ++r) ub[cc][r] = up[min(tid + 256 * r, ulim)];
+            for (int r = 0; r < NE; ++r) ub2[cc][r] = up[min(tid + 256 * r, ulim)];
         }
 #pragma unroll
-        for (int cc = 0; cc < CB; ++cc)
+        for (int cc = 0; cc < CB2; ++cc)
 #pragma unroll
             for (int r = 0; r < NE; ++r)
-                if (c0 + cc < nkc && tid + 256 * r <= ulim) u[r] += (double)ub[cc][r];
+                if (c0 + cc < nkc && tid + 256 * r <= ulim) u[r] += (double)ub2[cc][r];
     }
     // X_T to fp64 (registers first: the fp64 copy overwrites the fp32 buffers)
     constexpr int NX = MP * MP / 256;
@@ -626,17 +638,7 @@ __global__ __launch_bounds__(256) void ns_solve_kernel(const float* __restrict__
             if (a < m) U[(size_t)h * m * D1 + e] = (float)u[r];
         }
     }
-    // vbar = (sum of the key chunks' value sums) / n: 256 / D partial sums per column (chunks
-    // gq, gq + G, ... in order), then over the partials in order
-    {
-        const int gq = tid / D, cc = tid % D;
-        double s = 0.0;
-#pragma unroll
-        for (int i = 0; i < VK; ++i) s += (double)vpv[i];
-        for (int k = gq + G * VK; k < nkc; k += G) s += (double)vpart[((size_t)h * nkc + k) * D + cc];
-        svb[tid] = s;
-    }
-    __syncthreads();   // sX, sU, su1, svb
+    __syncthreads();   // sX, sU, su1 (svb since the start)
     if (tid < m) {
         double s = 0.0;
 #pragma unroll 16

@@ -94,7 +94,7 @@ __device__ __forceinline__ int xcd_rank(int i, int n, int base) {
 // ------------------------------------------------------------------------------------------
 // Landmark means and per-landmark statistics.  grid (m, BH), 256 threads.  Thread t always
 // reads the 8-column group t % (D/8) of its rows (the landmark's tokens t / (D/8) + (256 / (D/8)) i
-// of its segment or window, lm_tokens), four rows per thread in flight at a time.  Sums: per thread in fp32, then over the
+// of its segment or window, lm_tokens), eight rows per thread in flight at a time.  Sums: per thread in fp32, then over the
 // lanes of a wave that share a column group (a butterfly), then over the four waves in a fixed
 // order in fp64.  RV = false (the key side with the landmarks split over its waves, which forms
 // the value statistics itself): Q and K only, vseg and vsegmax untouched.
@@ -106,7 +106,7 @@ __global__ __launch_bounds__(256) void pool2_kernel(const uint16_t* __restrict__
                                                     int m, LmPool pl) {
     constexpr int CPR = D / 8;      // 16-byte chunks per row
     constexpr int RPI = 256 / CPR;  // rows per block iteration
-    constexpr int UNR = 4;          // row iterations in flight
+    constexpr int UNR = 8;          // row iterations in flight (256 tokens at D = 64 in one round trip)
     const int l = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
     const LmTokens tok = lm_tokens(pl, l, n, m);   // the landmark's tokens tok(0 .. count - 1)
     const int cntl = tok.count;
@@ -1392,6 +1392,15 @@ __global__ __launch_bounds__(kMfinalThreads) void mfinal_kernel(const float* __r
     const int g = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, w = tid / 64, l = tid & 63;
     const bool ones = g == NG - 1;
     const int c0 = 8 * g, nc = ones ? 1 : 8;   // operand columns of this group
+    // X_T (written by the previous launch, possibly through another XCD's L2) into registers
+    // first, every load in flight together; stored into LDS after the chunk sums
+    constexpr int NX = (4096 + kMfinalThreads - 1) / kMfinalThreads;
+    float xr[NX];
+#pragma unroll
+    for (int i = 0; i < NX; ++i) {
+        const int e = tid + i * kMfinalThreads;
+        xr[i] = e < 4096 ? XT[(size_t)h * 4096 + e] : 0.f;
+    }
     if (!ones && w == 0) {
         // lane (column l % 8, part l / 8): the key blocks k = part, part + 8, ... (the first
         // eight loads issued together), then the eight parts by a butterfly (the same order in
@@ -1443,7 +1452,11 @@ __global__ __launch_bounds__(kMfinalThreads) void mfinal_kernel(const float* __r
             }
         }
     }
-    for (int e = tid; e < 4096; e += kMfinalThreads) sX[(e >> 6) * 65 + (e & 63)] = XT[(size_t)h * 4096 + e];
+#pragma unroll
+    for (int i = 0; i < NX; ++i) {
+        const int e = tid + i * kMfinalThreads;
+        if (e < 4096) sX[(e >> 6) * 65 + (e & 63)] = xr[i];
+    }
     if (qq > 0 && cl < ncol) red[(qq - 1) * NI + f] = acc;
     __syncthreads();
     if (qq == 0 && cl < ncol) {

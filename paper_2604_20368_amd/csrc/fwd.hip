@@ -121,21 +121,26 @@ __global__ __launch_bounds__(256) void pool_small_kernel(const typename elem<DT>
     kt[o] = (float)(sk / cnt);
 }
 
-// The S parts of each landmark's sums, added in order.  grid (m, BH), d threads.
+// The S parts of each landmark's sums (S <= kPoolMaxSplit), added in order.  grid (m, BH),
+// 2 d threads rounded up to a wave: thread c < d the query sums of column c, d <= c < 2 d the key
+// sums of column c - d; the S loads are issued together.
+constexpr int kPoolMaxSplit = 16;
+
 __global__ void pool_combine_kernel(const double* __restrict__ part, float* __restrict__ qt, float* __restrict__ kt,
                                     int n, int d, int m, int S, LmPool pl) {
     const int l = blockIdx.x, h = blockIdx.y, c = threadIdx.x;
-    if (c >= d) return;
+    if (c >= 2 * d) return;
     const double* pp = part + ((size_t)h * m + l) * S * 2 * d + c;
-    double a = 0.0, b = 0.0;
-    for (int sp = 0; sp < S; ++sp) {
-        a += pp[(size_t)sp * 2 * d];
-        b += pp[(size_t)sp * 2 * d + d];
-    }
+    double v[kPoolMaxSplit];
+#pragma unroll
+    for (int sp = 0; sp < kPoolMaxSplit; ++sp) v[sp] = sp < S ? pp[(size_t)sp * 2 * d] : 0.0;
+    double a = 0.0;
+#pragma unroll
+    for (int sp = 0; sp < kPoolMaxSplit; ++sp)
+        if (sp < S) a += v[sp];
     const double cnt = (double)lm_tokens(pl, l, n, m).count;
-    const size_t o = ((size_t)h * m + l) * d + c;
-    qt[o] = (float)(a / cnt);
-    kt[o] = (float)(b / cnt);
+    const size_t o = ((size_t)h * m + l) * d + (c < d ? c : c - d);
+    (c < d ? qt : kt)[o] = (float)(a / cnt);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -851,7 +856,7 @@ static inline float kscale_of(float lambda) { return (float)(-1.4426950408889634
 int pool_split(int BH, int n, int m) {
     const int per = n / m;   // tokens per landmark (segments: this or one more; windows: exactly)
     int S = 1;
-    while (S < 16 && (long long)m * BH * S < 512 && per / (2 * S) >= 64) S *= 2;
+    while (S < kPoolMaxSplit && (long long)m * BH * S < 512 && per / (2 * S) >= 64) S *= 2;
     return S;
 }
 
@@ -878,7 +883,8 @@ hipError_t launch_pool(int dt, const void* Q, const void* K, float* qt, float* k
                            part, n, d, m, S, pl);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || S == 1) return e;
-    hipLaunchKernelGGL(pool_combine_kernel, dim3(m, BH), dim3(64), 0, st, part, qt, kt, n, d, m, S, pl);
+    hipLaunchKernelGGL(pool_combine_kernel, dim3(m, BH), dim3((2 * d + 63) / 64 * 64), 0, st, part, qt, kt, n, d, m,
+                       S, pl);
     return hipGetLastError();
 }
 

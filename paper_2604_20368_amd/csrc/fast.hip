@@ -94,7 +94,7 @@ __device__ __forceinline__ int xcd_rank(int i, int n, int base) {
 // ------------------------------------------------------------------------------------------
 // Landmark means and per-landmark statistics.  grid (m, BH), 256 threads.  Thread t always
 // reads the 8-column group t % (D/8) of its rows (the landmark's tokens t / (D/8) + (256 / (D/8)) i
-// of its segment or window, lm_tokens), eight rows per thread in flight at a time.  Sums: per thread in fp32, then over the
+// of its segment or window, lm_tokens), four rows per thread in flight at a time.  Sums: per thread in fp32, then over the
 // lanes of a wave that share a column group (a butterfly), then over the four waves in a fixed
 // order in fp64.  RV = false (the key side with the landmarks split over its waves, which forms
 // the value statistics itself): Q and K only, vseg and vsegmax untouched.
@@ -106,7 +106,7 @@ __global__ __launch_bounds__(256) void pool2_kernel(const uint16_t* __restrict__
                                                     int m, LmPool pl) {
     constexpr int CPR = D / 8;      // 16-byte chunks per row
     constexpr int RPI = 256 / CPR;  // rows per block iteration
-    constexpr int UNR = 8;          // row iterations in flight (256 tokens at D = 64 in one round trip)
+    constexpr int UNR = 4;          // row iterations in flight
     const int l = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
     const LmTokens tok = lm_tokens(pl, l, n, m);   // the landmark's tokens tok(0 .. count - 1)
     const int cntl = tok.count;
